@@ -1,0 +1,6 @@
+"""CPU oracle (test infrastructure only): see ``oracle.resonator_oracle``.
+
+Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import
+this package.  It shares no code with the HIP path.
+"""
+from .resonator_oracle import *  # noqa: F401,F403
