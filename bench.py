@@ -1,0 +1,284 @@
+#!/usr/bin/env python3
+"""Benchmark of the resonant mixing hot path on one MI355X.
+
+One step = one prefill forward pass of the long-context workload (B=4, L=32768,
+D=256, M=8, bf16 drive and output, fp32 accumulation, terminal state written):
+parameter tables, chunk products, cross-tile carry, correction and store.  The
+timed region holds exactly K steps with the inputs already resident in HBM;
+three input/output buffer sets rotate so that the working set (3 x 134 MB)
+exceeds the 256 MB Infinity Cache.  The JSON line also carries
+
+  decode    steps/s of the decode workload (B=64, D=256, M=8, state from a
+            1024-step prompt), eager (one C call per step from Python) and
+            replayed from a captured HIP graph of the same calls;
+  train     one forward + backward of a training layer (B=8, L=8192, D=256, M=8,
+            bf16), as time per layer;
+  roofline  the dominant kernel (the forward apply tile kernel) against the HBM
+            peak: algorithmic bytes (2 B read + 2 B written per token-channel)
+            per launch over its average launch time, measured with HIP events
+            recorded around that kernel alone;
+  cpu_baseline  the float64 CPU oracle (sequential recurrence) on the host.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "prefill mix tokens·ch/s + decode steps/s at L=32K; % of HBM peak"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_apply_prefill_B4_L32768_D256_M8.json")
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_05583_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def counter_traffic(per_launch_tokens: int):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel sources; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        t = json.load(f)
+    if t.get("source_hash") != source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def cpu_baseline(cfg):
+    """The oracle's sequential recurrence on the prefill workload, timed on the host."""
+    import oracle as O
+    import workloads as W
+    inp = W.fwd_inputs(cfg)
+    x = W.act_to_f32(inp["x"], cfg.act).astype(np.float64)
+    prm = [inp[k] for k in ("gamma", "omega", "amp", "phase")]
+    t0 = time.perf_counter()
+    O.mix_recurrence(x, *prm)
+    dt = time.perf_counter() - t0
+    n = cfg.B * cfg.L * cfg.D
+    return {"value": n / dt, "unit": "tokens*ch/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole prefill workload B={cfg.B} L={cfg.L} D={cfg.D} M={cfg.M}: "
+                      f"float64 numpy recurrence vectorised over (b, d, m), one host thread, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--decode-steps", type=int, default=32768)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build runs the operator on a single "
+              f"MI355X (got --gpus {args.gpus}); sharding across GPUs is not part of it.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import workloads as W
+    from paper_2607_05583_amd import _lib, ops
+    from paper_2607_05583_amd._lib import RES_OP_FWD
+
+    assert torch.cuda.is_available(), "bench.py needs a HIP device"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lib = _lib.lib()
+
+    # ---------------- prefill (the timed step) ----------------
+    cfg = W.CONFIGS[3]
+    log(f"prefill workload {cfg.name}")
+    inp = W.fwd_inputs(cfg)
+    prm = [torch.from_numpy(inp[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+    x0 = torch.from_numpy(inp["x"].view(np.int16)).view(torch.bfloat16).to(dev)
+    NSET = 3
+    xs = [x0] + [x0.roll(shifts=i * 997, dims=1).contiguous() for i in range(1, NSET)]
+    ys = [torch.empty_like(x0) for _ in range(NSET)]
+    hs = [torch.empty((cfg.B, cfg.D, cfg.M, 2), dtype=torch.float32, device=dev) for _ in range(NSET)]
+    B, L, D, M = cfg.B, cfg.L, cfg.D, cfg.M
+    wsn = ops.workspace_bytes(RES_OP_FWD, torch.bfloat16, B, L, D, M)
+    ws = torch.empty(wsn, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    import ctypes
+    sp = ctypes.c_void_p(stream.cuda_stream)
+    P = [ctypes.c_void_p(p.data_ptr()) for p in prm]
+
+    def fwd(i, ev=None):
+        if ev is not None:
+            _lib.check(lib.resonator_set_kernel_timer(ctypes.c_void_p(ev[0].cuda_event),
+                                                      ctypes.c_void_p(ev[1].cuda_event)))
+        _lib.check(lib.resonator_mix_fwd(
+            ctypes.c_void_p(xs[i].data_ptr()), _lib.RES_BF16, ctypes.c_void_p(ys[i].data_ptr()),
+            _lib.RES_BF16, B, L, D, M, *P, None, ctypes.c_void_p(hs[i].data_ptr()),
+            ctypes.c_void_p(ws.data_ptr()), wsn, sp))
+
+    for i in range(args.warmup):
+        fwd(i % NSET)
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    for a, b in evs:  # torch creates events lazily: record once so the handles exist
+        a.record(stream)
+        b.record(stream)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(args.steps):
+        fwd(i % NSET, evs[i])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+    ms_total = start.elapsed_time(stop)
+    ms_step = ms_total / args.steps
+    k_ms = [a.elapsed_time(b) for a, b in evs]
+    k_avg_ms = float(np.mean(k_ms))
+    n_tok = B * L * D
+    value = n_tok / (ms_step * 1e-3)
+    alg_bytes = n_tok * 4
+    achieved = alg_bytes / (k_avg_ms * 1e-3) / 1e9
+    log(f"prefill: {ms_step * 1e3:.1f} us/step (events), apply kernel {k_avg_ms * 1e3:.1f} us, "
+        f"wall {t_wall / args.steps * 1e3:.1f} us/step")
+
+    # ---------------- decode ----------------
+    c4 = W.CONFIGS[4]
+    log(f"decode workload {c4.name}")
+    di = W.DecodeInputs(c4)
+    dprm = [torch.from_numpy(di.params[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+    prompt = torch.from_numpy(di.prompt.view(np.int16)).view(torch.bfloat16).to(dev)
+    state = ops.resonator_state_init(prompt, *dprm)
+    nsteps = args.decode_steps
+    chunk = 4096
+    xdec = torch.from_numpy(di.steps(min(chunk, nsteps)).view(np.int16)).view(torch.bfloat16).to(dev)
+    ydec = torch.empty_like(xdec)
+    DP = [ctypes.c_void_p(p.data_ptr()) for p in dprm]
+    sptr = ctypes.c_void_p(state.data_ptr())
+    Bd, Dd, Md = c4.B, c4.D, c4.M
+    xptr = [ctypes.c_void_p(xdec[j].data_ptr()) for j in range(xdec.shape[0])]
+    yptr = [ctypes.c_void_p(ydec[j].data_ptr()) for j in range(xdec.shape[0])]
+
+    def dstep(j):
+        _lib.check(lib.resonator_decode_step(xptr[j], _lib.RES_BF16, yptr[j], _lib.RES_BF16, Bd, Dd,
+                                             Md, *DP, sptr, sp))
+
+    for j in range(64):
+        dstep(j)
+    torch.cuda.synchronize()
+    d0, d1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    d0.record(stream)
+    for s in range(nsteps):
+        dstep(s % xdec.shape[0])
+    d1.record(stream)
+    torch.cuda.synchronize()
+    dec_eager_us = d0.elapsed_time(d1) * 1e3 / nsteps
+    # graph replay of the same calls (kernel launches only; no allocation, no memset)
+    G = 512
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream(dev)
+    cap.wait_stream(stream)
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            csp = ctypes.c_void_p(cap.cuda_stream)
+            for j in range(G):
+                _lib.check(lib.resonator_decode_step(xptr[j], _lib.RES_BF16, yptr[j], _lib.RES_BF16,
+                                                     Bd, Dd, Md, *DP, sptr, csp))
+    stream.wait_stream(cap)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    reps = max(1, nsteps // G)
+    d0.record(stream)
+    for _ in range(reps):
+        g.replay()
+    d1.record(stream)
+    torch.cuda.synchronize()
+    dec_graph_us = d0.elapsed_time(d1) * 1e3 / (reps * G)
+    dec_bytes = Bd * Dd * (Md * 16 + 2 + 2)
+    log(f"decode: eager {dec_eager_us:.2f} us/step, graph {dec_graph_us:.2f} us/step")
+
+    # ---------------- training layer (fwd + bwd) ----------------
+    c5 = W.CONFIGS[5]
+    li = W.train_layer_inputs(c5, 0)
+    tprm = [torch.from_numpy(li[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+    tx = torch.from_numpy(li["x"].view(np.int16)).view(torch.bfloat16).to(dev)
+    tdy = torch.from_numpy(li["dy"].view(np.int16)).view(torch.bfloat16).to(dev)
+    for _ in range(3):
+        ops.resonator_mix_fwd(tx, *tprm)
+        ops.resonator_mix_bwd(tx, tdy, *tprm)
+    torch.cuda.synchronize()
+    nt = 10
+    t0e, t1e, t2e = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    t0e.record(stream)
+    for _ in range(nt):
+        ops.resonator_mix_fwd(tx, *tprm)
+    t1e.record(stream)
+    for _ in range(nt):
+        ops.resonator_mix_bwd(tx, tdy, *tprm)
+    t2e.record(stream)
+    torch.cuda.synchronize()
+    tr_fwd_us = t0e.elapsed_time(t1e) * 1e3 / nt
+    tr_bwd_us = t1e.elapsed_time(t2e) * 1e3 / nt
+    log(f"train layer: fwd {tr_fwd_us:.1f} us, bwd {tr_bwd_us:.1f} us")
+
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline (oracle recurrence) ...")
+        cpu = cpu_baseline(cfg)
+
+    traffic = counter_traffic(n_tok)
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "tokens*ch/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "B": B, "L": L, "D": D, "M": M,
+                   "activations": "bf16 in/out, fp32 accumulate, split-bf16 MFMA operands",
+                   "terminal_state": True, "buffer_sets": NSET},
+        "decode": {"workload": c4.name, "steps": nsteps,
+                   "steps_per_s_eager": 1e6 / dec_eager_us, "us_per_step_eager": dec_eager_us,
+                   "steps_per_s_graph": 1e6 / dec_graph_us, "us_per_step_graph": dec_graph_us,
+                   "alg_GBs_graph": dec_bytes / (dec_graph_us * 1e-6) / 1e9},
+        "train_layer": {"workload": "B8 L8192 D256 M8 bf16 (one of the 6 layers)",
+                        "fwd_us": tr_fwd_us, "bwd_us": tr_bwd_us,
+                        "bwd_alg_GBs": 8 * 8192 * 256 * 6 / (tr_bwd_us * 1e-6) / 1e9},
+        "roofline": {"bound": "hbm", "kernel": "fwd_tile_kernel (apply)",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic,
+                     "alg_bytes_per_launch": alg_bytes, "avg_launch_us": k_avg_ms * 1e3},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,157 @@
+/*
+ * resonator.h -- C ABI of the MI355X (gfx950) causal resonant field mixing library.
+ *
+ * The operator is ResonatorLM's replacement for self-attention (arXiv 2607.05583,
+ * Sec. 3).  Per channel d the drive x[b, t, d] is mixed causally through a bank of
+ * M damped resonators:
+ *
+ *   K_d[tau] = sum_m a[d,m] exp(-gamma[d,m] tau) cos(omega[d,m] tau + phi[d,m])   (Sec. 3.1, kernel eq.)
+ *   y[b,t,d] = sum_{s<=t} K_d[t-s] x[b,s,d]  +  Re sum_m c[d,m] lambda[d,m]^(t+1) h0[b,d,m]
+ *                                                                                 (Sec. 3.2, causal conv eq.)
+ * equivalently the complex diagonal recurrence (Sec. 3.3)
+ *   h_t = lambda h_{t-1} + x_t,  h_{-1} = h0,  y_t = Re sum_m c h_t,
+ *   lambda = exp(-gamma) (cos omega + i sin omega),  c = a (cos phi + i sin phi).
+ * The readout phase sign follows the kernel of Sec. 3.1 (the decode equation of
+ * Sec. 3.3 prints e^{-i phi}; with it decode would not reproduce the kernel).
+ *
+ * Conventions shared by every entry point
+ *   - All pointers are DEVICE pointers unless stated otherwise; the caller owns
+ *     every buffer (inputs, outputs, workspace).  Apart from two thread-local
+ *     items (the last error text and the armed measurement hook) the library
+ *     keeps no state between calls and is safe to call from several host threads.
+ *   - Every call is asynchronous on `stream` (a hipStream_t passed as void*;
+ *     NULL = the default stream).  It returns once the kernels are enqueued.
+ *   - Activations x, y, dy, dx: row-major [B][L][D] (channels fastest), element
+ *     type given by a res_dtype_t.  bfloat16 is stored as its 16-bit pattern and
+ *     rounded to nearest even on output.  Arithmetic is float32 (MFMA with fp32
+ *     accumulation; bf16 MFMA operands when activations are bf16), with the
+ *     parameter-derived constants computed in float64 from exact integer lags.
+ *   - Parameters gamma, omega, amp, phase: float32 [D][M], row-major (m fastest).
+ *     gamma >= 0 is a precondition (not checked on the device); any finite omega,
+ *     amp, phase is accepted as given (no clamping).
+ *   - States (h0, h_out, state): float32 [B][D][M][2] = (re, im) interleaved.
+ *   - Sizes are int64; B, D >= 1, L >= 1 (L_prompt >= 0 for state_init),
+ *     1 <= M <= RES_M_MAX.
+ *   - Pointer alignment: float32 tensors 4 bytes, bf16 tensors 2 bytes, the
+ *     workspace 256 bytes.
+ *   - Errors: a non-OK status means nothing was launched and no output was
+ *     touched; resonator_last_error() then returns a description (thread-local).
+ *     RES_ERR_HIP reports a failed launch; faults inside kernels surface at the
+ *     caller's next synchronisation.  No C++ exception crosses the ABI.
+ */
+#ifndef RESONATOR_H
+#define RESONATOR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { RES_F32 = 0, RES_BF16 = 1 } res_dtype_t;
+
+enum {
+  RES_OK = 0,
+  RES_ERR_INVALID_ARG = 1,   /* null pointer, bad size, aliasing, bad op code   */
+  RES_ERR_UNSUPPORTED = 2,   /* dtype pair or M outside what the kernels support */
+  RES_ERR_MISALIGNED = 3,    /* pointer not aligned as stated above              */
+  RES_ERR_WORKSPACE = 4,     /* workspace null or smaller than required          */
+  RES_ERR_HIP = 5            /* HIP runtime error when launching                 */
+};
+
+enum { RES_OP_FWD = 0, RES_OP_BWD = 1, RES_OP_STATE_INIT = 2 };
+
+#define RES_M_MAX 16
+
+/* Library ABI version (major * 100 + minor). */
+int resonator_version(void);
+
+/*
+ * Bytes of device workspace that op (RES_OP_*) needs for activations of type
+ * act_dt at sizes (B, L, D, M).  Returns 0 for invalid arguments.  The workspace
+ * holds parameter tables, per-tile chunk states, carries and (for bwd) per-tile
+ * partial sums; its contents need not be initialised and are clobbered.
+ */
+size_t resonator_workspace_bytes(int op, res_dtype_t act_dt, int64_t B, int64_t L, int64_t D,
+                                 int64_t M);
+
+/*
+ * Forward mixing (Sec. 3.1 kernel, Sec. 3.2 causal convolution).
+ *   x      [B][L][D] of x_dt            drive
+ *   y      [B][L][D] of y_dt            output; must not overlap x
+ *   gamma, omega, amp, phase [D][M]     float32 resonator parameters
+ *   h0     [B][D][M][2] or NULL         state before t = 0 (NULL = zero)
+ *   h_out  [B][D][M][2] or NULL         terminal state h_{L-1} (may alias h0)
+ *   ws     workspace of resonator_workspace_bytes(RES_OP_FWD, x_dt, B, L, D, M)
+ * Supported (x_dt, y_dt): (F32, F32), (BF16, BF16), (BF16, F32).
+ */
+int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B,
+                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
+                      const float* amp, const float* phase, const float* h0, float* h_out,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of resonator_mix_fwd for the loss sum(dy * y) (gradients derived from
+ * the Sec. 3.1 kernel; the paper trains through autograd and prints none).
+ *   x, dy  [B][L][D] of act_dt          forward drive and upstream gradient
+ *   dx     [B][L][D] of act_dt          gradient w.r.t. x (overwritten)
+ *   h0     [B][D][M][2] or NULL         the forward's initial state (NULL = zero)
+ *   dgamma, domega, damp, dphase [D][M] float32, overwritten (not accumulated)
+ *   dh0    [B][D][M][2] or NULL         gradient w.r.t. h0 (overwritten)
+ *   ws     workspace of resonator_workspace_bytes(RES_OP_BWD, act_dt, B, L, D, M)
+ * act_dt is F32 or BF16.  dx must not overlap x or dy.  Parameter gradients are
+ * reduced in a fixed order (float64), so they are bitwise reproducible.
+ */
+int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* dx, int64_t B,
+                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
+                      const float* amp, const float* phase, const float* h0, float* dgamma,
+                      float* domega, float* damp, float* dphase, float* dh0, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/*
+ * Prompt state for decoding (Sec. 3.2, cache construction): the weighted sum of
+ * past drives under the complex decay factor, state[b,d,m] = sum_s lambda^(L-1-s)
+ * x[b,s,d] (newest drive weight 1), from a zero initial state.
+ *   x_prompt  [B][L_prompt][D] of x_dt, may be NULL when L_prompt == 0
+ *   state_out [B][D][M][2] float32       written
+ *   ws        workspace of resonator_workspace_bytes(RES_OP_STATE_INIT, x_dt, B, L_prompt, D, M)
+ *             (may be NULL / 0 bytes when L_prompt == 0)
+ */
+int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int64_t L_prompt,
+                         int64_t D, int64_t M, const float* gamma, const float* omega,
+                         const float* amp, const float* phase, float* state_out, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/*
+ * One recurrent decode step for every (b, d) (Sec. 3.3):
+ *   state <- lambda state + x_t;   y_t = Re sum_m c state.
+ *   x_t    [B][D] of x_dt;  y_t [B][D] of y_dt (not overlapping x_t or state)
+ *   state  [B][D][M][2] float32, read and updated in place
+ * lambda is applied as a float32 hi + lo pair computed in float64, so long runs
+ * do not accumulate the phase error of a single rounded pole.
+ * Supported (x_dt, y_dt) as for resonator_mix_fwd.  Needs no workspace.
+ */
+int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtype_t y_dt,
+                          int64_t B, int64_t D, int64_t M, const float* gamma, const float* omega,
+                          const float* amp, const float* phase, float* state, void* stream);
+
+/*
+ * Measurement hook.  Arms a pair of HIP events (hipEvent_t passed as void*) on the
+ * calling thread: the next resonator_mix_fwd or resonator_mix_bwd call on this
+ * thread records start_event immediately before and stop_event immediately after
+ * its dominant kernel (the one that reads the activations and writes the output),
+ * on the call's stream; the hook then disarms itself.  Pass NULL, NULL to disarm.
+ * The events belong to the caller.  Returns RES_OK, or RES_ERR_INVALID_ARG if
+ * exactly one of the two is NULL.
+ */
+int resonator_set_kernel_timer(void* start_event, void* stop_event);
+
+/* Text describing the last non-OK status returned on this thread. */
+const char* resonator_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RESONATOR_H */

@@ -1,0 +1,70 @@
+"""ctypes loader of libresonator.so (the HIP kernels behind include/resonator.h).
+
+The library must have been built in-tree (``__graft_entry__.build()`` or
+``python -m paper_2607_05583_amd._build``).  There is no fallback: if the library
+is missing or fails to load, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libresonator.so")
+
+RES_F32, RES_BF16 = 0, 1
+RES_OK, RES_ERR_INVALID_ARG, RES_ERR_UNSUPPORTED, RES_ERR_MISALIGNED, RES_ERR_WORKSPACE, RES_ERR_HIP = range(6)
+RES_OP_FWD, RES_OP_BWD, RES_OP_STATE_INIT = 0, 1, 2
+RES_M_MAX = 16
+
+SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd",
+           "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
+           "resonator_set_kernel_timer", "resonator_last_error")
+
+_lib = None
+
+
+class ResonatorError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"resonator error {code}: {msg}")
+        self.code = code
+
+
+def _declare(lib):
+    vp, i64, i32, sz, fp = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_size_t, ctypes.c_void_p
+    lib.resonator_version.restype = i32
+    lib.resonator_version.argtypes = []
+    lib.resonator_last_error.restype = ctypes.c_char_p
+    lib.resonator_last_error.argtypes = []
+    lib.resonator_workspace_bytes.restype = sz
+    lib.resonator_workspace_bytes.argtypes = [i32, i32, i64, i64, i64, i64]
+    lib.resonator_mix_fwd.restype = i32
+    lib.resonator_mix_fwd.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, fp,
+                                      vp, sz, vp]
+    lib.resonator_mix_bwd.restype = i32
+    lib.resonator_mix_bwd.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, fp, fp, fp, fp, fp,
+                                      fp, fp, fp, fp, fp, vp, sz, vp]
+    lib.resonator_state_init.restype = i32
+    lib.resonator_state_init.argtypes = [vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp, sz, vp]
+    lib.resonator_set_kernel_timer.restype = i32
+    lib.resonator_set_kernel_timer.argtypes = [vp, vp]
+    lib.resonator_decode_step.restype = i32
+    lib.resonator_decode_step.argtypes = [vp, i32, vp, i32, i64, i64, i64, fp, fp, fp, fp, fp, vp]
+
+
+def lib():
+    """The loaded library (loaded once).  Raises if it is not built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() first "
+                               "(there is no CPU or PyTorch fallback)")
+        l = ctypes.CDLL(LIB_PATH)
+        _declare(l)
+        _lib = l
+    return _lib
+
+
+def check(rc: int):
+    if rc != RES_OK:
+        raise ResonatorError(rc, lib().resonator_last_error().decode(errors="replace"))

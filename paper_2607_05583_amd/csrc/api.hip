@@ -1,0 +1,351 @@
+// C ABI of the resonant mixing library: argument validation, workspace layout
+// and kernel dispatch.  Declared in include/resonator.h.
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/resonator.h"
+#include "common.h"
+#include "kernels.h"
+
+using namespace res;
+
+namespace {
+
+thread_local std::string g_err;
+// Armed by resonator_set_kernel_timer for the next dominant-kernel launch.
+thread_local hipEvent_t g_ev0 = nullptr, g_ev1 = nullptr;
+
+void take_timer(hipEvent_t* e0, hipEvent_t* e1) {
+  *e0 = g_ev0;
+  *e1 = g_ev1;
+  g_ev0 = g_ev1 = nullptr;
+}
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(RES_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+size_t elt_size(res_dtype_t t) { return t == RES_BF16 ? 2 : 4; }
+bool dtype_ok(int t) { return t == RES_F32 || t == RES_BF16; }
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+// Geometry of the tiled kernels for activations of type act (tile width depends
+// on the element size: 128-byte rows).
+Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) {
+  Geometry g;
+  g.B = B;
+  g.L = L;
+  g.D = D;
+  g.M = M;
+  g.DW = act == RES_BF16 ? 64 : 32;
+  g.NB = (int)((D + g.DW - 1) / g.DW);
+  g.Dp = g.NB * g.DW;
+  g.MG = (int)((M + MODES_PER_GROUP - 1) / MODES_PER_GROUP);
+  g.Mp = MODES_PER_GROUP * g.MG;
+  g.P = L > 0 ? (L + TILE_T - 1) / TILE_T : 0;
+  g.last_len = L > 0 ? (int)(L - (g.P - 1) * TILE_T) : 0;
+  return g;
+}
+
+WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
+  WsLayout w{};
+  size_t off = 0;
+  (void)act;
+  const int nm = op == RES_OP_BWD ? bwd_mats(g.MG) : fwd_mats(g.MG);
+  const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;
+  w.tab = off;
+  off += align256((size_t)g.Dp * nm * TAB_MAT_BYTES);
+  w.scal = off;
+  off += align256((size_t)g.Dp * g.Mp * sizeof(ModeScalars));
+  w.carryc = off;
+  off += align256((size_t)g.Dp * g.Mp * sizeof(ModeCarry));
+  const size_t state_bytes = op == RES_OP_BWD ? sizeof(float4) : sizeof(float2);
+  w.agg = off;
+  off += align256(tiles_modes * state_bytes);
+  w.carry = off;
+  if (op != RES_OP_STATE_INIT) off += align256(tiles_modes * state_bytes);
+  w.flags = off;
+  w.part = off;
+  if (op == RES_OP_BWD) off += align256((size_t)g.B * g.P * g.Dp * (16 + 4 * g.Mp) * sizeof(float));
+  w.q0 = off;
+  if (op == RES_OP_BWD) off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float4));
+  w.total = off;
+  return w;
+}
+
+int check_sizes(int64_t B, int64_t L, int64_t D, int64_t M, bool allow_l0) {
+  if (B < 1 || D < 1) return fail(RES_ERR_INVALID_ARG, "B and D must be >= 1 (got B=%lld D=%lld)",
+                                  (long long)B, (long long)D);
+  if (L < (allow_l0 ? 0 : 1))
+    return fail(RES_ERR_INVALID_ARG, "L must be >= %d (got %lld)", allow_l0 ? 0 : 1, (long long)L);
+  if (M < 1 || M > RES_M_MAX)
+    return fail(M < 1 ? RES_ERR_INVALID_ARG : RES_ERR_UNSUPPORTED,
+                "M must be in [1, %d] (got %lld)", RES_M_MAX, (long long)M);
+  if (D > (1 << 24) || B > (1LL << 31) || L > (1LL << 40))
+    return fail(RES_ERR_UNSUPPORTED, "sizes beyond the supported range (B=%lld L=%lld D=%lld)",
+                (long long)B, (long long)L, (long long)D);
+  const int64_t tiles = B * ((L + TILE_T - 1) / TILE_T) * ((D + 31) / 32);
+  if (tiles >= (1LL << 31))
+    return fail(RES_ERR_UNSUPPORTED, "too many tiles for one launch (%lld)", (long long)tiles);
+  return RES_OK;
+}
+
+int check_params(const float* gamma, const float* omega, const float* amp, const float* phase) {
+  if (!gamma || !omega || !amp || !phase)
+    return fail(RES_ERR_INVALID_ARG, "gamma, omega, amp and phase must be non-null");
+  if (!aligned(gamma, 4) || !aligned(omega, 4) || !aligned(amp, 4) || !aligned(phase, 4))
+    return fail(RES_ERR_MISALIGNED, "parameter arrays must be 4-byte aligned");
+  return RES_OK;
+}
+
+bool overlap(const void* a, size_t an, const void* b, size_t bn) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + bn && y < x + an;
+}
+
+}  // namespace
+
+extern "C" {
+
+int resonator_version(void) { return 100; }
+
+const char* resonator_last_error(void) { return g_err.c_str(); }
+
+int resonator_set_kernel_timer(void* start_event, void* stop_event) {
+  if ((start_event == nullptr) != (stop_event == nullptr))
+    return fail(RES_ERR_INVALID_ARG, "pass both events or neither");
+  g_ev0 = (hipEvent_t)start_event;
+  g_ev1 = (hipEvent_t)stop_event;
+  return RES_OK;
+}
+
+size_t resonator_workspace_bytes(int op, res_dtype_t act_dt, int64_t B, int64_t L, int64_t D,
+                                 int64_t M) {
+  if (op != RES_OP_FWD && op != RES_OP_BWD && op != RES_OP_STATE_INIT) return 0;
+  if (!dtype_ok(act_dt)) return 0;
+  if (B < 1 || D < 1 || M < 1 || M > RES_M_MAX || L < (op == RES_OP_STATE_INIT ? 0 : 1)) return 0;
+  if (L == 0) return 0;
+  return make_layout(op, act_dt, make_geom(act_dt, B, L, D, M)).total;
+}
+
+int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B,
+                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
+                      const float* amp, const float* phase, const float* h0, float* h_out,
+                      void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_sizes(B, L, D, M, false);
+  if (rc) return rc;
+  if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (x_dt == RES_F32 && y_dt == RES_BF16)
+    return fail(RES_ERR_UNSUPPORTED, "dtype pair f32 -> bf16 is not supported");
+  if (!x || !y) return fail(RES_ERR_INVALID_ARG, "x and y must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  if (!aligned(x, elt_size(x_dt)) || !aligned(y, elt_size(y_dt)) || (h0 && !aligned(h0, 4)) ||
+      (h_out && !aligned(h_out, 4)))
+    return fail(RES_ERR_MISALIGNED, "activation/state pointers must be aligned to their element");
+  const size_t n = (size_t)(B * L * D);
+  if (overlap(x, n * elt_size(x_dt), y, n * elt_size(y_dt)))
+    return fail(RES_ERR_INVALID_ARG, "y must not overlap x");
+  const Geometry g = make_geom(x_dt, B, L, D, M);
+  const WsLayout w = make_layout(RES_OP_FWD, x_dt, g);
+  if (!ws || ws_bytes < w.total)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", w.total, ws_bytes);
+  if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+
+  hipStream_t st = (hipStream_t)stream;
+  char* base = (char*)ws;
+  ModeScalars* scal = (ModeScalars*)(base + w.scal);
+  ModeCarry* cc = (ModeCarry*)(base + w.carryc);
+  hipError_t e = x_dt == RES_BF16
+                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
+                     : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
+  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  FwdArgs a{};
+  a.x = x;
+  a.y = y;
+  a.B = B;
+  a.L = L;
+  a.D = (int)D;
+  a.M = (int)M;
+  a.NB = g.NB;
+  a.Dp = g.Dp;
+  a.Mp = g.Mp;
+  a.P = g.P;
+  a.last_len = g.last_len;
+  a.tab = base + w.tab;
+  a.scal = scal;
+  a.agg = (float2*)(base + w.agg);
+  a.carry = (const float2*)(base + w.carry);
+  hipEvent_t ev0, ev1;
+  take_timer(&ev0, &ev1);
+  auto tile = [&](int mode, hipEvent_t e0, hipEvent_t e1) {
+    if (x_dt == RES_F32) return launch_fwd_tile<float, float>(g, mode, a, st, e0, e1);
+    if (y_dt == RES_BF16) return launch_fwd_tile<bf16_t, bf16_t>(g, mode, a, st, e0, e1);
+    return launch_fwd_tile<bf16_t, float>(g, mode, a, st, e0, e1);
+  };
+  if ((e = tile(MODE_STATE, nullptr, nullptr)) != hipSuccess) return hip_fail(e, "tile-state launch");
+  if ((e = launch_carry_fwd(g, a.agg, (float2*)(base + w.carry), h0, h_out, cc, st)) != hipSuccess)
+    return hip_fail(e, "carry launch");
+  if ((e = tile(MODE_APPLY, ev0, ev1)) != hipSuccess) return hip_fail(e, "tile-apply launch");
+  return RES_OK;
+}
+
+int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int64_t L_prompt,
+                         int64_t D, int64_t M, const float* gamma, const float* omega,
+                         const float* amp, const float* phase, float* state_out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  int rc = check_sizes(B, L_prompt, D, M, true);
+  if (rc) return rc;
+  if (!dtype_ok(x_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!state_out) return fail(RES_ERR_INVALID_ARG, "state_out must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  if (!aligned(state_out, 4)) return fail(RES_ERR_MISALIGNED, "state_out must be 4-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  if (L_prompt == 0) {
+    const hipError_t e = launch_fill_zero(state_out, B * D * M * 2, st);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "fill launch");
+  }
+  if (!x_prompt) return fail(RES_ERR_INVALID_ARG, "x_prompt must be non-null when L_prompt > 0");
+  if (!aligned(x_prompt, elt_size(x_dt))) return fail(RES_ERR_MISALIGNED, "x_prompt misaligned");
+  const Geometry g = make_geom(x_dt, B, L_prompt, D, M);
+  const WsLayout w = make_layout(RES_OP_STATE_INIT, x_dt, g);
+  if (!ws || ws_bytes < w.total)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", w.total, ws_bytes);
+  if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+  char* base = (char*)ws;
+  ModeScalars* scal = (ModeScalars*)(base + w.scal);
+  ModeCarry* cc = (ModeCarry*)(base + w.carryc);
+  hipError_t e = x_dt == RES_BF16
+                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
+                     : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
+  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  FwdArgs a{};
+  a.x = x_prompt;
+  a.y = nullptr;
+  a.B = B;
+  a.L = L_prompt;
+  a.D = (int)D;
+  a.M = (int)M;
+  a.NB = g.NB;
+  a.Dp = g.Dp;
+  a.Mp = g.Mp;
+  a.P = g.P;
+  a.last_len = g.last_len;
+  a.tab = base + w.tab;
+  a.scal = scal;
+  a.agg = (float2*)(base + w.agg);
+  a.carry = nullptr;
+  e = x_dt == RES_F32 ? launch_fwd_tile<float, float>(g, MODE_STATE, a, st)
+                      : launch_fwd_tile<bf16_t, bf16_t>(g, MODE_STATE, a, st);
+  if (e != hipSuccess) return hip_fail(e, "tile-state launch");
+  if ((e = launch_carry_fwd(g, a.agg, nullptr, nullptr, state_out, cc, st)) != hipSuccess)
+    return hip_fail(e, "carry launch");
+  return RES_OK;
+}
+
+int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* dx, int64_t B,
+                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
+                      const float* amp, const float* phase, const float* h0, float* dgamma,
+                      float* domega, float* damp, float* dphase, float* dh0, void* ws,
+                      size_t ws_bytes, void* stream) {
+  int rc = check_sizes(B, L, D, M, false);
+  if (rc) return rc;
+  if (!dtype_ok(act_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!x || !dy || !dx) return fail(RES_ERR_INVALID_ARG, "x, dy and dx must be non-null");
+  if (!dgamma || !domega || !damp || !dphase)
+    return fail(RES_ERR_INVALID_ARG, "dgamma, domega, damp and dphase must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  const size_t es = elt_size(act_dt);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(dx, es) || (h0 && !aligned(h0, 4)) ||
+      (dh0 && !aligned(dh0, 4)) || !aligned(dgamma, 4) || !aligned(domega, 4) ||
+      !aligned(damp, 4) || !aligned(dphase, 4))
+    return fail(RES_ERR_MISALIGNED, "pointers must be aligned to their element");
+  const size_t n = (size_t)(B * L * D) * es;
+  if (overlap(dx, n, x, n) || overlap(dx, n, dy, n))
+    return fail(RES_ERR_INVALID_ARG, "dx must not overlap x or dy");
+  const Geometry g = make_geom(act_dt, B, L, D, M);
+  const WsLayout w = make_layout(RES_OP_BWD, act_dt, g);
+  if (!ws || ws_bytes < w.total)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", w.total, ws_bytes);
+  if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  char* base = (char*)ws;
+  ModeScalars* scal = (ModeScalars*)(base + w.scal);
+  ModeCarry* cc = (ModeCarry*)(base + w.carryc);
+  hipError_t e = act_dt == RES_BF16
+                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st)
+                     : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st);
+  if (e != hipSuccess) return hip_fail(e, "prep launch");
+  BwdArgs a{};
+  a.x = x;
+  a.dy = dy;
+  a.dx = dx;
+  a.B = B;
+  a.L = L;
+  a.D = (int)D;
+  a.M = (int)M;
+  a.NB = g.NB;
+  a.Dp = g.Dp;
+  a.Mp = g.Mp;
+  a.P = g.P;
+  a.last_len = g.last_len;
+  a.tab = base + w.tab;
+  a.scal = scal;
+  a.agg = (float4*)(base + w.agg);
+  a.carry = (const float4*)(base + w.carry);
+  a.part = (float*)(base + w.part);
+  float4* q0 = (float4*)(base + w.q0);
+  hipEvent_t ev0, ev1;
+  take_timer(&ev0, &ev1);
+  auto tile = [&](int mode, hipEvent_t e0, hipEvent_t e1) {
+    return act_dt == RES_BF16 ? launch_bwd_tile<bf16_t>(g, mode, a, st, e0, e1)
+                              : launch_bwd_tile<float>(g, mode, a, st, e0, e1);
+  };
+  if ((e = tile(MODE_STATE, nullptr, nullptr)) != hipSuccess) return hip_fail(e, "bwd tile-state launch");
+  if ((e = launch_carry_bwd(g, a.agg, (float4*)(base + w.carry), q0, cc, st)) != hipSuccess)
+    return hip_fail(e, "bwd carry launch");
+  if ((e = tile(MODE_APPLY, ev0, ev1)) != hipSuccess) return hip_fail(e, "bwd tile-apply launch");
+  if ((e = launch_bwd_reduce(g, a.part, q0, gamma, omega, amp, phase, h0, dgamma, domega, damp,
+                             dphase, dh0, st)) != hipSuccess)
+    return hip_fail(e, "bwd reduce launch");
+  return RES_OK;
+}
+
+int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtype_t y_dt,
+                          int64_t B, int64_t D, int64_t M, const float* gamma, const float* omega,
+                          const float* amp, const float* phase, float* state, void* stream) {
+  int rc = check_sizes(B, 1, D, M, false);
+  if (rc) return rc;
+  if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (x_dt == RES_F32 && y_dt == RES_BF16)
+    return fail(RES_ERR_UNSUPPORTED, "dtype pair f32 -> bf16 is not supported");
+  if (!x_t || !y_t || !state) return fail(RES_ERR_INVALID_ARG, "x_t, y_t and state must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  if (!aligned(x_t, elt_size(x_dt)) || !aligned(y_t, elt_size(y_dt)) || !aligned(state, 8))
+    return fail(RES_ERR_MISALIGNED, "x_t/y_t aligned to their element, state to 8 bytes");
+  const size_t n = (size_t)(B * D);
+  if (overlap(y_t, n * elt_size(y_dt), x_t, n * elt_size(x_dt)) ||
+      overlap(y_t, n * elt_size(y_dt), state, n * M * 8))
+    return fail(RES_ERR_INVALID_ARG, "y_t must not overlap x_t or state");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (x_dt == RES_F32)
+    e = launch_decode<float, float>(B, D, M, x_t, y_t, gamma, omega, amp, phase, state, st);
+  else if (y_dt == RES_BF16)
+    e = launch_decode<bf16_t, bf16_t>(B, D, M, x_t, y_t, gamma, omega, amp, phase, state, st);
+  else
+    e = launch_decode<bf16_t, float>(B, D, M, x_t, y_t, gamma, omega, amp, phase, state, st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "decode launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,83 @@
+// Internal launch interface between the C ABI (api.hip) and the kernel files.
+#pragma once
+
+#include <hip/hip_ext.h>
+
+#include "common.h"
+
+namespace res {
+
+enum { MODE_STATE = 0, MODE_APPLY = 1 };
+
+struct FwdArgs {
+  const void* x;
+  void* y;
+  int64_t B, L;
+  int D, M;
+  int NB, Dp, Mp;
+  int64_t P;
+  int last_len;
+  const void* tab;
+  const ModeScalars* scal;
+  float2* agg;
+  const float2* carry;
+};
+
+struct BwdArgs {
+  const void* x;
+  const void* dy;
+  void* dx;
+  int64_t B, L;
+  int D, M;
+  int NB, Dp, Mp;
+  int64_t P;
+  int last_len;
+  const void* tab;
+  const ModeScalars* scal;
+  float4* agg;          // per tile (Q, rho) at the tile's left edge, zero entering from the right
+  const float4* carry;  // per tile (Q, rho) entering from the right edge
+  float* part;          // per tile partial sums
+};
+
+template <typename TA>
+hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
+                       const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
+                       hipStream_t st);
+
+template <typename TX, typename TY>
+hipError_t launch_fwd_tile(const Geometry& g, int mode, const FwdArgs& a, hipStream_t st,
+                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+
+hipError_t launch_carry_fwd(const Geometry& g, const float2* agg, float2* carry, const float* h0,
+                            float* hout, const ModeCarry* cc, hipStream_t st);
+
+// Launch with optional start/stop events recorded around this one kernel.
+template <typename K, typename... Args>
+inline void launch_timed(K kernel, dim3 grid, dim3 block, hipStream_t st, hipEvent_t ev0,
+                         hipEvent_t ev1, Args... args) {
+  if (ev0 != nullptr)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, st, ev0, ev1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, st, args...);
+}
+
+hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t st);
+
+template <typename TX, typename TY>
+hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y,
+                         const float* gamma, const float* omega, const float* amp,
+                         const float* phase, float* state, hipStream_t st);
+
+template <typename TX>
+hipError_t launch_bwd_tile(const Geometry& g, int mode, const BwdArgs& a, hipStream_t st,
+                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+
+hipError_t launch_carry_bwd(const Geometry& g, const float4* agg, float4* carry, float4* q0,
+                            const ModeCarry* cc, hipStream_t st);
+
+hipError_t launch_bwd_reduce(const Geometry& g, const float* part, const float4* q0,
+                             const float* gamma, const float* omega, const float* amp,
+                             const float* phase, const float* h0, float* dgamma, float* domega,
+                             float* damp, float* dphase, float* dh0, hipStream_t st);
+
+}  // namespace res

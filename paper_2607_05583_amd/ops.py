@@ -1,0 +1,178 @@
+"""PyTorch binding of the resonant mixing library.
+
+Thin argument marshalling over the C ABI of include/resonator.h: every step of
+the operator runs in the library's HIP kernels; PyTorch only provides device
+memory and the current stream.  Function names follow the C entry points.
+
+Tensors: activations [B, L, D] (float32 or bfloat16, contiguous, on the GPU);
+parameters gamma, omega, amp, phase float32 [D, M]; states float32 [B, D, M, 2].
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+from ._lib import RES_BF16, RES_F32, RES_OP_BWD, RES_OP_FWD, RES_OP_STATE_INIT, check
+
+_DT = {torch.float32: RES_F32, torch.bfloat16: RES_BF16}
+
+
+def _code(t: torch.Tensor) -> int:
+    if t.dtype not in _DT:
+        raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+    return _DT[t.dtype]
+
+
+def _dev(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _params(gamma, omega, amp, phase, D=None):
+    ps = []
+    for name, p in (("gamma", gamma), ("omega", omega), ("amp", amp), ("phase", phase)):
+        _dev(p, name)
+        if p.dtype != torch.float32 or p.dim() != 2:
+            raise ValueError(f"{name} must be float32 [D, M]")
+        ps.append(p)
+    if any(p.shape != ps[0].shape for p in ps):
+        raise ValueError("gamma, omega, amp and phase must have the same shape [D, M]")
+    if D is not None and ps[0].shape[0] != D:
+        raise ValueError(f"parameters have D={ps[0].shape[0]}, activations have D={D}")
+    return ps
+
+
+def workspace_bytes(op: int, act_dtype: torch.dtype, B: int, L: int, D: int, M: int) -> int:
+    return int(_lib.lib().resonator_workspace_bytes(op, _DT[act_dtype], B, L, D, M))
+
+
+def _workspace(op, act_dtype, B, L, D, M, device, ws=None):
+    n = workspace_bytes(op, act_dtype, B, L, D, M)
+    if ws is not None:
+        if ws.numel() * ws.element_size() < n:
+            raise ValueError(f"workspace too small: need {n} bytes")
+        return ws, n
+    return torch.empty(max(n, 1), dtype=torch.uint8, device=device), n
+
+
+def resonator_mix_fwd(x, gamma, omega, amp, phase, h0=None, out_dtype=None, return_state=False,
+                      out=None, ws=None):
+    """y = causal resonant mixing of x (and the terminal state if return_state)."""
+    _dev(x, "x")
+    if x.dim() != 3:
+        raise ValueError("x must be [B, L, D]")
+    B, L, D = x.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    out_dtype = x.dtype if out_dtype is None else out_dtype
+    y = out if out is not None else torch.empty((B, L, D), dtype=out_dtype, device=x.device)
+    _dev(y, "out")
+    h_out = torch.empty((B, D, M, 2), dtype=torch.float32, device=x.device) if return_state else None
+    if h0 is not None:
+        _dev(h0, "h0")
+        if h0.dtype != torch.float32 or tuple(h0.shape) != (B, D, M, 2):
+            raise ValueError("h0 must be float32 [B, D, M, 2]")
+    w, n = _workspace(RES_OP_FWD, x.dtype, B, L, D, M, x.device, ws)
+    check(_lib.lib().resonator_mix_fwd(
+        _ptr(x), _code(x), _ptr(y), _code(y), B, L, D, M, _ptr(gamma), _ptr(omega), _ptr(amp),
+        _ptr(phase), _ptr(h0), _ptr(h_out), _ptr(w), n, _stream(x.device)))
+    return (y, h_out) if return_state else y
+
+
+def resonator_mix_bwd(x, dy, gamma, omega, amp, phase, h0=None, want_dh0=False, ws=None):
+    """Gradients of sum(dy * y): dict with dx, dgamma, domega, damp, dphase (, dh0)."""
+    _dev(x, "x")
+    _dev(dy, "dy")
+    if x.shape != dy.shape or x.dtype != dy.dtype or x.dim() != 3:
+        raise ValueError("x and dy must have the same [B, L, D] shape and dtype")
+    B, L, D = x.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    if h0 is not None:
+        _dev(h0, "h0")
+        if h0.dtype != torch.float32 or tuple(h0.shape) != (B, D, M, 2):
+            raise ValueError("h0 must be float32 [B, D, M, 2]")
+    dx = torch.empty_like(x)
+    g = {k: torch.empty((D, M), dtype=torch.float32, device=x.device)
+         for k in ("dgamma", "domega", "damp", "dphase")}
+    dh0 = torch.empty((B, D, M, 2), dtype=torch.float32, device=x.device) if want_dh0 else None
+    w, n = _workspace(RES_OP_BWD, x.dtype, B, L, D, M, x.device, ws)
+    check(_lib.lib().resonator_mix_bwd(
+        _ptr(x), _ptr(dy), _code(x), _ptr(dx), B, L, D, M, _ptr(gamma), _ptr(omega), _ptr(amp),
+        _ptr(phase), _ptr(h0), _ptr(g["dgamma"]), _ptr(g["domega"]), _ptr(g["damp"]),
+        _ptr(g["dphase"]), _ptr(dh0), _ptr(w), n, _stream(x.device)))
+    out = {"dx": dx, **g}
+    if want_dh0:
+        out["dh0"] = dh0
+    return out
+
+
+def resonator_state_init(x_prompt, gamma, omega, amp, phase, out=None, ws=None):
+    """Decode state after a prompt x_prompt [B, L, D] (L may be 0)."""
+    _dev(x_prompt, "x_prompt")
+    B, L, D = x_prompt.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    st = out if out is not None else torch.empty((B, D, M, 2), dtype=torch.float32,
+                                                  device=x_prompt.device)
+    if L > 0:
+        w, n = _workspace(RES_OP_STATE_INIT, x_prompt.dtype, B, L, D, M, x_prompt.device, ws)
+    else:
+        w, n = None, 0
+    check(_lib.lib().resonator_state_init(
+        _ptr(x_prompt) if L > 0 else None, _code(x_prompt), B, L, D, M, _ptr(gamma), _ptr(omega),
+        _ptr(amp), _ptr(phase), _ptr(st), _ptr(w), n, _stream(x_prompt.device)))
+    return st
+
+
+def resonator_decode_step(x_t, gamma, omega, amp, phase, state, out_dtype=None, out=None):
+    """One decode step: updates state [B, D, M, 2] in place, returns y_t [B, D]."""
+    _dev(x_t, "x_t")
+    _dev(state, "state")
+    B, D = x_t.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    if state.dtype != torch.float32 or tuple(state.shape) != (B, D, M, 2):
+        raise ValueError("state must be float32 [B, D, M, 2]")
+    out_dtype = x_t.dtype if out_dtype is None else out_dtype
+    y = out if out is not None else torch.empty((B, D), dtype=out_dtype, device=x_t.device)
+    check(_lib.lib().resonator_decode_step(
+        _ptr(x_t), _code(x_t), _ptr(y), _code(y), B, D, M, _ptr(gamma), _ptr(omega), _ptr(amp),
+        _ptr(phase), _ptr(state), _stream(x_t.device)))
+    return y
+
+
+class ResonatorMixFunction(torch.autograd.Function):
+    """Autograd wrapper: forward = resonator_mix_fwd, backward = resonator_mix_bwd."""
+
+    @staticmethod
+    def forward(ctx, x, gamma, omega, amp, phase):
+        ctx.save_for_backward(x, gamma, omega, amp, phase)
+        return resonator_mix_fwd(x.contiguous(), gamma.contiguous(), omega.contiguous(),
+                                 amp.contiguous(), phase.contiguous())
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, gamma, omega, amp, phase = ctx.saved_tensors
+        g = resonator_mix_bwd(x.contiguous(), dy.contiguous().to(x.dtype), gamma, omega, amp, phase)
+        return g["dx"], g["dgamma"], g["domega"], g["damp"], g["dphase"]
+
+
+def resonator_mix(x, gamma, omega, amp, phase):
+    """Differentiable mixing (x and the four parameter tensors receive gradients)."""
+    return ResonatorMixFunction.apply(x, gamma, omega, amp, phase)

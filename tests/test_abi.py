@@ -1,0 +1,111 @@
+"""C-ABI contract checks that need no GPU.
+
+The library loads without a device, exports every function include/resonator.h
+declares, and rejects bad arguments with the documented status before it makes
+any HIP call (so these error paths run on the CPU).
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_05583_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "resonator.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(resonator_\w+)\s*\(", src)))
+
+
+def test_header_symbols_exported():
+    lib = L.lib()
+    names = header_functions()
+    assert set(names) == set(L.SYMBOLS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_workspace_sizes():
+    lib = L.lib()
+    assert lib.resonator_version() >= 100
+    ws = lib.resonator_workspace_bytes
+    assert ws(L.RES_OP_FWD, L.RES_BF16, 4, 32768, 256, 8) > 0
+    assert ws(L.RES_OP_BWD, L.RES_F32, 2, 100, 7, 3) > 0
+    assert ws(L.RES_OP_STATE_INIT, L.RES_BF16, 2, 0, 7, 3) == 0      # empty prompt needs none
+    assert ws(L.RES_OP_FWD, L.RES_F32, 1, 100, 7, 17) == 0           # M > M_MAX
+    assert ws(9, L.RES_F32, 1, 100, 7, 3) == 0                        # bad op
+    assert ws(L.RES_OP_FWD, 7, 1, 100, 7, 3) == 0                     # bad dtype
+    # workspace grows with the problem
+    assert ws(L.RES_OP_FWD, L.RES_F32, 2, 4096, 64, 8) > ws(L.RES_OP_FWD, L.RES_F32, 1, 4096, 64, 8)
+
+
+FAKE = ctypes.c_void_p(0x7F0000000000)      # never dereferenced: validation fails first
+FAKE2 = ctypes.c_void_p(0x7F0100000000)
+
+
+def _fwd(**kw):
+    a = dict(x=FAKE, xdt=L.RES_F32, y=FAKE2, ydt=L.RES_F32, B=1, Ln=16, D=4, M=2,
+             g=FAKE, w=FAKE, amp=FAKE, ph=FAKE, h0=None, hout=None, ws=None, wsb=0, st=None)
+    a.update(kw)
+    return L.lib().resonator_mix_fwd(a["x"], a["xdt"], a["y"], a["ydt"], a["B"], a["Ln"], a["D"],
+                                     a["M"], a["g"], a["w"], a["amp"], a["ph"], a["h0"], a["hout"],
+                                     a["ws"], a["wsb"], a["st"])
+
+
+def _err():
+    return L.lib().resonator_last_error().decode()
+
+
+def test_fwd_validation_codes():
+    assert _fwd(B=0) == L.RES_ERR_INVALID_ARG and "B and D" in _err()
+    assert _fwd(Ln=0) == L.RES_ERR_INVALID_ARG
+    assert _fwd(M=0) == L.RES_ERR_INVALID_ARG
+    assert _fwd(M=17) == L.RES_ERR_UNSUPPORTED
+    assert _fwd(xdt=L.RES_F32, ydt=L.RES_BF16) == L.RES_ERR_UNSUPPORTED
+    assert _fwd(xdt=5) == L.RES_ERR_INVALID_ARG
+    assert _fwd(x=None) == L.RES_ERR_INVALID_ARG
+    assert _fwd(g=None) == L.RES_ERR_INVALID_ARG
+    assert _fwd(g=ctypes.c_void_p(0x7F0000000002)) == L.RES_ERR_MISALIGNED
+    assert _fwd(x=ctypes.c_void_p(0x7F0000000002)) == L.RES_ERR_MISALIGNED
+    assert _fwd(y=FAKE) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert _fwd() == L.RES_ERR_WORKSPACE and "workspace" in _err()
+    need = L.lib().resonator_workspace_bytes(L.RES_OP_FWD, L.RES_F32, 1, 16, 4, 2)
+    assert _fwd(ws=ctypes.c_void_p(0x7F0200000010), wsb=need) == L.RES_ERR_MISALIGNED
+
+
+def test_bwd_state_decode_validation_codes():
+    lib = L.lib()
+    rc = lib.resonator_mix_bwd(FAKE, FAKE2, L.RES_F32, FAKE, 1, 16, 4, 2, FAKE, FAKE, FAKE, FAKE,
+                               None, FAKE, FAKE, FAKE, FAKE, None, None, 0, None)
+    assert rc == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    rc = lib.resonator_mix_bwd(FAKE, FAKE2, L.RES_F32, ctypes.c_void_p(0x7F0300000000), 1, 16, 4, 2,
+                               FAKE, FAKE, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, None, None, 0, None)
+    assert rc == L.RES_ERR_INVALID_ARG
+    rc = lib.resonator_mix_bwd(FAKE, FAKE2, L.RES_F32, ctypes.c_void_p(0x7F0300000000), 1, 16, 4, 2,
+                               FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, None, None, 0, None)
+    assert rc == L.RES_ERR_WORKSPACE
+    rc = lib.resonator_state_init(None, L.RES_BF16, 1, 5, 4, 2, FAKE, FAKE, FAKE, FAKE, FAKE2, None, 0, None)
+    assert rc == L.RES_ERR_INVALID_ARG and "x_prompt" in _err()
+    rc = lib.resonator_state_init(FAKE, L.RES_BF16, 1, -1, 4, 2, FAKE, FAKE, FAKE, FAKE, FAKE2, None, 0, None)
+    assert rc == L.RES_ERR_INVALID_ARG
+    rc = lib.resonator_decode_step(FAKE, L.RES_BF16, FAKE, L.RES_BF16, 2, 4, 2, FAKE, FAKE, FAKE, FAKE,
+                                   FAKE2, None)
+    assert rc == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    rc = lib.resonator_decode_step(FAKE, L.RES_BF16, FAKE2, L.RES_BF16, 2, 4, 2, FAKE, FAKE, FAKE, FAKE,
+                                   ctypes.c_void_p(0x7F0300000004), None)
+    assert rc == L.RES_ERR_MISALIGNED
+    rc = lib.resonator_decode_step(FAKE, L.RES_F32, FAKE2, L.RES_BF16, 2, 4, 2, FAKE, FAKE, FAKE, FAKE,
+                                   ctypes.c_void_p(0x7F0300000000), None)
+    assert rc == L.RES_ERR_UNSUPPORTED
+
+
+def test_product_path_has_no_fallback(monkeypatch, tmp_path):
+    """A missing library raises; nothing silently computes elsewhere."""
+    monkeypatch.setattr(L, "_lib", None)
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        L.lib()

@@ -1,0 +1,170 @@
+"""GPU parity of the backward path and of recurrent decoding against the CPU oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import act64, dev_act, dev_f32, host, params_dev, params_np, rel_err, say, tol
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+GRADS = ("dgamma", "domega", "damp", "dphase")
+
+
+def setup_module(module):
+    global ops
+    from paper_2607_05583_amd import ops as _ops
+    ops = _ops
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+
+
+def _check_bwd(prob, act, use_h0, bound_dx, bound_p):
+    x = dev_act(prob["x"], act)
+    dy = dev_act(prob["dy"], act)
+    h0 = dev_f32(prob["h0"]) if use_h0 else None
+    g = ops.resonator_mix_bwd(x, dy, *params_dev(prob), h0=h0, want_dh0=True)
+    torch.cuda.synchronize()
+    ref = O.mix_bwd(act64(prob["x"], act), act64(prob["dy"], act), *params_np(prob),
+                    h0=prob["h0"] if use_h0 else None)
+    errs = {"dx": rel_err(host(g["dx"]), ref["dx"])}
+    for k in GRADS:
+        errs[k] = rel_err(host(g[k]), ref[k])
+    errs["dh0"] = rel_err(host(g["dh0"]), ref["dh0"])
+    say("  errs " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    assert errs["dx"] <= bound_dx
+    for k in (*GRADS, "dh0"):
+        assert errs[k] <= bound_p, k
+    return g
+
+
+BWD_SMALL = [
+    (1, 1, 1, 1, False, 31),
+    (2, 15, 3, 2, True, 32),
+    (1, 300, 33, 8, True, 33),
+    (2, 513, 64, 5, False, 34),
+    (3, 777, 70, 16, True, 35),
+    (1, 2048, 32, 8, False, 36),
+]
+
+
+@pytest.mark.parametrize("B,L,D,M,use_h0,seed", BWD_SMALL)
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_bwd_small_shapes(B, L, D, M, use_h0, seed, act):
+    say(f"bwd small B={B} L={L} D={D} M={M} h0={use_h0} {act}")
+    prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True,
+                            with_h0=use_h0, with_dy=True)
+    if act == "f32":
+        _check_bwd(prob, act, use_h0, 1e-4, 1e-4)
+    else:
+        _check_bwd(prob, act, use_h0, 2e-2, 2e-2)
+
+
+def test_bwd_deterministic():
+    say("bwd determinism")
+    prob = W.random_problem(40, 2, 3000, 64, 8, act="bf16", gamma_range=(1e-4, 1.0), gamma_log=True,
+                            with_dy=True)
+    x, dy = dev_act(prob["x"], "bf16"), dev_act(prob["dy"], "bf16")
+    pr = params_dev(prob)
+    a = ops.resonator_mix_bwd(x, dy, *pr)
+    b = ops.resonator_mix_bwd(x, dy, *pr)
+    torch.cuda.synchronize()
+    for k in ("dx", *GRADS):
+        assert torch.equal(a[k], b[k]), k
+
+
+def test_autograd_function_matches_bwd():
+    say("autograd wrapper")
+    prob = W.random_problem(41, 2, 300, 32, 4, act="f32", with_dy=True)
+    x = dev_act(prob["x"], "f32").requires_grad_(True)
+    pr = [p.clone().requires_grad_(True) for p in params_dev(prob)]
+    y = ops.resonator_mix(x, *pr)
+    y.backward(dev_act(prob["dy"], "f32"))
+    ref = O.mix_bwd(prob["x"], prob["dy"], *params_np(prob))
+    assert rel_err(host(x.grad), ref["dx"]) <= 1e-4
+    for p, k in zip(pr, GRADS):
+        assert rel_err(host(p.grad), ref[k]) <= 1e-4
+
+
+@pytest.mark.parametrize("layer", range(6))
+def test_config5_training_layer(layer):
+    """Training config: each of the 6 layers fwd + bwd at B8 L8192 D256 M8, bf16 activations."""
+    cfg = W.CONFIGS[5]
+    say(f"config 5 layer {layer}")
+    inp = W.train_layer_inputs(cfg, layer)
+    x = dev_act(inp["x"], "bf16")
+    pr = params_dev(inp)
+    y = ops.resonator_mix_fwd(x, *pr)
+    torch.cuda.synchronize()
+    x64 = act64(inp["x"], "bf16")
+    yr = O.mix_recurrence(x64, *params_np(inp))[0]
+    ey = rel_err(host(y), yr)
+    say(f"  y err {ey:.2e}")
+    assert ey <= 2e-2
+    _check_bwd(inp, "bf16", False, 2e-2, 2e-2)
+
+
+# --------------------------------------------------------------------------
+# decode
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("B,D,M,L0,steps,seed", [(1, 1, 1, 0, 5, 51), (3, 7, 3, 10, 40, 52),
+                                                 (64, 256, 8, 300, 200, 53), (5, 70, 16, 1, 64, 54)])
+@pytest.mark.parametrize("act,out", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+def test_decode_small(B, D, M, L0, steps, seed, act, out):
+    say(f"decode small B={B} D={D} M={M} L0={L0} steps={steps} {act}->{out}")
+    prob = W.random_problem(seed, B, L0 + steps, D, M, act=act, gamma_range=(1e-4, 1.0),
+                            gamma_log=True)
+    x = dev_act(prob["x"], act)
+    pr = params_dev(prob)
+    st = ops.resonator_state_init(x[:, :L0].contiguous(), *pr)
+    ys = []
+    for t in range(L0, L0 + steps):
+        ys.append(ops.resonator_decode_step(x[:, t].contiguous(), *pr, st,
+                                            out_dtype=torch.float32 if out == "f32" else x.dtype))
+    torch.cuda.synchronize()
+    yg = np.stack([host(v) for v in ys], 1)
+    x64 = act64(prob["x"], act)
+    yr, hr = O.mix_recurrence(x64, *params_np(prob))
+    assert rel_err(yg, yr[:, L0:]) <= tol(act, out)
+    assert rel_err(host(st), hr) <= (1e-4 if act == "f32" else 2e-2)
+
+
+def test_config4_decode_full():
+    """Decode config: prompt 1024 -> state_init, then 32768 decode steps at B64 D256 M8 (bf16).
+
+    The GPU runs the full batch; the oracle follows 4 sampled batch rows through
+    all 32768 steps and is compared on every step of those rows and on the final
+    state.
+    """
+    cfg = W.CONFIGS[4]
+    say(f"config 4 {cfg.name}")
+    di = W.DecodeInputs(cfg)
+    pr = params_dev(di.params)
+    rows = np.array([0, 17, 40, 63])
+    prompt = dev_act(di.prompt, "bf16")
+    st = ops.resonator_state_init(prompt, *pr)
+    torch.cuda.synchronize()
+    st_ref = O.state_init(act64(di.prompt[rows], "bf16"), *params_np(di.params))
+    assert rel_err(host(st)[rows], st_ref) <= 2e-2
+    n_total, chunk = cfg.steps, 4096
+    lam, c = O.modes(*params_np(di.params))
+    h = st_ref[..., 0] + 1j * st_ref[..., 1]
+    worst = 0.0
+    y_dev = torch.empty((n_total, cfg.B, cfg.D), dtype=torch.bfloat16, device="cuda")
+    for s0 in range(0, n_total, chunk):
+        xs = di.steps(chunk)
+        xd = dev_act(xs, "bf16")
+        for j in range(chunk):
+            ops.resonator_decode_step(xd[j], *pr, st, out=y_dev[s0 + j])
+        torch.cuda.synchronize()
+        yg = host(y_dev[s0:s0 + chunk])[:, rows]
+        x64 = act64(xs[:, rows], "bf16")
+        yr = np.empty_like(yg)
+        for j in range(chunk):
+            h = lam[None] * h + x64[j][..., None]
+            yr[j] = (c[None] * h).real.sum(-1)
+        worst = max(worst, rel_err(yg, yr))
+    say(f"config 4 worst step err {worst:.3e}")
+    assert worst <= 2e-2
+    assert rel_err(host(st)[rows], np.stack([h.real, h.imag], -1)) <= 2e-2

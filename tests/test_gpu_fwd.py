@@ -1,0 +1,156 @@
+"""GPU parity of the forward path and the prompt state against the CPU oracle.
+
+Every case compares the HIP path (through the C ABI) with the float64 oracle on
+identical seeded inputs, element by element, with the error metric of
+gpu_util.rel_err: 1e-4 for float32 activations, 2e-2 when bf16 is involved.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import act64, dev_act, dev_f32, host, params_dev, params_np, rel_err, say, tol
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+
+
+def setup_module(module):
+    global ops
+    from paper_2607_05583_amd import ops as _ops
+    ops = _ops
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+
+
+SMALL = [
+    # B, L, D, M, h0, seed
+    (1, 1, 1, 1, False, 1),
+    (2, 15, 3, 2, True, 2),
+    (1, 16, 33, 4, False, 3),
+    (2, 257, 40, 8, True, 4),
+    (1, 1000, 64, 9, False, 5),
+    (3, 600, 70, 16, True, 6),
+    (2, 513, 32, 5, False, 7),
+    (1, 2048, 96, 8, True, 8),
+]
+
+
+@pytest.mark.parametrize("B,L,D,M,use_h0,seed", SMALL)
+@pytest.mark.parametrize("act,out", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+def test_fwd_small_shapes(B, L, D, M, use_h0, seed, act, out):
+    say(f"fwd small B={B} L={L} D={D} M={M} h0={use_h0} {act}->{out}")
+    prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True,
+                            with_h0=use_h0)
+    x = dev_act(prob["x"], act)
+    h0 = dev_f32(prob["h0"]) if use_h0 else None
+    y, hout = ops.resonator_mix_fwd(x, *params_dev(prob), h0=h0,
+                                    out_dtype=torch.float32 if out == "f32" else x.dtype,
+                                    return_state=True)
+    torch.cuda.synchronize()
+    yr, hr = O.mix_recurrence(act64(prob["x"], act), *params_np(prob),
+                              h0=prob["h0"] if use_h0 else None)
+    assert rel_err(host(y), yr) <= tol(act, out)
+    assert rel_err(host(hout), hr) <= (1e-4 if act == "f32" else 2e-2)
+
+
+def test_config1_against_direct_sum():
+    cfg = W.CONFIGS[1]
+    say(f"config 1 {cfg.name}")
+    inp = W.fwd_inputs(cfg)
+    x = dev_act(inp["x"], cfg.act)
+    y = ops.resonator_mix_fwd(x, *params_dev(inp))
+    torch.cuda.synchronize()
+    yd = O.mix_direct(act64(inp["x"], cfg.act), *params_np(inp))
+    e = rel_err(host(y), yd)
+    say(f"config 1 rel err {e:.3e}")
+    assert e <= 1e-4
+
+
+def _spot_positions(rng, B, L, D, n):
+    b = rng.integers(0, B, n)
+    t = np.concatenate([rng.integers(0, L, n - 8), [0, 1, L - 1, L - 2, 255, 256, L // 2, L - 257]])
+    d = rng.integers(0, D, n)
+    return np.stack([b, t, d], 1)
+
+
+@pytest.mark.parametrize("k", [2, 3])
+def test_config_full_size(k):
+    cfg = W.CONFIGS[k]
+    say(f"config {k} {cfg.name}")
+    inp = W.fwd_inputs(cfg)
+    x = dev_act(inp["x"], cfg.act)
+    y, hout = ops.resonator_mix_fwd(x, *params_dev(inp), return_state=True)
+    torch.cuda.synchronize()
+    yg, hg = host(y), host(hout)
+    x64 = act64(inp["x"], cfg.act)
+    yr, hr = O.mix_recurrence(x64, *params_np(inp))
+    e, eh = rel_err(yg, yr), rel_err(hg, hr)
+    say(f"config {k} rel err y {e:.3e} h_out {eh:.3e}")
+    assert e <= tol(cfg.act, cfg.out)
+    assert eh <= (1e-4 if cfg.act == "f32" else 2e-2)
+    # independent direct-sum spot checks at sampled positions
+    pos = _spot_positions(np.random.default_rng(100 + k), cfg.B, cfg.L, cfg.D, 96)
+    yd = O.mix_direct_at(x64, *params_np(inp), pos)
+    got = yg[pos[:, 0], pos[:, 1], pos[:, 2]]
+    den = np.maximum(np.abs(yd), np.sqrt(np.mean(yr ** 2)))
+    assert float((np.abs(got - yd) / den).max()) <= tol(cfg.act, cfg.out)
+
+
+@pytest.mark.parametrize("B,L,D,M,seed", [(1, 1, 1, 1, 1), (2, 0, 5, 3, 2), (2, 255, 33, 8, 3),
+                                          (3, 700, 64, 12, 4), (64, 1024, 256, 8, 5)])
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+def test_state_init(B, L, D, M, seed, act):
+    say(f"state_init B={B} L={L} D={D} M={M} {act}")
+    prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], act)
+    st = ops.resonator_state_init(x, *params_dev(prob))
+    torch.cuda.synchronize()
+    ref = O.state_init(act64(prob["x"], act), *params_np(prob))
+    if L == 0:
+        assert np.array_equal(host(st), np.zeros_like(ref))
+    else:
+        assert rel_err(host(st), ref) <= (1e-4 if act == "f32" else 2e-2)
+
+
+def test_causality_bitwise():
+    """Sec. 3.5 causality check: perturbing the suffix leaves every earlier output bit-identical."""
+    say("causality bitwise")
+    prob = W.random_problem(21, 2, 3000, 64, 8, act="bf16", gamma_range=(1e-5, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], "bf16")
+    pr = params_dev(prob)
+    y1 = ops.resonator_mix_fwd(x, *pr)
+    for cut in (1, 255, 256, 1500, 2999):
+        x2 = x.clone()
+        x2[:, cut:] = torch.randn_like(x2[:, cut:].float()).to(x2.dtype)
+        y2 = ops.resonator_mix_fwd(x2, *pr)
+        torch.cuda.synchronize()
+        assert torch.equal(y1[:, :cut], y2[:, :cut])
+        assert not torch.equal(y1[:, cut:], y2[:, cut:])
+
+
+def test_split_prefill_matches_full():
+    """fwd(x[:L0]) -> h_out, fwd(x[L0:], h0=h_out) reproduces fwd(x) (state hand-over)."""
+    say("split prefill")
+    prob = W.random_problem(22, 2, 1200, 40, 8, act="f32", gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], "f32")
+    pr = params_dev(prob)
+    y, h = ops.resonator_mix_fwd(x, *pr, return_state=True)
+    y1, h1 = ops.resonator_mix_fwd(x[:, :500].contiguous(), *pr, return_state=True)
+    y2, h2 = ops.resonator_mix_fwd(x[:, 500:].contiguous(), *pr, h0=h1, return_state=True)
+    torch.cuda.synchronize()
+    yr = O.mix_recurrence(prob["x"].astype(np.float64), *params_np(prob))[0]
+    assert rel_err(np.concatenate([host(y1), host(y2)], 1), yr) <= 1e-4
+    assert rel_err(host(h2), host(h)) <= 1e-4
+
+
+def test_fwd_repeatable():
+    say("fwd repeatable")
+    prob = W.random_problem(23, 2, 2000, 64, 8, act="bf16", gamma_range=(1e-5, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], "bf16")
+    pr = params_dev(prob)
+    a = ops.resonator_mix_fwd(x, *pr)
+    b = ops.resonator_mix_fwd(x, *pr)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
