@@ -13,6 +13,8 @@ using namespace res;
 namespace {
 
 thread_local std::string g_err;
+// words ahead of the per-tile flags: [0] tile ticket, [1] error word
+constexpr size_t FLAG_HEADER = 64;
 // Armed by resonator_set_kernel_timer for the next dominant-kernel launch.
 thread_local hipEvent_t g_ev0 = nullptr, g_ev1 = nullptr;
 
@@ -59,27 +61,38 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
 }
 
 WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
+  (void)act;
   WsLayout w{};
   size_t off = 0;
-  (void)act;
   const int nm = op == RES_OP_BWD ? bwd_mats(g.MG) : fwd_mats(g.MG);
-  const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;
+  const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;  // = tiles * DW * Mp
   w.tab = off;
   off += align256((size_t)g.Dp * nm * TAB_MAT_BYTES);
   w.scal = off;
   off += align256((size_t)g.Dp * g.Mp * sizeof(ModeScalars));
   w.carryc = off;
   off += align256((size_t)g.Dp * g.Mp * sizeof(ModeCarry));
-  const size_t state_bytes = op == RES_OP_BWD ? sizeof(float4) : sizeof(float2);
-  w.agg = off;
-  off += align256(tiles_modes * state_bytes);
-  w.carry = off;
-  if (op != RES_OP_STATE_INIT) off += align256(tiles_modes * state_bytes);
-  w.flags = off;
-  w.part = off;
-  if (op == RES_OP_BWD) off += align256((size_t)g.B * g.P * g.Dp * (16 + 4 * g.Mp) * sizeof(float));
-  w.q0 = off;
-  if (op == RES_OP_BWD) off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float4));
+  if (op == RES_OP_FWD) {
+    // ticket, error word, then one flag per tile; payloads per tile [DW][Mp]
+    w.flags = off;
+    off += align256((FLAG_HEADER + (size_t)g.B * g.P * g.NB) * sizeof(uint32_t));
+    w.agg = off;  // aggregate payloads
+    off += align256(tiles_modes * sizeof(float2));
+    w.carry = off;  // inclusive payloads
+    off += align256(tiles_modes * sizeof(float2));
+  } else if (op == RES_OP_STATE_INIT) {
+    w.agg = off;
+    off += align256(tiles_modes * sizeof(float2));
+  } else {
+    w.agg = off;
+    off += align256(tiles_modes * sizeof(float4));
+    w.carry = off;
+    off += align256(tiles_modes * sizeof(float4));
+    w.part = off;
+    off += align256((size_t)g.B * g.P * g.Dp * (16 + 4 * g.Mp) * sizeof(float));
+    w.q0 = off;
+    off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float4));
+  }
   w.total = off;
   return w;
 }
@@ -166,9 +179,12 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   char* base = (char*)ws;
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
-  hipError_t e = x_dt == RES_BF16
-                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
-                     : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
+  uint32_t* fl = (uint32_t*)(base + w.flags);
+  const int64_t nflags = FLAG_HEADER + g.B * g.P * g.NB;
+  hipError_t e =
+      x_dt == RES_BF16
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, fl, nflags, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, fl, nflags, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x;
@@ -184,19 +200,22 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   a.last_len = g.last_len;
   a.tab = base + w.tab;
   a.scal = scal;
-  a.agg = (float2*)(base + w.agg);
-  a.carry = (const float2*)(base + w.carry);
+  a.h0 = h0;
+  a.h_out = h_out;
+  a.ticket = fl;
+  a.error = fl + 1;
+  a.flags = fl + FLAG_HEADER;
+  a.pay_agg = (float2*)(base + w.agg);
+  a.pay_inc = (float2*)(base + w.carry);
   hipEvent_t ev0, ev1;
   take_timer(&ev0, &ev1);
-  auto tile = [&](int mode, hipEvent_t e0, hipEvent_t e1) {
-    if (x_dt == RES_F32) return launch_fwd_tile<float, float>(g, mode, a, st, e0, e1);
-    if (y_dt == RES_BF16) return launch_fwd_tile<bf16_t, bf16_t>(g, mode, a, st, e0, e1);
-    return launch_fwd_tile<bf16_t, float>(g, mode, a, st, e0, e1);
-  };
-  if ((e = tile(MODE_STATE, nullptr, nullptr)) != hipSuccess) return hip_fail(e, "tile-state launch");
-  if ((e = launch_carry_fwd(g, a.agg, (float2*)(base + w.carry), h0, h_out, cc, st)) != hipSuccess)
-    return hip_fail(e, "carry launch");
-  if ((e = tile(MODE_APPLY, ev0, ev1)) != hipSuccess) return hip_fail(e, "tile-apply launch");
+  if (x_dt == RES_F32)
+    e = launch_fwd_fused<float, float>(g, a, st, ev0, ev1);
+  else if (y_dt == RES_BF16)
+    e = launch_fwd_fused<bf16_t, bf16_t>(g, a, st, ev0, ev1);
+  else
+    e = launch_fwd_fused<bf16_t, float>(g, a, st, ev0, ev1);
+  if (e != hipSuccess) return hip_fail(e, "forward launch");
   return RES_OK;
 }
 
@@ -225,9 +244,10 @@ int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int6
   char* base = (char*)ws;
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
-  hipError_t e = x_dt == RES_BF16
-                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
-                     : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
+  hipError_t e =
+      x_dt == RES_BF16
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, nullptr, 0, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, nullptr, 0, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x_prompt;
@@ -244,11 +264,9 @@ int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int6
   a.tab = base + w.tab;
   a.scal = scal;
   a.agg = (float2*)(base + w.agg);
-  a.carry = nullptr;
-  e = x_dt == RES_F32 ? launch_fwd_tile<float, float>(g, MODE_STATE, a, st)
-                      : launch_fwd_tile<bf16_t, bf16_t>(g, MODE_STATE, a, st);
+  e = x_dt == RES_F32 ? launch_fwd_state<float>(g, a, st) : launch_fwd_state<bf16_t>(g, a, st);
   if (e != hipSuccess) return hip_fail(e, "tile-state launch");
-  if ((e = launch_carry_fwd(g, a.agg, nullptr, nullptr, state_out, cc, st)) != hipSuccess)
+  if ((e = launch_carry_fwd(g, a.agg, state_out, cc, st)) != hipSuccess)
     return hip_fail(e, "carry launch");
   return RES_OK;
 }
@@ -282,9 +300,10 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
   char* base = (char*)ws;
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
-  hipError_t e = act_dt == RES_BF16
-                     ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st)
-                     : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st);
+  hipError_t e =
+      act_dt == RES_BF16
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, nullptr, 0, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, nullptr, 0, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   BwdArgs a{};
   a.x = x;

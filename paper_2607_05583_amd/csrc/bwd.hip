@@ -74,9 +74,9 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
   const int64_t t0 = p * TILE_T;
   const int d0 = nb * DW;
 
-  load_tile<TX, DW>(reinterpret_cast<const TX*>(a.dy), dyt, b, t0, d0, a.L, a.D, tid);
+  load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.dy), dyt, b, t0, d0, a.L, a.D, tid);
   if (MODE == MODE_APPLY)
-    load_tile<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
+    load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
   __syncthreads();
 
   const char* tab = reinterpret_cast<const char*>(a.tab);
@@ -159,9 +159,9 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
         const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
         const XOp xv = PT::load_x(&xt[ch * XP + PT::x_off(li, lq)]);
         const float* srow = &sb[k * KSTR];
-        // dx += Ub Qin
-        dxacc[k] = PT::mma_state(PT::load_a(tp + (5 + 5 * g) * TAB_MAT_BYTES), &srow[li * NSTR + PT::h_off(lq)],
-                                 dxacc[k]);
+        // dx += Ub Qin (float32 product of the carried states)
+        dxacc[k] = mma_f32(load_f4(tp + (5 + 5 * g) * TAB_MAT_BYTES),
+                           load_f4(&srow[li * NSTR + lq * 4]), dxacc[k]);
         // Xs^T, Xw^T: rows = chunks, columns = components (the table is the B operand)
         const f4 xs = PT::mma(xv, PT::load_a(tp + (3 + 5 * g) * TAB_MAT_BYTES), zero);
         const f4 xw = PT::mma(xv, PT::load_a(tp + (4 + 5 * g) * TAB_MAT_BYTES), zero);
@@ -172,8 +172,8 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
           qt[r] = srow[(4 * lq + r) * NSTR + li];
           rt[r] = srow[(4 * lq + r) * NSTR + 16 + li];
         }
-        dwacc[k] = mma_k16(xs, qt, zero, (TX*)nullptr);
-        dracc[k] = mma_k16(xs, rt, mma_k16(xw, qt, zero, (TX*)nullptr), (TX*)nullptr);
+        dwacc[k] = mma_f32(xs, qt, zero);
+        dracc[k] = mma_f32(xs, rt, mma_f32(xw, qt, zero));
       }
       __syncthreads();
       // ---- dump P (first group) and the 2x2 diagonal blocks, then reduce -------
@@ -242,7 +242,7 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
   }
   if (MODE == MODE_APPLY) {
     __syncthreads();
-    store_tile<TX, DW>(reinterpret_cast<TX*>(a.dx), dyt, b, t0, d0, a.L, a.D, tid);
+    store_tile_any<TX, DW>(reinterpret_cast<TX*>(a.dx), dyt, b, t0, d0, a.L, a.D, tid);
   }
 }
 

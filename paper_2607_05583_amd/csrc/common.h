@@ -49,103 +49,59 @@ template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
 // 16x16 MFMA operands.  Lane = i + 16 q (i = 0..15, q = 0..3); results D[4q + r][n],
 // r = 0..3, sit in lane (n, q) for every instruction used here.
 //
-// Path<float>: a 16-deep contraction as four v_mfma_f32_16x16x4_f32 whose slot
-// (kk, q) is index 4q + kk: lane (i, q) holds A[i][4q..4q+3] and lane (n, q)
-// holds B[4q..4q+3][n].
-//
-// Path<bf16_t>: split-bf16 on v_mfma_f32_16x16x32_bf16.  A per-channel matrix A
-// (from float64) is stored as A = Ah + Al with Ah = bf16(A), Al = bf16(A - Ah);
-// lane (i, q) holds [Ah | Al][i][8q..8q+7], i.e. Ah[i][8q..] for q < 2 and
-// Al[i][8(q-2)..] for q >= 2.  The other operand is duplicated along the
-// 32-deep contraction (lane (n, q) holds B[8(q&1)..8(q&1)+7][n]), so one
-// instruction yields (Ah + Al) B.  Activations are exact in bf16; computed
-// float32 operands (states) are split the same way and take two instructions.
-// This keeps parameter tables and carried states at ~2^-17 relative precision.
+// Products with an activation operand (x or dy) use Path<T> of the activation
+// type T:
+//   Path<float>: a 16-deep contraction as four v_mfma_f32_16x16x4_f32 whose
+//     slot (kk, q) is index 4q + kk: lane (i, q) holds A[i][4q..4q+3] and lane
+//     (n, q) holds B[4q..4q+3][n].
+//   Path<bf16_t>: split-bf16 on v_mfma_f32_16x16x32_bf16.  A per-channel matrix
+//     A (from float64) is stored as A = Ah + Al with Ah = bf16(A), Al =
+//     bf16(A - Ah); lane (i, q) holds [Ah | Al][i][8q..8q+7] (Ah for q < 2, Al
+//     for q >= 2).  The activation operand is duplicated along the 32-deep
+//     contraction (lane (n, q) holds B[8(q&1)..8(q&1)+7][n]); activations are
+//     exact in bf16, so one instruction gives (Ah + Al) B with the tables at
+//     ~2^-17 relative precision.
+// Products of two computed float32 quantities (carried states, cross sums) use
+// mma_f32: the fp32 layout of Path<float>, whatever the activation type.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
-typedef short s8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f4 mma_f32(const f4& a, const f4& b, f4 c) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
+  return c;
+}
+__device__ __forceinline__ f4 load_f4(const void* p) { return *reinterpret_cast<const f4*>(p); }
 
 template <typename TX> struct Path;
 
 template <> struct Path<float> {
   typedef f4 AOp;  // table operand (16 bytes per lane)
   typedef f4 XOp;  // activation operand
-  static constexpr int XW = 4;         // activations per lane
-  static constexpr int HW = 4;         // state components per lane (contraction operand)
   __device__ static __forceinline__ int x_off(int li, int lq) { return li * 16 + lq * 4; }
-  __device__ static __forceinline__ int h_off(int lq) { return lq * 4; }
   __device__ static __forceinline__ XOp load_x(const float* p) { return *reinterpret_cast<const f4*>(p); }
   __device__ static __forceinline__ AOp load_a(const void* p) { return *reinterpret_cast<const f4*>(p); }
-  __device__ static __forceinline__ f4 mma(const f4& a, const f4& b, f4 c) {
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[0], b[0], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[1], b[1], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[2], b[2], c, 0, 0, 0);
-    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[3], b[3], c, 0, 0, 0);
-    return c;
-  }
-  // A (table) times a float32 operand h given as the lane's HW values.
-  __device__ static __forceinline__ f4 mma_state(const AOp& a, const float* h, f4 c) {
-    const f4 b = {h[0], h[1], h[2], h[3]};
-    return mma(a, b, c);
-  }
+  __device__ static __forceinline__ f4 mma(const f4& a, const f4& b, f4 c) { return mma_f32(a, b, c); }
 };
 
 template <> struct Path<bf16_t> {
   typedef bf8 AOp;
   typedef bf8 XOp;
-  static constexpr int XW = 8;
-  static constexpr int HW = 8;
   __device__ static __forceinline__ int x_off(int li, int lq) { return li * 16 + (lq & 1) * 8; }
-  __device__ static __forceinline__ int h_off(int lq) { return (lq & 1) * 8; }
   __device__ static __forceinline__ XOp load_x(const bf16_t* p) { return *reinterpret_cast<const bf8*>(p); }
   __device__ static __forceinline__ AOp load_a(const void* p) { return *reinterpret_cast<const bf8*>(p); }
   __device__ static __forceinline__ f4 mma(const bf8& a, const bf8& b, f4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
-  __device__ static __forceinline__ f4 mma_state(const AOp& a, const float* h, f4 c) {
-    bf8 hi, lo;
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      hi[r] = (__bf16)h[r];
-      lo[r] = (__bf16)(h[r] - (float)hi[r]);
-    }
-    c = mma(a, hi, c);
-    return mma(a, lo, c);
-  }
 };
 
-// 16x16x16 products of two computed float32 operands (both in the K16 layout:
-// lane (i, q) holds A[i][4q..4q+3], lane (n, q) holds B[4q..4q+3][n]).
-__device__ __forceinline__ f4 mma_k16(const f4& a, const f4& b, f4 c, float*) {
-  return Path<float>::mma(a, b, c);
-}
-__device__ __forceinline__ s4 bf16x4(const f4& v) {
-  s4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) r[i] = (short)__builtin_bit_cast(bf16_t, (__bf16)v[i]);
-  return r;
-}
-__device__ __forceinline__ f4 bf16x4_value(const s4& v) {
-  f4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) r[i] = __uint_as_float((uint32_t)(uint16_t)v[i] << 16);
-  return r;
-}
-// split-bf16 product (Ah + Al)(Bh + Bl) without the Al Bl term
-__device__ __forceinline__ f4 mma_k16(const f4& a, const f4& b, f4 c, bf16_t*) {
-  const s4 ah = bf16x4(a), bh = bf16x4(b);
-  const s4 al = bf16x4(a - bf16x4_value(ah)), bl = bf16x4(b - bf16x4_value(bh));
-  c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ah, bh, c, 0, 0, 0);
-  c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ah, bl, c, 0, 0, 0);
-  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(al, bh, c, 0, 0, 0);
-}
-// exact product of bf16 activations (K16 layout)
+// exact product of two activation gathers (K16 layout)
 __device__ __forceinline__ f4 mma_k16_act(const s4& a, const s4& b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
-__device__ __forceinline__ f4 mma_k16_act(const f4& a, const f4& b, f4 c) {
-  return Path<float>::mma(a, b, c);
-}
+__device__ __forceinline__ f4 mma_k16_act(const f4& a, const f4& b, f4 c) { return mma_f32(a, b, c); }
 
 // ---------------------------------------------------------------------------
 // Complex helpers (float2 / double2 as re, im)
@@ -185,8 +141,14 @@ constexpr size_t TAB_LANE_BYTES = 16;
 constexpr size_t TAB_MAT_BYTES = 64 * TAB_LANE_BYTES;
 
 // Number of 16x16 operand matrices per channel in the parameter table.
-__host__ __device__ inline int fwd_mats(int MG) { return 1 + 2 * MG; }  // T, V[g], U[g]
-__host__ __device__ inline int bwd_mats(int MG) { return 1 + 5 * MG; }  // Tt, Eq, Er, Xs, Xw, Ub
+// Forward: T, then per mode group V[g], U[g].  Backward: Tt, then per mode group
+// Eq[g], Er[g], Xs[g], Xw[g], Ub[g].  U and Ub multiply float32 states and are
+// stored in the float32 layout; the others multiply activations and use the
+// activation path's layout.
+__host__ __device__ inline int fwd_mats(int MG) { return 1 + 2 * MG; }
+__host__ __device__ inline int bwd_mats(int MG) { return 1 + 5 * MG; }
+__host__ __device__ inline bool fwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 2 == 1; }
+__host__ __device__ inline bool bwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 5 == 4; }
 
 // Per-mode float scalars of the tables (fwd and bwd).
 struct ModeScalars {
@@ -205,5 +167,8 @@ struct ModeCarry {
 struct WsLayout {
   size_t tab, scal, carryc, agg, carry, flags, part, q0, total;
 };
+
+// Tile flags of the single-pass chained scan.
+enum : uint32_t { FLAG_NONE = 0, FLAG_AGG = 1, FLAG_INCL = 2 };
 
 }  // namespace res

@@ -19,8 +19,15 @@ struct FwdArgs {
   int last_len;
   const void* tab;
   const ModeScalars* scal;
-  float2* agg;
-  const float2* carry;
+  const float* h0;   // [B][D][M][2] or null
+  float* h_out;      // [B][D][M][2] or null
+  float2* agg;       // prompt state: per-tile aggregates [B][P][Dp][Mp]
+  // single-pass chaining (ticket order = time-major over chains (b, channel block))
+  uint32_t* ticket;  // tile ticket counter
+  uint32_t* flags;   // per tile: FLAG_NONE / FLAG_AGG / FLAG_INCL
+  uint32_t* error;   // set when a bounded wait gives up
+  float2* pay_agg;   // per tile [DW][Mp]: end state of the tile's own drives
+  float2* pay_inc;   // per tile [DW][Mp]: end state including all earlier tiles
 };
 
 struct BwdArgs {
@@ -42,14 +49,17 @@ struct BwdArgs {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st);
+                       uint32_t* flags, int64_t nflags, hipStream_t st);
+
+template <typename TX>
+hipError_t launch_fwd_state(const Geometry& g, const FwdArgs& a, hipStream_t st);
 
 template <typename TX, typename TY>
-hipError_t launch_fwd_tile(const Geometry& g, int mode, const FwdArgs& a, hipStream_t st,
-                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+hipError_t launch_fwd_fused(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
+                            hipEvent_t ev1);
 
-hipError_t launch_carry_fwd(const Geometry& g, const float2* agg, float2* carry, const float* h0,
-                            float* hout, const ModeCarry* cc, hipStream_t st);
+hipError_t launch_carry_fwd(const Geometry& g, const float2* agg, float* hout, const ModeCarry* cc,
+                            hipStream_t st);
 
 // Launch with optional start/stop events recorded around this one kernel.
 template <typename K, typename... Args>
