@@ -13,8 +13,6 @@ using namespace res;
 namespace {
 
 thread_local std::string g_err;
-// words ahead of the per-tile flags: [0] tile ticket, [1] error word
-constexpr size_t FLAG_HEADER = 64;
 // Armed by resonator_set_kernel_timer for the next dominant-kernel launch.
 thread_local hipEvent_t g_ev0 = nullptr, g_ev1 = nullptr;
 
@@ -72,17 +70,16 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
   off += align256((size_t)g.Dp * g.Mp * sizeof(ModeScalars));
   w.carryc = off;
   off += align256((size_t)g.Dp * g.Mp * sizeof(ModeCarry));
-  if (op == RES_OP_FWD) {
-    // ticket, error word, then one flag per tile; payloads per tile [DW][Mp]
-    w.flags = off;
-    off += align256((FLAG_HEADER + (size_t)g.B * g.P * g.NB) * sizeof(uint32_t));
-    w.agg = off;  // aggregate payloads
-    off += align256(tiles_modes * sizeof(float2));
-    w.carry = off;  // inclusive payloads
-    off += align256(tiles_modes * sizeof(float2));
-  } else if (op == RES_OP_STATE_INIT) {
+  if (op == RES_OP_FWD || op == RES_OP_STATE_INIT) {
+    // per tile [DW * Mp] float4 records: half-tile aggregates, then entry states
     w.agg = off;
-    off += align256(tiles_modes * sizeof(float2));
+    off += align256(tiles_modes * sizeof(float4));
+    if (op == RES_OP_FWD) {
+      w.carry = off;
+      off += align256(tiles_modes * sizeof(float4));
+    }
+    w.alast = off;  // [B][Dp][Mp] state at t = L-1 from a zero start at the last tile
+    off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float2));
   } else {
     w.agg = off;
     off += align256(tiles_modes * sizeof(float4));
@@ -179,12 +176,10 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   char* base = (char*)ws;
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
-  uint32_t* fl = (uint32_t*)(base + w.flags);
-  const int64_t nflags = FLAG_HEADER + g.B * g.P * g.NB;
   hipError_t e =
       x_dt == RES_BF16
-          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, fl, nflags, st)
-          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, fl, nflags, st);
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x;
@@ -198,24 +193,29 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   a.Mp = g.Mp;
   a.P = g.P;
   a.last_len = g.last_len;
+  // 16-byte row segments: both activation pointers 16-byte aligned, rows a multiple of 16 bytes
+  a.fast_io = aligned(x, 16) && aligned(y, 16) && (D * elt_size(x_dt)) % 16 == 0 &&
+              (D * elt_size(y_dt)) % 16 == 0;
   a.tab = base + w.tab;
   a.scal = scal;
+  a.cc = cc;
   a.h0 = h0;
   a.h_out = h_out;
-  a.ticket = fl;
-  a.error = fl + 1;
-  a.flags = fl + FLAG_HEADER;
-  a.pay_agg = (float2*)(base + w.agg);
-  a.pay_inc = (float2*)(base + w.carry);
+  a.agg = base + w.agg;
+  a.car = base + w.carry;
+  a.alast = (float2*)(base + w.alast);
+  e = x_dt == RES_F32 ? launch_fwd_agg<float>(g, a, st) : launch_fwd_agg<bf16_t>(g, a, st);
+  if (e != hipSuccess) return hip_fail(e, "aggregate launch");
+  if ((e = launch_fwd_carry(g, a, st)) != hipSuccess) return hip_fail(e, "carry launch");
   hipEvent_t ev0, ev1;
   take_timer(&ev0, &ev1);
   if (x_dt == RES_F32)
-    e = launch_fwd_fused<float, float>(g, a, st, ev0, ev1);
+    e = launch_fwd_apply<float, float>(g, a, st, ev0, ev1);
   else if (y_dt == RES_BF16)
-    e = launch_fwd_fused<bf16_t, bf16_t>(g, a, st, ev0, ev1);
+    e = launch_fwd_apply<bf16_t, bf16_t>(g, a, st, ev0, ev1);
   else
-    e = launch_fwd_fused<bf16_t, float>(g, a, st, ev0, ev1);
-  if (e != hipSuccess) return hip_fail(e, "forward launch");
+    e = launch_fwd_apply<bf16_t, float>(g, a, st, ev0, ev1);
+  if (e != hipSuccess) return hip_fail(e, "apply launch");
   return RES_OK;
 }
 
@@ -246,8 +246,8 @@ int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int6
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
   hipError_t e =
       x_dt == RES_BF16
-          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, nullptr, 0, st)
-          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, nullptr, 0, st);
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x_prompt;
@@ -261,13 +261,17 @@ int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int6
   a.Mp = g.Mp;
   a.P = g.P;
   a.last_len = g.last_len;
+  a.fast_io = aligned(x_prompt, 16) && (D * elt_size(x_dt)) % 16 == 0;
   a.tab = base + w.tab;
   a.scal = scal;
-  a.agg = (float2*)(base + w.agg);
-  e = x_dt == RES_F32 ? launch_fwd_state<float>(g, a, st) : launch_fwd_state<bf16_t>(g, a, st);
-  if (e != hipSuccess) return hip_fail(e, "tile-state launch");
-  if ((e = launch_carry_fwd(g, a.agg, state_out, cc, st)) != hipSuccess)
-    return hip_fail(e, "carry launch");
+  a.cc = cc;
+  a.h_out = state_out;
+  a.agg = base + w.agg;
+  a.car = nullptr;
+  a.alast = (float2*)(base + w.alast);
+  e = x_dt == RES_F32 ? launch_fwd_agg<float>(g, a, st) : launch_fwd_agg<bf16_t>(g, a, st);
+  if (e != hipSuccess) return hip_fail(e, "aggregate launch");
+  if ((e = launch_fwd_carry(g, a, st)) != hipSuccess) return hip_fail(e, "carry launch");
   return RES_OK;
 }
 
@@ -302,8 +306,8 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
   hipError_t e =
       act_dt == RES_BF16
-          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, nullptr, 0, st)
-          : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, nullptr, 0, st);
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   BwdArgs a{};
   a.x = x;

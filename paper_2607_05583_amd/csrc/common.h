@@ -154,21 +154,19 @@ __host__ __device__ inline bool bwd_mat_is_state(int mat) { return mat > 0 && (m
 struct ModeScalars {
   float2 lam;     // lambda
   float2 mu;      // lambda^CHUNK
+  float2 mu8;     // lambda^(TILE_T / 2): the hop over half a tile (8 chunks)
   float2 lamT;    // lambda^TILE_T
-  float2 lamEll;  // lambda^last_len
 };
 // Per-mode float64 scalars for the cross-tile carry chain.
 struct ModeCarry {
-  double2 lamT;
-  double2 lamEll;
+  double2 lamT;    // lambda^TILE_T
+  double2 lamEll;  // lambda^last_len
+  double2 mu8;     // lambda^(TILE_T / 2)
 };
 
 // Offsets (bytes) of the workspace regions.
 struct WsLayout {
-  size_t tab, scal, carryc, agg, carry, flags, part, q0, total;
+  size_t tab, scal, carryc, agg, carry, alast, part, q0, total;
 };
-
-// Tile flags of the single-pass chained scan.
-enum : uint32_t { FLAG_NONE = 0, FLAG_AGG = 1, FLAG_INCL = 2 };
 
 }  // namespace res

@@ -26,7 +26,7 @@ namespace res {
 // float64 exp/sincos each; lambda^tau (tau <= 16) by float64 products,
 // lambda^256 by squaring, lambda^last_len by binary powering (relative error
 // ~1e-14, far below float32 resolution).  Entries are rounded once to the
-// operand type.  The grid also clears the flags of the chained scan.
+// operand type.
 // ---------------------------------------------------------------------------
 template <typename TA, bool BWD>
 __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gamma,
@@ -35,20 +35,13 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
                                                    const float* __restrict__ phase, int D, int M,
                                                    int MG, int last_len, TA* __restrict__ tab,
                                                    ModeScalars* __restrict__ scal,
-                                                   ModeCarry* __restrict__ cc,
-                                                   uint32_t* __restrict__ flags, int64_t nflags) {
+                                                   ModeCarry* __restrict__ cc) {
   const int d = blockIdx.x;
   const int Mp = MODES_PER_GROUP * MG;
   __shared__ double2 pw[MODES_PER_GROUP * MG_MAX][CHUNK + 1];  // lambda^tau, tau = 0..16
   __shared__ double2 cm[MODES_PER_GROUP * MG_MAX];             // c
   __shared__ double ev[MODES_PER_GROUP * MG_MAX][5];           // e^-g, cos w, sin w, cos p, sin p
   __shared__ double taps[CHUNK + 1];
-
-  if (flags != nullptr) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nflags;
-         i += (int64_t)gridDim.x * blockDim.x)
-      flags[i] = FLAG_NONE;
-  }
 
   const bool dvalid = d < D;
   // one transcendental per thread: (m, which) with which = exp | sincos(omega) | sincos(phi)
@@ -83,8 +76,9 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
       pw[m][tau] = pk;
       pk = zmul(pk, lam);
     }
-    double2 lT = pw[m][CHUNK];                      // lambda^16 -> lambda^256
-    for (int s = 0; s < 4; ++s) lT = zmul(lT, lT);
+    double2 lH = pw[m][CHUNK];                      // lambda^16 -> lambda^128
+    for (int s = 0; s < 3; ++s) lH = zmul(lH, lH);
+    const double2 lT = zmul(lH, lH);                // lambda^256
     double2 lE = make_double2(valid ? 1.0 : 0.0, 0.0), base = lam;  // lambda^last_len
     for (int e = last_len; e > 0; e >>= 1) {
       if (e & 1) lE = zmul(lE, base);
@@ -93,12 +87,13 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     ModeScalars ms;
     ms.lam = make_float2((float)lam.x, (float)lam.y);
     ms.mu = make_float2((float)pw[m][CHUNK].x, (float)pw[m][CHUNK].y);
+    ms.mu8 = make_float2((float)lH.x, (float)lH.y);
     ms.lamT = make_float2((float)lT.x, (float)lT.y);
-    ms.lamEll = make_float2((float)lE.x, (float)lE.y);
     scal[(size_t)d * Mp + m] = ms;
     ModeCarry mc;
     mc.lamT = lT;
     mc.lamEll = lE;
+    mc.mu8 = lH;
     cc[(size_t)d * Mp + m] = mc;
   }
   __syncthreads();
@@ -164,416 +159,436 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
 }
 
 // ---------------------------------------------------------------------------
-// Shared tile phases
+// Forward tile machinery.
+//
+// A tile is one batch row b, 256 steps and DW channels (64 bf16 / 32 fp32, so a
+// time row of the tile is one 128-byte segment).  Four waves each own CPW = DW/4
+// channels, handled in groups of 4.
+//
+// LDS.  The drive tile is time-major: 32 groups of 8 rows (128 B each) with a
+// 4-byte pad per group, filled by direct-to-LDS 16-byte loads.  Each output
+// channel overwrites its own drive column once its products are done, and the
+// tile leaves as 16-byte row stores.  Each wave has a scan buffer
+// [4 channels][16 chunks][16 MG floats]: chunk states go from the MFMA layout
+// (lane (n, q) holds components 4q..4q+3 of chunk n) to the scan layout, and
+// the carried states come back the same way.
+//
+// Scan layout: lane 16 c + 2 m + h holds channel c of the group, mode m, for the
+// chunk half h (chunks 8h .. 8h+7).  With A_h the end state of half h from a
+// zero start (A_h = sum_j mu^(7-j) S[8h+j], mu = lambda^16), the tile's own
+// end state is mu^8 A_0 + A_1, and half 1 of a tile entered with state c enters
+// with mu^8 c + A_0.
+//
+// Per-tile records ([tile][DW * Mp] float4, slot q = wave * 32 PAIRS + 32 (grp
+// MG + g) + 8 c + m): the aggregate kernel writes (A_0, A_1); the carry kernel
+// writes the entry states (c, mu^8 c + A_0) of both halves.
 // ---------------------------------------------------------------------------
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+constexpr int XROW = 128;                      // bytes per time row of a tile
+constexpr int XGRP = 8 * XROW + 4;             // 8 rows + pad (conflict-free operand reads)
+constexpr int XT_BYTES = (TILE_T / 8) * XGRP;  // 32896
+
+__device__ __forceinline__ int xt_off(int t) { return (t >> 3) * XGRP + (t & 7) * XROW; }
+
+// Compiler-level ordering of LDS accesses inside one wave (the LDS executes a
+// wave's accesses in program order).
+__device__ __forceinline__ void wave_lds_order() { asm volatile("" ::: "memory"); }
+
+// Drive tile [t0, t0 + 256) x [d0, d0 + DW) of row b into the time-major LDS
+// tile; zeros outside [0, L) x [0, D).  full: the whole tile is in range and the
+// rows are 16-byte aligned (direct-to-LDS loads); the caller waits (vmcnt) and
+// synchronises before reading.
+template <typename TX>
+__device__ __forceinline__ void tile_load(char* xt, const TX* x, int64_t b, int64_t t0, int d0,
+                                          int64_t L, int D, bool full, int tid) {
+  constexpr int DW = tile_channels<TX>(), XE = (int)sizeof(TX);
+  const int lane = tid & 63, wave = tid >> 6;
+  if (full) {
+    const char* src = reinterpret_cast<const char*>(x) + ((b * L + t0) * D + d0) * XE;
+    const int64_t rowb = (int64_t)D * XE;
+#pragma unroll
+    for (int i = 0; i < TILE_T / 8 / NWAVES; ++i) {
+      const int g = wave * (TILE_T / 8 / NWAVES) + i;
+      const char* s = src + (int64_t)(8 * g + (lane >> 3)) * rowb + (lane & 7) * 16;
+      __builtin_amdgcn_global_load_lds((gvoid_t*)s, (lvoid_t*)(xt + g * XGRP), 16, 0, 0);
+    }
+  } else {
+    for (int idx = tid; idx < TILE_T * DW; idx += NTHREADS) {
+      const int t = idx / DW, c = idx % DW;
+      TX v = from_f32<TX>(0.f);
+      if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
+      *reinterpret_cast<TX*>(xt + xt_off(t) + c * XE) = v;
+    }
+  }
+}
+
+template <typename TY>
+__device__ __forceinline__ void tile_store(TY* y, const char* xt, int64_t b, int64_t t0, int d0,
+                                           int64_t L, int D, bool full, int tid) {
+  constexpr int DW = tile_channels<TY>(), YE = (int)sizeof(TY);
+  const int lane = tid & 63, wave = tid >> 6;
+  if (full) {
+    char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE;
+    const int64_t rowb = (int64_t)D * YE;
+#pragma unroll
+    for (int i = 0; i < TILE_T / 8 / NWAVES; ++i) {
+      const int g = wave * (TILE_T / 8 / NWAVES) + i;
+      const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XGRP + lane * 16);
+      *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g + (lane >> 3)) * rowb + (lane & 7) * 16) = v;
+    }
+  } else {
+    for (int idx = tid; idx < TILE_T * DW; idx += NTHREADS) {
+      const int t = idx / DW, c = idx % DW;
+      if (t0 + t < L && d0 + c < D)
+        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + xt_off(t) + c * YE);
+    }
+  }
+}
+
+// Activation operand of chunk n for channel ch from the time-major tile.
+template <typename TX> struct XGather;
+template <> struct XGather<bf16_t> {
+  // lane (n, q): taps 8(q&1) .. +7 = rows 16n + 8(q&1) + r = group 2n + (q&1), row r
+  __device__ static __forceinline__ bf8 get(const char* xt, int ch, int n, int q) {
+    const char* p = xt + (2 * n + (q & 1)) * XGRP + ch * 2;
+    bf8 v;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) v[r] = *reinterpret_cast<const __bf16*>(p + r * XROW);
+    return v;
+  }
+};
+template <> struct XGather<float> {
+  // lane (n, q), slot kk: tap 4q + kk = row 16n + 4q + kk = group 2n + (q>>1), row 4(q&1) + kk
+  __device__ static __forceinline__ f4 get(const char* xt, int ch, int n, int q) {
+    const char* p = xt + (2 * n + (q >> 1)) * XGRP + 4 * (q & 1) * XROW + ch * 4;
+    f4 v;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) v[kk] = *reinterpret_cast<const float*>(p + kk * XROW);
+    return v;
+  }
+};
+
+__device__ __forceinline__ float swap_pair(float v) {  // value of the neighbouring lane (lane ^ 1)
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1,
+                                                               0xF, 0xF, false));
+}
+
 template <typename TX, int MG>
 struct FwdTile {
   typedef Path<TX> PT;
   static constexpr int DW = tile_channels<TX>();
-  static constexpr int CPW = DW / NWAVES;      // channels per wave
-  static constexpr int NCG = CPW / 8;          // scan groups of 8 channels per wave
-  static constexpr int XP = TileGeom<TX, DW>::PITCH;
-  static constexpr int NSTR = 16 * MG;         // floats per chunk in the scan buffer
-  static constexpr int KSTR = 16 * NSTR + 16;  // floats per channel in the scan buffer
-  static constexpr int WSB = 8 * KSTR;         // floats per wave
+  static constexpr int CPW = DW / NWAVES;     // channels per wave
+  static constexpr int NGRP = CPW / 4;       // scan groups of 4 channels
+  static constexpr int NSTR = 16 * MG;       // floats per chunk row of the scan buffer
+  static constexpr int CSTR = 16 * NSTR + 8; // floats per channel of the scan buffer
+  static constexpr int WBUF = 4 * CSTR;      // floats per wave
   static constexpr int NM = 1 + 2 * MG;
+  static constexpr int PAIRS = NGRP * MG;    // (group, mode group) states per scan lane
 };
 
-// Chunk products of one wave's channels: yacc = T x (if WANT_Y) and the chunk
-// end states S -> scan buffer; then the in-tile scan: hx[n] = state entering
-// chunk n from zero at the tile start, aggv = state at the tile end.
-// With KEEP_HX false only the state entering chunk nsel is kept (in hx[cg][g][0]).
-template <typename TX, int MG, bool WANT_Y, bool KEEP_HX = true>
-__device__ __forceinline__ void fwd_chunk_phase(const TX* xt, float* sb, const char* tab,
-                                                const ModeScalars* scal, int Mp, int d0, int wave,
-                                                int lane, f4* yacc,
-                                                float2 (&hx)[FwdTile<TX, MG>::NCG][MG][NCHUNK],
-                                                float2 (&aggv)[FwdTile<TX, MG>::NCG][MG],
-                                                int nsel = 0) {
+// S = V x for the 4 channels of a group into the wave's scan buffer.
+template <typename TX, int MG>
+__device__ __forceinline__ void group_states(const char* xt, float* wb, int ch0,
+                                             const typename Path<TX>::AOp (&vop)[4][MG],
+                                             typename Path<TX>::XOp (&xv)[4], int ln, int lq) {
   typedef FwdTile<TX, MG> F;
-  typedef typename F::PT PT;
-  const int li = lane & 15, lq = lane >> 4;
-  const int sk = lane >> 3, sj = lane & 7;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int cg = 0; cg < F::NCG; ++cg) {
+  for (int k = 0; k < 4; ++k) {
+    xv[k] = XGather<TX>::get(xt, ch0 + k, ln, lq);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int ch = wave * F::CPW + cg * 8 + k;
-      const char* tp = tab + (size_t)(d0 + ch) * F::NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-      const typename PT::XOp xv = PT::load_x(&xt[ch * F::XP + PT::x_off(li, lq)]);
-      if (WANT_Y) yacc[cg * 8 + k] = PT::mma(PT::load_a(tp), xv, zero);
-#pragma unroll
-      for (int g = 0; g < MG; ++g) {
-        const f4 s = PT::mma(PT::load_a(tp + (1 + 2 * g) * TAB_MAT_BYTES), xv, zero);
-        *reinterpret_cast<f4*>(&sb[k * F::KSTR + li * F::NSTR + g * 16 + lq * 4]) = s;
-      }
-    }
-    __syncthreads();
-    {
-      const int dch = d0 + wave * F::CPW + cg * 8 + sk;
-#pragma unroll
-      for (int g = 0; g < MG; ++g) {
-        const float2 mu = scal[(size_t)dch * Mp + g * 8 + sj].mu;
-        float2 run = make_float2(0.f, 0.f);
-#pragma unroll
-        for (int n = 0; n < NCHUNK; ++n) {
-          if (KEEP_HX)
-            hx[cg][g][n] = run;
-          else if (n == nsel)
-            hx[cg][g][0] = run;
-          const float2 s =
-              *reinterpret_cast<const float2*>(&sb[sk * F::KSTR + n * F::NSTR + g * 16 + 2 * sj]);
-          run = cfma(mu, run, s);
-        }
-        aggv[cg][g] = run;
-      }
-    }
-    __syncthreads();
+    for (int g = 0; g < MG; ++g)
+      *reinterpret_cast<f4*>(&wb[k * F::CSTR + ln * F::NSTR + g * 16 + lq * 4]) =
+          Path<TX>::mma(vop[k][g], xv[k], zero);
   }
 }
 
-// State at t = L-1 from the state h entering chunk nstar and the chunk's drives.
-template <typename TX>
-__device__ __forceinline__ float2 tail_state(float2 h, const TX* row, int nstar, int jstar,
-                                             float2 lam) {
-  for (int j = 0; j <= jstar; ++j)
-    h = cfma(lam, h, make_float2(to_f32(row[nstar * CHUNK + j]), 0.f));
-  return h;
-}
-
 // ---------------------------------------------------------------------------
-// Prompt state: chunk states -> scan -> per-tile aggregate (end state of the
-// tile's own drives from a zero state); the last tile of a row writes the state
-// at t = L-1 instead.  carry_fwd_kernel then chains the tiles.
+// Aggregate kernel: per tile and scan lane, the half-tile end states (A_0, A_1)
+// from a zero start; the last tile of a row also gives the state at t = L-1
+// from a zero start at its first step (alast).
 // ---------------------------------------------------------------------------
 template <typename TX, int MG>
-__global__ __launch_bounds__(NTHREADS) void fwd_state_kernel(FwdArgs a) {
-  typedef FwdTile<TX, MG> F;
-  __shared__ __align__(16) TX xt[F::DW * F::XP];
-  __shared__ __align__(16) float sbuf[NWAVES * F::WSB];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int sk = lane >> 3, sj = lane & 7;
-  const int64_t tile = blockIdx.x;
-  const int nb = (int)(tile % a.NB);
-  const int64_t rest = tile / a.NB;
-  const int64_t b = rest % a.B;
-  const int64_t p = rest / a.B;
-  const int64_t t0 = p * TILE_T;
-  const int d0 = nb * F::DW;
-  load_tile_any<TX, F::DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
-  __syncthreads();
-  const bool last = (p == a.P - 1);
-  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
-  float2 hx[F::NCG][MG][NCHUNK];
-  float2 aggv[F::NCG][MG];
-  fwd_chunk_phase<TX, MG, false, false>(xt, sbuf + wave * F::WSB,
-                                        reinterpret_cast<const char*>(a.tab), a.scal, a.Mp, d0,
-                                        wave, lane, nullptr, hx, aggv, nstar);
-#pragma unroll
-  for (int cg = 0; cg < F::NCG; ++cg) {
-    const int ch = wave * F::CPW + cg * 8 + sk;
-    const int dch = d0 + ch;
-#pragma unroll
-    for (int g = 0; g < MG; ++g) {
-      const int m = g * 8 + sj;
-      float2 v = aggv[cg][g];
-      if (last)
-        v = tail_state(hx[cg][g][0], &xt[ch * F::XP], nstar, jstar,
-                       a.scal[(size_t)dch * a.Mp + m].lam);
-      a.agg[((size_t)(b * a.P + p) * a.Dp + dch) * a.Mp + m] = v;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Single-pass forward.
-//
-// Work-groups take tiles in ticket order (time-major over the chains (b,
-// channel block)).  A tile publishes the end state of its own
-// drives (aggregate), resolves the state entering it from its predecessors and
-// publishes the end state including them (inclusive).  The state entering tile
-// p is always the canonical value inc(p-1), where inc(-1) = h0 and
-// inc(i) = lambda^256 inc(i-1) + agg(i) in float32: a tile finds the nearest
-// predecessor whose inclusive state is out (polling a window of 64 flags at
-// once) and applies the recurrence forward through the aggregates after it, so
-// the result does not depend on timing (bitwise reproducible).  Every wait is on
-// a smaller ticket, which a running work-group took, and every wait is bounded.
-// Payloads and flags are agent-coherent (device-scope) accesses; a publisher
-// completes its payload stores before the flag store that releases them.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void st_agent(float2* p, float2 v) {
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 ld_agent(const float2* p) {
-  return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const uint64_t*>(p),
-                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-__device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
-  return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_flag(uint32_t* f, uint32_t v) {
-  __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-// Upper bound on window polls (about a second); reached only if a predecessor
-// never publishes, which the ticket order rules out.  The tile then starts from
-// the row's initial state and records the event in the error word.
-constexpr uint32_t SPIN_LIMIT = 1u << 20;
-
-template <typename TX, typename TY, int MG>
-__global__ __launch_bounds__(NTHREADS, MG == 1 ? 2 : 1) void fwd_fused_kernel(FwdArgs a) {
+__global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_agg_kernel(FwdArgs a) {
   typedef FwdTile<TX, MG> F;
   typedef typename F::PT PT;
-  constexpr int DW = F::DW, CPW = F::CPW, NCG = F::NCG, XP = F::XP;
-  // bf16 drive with float32 output: y leaves straight from the MFMA registers
-  constexpr bool SEPY = !__is_same(TX, TY);
-  __shared__ __align__(16) TX xt[DW * XP];
-  __shared__ __align__(16) float sbuf[NWAVES * F::WSB];
-  __shared__ uint32_t s_u[2];
-  __shared__ int64_t s_j;
+  constexpr int DW = F::DW, CPW = F::CPW, NGRP = F::NGRP, XE = (int)sizeof(TX);
+  __shared__ __align__(16) char xt[XT_BYTES];
+  __shared__ __align__(16) float sbuf[NWAVES * F::WBUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int li = lane & 15, lq = lane >> 4;
-  const int sk = lane >> 3, sj = lane & 7;
+  const int ln = lane & 15, lq = lane >> 4;
+  const int sh = lane & 1, sm = (lane >> 1) & 7, sc = lane >> 4;
   const int nchains = (int)(a.B * a.NB);
-  const char* tab = reinterpret_cast<const char*>(a.tab);
-  float* sb = sbuf + wave * F::WSB;
-  const int nstar = (a.last_len - 1) / CHUNK, jstar_l = (a.last_len - 1) % CHUNK;
-
-  if (tid == 0) s_u[0] = atomicAdd(a.ticket, 1u);
-  __syncthreads();
-  const int64_t tk = s_u[0];
-  const int64_t p = tk / nchains;
-  const int chain = (int)(tk % nchains);
+  const int64_t tile = blockIdx.x;
+  const int64_t p = tile / nchains;
+  const int chain = (int)(tile % nchains);
   const int64_t b = chain / a.NB;
   const int d0 = (chain % a.NB) * DW;
   const int64_t t0 = p * TILE_T;
   const bool last = (p == a.P - 1);
+  const bool full = a.fast_io && t0 + TILE_T <= a.L && d0 + DW <= a.D;
+  const int cw0 = wave * CPW;
+  const char* tab = reinterpret_cast<const char*>(a.tab);
+  float* wb = sbuf + wave * F::WBUF;
 
-  // per scan lane (channel wave*CPW + cg*8 + sk, mode g*8 + sj): its scalars
-  ModeScalars msc[NCG][MG];
+  typename PT::AOp vop[4][MG];
+  auto fetch_v = [&](int grp) {
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg)
+    for (int k = 0; k < 4; ++k)
 #pragma unroll
-    for (int g = 0; g < MG; ++g)
-      msc[cg][g] = a.scal[(size_t)(d0 + wave * CPW + cg * 8 + sk) * a.Mp + g * 8 + sj];
-
-  load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
+      for (int g = 0; g < MG; ++g)
+        vop[k][g] = PT::load_a(tab + (size_t)(d0 + cw0 + 4 * grp + k) * F::NM * TAB_MAT_BYTES +
+                               lane * TAB_LANE_BYTES + (1 + 2 * g) * TAB_MAT_BYTES);
+  };
+  fetch_v(0);
+  tile_load<TX>(xt, reinterpret_cast<const TX*>(a.x), b, t0, d0, a.L, a.D, full, tid);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  // ---- chunk end states and in-tile scan ---------------------------------
-  float2 hx[NCG][MG][NCHUNK];
-  float2 aggv[NCG][MG];
-  fwd_chunk_phase<TX, MG, false>(xt, sb, tab, a.scal, a.Mp, d0, wave, lane, nullptr, hx, aggv);
+  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
+  float4* rec = reinterpret_cast<float4*>(a.agg) + (size_t)tile * DW * a.Mp + wave * 32 * F::PAIRS;
+#pragma unroll
+  for (int grp = 0; grp < NGRP; ++grp) {
+    typename PT::XOp xv[4];
+    group_states<TX, MG>(xt, wb, cw0 + 4 * grp, vop, xv, ln, lq);
+    if (grp + 1 < NGRP) fetch_v(grp + 1);
+    wave_lds_order();
+    const int ch = cw0 + 4 * grp + sc;
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      const int m = g * 8 + sm;
+      const float2 mu = a.scal[(size_t)(d0 + ch) * a.Mp + m].mu;
+      float2 run = make_float2(0.f, 0.f), hl = run;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        if (8 * sh + j == nstar) hl = run;  // state entering chunk nstar (from this half's start)
+        const float2 sv =
+            *reinterpret_cast<const float2*>(&wb[sc * F::CSTR + (8 * sh + j) * F::NSTR + g * 16 + 2 * sm]);
+        run = cfma(mu, run, sv);
+      }
+      const float2 oth = make_float2(swap_pair(run.x), swap_pair(run.y));
+      const float2 A0 = sh ? oth : run, A1 = sh ? run : oth;
+      if (sh == 0) rec[(grp * MG + g) * 32 + sc * 8 + sm] = make_float4(A0.x, A0.y, A1.x, A1.y);
+      if (last && a.alast != nullptr && sh == (nstar >> 3)) {
+        // state at t = L-1 from a zero start at the tile's first step
+        const ModeScalars ms = a.scal[(size_t)(d0 + ch) * a.Mp + m];
+        if (sh == 1) {  // half 0 contributes mu^(nstar - 8) A_0
+          float2 w = A0;
+          for (int i = 8; i < nstar; ++i) w = cmul(ms.mu, w);
+          hl = make_float2(hl.x + w.x, hl.y + w.y);
+        }
+        for (int i = 0; i <= jstar; ++i) {
+          const TX xv1 = *reinterpret_cast<const TX*>(xt + xt_off(nstar * CHUNK + i) + ch * XE);
+          hl = cfma(ms.lam, hl, make_float2(to_f32(xv1), 0.f));
+        }
+        a.alast[((size_t)b * a.Dp + d0 + ch) * a.Mp + m] = hl;
+      }
+    }
+    wave_lds_order();
+  }
+}
 
-  // ---- state entering the tile -------------------------------------------
-  auto pay_idx = [&](int64_t t, int cg, int g) {
-    return ((size_t)t * DW + wave * CPW + cg * 8 + sk) * a.Mp + g * 8 + sj;
-  };
-  auto h0_at = [&](int cg, int g) {
-    const int d = d0 + wave * CPW + cg * 8 + sk, m = g * 8 + sj;
-    if (a.h0 == nullptr || d >= a.D || m >= a.M) return make_float2(0.f, 0.f);
+// ---------------------------------------------------------------------------
+// Carry kernel: for every (row, channel, mode) the states entering each tile.
+// The tiles of a row are cut into segments of SEG; thread (pair, segment) folds
+// its segment's aggregates from zero (float64), the segment entry states follow
+// from the segment aggregates in order, and each thread replays its segment to
+// write the entry states of both tile halves (c, mu^8 c + A_0).  The last
+// segment also writes the state at t = L-1: lambda^last_len c_last + alast.
+// The fold order is fixed by P alone, so the result is bitwise reproducible.
+// ---------------------------------------------------------------------------
+constexpr int CARRY_SEG_MAX = 64;  // segments per row (threads per pair)
+
+__global__ __launch_bounds__(256) void fwd_carry_kernel(FwdArgs a, int seg_len, int nseg, int nsegp,
+                                                        int pairs_per_tile, int cpw, int pairs_w) {
+  __shared__ double2 sg[256];  // segment aggregates, then entry states
+  const int tid = threadIdx.x;
+  const int pw = 256 / nsegp;                    // pairs per block
+  const int seg = tid / pw, pl = tid % pw;
+  const int64_t pair = (int64_t)blockIdx.x * pw + pl;  // (chain, q)
+  const int nchains = (int)(a.B * a.NB);
+  const bool valid = pair < (int64_t)nchains * pairs_per_tile && seg < nseg;
+  const int chain = (int)(pair / pairs_per_tile), q = (int)(pair % pairs_per_tile);
+  // slot q -> (channel, mode): q = wave * 32 PAIRS + 32 (grp MG + g) + 8 c + m
+  const int MG = a.Mp / 8;
+  const int wv = q / (32 * pairs_w), s = q % (32 * pairs_w);
+  const int grp = s / (32 * MG), g = (s / 32) % MG, c = (s / 8) % 4, m8 = s % 8;
+  const int ch = wv * cpw + 4 * grp + c, m = g * 8 + m8;
+  const int64_t b = chain / a.NB;
+  const int d = (chain % a.NB) * (cpw * NWAVES) + ch;
+  const float4* agg = reinterpret_cast<const float4*>(a.agg);
+  float4* car = reinterpret_cast<float4*>(a.car);
+
+  double2 lamT = make_double2(0.0, 0.0), mu8 = lamT;
+  if (valid) {
+    const ModeCarry cc = a.cc[(size_t)d * a.Mp + m];
+    lamT = cc.lamT;
+    mu8 = cc.mu8;
+  }
+  const int64_t p0 = (int64_t)seg * seg_len;
+  const int64_t p1 = p0 + seg_len < a.P ? p0 + seg_len : a.P;  // tiles of this segment
+  // pass 1: the segment's end state from zero over tiles p0 .. min(p1, P-1)-1
+  double2 acc = make_double2(0.0, 0.0);
+  if (valid) {
+    for (int64_t pp = p0; pp < p1; ++pp) {
+      if (pp >= a.P - 1) break;  // the last tile feeds no carry
+      const float4 r = agg[(size_t)(pp * nchains + chain) * pairs_per_tile + q];
+      const double2 A0 = make_double2(r.x, r.y), A1 = make_double2(r.z, r.w);
+      acc = zfma(lamT, acc, zfma(mu8, A0, A1));
+    }
+  }
+  sg[tid] = acc;
+  __syncthreads();
+  // entry state of this segment: h0, then hop over the earlier segments in order
+  double2 lamS = lamT;  // lambda^(256 seg_len), seg_len a power of two
+  for (int e = seg_len; e > 1; e >>= 1) lamS = zmul(lamS, lamS);
+  double2 ent = make_double2(0.0, 0.0);
+  if (valid && a.h0 != nullptr && d < a.D && m < a.M) {
     const float* h = a.h0 + ((size_t)(b * a.D + d) * a.M + m) * 2;
-    return make_float2(h[0], h[1]);
-  };
-  float2 carry[NCG][MG];
-  if (p == 0) {
-#pragma unroll
-    for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-      for (int g = 0; g < MG; ++g) carry[cg][g] = h0_at(cg, g);
-  } else {
-    if (tid == 0) s_u[1] = ld_flag(a.flags + (tk - nchains));
-    __syncthreads();
-    const uint32_t fpred = s_u[1];
-    if (fpred != FLAG_INCL && !last) {
-      // the predecessor is not resolved yet: publish this tile's aggregate first
-#pragma unroll
-      for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-        for (int g = 0; g < MG; ++g) st_agent(a.pay_agg + pay_idx(tk, cg, g), aggv[cg][g]);
-      __builtin_amdgcn_s_waitcnt(0);
-      __syncthreads();
-      if (tid == 0) st_flag(a.flags + tk, FLAG_AGG);
-    }
-    int64_t jres;  // nearest chain tile with its inclusive state out (-1: row start)
-    if (fpred == FLAG_INCL) {
-      jres = p - 1;
-    } else {
-      if (wave == 0) {
-        int64_t top = p - 1;
-        int64_t res = -2;
-        uint32_t it = 0;
-        while (res == -2) {
-          const int64_t j = top - lane;
-          const uint32_t fl = (j >= 0) ? ld_flag(a.flags + j * nchains + chain) : FLAG_INCL;
-          const uint64_t incl = __ballot(fl == FLAG_INCL);
-          const uint64_t none = __ballot(fl == FLAG_NONE);
-          if (incl != 0) {
-            const int l = __ffsll((unsigned long long)incl) - 1;
-            const uint64_t nearer = (l == 0) ? 0ull : (~0ull >> (64 - l));
-            if ((none & nearer) == 0) res = top - l;
-          } else if (none == 0) {
-            top -= 64;  // the whole window holds aggregates: keep looking further back
-            continue;
-          }
-          if (res == -2) {
-            if (++it >= SPIN_LIMIT) {
-              if (lane == 0) atomicOr(a.error, 1u);
-              res = -1;
-            } else {
-              __builtin_amdgcn_s_sleep(1);
-            }
-          }
+    ent = make_double2(h[0], h[1]);
+  }
+  for (int s2 = 0; s2 < seg; ++s2) ent = zfma(lamS, ent, sg[s2 * pw + pl]);
+  // pass 2: replay, writing the entry states of every tile of the segment
+  if (valid) {
+    double2 cst = ent;
+    for (int64_t pp = p0; pp < p1; ++pp) {
+      const size_t idx = (size_t)(pp * nchains + chain) * pairs_per_tile + q;
+      const float4 r = agg[idx];
+      const double2 A0 = make_double2(r.x, r.y), A1 = make_double2(r.z, r.w);
+      const double2 half = zfma(mu8, cst, A0);
+      if (car != nullptr) car[idx] = make_float4((float)cst.x, (float)cst.y, (float)half.x, (float)half.y);
+      if (pp == a.P - 1) {
+        if (a.h_out != nullptr && d < a.D && m < a.M) {
+          const double2 lE = a.cc[(size_t)d * a.Mp + m].lamEll;
+          const float2 al = a.alast[((size_t)b * a.Dp + d) * a.Mp + m];
+          const double2 hL = zfma(lE, cst, make_double2(al.x, al.y));
+          float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + m) * 2;
+          ho[0] = (float)hL.x;
+          ho[1] = (float)hL.y;
         }
-        if (lane == 0) s_j = res;
+      } else {
+        cst = zfma(lamT, cst, zfma(mu8, A0, A1));
       }
-      __syncthreads();
-      jres = s_j;
-    }
-    // canonical forward recurrence from the resolved state; the aggregates are
-    // loaded in batches so that their latencies overlap
-#pragma unroll
-    for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-      for (int g = 0; g < MG; ++g)
-        carry[cg][g] = (jres >= 0) ? ld_agent(a.pay_inc + pay_idx(jres * nchains + chain, cg, g))
-                                   : h0_at(cg, g);
-    constexpr int LB = 8;
-    for (int64_t i = jres + 1; i < p; i += LB) {
-      const int n = (p - i) < LB ? (int)(p - i) : LB;
-      float2 v[NCG][MG][LB];
-#pragma unroll
-      for (int u = 0; u < LB; ++u)
-#pragma unroll
-        for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-          for (int g = 0; g < MG; ++g)
-            v[cg][g][u] = (u < n) ? ld_agent(a.pay_agg + pay_idx((i + u) * nchains + chain, cg, g))
-                                  : make_float2(0.f, 0.f);
-#pragma unroll
-      for (int u = 0; u < LB; ++u)
-        if (u < n) {
-#pragma unroll
-          for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-            for (int g = 0; g < MG; ++g)
-              carry[cg][g] = cfma(msc[cg][g].lamT, carry[cg][g], v[cg][g][u]);
-        }
     }
   }
-  if (!last) {
-    // publish the inclusive state: lambda^256 carry + own aggregate
-#pragma unroll
-    for (int cg = 0; cg < NCG; ++cg)
-#pragma unroll
-      for (int g = 0; g < MG; ++g)
-        st_agent(a.pay_inc + pay_idx(tk, cg, g), cfma(msc[cg][g].lamT, carry[cg][g], aggv[cg][g]));
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (tid == 0) st_flag(a.flags + tk, FLAG_INCL);
-  }
+}
 
-  // ---- per channel group: carried state per chunk, then y = T x + U H -------
+// ---------------------------------------------------------------------------
+// Apply kernel: each scan lane runs its 8 chunks from its half's entry state
+// and leaves the state entering every chunk in the scan buffer; then per channel
+// y = T x + U H on MFMA, written over the drive column; the tile leaves as rows.
+// ---------------------------------------------------------------------------
+template <typename TX, typename TY, int MG>
+__global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(FwdArgs a) {
+  typedef FwdTile<TX, MG> F;
+  typedef typename F::PT PT;
+  constexpr int DW = F::DW, CPW = F::CPW, NGRP = F::NGRP;
+  // bf16 drive with float32 output: y leaves straight from the MFMA registers
+  constexpr bool SEPY = !__is_same(TX, TY);
+  __shared__ __align__(16) char xt[XT_BYTES];
+  __shared__ __align__(16) float sbuf[NWAVES * F::WBUF];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ln = lane & 15, lq = lane >> 4;
+  const int sh = lane & 1, sm = (lane >> 1) & 7, sc = lane >> 4;
+  const int nchains = (int)(a.B * a.NB);
+  const int64_t tile = blockIdx.x;
+  const int64_t p = tile / nchains;
+  const int chain = (int)(tile % nchains);
+  const int64_t b = chain / a.NB;
+  const int d0 = (chain % a.NB) * DW;
+  const int64_t t0 = p * TILE_T;
+  const bool full = a.fast_io && t0 + TILE_T <= a.L && d0 + DW <= a.D;
+  const int cw0 = wave * CPW;
+  const char* tab = reinterpret_cast<const char*>(a.tab);
+  float* wb = sbuf + wave * F::WBUF;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
+
+  auto tab_of = [&](int ch) {
+    return tab + (size_t)(d0 + ch) * F::NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+  };
+  typename PT::AOp vop[4][MG], top[4];
+  f4 uop[4][MG];
+  auto fetch_v = [&](int grp) {
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg) {
-    {
-      const int ch = wave * CPW + cg * 8 + sk;
+    for (int k = 0; k < 4; ++k)
 #pragma unroll
-      for (int g = 0; g < MG; ++g) {
-        float2 w = carry[cg][g];
-        float2 hlast = w;
+      for (int g = 0; g < MG; ++g) vop[k][g] = PT::load_a(tab_of(cw0 + 4 * grp + k) + (1 + 2 * g) * TAB_MAT_BYTES);
+  };
+  auto fetch_tu = [&](int grp) {
 #pragma unroll
-        for (int n = 0; n < NCHUNK; ++n) {
-          const float2 h = make_float2(hx[cg][g][n].x + w.x, hx[cg][g][n].y + w.y);
-          *reinterpret_cast<float2*>(&sb[sk * F::KSTR + n * F::NSTR + g * 16 + 2 * sj]) = h;
-          if (n == nstar) hlast = h;
-          w = cmul(msc[cg][g].mu, w);
-        }
-        const int dch = d0 + ch, m = g * 8 + sj;
-        if (last && a.h_out != nullptr && dch < a.D && m < a.M) {
-          const float2 hL = tail_state(hlast, &xt[ch * XP], nstar, jstar_l, msc[cg][g].lam);
-          float* ho = a.h_out + ((size_t)(b * a.D + dch) * a.M + m) * 2;
-          ho[0] = hL.x;
-          ho[1] = hL.y;
-        }
+    for (int k = 0; k < 4; ++k) {
+      const char* tp = tab_of(cw0 + 4 * grp + k);
+      top[k] = PT::load_a(tp);
+#pragma unroll
+      for (int g = 0; g < MG; ++g) uop[k][g] = load_f4(tp + (2 + 2 * g) * TAB_MAT_BYTES);
+    }
+  };
+  // entry state of this lane's half, per (group, mode group)
+  const float2* car = reinterpret_cast<const float2*>(reinterpret_cast<const float4*>(a.car) +
+                                                      (size_t)tile * DW * a.Mp + wave * 32 * F::PAIRS);
+  float2 ent[NGRP][MG];
+#pragma unroll
+  for (int grp = 0; grp < NGRP; ++grp)
+#pragma unroll
+    for (int g = 0; g < MG; ++g) ent[grp][g] = car[2 * ((grp * MG + g) * 32 + sc * 8 + sm) + sh];
+  fetch_v(0);
+  fetch_tu(0);
+  tile_load<TX>(xt, reinterpret_cast<const TX*>(a.x), b, t0, d0, a.L, a.D, full, tid);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+#pragma unroll
+  for (int grp = 0; grp < NGRP; ++grp) {
+    typename PT::XOp xv[4];
+    group_states<TX, MG>(xt, wb, cw0 + 4 * grp, vop, xv, ln, lq);
+    if (grp + 1 < NGRP) fetch_v(grp + 1);
+    wave_lds_order();
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      const float2 mu = a.scal[(size_t)(d0 + cw0 + 4 * grp + sc) * a.Mp + g * 8 + sm].mu;
+      float2 run = ent[grp][g];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        float* hp = &wb[sc * F::CSTR + (8 * sh + j) * F::NSTR + g * 16 + 2 * sm];
+        const float2 sv = *reinterpret_cast<const float2*>(hp);
+        *reinterpret_cast<float2*>(hp) = run;  // state entering chunk 8 sh + j
+        run = cfma(mu, run, sv);
       }
     }
-    __syncthreads();
+    wave_lds_order();
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int ch = wave * CPW + cg * 8 + k;
-      const char* tp = tab + (size_t)(d0 + ch) * F::NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-      f4 acc = PT::mma(PT::load_a(tp), PT::load_x(&xt[ch * XP + PT::x_off(li, lq)]), zero);
+    for (int k = 0; k < 4; ++k) {
+      const int ch = cw0 + 4 * grp + k;
+      f4 acc = PT::mma(top[k], xv[k], zero);
 #pragma unroll
       for (int g = 0; g < MG; ++g)
-        acc = mma_f32(load_f4(tp + (2 + 2 * g) * TAB_MAT_BYTES),
-                      load_f4(&sb[k * F::KSTR + li * F::NSTR + g * 16 + lq * 4]), acc);
+        acc = mma_f32(uop[k][g], *reinterpret_cast<const f4*>(&wb[k * F::CSTR + ln * F::NSTR + g * 16 + lq * 4]),
+                      acc);
       if (SEPY) {
         const int d = d0 + ch;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int64_t t = t0 + li * CHUNK + lq * 4 + r;
-          if (d < a.D && t < a.L)
-            reinterpret_cast<float*>(a.y)[(b * a.L + t) * (int64_t)a.D + d] = acc[r];
+          const int64_t t = t0 + ln * CHUNK + lq * 4 + r;
+          if (d < a.D && t < a.L) reinterpret_cast<float*>(a.y)[(b * a.L + t) * (int64_t)a.D + d] = acc[r];
         }
       } else {
-        TY v[4];
+        // rows 16 ln + 4 lq + r: group 2 ln + (lq >> 1), rows 4 (lq & 1) + r
+        char* dst = xt + (2 * ln + (lq >> 1)) * XGRP + 4 * (lq & 1) * XROW + ch * (int)sizeof(TY);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = from_f32<TY>(acc[r]);
-        TY* dst = reinterpret_cast<TY*>(xt) + ch * XP + li * CHUNK + lq * 4;
-        if (sizeof(TY) == 2)
-          *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(v);
-        else
-          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
+        for (int r = 0; r < 4; ++r) *reinterpret_cast<TY*>(dst + r * XROW) = from_f32<TY>(acc[r]);
       }
     }
+    if (grp + 1 < NGRP) fetch_tu(grp + 1);
+    wave_lds_order();
+  }
+  if (!SEPY) {
     __syncthreads();
+    tile_store<TY>(reinterpret_cast<TY*>(a.y), xt, b, t0, d0, a.L, a.D, full, tid);
   }
-
-  if (!SEPY)
-    store_tile_any<TY, DW>(reinterpret_cast<TY*>(a.y), reinterpret_cast<const TY*>(xt), b, t0, d0,
-                           a.L, a.D, tid);
-}
-
-// ---------------------------------------------------------------------------
-// Cross-tile carry for the prompt state: for each (b, d, m), in float64,
-//   h = lambda^TILE_T h + agg[p] for p < P-1, then h_{L-1} = lambda^last_len h + agg[P-1].
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void carry_fwd_kernel(const float2* __restrict__ agg,
-                                                        float* __restrict__ hout,
-                                                        const ModeCarry* __restrict__ cc, int B,
-                                                        int64_t P, int D, int M, int Dp, int Mp) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)B * Dp * Mp) return;
-  const int m = (int)(idx % Mp);
-  const int d = (int)((idx / Mp) % Dp);
-  const int64_t b = idx / ((int64_t)Mp * Dp);
-  if (d >= D || m >= M) return;
-  double2 h = make_double2(0.0, 0.0);
-  const ModeCarry c = cc[(size_t)d * Mp + m];
-  constexpr int BATCH = 16;
-  for (int64_t p0 = 0; p0 < P; p0 += BATCH) {
-    float2 ag[BATCH];
-#pragma unroll
-    for (int j = 0; j < BATCH; ++j) {
-      const int64_t p = p0 + j;
-      ag[j] = (p < P) ? agg[((size_t)(b * P + p) * Dp + d) * Mp + m] : make_float2(0.f, 0.f);
-    }
-#pragma unroll
-    for (int j = 0; j < BATCH; ++j) {
-      const int64_t p = p0 + j;
-      if (p < P) {
-        const double2 prop = (p < P - 1) ? c.lamT : c.lamEll;
-        h = zfma(prop, h, make_double2((double)ag[j].x, (double)ag[j].y));
-      }
-    }
-  }
-  const size_t sidx = ((size_t)(b * D + d) * M + m) * 2;
-  hout[sidx] = (float)h.x;
-  hout[sidx + 1] = (float)h.y;
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t n) {
@@ -587,60 +602,71 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t n) {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       uint32_t* flags, int64_t nflags, hipStream_t st) {
+                       hipStream_t st) {
   if (bwd)
     hipLaunchKernelGGL((prep_kernel<TA, true>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc, flags,
-                       nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc);
   else
     hipLaunchKernelGGL((prep_kernel<TA, false>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc, flags,
-                       nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc);
   return hipGetLastError();
 }
 template hipError_t launch_prep<float>(const Geometry&, const float*, const float*, const float*,
                                        const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                       uint32_t*, int64_t, hipStream_t);
+                                       hipStream_t);
 template hipError_t launch_prep<bf16_t>(const Geometry&, const float*, const float*, const float*,
                                         const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                        uint32_t*, int64_t, hipStream_t);
+                                       hipStream_t);
 
 template <typename TX>
-hipError_t launch_fwd_state(const Geometry& g, const FwdArgs& a, hipStream_t st) {
+hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
+                          hipEvent_t ev1) {
   const dim3 grid((unsigned)(g.B * g.P * g.NB)), block(NTHREADS);
   if (g.MG == 1)
-    hipLaunchKernelGGL((fwd_state_kernel<TX, 1>), grid, block, 0, st, a);
+    launch_timed(fwd_agg_kernel<TX, 1>, grid, block, st, ev0, ev1, a);
   else
-    hipLaunchKernelGGL((fwd_state_kernel<TX, 2>), grid, block, 0, st, a);
+    launch_timed(fwd_agg_kernel<TX, 2>, grid, block, st, ev0, ev1, a);
   return hipGetLastError();
 }
-template hipError_t launch_fwd_state<float>(const Geometry&, const FwdArgs&, hipStream_t);
-template hipError_t launch_fwd_state<bf16_t>(const Geometry&, const FwdArgs&, hipStream_t);
+template hipError_t launch_fwd_agg<float>(const Geometry&, const FwdArgs&, hipStream_t, hipEvent_t,
+                                          hipEvent_t);
+template hipError_t launch_fwd_agg<bf16_t>(const Geometry&, const FwdArgs&, hipStream_t, hipEvent_t,
+                                           hipEvent_t);
+
+hipError_t launch_fwd_carry(const Geometry& g, const FwdArgs& a, hipStream_t st) {
+  // segments: at most CARRY_SEG_MAX per row, each a power-of-two number of tiles
+  int seg_len = 1;
+  while ((g.P + seg_len - 1) / seg_len > CARRY_SEG_MAX) seg_len *= 2;
+  if (seg_len < 16 && g.P > 16) seg_len = 16;
+  const int nseg = (int)((g.P + seg_len - 1) / seg_len);
+  int nsegp = 1;
+  while (nsegp < nseg) nsegp *= 2;
+  const int pw = 256 / nsegp;
+  const int pairs_per_tile = g.DW * g.Mp;
+  const int64_t npairs = g.B * g.NB * (int64_t)pairs_per_tile;
+  const int cpw = g.DW / NWAVES;
+  const int pairs_w = (cpw / 4) * g.MG;
+  hipLaunchKernelGGL(fwd_carry_kernel, dim3((unsigned)((npairs + pw - 1) / pw)), dim3(256), 0, st, a,
+                     seg_len, nseg, nsegp, pairs_per_tile, cpw, pairs_w);
+  return hipGetLastError();
+}
 
 template <typename TX, typename TY>
-hipError_t launch_fwd_fused(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
+hipError_t launch_fwd_apply(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1) {
   const dim3 grid((unsigned)(g.B * g.P * g.NB)), block(NTHREADS);
   if (g.MG == 1)
-    launch_timed(fwd_fused_kernel<TX, TY, 1>, grid, block, st, ev0, ev1, a);
+    launch_timed(fwd_apply_kernel<TX, TY, 1>, grid, block, st, ev0, ev1, a);
   else
-    launch_timed(fwd_fused_kernel<TX, TY, 2>, grid, block, st, ev0, ev1, a);
+    launch_timed(fwd_apply_kernel<TX, TY, 2>, grid, block, st, ev0, ev1, a);
   return hipGetLastError();
 }
-template hipError_t launch_fwd_fused<float, float>(const Geometry&, const FwdArgs&, hipStream_t,
+template hipError_t launch_fwd_apply<float, float>(const Geometry&, const FwdArgs&, hipStream_t,
                                                    hipEvent_t, hipEvent_t);
-template hipError_t launch_fwd_fused<bf16_t, bf16_t>(const Geometry&, const FwdArgs&, hipStream_t,
+template hipError_t launch_fwd_apply<bf16_t, bf16_t>(const Geometry&, const FwdArgs&, hipStream_t,
                                                      hipEvent_t, hipEvent_t);
-template hipError_t launch_fwd_fused<bf16_t, float>(const Geometry&, const FwdArgs&, hipStream_t,
+template hipError_t launch_fwd_apply<bf16_t, float>(const Geometry&, const FwdArgs&, hipStream_t,
                                                     hipEvent_t, hipEvent_t);
-
-hipError_t launch_carry_fwd(const Geometry& g, const float2* agg, float* hout, const ModeCarry* cc,
-                            hipStream_t st) {
-  const int64_t n = g.B * (int64_t)g.Dp * g.Mp;
-  hipLaunchKernelGGL(carry_fwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, agg,
-                     hout, cc, (int)g.B, g.P, (int)g.D, (int)g.M, g.Dp, g.Mp);
-  return hipGetLastError();
-}
 
 hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t st) {
   if (n <= 0) return hipSuccess;

@@ -11,23 +11,21 @@ enum { MODE_STATE = 0, MODE_APPLY = 1 };
 
 struct FwdArgs {
   const void* x;
-  void* y;
+  void* y;           // null for the prompt state
   int64_t B, L;
   int D, M;
   int NB, Dp, Mp;
   int64_t P;
   int last_len;
+  int fast_io;       // x and y 16-byte aligned and D * element size a multiple of 16
   const void* tab;
   const ModeScalars* scal;
+  const ModeCarry* cc;
   const float* h0;   // [B][D][M][2] or null
-  float* h_out;      // [B][D][M][2] or null
-  float2* agg;       // prompt state: per-tile aggregates [B][P][Dp][Mp]
-  // single-pass chaining (ticket order = time-major over chains (b, channel block))
-  uint32_t* ticket;  // tile ticket counter
-  uint32_t* flags;   // per tile: FLAG_NONE / FLAG_AGG / FLAG_INCL
-  uint32_t* error;   // set when a bounded wait gives up
-  float2* pay_agg;   // per tile [DW][Mp]: end state of the tile's own drives
-  float2* pay_inc;   // per tile [DW][Mp]: end state including all earlier tiles
+  float* h_out;      // [B][D][M][2] or null: state at t = L-1
+  void* agg;         // per tile [DW * Mp] float4: half-tile end states (A_0, A_1)
+  void* car;         // per tile [DW * Mp] float4: entry states of both halves (null: none)
+  float2* alast;     // [B][Dp][Mp]: state at t = L-1 from a zero start at the last tile
 };
 
 struct BwdArgs {
@@ -49,17 +47,17 @@ struct BwdArgs {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       uint32_t* flags, int64_t nflags, hipStream_t st);
+                       hipStream_t st);
 
 template <typename TX>
-hipError_t launch_fwd_state(const Geometry& g, const FwdArgs& a, hipStream_t st);
+hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st,
+                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+
+hipError_t launch_fwd_carry(const Geometry& g, const FwdArgs& a, hipStream_t st);
 
 template <typename TX, typename TY>
-hipError_t launch_fwd_fused(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
+hipError_t launch_fwd_apply(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
                             hipEvent_t ev1);
-
-hipError_t launch_carry_fwd(const Geometry& g, const float2* agg, float* hout, const ModeCarry* cc,
-                            hipStream_t st);
 
 // Launch with optional start/stop events recorded around this one kernel.
 template <typename K, typename... Args>
