@@ -42,6 +42,12 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // Geometry of the tiled kernels for activations of type act (tile width depends
 // on the element size: 128-byte rows).
+// words ahead of the segment flags: [0] segment ticket, [1] error word
+constexpr size_t FLAG_HEADER = 64;
+// segments of the single-kernel forward: the work-groups of one wave over the
+// 256 compute units of an MI355X
+constexpr int64_t SEG_TARGET = 256;
+
 Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) {
   Geometry g;
   g.B = B;
@@ -55,6 +61,10 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
   g.Mp = MODES_PER_GROUP * g.MG;
   g.P = L > 0 ? (L + TILE_T - 1) / TILE_T : 0;
   g.last_len = L > 0 ? (int)(L - (g.P - 1) * TILE_T) : 0;
+  // single-kernel forward: about SEG_TARGET segments over all rows (one work-group per CU)
+  const int64_t tiles = B * g.NB * g.P;
+  g.seg_len = tiles > 0 ? (int)((tiles + SEG_TARGET - 1) / SEG_TARGET) : 1;
+  if (g.seg_len > g.P) g.seg_len = (int)(g.P > 0 ? g.P : 1);
   return g;
 }
 
@@ -80,6 +90,10 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
     }
     w.alast = off;  // [B][Dp][Mp] state at t = L-1 from a zero start at the last tile
     off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float2));
+    if (op == RES_OP_FWD) {  // segment flags: ticket, error word, one per (segment, wave)
+      w.flags = off;
+      off += align256((FLAG_HEADER + (size_t)g.B * g.P * g.NB * SEG_WAVES) * sizeof(uint32_t));
+    }
   } else {
     w.agg = off;
     off += align256(tiles_modes * sizeof(float4));
@@ -176,10 +190,16 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   char* base = (char*)ws;
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
+  const bool segs = g.MG == 1;  // single-kernel forward for M <= 8
+  uint32_t* fl = (uint32_t*)(base + w.flags);
+  const int64_t nflags =
+      segs ? (int64_t)(FLAG_HEADER + g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len) * SEG_WAVES) : 0;
   hipError_t e =
       x_dt == RES_BF16
-          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
-          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
+                                segs ? fl : nullptr, nflags)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
+                               segs ? fl : nullptr, nflags);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x;
@@ -201,14 +221,32 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   a.cc = cc;
   a.h0 = h0;
   a.h_out = h_out;
+  hipEvent_t ev0, ev1;
+  take_timer(&ev0, &ev1);
+  if (segs) {
+    const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;
+    a.seg_len = g.seg_len;
+    a.seg_per_chain = (int)((g.P + g.seg_len - 1) / g.seg_len);
+    a.ticket = fl;
+    a.error = fl + 1;
+    a.flags = fl + FLAG_HEADER;
+    a.pay_agg = (float2*)(base + w.agg);
+    a.pay_inc = a.pay_agg + tiles_modes;
+    if (x_dt == RES_F32)
+      e = launch_fwd_segments<float, float>(g, a, st, ev0, ev1);
+    else if (y_dt == RES_BF16)
+      e = launch_fwd_segments<bf16_t, bf16_t>(g, a, st, ev0, ev1);
+    else
+      e = launch_fwd_segments<bf16_t, float>(g, a, st, ev0, ev1);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    return RES_OK;
+  }
   a.agg = base + w.agg;
   a.car = base + w.carry;
   a.alast = (float2*)(base + w.alast);
   e = x_dt == RES_F32 ? launch_fwd_agg<float>(g, a, st) : launch_fwd_agg<bf16_t>(g, a, st);
   if (e != hipSuccess) return hip_fail(e, "aggregate launch");
   if ((e = launch_fwd_carry(g, a, st)) != hipSuccess) return hip_fail(e, "carry launch");
-  hipEvent_t ev0, ev1;
-  take_timer(&ev0, &ev1);
   if (x_dt == RES_F32)
     e = launch_fwd_apply<float, float>(g, a, st, ev0, ev1);
   else if (y_dt == RES_BF16)

@@ -9,6 +9,9 @@ namespace res {
 
 enum { MODE_STATE = 0, MODE_APPLY = 1 };
 
+// waves per work-group of the single-kernel forward (each publishes its own sub-chain)
+constexpr int SEG_WAVES = 8;
+
 struct FwdArgs {
   const void* x;
   void* y;           // null for the prompt state
@@ -26,6 +29,13 @@ struct FwdArgs {
   void* agg;         // per tile [DW * Mp] float4: half-tile end states (A_0, A_1)
   void* car;         // per tile [DW * Mp] float4: entry states of both halves (null: none)
   float2* alast;     // [B][Dp][Mp]: state at t = L-1 from a zero start at the last tile
+  // single-kernel forward: segments of seg_len tiles, ticket order time-major over chains
+  int seg_len, seg_per_chain;
+  uint32_t* ticket;  // segment ticket counter
+  uint32_t* flags;   // per (segment, wave): FLAG_NONE / FLAG_AGG / FLAG_INCL
+  uint32_t* error;   // set when a bounded wait gives up
+  float2* pay_agg;   // per (segment, wave) [32 Mp / 8]: the segment's own end state
+  float2* pay_inc;   // per (segment, wave): end state including all earlier segments
 };
 
 struct BwdArgs {
@@ -47,13 +57,17 @@ struct BwdArgs {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st);
+                       hipStream_t st, uint32_t* flags = nullptr, int64_t nflags = 0);
 
 template <typename TX>
 hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st,
                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 hipError_t launch_fwd_carry(const Geometry& g, const FwdArgs& a, hipStream_t st);
+
+template <typename TX, typename TY>
+hipError_t launch_fwd_segments(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
+                               hipEvent_t ev1);
 
 template <typename TX, typename TY>
 hipError_t launch_fwd_apply(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
