@@ -13,7 +13,7 @@ exceeds the 256 MB Infinity Cache.  The JSON line also carries
             replayed from a captured HIP graph of the same calls;
   train     one forward + backward of a training layer (B=8, L=8192, D=256, M=8,
             bf16), as time per layer;
-  roofline  the dominant kernel (the single-pass forward tile kernel) against the HBM
+  roofline  the dominant kernel (the single-pass forward segment kernel) against the HBM
             peak: algorithmic bytes (2 B read + 2 B written per token-channel)
             per launch over its average launch time, measured with HIP events
             recorded around that kernel alone;
@@ -37,7 +37,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 COPY_BYTES = 256 << 20  # calibration copy of the counter run
 METRIC = "prefill mix tokens·ch/s + decode steps/s at L=32K; % of HBM peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_fused_prefill_B4_L32768_D256_M8.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_seg_prefill_B4_L32768_D256_M8.json")
 
 
 def log(msg):
@@ -167,7 +167,7 @@ def main():
     value = n_tok / (ms_step * 1e-3)
     alg_bytes = n_tok * 4
     achieved = alg_bytes / (k_avg_ms * 1e-3) / 1e9
-    log(f"prefill: {ms_step * 1e3:.1f} us/step (events), apply kernel {k_avg_ms * 1e3:.1f} us, "
+    log(f"prefill: {ms_step * 1e3:.1f} us/step (events), segment kernel {k_avg_ms * 1e3:.1f} us, "
         f"wall {t_wall / args.steps * 1e3:.1f} us/step")
 
     # ---------------- decode ----------------
@@ -279,7 +279,7 @@ def main():
         "train_layer": {"workload": "B8 L8192 D256 M8 bf16 (one of the 6 layers)",
                         "fwd_us": tr_fwd_us, "bwd_us": tr_bwd_us,
                         "bwd_alg_GBs": 8 * 8192 * 256 * 6 / (tr_bwd_us * 1e-6) / 1e9},
-        "roofline": {"bound": "hbm", "kernel": "fwd_fused_kernel",
+        "roofline": {"bound": "hbm", "kernel": "fwd_seg_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic,

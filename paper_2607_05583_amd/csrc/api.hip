@@ -69,9 +69,9 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
 }
 
 WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
-  (void)act;
   WsLayout w{};
   size_t off = 0;
+  (void)act;
   const int nm = op == RES_OP_BWD ? bwd_mats(g.MG) : fwd_mats(g.MG);
   const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;  // = tiles * DW * Mp
   w.tab = off;
@@ -93,6 +93,10 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
     if (op == RES_OP_FWD) {  // segment flags: ticket, error word, one per (segment, wave)
       w.flags = off;
       off += align256((FLAG_HEADER + (size_t)g.B * g.P * g.NB * SEG_WAVES) * sizeof(uint32_t));
+      w.mpow = off;  // [Dp][16][Mp] lambda^(16 j)
+      off += align256((size_t)g.Dp * CHUNK * g.Mp * sizeof(float2));
+      w.spow = off;  // [Dp][17][Mp] lambda^(256 seg_len n)
+      off += align256((size_t)g.Dp * (CHUNK + 1) * g.Mp * sizeof(float2));
     }
   } else {
     w.agg = off;
@@ -192,14 +196,16 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
   const bool segs = g.MG == 1;  // single-kernel forward for M <= 8
   uint32_t* fl = (uint32_t*)(base + w.flags);
+  float2* mpow = (float2*)(base + w.mpow);
+  float2* spow = (float2*)(base + w.spow);
   const int64_t nflags =
       segs ? (int64_t)(FLAG_HEADER + g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len) * SEG_WAVES) : 0;
   hipError_t e =
       x_dt == RES_BF16
           ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
-                                segs ? fl : nullptr, nflags)
+                                segs ? mpow : nullptr, segs ? spow : nullptr, segs ? fl : nullptr, nflags)
           : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
-                               segs ? fl : nullptr, nflags);
+                               segs ? mpow : nullptr, segs ? spow : nullptr, segs ? fl : nullptr, nflags);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x;
@@ -219,19 +225,19 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   a.tab = base + w.tab;
   a.scal = scal;
   a.cc = cc;
+  a.mpow = mpow;
+  a.spow = spow;
   a.h0 = h0;
   a.h_out = h_out;
   hipEvent_t ev0, ev1;
   take_timer(&ev0, &ev1);
   if (segs) {
-    const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;
     a.seg_len = g.seg_len;
     a.seg_per_chain = (int)((g.P + g.seg_len - 1) / g.seg_len);
     a.ticket = fl;
     a.error = fl + 1;
     a.flags = fl + FLAG_HEADER;
     a.pay_agg = (float2*)(base + w.agg);
-    a.pay_inc = a.pay_agg + tiles_modes;
     if (x_dt == RES_F32)
       e = launch_fwd_segments<float, float>(g, a, st, ev0, ev1);
     else if (y_dt == RES_BF16)

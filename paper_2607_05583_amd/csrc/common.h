@@ -98,44 +98,17 @@ template <> struct Path<bf16_t> {
 };
 
 // ---------------------------------------------------------------------------
-// Carried-state products y += U H of the forward (per channel, chunks as the 16
-// columns).  The scan lanes put the state entering chunk n of (channel, mode
-// m) into the chunk's 16-float row of the scan buffer; the MFMA lanes read it
-// back as the B operand.
-//   float drives: float32 states, four v_mfma_f32_16x16x4_f32 (row = 16 floats).
-//   bf16 drives: the row holds [Hh | Hl] (16 + 16 bf16, H = Hh + Hl split at
-//     the put); with the table operand [Uh | Ul] two v_mfma_f32_16x16x32_bf16
-//     give [Uh | Ul][Hh; Hh] + [Uh | Ul][Hl; 0] = Uh Hh + Ul Hh + Uh Hl, which
-//     misses only Ul Hl (~2^-18 relative).
+// Carried-state rows of the multi-group forward: the state entering chunk n of
+// (channel, mode m) is put into the chunk's row of a scan buffer as float32
+// (re, im) at floats 2m, 2m+1; the MFMA lanes read the row back as the B
+// operand of y += U H (float32 layout, four v_mfma_f32_16x16x4_f32).
 // ---------------------------------------------------------------------------
-template <typename TX> struct StateOp;
-template <> struct StateOp<float> {
-  typedef f4 UOp;
-  __device__ static __forceinline__ UOp load_u(const void* p) { return *reinterpret_cast<const f4*>(p); }
+struct StateRow {
   __device__ static __forceinline__ void put(float* row, int m, float2 h) {
     *reinterpret_cast<float2*>(row + 2 * m) = h;
   }
   __device__ static __forceinline__ f4 apply(const f4& u, const float* row, int lq, f4 acc) {
     return mma_f32(u, *reinterpret_cast<const f4*>(row + 4 * lq), acc);
-  }
-};
-template <> struct StateOp<bf16_t> {
-  typedef bf8 UOp;
-  typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
-  __device__ static __forceinline__ UOp load_u(const void* p) { return *reinterpret_cast<const bf8*>(p); }
-  __device__ static __forceinline__ void put(float* row, int m, float2 h) {
-    const bf2 hi = {(__bf16)h.x, (__bf16)h.y};
-    const bf2 lo = {(__bf16)(h.x - (float)hi[0]), (__bf16)(h.y - (float)hi[1])};
-    reinterpret_cast<bf2*>(row)[m] = hi;
-    reinterpret_cast<bf2*>(row)[8 + m] = lo;
-  }
-  __device__ static __forceinline__ f4 apply(const bf8& u, const float* row, int lq, f4 acc) {
-    const char* r = reinterpret_cast<const char*>(row) + 16 * (lq & 1);
-    const bf8 hh = *reinterpret_cast<const bf8*>(r);
-    bf8 hl = *reinterpret_cast<const bf8*>(r + 32);
-    if (lq >= 2) hl = bf8{};
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u, hh, acc, 0, 0, 0);
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(u, hl, acc, 0, 0, 0);
   }
 };
 
@@ -185,10 +158,11 @@ constexpr size_t TAB_MAT_BYTES = 64 * TAB_LANE_BYTES;
 
 // Number of 16x16 operand matrices per channel in the parameter table.
 // Forward: T, then per mode group V[g], U[g].  Backward: Tt, then per mode group
-// Eq[g], Er[g], Xs[g], Xw[g], Ub[g].  All use the activation path's layout
-// except the backward's Ub, which multiplies float32 states and is stored in
-// the float32 layout (the forward's U pairs with split states, see StateOp).
-__host__ __device__ inline int fwd_mats(int MG) { return 1 + 2 * MG; }
+// Eq[g], Er[g], Xs[g], Xw[g], Ub[g].  Matrices that multiply an activation use
+// the activation path's layout; those that multiply computed float32 states
+// (the forward's U, the backward's Ub) use the float32 layout.
+__host__ __device__ constexpr int fwd_mats(int MG) { return 1 + 2 * MG; }
+__host__ __device__ inline bool fwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 2 == 1; }
 __host__ __device__ inline int bwd_mats(int MG) { return 1 + 5 * MG; }
 __host__ __device__ inline bool bwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 5 == 4; }
 
@@ -198,7 +172,6 @@ struct ModeScalars {
   float2 mu;      // lambda^CHUNK
   float2 mu8;     // lambda^(TILE_T / 2): the hop over half a tile (8 chunks)
   float2 lamT;    // lambda^TILE_T
-  float2 lamS;    // lambda^(TILE_T * seg_len): the hop over a segment of tiles
 };
 // Per-mode float64 scalars for the cross-tile carry chain.
 struct ModeCarry {
@@ -209,10 +182,10 @@ struct ModeCarry {
 
 // Offsets (bytes) of the workspace regions.
 struct WsLayout {
-  size_t tab, scal, carryc, agg, carry, alast, flags, part, q0, total;
+  size_t tab, scal, carryc, mpow, spow, agg, carry, alast, flags, part, q0, total;
 };
 
 // Flags of the segment look-back.
-enum : uint32_t { FLAG_NONE = 0, FLAG_AGG = 1, FLAG_INCL = 2 };
+enum : uint32_t { FLAG_NONE = 0, FLAG_AGG = 1 };
 
 }  // namespace res

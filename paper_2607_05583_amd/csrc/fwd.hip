@@ -38,9 +38,11 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
                                                    TA* __restrict__ tab,
                                                    ModeScalars* __restrict__ scal,
                                                    ModeCarry* __restrict__ cc,
+                                                   float2* __restrict__ mpow,
+                                                   float2* __restrict__ spow,
                                                    uint32_t* __restrict__ flags, int64_t nflags) {
-  // lambda^0..16, then lambda^128, lambda^256, lambda^last_len, lambda^seg_steps
-  constexpr int NPW = CHUNK + 1 + 4;
+  // lambda^0..16, then lambda^128, lambda^256, lambda^last_len
+  constexpr int NPW = CHUNK + 1 + 3;
   const int d = blockIdx.x;
   const int Mp = MODES_PER_GROUP * MG;
   __shared__ double2 pw[MODES_PER_GROUP * MG_MAX][NPW];
@@ -59,8 +61,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
       const int n = k <= CHUNK          ? k
                     : k == CHUNK + 1 ? TILE_T / 2
                     : k == CHUNK + 2 ? TILE_T
-                    : k == CHUNK + 3 ? last_len
-                                     : seg_steps;
+                                     : last_len;
       double2 z = make_double2(0.0, 0.0);
       if (valid) {
         double sn, cs;
@@ -88,7 +89,6 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     ms.mu = make_float2((float)pw[m][CHUNK].x, (float)pw[m][CHUNK].y);
     ms.mu8 = make_float2((float)lH.x, (float)lH.y);
     ms.lamT = make_float2((float)lT.x, (float)lT.y);
-    ms.lamS = make_float2((float)pw[m][CHUNK + 4].x, (float)pw[m][CHUNK + 4].y);
     scal[(size_t)d * Mp + m] = ms;
     ModeCarry mc;
     mc.lamT = lT;
@@ -96,6 +96,30 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     mc.mu8 = lH;
     cc[(size_t)d * Mp + m] = mc;
   }
+  if (mpow != nullptr)  // lambda^(16 j), j = 0..15, as [d][j][Mp]
+    for (int t = threadIdx.x; t < CHUNK * Mp; t += blockDim.x) {
+      const int j = t / Mp, m = t % Mp;
+      float2 z = make_float2(0.f, 0.f);
+      if (dvalid && m < M) {
+        double sn, cs;
+        sincos((double)omega[d * M + m] * (CHUNK * j), &sn, &cs);
+        const double e = exp(-(double)gamma[d * M + m] * (CHUNK * j));
+        z = make_float2((float)(e * cs), (float)(e * sn));
+      }
+      mpow[((size_t)d * CHUNK + j) * Mp + m] = z;
+    }
+  if (spow != nullptr)  // lambda^(seg_steps n), n = 0..16, as [d][n][Mp]
+    for (int t = threadIdx.x; t < (CHUNK + 1) * Mp; t += blockDim.x) {
+      const int n = t / Mp, m = t % Mp;
+      float2 z = make_float2(0.f, 0.f);
+      if (dvalid && m < M) {
+        double sn, cs;
+        sincos((double)omega[d * M + m] * ((double)seg_steps * n), &sn, &cs);
+        const double e = exp(-(double)gamma[d * M + m] * ((double)seg_steps * n));
+        z = make_float2((float)(e * cs), (float)(e * sn));
+      }
+      spow[((size_t)d * (CHUNK + 1) + n) * Mp + m] = z;
+    }
   for (int tau = threadIdx.x; tau <= CHUNK; tau += blockDim.x) {  // K[tau] = Re sum_m c lambda^tau
     double s = 0.0;
     for (int m = 0; m < Mp; ++m) s += cm[m].x * pw[m][tau].x - cm[m].y * pw[m][tau].y;
@@ -135,7 +159,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
   const int nm = BWD ? bwd_mats(MG) : fwd_mats(MG);
   for (int task = threadIdx.x; task < nm * 64; task += blockDim.x) {
     const int mat = task / 64, l = task % 64, i = l % 16, q = l / 16;
-    const bool state_mat = BWD && bwd_mat_is_state(mat);
+    const bool state_mat = BWD ? bwd_mat_is_state(mat) : fwd_mat_is_state(mat);
     uint4 out;
     if (sizeof(TA) == 4 || state_mat) {
       float v[4];
@@ -185,11 +209,17 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
 typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
 
-constexpr int XROW = 128;                      // bytes per time row of a tile
-constexpr int XGRP = 8 * XROW + 4;             // 8 rows + pad (conflict-free operand reads)
-constexpr int XT_BYTES = (TILE_T / 8) * XGRP;  // 32896
-
-__device__ __forceinline__ int xt_off(int t) { return (t >> 3) * XGRP + (t & 7) * XROW; }
+// Time-major LDS tile of elements of ES bytes: rows of 128 bytes (the tile's
+// channels), groups of 8 rows padded so that every group starts on a 16-byte
+// boundary for the direct-to-LDS loads and row stores (bf16: +8 bytes, so the
+// 8-byte operand gathers of 16 lanes from 16 different groups spread over the
+// banks; float: +16 bytes).
+constexpr int XROW = 128;
+template <int ES> struct XLay {
+  static constexpr int GRP = 8 * XROW + (ES == 2 ? 8 : 16);
+  static constexpr int BYTES = (TILE_T / 8) * GRP;
+  __device__ static __forceinline__ int off(int t) { return (t >> 3) * GRP + (t & 7) * XROW; }
+};
 
 // Compiler-level ordering of LDS accesses inside one wave (the LDS executes a
 // wave's accesses in program order).
@@ -211,14 +241,14 @@ __device__ __forceinline__ void tile_load(char* xt, const TX* x, int64_t b, int6
     for (int i = 0; i < TILE_T / 8 / NWAVES; ++i) {
       const int g = wave * (TILE_T / 8 / NWAVES) + i;
       const char* s = src + (int64_t)(8 * g + (lane >> 3)) * rowb + (lane & 7) * 16;
-      __builtin_amdgcn_global_load_lds((gvoid_t*)s, (lvoid_t*)(xt + g * XGRP), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds((gvoid_t*)s, (lvoid_t*)(xt + g * XLay<XE>::GRP), 16, 0, 0);
     }
   } else {
     for (int idx = tid; idx < TILE_T * DW; idx += NTHREADS) {
       const int t = idx / DW, c = idx % DW;
       TX v = from_f32<TX>(0.f);
       if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
-      *reinterpret_cast<TX*>(xt + xt_off(t) + c * XE) = v;
+      *reinterpret_cast<TX*>(xt + XLay<XE>::off(t) + c * XE) = v;
     }
   }
 }
@@ -234,44 +264,97 @@ __device__ __forceinline__ void tile_store(TY* y, const char* xt, int64_t b, int
 #pragma unroll
     for (int i = 0; i < TILE_T / 8 / NWAVES; ++i) {
       const int g = wave * (TILE_T / 8 / NWAVES) + i;
-      const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XGRP + lane * 16);
+      const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XLay<YE>::GRP + lane * 16);
       *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g + (lane >> 3)) * rowb + (lane & 7) * 16) = v;
     }
   } else {
     for (int idx = tid; idx < TILE_T * DW; idx += NTHREADS) {
       const int t = idx / DW, c = idx % DW;
       if (t0 + t < L && d0 + c < D)
-        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + xt_off(t) + c * YE);
+        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + XLay<YE>::off(t) + c * YE);
     }
   }
 }
 
 // Activation operand of chunk n for channel ch from the time-major tile.
+// Activations of the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4)
+// as MFMA B operands, one LDS read of the 4 channels per tile row.
 template <typename TX> struct XGather;
 template <> struct XGather<bf16_t> {
   // lane (n, q): taps 8(q&1) .. +7 = rows 16n + 8(q&1) + r = group 2n + (q&1), row r
-  __device__ static __forceinline__ bf8 get(const char* xt, int ch, int n, int q) {
-    const char* p = xt + (2 * n + (q & 1)) * XGRP + ch * 2;
-    bf8 v;
+  __device__ static __forceinline__ void get4(const char* xt, int ch0, int n, int q, bf8 (&xv)[4]) {
+    const char* p = xt + (2 * n + (q & 1)) * XLay<2>::GRP + ch0 * 2;
+    uint2 w[8];
 #pragma unroll
-    for (int r = 0; r < 8; ++r) v[r] = *reinterpret_cast<const __bf16*>(p + r * XROW);
-    return v;
+    for (int r = 0; r < 8; ++r) w[r] = *reinterpret_cast<const uint2*>(p + r * XROW);
+    // channel c of row r is the (c & 1) half of word c >> 1 of w[r]
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      uint32_t o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint32_t lo = (c >> 1) ? w[2 * j].y : w[2 * j].x;
+        const uint32_t hi = (c >> 1) ? w[2 * j + 1].y : w[2 * j + 1].x;
+        o[j] = (c & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      xv[c] = __builtin_bit_cast(bf8, *reinterpret_cast<const uint4*>(o));
+    }
   }
 };
 template <> struct XGather<float> {
   // lane (n, q), slot kk: tap 4q + kk = row 16n + 4q + kk = group 2n + (q>>1), row 4(q&1) + kk
-  __device__ static __forceinline__ f4 get(const char* xt, int ch, int n, int q) {
-    const char* p = xt + (2 * n + (q >> 1)) * XGRP + 4 * (q & 1) * XROW + ch * 4;
-    f4 v;
+  __device__ static __forceinline__ void get4(const char* xt, int ch0, int n, int q, f4 (&xv)[4]) {
+    const char* p = xt + (2 * n + (q >> 1)) * XLay<4>::GRP + 4 * (q & 1) * XROW + ch0 * 4;
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) v[kk] = *reinterpret_cast<const float*>(p + kk * XROW);
-    return v;
+    for (int kk = 0; kk < 4; ++kk) {
+      const f4 w = *reinterpret_cast<const f4*>(p + kk * XROW);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) xv[c][kk] = w[c];
+    }
   }
 };
+
+// Outputs of the 4 consecutive channels ch0 .. ch0+3 of a group (MFMA D layout,
+// lane (n, q) holds rows 16n + 4q + r) into the time-major LDS tile.
+template <typename TY>
+__device__ __forceinline__ void put_y4(char* xt, int ch0, int n, int q, const f4 (&acc)[4]) {
+  // rows 16n + 4q + r: group 2n + (q >> 1), rows 4 (q & 1) + r
+  char* dst = xt + (2 * n + (q >> 1)) * XLay<sizeof(TY)>::GRP + 4 * (q & 1) * XROW + ch0 * (int)sizeof(TY);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (sizeof(TY) == 2) {
+      typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+      const bf4 v = {(__bf16)acc[0][r], (__bf16)acc[1][r], (__bf16)acc[2][r], (__bf16)acc[3][r]};
+      *reinterpret_cast<bf4*>(dst + r * XROW) = v;
+    } else {
+      const f4 v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+      *reinterpret_cast<f4*>(dst + r * XROW) = v;
+    }
+  }
+}
 
 __device__ __forceinline__ float swap_pair(float v) {  // value of the neighbouring lane (lane ^ 1)
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1,
                                                                0xF, 0xF, false));
+}
+
+// float32 outputs straight from the MFMA registers: rows t .. t+3 of the 4
+// channels d .. d+3, 16 bytes per row where all 4 channels exist.
+__device__ __forceinline__ void put_y4_global(float* y, const f4 (&acc)[4], int64_t b, int64_t t, int d,
+                                              int64_t L, int D) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if (t + r >= L) break;
+    float* dst = y + (b * L + t + r) * (int64_t)D + d;
+    if (d + 4 <= D && (D & 3) == 0) {
+      const f4 v = {acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+      *reinterpret_cast<f4*>(dst) = v;
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (d + c < D) dst[c] = acc[c][r];
+    }
+  }
 }
 
 template <typename TX, int MG>
@@ -283,7 +366,7 @@ struct FwdTile {
   static constexpr int NSTR = 16 * MG;       // floats per chunk row of the scan buffer
   static constexpr int CSTR = 16 * NSTR + 8; // floats per channel of the scan buffer
   static constexpr int WBUF = 4 * CSTR;      // floats per wave
-  static constexpr int NM = 1 + 2 * MG;
+  static constexpr int NM = fwd_mats(MG);
   static constexpr int PAIRS = NGRP * MG;    // (group, mode group) states per scan lane
 };
 
@@ -294,9 +377,9 @@ __device__ __forceinline__ void group_states(const char* xt, float* wb, int ch0,
                                              typename Path<TX>::XOp (&xv)[4], int ln, int lq) {
   typedef FwdTile<TX, MG> F;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  XGather<TX>::get4(xt, ch0, ln, lq, xv);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    xv[k] = XGather<TX>::get(xt, ch0 + k, ln, lq);
 #pragma unroll
     for (int g = 0; g < MG; ++g)
       *reinterpret_cast<f4*>(&wb[k * F::CSTR + ln * F::NSTR + g * 16 + lq * 4]) =
@@ -314,7 +397,7 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_agg_kernel(FwdA
   typedef FwdTile<TX, MG> F;
   typedef typename F::PT PT;
   constexpr int DW = F::DW, CPW = F::CPW, NGRP = F::NGRP, XE = (int)sizeof(TX);
-  __shared__ __align__(16) char xt[XT_BYTES];
+  __shared__ __align__(16) char xt[XLay<XE>::BYTES];
   __shared__ __align__(16) float sbuf[NWAVES * F::WBUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -380,7 +463,7 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_agg_kernel(FwdA
           hl = make_float2(hl.x + w.x, hl.y + w.y);
         }
         for (int i = 0; i <= jstar; ++i) {
-          const TX xv1 = *reinterpret_cast<const TX*>(xt + xt_off(nstar * CHUNK + i) + ch * XE);
+          const TX xv1 = *reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + i) + ch * XE);
           hl = cfma(ms.lam, hl, make_float2(to_f32(xv1), 0.f));
         }
         a.alast[((size_t)b * a.Dp + d0 + ch) * a.Mp + m] = hl;
@@ -509,7 +592,7 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
   constexpr int DW = F::DW, CPW = F::CPW, NGRP = F::NGRP;
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
-  __shared__ __align__(16) char xt[XT_BYTES];
+  __shared__ __align__(16) char xt[XLay<sizeof(TX)>::BYTES];
   __shared__ __align__(16) float sbuf[NWAVES * F::WBUF];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -531,9 +614,9 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
   auto tab_of = [&](int ch) {
     return tab + (size_t)(d0 + ch) * F::NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
   };
-  typedef StateOp<TX> SO;
+  typedef StateRow SO;
   typename PT::AOp vop[4][MG], top[4];
-  typename SO::UOp uop[4][MG];
+  f4 uop[4][MG];
   auto fetch_v = [&](int grp) {
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -546,7 +629,7 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
       const char* tp = tab_of(cw0 + 4 * grp + k);
       top[k] = PT::load_a(tp);
 #pragma unroll
-      for (int g = 0; g < MG; ++g) uop[k][g] = SO::load_u(tp + (2 + 2 * g) * TAB_MAT_BYTES);
+      for (int g = 0; g < MG; ++g) uop[k][g] = load_f4(tp + (2 + 2 * g) * TAB_MAT_BYTES);
     }
   };
   // entry state of this lane's half, per (group, mode group)
@@ -582,27 +665,19 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
       }
     }
     wave_lds_order();
+    f4 acc[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      const int ch = cw0 + 4 * grp + k;
-      f4 acc = PT::mma(top[k], xv[k], zero);
+      acc[k] = PT::mma(top[k], xv[k], zero);
 #pragma unroll
       for (int g = 0; g < MG; ++g)
-        acc = SO::apply(uop[k][g], &wb[k * F::CSTR + ln * F::NSTR + g * 16], lq, acc);
-      if (SEPY) {
-        const int d = d0 + ch;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int64_t t = t0 + ln * CHUNK + lq * 4 + r;
-          if (d < a.D && t < a.L) reinterpret_cast<float*>(a.y)[(b * a.L + t) * (int64_t)a.D + d] = acc[r];
-        }
-      } else {
-        // rows 16 ln + 4 lq + r: group 2 ln + (lq >> 1), rows 4 (lq & 1) + r
-        char* dst = xt + (2 * ln + (lq >> 1)) * XGRP + 4 * (lq & 1) * XROW + ch * (int)sizeof(TY);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) *reinterpret_cast<TY*>(dst + r * XROW) = from_f32<TY>(acc[r]);
-      }
+        acc[k] = SO::apply(uop[k][g], &wb[k * F::CSTR + ln * F::NSTR + g * 16], lq, acc[k]);
     }
+    if (SEPY)
+      put_y4_global(reinterpret_cast<float*>(a.y), acc, b, t0 + ln * CHUNK + lq * 4, d0 + cw0 + 4 * grp,
+                    a.L, a.D);
+    else
+      put_y4<TY>(xt, cw0 + 4 * grp, ln, lq, acc);
     if (grp + 1 < NGRP) fetch_tu(grp + 1);
     wave_lds_order();
   }
@@ -613,28 +688,31 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
 }
 
 // ---------------------------------------------------------------------------
-// Single-kernel forward over row segments (M <= 8).
+// Single-kernel forward over row segments (one mode group, M <= 8).
 //
-// A work-group owns seg_len consecutive tiles of one chain (batch row b,
-// channel block) and DW/4 waves, one group of 4 channels each; a wave keeps its
-// channels' T, V and U operands in registers for the whole segment.  Tiles
-// stream through two LDS tile buffers: the direct-to-LDS load of the next tile
-// is in flight while the current one is computed.
-//   pass 1  per tile S = V x and the half folds A_0, A_1; the segment's own end
-//           state agg_s = fold over its tiles of lambda^256 agg + (mu^8 A_0 + A_1)
-//   look-back  per wave (its channels form their own sub-chain): publish agg_s,
-//           find the state entering the segment from the nearest published
-//           inclusive state and the aggregates after it (the canonical
-//           recurrence inc(s) = lambda^(256 seg_len) inc(s-1) + agg_s, so the
-//           result does not depend on timing), publish inc(s)
-//   pass 2  the segment streams again: per tile the scan lanes run their chunks
-//           from the carried state (half 1 enters with mu^8 c + A_0) leaving
-//           the state entering each chunk in the scan buffer, y = T x + U H on
-//           MFMA over the drive column, the tile leaves as rows; the state
-//           after the tile is carried to the next tile in registers.
-// Work-groups take segments in ticket order (time-major over the chains), so
-// every wait is on a smaller ticket, which a running work-group took; every
-// wait is bounded.  Payloads and flags are agent-coherent (device-scope)
+// A work-group (8 waves) owns seg_len consecutive tiles of one chain (batch row
+// b, channel block); each wave owns CW channels of the tile and keeps their
+// operands in registers for the whole segment.  Per channel the state MFMA
+// S = V x leaves, in lane (n, q), the drives of chunk n for the modes 2q and
+// 2q+1; everything on the chunk axis then runs across the 16 lanes of a row.
+//   pass 1  per tile, lane-wise acc = lambda^256 acc + mu^(15-n) S; the row sum
+//           of acc is the segment's own end state from a zero start (agg_s);
+//   carry   per wave (its channels form their own sub-chain): publish agg_s,
+//           wait for the aggregates of all earlier segments of the row and
+//           fold them, with the row's initial state, into the state entering
+//           the segment (a fixed-order weighted sum, lanes in parallel);
+//   pass 2  the segment streams again: per tile and channel, the entering state
+//           c is added to lane 0 as mu c, the chunk recurrence
+//           Q[n] = mu Q[n-1] + S[n] is a four-step prefix scan over the row
+//           (shifts 1, 2, 4, 8 with multipliers mu, mu^2, mu^4, mu^8), the
+//           state entering chunk n is Q[n-1] (c for n = 0) and feeds
+//           y = T x + U H directly as the float32 MFMA operand; Q[15] is the
+//           next tile's entering state.
+// Tiles stream through three LDS tile buffers; wave 0 alone issues the
+// direct-to-LDS loads (two tiles in flight), the other waves store the output
+// rows.  Work-groups take segments in ticket order (time-major over the chains),
+// so every wait is on a smaller ticket, which a running work-group took and
+// publishes without waiting; every wait is bounded.  Payloads and flags are agent-coherent (device-scope)
 // accesses; a publisher completes its payload stores before the flag store.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void st_agent(float2* p, float2 v) {
@@ -644,6 +722,16 @@ __device__ __forceinline__ void st_agent(float2* p, float2 v) {
 __device__ __forceinline__ float2 ld_agent(const float2* p) {
   return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const uint64_t*>(p),
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
+}
+// the two modes of a lane as (re, im, re, im)
+__device__ __forceinline__ void st_agent4(float2* p, f4 v) {
+  st_agent(p, make_float2(v[0], v[1]));
+  st_agent(p + 1, make_float2(v[2], v[3]));
+}
+__device__ __forceinline__ f4 ld_agent4(const float2* p) {
+  const float2 u = ld_agent(p), w = ld_agent(p + 1);
+  const f4 r = {u.x, u.y, w.x, w.y};
+  return r;
 }
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
   return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -656,16 +744,65 @@ __device__ __forceinline__ void st_flag(uint32_t* f, uint32_t v) {
 // the row's initial state and records the event in the error word.
 constexpr uint32_t SPIN_LIMIT = 1u << 20;
 
+// Complex arithmetic on the two modes of a lane, (re_a, im_a, re_b, im_b).
+__device__ __forceinline__ f4 c2mul(const f4& a, const f4& b) {
+  f4 r;
+  r[0] = fmaf(a[0], b[0], -a[1] * b[1]);
+  r[1] = fmaf(a[0], b[1], a[1] * b[0]);
+  r[2] = fmaf(a[2], b[2], -a[3] * b[3]);
+  r[3] = fmaf(a[2], b[3], a[3] * b[2]);
+  return r;
+}
+__device__ __forceinline__ f4 c2fma(const f4& a, const f4& b, const f4& c) {  // a b + c
+  f4 r;
+  r[0] = fmaf(a[0], b[0], fmaf(-a[1], b[1], c[0]));
+  r[1] = fmaf(a[0], b[1], fmaf(a[1], b[0], c[1]));
+  r[2] = fmaf(a[2], b[2], fmaf(-a[3], b[3], c[2]));
+  r[3] = fmaf(a[2], b[3], fmaf(a[3], b[2], c[3]));
+  return r;
+}
+__device__ __forceinline__ f4 mode_pair(float2 u, float2 w) {
+  const f4 r = {u.x, u.y, w.x, w.y};
+  return r;
+}
+
+// Lane moves inside rows of 16 lanes (DPP).  BOUND0: lanes without a source
+// lane read zero; otherwise they keep `old`.
+constexpr int DPP_ROW_SHL(int n) { return 0x100 + n; }   // lane i <- lane i + n
+constexpr int DPP_ROW_SHR(int n) { return 0x110 + n; }   // lane i <- lane i - n
+constexpr int DPP_QUAD(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
+constexpr int DPP_ROW_MIRROR = 0x140;                    // lane i <- lane 15 - i
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;               // lane i <- lane 7 - i (per half row)
+template <int CTRL, bool BOUND0>
+__device__ __forceinline__ f4 dpp4(const f4& old, const f4& v) {
+  f4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float o = old[i], x = v[i];  // scalars: a vector element is no lvalue for bit_cast
+    r[i] = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, o),
+                                                                 __builtin_bit_cast(int, x), CTRL,
+                                                                 0xF, 0xF, BOUND0));
+  }
+  return r;
+}
+// Sum over the 16 lanes of each row, in every lane of the row (the same order in
+// every lane, so the copies agree bitwise).
+__device__ __forceinline__ f4 row_sum(f4 v) {
+  v += dpp4<DPP_QUAD(1, 0, 3, 2), false>(v, v);
+  v += dpp4<DPP_QUAD(2, 3, 0, 1), false>(v, v);
+  v += dpp4<DPP_ROW_HALF_MIRROR, false>(v, v);
+  v += dpp4<DPP_ROW_MIRROR, false>(v, v);
+  return v;
+}
+
 template <typename TX>
 struct SegGeo {
   static constexpr int DW = tile_channels<TX>();
-  static constexpr int NW = SEG_WAVES;              // waves
-  static constexpr int NG = DW / (4 * NW);          // scan groups of 4 channels per wave
-  static constexpr int NT = 64 * NW;                // threads
-  static constexpr int NSTR = 16;                   // floats per chunk row (one mode group)
-  static constexpr int CSTR = 16 * NSTR + 8;        // floats per channel of the scan buffer
-  static constexpr int WBUF = 4 * CSTR;             // floats per wave (one group at a time)
-  static constexpr int NBUF = 3;                    // LDS tile buffers (two loads in flight)
+  static constexpr int NW = SEG_WAVES;  // waves
+  static constexpr int CW = DW / NW;    // channels per wave (bf16 8, float 4)
+  static constexpr int NG = CW / 4;     // operand gathers of 4 channels per wave
+  static constexpr int NT = 64 * NW;    // threads
+  static constexpr int NBUF = 3;        // LDS tile buffers (two loads in flight)
 };
 
 // s_waitcnt until at most n vector-memory operations of this wave are
@@ -694,14 +831,14 @@ __device__ __forceinline__ void seg_tile_load(char* xt, const TX* x, int64_t b, 
 #pragma unroll
       for (int g = 0; g < TILE_T / 8; ++g)
         __builtin_amdgcn_global_load_lds((gvoid_t*)(src + (int64_t)(8 * g) * rowb + loff),
-                                         (lvoid_t*)(xt + g * XGRP), 16, 0, 0);
+                                         (lvoid_t*)(xt + g * XLay<XE>::GRP), 16, 0, 0);
     }
   } else {
     for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
       const int t = idx / DW, c = idx % DW;
       TX v = from_f32<TX>(0.f);
       if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
-      *reinterpret_cast<TX*>(xt + xt_off(t) + c * XE) = v;
+      *reinterpret_cast<TX*>(xt + XLay<XE>::off(t) + c * XE) = v;
     }
   }
 }
@@ -721,7 +858,7 @@ __device__ __forceinline__ void seg_tile_store(TY* y, const char* xt, int64_t b,
       const int64_t rowb = (int64_t)D * YE;
       const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
       for (int g = wave - 1; g < TILE_T / 8; g += G::NW - 1) {
-        const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XGRP + lane * 16);
+        const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XLay<YE>::GRP + lane * 16);
         *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g) * rowb + loff) = v;
       }
     }
@@ -729,7 +866,7 @@ __device__ __forceinline__ void seg_tile_store(TY* y, const char* xt, int64_t b,
     for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
       const int t = idx / DW, c = idx % DW;
       if (t0 + t < L && d0 + c < D)
-        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + xt_off(t) + c * YE);
+        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + XLay<YE>::off(t) + c * YE);
     }
   }
 }
@@ -738,21 +875,21 @@ template <typename TX, typename TY>
 __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   typedef SegGeo<TX> G;
   typedef Path<TX> PT;
-  typedef StateOp<TX> SO;
-  constexpr int DW = G::DW, NW = G::NW, NG = G::NG, XE = (int)sizeof(TX);
-  constexpr int NM = 3;  // T, V, U
+  constexpr int DW = G::DW, NW = G::NW, CW = G::CW, NG = G::NG, XE = (int)sizeof(TX);
+  constexpr int NM = fwd_mats(1);  // T, V, U
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
-  __shared__ __align__(16) char xb[G::NBUF][XT_BYTES];
-  __shared__ __align__(16) float sbuf[NW * G::WBUF];
+  __shared__ __align__(16) char xb[G::NBUF][XLay<XE>::BYTES];
+  // per (channel, power s, row q): mu^(2^s) of the modes 2q, 2q+1
+  __shared__ __align__(16) f4 s_pw[DW * 4 * 4];
+  // per (channel, row q): the state entering the next tile; then a zero entry
+  __shared__ __align__(16) f4 s_c[DW * 4 + 1];
   __shared__ uint32_t s_tk;
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);      // wave-uniform (scalar)
-  const int ln = lane & 15, lq = lane >> 4;                       // MFMA layout
-  const int sh = lane & 1, sm = (lane >> 1) & 7, sc = lane >> 4;  // scan layout
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
+  const int ln = lane & 15, lq = lane >> 4;                   // chunk, mode pair (2 lq, 2 lq + 1)
   const int nchains = (int)(a.B * a.NB);
-  float* wb = sbuf + wave * G::WBUF;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
 
   if (tid == 0) s_tk = atomicAdd(a.ticket, 1u);
@@ -762,33 +899,17 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   const int chain = (int)(tk % nchains);
   const int64_t b = chain / a.NB;
   const int d0 = (chain % a.NB) * DW;
-  const int64_t pb = seg * a.seg_len;                               // first tile
+  const int64_t pb = seg * a.seg_len;                                 // first tile
   const int nt = (int)(a.P - pb < a.seg_len ? a.P - pb : a.seg_len);  // tiles of the segment
   const bool last_seg = (seg == a.seg_per_chain - 1);
-  const int ch0 = wave * 4 * NG;  // this wave's first channel within the tile
+  const int c0 = wave * CW;  // this wave's first channel within the tile
 
-  // resident operands T, V, U of the wave's channels
   const char* tab = reinterpret_cast<const char*>(a.tab);
   auto tab_of = [&](int k) {
-    return tab + (size_t)(d0 + ch0 + k) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+    return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
   };
-  typename PT::AOp top[4 * NG], vop[4 * NG];
-  typename SO::UOp uop[4 * NG];
-#pragma unroll
-  for (int k = 0; k < 4 * NG; ++k) {
-    top[k] = PT::load_a(tab_of(k));
-    vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);
-    uop[k] = SO::load_u(tab_of(k) + 2 * TAB_MAT_BYTES);
-  }
-  // scan-lane scalars: group gr, channel ch0 + 4 gr + sc, mode sm
-  float2 mu[NG], mu8[NG], lamT[NG];
-#pragma unroll
-  for (int gr = 0; gr < NG; ++gr) {
-    const ModeScalars& ms = a.scal[(size_t)(d0 + ch0 + 4 * gr + sc) * a.Mp + sm];
-    mu[gr] = ms.mu;
-    mu8[gr] = ms.mu8;
-    lamT[gr] = ms.lamT;
-  }
+  // scalars of the lane's two modes of channel c0 + k
+  auto scal_of = [&](int k) { return a.scal + (size_t)(d0 + c0 + k) * a.Mp + 2 * lq; };
 
   auto tile_full = [&](int64_t p) {
     return a.fast_io && (p + 1) * TILE_T <= a.L && d0 + DW <= a.D;
@@ -810,150 +931,128 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
         __builtin_amdgcn_s_waitcnt(0);
     }
   };
-  // S = V x for the 4 channels of group gr into the wave's scan buffer; keeps the operands
-  auto states = [&](const char* xt, int gr, typename PT::XOp (&xv)[4]) {
+
+  typename PT::AOp vop[CW];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      xv[k] = XGather<TX>::get(xt, ch0 + 4 * gr + k, ln, lq);
-      *reinterpret_cast<f4*>(&wb[k * G::CSTR + ln * G::NSTR + lq * 4]) =
-          PT::mma(vop[4 * gr + k], xv[k], zero);
-    }
-  };
-  // row of chunk n of scan channel c (of the group in the buffer)
-  auto row = [&](int c, int n) -> float* { return &wb[c * G::CSTR + n * G::NSTR]; };
+  for (int k = 0; k < CW; ++k) vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);
+  // scan multipliers mu, mu^2, mu^4, mu^8 = lambda^(16 j), j = 1, 2, 4, 8
+  for (int e = tid; e < DW * 4 * MODES_PER_GROUP; e += G::NT) {
+    const int ch = e / (4 * MODES_PER_GROUP), sp = (e / MODES_PER_GROUP) % 4, m = e % MODES_PER_GROUP;
+    reinterpret_cast<float2*>(s_pw)[e] = a.mpow[((size_t)(d0 + ch) * CHUNK + (1 << sp)) * a.Mp + m];
+  }
+  if (tid < 4) s_c[DW * 4][tid] = 0.f;
 
   // ---- pass 1: the segment's own end state ---------------------------------
-  float2 sagg[NG];
+  f4 sagg[CW];
+  {
+    f4 w[CW], lt[CW];
 #pragma unroll
-  for (int gr = 0; gr < NG; ++gr) sagg[gr] = make_float2(0.f, 0.f);
-  load(0);
-  if (nt > 1) load(1);
-  for (int i = 0; i < nt; ++i) {
-    wait_tile(i);
-    __syncthreads();  // tile i is in; every wave is done with tile i-1's buffer
-    if (i + 2 < nt) load(i + 2);
-    const char* xt = xb[i % G::NBUF];
-#pragma unroll
-    for (int gr = 0; gr < NG; ++gr) {
-      typename PT::XOp xv[4];
-      states(xt, gr, xv);
-      wave_lds_order();
-      float2 run = make_float2(0.f, 0.f);
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        run = cfma(mu[gr], run, *reinterpret_cast<const float2*>(row(sc, 8 * sh + j) + 2 * sm));
-      const float2 oth = make_float2(swap_pair(run.x), swap_pair(run.y));
-      const float2 A0 = sh ? oth : run, A1 = sh ? run : oth;
-      sagg[gr] = cfma(lamT[gr], sagg[gr], cfma(mu8[gr], A0, A1));
-      wave_lds_order();
+    for (int k = 0; k < CW; ++k) {
+      // mu^(15-n) of the lane's modes (rows [d][j][Mp] of lambda^(16 j))
+      w[k] = load_f4(a.mpow + ((size_t)(d0 + c0 + k) * CHUNK + (CHUNK - 1 - ln)) * a.Mp + 2 * lq);
+      const ModeScalars* ms = scal_of(k);
+      lt[k] = mode_pair(ms[0].lamT, ms[1].lamT);
+      sagg[k] = zero;
     }
-  }
-
-  // ---- look-back over segments (per wave sub-chain) --------------------------
-  const int64_t sub = tk * NW + wave;
-  const int64_t stride = (int64_t)nchains * NW;  // sub-chain step between segments of a row
-  auto pay = [&](int64_t s, int gr) { return ((size_t)s * NG + gr) * 32 + sc * 8 + sm; };
-  float2 carry[NG];
+    load(0);
+    if (nt > 1) load(1);
+    for (int i = 0; i < nt; ++i) {
+      wait_tile(i);
+      __syncthreads();  // tile i is in; every wave is done with tile i-1's buffer
+      if (i + 2 < nt) load(i + 2);
+      const char* xt = xb[i % G::NBUF];
 #pragma unroll
-  for (int gr = 0; gr < NG; ++gr) {
-    const int d = d0 + ch0 + 4 * gr + sc;
-    carry[gr] = make_float2(0.f, 0.f);
-    if (a.h0 != nullptr && d < a.D && sm < a.M) {
-      const float* h = a.h0 + ((size_t)(b * a.D + d) * a.M + sm) * 2;
-      carry[gr] = make_float2(h[0], h[1]);
-    }
-  }
-  if (seg > 0) {
-    // publish this segment's aggregate (successors may fold it before this
-    // segment's own inclusive state is released)
-    if (!last_seg) {
-      if (sh == 0)
+      for (int gr = 0; gr < NG; ++gr) {
+        typename PT::XOp xv[4];
+        XGather<TX>::get4(xt, c0 + 4 * gr, ln, lq, xv);
 #pragma unroll
-        for (int gr = 0; gr < NG; ++gr) st_agent(a.pay_agg + pay(sub, gr), sagg[gr]);
-      __builtin_amdgcn_s_waitcnt(0);
-      if (lane == 0) st_flag(a.flags + sub, FLAG_AGG);
-    }
-    const uint32_t fpred = ld_flag(a.flags + sub - stride);
-    int64_t jres;  // nearest segment of the row with its inclusive state out (-1: row start)
-    if (fpred == FLAG_INCL) {
-      jres = seg - 1;
-    } else {
-      int64_t top_j = seg - 1;
-      jres = -2;
-      uint32_t it = 0;
-      while (jres == -2) {
-        const int64_t j = top_j - lane;
-        const uint32_t fl = (j >= 0) ? ld_flag(a.flags + (j * nchains + chain) * NW + wave) : FLAG_INCL;
-        const uint64_t incl = __ballot(fl == FLAG_INCL);
-        const uint64_t none = __ballot(fl == FLAG_NONE);
-        if (incl != 0) {
-          const int l = __ffsll((unsigned long long)incl) - 1;
-          const uint64_t nearer = (l == 0) ? 0ull : (~0ull >> (64 - l));
-          if ((none & nearer) == 0) jres = top_j - l;
-        } else if (none == 0) {
-          top_j -= 64;  // the whole window holds aggregates: keep looking further back
-          continue;
-        }
-        if (jres == -2) {
-          if (++it >= SPIN_LIMIT) {
-            if (lane == 0) atomicOr(a.error, 1u);
-            jres = -1;
-          } else {
-            __builtin_amdgcn_s_sleep(1);
-          }
+        for (int kk = 0; kk < 4; ++kk) {
+          const int k = 4 * gr + kk;
+          sagg[k] = c2fma(lt[k], sagg[k], c2mul(w[k], PT::mma(vop[k], xv[kk], zero)));
         }
       }
     }
-    if (jres >= 0) {
-      const int64_t js = (jres * nchains + chain) * NW + wave;
+  }
 #pragma unroll
-      for (int gr = 0; gr < NG; ++gr) carry[gr] = ld_agent(a.pay_inc + pay(js, gr));
-    }
-    float2 lamS[NG];
+  for (int k = 0; k < CW; ++k) sagg[k] = row_sum(sagg[k]);
+
+  // ---- the state entering the segment (per wave sub-chain) ----------------------
+  // c = lamS^seg h0 + sum_{j<seg} lamS^(seg-1-j) agg_j with lamS = lambda^(256
+  // seg_len): term u = seg-1-j (u = seg: h0) goes to lane u % 16 of every row,
+  // weighted by lamS^(u % 16) and summed over the row; blocks of 16 terms are
+  // combined farthest first by Horner's rule with lamS^16.  The order is fixed
+  // by seg alone, so the result is bitwise reproducible.
+  const int64_t sub = tk * NW + wave;
+  // payload of sub-chain s, channel k: 8 modes as float2; the lane's pair at 2 lq
+  auto pay = [&](int64_t s, int k) { return ((size_t)s * CW + k) * MODES_PER_GROUP + 2 * lq; };
+  if (!last_seg) {  // publish this segment's own end state
+    if (ln == 0)
 #pragma unroll
-    for (int gr = 0; gr < NG; ++gr) lamS[gr] = a.scal[(size_t)(d0 + ch0 + 4 * gr + sc) * a.Mp + sm].lamS;
-    constexpr int LB = 16 / NG;
-    for (int64_t i = jres + 1; i < seg; i += LB) {
-      const int n = (seg - i) < LB ? (int)(seg - i) : LB;
-      float2 v[LB][NG];
-#pragma unroll
-      for (int u = 0; u < LB; ++u)
-#pragma unroll
-        for (int gr = 0; gr < NG; ++gr)
-          v[u][gr] = (u < n) ? ld_agent(a.pay_agg + pay(((i + u) * nchains + chain) * NW + wave, gr))
-                             : make_float2(0.f, 0.f);
-#pragma unroll
-      for (int u = 0; u < LB; ++u)
-        if (u < n)
-#pragma unroll
-          for (int gr = 0; gr < NG; ++gr) carry[gr] = cfma(lamS[gr], carry[gr], v[u][gr]);
+      for (int k = 0; k < CW; ++k) st_agent4(a.pay_agg + pay(sub, k), sagg[k]);
+    __builtin_amdgcn_s_waitcnt(0);
+    if (lane == 0) st_flag(a.flags + sub, FLAG_AGG);
+  }
+  // wait until every earlier segment of the row has published
+  for (int64_t top = seg - 1; top >= 0; top -= 64) {
+    const int64_t j = top - lane;
+    for (uint32_t it = 0;; ++it) {
+      const bool ok = j < 0 || ld_flag(a.flags + (j * nchains + chain) * NW + wave) != FLAG_NONE;
+      if (__ballot(!ok) == 0) break;
+      if (it >= SPIN_LIMIT) {
+        if (lane == 0) atomicOr(a.error, 1u);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
     }
   }
-  // the inclusive state is stored now; the first segment of a row releases it
-  // at once, the others once pass 2 is under way (later segments fold the
-  // aggregates back to the row's first segment meanwhile)
-  if (!last_seg && sh == 0)
+  f4 carry[CW];
+  {
+    // lamS^n of the lane's modes (rows [d][n][Mp], n = 0..16)
+    auto spw = [&](int k, int n) {
+      return load_f4(a.spow + ((size_t)(d0 + c0 + k) * (CHUNK + 1) + n) * a.Mp + 2 * lq);
+    };
+    f4 wn[CW], w16[CW];
 #pragma unroll
-    for (int gr = 0; gr < NG; ++gr) {
-      const float2 ls = a.scal[(size_t)(d0 + ch0 + 4 * gr + sc) * a.Mp + sm].lamS;
-      st_agent(a.pay_inc + pay(sub, gr), cfma(ls, carry[gr], sagg[gr]));
+    for (int k = 0; k < CW; ++k) {
+      wn[k] = spw(k, ln);
+      w16[k] = spw(k, CHUNK);
+      carry[k] = zero;
     }
-  if (!last_seg && seg == 0) {
-    __builtin_amdgcn_s_waitcnt(0);
-    if (lane == 0) st_flag(a.flags + sub, FLAG_INCL);
+    for (int64_t blk = seg / CHUNK; blk >= 0; --blk) {
+      const int64_t u = blk * CHUNK + ln;
+      f4 v[CW];
+#pragma unroll
+      for (int k = 0; k < CW; ++k) {
+        v[k] = zero;
+        if (u < seg) {
+          v[k] = ld_agent4(a.pay_agg + pay(((seg - 1 - u) * nchains + chain) * NW + wave, k));
+        } else if (u == seg && a.h0 != nullptr && d0 + c0 + k < a.D) {
+          const float* h = a.h0 + ((size_t)(b * a.D + d0 + c0 + k) * a.M + 2 * lq) * 2;
+          if (2 * lq < a.M) v[k][0] = h[0], v[k][1] = h[1];
+          if (2 * lq + 1 < a.M) v[k][2] = h[2], v[k][3] = h[3];
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < CW; ++k) carry[k] = c2fma(w16[k], carry[k], row_sum(c2mul(wn[k], v[k])));
+    }
   }
 
-  // ---- pass 2: carried states and outputs --------------------------------------
+  // ---- pass 2: the chunk scans and the outputs ----------------------------------
   const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
   __syncthreads();  // every wave is done with pass 1's buffers
   load(0);
   if (nt > 1) load(1);
+  typename PT::AOp top[CW];
+  f4 uop[CW];
+#pragma unroll
+  for (int k = 0; k < CW; ++k) {
+    top[k] = PT::load_a(tab_of(k));
+    uop[k] = load_f4(tab_of(k) + 2 * TAB_MAT_BYTES);
+    if (ln == 0) s_c[(c0 + k) * 4 + lq] = carry[k];
+  }
+  wave_lds_order();
   for (int i = 0; i < nt; ++i) {
     wait_tile(i);
-    if (i == 0 && !last_seg && seg > 0) {  // release the inclusive state
-      __builtin_amdgcn_s_waitcnt(0);
-      if (lane == 0) st_flag(a.flags + sub, FLAG_INCL);
-    }
     __syncthreads();  // tile i is in; every wave is done with tile i-1's buffer
     if (i + 2 < nt) load(i + 2);
     char* xt = xb[i % G::NBUF];
@@ -961,62 +1060,48 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
 #pragma unroll
     for (int gr = 0; gr < NG; ++gr) {
       typename PT::XOp xv[4];
-      states(xt, gr, xv);
-      wave_lds_order();
-      // half 1 enters with mu^8 c + A_0; both halves then run their chunks
-      float2 A0 = make_float2(0.f, 0.f);
-      if (sh) {
+      XGather<TX>::get4(xt, c0 + 4 * gr, ln, lq, xv);
+      f4 acc[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) A0 = cfma(mu[gr], A0, *reinterpret_cast<const float2*>(row(sc, j) + 2 * sm));
-      }
-      float2 run = sh ? cfma(mu8[gr], carry[gr], A0) : carry[gr];
-      float2 hl = run;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int n = 8 * sh + j;
-        const float2 sv = *reinterpret_cast<const float2*>(row(sc, n) + 2 * sm);
-        SO::put(row(sc, n), sm, run);  // state entering chunk n
-        if (n == nstar) hl = run;
-        run = cfma(mu[gr], run, sv);
-      }
-      // the state after the tile (from half 1) carries to the next tile
-      const float2 oth = make_float2(swap_pair(run.x), swap_pair(run.y));
-      carry[gr] = sh ? run : oth;
-      if (p == a.P - 1 && a.h_out != nullptr && sh == (nstar >> 3)) {
-        // terminal state at t = L-1 from the state entering chunk nstar
-        const int chs = ch0 + 4 * gr + sc, d = d0 + chs;
-        const float2 lam = a.scal[(size_t)d * a.Mp + sm].lam;
-        for (int j = 0; j <= jstar; ++j) {
-          const TX xv1 = *reinterpret_cast<const TX*>(xt + xt_off(nstar * CHUNK + j) + chs * XE);
-          hl = cfma(lam, hl, make_float2(to_f32(xv1), 0.f));
-        }
-        if (d < a.D && sm < a.M) {
-          float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + sm) * 2;
-          ho[0] = hl.x;
-          ho[1] = hl.y;
-        }
-      }
-      wave_lds_order();
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int ch = ch0 + 4 * gr + k;
-        f4 acc = PT::mma(top[4 * gr + k], xv[k], zero);
-        acc = SO::apply(uop[4 * gr + k], &wb[k * G::CSTR + ln * G::NSTR], lq, acc);
-        if (SEPY) {
-          const int d = d0 + ch;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int64_t t = p * TILE_T + ln * CHUNK + lq * 4 + r;
-            if (d < a.D && t < a.L) reinterpret_cast<float*>(a.y)[(b * a.L + t) * (int64_t)a.D + d] = acc[r];
+      for (int kk = 0; kk < 4; ++kk) {
+        const int k = 4 * gr + kk;
+        const f4* pw = s_pw + (c0 + k) * 16 + lq;  // mu^(2^s) at pw[4 s]
+        // the entering state c in lane 0 of each row, zero in the others
+        const f4 c = s_c[ln == 0 ? (c0 + k) * 4 + lq : DW * 4];
+        // Q[n] = sum_{j <= n} mu^(n-j) S[j] + mu^(n+1) c, four shift steps
+        f4 q = c2fma(pw[0], c, PT::mma(vop[k], xv[kk], zero));
+        q = c2fma(pw[0], dpp4<DPP_ROW_SHR(1), true>(zero, q), q);
+        q = c2fma(pw[4], dpp4<DPP_ROW_SHR(2), true>(zero, q), q);
+        q = c2fma(pw[8], dpp4<DPP_ROW_SHR(4), true>(zero, q), q);
+        q = c2fma(pw[12], dpp4<DPP_ROW_SHR(8), true>(zero, q), q);
+        const f4 h = dpp4<DPP_ROW_SHR(1), false>(c, q);  // state entering chunk n (c for n = 0)
+        if (ln == CHUNK - 1) s_c[(c0 + k) * 4 + lq] = q;   // state after the tile
+        acc[kk] = mma_f32(uop[k], h, PT::mma(top[k], xv[kk], zero));
+        if (p == a.P - 1 && a.h_out != nullptr && ln == nstar) {
+          // terminal state at t = L-1 from the state entering chunk nstar
+          const int d = d0 + c0 + k;
+          const ModeScalars* ms = scal_of(k);
+          const f4 lam = mode_pair(ms[0].lam, ms[1].lam);
+          f4 hl = h;
+          for (int j = 0; j <= jstar; ++j) {
+            const float xr = to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + j) +
+                                                                 (c0 + k) * XE));
+            const f4 xin = {xr, 0.f, xr, 0.f};
+            hl = c2fma(lam, hl, xin);
           }
-        } else {
-          // rows 16 ln + 4 lq + r: group 2 ln + (lq >> 1), rows 4 (lq & 1) + r
-          char* dst = xt + (2 * ln + (lq >> 1)) * XGRP + 4 * (lq & 1) * XROW + ch * (int)sizeof(TY);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) *reinterpret_cast<TY*>(dst + r * XROW) = from_f32<TY>(acc[r]);
+          if (d < a.D) {
+            float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + 2 * lq) * 2;
+            if (2 * lq < a.M) ho[0] = hl[0], ho[1] = hl[1];
+            if (2 * lq + 1 < a.M) ho[2] = hl[2], ho[3] = hl[3];
+          }
+          wave_lds_order();  // the drive reads above precede the output writes below
         }
       }
-      wave_lds_order();
+      if (SEPY)
+        put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4,
+                      d0 + c0 + 4 * gr, a.L, a.D);
+      else
+        put_y4<TY>(xt, c0 + 4 * gr, ln, lq, acc);
     }
     if (!SEPY) {
       __syncthreads();  // the whole output tile is in the buffer
@@ -1037,23 +1122,23 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t n) {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st, uint32_t* flags, int64_t nflags) {
+                       hipStream_t st, float2* mpow, float2* spow, uint32_t* flags, int64_t nflags) {
   if (bwd)
     hipLaunchKernelGGL((prep_kernel<TA, true>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, flags,
-                       nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
+                       spow, flags, nflags);
   else
     hipLaunchKernelGGL((prep_kernel<TA, false>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, flags,
-                       nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
+                       spow, flags, nflags);
   return hipGetLastError();
 }
 template hipError_t launch_prep<float>(const Geometry&, const float*, const float*, const float*,
                                        const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                       hipStream_t, uint32_t*, int64_t);
+                                       hipStream_t, float2*, float2*, uint32_t*, int64_t);
 template hipError_t launch_prep<bf16_t>(const Geometry&, const float*, const float*, const float*,
                                         const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                       hipStream_t, uint32_t*, int64_t);
+                                        hipStream_t, float2*, float2*, uint32_t*, int64_t);
 
 template <typename TX>
 hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,

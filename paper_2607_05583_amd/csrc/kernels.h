@@ -24,6 +24,8 @@ struct FwdArgs {
   const void* tab;
   const ModeScalars* scal;
   const ModeCarry* cc;
+  const float2* mpow;  // [Dp][16][Mp]: lambda^(16 j), j = 0..15 (single-kernel forward)
+  const float2* spow;  // [Dp][17][Mp]: lambda^(256 seg_len n), n = 0..16
   const float* h0;   // [B][D][M][2] or null
   float* h_out;      // [B][D][M][2] or null: state at t = L-1
   void* agg;         // per tile [DW * Mp] float4: half-tile end states (A_0, A_1)
@@ -32,10 +34,9 @@ struct FwdArgs {
   // single-kernel forward: segments of seg_len tiles, ticket order time-major over chains
   int seg_len, seg_per_chain;
   uint32_t* ticket;  // segment ticket counter
-  uint32_t* flags;   // per (segment, wave): FLAG_NONE / FLAG_AGG / FLAG_INCL
+  uint32_t* flags;   // per (segment, wave): FLAG_NONE / FLAG_AGG
   uint32_t* error;   // set when a bounded wait gives up
-  float2* pay_agg;   // per (segment, wave) [32 Mp / 8]: the segment's own end state
-  float2* pay_inc;   // per (segment, wave): end state including all earlier segments
+  float2* pay_agg;   // per (segment, wave) [channels][8 modes]: the segment's own end state
 };
 
 struct BwdArgs {
@@ -57,7 +58,8 @@ struct BwdArgs {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st, uint32_t* flags = nullptr, int64_t nflags = 0);
+                       hipStream_t st, float2* mpow = nullptr, float2* spow = nullptr,
+                       uint32_t* flags = nullptr, int64_t nflags = 0);
 
 template <typename TX>
 hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st,

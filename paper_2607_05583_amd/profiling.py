@@ -26,7 +26,7 @@ import os
 import sqlite3
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-FUSED = "fwd_fused_kernel"
+FUSED = "fwd_seg_kernel"
 COPY = "copyBuffer"
 
 
