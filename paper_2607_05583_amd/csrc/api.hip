@@ -43,7 +43,11 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 // Geometry of the tiled kernels for activations of type act (tile width depends
 // on the element size: 128-byte rows).
 // words ahead of the segment flags: [0] segment ticket, [1] error word
-constexpr size_t FLAG_HEADER = 64;
+// payload words of the single-kernel forward: per segment and channel, 8 modes (re, im)
+inline size_t seg_payload_words(const Geometry& g) {
+  const int64_t segs = g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len);
+  return (size_t)segs * g.Dp / g.NB * MODES_PER_GROUP * 2;
+}
 // segments of the single-kernel forward: the work-groups of one wave over the
 // 256 compute units of an MI355X
 constexpr int64_t SEG_TARGET = 256;
@@ -90,9 +94,9 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
     }
     w.alast = off;  // [B][Dp][Mp] state at t = L-1 from a zero start at the last tile
     off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float2));
-    if (op == RES_OP_FWD) {  // segment flags: ticket, error word, one per (segment, wave)
+    if (op == RES_OP_FWD) {  // single-kernel forward: header words, then per (segment, wave) payloads
       w.flags = off;
-      off += align256((FLAG_HEADER + (size_t)g.B * g.P * g.NB * SEG_WAVES) * sizeof(uint32_t));
+      off += align256((SEG_HEADER_WORDS + seg_payload_words(g)) * sizeof(uint32_t));
       w.mpow = off;  // [Dp][16][Mp] lambda^(16 j)
       off += align256((size_t)g.Dp * CHUNK * g.Mp * sizeof(float2));
       w.spow = off;  // [Dp][17][Mp] lambda^(256 seg_len n)
@@ -198,8 +202,7 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   uint32_t* fl = (uint32_t*)(base + w.flags);
   float2* mpow = (float2*)(base + w.mpow);
   float2* spow = (float2*)(base + w.spow);
-  const int64_t nflags =
-      segs ? (int64_t)(FLAG_HEADER + g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len) * SEG_WAVES) : 0;
+  const int64_t nflags = segs ? (int64_t)(SEG_HEADER_WORDS + seg_payload_words(g)) : 0;
   hipError_t e =
       x_dt == RES_BF16
           ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
@@ -236,8 +239,7 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
     a.seg_per_chain = (int)((g.P + g.seg_len - 1) / g.seg_len);
     a.ticket = fl;
     a.error = fl + 1;
-    a.flags = fl + FLAG_HEADER;
-    a.pay_agg = (float2*)(base + w.agg);
+    a.pay_agg = (float2*)(fl + SEG_HEADER_WORDS);
     if (x_dt == RES_F32)
       e = launch_fwd_segments<float, float>(g, a, st, ev0, ev1);
     else if (y_dt == RES_BF16)

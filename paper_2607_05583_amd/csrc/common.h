@@ -172,6 +172,7 @@ struct ModeScalars {
   float2 mu;      // lambda^CHUNK
   float2 mu8;     // lambda^(TILE_T / 2): the hop over half a tile (8 chunks)
   float2 lamT;    // lambda^TILE_T
+  float2 lamTail; // lambda^(jstar+1): the steps of the last chunk up to t = L-1
 };
 // Per-mode float64 scalars for the cross-tile carry chain.
 struct ModeCarry {
@@ -186,6 +187,10 @@ struct WsLayout {
 };
 
 // Flags of the segment look-back.
-enum : uint32_t { FLAG_NONE = 0, FLAG_AGG = 1 };
+// Single-kernel forward: header words (ticket, error) before the payloads, and
+// the pattern of an unpublished payload word (a signalling NaN, which no
+// arithmetic result is).
+constexpr int64_t SEG_HEADER_WORDS = 64;
+constexpr uint32_t PAY_EMPTY_WORD = 0x7FBADBADu;
 
 }  // namespace res

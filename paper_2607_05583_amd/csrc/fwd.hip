@@ -49,10 +49,10 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
   __shared__ double2 cm[MODES_PER_GROUP * MG_MAX];  // c
   __shared__ double taps[CHUNK + 1];
 
-  if (flags != nullptr)  // segment flags of the single-kernel forward
+  if (flags != nullptr)  // single-kernel forward: header words, then unpublished payload words
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nflags;
          i += (int64_t)gridDim.x * blockDim.x)
-      flags[i] = FLAG_NONE;
+      flags[i] = i < SEG_HEADER_WORDS ? 0u : PAY_EMPTY_WORD;
   const bool dvalid = d < D;
   for (int t = threadIdx.x; t < Mp * (NPW + 1); t += blockDim.x) {
     const int m = t / (NPW + 1), k = t % (NPW + 1);
@@ -89,6 +89,8 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     ms.mu = make_float2((float)pw[m][CHUNK].x, (float)pw[m][CHUNK].y);
     ms.mu8 = make_float2((float)lH.x, (float)lH.y);
     ms.lamT = make_float2((float)lT.x, (float)lT.y);
+    const int ntail = last_len > 0 ? (last_len - 1) % CHUNK + 1 : 0;
+    ms.lamTail = make_float2((float)pw[m][ntail].x, (float)pw[m][ntail].y);
     scal[(size_t)d * Mp + m] = ms;
     ModeCarry mc;
     mc.lamT = lT;
@@ -166,7 +168,17 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = (float)entry(mat, i, 4 * q + r);
       out = *reinterpret_cast<const uint4*>(v);
-    } else {
+    } else if (!BWD) {  // Ah[i][4q..4q+3], then Al[i][4q..4q+3]
+      bf16_t v[8];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const double e = entry(mat, i, 4 * q + r);
+        const bf16_t hi = from_f32<bf16_t>((float)e);
+        v[r] = hi;
+        v[4 + r] = from_f32<bf16_t>((float)(e - (double)to_f32(hi)));
+      }
+      out = *reinterpret_cast<const uint4*>(v);
+    } else {  // [Ah | Al][i][8q..8q+7] (32-deep contraction, activation duplicated)
       bf16_t v[8];
 #pragma unroll
       for (int r = 0; r < 8; ++r) {
@@ -276,40 +288,109 @@ __device__ __forceinline__ void tile_store(TY* y, const char* xt, int64_t b, int
   }
 }
 
-// Activation operand of chunk n for channel ch from the time-major tile.
-// Activations of the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4)
-// as MFMA B operands, one LDS read of the 4 channels per tile row.
-template <typename TX> struct XGather;
-template <> struct XGather<bf16_t> {
-  // lane (n, q): taps 8(q&1) .. +7 = rows 16n + 8(q&1) + r = group 2n + (q&1), row r
-  __device__ static __forceinline__ void get4(const char* xt, int ch0, int n, int q, bf8 (&xv)[4]) {
-    const char* p = xt + (2 * n + (q & 1)) * XLay<2>::GRP + ch0 * 2;
-    uint2 w[8];
-#pragma unroll
-    for (int r = 0; r < 8; ++r) w[r] = *reinterpret_cast<const uint2*>(p + r * XROW);
-    // channel c of row r is the (c & 1) half of word c >> 1 of w[r]
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      uint32_t o[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const uint32_t lo = (c >> 1) ? w[2 * j].y : w[2 * j].x;
-        const uint32_t hi = (c >> 1) ? w[2 * j + 1].y : w[2 * j + 1].x;
-        o[j] = (c & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      xv[c] = __builtin_bit_cast(bf8, *reinterpret_cast<const uint4*>(o));
-    }
-  }
-};
-template <> struct XGather<float> {
-  // lane (n, q), slot kk: tap 4q + kk = row 16n + 4q + kk = group 2n + (q>>1), row 4(q&1) + kk
-  __device__ static __forceinline__ void get4(const char* xt, int ch0, int n, int q, f4 (&xv)[4]) {
+// ---------------------------------------------------------------------------
+// Forward operands: every product contracts one chunk (16 steps).
+//   FPath<float>: four v_mfma_f32_16x16x4_f32, slot (kk, q) = index 4q + kk:
+//     lane (i, q) holds A[i][4q..4q+3], lane (n, q) holds B[4q..4q+3][n].
+//   FPath<bf16_t>: split-bf16 on v_mfma_f32_16x16x16_bf16.  A per-channel
+//     matrix A (from float64) is stored as Ah = bf16(A), Al = bf16(A - Ah); lane
+//     (i, q) holds Ah[i][4q..4q+3] then Al[i][4q..4q+3] (16 bytes).  The
+//     activations are exact in bf16; lane (n, q) holds x[16n+4q .. 16n+4q+3],
+//     and two instructions give (Ah + Al) x (tables at ~2^-17 relative).
+// In both, lane (n, q) of the activation operand reads tile rows 16n + 4q + r,
+// r = 0..3: group 2n + (q >> 1), rows 4 (q & 1) + r.
+// ---------------------------------------------------------------------------
+template <typename TX> struct FPath;
+template <> struct FPath<float> {
+  typedef f4 AOp;
+  typedef f4 XOp;
+  __device__ static __forceinline__ AOp load_a(const void* p) { return load_f4(p); }
+  __device__ static __forceinline__ f4 mma(const AOp& a, const XOp& x, f4 c) { return mma_f32(a, x, c); }
+  // (A x)^T: lane (i, q) gets columns 4q .. 4q+3 of row i of A x
+  __device__ static __forceinline__ f4 mma_t(const XOp& x, const AOp& a, f4 c) { return mma_f32(x, a, c); }
+  // y += U H for float32 states H (lane (n, q): components 4q .. 4q+3 of chunk n)
+  typedef f4 UOp;
+  __device__ static __forceinline__ UOp u_op(const f4& u) { return u; }
+  __device__ static __forceinline__ f4 mma_u(const UOp& u, const f4& h, f4 c) { return mma_f32(u, h, c); }
+  // the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4), one 16-byte read per row
+  __device__ static __forceinline__ void gather4(const char* xt, int ch0, int n, int q, XOp (&xv)[4]) {
     const char* p = xt + (2 * n + (q >> 1)) * XLay<4>::GRP + 4 * (q & 1) * XROW + ch0 * 4;
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
       const f4 w = *reinterpret_cast<const f4*>(p + kk * XROW);
 #pragma unroll
       for (int c = 0; c < 4; ++c) xv[c][kk] = w[c];
+    }
+  }
+};
+template <> struct FPath<bf16_t> {
+  struct AOp {
+    s4 hi, lo;
+  };
+  typedef s4 XOp;
+  __device__ static __forceinline__ AOp load_a(const void* p) {
+    const uint4 u = *reinterpret_cast<const uint4*>(p);
+    AOp a;
+    a.hi = __builtin_bit_cast(s4, make_uint2(u.x, u.y));
+    a.lo = __builtin_bit_cast(s4, make_uint2(u.z, u.w));
+    return a;
+  }
+  __device__ static __forceinline__ f4 mma(const AOp& a, const XOp& x, f4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.hi, x, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a.lo, x, c, 0, 0, 0);
+  }
+  // (A x)^T: lane (i, q) gets columns 4q .. 4q+3 of row i of A x
+  __device__ static __forceinline__ f4 mma_t(const XOp& x, const AOp& a, f4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x, a.hi, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x, a.lo, c, 0, 0, 0);
+  }
+  // y += U H for float32 states H (lane (n, q): components 4q .. 4q+3 of chunk n):
+  // U (float32 table) and H split into bf16 halves, Uh Hh + Ul Hh + Uh Hl
+  // (the omitted Ul Hl is ~2^-16 relative)
+  typedef AOp UOp;
+  __device__ static __forceinline__ UOp u_op(const f4& u) {
+    UOp r;
+    typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+    b4 hi, lo;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      hi[i] = (__bf16)u[i];
+      lo[i] = (__bf16)(u[i] - (float)hi[i]);
+    }
+    r.hi = __builtin_bit_cast(s4, hi);
+    r.lo = __builtin_bit_cast(s4, lo);
+    return r;
+  }
+  __device__ static __forceinline__ f4 mma_u(const UOp& u, const f4& h, f4 c) {
+    typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+    b4 hh, hl;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      hh[i] = (__bf16)h[i];
+      hl[i] = (__bf16)(h[i] - (float)hh[i]);
+    }
+    const s4 bh = __builtin_bit_cast(s4, hh), bl = __builtin_bit_cast(s4, hl);
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.hi, bh, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.lo, bh, c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.hi, bl, c, 0, 0, 0);
+  }
+  // the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4), one 8-byte read per row
+  __device__ static __forceinline__ void gather4(const char* xt, int ch0, int n, int q, XOp (&xv)[4]) {
+    const char* p = xt + (2 * n + (q >> 1)) * XLay<2>::GRP + 4 * (q & 1) * XROW + ch0 * 2;
+    uint2 w[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const uint2*>(p + r * XROW);
+    // channel c of row r is the (c & 1) half of word c >> 1 of w[r]
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      uint32_t o[2];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const uint32_t lo = (c >> 1) ? w[2 * j].y : w[2 * j].x;
+        const uint32_t hi = (c >> 1) ? w[2 * j + 1].y : w[2 * j + 1].x;
+        o[j] = (c & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      xv[c] = __builtin_bit_cast(s4, make_uint2(o[0], o[1]));
     }
   }
 };
@@ -359,7 +440,7 @@ __device__ __forceinline__ void put_y4_global(float* y, const f4 (&acc)[4], int6
 
 template <typename TX, int MG>
 struct FwdTile {
-  typedef Path<TX> PT;
+  typedef FPath<TX> PT;
   static constexpr int DW = tile_channels<TX>();
   static constexpr int CPW = DW / NWAVES;     // channels per wave
   static constexpr int NGRP = CPW / 4;       // scan groups of 4 channels
@@ -373,17 +454,17 @@ struct FwdTile {
 // S = V x for the 4 channels of a group into the wave's scan buffer.
 template <typename TX, int MG>
 __device__ __forceinline__ void group_states(const char* xt, float* wb, int ch0,
-                                             const typename Path<TX>::AOp (&vop)[4][MG],
-                                             typename Path<TX>::XOp (&xv)[4], int ln, int lq) {
+                                             const typename FPath<TX>::AOp (&vop)[4][MG],
+                                             typename FPath<TX>::XOp (&xv)[4], int ln, int lq) {
   typedef FwdTile<TX, MG> F;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
-  XGather<TX>::get4(xt, ch0, ln, lq, xv);
+  FPath<TX>::gather4(xt, ch0, ln, lq, xv);
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
 #pragma unroll
     for (int g = 0; g < MG; ++g)
       *reinterpret_cast<f4*>(&wb[k * F::CSTR + ln * F::NSTR + g * 16 + lq * 4]) =
-          Path<TX>::mma(vop[k][g], xv[k], zero);
+          FPath<TX>::mma(vop[k][g], xv[k], zero);
   }
 }
 
@@ -743,6 +824,7 @@ __device__ __forceinline__ void st_flag(uint32_t* f, uint32_t v) {
 // never publishes, which the ticket order rules out.  The wave then starts from
 // the row's initial state and records the event in the error word.
 constexpr uint32_t SPIN_LIMIT = 1u << 20;
+constexpr uint32_t PAY_EMPTY = PAY_EMPTY_WORD;
 
 // Complex arithmetic on the two modes of a lane, (re_a, im_a, re_b, im_b).
 __device__ __forceinline__ f4 c2mul(const f4& a, const f4& b) {
@@ -785,6 +867,11 @@ __device__ __forceinline__ f4 dpp4(const f4& old, const f4& v) {
   }
   return r;
 }
+// the value of lane i ^ 1 (the other component of a complex number)
+__device__ __forceinline__ float partner(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), DPP_QUAD(1, 0, 3, 2), 0xF,
+                                                            0xF, true));
+}
 // Sum over the 16 lanes of each row, in every lane of the row (the same order in
 // every lane, so the copies agree bitwise).
 __device__ __forceinline__ f4 row_sum(f4 v) {
@@ -802,65 +889,58 @@ struct SegGeo {
   static constexpr int CW = DW / NW;    // channels per wave (bf16 8, float 4)
   static constexpr int NG = CW / 4;     // operand gathers of 4 channels per wave
   static constexpr int NT = 64 * NW;    // threads
-  static constexpr int NBUF = 3;        // LDS tile buffers (two loads in flight)
+  static constexpr int NBUF = SEG_BUFS;  // tile buffers; wave b loads the tiles of buffer b
+  static_assert(NBUF < NW, "loading waves and storing waves");
 };
 
-// s_waitcnt until at most n vector-memory operations of this wave are
-// outstanding (expcnt and lgkmcnt not waited on); n < 64.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+// Direct-to-LDS load of a full tile by the calling wave: 32 loads of 16 bytes
+// per lane, 8 rows of 128 bytes each.
+template <typename TX>
+__device__ __forceinline__ void dma_tile(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
+                                         int D, int lane) {
+  constexpr int XE = (int)sizeof(TX);
+  const char* src = reinterpret_cast<const char*>(x) + ((b * L + t0) * D + d0) * XE;
+  const int64_t rowb = (int64_t)D * XE;
+  const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
+#pragma unroll
+  for (int g = 0; g < TILE_T / 8; ++g)
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(src + (int64_t)(8 * g) * rowb + loff),
+                                     (lvoid_t*)(xt + g * XLay<XE>::GRP), 16, 0, 0);
 }
 
-// Drive tile into one LDS buffer (all threads call).  Full tiles: wave 0 alone
-// issues the direct-to-LDS loads, so the loads are the only vector-memory
-// operations it has in flight and it can wait for them exactly; other tiles:
-// element loads by all threads, zeros outside the tensor.
+// Element copy of a tile that is not full (all threads); zeros outside the tensor.
 template <typename TX>
-__device__ __forceinline__ void seg_tile_load(char* xt, const TX* x, int64_t b, int64_t t0, int d0,
-                                              int64_t L, int D, bool full, int tid, int wave) {
+__device__ __forceinline__ void copy_tile(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
+                                          int D, int tid) {
   typedef SegGeo<TX> G;
   constexpr int DW = G::DW, XE = (int)sizeof(TX);
-  const int lane = tid & 63;
-  if (full) {
-    if (wave == 0) {
-      const char* src = reinterpret_cast<const char*>(x) + ((b * L + t0) * D + d0) * XE;
-      const int64_t rowb = (int64_t)D * XE;
-      const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
-#pragma unroll
-      for (int g = 0; g < TILE_T / 8; ++g)
-        __builtin_amdgcn_global_load_lds((gvoid_t*)(src + (int64_t)(8 * g) * rowb + loff),
-                                         (lvoid_t*)(xt + g * XLay<XE>::GRP), 16, 0, 0);
-    }
-  } else {
-    for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
-      const int t = idx / DW, c = idx % DW;
-      TX v = from_f32<TX>(0.f);
-      if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
-      *reinterpret_cast<TX*>(xt + XLay<XE>::off(t) + c * XE) = v;
-    }
+  for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
+    const int t = idx / DW, c = idx % DW;
+    TX v = from_f32<TX>(0.f);
+    if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
+    *reinterpret_cast<TX*>(xt + XLay<XE>::off(t) + c * XE) = v;
   }
 }
 
-// Output tile from one LDS buffer (all threads call).  Full tiles: 16-byte row
-// stores by waves 1 .. NW-1 (wave 0 keeps a load-only queue); other tiles:
-// guarded element stores by all threads.
+// Output tile from one LDS buffer (all threads call): full tiles as 16-byte row
+// stores by waves NBUF .. NW-1 (the loading waves keep load-only queues), read
+// from LDS as 8-byte pairs; other tiles as guarded element stores by all threads.
 template <typename TY>
-__device__ __forceinline__ void seg_tile_store(TY* y, const char* xt, int64_t b, int64_t t0, int d0,
-                                               int64_t L, int D, bool full, int tid, int wave) {
+__device__ __forceinline__ void store_tile(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
+                                           int D, bool full, int tid, int wave) {
   typedef SegGeo<TY> G;
   constexpr int DW = G::DW, YE = (int)sizeof(TY);
   const int lane = tid & 63;
   if (full) {
-    if (wave > 0) {
-      char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE;
-      const int64_t rowb = (int64_t)D * YE;
-      const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
-      for (int g = wave - 1; g < TILE_T / 8; g += G::NW - 1) {
-        const uint4 v = *reinterpret_cast<const uint4*>(xt + g * XLay<YE>::GRP + lane * 16);
-        *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g) * rowb + loff) = v;
-      }
+    if (wave < G::NBUF) return;
+    char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE;
+    const int64_t rowb = (int64_t)D * YE;
+    const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
+#pragma unroll
+    for (int g = wave - G::NBUF; g < TILE_T / 8; g += G::NW - G::NBUF) {
+      const uint2* s = reinterpret_cast<const uint2*>(xt + g * XLay<YE>::GRP + lane * 16);
+      const uint2 u = s[0], w = s[1];
+      *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g) * rowb + loff) = make_uint4(u.x, u.y, w.x, w.y);
     }
   } else {
     for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
@@ -874,24 +954,32 @@ __device__ __forceinline__ void seg_tile_store(TY* y, const char* xt, int64_t b,
 template <typename TX, typename TY>
 __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   typedef SegGeo<TX> G;
-  typedef Path<TX> PT;
-  constexpr int DW = G::DW, NW = G::NW, CW = G::CW, NG = G::NG, XE = (int)sizeof(TX);
+  typedef FPath<TX> PT;
+  constexpr int DW = G::DW, NW = G::NW, CW = G::CW, NG = G::NG, NBUF = G::NBUF, XE = (int)sizeof(TX);
   constexpr int NM = fwd_mats(1);  // T, V, U
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
-  __shared__ __align__(16) char xb[G::NBUF][XLay<XE>::BYTES];
-  // per (channel, power s, row q): mu^(2^s) of the modes 2q, 2q+1
-  __shared__ __align__(16) f4 s_pw[DW * 4 * 4];
-  // per (channel, row q): the state entering the next tile; then a zero entry
-  __shared__ __align__(16) f4 s_c[DW * 4 + 1];
+  __shared__ __align__(16) char xb[NBUF][XLay<XE>::BYTES];  // the segment's tile buffers
+  // per wave: block aggregates of 4 channels [channel][component][block], and the
+  // chunk states of one channel [component][chunk] (rows of HSTR floats)
+  constexpr int HSTR = 20;
+  __shared__ __align__(16) float s_blk[NW][4][16][4];
+  __shared__ __align__(16) float s_h[NW][4][16 * HSTR];
+  // per (channel, row q), last tile of a row: the drive part of the state at
+  // t = L-1, then the state entering its chunk
+  __shared__ __align__(16) f4 s_tail[DW * 4], s_hn[DW * 4];
   __shared__ uint32_t s_tk;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
   const int ln = lane & 15, lq = lane >> 4;                   // chunk, mode pair (2 lq, 2 lq + 1)
   const int nchains = (int)(a.B * a.NB);
-  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  const f4 zero = {0.f, 0.f, 0.f, 0.f}, one = {1.f, 0.f, 1.f, 0.f};
+  const char* tab = reinterpret_cast<const char*>(a.tab);
+  const int c0 = wave * CW;  // this wave's first channel within the tile
 
+  // segment of the ticket: time-major over the chains, so that every segment's
+  // predecessors in its row hold smaller tickets (taken by running work-groups)
   if (tid == 0) s_tk = atomicAdd(a.ticket, 1u);
   __syncthreads();
   const int64_t tk = (int64_t)__builtin_amdgcn_readfirstlane(s_tk);
@@ -902,73 +990,87 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   const int64_t pb = seg * a.seg_len;                                 // first tile
   const int nt = (int)(a.P - pb < a.seg_len ? a.P - pb : a.seg_len);  // tiles of the segment
   const bool last_seg = (seg == a.seg_per_chain - 1);
-  const int c0 = wave * CW;  // this wave's first channel within the tile
+  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
 
-  const char* tab = reinterpret_cast<const char*>(a.tab);
   auto tab_of = [&](int k) {
     return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
   };
-  // scalars of the lane's two modes of channel c0 + k
   auto scal_of = [&](int k) { return a.scal + (size_t)(d0 + c0 + k) * a.Mp + 2 * lq; };
-
-  auto tile_full = [&](int64_t p) {
-    return a.fast_io && (p + 1) * TILE_T <= a.L && d0 + DW <= a.D;
+  auto tile_full = [&](int t) { return a.fast_io && (pb + t + 1) * TILE_T <= a.L && d0 + DW <= a.D; };
+  // tile t of the segment into buffer u: full tiles by the buffer's own wave
+  // (direct to LDS; that wave issues no stores, so it waits for its tile
+  // exactly); the others are copied by all threads when they are used
+  auto request = [&](int t, int u) {
+    if (t < nt && wave == u && tile_full(t))
+      dma_tile<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, lane);
   };
-  auto load = [&](int i) {
-    const int64_t p = pb + i;
-    seg_tile_load<TX>(xb[i % G::NBUF], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D,
-                      tile_full(p), tid, wave);
-  };
-  // wave 0 issues the tile loads and no stores: wait until tile i's loads are in
-  // while tile i+1's (issued later, if by direct-to-LDS loads) stay in flight.
-  // (Loads complete in order among themselves; with float32 outputs stored
-  // straight from registers wave 0 also stores, so it then waits for all.)
-  auto wait_tile = [&](int i) {
-    if (wave == 0) {
-      if (!SEPY && i + 1 < nt && tile_full(pb + i + 1))
-        wait_vmcnt<TILE_T / 8>();
-      else
-        __builtin_amdgcn_s_waitcnt(0);
+  // make tile t in buffer u usable: wait for its load, or copy it; the caller synchronises
+  auto arrive = [&](int t, int u) {
+    if (tile_full(t)) {
+      if (wave == u) __builtin_amdgcn_s_waitcnt(0);
+    } else {
+      copy_tile<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, tid);
     }
   };
 
+  // operands and multipliers first, so that waiting for them waits for no tile
   typename PT::AOp vop[CW];
 #pragma unroll
   for (int k = 0; k < CW; ++k) vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);
-  // scan multipliers mu, mu^2, mu^4, mu^8 = lambda^(16 j), j = 1, 2, 4, 8
-  for (int e = tid; e < DW * 4 * MODES_PER_GROUP; e += G::NT) {
-    const int ch = e / (4 * MODES_PER_GROUP), sp = (e / MODES_PER_GROUP) % 4, m = e % MODES_PER_GROUP;
-    reinterpret_cast<float2*>(s_pw)[e] = a.mpow[((size_t)(d0 + ch) * CHUNK + (1 << sp)) * a.Mp + m];
+  // pass 1 weights: mu^(15-n) of the lane's modes (rows [d][j][Mp] of lambda^(16 j)), lambda^256
+  f4 ww[CW], lt[CW];
+#pragma unroll
+  for (int k = 0; k < CW; ++k) {
+    ww[k] = load_f4(a.mpow + ((size_t)(d0 + c0 + k) * CHUNK + (CHUNK - 1 - ln)) * a.Mp + 2 * lq);
+    const ModeScalars* ms = scal_of(k);
+    lt[k] = mode_pair(ms[0].lamT, ms[1].lamT);
   }
-  if (tid < 4) s_c[DW * 4][tid] = 0.f;
+  // Pass 1 visits the tiles last to first, so that tiles 0 .. R-1 (R =
+  // min(nt, NBUF)) are the ones still in the buffers when pass 2 starts.  Pass
+  // 1's j-th tile (tile nt-1-j) uses buffer j % NBUF; in pass 2 tile t uses
+  // buffer (nt-1-(t % NBUF)) % NBUF, which agrees for t < R, and tile t >= R
+  // follows tile t - NBUF into its buffer.
+  const int R = nt < NBUF ? nt : NBUF;
+  auto buf2 = [&](int t) { return (nt - 1 - (t % NBUF)) % NBUF; };
+  for (int j = 0; j < NBUF && j < nt; ++j) request(nt - 1 - j, j);
 
   // ---- pass 1: the segment's own end state ---------------------------------
+  // sagg = sum over tiles t and chunks n of lambda^(256 (nt-1-t)) mu^(15-n) S_t[n];
+  // lane-wise, with the weight carried from tile to tile (last tile first)
   f4 sagg[CW];
   {
-    f4 w[CW], lt[CW];
 #pragma unroll
-    for (int k = 0; k < CW; ++k) {
-      // mu^(15-n) of the lane's modes (rows [d][j][Mp] of lambda^(16 j))
-      w[k] = load_f4(a.mpow + ((size_t)(d0 + c0 + k) * CHUNK + (CHUNK - 1 - ln)) * a.Mp + 2 * lq);
-      const ModeScalars* ms = scal_of(k);
-      lt[k] = mode_pair(ms[0].lamT, ms[1].lamT);
-      sagg[k] = zero;
-    }
-    load(0);
-    if (nt > 1) load(1);
-    for (int i = 0; i < nt; ++i) {
-      wait_tile(i);
-      __syncthreads();  // tile i is in; every wave is done with tile i-1's buffer
-      if (i + 2 < nt) load(i + 2);
-      const char* xt = xb[i % G::NBUF];
+    for (int k = 0; k < CW; ++k) sagg[k] = zero;
+    for (int j = 0; j < nt; ++j) {
+      const int t = nt - 1 - j;
+      arrive(t, j % NBUF);
+      __syncthreads();  // tile t is in; the buffer of the tile visited before it is free
+      if (j >= 1 && j + NBUF - 1 < nt) request(nt - j - NBUF, (j + NBUF - 1) % NBUF);
+      const char* xt = xb[j % NBUF];
 #pragma unroll
       for (int gr = 0; gr < NG; ++gr) {
         typename PT::XOp xv[4];
-        XGather<TX>::get4(xt, c0 + 4 * gr, ln, lq, xv);
+        PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
 #pragma unroll
         for (int kk = 0; kk < 4; ++kk) {
           const int k = 4 * gr + kk;
-          sagg[k] = c2fma(lt[k], sagg[k], c2mul(w[k], PT::mma(vop[k], xv[kk], zero)));
+          sagg[k] = c2fma(ww[k], PT::mma(vop[k], xv[kk], zero), sagg[k]);
+          ww[k] = c2mul(ww[k], lt[k]);
+        }
+      }
+      if (pb + t == a.P - 1 && a.h_out != nullptr && ln == nstar) {
+        // last tile of the row: sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
+        for (int k = 0; k < CW; ++k) {
+          const ModeScalars* ms = scal_of(k);
+          const f4 lam = mode_pair(ms[0].lam, ms[1].lam);
+          f4 tl = zero;
+          for (int i = 0; i <= jstar; ++i) {
+            const float xr =
+                to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + i) + (c0 + k) * XE));
+            const f4 xin = {xr, 0.f, xr, 0.f};
+            tl = c2fma(lam, tl, xin);
+          }
+          s_tail[(c0 + k) * 4 + lq] = tl;
         }
       }
     }
@@ -981,132 +1083,171 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   // seg_len): term u = seg-1-j (u = seg: h0) goes to lane u % 16 of every row,
   // weighted by lamS^(u % 16) and summed over the row; blocks of 16 terms are
   // combined farthest first by Horner's rule with lamS^16.  The order is fixed
-  // by seg alone, so the result is bitwise reproducible.
+  // by seg alone, so the result is bitwise reproducible.  Payload words start
+  // as a signalling-NaN pattern, which arithmetic never produces, so a word
+  // that differs from it has been published.
   const int64_t sub = tk * NW + wave;
   // payload of sub-chain s, channel k: 8 modes as float2; the lane's pair at 2 lq
   auto pay = [&](int64_t s, int k) { return ((size_t)s * CW + k) * MODES_PER_GROUP + 2 * lq; };
-  if (!last_seg) {  // publish this segment's own end state
-    if (ln == 0)
+  if (!last_seg && ln == 0)  // publish this segment's own end state
 #pragma unroll
-      for (int k = 0; k < CW; ++k) st_agent4(a.pay_agg + pay(sub, k), sagg[k]);
-    __builtin_amdgcn_s_waitcnt(0);
-    if (lane == 0) st_flag(a.flags + sub, FLAG_AGG);
-  }
-  // wait until every earlier segment of the row has published
-  for (int64_t top = seg - 1; top >= 0; top -= 64) {
-    const int64_t j = top - lane;
-    for (uint32_t it = 0;; ++it) {
-      const bool ok = j < 0 || ld_flag(a.flags + (j * nchains + chain) * NW + wave) != FLAG_NONE;
-      if (__ballot(!ok) == 0) break;
-      if (it >= SPIN_LIMIT) {
-        if (lane == 0) atomicOr(a.error, 1u);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  }
+    for (int k = 0; k < CW; ++k) st_agent4(a.pay_agg + pay(sub, k), sagg[k]);
   f4 carry[CW];
   {
-    // lamS^n of the lane's modes (rows [d][n][Mp], n = 0..16)
+    // lamS^n (n the lane's chunk) and lamS^16 of the lane's modes, from the table
     auto spw = [&](int k, int n) {
       return load_f4(a.spow + ((size_t)(d0 + c0 + k) * (CHUNK + 1) + n) * a.Mp + 2 * lq);
     };
-    f4 wn[CW], w16[CW];
 #pragma unroll
-    for (int k = 0; k < CW; ++k) {
-      wn[k] = spw(k, ln);
-      w16[k] = spw(k, CHUNK);
-      carry[k] = zero;
-    }
+    for (int k = 0; k < CW; ++k) carry[k] = zero;
     for (int64_t blk = seg / CHUNK; blk >= 0; --blk) {
       const int64_t u = blk * CHUNK + ln;
+      const float2* src = a.pay_agg + pay(((seg - 1 - u) * nchains + chain) * NW + wave, 0);
       f4 v[CW];
-#pragma unroll
-      for (int k = 0; k < CW; ++k) {
-        v[k] = zero;
+      for (uint32_t it = 0;; ++it) {
+        bool ok = true;
         if (u < seg) {
-          v[k] = ld_agent4(a.pay_agg + pay(((seg - 1 - u) * nchains + chain) * NW + wave, k));
-        } else if (u == seg && a.h0 != nullptr && d0 + c0 + k < a.D) {
-          const float* h = a.h0 + ((size_t)(b * a.D + d0 + c0 + k) * a.M + 2 * lq) * 2;
-          if (2 * lq < a.M) v[k][0] = h[0], v[k][1] = h[1];
-          if (2 * lq + 1 < a.M) v[k][2] = h[2], v[k][3] = h[3];
+#pragma unroll
+          for (int k = 0; k < CW; ++k) {
+            v[k] = ld_agent4(src + (size_t)k * MODES_PER_GROUP);
+            ok = ok && __float_as_uint(v[k][0]) != PAY_EMPTY && __float_as_uint(v[k][1]) != PAY_EMPTY &&
+                 __float_as_uint(v[k][2]) != PAY_EMPTY && __float_as_uint(v[k][3]) != PAY_EMPTY;
+          }
         }
+        if (__ballot(!ok) == 0) break;
+        if (it >= SPIN_LIMIT) {  // unreachable in ticket order; give up and flag it
+          if (lane == 0) atomicOr(a.error, 1u);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
       }
 #pragma unroll
-      for (int k = 0; k < CW; ++k) carry[k] = c2fma(w16[k], carry[k], row_sum(c2mul(wn[k], v[k])));
+      for (int k = 0; k < CW; ++k) {
+        if (u >= seg) {
+          v[k] = zero;
+          if (u == seg && a.h0 != nullptr && d0 + c0 + k < a.D) {
+            const float* h = a.h0 + ((size_t)(b * a.D + d0 + c0 + k) * a.M + 2 * lq) * 2;
+            if (2 * lq < a.M) v[k][0] = h[0], v[k][1] = h[1];
+            if (2 * lq + 1 < a.M) v[k][2] = h[2], v[k][3] = h[3];
+          }
+        }
+        carry[k] = c2fma(spw(k, CHUNK), carry[k], row_sum(c2mul(spw(k, ln), v[k])));
+      }
     }
   }
 
   // ---- pass 2: the chunk scans and the outputs ----------------------------------
-  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
-  __syncthreads();  // every wave is done with pass 1's buffers
-  load(0);
-  if (nt > 1) load(1);
+  // S^T = (V x)^T puts component c = ln of chunks 4q .. 4q+3 (q = lq) in lane
+  // (c, q); the partner component (re <-> im of the same mode) is in lane c ^ 1.
+  // Per tile and channel: block aggregates A_q (Horner over the lane's 4
+  // chunks), their exchange through LDS, the block entry states
+  // E_{q+1} = mu^4 E_q + A_q from the tile's entering state E_0, the lane's 4
+  // chunk states from E_q, and their transpose through LDS into the B operand
+  // of y += U H.  A complex factor z acts on a component v with partner p as
+  // Re z v + s Im z p, s = -1 for the real part and +1 for the imaginary part.
   typename PT::AOp top[CW];
-  f4 uop[CW];
+  typename PT::UOp uop[CW];
+  float cin[CW], m1r[CW], m1s[CW], m4r[CW], m4s[CW];
+  // the entering state as component ln (the fold leaves modes 2 lq, 2 lq + 1 in row lq)
+  if (ln == 0)
+#pragma unroll
+    for (int k = 0; k < CW; ++k) *reinterpret_cast<f4*>(&s_h[wave][0][k * 16 + 4 * lq]) = carry[k];
+  wave_lds_order();
+#pragma unroll
+  for (int k = 0; k < CW; ++k) cin[k] = s_h[wave][0][k * 16 + ln];
+  wave_lds_order();
 #pragma unroll
   for (int k = 0; k < CW; ++k) {
+    vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);  // (not held through the carry phase)
     top[k] = PT::load_a(tab_of(k));
-    uop[k] = load_f4(tab_of(k) + 2 * TAB_MAT_BYTES);
-    if (ln == 0) s_c[(c0 + k) * 4 + lq] = carry[k];
+    uop[k] = PT::u_op(load_f4(tab_of(k) + 2 * TAB_MAT_BYTES));
+    const int m = ln >> 1;
+    const float sgn = (ln & 1) ? 1.f : -1.f;
+    const float2 z1 = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 1) * a.Mp + m];
+    const float2 z4 = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 4) * a.Mp + m];
+    m1r[k] = z1.x;
+    m1s[k] = sgn * z1.y;
+    m4r[k] = z4.x;
+    m4s[k] = sgn * z4.y;
   }
-  wave_lds_order();
-  for (int i = 0; i < nt; ++i) {
-    wait_tile(i);
-    __syncthreads();  // tile i is in; every wave is done with tile i-1's buffer
-    if (i + 2 < nt) load(i + 2);
-    char* xt = xb[i % G::NBUF];
-    const int64_t p = pb + i;
+  // z v + (partner): one complex multiply-add on the lane's component
+  auto cstep = [](float zr, float zs, float v, float add) {
+    return fmaf(zr, v, fmaf(zs, partner(v), add));
+  };
+  for (int t = 0; t < nt; ++t) {
+    if (t >= R) arrive(t, buf2(t));  // tiles 0 .. R-1 are still in their buffers from pass 1
+    // tile t is in; tile t-1's buffer has been read for its stores, so tile
+    // t-1+NBUF may follow into it
+    __syncthreads();
+    if (t >= 1) request(t - 1 + NBUF, buf2(t - 1));
+    char* xt = xb[buf2(t)];
+    const int64_t p = pb + t;
 #pragma unroll
     for (int gr = 0; gr < NG; ++gr) {
       typename PT::XOp xv[4];
-      XGather<TX>::get4(xt, c0 + 4 * gr, ln, lq, xv);
-      f4 acc[4];
+      PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
+      f4 st[4], acc[4];
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int k = 4 * gr + kk;
-        const f4* pw = s_pw + (c0 + k) * 16 + lq;  // mu^(2^s) at pw[4 s]
-        // the entering state c in lane 0 of each row, zero in the others
-        const f4 c = s_c[ln == 0 ? (c0 + k) * 4 + lq : DW * 4];
-        // Q[n] = sum_{j <= n} mu^(n-j) S[j] + mu^(n+1) c, four shift steps
-        f4 q = c2fma(pw[0], c, PT::mma(vop[k], xv[kk], zero));
-        q = c2fma(pw[0], dpp4<DPP_ROW_SHR(1), true>(zero, q), q);
-        q = c2fma(pw[4], dpp4<DPP_ROW_SHR(2), true>(zero, q), q);
-        q = c2fma(pw[8], dpp4<DPP_ROW_SHR(4), true>(zero, q), q);
-        q = c2fma(pw[12], dpp4<DPP_ROW_SHR(8), true>(zero, q), q);
-        const f4 h = dpp4<DPP_ROW_SHR(1), false>(c, q);  // state entering chunk n (c for n = 0)
-        if (ln == CHUNK - 1) s_c[(c0 + k) * 4 + lq] = q;   // state after the tile
-        acc[kk] = mma_f32(uop[k], h, PT::mma(top[k], xv[kk], zero));
-        if (p == a.P - 1 && a.h_out != nullptr && ln == nstar) {
-          // terminal state at t = L-1 from the state entering chunk nstar
-          const int d = d0 + c0 + k;
-          const ModeScalars* ms = scal_of(k);
-          const f4 lam = mode_pair(ms[0].lam, ms[1].lam);
-          f4 hl = h;
-          for (int j = 0; j <= jstar; ++j) {
-            const float xr = to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + j) +
-                                                                 (c0 + k) * XE));
-            const f4 xin = {xr, 0.f, xr, 0.f};
-            hl = c2fma(lam, hl, xin);
-          }
-          if (d < a.D) {
-            float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + 2 * lq) * 2;
-            if (2 * lq < a.M) ho[0] = hl[0], ho[1] = hl[1];
-            if (2 * lq + 1 < a.M) ho[2] = hl[2], ho[3] = hl[3];
-          }
-          wave_lds_order();  // the drive reads above precede the output writes below
-        }
+        st[kk] = PT::mma_t(xv[kk], vop[k], zero);
+        float ag = st[kk][0];
+#pragma unroll
+        for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, st[kk][r]);
+        s_blk[wave][kk][ln][lq] = ag;  // A_lq of component ln
       }
+      wave_lds_order();
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int k = 4 * gr + kk;
+        const f4 A = *reinterpret_cast<const f4*>(&s_blk[wave][kk][ln][0]);
+        // block entry states: E_0 = c, E_{q+1} = mu^4 E_q + A_q; E_4 enters the next tile
+        float e = cin[k], eq = e;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          e = cstep(m4r[k], m4s[k], e, A[q]);
+          if (lq == q + 1) eq = e;
+        }
+        cin[k] = e;
+        // states entering chunks 4 lq .. 4 lq + 3, into the channel's transpose slot
+        f4 h;
+        h[0] = eq;
+#pragma unroll
+        for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], st[kk][r - 1]);
+        *reinterpret_cast<f4*>(&s_h[wave][kk][ln * HSTR + 4 * lq]) = h;
+      }
+      wave_lds_order();
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        const int k = 4 * gr + kk;
+        // lane (n, q) takes components 4q .. 4q+3 of chunk n
+        f4 hb;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) hb[j] = s_h[wave][kk][(4 * lq + j) * HSTR + ln];
+        acc[kk] = PT::mma_u(uop[k], hb, PT::mma(top[k], xv[kk], zero));
+        if (p == a.P - 1 && ln == nstar) s_hn[(c0 + k) * 4 + lq] = hb;  // state entering chunk nstar
+      }
+      wave_lds_order();
       if (SEPY)
         put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4,
                       d0 + c0 + 4 * gr, a.L, a.D);
       else
         put_y4<TY>(xt, c0 + 4 * gr, ln, lq, acc);
     }
-    if (!SEPY) {
-      __syncthreads();  // the whole output tile is in the buffer
-      seg_tile_store<TY>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, tile_full(p), tid,
-                         wave);
+    __syncthreads();  // tile t's outputs are in its buffer
+    if (!SEPY)
+      store_tile<TY>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, tile_full(t), tid, wave);
+  }
+  if (pb + nt == a.P && a.h_out != nullptr && lane < 4 * CW) {
+    // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar,
+    // plus the drive part from pass 1 (the wave's own entries)
+    const int k = lane >> 2, r = lane & 3, d = d0 + c0 + k;
+    const ModeScalars* ms = a.scal + (size_t)d * a.Mp + 2 * r;
+    const f4 hl = c2fma(mode_pair(ms[0].lamTail, ms[1].lamTail), s_hn[(c0 + k) * 4 + r], s_tail[(c0 + k) * 4 + r]);
+    if (d < a.D) {
+      float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + 2 * r) * 2;
+      if (2 * r < a.M) ho[0] = hl[0], ho[1] = hl[1];
+      if (2 * r + 1 < a.M) ho[2] = hl[2], ho[3] = hl[3];
     }
   }
 }

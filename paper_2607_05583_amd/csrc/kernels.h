@@ -11,6 +11,8 @@ enum { MODE_STATE = 0, MODE_APPLY = 1 };
 
 // waves per work-group of the single-kernel forward (each publishes its own sub-chain)
 constexpr int SEG_WAVES = 8;
+// LDS tile buffers of the single-kernel forward
+constexpr int SEG_BUFS = 3;
 
 struct FwdArgs {
   const void* x;
@@ -34,7 +36,6 @@ struct FwdArgs {
   // single-kernel forward: segments of seg_len tiles, ticket order time-major over chains
   int seg_len, seg_per_chain;
   uint32_t* ticket;  // segment ticket counter
-  uint32_t* flags;   // per (segment, wave): FLAG_NONE / FLAG_AGG
   uint32_t* error;   // set when a bounded wait gives up
   float2* pay_agg;   // per (segment, wave) [channels][8 modes]: the segment's own end state
 };
