@@ -48,8 +48,8 @@ inline size_t seg_payload_words(const Geometry& g) {
   const int64_t segs = g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len);
   return (size_t)segs * g.Dp / g.NB * MODES_PER_GROUP * 2;
 }
-// segments of the single-kernel forward: the work-groups of one wave over the
-// 256 compute units of an MI355X
+// segments of the single-kernel forward: one work-group per compute unit of an
+// MI355X (256)
 constexpr int64_t SEG_TARGET = 256;
 
 Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) {
@@ -65,7 +65,8 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
   g.Mp = MODES_PER_GROUP * g.MG;
   g.P = L > 0 ? (L + TILE_T - 1) / TILE_T : 0;
   g.last_len = L > 0 ? (int)(L - (g.P - 1) * TILE_T) : 0;
-  // single-kernel forward: about SEG_TARGET segments over all rows (one work-group per CU)
+  // single-kernel forward: about SEG_TARGET segments over all rows, so that all
+  // of them are resident at once
   const int64_t tiles = B * g.NB * g.P;
   g.seg_len = tiles > 0 ? (int)((tiles + SEG_TARGET - 1) / SEG_TARGET) : 1;
   if (g.seg_len > g.P) g.seg_len = (int)(g.P > 0 ? g.P : 1);

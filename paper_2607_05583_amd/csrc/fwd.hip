@@ -11,10 +11,11 @@
 // where H_m[n] is the state entering chunk n.  Per channel the three products
 // are 16x16 MFMAs whose 16 columns are the chunks of one tile (256 steps); all
 // chunks share the per-channel matrices because the filter is time invariant.
-// Inside a tile the chunk scan runs one lane per (channel, mode).  Across tiles
-// the state is chained in a single pass (decoupled look-back): each tile
-// publishes the end state of its own drives, then the state entering it,
-// computed from its predecessors' published states.
+// The single-kernel forward (M <= 8) cuts each row into segments of tiles: a
+// segment computes its own end state, combines the published end states of the
+// segments before it into its entering state, and then runs the chunk scan and
+// the output products tile by tile.  With more than 8 modes the same steps run
+// as three kernels (tile aggregates, carry fold, output pass).
 #include "common.h"
 #include "kernels.h"
 #include "tile_io.h"
@@ -867,11 +868,21 @@ __device__ __forceinline__ f4 dpp4(const f4& old, const f4& v) {
   }
   return r;
 }
-// the value of lane i ^ 1 (the other component of a complex number)
-__device__ __forceinline__ float partner(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), DPP_QUAD(1, 0, 3, 2), 0xF,
-                                                            0xF, true));
+
+// One complex multiply-add on the lane's component of a (re, im) lane pair:
+// zr v + zs v' + add, with v' the value of lane i ^ 1 (the other component),
+// zs = -Im z on the re lane and +Im z on the im lane.  The partner product is
+// one fused multiply-add whose first operand is read across the pair (DPP
+// quad_perm [1,0,3,2]); the two wait states ahead of it cover a vector write
+// of v by the instruction just before.
+__device__ __forceinline__ float cfma_pair(float zr, float zs, float v, float add) {
+  float acc = fmaf(zr, v, add);
+  asm("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+      : "+v"(acc)
+      : "v"(v), "v"(zs));
+  return acc;
 }
+
 // Sum over the 16 lanes of each row, in every lane of the row (the same order in
 // every lane, so the copies agree bitwise).
 __device__ __forceinline__ f4 row_sum(f4 v) {
@@ -885,27 +896,82 @@ __device__ __forceinline__ f4 row_sum(f4 v) {
 template <typename TX>
 struct SegGeo {
   static constexpr int DW = tile_channels<TX>();
-  static constexpr int NW = SEG_WAVES;  // waves
-  static constexpr int CW = DW / NW;    // channels per wave (bf16 8, float 4)
+  static constexpr int NW = sizeof(TX) == 2 ? 16 : 8;  // waves
+  static constexpr int CW = DW / NW;    // channels per wave (4)
+  // 16 waves: one channel at a time through the scan (one LDS slot per wave);
+  // 8 waves: four channels at a time (four slots per wave)
+  static constexpr int SLOTS = NW == 16 ? 1 : 4;
   static constexpr int NG = CW / 4;     // operand gathers of 4 channels per wave
   static constexpr int NT = 64 * NW;    // threads
-  static constexpr int NBUF = SEG_BUFS;  // tile buffers; wave b loads the tiles of buffer b
-  static_assert(NBUF < NW, "loading waves and storing waves");
+  // tile buffers; the waves w with w % NBUF == u load the tiles of buffer u
+  static constexpr int NBUF = seg_bufs((int)sizeof(TX));
+  static_assert(NBUF <= NW, "a loading wave per buffer");
 };
 
-// Direct-to-LDS load of a full tile by the calling wave: 32 loads of 16 bytes
-// per lane, 8 rows of 128 bytes each.
+// One 16-byte-per-lane load straight into LDS (64 lanes, 1 KB at lds) from
+// base + off (base wave-uniform, off the lane's byte offset).  Issued as an
+// opaque instruction: the compiler then does not wait for it before every later
+// LDS read of the issuing wave (it cannot tell which buffer a read touches); the
+// kernel waits for its own tiles explicitly (vmcnt) before the barrier that
+// publishes them.
+__device__ __forceinline__ void lds_dma16(const void* base, uint32_t off, const void* lds) {
+  const uint32_t la = (uint32_t)(size_t)(lvoid_t*)lds;
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(la) : "memory");
+}
+
+// Wait until at most n vector memory operations of the wave are outstanding
+// (n <= 15; exp and lgkm counts not waited for).
+__device__ __forceinline__ void wait_vmcnt(int n) {
+  switch (n) {
+#define RES_VMCNT(k) \
+  case k: __builtin_amdgcn_s_waitcnt(0x0F70 | k); break;
+    RES_VMCNT(0) RES_VMCNT(1) RES_VMCNT(2) RES_VMCNT(3) RES_VMCNT(4) RES_VMCNT(5) RES_VMCNT(6) RES_VMCNT(7)
+    RES_VMCNT(8) RES_VMCNT(9) RES_VMCNT(10) RES_VMCNT(11) RES_VMCNT(12) RES_VMCNT(13) RES_VMCNT(14)
+#undef RES_VMCNT
+    default: __builtin_amdgcn_s_waitcnt(0x0F70 | 15); break;
+  }
+}
+
+// 16-byte store of each lane to base + off (base wave-uniform), as an opaque
+// instruction like lds_dma16, so that the compiler keeps the 64-bit base in
+// scalar registers and the lane offset in one vector register.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void st_row16(void* base, uint32_t off, u32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, %2" ::"v"(off), "v"(v), "s"(base) : "memory");
+}
+
+// Direct-to-LDS load of row group g (8 rows of 128 bytes, one 16-byte load
+// per lane) of a full tile by the calling wave.  While the memory system is
+// busy, issuing such a load holds the wave for a while, so a tile's groups are
+// spread over all waves and over their compute.
 template <typename TX>
-__device__ __forceinline__ void dma_tile(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
-                                         int D, int lane) {
+__device__ __forceinline__ void dma_group(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
+                                          int D, int lane, int g) {
   constexpr int XE = (int)sizeof(TX);
-  const char* src = reinterpret_cast<const char*>(x) + ((b * L + t0) * D + d0) * XE;
   const int64_t rowb = (int64_t)D * XE;
-  const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
-#pragma unroll
-  for (int g = 0; g < TILE_T / 8; ++g)
-    __builtin_amdgcn_global_load_lds((gvoid_t*)(src + (int64_t)(8 * g) * rowb + loff),
-                                     (lvoid_t*)(xt + g * XLay<XE>::GRP), 16, 0, 0);
+  const char* src = reinterpret_cast<const char*>(x) + ((b * L + t0) * D + d0) * XE + (int64_t)(8 * g) * rowb;
+  // the lane's offset, recomputed here rather than kept live across the loops
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
+  const uint32_t loff = (uint32_t)((ln >> 3) * rowb) + (ln & 7) * 16;
+  lds_dma16(src, loff, xt + g * XLay<XE>::GRP);
+}
+
+// Row group g of a full output tile from its LDS buffer by the calling wave:
+// a 16-byte row store per lane, read from LDS as an 8-byte pair.
+template <typename TY>
+__device__ __forceinline__ void store_group(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
+                                            int D, int lane, int g) {
+  constexpr int YE = (int)sizeof(TY);
+  const int64_t rowb = (int64_t)D * YE;
+  char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE + (int64_t)(8 * g) * rowb;
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
+  const uint32_t loff = (uint32_t)((ln >> 3) * rowb) + (ln & 7) * 16;
+  const uint2* s = reinterpret_cast<const uint2*>(xt + g * XLay<YE>::GRP + ln * 16);
+  const uint2 u = s[0], w = s[1];
+  const u32x4 v = {u.x, u.y, w.x, w.y};
+  st_row16(dst, loff, v);
 }
 
 // Element copy of a tile that is not full (all threads); zeros outside the tensor.
@@ -922,32 +988,17 @@ __device__ __forceinline__ void copy_tile(char* xt, const TX* x, int64_t b, int6
   }
 }
 
-// Output tile from one LDS buffer (all threads call): full tiles as 16-byte row
-// stores by waves NBUF .. NW-1 (the loading waves keep load-only queues), read
-// from LDS as 8-byte pairs; other tiles as guarded element stores by all threads.
+// Output tile that is not full, from its LDS buffer (all threads): guarded
+// element stores.
 template <typename TY>
-__device__ __forceinline__ void store_tile(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
-                                           int D, bool full, int tid, int wave) {
+__device__ __forceinline__ void store_tile_part(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
+                                                int D, int tid) {
   typedef SegGeo<TY> G;
   constexpr int DW = G::DW, YE = (int)sizeof(TY);
-  const int lane = tid & 63;
-  if (full) {
-    if (wave < G::NBUF) return;
-    char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE;
-    const int64_t rowb = (int64_t)D * YE;
-    const uint32_t loff = (uint32_t)((lane >> 3) * rowb) + (lane & 7) * 16;  // per-lane part
-#pragma unroll
-    for (int g = wave - G::NBUF; g < TILE_T / 8; g += G::NW - G::NBUF) {
-      const uint2* s = reinterpret_cast<const uint2*>(xt + g * XLay<YE>::GRP + lane * 16);
-      const uint2 u = s[0], w = s[1];
-      *reinterpret_cast<uint4*>(dst + (int64_t)(8 * g) * rowb + loff) = make_uint4(u.x, u.y, w.x, w.y);
-    }
-  } else {
-    for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
-      const int t = idx / DW, c = idx % DW;
-      if (t0 + t < L && d0 + c < D)
-        y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + XLay<YE>::off(t) + c * YE);
-    }
+  for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
+    const int t = idx / DW, c = idx % DW;
+    if (t0 + t < L && d0 + c < D)
+      y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + XLay<YE>::off(t) + c * YE);
   }
 }
 
@@ -960,11 +1011,13 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
   __shared__ __align__(16) char xb[NBUF][XLay<XE>::BYTES];  // the segment's tile buffers
-  // per wave: block aggregates of 4 channels [channel][component][block], and the
-  // chunk states of one channel [component][chunk] (rows of HSTR floats)
+  // per wave and slot: the chunk states of one channel [component][chunk]
+  // (rows of HSTR floats) and the block aggregates [component][block]; with
+  // one slot the aggregates sit in the 4 spare floats of each state row
   constexpr int HSTR = 20;
-  __shared__ __align__(16) float s_blk[NW][4][16][4];
-  __shared__ __align__(16) float s_h[NW][4][16 * HSTR];
+  constexpr int SLOTS = G::SLOTS;
+  __shared__ __align__(16) float s_h[NW][SLOTS][16 * HSTR];
+  __shared__ __align__(16) float s_blk_sep[SLOTS == 1 ? 1 : NW][SLOTS][16][4];
   // per (channel, row q), last tile of a row: the drive part of the state at
   // t = L-1, then the state entering its chunk
   __shared__ __align__(16) f4 s_tail[DW * 4], s_hn[DW * 4];
@@ -996,18 +1049,45 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
     return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
   };
   auto scal_of = [&](int k) { return a.scal + (size_t)(d0 + c0 + k) * a.Mp + 2 * lq; };
-  auto tile_full = [&](int t) { return a.fast_io && (pb + t + 1) * TILE_T <= a.L && d0 + DW <= a.D; };
-  // tile t of the segment into buffer u: full tiles by the buffer's own wave
-  // (direct to LDS; that wave issues no stores, so it waits for its tile
-  // exactly); the others are copied by all threads when they are used
-  auto request = [&](int t, int u) {
-    if (t < nt && wave == u && tile_full(t))
-      dma_tile<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, lane);
+  // tiles 0 .. nfull-1 of the segment are full: whole channel block, aligned
+  // rows, all TILE_T steps inside the sequence (only a row's last tile can be short)
+  const int nfull = __builtin_amdgcn_readfirstlane(
+      (a.fast_io && d0 + DW <= a.D) ? ((pb + nt) * TILE_T <= a.L ? nt : nt - 1) : 0);
+  auto tile_full = [&](int t) { return t < nfull; };
+  // Tile t of the segment into buffer u.  Full tiles go straight to LDS, each
+  // wave loading row groups wave, wave + NW, ... (while the memory system is
+  // busy, issuing a load holds the wave; spread over all waves, that time is the
+  // same for each).  Other tiles are copied by all threads when they are used.
+  constexpr int LPT = TILE_T / 8 / NW;  // row groups per wave and tile (loads, stores)
+  // this wave's row group i (< LPT) of tile t into buffer u
+  auto request_group = [&](int t, int u, int i) {
+    if (t < nt && tile_full(t))
+      dma_group<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, lane, wave + NW * i);
   };
-  // make tile t in buffer u usable: wait for its load, or copy it; the caller synchronises
-  auto arrive = [&](int t, int u) {
+  auto request = [&](int t, int u) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i) request_group(t, u, i);
+  };
+  // the row groups a wave issues after its channel k: i with i CW / LPT == k
+  auto groups_at = [&](int k, auto&& f) {
+#pragma unroll
+    for (int i = 0; i < LPT; ++i)
+      if ((i * CW) / LPT == k) f(i);
+  };
+  auto full_in = [&](int lo, int hi) {  // full tiles among lo .. hi
+    int n = 0;
+    for (int u = lo; u <= hi; ++u) n += tile_full(u) ? 1 : 0;
+    return n;
+  };
+  // Make tile t in buffer u usable: wait for this wave's share of it, or copy
+  // it; the caller synchronises.  `later` full tiles have been requested after
+  // tile t.  Loads complete in order, so while a load of tile t is pending, so
+  // are the LPT * later loads issued after it: vmcnt(LPT * later) waits for
+  // tile t exactly (pending stores only raise the count, which errs on the
+  // side of waiting).
+  auto arrive = [&](int t, int u, int later) {
     if (tile_full(t)) {
-      if (wave == u) __builtin_amdgcn_s_waitcnt(0);
+      wait_vmcnt(LPT * later);
     } else {
       copy_tile<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, tid);
     }
@@ -1032,6 +1112,15 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   // follows tile t - NBUF into its buffer.
   const int R = nt < NBUF ? nt : NBUF;
   auto buf2 = [&](int t) { return (nt - 1 - (t % NBUF)) % NBUF; };
+  // block aggregate slot of (channel slot kk, component i): 4 floats
+  auto blk = [&](int kk, int i) -> float* {
+    if (SLOTS == 1) return &s_h[wave][0][i * HSTR + 16];
+    return &s_blk_sep[wave][kk][i][0];
+  };
+  // The operand loads above are complete before the first tile is requested:
+  // the compiler does not see the tile loads, and a wait it places for an
+  // operand inside the loops would also wait for them.
+  __builtin_amdgcn_s_waitcnt(0);
   for (int j = 0; j < NBUF && j < nt; ++j) request(nt - 1 - j, j);
 
   // ---- pass 1: the segment's own end state ---------------------------------
@@ -1043,9 +1132,13 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
     for (int k = 0; k < CW; ++k) sagg[k] = zero;
     for (int j = 0; j < nt; ++j) {
       const int t = nt - 1 - j;
-      arrive(t, j % NBUF);
+      // visits requested so far: 0 .. NBUF-1, then one more per visit from the second on
+      const int last = min((j == 0 ? NBUF - 1 : j + NBUF - 2), nt - 1);
+      arrive(t, j % NBUF, full_in(nt - 1 - last, t - 1));
       __syncthreads();  // tile t is in; the buffer of the tile visited before it is free
-      if (j >= 1 && j + NBUF - 1 < nt) request(nt - j - NBUF, (j + NBUF - 1) % NBUF);
+      // the next request (into the buffer of the tile visited before), spread over the channels
+      const bool req = j >= 1 && j + NBUF - 1 < nt;
+      const int rt = nt - j - NBUF, ru = (j + NBUF - 1) % NBUF;
       const char* xt = xb[j % NBUF];
 #pragma unroll
       for (int gr = 0; gr < NG; ++gr) {
@@ -1056,6 +1149,7 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
           const int k = 4 * gr + kk;
           sagg[k] = c2fma(ww[k], PT::mma(vop[k], xv[kk], zero), sagg[k]);
           ww[k] = c2mul(ww[k], lt[k]);
+          if (req) groups_at(k, [&](int i) { request_group(rt, ru, i); });
         }
       }
       if (pb + t == a.P - 1 && a.h_out != nullptr && ln == nstar) {
@@ -1171,15 +1265,37 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
     m4s[k] = sgn * z4.y;
   }
   // z v + (partner): one complex multiply-add on the lane's component
-  auto cstep = [](float zr, float zs, float v, float add) {
-    return fmaf(zr, v, fmaf(zs, partner(v), add));
-  };
+  auto cstep = [](float zr, float zs, float v, float add) { return cfma_pair(zr, zs, v, add); };
+  // At the top of tile t (after the barrier) all threads store tile t-1's
+  // outputs from its buffer, and the buffer whose stores were issued one tile
+  // earlier (all waves have since passed a barrier, so its LDS reads are done)
+  // takes the next tile.  With float32 outputs leaving from the MFMA registers,
+  // tile t-1's buffer is free at once.
+  constexpr int LAG = SEPY ? 1 : 2;
+  // (pass 2's operands are in registers before its first tile load; the wait
+  // also covers the loads of the carry phase)
+  __builtin_amdgcn_s_waitcnt(0);
   for (int t = 0; t < nt; ++t) {
-    if (t >= R) arrive(t, buf2(t));  // tiles 0 .. R-1 are still in their buffers from pass 1
-    // tile t is in; tile t-1's buffer has been read for its stores, so tile
-    // t-1+NBUF may follow into it
-    __syncthreads();
-    if (t >= 1) request(t - 1 + NBUF, buf2(t - 1));
+    // tiles 0 .. R-1 are still in their buffers from pass 1; before tile t,
+    // tiles up to t - 1 - LAG + NBUF have been requested
+    if (t >= R) arrive(t, buf2(t), full_in(t + 1, min(t - 1 - LAG + NBUF, nt - 1)));
+    __syncthreads();  // tile t is in; tile t-1's outputs are in its buffer
+    // tile t-1's stores and the next request, spread over the channels (a tile
+    // that is not full is stored here by all threads)
+    const bool stf = !SEPY && t >= 1 && tile_full(t - 1);
+    if (!SEPY && t >= 1 && !tile_full(t - 1))
+      store_tile_part<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(t - 1)], b, (pb + t - 1) * TILE_T, d0, a.L, a.D,
+                          tid);
+    const bool req = t >= LAG;
+    const int rt = t - LAG + NBUF, ru = req ? buf2(t - LAG) : 0;
+    auto side = [&](int k) {
+      groups_at(k, [&](int i) {
+        if (stf)
+          store_group<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(t - 1)], b, (pb + t - 1) * TILE_T, d0, a.L, a.D,
+                          lane, wave + NW * i);
+        if (req) request_group(rt, ru, i);
+      });
+    };
     char* xt = xb[buf2(t)];
     const int64_t p = pb + t;
 #pragma unroll
@@ -1187,6 +1303,47 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
       typename PT::XOp xv[4];
       PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
       f4 st[4], acc[4];
+      // y of channel k from its transposed states: lane (n, q) takes components
+      // 4q .. 4q+3 of chunk n
+      auto apply = [&](int kk, int k, const float* sh) {
+        f4 hb;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) hb[j] = sh[(4 * lq + j) * HSTR + ln];
+        acc[kk] = PT::mma_u(uop[k], hb, PT::mma(top[k], xv[kk], zero));
+        if (p == a.P - 1 && ln == nstar) s_hn[(c0 + k) * 4 + lq] = hb;  // state entering chunk nstar
+      };
+      if (SLOTS == 1) {
+        // one channel at a time: block aggregates, block entry states, chunk
+        // entry states, then y through the transpose slot
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int k = 4 * gr + kk;
+          const f4 sk = PT::mma_t(xv[kk], vop[k], zero);
+          float ag = sk[0];
+#pragma unroll
+          for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, sk[r]);
+          wave_lds_order();
+          blk(0, ln)[lq] = ag;
+          wave_lds_order();
+          const f4 A = *reinterpret_cast<const f4*>(blk(0, ln));
+          float e = cin[k], eq = e;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            e = cstep(m4r[k], m4s[k], e, A[q]);
+            if (lq == q + 1) eq = e;
+          }
+          cin[k] = e;
+          f4 h;
+          h[0] = eq;
+#pragma unroll
+          for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], sk[r - 1]);
+          wave_lds_order();
+          *reinterpret_cast<f4*>(&s_h[wave][0][ln * HSTR + 4 * lq]) = h;
+          wave_lds_order();
+          apply(kk, k, s_h[wave][0]);
+          side(k);
+        }
+      } else {
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int k = 4 * gr + kk;
@@ -1194,13 +1351,14 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
         float ag = st[kk][0];
 #pragma unroll
         for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, st[kk][r]);
-        s_blk[wave][kk][ln][lq] = ag;  // A_lq of component ln
+        blk(kk % SLOTS, ln)[lq] = ag;  // A_lq of component ln
+        side(k);
       }
       wave_lds_order();
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         const int k = 4 * gr + kk;
-        const f4 A = *reinterpret_cast<const f4*>(&s_blk[wave][kk][ln][0]);
+        const f4 A = *reinterpret_cast<const f4*>(blk(kk % SLOTS, ln));
         // block entry states: E_0 = c, E_{q+1} = mu^4 E_q + A_q; E_4 enters the next tile
         float e = cin[k], eq = e;
 #pragma unroll
@@ -1214,18 +1372,11 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
         h[0] = eq;
 #pragma unroll
         for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], st[kk][r - 1]);
-        *reinterpret_cast<f4*>(&s_h[wave][kk][ln * HSTR + 4 * lq]) = h;
+        *reinterpret_cast<f4*>(&s_h[wave][kk % SLOTS][ln * HSTR + 4 * lq]) = h;
       }
       wave_lds_order();
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int k = 4 * gr + kk;
-        // lane (n, q) takes components 4q .. 4q+3 of chunk n
-        f4 hb;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) hb[j] = s_h[wave][kk][(4 * lq + j) * HSTR + ln];
-        acc[kk] = PT::mma_u(uop[k], hb, PT::mma(top[k], xv[kk], zero));
-        if (p == a.P - 1 && ln == nstar) s_hn[(c0 + k) * 4 + lq] = hb;  // state entering chunk nstar
+      for (int kk = 0; kk < 4; ++kk) apply(kk, 4 * gr + kk, s_h[wave][kk % SLOTS]);
       }
       wave_lds_order();
       if (SEPY)
@@ -1234,9 +1385,18 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
       else
         put_y4<TY>(xt, c0 + 4 * gr, ln, lq, acc);
     }
-    __syncthreads();  // tile t's outputs are in its buffer
-    if (!SEPY)
-      store_tile<TY>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, tile_full(t), tid, wave);
+  }
+  __syncthreads();  // the last tile's outputs are in its buffer
+  if (!SEPY) {
+    if (tile_full(nt - 1)) {
+#pragma unroll
+      for (int i = 0; i < LPT; ++i)
+        store_group<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(nt - 1)], b, (pb + nt - 1) * TILE_T, d0, a.L, a.D,
+                        lane, wave + NW * i);
+    } else {
+      store_tile_part<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(nt - 1)], b, (pb + nt - 1) * TILE_T, d0, a.L, a.D,
+                          tid);
+    }
   }
   if (pb + nt == a.P && a.h_out != nullptr && lane < 4 * CW) {
     // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar,

@@ -9,10 +9,10 @@ namespace res {
 
 enum { MODE_STATE = 0, MODE_APPLY = 1 };
 
-// waves per work-group of the single-kernel forward (each publishes its own sub-chain)
-constexpr int SEG_WAVES = 8;
-// LDS tile buffers of the single-kernel forward
-constexpr int SEG_BUFS = 3;
+// LDS tile buffers of the single-kernel forward work-group, by activation size
+// (bf16: 16 waves, 4 buffers; float32: 8 waves, 3 buffers)
+constexpr int seg_bufs(int elem_bytes) { return elem_bytes == 2 ? 4 : 3; }
+
 
 struct FwdArgs {
   const void* x;
