@@ -99,30 +99,37 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     mc.mu8 = lH;
     cc[(size_t)d * Mp + m] = mc;
   }
-  if (mpow != nullptr)  // lambda^(16 j), j = 0..15, as [d][j][Mp]
-    for (int t = threadIdx.x; t < CHUNK * Mp; t += blockDim.x) {
-      const int j = t / Mp, m = t % Mp;
-      float2 z = make_float2(0.f, 0.f);
-      if (dvalid && m < M) {
-        double sn, cs;
-        sincos((double)omega[d * M + m] * (CHUNK * j), &sn, &cs);
-        const double e = exp(-(double)gamma[d * M + m] * (CHUNK * j));
-        z = make_float2((float)(e * cs), (float)(e * sn));
+  // lambda^(16 j), j = 0..15, as [d][j][Mp], and lambda^(seg_steps n), n =
+  // 0..16, as [d][n][Mp]: float64 powers of mu = lambda^16 and of
+  // lambda^seg_steps (the latter evaluated directly), by repeated products
+  // (at most 16 roundings of 2^-53 each)
+  for (int t = threadIdx.x; t < 2 * Mp; t += blockDim.x) {
+    const int m = t % Mp;
+    const bool valid = dvalid && m < M;
+    if (t < Mp) {
+      if (mpow == nullptr) continue;
+      const double2 mu = pw[m][CHUNK];
+      double2 z = make_double2(valid ? 1.0 : 0.0, 0.0);
+      for (int j = 0; j < CHUNK; ++j) {
+        mpow[((size_t)d * CHUNK + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
+        z = zmul(z, mu);
       }
-      mpow[((size_t)d * CHUNK + j) * Mp + m] = z;
-    }
-  if (spow != nullptr)  // lambda^(seg_steps n), n = 0..16, as [d][n][Mp]
-    for (int t = threadIdx.x; t < (CHUNK + 1) * Mp; t += blockDim.x) {
-      const int n = t / Mp, m = t % Mp;
-      float2 z = make_float2(0.f, 0.f);
-      if (dvalid && m < M) {
+    } else {
+      if (spow == nullptr) continue;
+      double2 ls = make_double2(0.0, 0.0);
+      if (valid) {
         double sn, cs;
-        sincos((double)omega[d * M + m] * ((double)seg_steps * n), &sn, &cs);
-        const double e = exp(-(double)gamma[d * M + m] * ((double)seg_steps * n));
-        z = make_float2((float)(e * cs), (float)(e * sn));
+        sincos((double)omega[d * M + m] * (double)seg_steps, &sn, &cs);
+        const double e = exp(-(double)gamma[d * M + m] * (double)seg_steps);
+        ls = make_double2(e * cs, e * sn);
       }
-      spow[((size_t)d * (CHUNK + 1) + n) * Mp + m] = z;
+      double2 z = make_double2(valid ? 1.0 : 0.0, 0.0);
+      for (int n = 0; n <= CHUNK; ++n) {
+        spow[((size_t)d * (CHUNK + 1) + n) * Mp + m] = make_float2((float)z.x, (float)z.y);
+        z = zmul(z, ls);
+      }
     }
+  }
   for (int tau = threadIdx.x; tau <= CHUNK; tau += blockDim.x) {  // K[tau] = Re sum_m c lambda^tau
     double s = 0.0;
     for (int m = 0; m < Mp; ++m) s += cm[m].x * pw[m][tau].x - cm[m].y * pw[m][tau].y;
@@ -375,23 +382,18 @@ template <> struct FPath<bf16_t> {
     c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.lo, bh, c, 0, 0, 0);
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.hi, bl, c, 0, 0, 0);
   }
-  // the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4), one 8-byte read per row
+  // the 4 consecutive channels ch0 .. ch0+3 (ch0 a multiple of 4): element r of
+  // channel c from row r (the compiler reads each row once and packs with byte
+  // permutes)
   __device__ static __forceinline__ void gather4(const char* xt, int ch0, int n, int q, XOp (&xv)[4]) {
     const char* p = xt + (2 * n + (q >> 1)) * XLay<2>::GRP + 4 * (q & 1) * XROW + ch0 * 2;
-    uint2 w[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const uint2*>(p + r * XROW);
-    // channel c of row r is the (c & 1) half of word c >> 1 of w[r]
+    typedef unsigned short us4 __attribute__((ext_vector_type(4)));
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      uint32_t o[2];
+      us4 v;
 #pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const uint32_t lo = (c >> 1) ? w[2 * j].y : w[2 * j].x;
-        const uint32_t hi = (c >> 1) ? w[2 * j + 1].y : w[2 * j + 1].x;
-        o[j] = (c & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      xv[c] = __builtin_bit_cast(s4, make_uint2(o[0], o[1]));
+      for (int r = 0; r < 4; ++r) v[r] = *reinterpret_cast<const unsigned short*>(p + r * XROW + c * 2);
+      xv[c] = __builtin_bit_cast(s4, v);
     }
   }
 };
@@ -1012,12 +1014,11 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   constexpr bool SEPY = !__is_same(TX, TY);
   __shared__ __align__(16) char xb[NBUF][XLay<XE>::BYTES];  // the segment's tile buffers
   // per wave and slot: the chunk states of one channel [component][chunk]
-  // (rows of HSTR floats) and the block aggregates [component][block]; with
-  // one slot the aggregates sit in the 4 spare floats of each state row
+  // (rows of HSTR floats) and, in the 4 spare floats of each row, the block
+  // aggregates [component][block]
   constexpr int HSTR = 20;
   constexpr int SLOTS = G::SLOTS;
   __shared__ __align__(16) float s_h[NW][SLOTS][16 * HSTR];
-  __shared__ __align__(16) float s_blk_sep[SLOTS == 1 ? 1 : NW][SLOTS][16][4];
   // per (channel, row q), last tile of a row: the drive part of the state at
   // t = L-1, then the state entering its chunk
   __shared__ __align__(16) f4 s_tail[DW * 4], s_hn[DW * 4];
@@ -1113,10 +1114,7 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   const int R = nt < NBUF ? nt : NBUF;
   auto buf2 = [&](int t) { return (nt - 1 - (t % NBUF)) % NBUF; };
   // block aggregate slot of (channel slot kk, component i): 4 floats
-  auto blk = [&](int kk, int i) -> float* {
-    if (SLOTS == 1) return &s_h[wave][0][i * HSTR + 16];
-    return &s_blk_sep[wave][kk][i][0];
-  };
+  auto blk = [&](int j, int i) -> float* { return &s_h[wave][j][i * HSTR + 16]; };
   // The operand loads above are complete before the first tile is requested:
   // the compiler does not see the tile loads, and a wait it places for an
   // operand inside the loops would also wait for them.
@@ -1302,7 +1300,7 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
     for (int gr = 0; gr < NG; ++gr) {
       typename PT::XOp xv[4];
       PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
-      f4 st[4], acc[4];
+      f4 acc[4];
       // y of channel k from its transposed states: lane (n, q) takes components
       // 4q .. 4q+3 of chunk n
       auto apply = [&](int kk, int k, const float* sh) {
@@ -1312,20 +1310,28 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
         acc[kk] = PT::mma_u(uop[k], hb, PT::mma(top[k], xv[kk], zero));
         if (p == a.P - 1 && ln == nstar) s_hn[(c0 + k) * 4 + lq] = hb;  // state entering chunk nstar
       };
-      if (SLOTS == 1) {
-        // one channel at a time: block aggregates, block entry states, chunk
-        // entry states, then y through the transpose slot
+      // SLOTS channels at a time: block aggregates (A_q, into the spare
+      // columns of the channel's slot), block entry states E_q, chunk entry
+      // states (into the slot, transposed on the way out), then y
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int k = 4 * gr + kk;
-          const f4 sk = PT::mma_t(xv[kk], vop[k], zero);
-          float ag = sk[0];
+      for (int k0 = 0; k0 < 4; k0 += SLOTS) {
+        f4 sk[SLOTS];
 #pragma unroll
-          for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, sk[r]);
-          wave_lds_order();
-          blk(0, ln)[lq] = ag;
-          wave_lds_order();
-          const f4 A = *reinterpret_cast<const f4*>(blk(0, ln));
+        for (int j = 0; j < SLOTS; ++j) {
+          const int kk = k0 + j, k = 4 * gr + kk;
+          sk[j] = PT::mma_t(xv[kk], vop[k], zero);
+          float ag = sk[j][0];
+#pragma unroll
+          for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, sk[j][r]);
+          blk(j, ln)[lq] = ag;  // A_lq of component ln
+          side(k);
+        }
+        wave_lds_order();
+#pragma unroll
+        for (int j = 0; j < SLOTS; ++j) {
+          const int kk = k0 + j, k = 4 * gr + kk;
+          const f4 A = *reinterpret_cast<const f4*>(blk(j, ln));
+          // E_0 = c, E_{q+1} = mu^4 E_q + A_q; E_4 enters the next tile
           float e = cin[k], eq = e;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
@@ -1333,50 +1339,17 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
             if (lq == q + 1) eq = e;
           }
           cin[k] = e;
+          // states entering chunks 4 lq .. 4 lq + 3
           f4 h;
           h[0] = eq;
 #pragma unroll
-          for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], sk[r - 1]);
-          wave_lds_order();
-          *reinterpret_cast<f4*>(&s_h[wave][0][ln * HSTR + 4 * lq]) = h;
-          wave_lds_order();
-          apply(kk, k, s_h[wave][0]);
-          side(k);
+          for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], sk[j][r - 1]);
+          *reinterpret_cast<f4*>(&s_h[wave][j][ln * HSTR + 4 * lq]) = h;
         }
-      } else {
+        wave_lds_order();
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int k = 4 * gr + kk;
-        st[kk] = PT::mma_t(xv[kk], vop[k], zero);
-        float ag = st[kk][0];
-#pragma unroll
-        for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, st[kk][r]);
-        blk(kk % SLOTS, ln)[lq] = ag;  // A_lq of component ln
-        side(k);
-      }
-      wave_lds_order();
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int k = 4 * gr + kk;
-        const f4 A = *reinterpret_cast<const f4*>(blk(kk % SLOTS, ln));
-        // block entry states: E_0 = c, E_{q+1} = mu^4 E_q + A_q; E_4 enters the next tile
-        float e = cin[k], eq = e;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          e = cstep(m4r[k], m4s[k], e, A[q]);
-          if (lq == q + 1) eq = e;
-        }
-        cin[k] = e;
-        // states entering chunks 4 lq .. 4 lq + 3, into the channel's transpose slot
-        f4 h;
-        h[0] = eq;
-#pragma unroll
-        for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], st[kk][r - 1]);
-        *reinterpret_cast<f4*>(&s_h[wave][kk % SLOTS][ln * HSTR + 4 * lq]) = h;
-      }
-      wave_lds_order();
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) apply(kk, 4 * gr + kk, s_h[wave][kk % SLOTS]);
+        for (int j = 0; j < SLOTS; ++j) apply(k0 + j, 4 * gr + k0 + j, s_h[wave][j]);
+        wave_lds_order();
       }
       wave_lds_order();
       if (SEPY)
