@@ -1037,6 +1037,12 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   if (tid == 0) s_tk = atomicAdd(a.ticket, 1u);
   __syncthreads();
   const int64_t tk = (int64_t)__builtin_amdgcn_readfirstlane(s_tk);
+  // a ticket past the last segment means the counter was not reset for this
+  // launch: flag it and touch nothing (uniform over the work-group)
+  if (tk >= (int64_t)nchains * a.seg_per_chain) {
+    if (tid == 0) atomicOr(a.error, 2u);
+    return;
+  }
   const int64_t seg = tk / nchains;
   const int chain = (int)(tk % nchains);
   const int64_t b = chain / a.NB;

@@ -36,7 +36,7 @@ struct FwdArgs {
   // single-kernel forward: segments of seg_len tiles, ticket order time-major over chains
   int seg_len, seg_per_chain;
   uint32_t* ticket;  // segment ticket counter
-  uint32_t* error;   // set when a bounded wait gives up
+  uint32_t* error;   // bit 0: a bounded wait gave up; bit 1: a ticket past the last segment
   float2* pay_agg;   // per (segment, wave) [channels][8 modes]: the segment's own end state
 };
 
