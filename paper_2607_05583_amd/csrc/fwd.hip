@@ -1052,8 +1052,12 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   const bool last_seg = (seg == a.seg_per_chain - 1);
   const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
 
+  // the lane's operand rows (the lane offset recomputed at each use rather than
+  // kept live in a 64-bit register)
   auto tab_of = [&](int k) {
-    return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+    int l = lane;
+    asm volatile("" : "+v"(l));
+    return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + (uint32_t)l * TAB_LANE_BYTES;
   };
   auto scal_of = [&](int k) { return a.scal + (size_t)(d0 + c0 + k) * a.Mp + 2 * lq; };
   // tiles 0 .. nfull-1 of the segment are full: whole channel block, aligned
@@ -1187,6 +1191,19 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   const int64_t sub = tk * NW + wave;
   // payload of sub-chain s, channel k: 8 modes as float2; the lane's pair at 2 lq
   auto pay = [&](int64_t s, int k) { return ((size_t)s * CW + k) * MODES_PER_GROUP + 2 * lq; };
+  // pass 2's T and U operands and chunk multipliers, requested now (ahead of
+  // the publishing stores, whose completion later loads of the wave wait for)
+  // so that their latency overlaps the wait for the predecessors
+  typename PT::AOp top[CW];
+  typename PT::UOp uop[CW];
+  float2 z1[CW], z4[CW];
+#pragma unroll
+  for (int k = 0; k < CW; ++k) {
+    top[k] = PT::load_a(tab_of(k));
+    uop[k] = PT::u_op(load_f4(tab_of(k) + 2 * TAB_MAT_BYTES));
+    z1[k] = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 1) * a.Mp + (ln >> 1)];
+    z4[k] = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 4) * a.Mp + (ln >> 1)];
+  }
   if (!last_seg && ln == 0)  // publish this segment's own end state
 #pragma unroll
     for (int k = 0; k < CW; ++k) st_agent4(a.pay_agg + pay(sub, k), sagg[k]);
@@ -1229,7 +1246,9 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
             if (2 * lq + 1 < a.M) v[k][2] = h[2], v[k][3] = h[3];
           }
         }
-        carry[k] = c2fma(spw(k, CHUNK), carry[k], row_sum(c2mul(spw(k, ln), v[k])));
+        const f4 blk_sum = row_sum(c2mul(spw(k, ln), v[k]));
+        // (the farthest block starts from zero)
+        carry[k] = blk == seg / CHUNK ? blk_sum : c2fma(spw(k, CHUNK), carry[k], blk_sum);
       }
     }
   }
@@ -1243,8 +1262,6 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   // chunk states from E_q, and their transpose through LDS into the B operand
   // of y += U H.  A complex factor z acts on a component v with partner p as
   // Re z v + s Im z p, s = -1 for the real part and +1 for the imaginary part.
-  typename PT::AOp top[CW];
-  typename PT::UOp uop[CW];
   float cin[CW], m1r[CW], m1s[CW], m4r[CW], m4s[CW];
   // the entering state as component ln (the fold leaves modes 2 lq, 2 lq + 1 in row lq)
   if (ln == 0)
@@ -1257,16 +1274,11 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
 #pragma unroll
   for (int k = 0; k < CW; ++k) {
     vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);  // (not held through the carry phase)
-    top[k] = PT::load_a(tab_of(k));
-    uop[k] = PT::u_op(load_f4(tab_of(k) + 2 * TAB_MAT_BYTES));
-    const int m = ln >> 1;
     const float sgn = (ln & 1) ? 1.f : -1.f;
-    const float2 z1 = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 1) * a.Mp + m];
-    const float2 z4 = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 4) * a.Mp + m];
-    m1r[k] = z1.x;
-    m1s[k] = sgn * z1.y;
-    m4r[k] = z4.x;
-    m4s[k] = sgn * z4.y;
+    m1r[k] = z1[k].x;
+    m1s[k] = sgn * z1[k].y;
+    m4r[k] = z4[k].x;
+    m4s[k] = sgn * z4[k].y;
   }
   // z v + (partner): one complex multiply-add on the lane's component
   auto cstep = [](float zr, float zs, float v, float add) { return cfma_pair(zr, zs, v, add); };
