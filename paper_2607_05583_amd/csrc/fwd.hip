@@ -370,14 +370,20 @@ template <> struct FPath<bf16_t> {
     return r;
   }
   __device__ static __forceinline__ f4 mma_u(const UOp& u, const f4& h, f4 c) {
-    typedef __bf16 b4 __attribute__((ext_vector_type(4)));
-    b4 hh, hl;
+    // pairs rounded together; the float value of each rounded half read back
+    // from the packed word (low half: shift, high half: mask)
+    typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    uint32_t ph[2], pl[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      hh[i] = (__bf16)h[i];
-      hl[i] = (__bf16)(h[i] - (float)hh[i]);
+    for (int i = 0; i < 2; ++i) {
+      const b2 hi = {(__bf16)h[2 * i], (__bf16)h[2 * i + 1]};
+      ph[i] = __builtin_bit_cast(uint32_t, hi);
+      const b2 lo = {(__bf16)(h[2 * i] - __uint_as_float(ph[i] << 16)),
+                     (__bf16)(h[2 * i + 1] - __uint_as_float(ph[i] & 0xFFFF0000u))};
+      pl[i] = __builtin_bit_cast(uint32_t, lo);
     }
-    const s4 bh = __builtin_bit_cast(s4, hh), bl = __builtin_bit_cast(s4, hl);
+    const s4 bh = __builtin_bit_cast(s4, make_uint2(ph[0], ph[1]));
+    const s4 bl = __builtin_bit_cast(s4, make_uint2(pl[0], pl[1]));
     c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.hi, bh, c, 0, 0, 0);
     c = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.lo, bh, c, 0, 0, 0);
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(u.hi, bl, c, 0, 0, 0);
@@ -875,11 +881,12 @@ __device__ __forceinline__ f4 dpp4(const f4& old, const f4& v) {
 // zr v + zs v' + add, with v' the value of lane i ^ 1 (the other component),
 // zs = -Im z on the re lane and +Im z on the im lane.  The partner product is
 // one fused multiply-add whose first operand is read across the pair (DPP
-// quad_perm [1,0,3,2]); the two wait states ahead of it cover a vector write
-// of v by the instruction just before.
+// quad_perm [1,0,3,2]).  A DPP read needs two wait states after a vector
+// write of its source: the multiply-add on v, which must come between any
+// write of v and this instruction, is one, the s_nop the other.
 __device__ __forceinline__ float cfma_pair(float zr, float zs, float v, float add) {
   float acc = fmaf(zr, v, add);
-  asm("s_nop 1\n\tv_fmac_f32_dpp %0, %1, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+  asm("s_nop 0\n\tv_fmac_f32_dpp %0, %1, %2 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
       : "+v"(acc)
       : "v"(v), "v"(zs));
   return acc;
