@@ -1295,6 +1295,7 @@ __global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
   // takes the next tile.  With float32 outputs leaving from the MFMA registers,
   // tile t-1's buffer is free at once.
   constexpr int LAG = SEPY ? 1 : 2;
+  static_assert(NBUF > LAG, "a tile is requested before the tile that follows it into its buffer arrives");
   // (pass 2's operands are in registers before its first tile load; the wait
   // also covers the loads of the carry phase)
   __builtin_amdgcn_s_waitcnt(0);
