@@ -12,7 +12,8 @@ writes the few figures that the benchmark line cites:
                 size in the same process (``bench.py --counters``).
 
 Usage:
-  python -m paper_2607_05583_amd.profiling kernel-trace DB_DIR OUT.md --command "..."
+  python -m paper_2607_05583_amd.profiling kernel-trace DB_DIR OUT.md --command "..." \
+      [--prefill-launches N]
   python -m paper_2607_05583_amd.profiling traffic FETCH_DIR WRITE_DIR OUT.json \
       --copy-bytes N --command "..."
 """
@@ -62,7 +63,14 @@ def kernel_rows(db_path: str):
                  max_us=r[6] / 1e3, total_us=r[7] / 1e3) for r in cur.execute(q)]
 
 
-def write_kernel_trace(db_dir: str, out: str, command: str, top: int = 20):
+def first_launches(db_path: str, pattern: str, n: int):
+    """Durations (us) of the first n launches of the kernels matching pattern, in launch order."""
+    cur = _db(db_path).cursor()
+    q = "select duration from kernels where name like ? order by start limit ?"
+    return [r[0] / 1e3 for r in cur.execute(q, (f"%{pattern}%", n))]
+
+
+def write_kernel_trace(db_dir: str, out: str, command: str, top: int = 20, prefill_launches: int = 0):
     rows = kernel_rows(db_dir)
     tot = sum(r["total_us"] for r in rows)
     lines = ["# rocprofv3 kernel trace", "", "Command (from the repository root, on one MI355X):", "",
@@ -74,6 +82,13 @@ def write_kernel_trace(db_dir: str, out: str, command: str, top: int = 20):
                      f"{r['avg_us']:.2f} | {r['min_us']:.2f} | {r['max_us']:.2f} | "
                      f"{100 * r['total_us'] / tot:.1f} |")
     lines.append("")
+    if prefill_launches > 0:
+        # the bench runs the prefill first: its warmup and timed launches are the
+        # first ones of the forward kernel (later ones belong to other workloads)
+        d = first_launches(db_dir, FUSED, prefill_launches)
+        lines += [f"Prefill workload only (the first {len(d)} `{FUSED}` launches: warm-up and timed steps):",
+                  "", "| launches | avg us | min us | max us |", "|---:|---:|---:|---:|",
+                  f"| {len(d)} | {sum(d) / len(d):.2f} | {min(d):.2f} | {max(d):.2f} |", ""]
     with open(out, "w") as f:
         f.write("\n".join(lines))
     return rows
@@ -131,6 +146,8 @@ def main():
     a.add_argument("db_dir")
     a.add_argument("out")
     a.add_argument("--command", required=True)
+    a.add_argument("--prefill-launches", type=int, default=0,
+                   help="also summarise the first N launches of the forward kernel (the prefill)")
     b = sub.add_parser("traffic")
     b.add_argument("fetch_dir")
     b.add_argument("write_dir")
@@ -139,7 +156,8 @@ def main():
     b.add_argument("--command", required=True)
     args = ap.parse_args()
     if args.cmd == "kernel-trace":
-        for r in write_kernel_trace(args.db_dir, args.out, args.command)[:8]:
+        for r in write_kernel_trace(args.db_dir, args.out, args.command,
+                                    prefill_launches=args.prefill_launches)[:8]:
             print(f"{short_name(r['name'])[:60]:60s} grid {r['grid']:>8} n {r['calls']:>6} avg {r['avg_us']:.2f} us")
     else:
         print(json.dumps(write_traffic(args.fetch_dir, args.write_dir, args.out, args.command,
