@@ -302,24 +302,47 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const float* __restrict__ h0, float* __restrict__ dgamma, float* __restrict__ domega,
     float* __restrict__ damp, float* __restrict__ dphase, float* __restrict__ dh0, int B,
     int64_t P, int D, int M, int Dp, int Mp) {
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= D * M) return;
-  const int d = idx / M, m = idx % M;
+  // One block per channel d.  The ps columns of the per-tile partial rows of d
+  // are summed over the B P tiles in float64: thread (row group rg, column col)
+  // takes tiles rg, rg + NRG, ... in order (two interleaved accumulators, so that
+  // loads overlap), then the row groups are added in order.  The order is fixed,
+  // so the result is bitwise reproducible.
+  const int d = blockIdx.x;
   const int ps = part_stride(Mp);
+  const int nrg = blockDim.x / ps;
+  const int64_t nbp = (int64_t)B * P;
+  __shared__ double s_acc[256];
+  __shared__ double s_col[16 + 4 * MODES_PER_GROUP * MG_MAX];
+  {
+    const int col = threadIdx.x % ps, rg = threadIdx.x / ps;
+    double acc = 0.0;
+    if (rg < nrg) {
+      double a0 = 0.0, a1 = 0.0;
+      int64_t bp = rg;
+      for (; bp + nrg < nbp; bp += 2 * nrg) {
+        a0 += part[((size_t)bp * Dp + d) * ps + col];
+        a1 += part[((size_t)(bp + nrg) * Dp + d) * ps + col];
+      }
+      if (bp < nbp) a0 += part[((size_t)bp * Dp + d) * ps + col];
+      acc = a0 + a1;
+    }
+    s_acc[threadIdx.x] = acc;
+  }
+  __syncthreads();
+  for (int col = threadIdx.x; col < ps; col += blockDim.x) {
+    double t = 0.0;
+    for (int rg = 0; rg < nrg; ++rg) t += s_acc[rg * ps + col];
+    s_col[col] = t;
+  }
+  __syncthreads();
+  const int m = threadIdx.x;
+  if (m >= M) return;
+  const int idx = d * M + m;
   double G[16];
 #pragma unroll
-  for (int t = 0; t < 16; ++t) G[t] = 0.0;
-  double Wr = 0, Wi = 0, Rr = 0, Ri = 0;
-  for (int64_t bp = 0; bp < (int64_t)B * P; ++bp) {
-    const float* src = part + ((size_t)bp * Dp + d) * ps;
-#pragma unroll
-    for (int t = 0; t < 16; ++t) G[t] += src[t];
-    const float4 v = *reinterpret_cast<const float4*>(&src[16 + 4 * m]);
-    Wr += v.x;
-    Wi += v.y;
-    Rr += v.z;
-    Ri += v.w;
-  }
+  for (int t = 0; t < 16; ++t) G[t] = s_col[t];
+  double Wr = s_col[16 + 4 * m], Wi = s_col[16 + 4 * m + 1], Rr = s_col[16 + 4 * m + 2],
+         Ri = s_col[16 + 4 * m + 3];
   const double g = gamma[idx], w = omega[idx], a = amp[idx], ph = phase[idx];
 #pragma unroll
   for (int t = 0; t < 16; ++t) {
@@ -401,8 +424,7 @@ hipError_t launch_bwd_reduce(const Geometry& g, const float* part, const float4*
                              const float* gamma, const float* omega, const float* amp,
                              const float* phase, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st) {
-  const int n = (int)(g.D * g.M);
-  hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, part,
+  hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g.D), dim3(256), 0, st, part,
                      q0, gamma, omega, amp, phase, h0, dgamma, domega, damp, dphase, dh0,
                      (int)g.B, g.P, (int)g.D, (int)g.M, g.Dp, g.Mp);
   return hipGetLastError();
