@@ -14,7 +14,7 @@ namespace res {
 constexpr int DEC_CH = 4;
 constexpr int DEC_ROWS = 64;
 
-template <typename TX, typename TY>
+template <typename TX, typename TY, int MF>
 __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
     const TX* __restrict__ x, TY* __restrict__ y, int B, int D, int M,
     const float* __restrict__ gamma, const float* __restrict__ omega,
@@ -23,6 +23,21 @@ __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
   const int tid = threadIdx.x;
   const int d0 = blockIdx.x * DEC_CH;
   const int b0 = blockIdx.y * DEC_ROWS;
+  // MF > 0: M == MF is known, and the thread's state (MF complex modes) and
+  // drive are loaded before the constants are computed, so their latency
+  // overlaps that work
+  float4 hv[MF > 0 ? MF / 2 : 1];
+  float xf = 0.f;
+  if (MF > 0) {
+    const int dlf = tid % DEC_CH, bf = b0 + tid / DEC_CH, df = d0 + dlf;
+    if (bf < B && df < D) {
+      const size_t rowf = (size_t)bf * D + df;
+      xf = to_f32(x[rowf]);
+      const float4* sv = reinterpret_cast<const float4*>(state) + rowf * (MF / 2);
+#pragma unroll
+      for (int i = 0; i < MF / 2; ++i) hv[i] = sv[i];
+    }
+  }
   for (int t = tid; t < DEC_CH * M; t += blockDim.x) {
     const int dl = t / M, m = t % M, d = d0 + dl;
     float2 hi = make_float2(0.f, 0.f), lo = hi, c = hi;
@@ -48,9 +63,29 @@ __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
   const int d = d0 + dl;
   if (b >= B || d >= D) return;
   const size_t row = (size_t)b * D + d;
+  float yv = 0.f;
+  if (MF > 0) {
+    float4* sv = reinterpret_cast<float4*>(state) + row * (MF / 2);
+#pragma unroll
+    for (int i = 0; i < MF / 2; ++i) {
+      float h[4] = {hv[i].x, hv[i].y, hv[i].z, hv[i].w};
+      float hn[4];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int m = 2 * i + j;
+        const float2 hi = lhi[dl][m], lo = llo[dl][m], c = cs[dl][m];
+        const float2 t = cmul(lo, make_float2(h[2 * j], h[2 * j + 1]));
+        hn[2 * j] = fmaf(hi.x, h[2 * j], fmaf(-hi.y, h[2 * j + 1], t.x + xf));
+        hn[2 * j + 1] = fmaf(hi.x, h[2 * j + 1], fmaf(hi.y, h[2 * j], t.y));
+        yv = fmaf(c.x, hn[2 * j], fmaf(-c.y, hn[2 * j + 1], yv));
+      }
+      sv[i] = make_float4(hn[0], hn[1], hn[2], hn[3]);
+    }
+    y[row] = from_f32<TY>(yv);
+    return;
+  }
   const float xv = to_f32(x[row]);
   float2* st = reinterpret_cast<float2*>(state) + row * M;
-  float yv = 0.f;
   for (int m = 0; m < M; ++m) {
     const float2 h = st[m];
     const float2 hi = lhi[dl][m], lo = llo[dl][m], c = cs[dl][m];
@@ -69,9 +104,14 @@ hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y
                          const float* gamma, const float* omega, const float* amp,
                          const float* phase, float* state, hipStream_t st) {
   const dim3 grid((unsigned)((D + DEC_CH - 1) / DEC_CH), (unsigned)((B + DEC_ROWS - 1) / DEC_ROWS));
-  hipLaunchKernelGGL((decode_kernel<TX, TY>), grid, dim3(DEC_CH * DEC_ROWS), 0, st,
-                     reinterpret_cast<const TX*>(x), reinterpret_cast<TY*>(y), (int)B, (int)D,
-                     (int)M, gamma, omega, amp, phase, state);
+  if (M == 8 && ((uintptr_t)state & 15) == 0)  // 16-byte state loads
+    hipLaunchKernelGGL((decode_kernel<TX, TY, 8>), grid, dim3(DEC_CH * DEC_ROWS), 0, st,
+                       reinterpret_cast<const TX*>(x), reinterpret_cast<TY*>(y), (int)B, (int)D,
+                       (int)M, gamma, omega, amp, phase, state);
+  else
+    hipLaunchKernelGGL((decode_kernel<TX, TY, 0>), grid, dim3(DEC_CH * DEC_ROWS), 0, st,
+                       reinterpret_cast<const TX*>(x), reinterpret_cast<TY*>(y), (int)B, (int)D,
+                       (int)M, gamma, omega, amp, phase, state);
   return hipGetLastError();
 }
 
