@@ -4,3 +4,4 @@ Only tests/, __graft_entry__.smoke() and bench.py's cpu_baseline leg may import
 this package.  It shares no code with the HIP path.
 """
 from .resonator_oracle import *  # noqa: F401,F403
+from .epilogue_oracle import coupling_matrix, epilogue_fwd, epilogue_bwd  # noqa: F401
