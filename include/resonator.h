@@ -137,6 +137,43 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
                           const float* amp, const float* phase, float* state, void* stream);
 
 /*
+ * Mixer epilogue around the mixing output (Sec. 3.4, head coupling and local
+ * lexical path; the gate of Sec. 3.1's last paragraph):
+ *   C = I + (lambda_c / sqrt(H)) tanh(Ct)                          (coupling eq.)
+ *   ybar[b,t,g*dh+j] = sum_h C[g][h] y[b,t,h*dh+j]                 (head mixing eq.)
+ *   l[b,t,c] = sum_{k<K} w[c][k] v[b,t-k,c]  (zero before t = 0)   (causal depthwise conv)
+ *   z = sigmoid(gate) * ybar + s * l                               (combine eq.)
+ *   y, gate, v, z  [B][L][D] of act_dt, D = H * dh, channel c = h * dh + j
+ *                  (v: the token stream the local path reads; may be NULL when K == 0)
+ *   Ct [H][H], w [D][K], s [D]  float32 device arrays (w, s may be NULL when K == 0)
+ *   lambda_c       coupling strength (host value); 0 gives uncoupled heads
+ * 1 <= H <= 32, dh >= 1, 0 <= K <= 16 (K = 0: no local path).  z must not
+ * overlap y, gate or v.  Needs no workspace.
+ */
+int resonator_epilogue_fwd(const void* y, const void* gate, const void* v, res_dtype_t act_dt, void* z,
+                           int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K, const float* Ct,
+                           float lambda_c, const float* w, const float* s, void* stream);
+
+/* Workspace bytes of resonator_epilogue_bwd (0 for invalid sizes). */
+size_t resonator_epilogue_workspace_bytes(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K);
+
+/*
+ * Backward of resonator_epilogue_fwd for the loss sum(dz * z):
+ *   dz               [B][L][D] of act_dt
+ *   dy, dgate, dv    [B][L][D] of act_dt, overwritten (dv may be NULL when K == 0);
+ *                    none may overlap the inputs or each other
+ *   dCt [H][H], dw [D][K], ds [D], dlambda_c [1]  float32 device arrays, overwritten
+ *                    (dw, ds may be NULL when K == 0)
+ *   ws               workspace of resonator_epilogue_workspace_bytes(B, L, H, dh, K)
+ * The parameter gradients are reduced in a fixed order (per block of rows, then
+ * over blocks in float64), so they are bitwise reproducible.
+ */
+int resonator_epilogue_bwd(const void* y, const void* gate, const void* v, const void* dz, res_dtype_t act_dt,
+                           void* dy, void* dgate, void* dv, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K,
+                           const float* Ct, float lambda_c, const float* w, const float* s, float* dCt,
+                           float* dlambda_c, float* dw, float* ds, void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Measurement hook.  Arms a pair of HIP events (hipEvent_t passed as void*) on the
  * calling thread: the next resonator_mix_fwd or resonator_mix_bwd call on this
  * thread records start_event immediately before and stop_event immediately after

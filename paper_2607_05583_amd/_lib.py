@@ -19,7 +19,8 @@ RES_M_MAX = 16
 
 SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd",
            "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
-           "resonator_set_kernel_timer", "resonator_last_error")
+           "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
+           "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes")
 
 _lib = None
 
@@ -48,6 +49,14 @@ def _declare(lib):
     lib.resonator_state_init.argtypes = [vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_set_kernel_timer.restype = i32
     lib.resonator_set_kernel_timer.argtypes = [vp, vp]
+    f32 = ctypes.c_float
+    lib.resonator_epilogue_fwd.restype = i32
+    lib.resonator_epilogue_fwd.argtypes = [vp, vp, vp, i32, vp, i64, i64, i64, i64, i64, fp, f32, fp, fp, vp]
+    lib.resonator_epilogue_workspace_bytes.restype = sz
+    lib.resonator_epilogue_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
+    lib.resonator_epilogue_bwd.restype = i32
+    lib.resonator_epilogue_bwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, i64, i64, i64, i64, i64, fp, f32,
+                                           fp, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_decode_step.restype = i32
     lib.resonator_decode_step.argtypes = [vp, i32, vp, i32, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

@@ -1,6 +1,7 @@
 // C ABI of the resonant mixing library: argument validation, workspace layout
 // and kernel dispatch.  Declared in include/resonator.h.
 #include <cstdarg>
+#include <initializer_list>
 #include <cstdio>
 #include <string>
 
@@ -416,6 +417,93 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
   else
     e = launch_decode<bf16_t, float>(B, D, M, x_t, y_t, gamma, omega, amp, phase, state, st);
   return e == hipSuccess ? RES_OK : hip_fail(e, "decode launch");
+}
+
+// ---------------------------------------------------------------------------
+// Mixer epilogue (Sec. 3.4)
+// ---------------------------------------------------------------------------
+static int epi_check(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {
+  if (B < 1 || L < 1 || H < 1 || dh < 1)
+    return fail(RES_ERR_INVALID_ARG, "B, L, H, dh must be >= 1 (got %lld %lld %lld %lld)", (long long)B,
+                (long long)L, (long long)H, (long long)dh);
+  if (H > EPI_H_MAX || K < 0 || K > EPI_K_MAX || H * dh > (1 << 24) || B * L > (1LL << 40))
+    return fail(RES_ERR_UNSUPPORTED, "epilogue needs H <= %d, 0 <= K <= %d, H dh <= 2^24 (got H=%lld dh=%lld K=%lld)",
+                EPI_H_MAX, EPI_K_MAX, (long long)H, (long long)dh, (long long)K);
+  return RES_OK;
+}
+
+// two channels per thread when a head holds an even number of channels and every
+// activation pointer is aligned to two elements
+static int epi_vec(int64_t dh, size_t es, std::initializer_list<const void*> ps) {
+  if (dh % 2) return 1;
+  for (const void* p : ps)
+    if (p && !aligned(p, 2 * es)) return 1;
+  return 2;
+}
+
+size_t resonator_epilogue_workspace_bytes(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {
+  if (B < 1 || L < 1 || H < 1 || H > EPI_H_MAX || dh < 1 || K < 0 || K > EPI_K_MAX) return 0;
+  return epi_workspace_bytes(B, L, H, dh, K);
+}
+
+int resonator_epilogue_fwd(const void* y, const void* gate, const void* v, res_dtype_t act_dt, void* z,
+                           int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K, const float* Ct,
+                           float lambda_c, const float* w, const float* s, void* stream) {
+  int rc = epi_check(B, L, H, dh, K);
+  if (rc) return rc;
+  if (!dtype_ok(act_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!y || !gate || !z || !Ct) return fail(RES_ERR_INVALID_ARG, "y, gate, z and Ct must be non-null");
+  if (K > 0 && (!v || !w || !s)) return fail(RES_ERR_INVALID_ARG, "v, w and s must be non-null when K > 0");
+  const size_t es = elt_size(act_dt), n = (size_t)(B * L * H * dh) * es;
+  if (!aligned(y, es) || !aligned(gate, es) || !aligned(z, es) || (K > 0 && !aligned(v, es)) || !aligned(Ct, 4) ||
+      (w && !aligned(w, 4)) || (s && !aligned(s, 4)))
+    return fail(RES_ERR_MISALIGNED, "activations aligned to their element, parameters to 4 bytes");
+  if (overlap(z, n, y, n) || overlap(z, n, gate, n) || (K > 0 && overlap(z, n, v, n)))
+    return fail(RES_ERR_INVALID_ARG, "z must not overlap y, gate or v");
+  const int vec = epi_vec(dh, es, {y, gate, z, K > 0 ? v : nullptr});
+  hipStream_t st = (hipStream_t)stream;
+  const hipError_t e =
+      act_dt == RES_BF16
+          ? launch_epi_fwd<bf16_t>(y, gate, v, z, B, L, (int)H, (int)dh, (int)K, Ct, lambda_c, w, s, vec, st)
+          : launch_epi_fwd<float>(y, gate, v, z, B, L, (int)H, (int)dh, (int)K, Ct, lambda_c, w, s, vec, st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "epilogue launch");
+}
+
+int resonator_epilogue_bwd(const void* y, const void* gate, const void* v, const void* dz, res_dtype_t act_dt,
+                           void* dy, void* dgate, void* dv, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K,
+                           const float* Ct, float lambda_c, const float* w, const float* s, float* dCt,
+                           float* dlambda_c, float* dw, float* ds, void* ws, size_t ws_bytes, void* stream) {
+  int rc = epi_check(B, L, H, dh, K);
+  if (rc) return rc;
+  if (!dtype_ok(act_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!y || !gate || !dz || !dy || !dgate || !Ct || !dCt || !dlambda_c)
+    return fail(RES_ERR_INVALID_ARG, "y, gate, dz, dy, dgate, Ct, dCt and dlambda_c must be non-null");
+  if (K > 0 && (!v || !w || !s || !dv || !dw || !ds))
+    return fail(RES_ERR_INVALID_ARG, "v, w, s, dv, dw and ds must be non-null when K > 0");
+  const size_t need = epi_workspace_bytes(B, L, H, dh, K);
+  if (!ws || ws_bytes < need)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", need, ws_bytes);
+  const size_t es = elt_size(act_dt), n = (size_t)(B * L * H * dh) * es;
+  if (!aligned(y, es) || !aligned(gate, es) || !aligned(dz, es) || !aligned(dy, es) || !aligned(dgate, es) ||
+      (K > 0 && (!aligned(v, es) || !aligned(dv, es))) || !aligned(ws, 256))
+    return fail(RES_ERR_MISALIGNED, "activations aligned to their element, workspace to 256 bytes");
+  for (const void* o : {(const void*)dy, (const void*)dgate, (const void*)(K > 0 ? dv : nullptr)}) {
+    if (!o) continue;
+    if (overlap(o, n, y, n) || overlap(o, n, gate, n) || overlap(o, n, dz, n) || (K > 0 && overlap(o, n, v, n)))
+      return fail(RES_ERR_INVALID_ARG, "dy, dgate and dv must not overlap the inputs");
+  }
+  if (overlap(dy, n, dgate, n) || (K > 0 && (overlap(dv, n, dy, n) || overlap(dv, n, dgate, n))))
+    return fail(RES_ERR_INVALID_ARG, "dy, dgate and dv must not overlap each other");
+  const int vec = epi_vec(dh, es, {y, gate, dz, dy, dgate, K > 0 ? dv : nullptr});
+  hipStream_t st = (hipStream_t)stream;
+  float* part = (float*)ws;
+  const hipError_t e =
+      act_dt == RES_BF16
+          ? launch_epi_bwd<bf16_t>(y, gate, v, dz, dy, dgate, dv, B, L, (int)H, (int)dh, (int)K, Ct, lambda_c, w,
+                                   s, dCt, dlambda_c, dw, ds, part, vec, st)
+          : launch_epi_bwd<float>(y, gate, v, dz, dy, dgate, dv, B, L, (int)H, (int)dh, (int)K, Ct, lambda_c, w, s,
+                                  dCt, dlambda_c, dw, ds, part, vec, st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "epilogue backward launch");
 }
 
 }  // extern "C"

@@ -9,6 +9,20 @@ namespace res {
 
 enum { MODE_STATE = 0, MODE_APPLY = 1 };
 
+// Mixer epilogue: limits and the block of rows of the parameter sums
+constexpr int EPI_H_MAX = 32;   // heads
+constexpr int EPI_K_MAX = 16;   // local-path taps
+constexpr int EPI_ROWS = 64;    // rows per block partial
+// floats of block partials (then H*H float64 terms) in the epilogue backward workspace
+inline int64_t epi_part_floats(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {
+  const int64_t nblk = B * ((L + EPI_ROWS - 1) / EPI_ROWS);
+  const int64_t P = H * H + H * dh + H * dh * K;
+  return (nblk * P + 1) & ~(int64_t)1;  // even, so the float64 terms that follow are 8-byte aligned
+}
+inline size_t epi_workspace_bytes(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {
+  return (size_t)epi_part_floats(B, L, H, dh, K) * sizeof(float) + (size_t)(H * H) * sizeof(double);
+}
+
 // LDS tile buffers of the single-kernel forward work-group, by activation size
 // (bf16: 16 waves, 4 buffers; float32: 8 waves, 3 buffers)
 constexpr int seg_bufs(int elem_bytes) { return elem_bytes == 2 ? 4 : 3; }
@@ -104,5 +118,15 @@ hipError_t launch_bwd_reduce(const Geometry& g, const float* part, const float4*
                              const float* gamma, const float* omega, const float* amp,
                              const float* phase, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st);
+
+template <typename T>
+hipError_t launch_epi_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H,
+                          int dh, int K, const float* Ct, float lambda_c, const float* w, const float* s, int vec,
+                          hipStream_t st);
+template <typename T>
+hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const void* dz, void* dy, void* dgate,
+                          void* dv, int64_t B, int64_t L, int H, int dh, int K, const float* Ct, float lambda_c,
+                          const float* w, const float* s, float* dCt, float* dlambda_c, float* dw, float* ds,
+                          float* part, int vec, hipStream_t st);
 
 }  // namespace res

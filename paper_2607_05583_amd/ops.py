@@ -176,3 +176,71 @@ class ResonatorMixFunction(torch.autograd.Function):
 def resonator_mix(x, gamma, omega, amp, phase):
     """Differentiable mixing (x and the four parameter tensors receive gradients)."""
     return ResonatorMixFunction.apply(x, gamma, omega, amp, phase)
+
+
+# ---------------------------------------------------------------------------
+# Mixer epilogue (Sec. 3.4: head coupling, gate, local path)
+# ---------------------------------------------------------------------------
+def _epi_params(Ct, w, s, H, D, K):
+    _dev(Ct, "Ct")
+    if Ct.dtype != torch.float32 or tuple(Ct.shape) != (H, H):
+        raise ValueError("Ct must be float32 [H, H]")
+    if K > 0:
+        for name, p, shape in (("w", w, (D, K)), ("s", s, (D,))):
+            _dev(p, name)
+            if p.dtype != torch.float32 or tuple(p.shape) != shape:
+                raise ValueError(f"{name} must be float32 {list(shape)}")
+
+
+def resonator_epilogue_fwd(y, gate, v, Ct, lambda_c, w, s, H, out=None):
+    """z = sigmoid(gate) * (C (x) I_dh) y + s * causal_depthwise_conv(v, w), C = I + lc/sqrt(H) tanh(Ct).
+
+    y, gate, v: [B, L, D] (same dtype), D = H * dh; w: [D, K] float32 (K = w.shape[1];
+    w = None or K = 0 disables the local path, and v, s may then be None).
+    """
+    _dev(y, "y"); _dev(gate, "gate")
+    B, L, D = y.shape
+    if gate.shape != y.shape or gate.dtype != y.dtype:
+        raise ValueError("gate must match y in shape and dtype")
+    if D % H:
+        raise ValueError(f"D={D} is not a multiple of H={H}")
+    K = 0 if w is None else int(w.shape[1])
+    if K > 0:
+        _dev(v, "v")
+        if v.shape != y.shape or v.dtype != y.dtype:
+            raise ValueError("v must match y in shape and dtype")
+    _epi_params(Ct, w, s, H, D, K)
+    z = torch.empty_like(y) if out is None else _dev(out, "out")
+    check(_lib.lib().resonator_epilogue_fwd(
+        _ptr(y), _ptr(gate), _ptr(v) if K else None, _code(y), _ptr(z), B, L, H, D // H, K, _ptr(Ct),
+        float(lambda_c), _ptr(w) if K else None, _ptr(s) if K else None, _stream(y.device)))
+    return z
+
+
+def resonator_epilogue_bwd(y, gate, v, dz, Ct, lambda_c, w, s, H, ws=None):
+    """Gradients of sum(dz * z) for z = resonator_epilogue_fwd(...).
+
+    Returns (dy, dgate, dv, dCt, dlambda_c, dw, ds); dv, dw, ds are None when K = 0.
+    """
+    _dev(y, "y"); _dev(gate, "gate"); _dev(dz, "dz")
+    B, L, D = y.shape
+    K = 0 if w is None else int(w.shape[1])
+    for name, t in (("gate", gate), ("dz", dz)) + ((("v", v),) if K else ()):
+        _dev(t, name)
+        if t.shape != y.shape or t.dtype != y.dtype:
+            raise ValueError(f"{name} must match y in shape and dtype")
+    _epi_params(Ct, w, s, H, D, K)
+    dy, dgate = torch.empty_like(y), torch.empty_like(y)
+    dv = torch.empty_like(y) if K else None
+    f32 = dict(dtype=torch.float32, device=y.device)
+    dCt, dlam = torch.empty((H, H), **f32), torch.empty((1,), **f32)
+    dw = torch.empty((D, K), **f32) if K else None
+    ds = torch.empty((D,), **f32) if K else None
+    n = _lib.lib().resonator_epilogue_workspace_bytes(B, L, H, D // H, K)
+    if ws is None or ws.numel() < n:
+        ws = torch.empty(n, dtype=torch.uint8, device=y.device)
+    check(_lib.lib().resonator_epilogue_bwd(
+        _ptr(y), _ptr(gate), _ptr(v) if K else None, _ptr(dz), _code(y), _ptr(dy), _ptr(dgate), _ptr(dv), B, L,
+        H, D // H, K, _ptr(Ct), float(lambda_c), _ptr(w) if K else None, _ptr(s) if K else None, _ptr(dCt),
+        _ptr(dlam), _ptr(dw), _ptr(ds), _ptr(ws), ws.numel(), _stream(y.device)))
+    return dy, dgate, dv, dCt, dlam, dw, ds

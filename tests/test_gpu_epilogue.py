@@ -1,0 +1,128 @@
+"""GPU parity of the mixer epilogue (head coupling, gate, local path; Sec. 3.4)
+against the CPU oracle, through the C ABI.
+
+Tolerances: float32 activations 1e-4 (sigmoid and tanh in float32, sums in
+float32); bf16 activations 1.5e-2 for the outputs (one bf16 rounding of the
+result, 2^-8 relative, plus float32 arithmetic on exact bf16 inputs) and 1e-3
+for the parameter gradients (float32 partial sums of exact products, float64
+across blocks).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import act64, dev_act, dev_f32, host, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+
+CASES = [
+    # (B, L, H, dh, K, act): ragged L, odd dh (one channel per thread), K = 0, one head
+    (2, 37, 4, 6, 3, "f32"),
+    (2, 37, 4, 6, 3, "bf16"),
+    (1, 70, 3, 5, 4, "f32"),
+    (1, 70, 3, 5, 4, "bf16"),
+    (2, 65, 8, 4, 0, "bf16"),
+    (1, 40, 1, 16, 2, "f32"),
+    (1, 33, 32, 2, 16, "f32"),
+]
+
+
+def setup_module(module):
+    global ops
+    from paper_2607_05583_amd import ops as _ops
+    ops = _ops
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+
+
+def _dev_inputs(p, act):
+    K = p["K"]
+    t = {k: dev_act(p[k], act) for k in ("y", "gate", "v", "dz")}
+    t["Ct"] = dev_f32(p["Ct"])
+    t["w"] = dev_f32(p["w"]) if K else None
+    t["s"] = dev_f32(p["s"]) if K else None
+    return t
+
+
+def _ref_inputs(p, act):
+    return {k: act64(p[k], act) for k in ("y", "gate", "v", "dz")}
+
+
+def _bounds(act):
+    return (1e-4, 1e-4) if act == "f32" else (1.5e-2, 1e-3)
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_L{}_H{}_dh{}_K{}_{}".format(*c))
+def test_epilogue_fwd_parity(case):
+    B, L, H, dh, K, act = case
+    say(f"epilogue fwd {case}")
+    p = W.epilogue_inputs(7, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    z = ops.resonator_epilogue_fwd(t["y"], t["gate"], t["v"] if K else None, t["Ct"], p["lambda_c"], t["w"],
+                                   t["s"], H)
+    torch.cuda.synchronize()
+    r = _ref_inputs(p, act)
+    ref = O.epilogue_fwd(r["y"], r["gate"], r["v"], p["Ct"], p["lambda_c"], p["w"] if K else None, p["s"], H)
+    err = rel_err(host(z), ref)
+    say(f"  err {err:.2e}")
+    assert err <= _bounds(act)[0]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "B{}_L{}_H{}_dh{}_K{}_{}".format(*c))
+def test_epilogue_bwd_parity(case):
+    B, L, H, dh, K, act = case
+    say(f"epilogue bwd {case}")
+    p = W.epilogue_inputs(8, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    g = ops.resonator_epilogue_bwd(t["y"], t["gate"], t["v"] if K else None, t["dz"], t["Ct"], p["lambda_c"],
+                                   t["w"], t["s"], H)
+    torch.cuda.synchronize()
+    r = _ref_inputs(p, act)
+    ref = O.epilogue_bwd(r["y"], r["gate"], r["v"], r["dz"], p["Ct"], p["lambda_c"], p["w"] if K else None,
+                         p["s"], H)
+    names = ("dy", "dgate", "dv", "dCt", "dlambda_c", "dw", "ds")
+    b_act, b_par = _bounds(act)
+    errs = {}
+    for i, n in enumerate(names):
+        if ref[i] is None:
+            assert g[i] is None
+            continue
+        errs[n] = rel_err(host(g[i]).reshape(np.shape(ref[i])), ref[i])
+    say("  errs " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for n, e in errs.items():
+        assert e <= (b_act if n in ("dy", "dgate", "dv") else b_par), n
+
+
+def test_epilogue_bwd_is_deterministic():
+    B, L, H, dh, K, act = 2, 300, 8, 8, 4, "bf16"
+    say("epilogue bwd determinism")
+    p = W.epilogue_inputs(9, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    a = ops.resonator_epilogue_bwd(t["y"], t["gate"], t["v"], t["dz"], t["Ct"], p["lambda_c"], t["w"], t["s"], H)
+    b = ops.resonator_epilogue_bwd(t["y"], t["gate"], t["v"], t["dz"], t["Ct"], p["lambda_c"], t["w"], t["s"], H)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_epilogue_fwd_full_size_sampled():
+    """The prefill shape (B4 L32768, H8 x dh32 = 256 channels, K = 4, bf16), checked
+    on sampled rows against the oracle evaluated on those rows and their K-1
+    predecessors."""
+    B, L, H, dh, K, act = 4, 32768, 8, 32, 4, "bf16"
+    say("epilogue fwd full size")
+    p = W.epilogue_inputs(10, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    z = ops.resonator_epilogue_fwd(t["y"], t["gate"], t["v"], t["Ct"], p["lambda_c"], t["w"], t["s"], H)
+    torch.cuda.synchronize()
+    zh = host(z)
+    rng = np.random.default_rng(0)
+    for b, t0 in zip(rng.integers(0, B, 12), rng.integers(0, L, 12)):
+        lo = max(0, t0 - (K - 1))
+        sl = lambda a: act64(a[b:b + 1, lo:t0 + 1], act)
+        ref = O.epilogue_fwd(sl(p["y"]), sl(p["gate"]), sl(p["v"]), p["Ct"], p["lambda_c"], p["w"], p["s"], H)
+        err = rel_err(zh[b, t0], ref[0, -1])
+        assert err <= 1.5e-2, (b, t0, err)

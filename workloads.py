@@ -167,3 +167,24 @@ def random_problem(seed: int, B: int, L: int, D: int, M: int, act: str = "f32",
 def act_to_f32(a, act: str) -> np.ndarray:
     """Activation array (float32 or bf16 bits) as float32 values."""
     return bf16_bits_to_f32(a) if act == "bf16" else np.asarray(a, dtype=np.float32)
+
+
+# --------------------------------------------------------------------------
+# mixer epilogue (head coupling, gate, local path)
+# --------------------------------------------------------------------------
+def epilogue_inputs(seed: int, B: int, L: int, H: int, dh: int, K: int, act: str = "f32",
+                    lambda_c: float = 0.5):
+    """Seeded inputs of the mixer epilogue: y, gate, v, dz [B, L, H dh] standard
+    normals (float32 or bf16 bits); Ct [H, H] standard normal; w [D, K] N(0, 1/K)
+    (a K-tap filter of unit gain on average); s [D] N(0, 1).  Draw order y, gate,
+    v, dz, Ct, w, s."""
+    rng = np.random.default_rng(seed)
+    D = H * dh
+    y = _act(rng, (B, L, D), act)
+    gate = _act(rng, (B, L, D), act)
+    v = _act(rng, (B, L, D), act)
+    dz = _act(rng, (B, L, D), act)
+    Ct = rng.standard_normal((H, H)).astype(np.float32)
+    w = (rng.standard_normal((D, K)) / math.sqrt(max(K, 1))).astype(np.float32)
+    s = rng.standard_normal(D).astype(np.float32)
+    return dict(y=y, gate=gate, v=v, dz=dz, Ct=Ct, w=w, s=s, lambda_c=float(lambda_c), H=H, K=K)
