@@ -250,6 +250,31 @@ def main():
     tr_bwd_us = t1e.elapsed_time(t2e) * 1e3 / nt
     log(f"train layer: fwd {tr_fwd_us:.1f} us, bwd {tr_bwd_us:.1f} us")
 
+    # ---------------- mixer epilogue (head coupling, gate, local path) ----------------
+    eB, eL, eH, edh, eK = cfg.B, cfg.L, 8, cfg.D // 8, 4
+    ep = W.epilogue_inputs(11, eB, eL, eH, edh, eK, "bf16")
+    et = {k: torch.from_numpy(ep[k].view(np.int16)).view(torch.bfloat16).to(dev) for k in ("y", "gate", "v", "dz")}
+    eCt, ew, es = (torch.from_numpy(ep[k]).to(dev) for k in ("Ct", "w", "s"))
+    del ep
+    efwd = lambda: ops.resonator_epilogue_fwd(et["y"], et["gate"], et["v"], eCt, 0.5, ew, es, eH)
+    ebwd = lambda: ops.resonator_epilogue_bwd(et["y"], et["gate"], et["v"], et["dz"], eCt, 0.5, ew, es, eH)
+    for _ in range(3):
+        efwd(), ebwd()
+    torch.cuda.synchronize()
+    t0e.record(stream)
+    for _ in range(nt):
+        efwd()
+    t1e.record(stream)
+    for _ in range(nt):
+        ebwd()
+    t2e.record(stream)
+    torch.cuda.synchronize()
+    ep_fwd_us = t0e.elapsed_time(t1e) * 1e3 / nt
+    ep_bwd_us = t1e.elapsed_time(t2e) * 1e3 / nt
+    n_ep = eB * eL * eH * edh
+    log(f"mixer epilogue: fwd {ep_fwd_us:.1f} us, bwd {ep_bwd_us:.1f} us")
+    del et
+
     cpu = None
     if not args.no_cpu:
         log("cpu baseline (oracle recurrence) ...")
@@ -279,6 +304,10 @@ def main():
         "train_layer": {"workload": "B8 L8192 D256 M8 bf16 (one of the 6 layers)",
                         "fwd_us": tr_fwd_us, "bwd_us": tr_bwd_us,
                         "bwd_alg_GBs": 8 * 8192 * 256 * 6 / (tr_bwd_us * 1e-6) / 1e9},
+        "mixer_epilogue": {"workload": f"B{eB} L{eL} H{eH} dh{edh} K{eK} bf16 (coupling, gate, local path)",
+                           "fwd_us": ep_fwd_us, "bwd_us": ep_bwd_us,
+                           "fwd_alg_GBs": n_ep * 8 / (ep_fwd_us * 1e-6) / 1e9,
+                           "bwd_alg_GBs": n_ep * 14 / (ep_bwd_us * 1e-6) / 1e9},
         "roofline": {"bound": "hbm", "kernel": "fwd_seg_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,

@@ -432,13 +432,17 @@ static int epi_check(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {
   return RES_OK;
 }
 
-// two channels per thread when a head holds an even number of channels and every
-// activation pointer is aligned to two elements
+// channels a thread may move as one vector: the widest of 16 bytes, 8 bytes, two
+// elements, one element that divides the head size and to which every
+// activation pointer is aligned
 static int epi_vec(int64_t dh, size_t es, std::initializer_list<const void*> ps) {
-  if (dh % 2) return 1;
-  for (const void* p : ps)
-    if (p && !aligned(p, 2 * es)) return 1;
-  return 2;
+  for (int vec : {(int)(16 / es), (int)(8 / es), 2}) {
+    if (vec < 2 || dh % vec) continue;
+    bool ok = true;
+    for (const void* p : ps) ok = ok && (!p || aligned(p, (size_t)vec * es));
+    if (ok) return vec;
+  }
+  return 1;
 }
 
 size_t resonator_epilogue_workspace_bytes(int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K) {

@@ -290,7 +290,7 @@ __global__ __launch_bounds__(256) void carry_bwd_kernel(const float4* __restrict
 }
 
 // ---------------------------------------------------------------------------
-// Fixed-order reduction of the per-tile partials (float64), one thread per (d, m):
+// Fixed-order reduction of the per-tile partials (float64), one block per channel d:
 //   W = sum_tiles W_inter + sum_tau lambda^tau G[tau] + sum_b lambda q0 h0
 //   R = sum_tiles R_inter + sum_tau tau lambda^tau G[tau] + sum_b lambda (q0 + rho0) h0
 //   damp = Re(e^{i phi} W), dphase = -Im(c W), dgamma = -Re(c R), domega = -Im(c R)

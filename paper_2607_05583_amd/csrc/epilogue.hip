@@ -287,23 +287,456 @@ __global__ void epi_bwd_lambda_kernel(const double* __restrict__ lam_terms, int 
 }
 
 // ---------------------------------------------------------------------------
+// Tile kernels.  A block works on chunks of R consecutive rows of one batch
+// row.  A thread owns one piece of CPT adjacent channels (a 16-byte vector in
+// the forward, an 8-byte one in the backward, or one element when the heads or
+// pointers do not allow that) in every RP-th row of the chunk: thread (rr, cg)
+// has piece cg of rows rr, rr + RP, ...  Every activation row window a chunk
+// needs (its own rows; the K-1 rows before it for the local path, after it for
+// dv) is copied to LDS with one pass of vector loads issued before any LDS
+// store, so the head sums and the taps read LDS.  In the backward a thread's
+// piece is the same in every chunk, so the parameter sums (dC, ds, dw) stay in
+// registers across all chunks the block takes, and each block writes one
+// partial row [H*H dC | D ds | D*K dw] at the end.
+// ---------------------------------------------------------------------------
+template <int N> struct U32V { typedef uint32_t type __attribute__((ext_vector_type(N))); };
+template <int N> struct F32V { typedef float type __attribute__((ext_vector_type(N))); };
+
+// A piece: raw = the activation bits moved by one load or store, fraw = a
+// float32 copy kept in LDS.
+template <typename T, int CPT> struct Pc;
+template <int CPT> struct Pc<bf16_t, CPT> {
+  typedef typename U32V<CPT / 2>::type raw;
+  typedef typename F32V<CPT>::type fraw;
+  __device__ static void unpack(raw r, float (&f)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT / 2; ++i)
+      f[2 * i] = __uint_as_float(r[i] << 16), f[2 * i + 1] = __uint_as_float(r[i] & 0xFFFF0000u);
+  }
+  __device__ static raw pack(const float (&f)[CPT]) {
+    raw r;
+#pragma unroll
+    for (int i = 0; i < CPT / 2; ++i)
+      r[i] = (uint32_t)from_f32<bf16_t>(f[2 * i]) | ((uint32_t)from_f32<bf16_t>(f[2 * i + 1]) << 16);
+    return r;
+  }
+};
+template <int CPT> struct Pc<float, CPT> {
+  typedef typename U32V<CPT>::type raw;
+  typedef typename F32V<CPT>::type fraw;
+  __device__ static void unpack(raw r, float (&f)[CPT]) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) f[i] = __uint_as_float(r[i]);
+  }
+  __device__ static raw pack(const float (&f)[CPT]) {
+    raw r;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) r[i] = __float_as_uint(f[i]);
+    return r;
+  }
+};
+template <> struct Pc<bf16_t, 1> {
+  typedef bf16_t raw;
+  typedef float fraw;
+  __device__ static void unpack(raw r, float (&f)[1]) { f[0] = to_f32(r); }
+  __device__ static raw pack(const float (&f)[1]) { return from_f32<bf16_t>(f[0]); }
+};
+template <> struct Pc<float, 1> {
+  typedef float raw;
+  typedef float fraw;
+  __device__ static void unpack(raw r, float (&f)[1]) { f[0] = r; }
+  __device__ static raw pack(const float (&f)[1]) { return f[0]; }
+};
+template <int CPT> __device__ __forceinline__ void funpack(typename F32V<CPT>::type r, float (&f)[CPT]) {
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) f[i] = r[i];
+}
+__device__ __forceinline__ void funpack(float r, float (&f)[1]) { f[0] = r; }
+template <int CPT> __device__ __forceinline__ typename F32V<CPT>::type fpack(const float (&f)[CPT]) {
+  typename F32V<CPT>::type r;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) r[i] = f[i];
+  return r;
+}
+__device__ __forceinline__ float fpack(const float (&f)[1]) { return f[0]; }
+
+// channels per piece: 16 bytes forward, 8 bytes backward (register budget)
+template <typename T> constexpr int tile_wide(bool bwd) { return (bwd ? 8 : 16) / (int)sizeof(T); }
+constexpr int tile_kmax(int cpt) { return cpt > 1 ? 4 : EPI_K_MAX; }
+
+struct TileGeo {
+  int D, G, RP;  // channels, pieces per row, rows per pass (threads G * RP)
+};
+__host__ __device__ inline TileGeo tile_geo(int D, int cpt) {
+  TileGeo t;
+  t.D = D, t.G = D / cpt, t.RP = 256 / t.G;
+  return t;
+}
+
+// Row windows to copy: rows t_first .. t_first + nrows - 1 of batch row b (zero
+// outside [0, L)) into dst[nrows][G], as float32 (Win) or as they are (WinRaw).
+template <typename T, int CPT> struct Win {
+  typename Pc<T, CPT>::fraw* dst;
+  const T* src;
+  int64_t t_first;
+  int nrows;
+};
+template <typename T, int CPT> struct WinRaw {
+  typename Pc<T, CPT>::raw* dst;
+  const T* src;
+  int64_t t_first;
+  int nrows;
+};
+
+template <typename T, int CPT, int NF>
+__device__ __forceinline__ void stage_windows(const WinRaw<T, CPT>& wr, const Win<T, CPT> (&wf)[NF], int64_t b,
+                                              int64_t L, int D, int G, int rr, int cg, int RP, int maxrows) {
+  typedef Pc<T, CPT> PC;
+  typedef typename PC::raw P;
+  for (int i0 = rr; i0 < maxrows; i0 += 4 * RP) {
+    P rg[4], r[NF][4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * RP;
+      const int64_t t = wr.t_first + i;
+      if (i < wr.nrows && t >= 0 && t < L)
+        rg[u] = *reinterpret_cast<const P*>(wr.src + (b * L + t) * D + cg * CPT);
+      else
+        rg[u] = P(0);
+    }
+#pragma unroll
+    for (int q = 0; q < NF; ++q)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * RP;
+        const int64_t t = wf[q].t_first + i;
+        if (i < wf[q].nrows && t >= 0 && t < L)
+          r[q][u] = *reinterpret_cast<const P*>(wf[q].src + (b * L + t) * D + cg * CPT);
+        else
+          r[q][u] = P(0);
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i0 + u * RP < wr.nrows) wr.dst[(i0 + u * RP) * G + cg] = rg[u];
+#pragma unroll
+    for (int q = 0; q < NF; ++q)
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (i0 + u * RP < wf[q].nrows) {
+          float f[CPT];
+          PC::unpack(r[q][u], f);
+          wf[q].dst[(i0 + u * RP) * G + cg] = fpack(f);
+        }
+  }
+}
+
+template <typename T, int CPT>
+__global__ __launch_bounds__(256) void epi_fwd_tile_kernel(const T* __restrict__ y, const T* __restrict__ gate,
+                                                           const T* __restrict__ v, T* __restrict__ z, int64_t B,
+                                                           int64_t L, int H, int dh, int K, int R,
+                                                           const float* __restrict__ Ct, float lambda_c,
+                                                           const float* __restrict__ w,
+                                                           const float* __restrict__ s) {
+  typedef Pc<T, CPT> PC;
+  typedef typename PC::raw P;
+  typedef typename PC::fraw PF;
+  constexpr int KM = tile_kmax(CPT);
+  __shared__ float sC[EPI_H_MAX * EPI_H_MAX];
+  extern __shared__ __align__(16) unsigned char smem[];
+  const TileGeo tg = tile_geo(H * dh, CPT);
+  const int D = tg.D, G = tg.G, RP = tg.RP, KH = K > 0 ? K - 1 : 0;
+  PF* ys = reinterpret_cast<PF*>(smem);  // [R][G]
+  PF* vs = ys + R * G;                   // [R + KH][G]: rows t0 - KH .. t0 + R - 1
+  P* gs = reinterpret_cast<P*>(vs + (K > 0 ? R + KH : 0) * G);  // [R][G] gate as it is
+  coupling_to_lds(sC, Ct, lambda_c, H);
+  const int rr = threadIdx.x / G, cg = threadIdx.x % G;
+  const bool act = rr < RP;
+  const int c0 = cg * CPT, g = c0 / dh, j0 = c0 % dh;
+  float wk[KM][CPT], sc[CPT];
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) {
+    sc[e] = (act && K > 0) ? s[c0 + e] : 0.f;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) wk[k][e] = (act && k < K) ? w[(c0 + e) * K + k] : 0.f;
+  }
+  const int64_t nct = (L + R - 1) / R;
+  for (int64_t ch = blockIdx.x; ch < B * nct; ch += gridDim.x) {
+    const int64_t b = ch / nct, t0 = (ch % nct) * R;
+    const int n = (int)(L - t0 < R ? L - t0 : R);
+    __syncthreads();  // the previous chunk's LDS reads are done
+    if (act) {
+      const WinRaw<T, CPT> wg = {gs, gate, t0, n};
+      const Win<T, CPT> win[2] = {{ys, y, t0, n}, {vs, v, t0 - KH, K > 0 ? n + KH : 0}};
+      stage_windows<T, CPT, 2>(wg, win, b, L, D, G, rr, cg, RP, n + KH);
+    }
+    __syncthreads();
+    if (!act) continue;
+    for (int i = rr; i < n; i += RP) {
+      const int64_t o = (b * L + t0 + i) * D + c0;
+      float acc[CPT], u[CPT];
+      PC::unpack(gs[i * G + cg], u);
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) acc[e] = 0.f;
+      for (int h = 0; h < H; ++h) {
+        float yh[CPT];
+        funpack(ys[i * G + (h * dh + j0) / CPT], yh);
+        const float cgh = sC[g * H + h];
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) acc[e] = fmaf(cgh, yh[e], acc[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) acc[e] *= sigmoidf_(u[e]);
+      if (K > 0) {
+        float l[CPT];
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) l[e] = 0.f;
+#pragma unroll
+        for (int k = 0; k < KM; ++k)
+          if (k < K) {
+            float vv[CPT];
+            funpack(vs[(i + KH - k) * G + cg], vv);
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) l[e] = fmaf(wk[k][e], vv[e], l[e]);
+          }
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) acc[e] = fmaf(sc[e], l[e], acc[e]);
+      }
+      *reinterpret_cast<P*>(z + o) = PC::pack(acc);
+    }
+  }
+}
+
+template <typename T, int CPT, int HM>
+__global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__ y, const T* __restrict__ gate,
+                                                           const T* __restrict__ v, const T* __restrict__ dz,
+                                                           T* __restrict__ dy, T* __restrict__ dgate,
+                                                           T* __restrict__ dv, int64_t B, int64_t L, int H, int dh,
+                                                           int K, int R, const float* __restrict__ Ct,
+                                                           float lambda_c,
+                                                           const float* __restrict__ w,
+                                                           const float* __restrict__ s, float* __restrict__ part) {
+  typedef Pc<T, CPT> PC;
+  typedef typename PC::raw P;
+  typedef typename PC::fraw PF;
+  constexpr int KM = tile_kmax(CPT);
+  __shared__ float sC[EPI_H_MAX * EPI_H_MAX];
+  extern __shared__ __align__(16) unsigned char smem[];
+  const TileGeo tg = tile_geo(H * dh, CPT);
+  const int D = tg.D, G = tg.G, RP = tg.RP, KH = K > 0 ? K - 1 : 0;
+  PF* dybs = reinterpret_cast<PF*>(smem);  // [R][G]  dz sigmoid(gate)
+  PF* ys = dybs + R * G;                   // [R][G]
+  PF* dzs = ys + R * G;                    // [R + KH][G]: rows t0 .. t0 + R + KH - 1
+  PF* vs = dzs + (R + KH) * G;             // [R + KH][G]: rows t0 - KH .. t0 + R - 1
+  P* gs = reinterpret_cast<P*>(vs + (K > 0 ? R + KH : 0) * G);  // [R][G] gate as it is
+  coupling_to_lds(sC, Ct, lambda_c, H);
+  const int rr = threadIdx.x / G, cg = threadIdx.x % G;
+  const bool act = rr < RP;
+  const int c0 = cg * CPT, g = c0 / dh, j0 = c0 % dh;
+  float wk[KM][CPT], sc[CPT], dw[KM][CPT], ds[CPT], dc[HM];
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) {
+    sc[e] = (act && K > 0) ? s[c0 + e] : 0.f;
+    ds[e] = 0.f;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      wk[k][e] = (act && k < K) ? w[(c0 + e) * K + k] : 0.f;
+      dw[k][e] = 0.f;
+    }
+  }
+#pragma unroll
+  for (int h = 0; h < HM; ++h) dc[h] = 0.f;
+  const int64_t nct = (L + R - 1) / R;
+  for (int64_t ch = blockIdx.x; ch < B * nct; ch += gridDim.x) {
+    const int64_t b = ch / nct, t0 = (ch % nct) * R;
+    const int n = (int)(L - t0 < R ? L - t0 : R);
+    __syncthreads();
+    if (act) {
+      const WinRaw<T, CPT> wg = {gs, gate, t0, n};
+      const Win<T, CPT> win[3] = {
+          {ys, y, t0, n}, {dzs, dz, t0, n + KH}, {vs, v, t0 - KH, K > 0 ? n + KH : 0}};
+      stage_windows<T, CPT, 3>(wg, win, b, L, D, G, rr, cg, RP, n + KH);
+      for (int i = rr; i < n; i += RP) {  // own pieces, staged by this thread
+        float u[CPT], zz[CPT], db[CPT];
+        PC::unpack(gs[i * G + cg], u);
+        funpack(dzs[i * G + cg], zz);
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) db[e] = zz[e] * sigmoidf_(u[e]);
+        dybs[i * G + cg] = fpack(db);
+      }
+    }
+    __syncthreads();
+    if (!act) continue;
+    for (int i = rr; i < n; i += RP) {
+      const int64_t o = (b * L + t0 + i) * D + c0;
+      float zz[CPT], sg[CPT], db[CPT], ybar[CPT], dyh[CPT];
+      funpack(dzs[i * G + cg], zz);
+      PC::unpack(gs[i * G + cg], sg);
+      funpack(dybs[i * G + cg], db);
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) sg[e] = sigmoidf_(sg[e]);
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) ybar[e] = dyh[e] = 0.f;
+#pragma unroll
+      for (int h = 0; h < HM; ++h) {
+        if (h < H) {
+          float yh[CPT], dp[CPT];
+          funpack(ys[i * G + (h * dh + j0) / CPT], yh);
+          funpack(dybs[i * G + (h * dh + j0) / CPT], dp);
+          const float cgh = sC[g * H + h], chg = sC[h * H + g];
+          float a = 0.f;
+#pragma unroll
+          for (int e = 0; e < CPT; ++e) {
+            ybar[e] = fmaf(cgh, yh[e], ybar[e]);
+            dyh[e] = fmaf(chg, dp[e], dyh[e]);
+            a = fmaf(db[e], yh[e], a);
+          }
+          dc[h] += a;
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < CPT; ++e) ybar[e] = zz[e] * ybar[e] * sg[e] * (1.f - sg[e]);
+      *reinterpret_cast<P*>(dy + o) = PC::pack(dyh);
+      *reinterpret_cast<P*>(dgate + o) = PC::pack(ybar);
+      if (K > 0) {
+        float l[CPT], dvv[CPT];
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) l[e] = dvv[e] = 0.f;
+#pragma unroll
+        for (int k = 0; k < KM; ++k)
+          if (k < K) {
+            float vv[CPT], za[CPT];
+            funpack(vs[(i + KH - k) * G + cg], vv);
+            funpack(dzs[(i + k) * G + cg], za);  // zero past t = L - 1
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) {
+              l[e] = fmaf(wk[k][e], vv[e], l[e]);
+              dw[k][e] = fmaf(zz[e] * sc[e], vv[e], dw[k][e]);
+              dvv[e] = fmaf(wk[k][e] * sc[e], za[e], dvv[e]);
+            }
+          }
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) ds[e] = fmaf(zz[e], l[e], ds[e]);
+        *reinterpret_cast<P*>(dv + o) = PC::pack(dvv);
+      }
+    }
+  }
+  // block partial [H*H dC | D ds | D*K dw]; sums over threads in a fixed order
+  const int PW = H * H + D + D * K;
+  float* out = part + (size_t)blockIdx.x * PW;
+  float* sx = reinterpret_cast<float*>(smem);
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < HM; ++h)
+    if (h < H) sx[threadIdx.x * H + h] = act ? dc[h] : 0.f;
+  __syncthreads();
+  const int gpp = dh / CPT;  // pieces per head
+  for (int e = threadIdx.x; e < H * H; e += blockDim.x) {
+    const int gg = e / H, h = e % H;
+    float acc = 0.f;
+    for (int r = 0; r < RP; ++r)
+      for (int q = gg * gpp; q < (gg + 1) * gpp; ++q) acc += sx[(r * G + q) * H + h];
+    out[e] = acc;
+  }
+  if (K == 0) return;
+  __syncthreads();
+  const int NX = (1 + K) * CPT;  // per thread: ds[CPT], then dw[k][CPT]
+  if (act) {
+#pragma unroll
+    for (int e = 0; e < CPT; ++e) {
+      sx[threadIdx.x * NX + e] = ds[e];
+#pragma unroll
+      for (int k = 0; k < KM; ++k)
+        if (k < K) sx[threadIdx.x * NX + (1 + k) * CPT + e] = dw[k][e];
+    }
+  }
+  __syncthreads();
+  for (int x = threadIdx.x; x < D * (1 + K); x += blockDim.x) {
+    const int c = x % D, f = x / D;  // f = 0: ds; f = 1 + k: dw[., k]
+    const int q = c / CPT, e = c % CPT;
+    float acc = 0.f;
+    for (int r = 0; r < RP; ++r) acc += sx[(r * G + q) * NX + f * CPT + e];
+    if (f == 0)
+      out[H * H + c] = acc;
+    else
+      out[H * H + D + c * K + (f - 1)] = acc;
+  }
+}
+
+// LDS bytes of the tile kernels for chunks of R rows
+inline size_t epi_tile_lds(bool bwd, int D, int H, int K, int cpt, size_t es, int R) {
+  const size_t KH = K > 0 ? K - 1 : 0, halo = K > 0 ? R + KH : 0;
+  if (!bwd) return (R + halo) * D * 4 + (size_t)R * D * es;
+  const size_t stage = (2 * R + (R + KH) + halo) * D * 4 + (size_t)R * D * es;
+  const size_t xchg = (size_t)256 * (H > (1 + K) * cpt ? H : (1 + K) * cpt) * 4;
+  return stage > xchg ? stage : xchg;
+}
+// Rows per chunk: a multiple of the rows per pass, at least 16 (forward) or 8
+// (backward) where the LDS allows, within 64 KB; 0 when one pass does not fit.
+inline int epi_tile_rows(bool bwd, int D, int H, int K, int cpt, size_t es) {
+  const TileGeo tg = tile_geo(D, cpt);
+  const int want = bwd ? 8 : 16;
+  for (int m = (want + tg.RP - 1) / tg.RP; m >= 1; --m)
+    if (epi_tile_lds(bwd, D, H, K, cpt, es, tg.RP * m) <= 64 * 1024) return tg.RP * m;
+  return 0;
+}
+// channels per piece of the tile kernels for these shapes, 0 when they do not apply
+template <typename T> inline int epi_tile_cpt(int vec, int D, int H, int K, bool bwd) {
+  const int wide = tile_wide<T>(bwd);
+  int cpt = 0;
+  if (vec >= wide && K <= tile_kmax(wide) && D / wide <= 256) cpt = wide;
+  else if (D <= 256) cpt = 1;
+  if (cpt && epi_tile_rows(bwd, D, H, K, cpt, sizeof(T)) == 0) cpt = 0;
+  return cpt;
+}
+
+// ---------------------------------------------------------------------------
 static unsigned epi_grid(int64_t items) {
   const int64_t g = (items + 255) / 256;
   return (unsigned)(g < 8192 ? (g > 0 ? g : 1) : 8192);
+}
+
+template <typename T, int CPT>
+static void tile_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H, int dh,
+                     int K, const float* Ct, float lambda_c, const float* w, const float* s, hipStream_t st) {
+  const int R = epi_tile_rows(false, H * dh, H, K, CPT, sizeof(T));
+  const int64_t nch = B * ((L + R - 1) / R);
+  hipLaunchKernelGGL((epi_fwd_tile_kernel<T, CPT>), dim3((unsigned)(nch < 4096 ? nch : 4096)), dim3(256),
+                     epi_tile_lds(false, H * dh, H, K, CPT, sizeof(T), R), st, (const T*)y, (const T*)gate,
+                     (const T*)v, (T*)z, B, L, H, dh, K, R, Ct, lambda_c, w, s);
+}
+
+template <typename T, int CPT, int HM>
+static void tile_bwd(const void* y, const void* gate, const void* v, const void* dz, void* dy, void* dgate, void* dv,
+                     int64_t B, int64_t L, int H, int dh, int K, const float* Ct, float lambda_c, const float* w,
+                     const float* s, float* part, unsigned nparts, hipStream_t st) {
+  const int R = epi_tile_rows(true, H * dh, H, K, CPT, sizeof(T));
+  hipLaunchKernelGGL((epi_bwd_tile_kernel<T, CPT, HM>), dim3(nparts), dim3(256),
+                     epi_tile_lds(true, H * dh, H, K, CPT, sizeof(T), R), st, (const T*)y, (const T*)gate,
+                     (const T*)v, (const T*)dz, (T*)dy, (T*)dgate, (T*)dv, B, L, H, dh, K, R, Ct, lambda_c, w, s,
+                     part);
 }
 
 template <typename T>
 hipError_t launch_epi_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H,
                           int dh, int K, const float* Ct, float lambda_c, const float* w, const float* s, int vec,
                           hipStream_t st) {
-  const int64_t rows = B * L;
-  const int64_t items = rows * (int64_t)(H * dh / vec);
-  if (vec == 2)
-    hipLaunchKernelGGL((epi_fwd_kernel<T, 2>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                       (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
-  else
-    hipLaunchKernelGGL((epi_fwd_kernel<T, 1>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                       (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
+  constexpr int WIDE = tile_wide<T>(false);
+  const int cpt = epi_tile_cpt<T>(vec, H * dh, H, K, false);
+  if (cpt == WIDE)
+    tile_fwd<T, WIDE>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
+  else if (cpt == 1)
+    tile_fwd<T, 1>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
+  else {
+    const int64_t rows = B * L;
+    const int ov = vec >= 2 ? 2 : 1;
+    const int64_t items = rows * (int64_t)(H * dh / ov);
+    if (ov == 2)
+      hipLaunchKernelGGL((epi_fwd_kernel<T, 2>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
+                         (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
+    else
+      hipLaunchKernelGGL((epi_fwd_kernel<T, 1>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
+                         (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
+  }
   return hipGetLastError();
 }
 
@@ -312,24 +745,44 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
                           void* dv, int64_t B, int64_t L, int H, int dh, int K, const float* Ct, float lambda_c,
                           const float* w, const float* s, float* dCt, float* dlambda_c, float* dw, float* ds,
                           float* part, int vec, hipStream_t st) {
-  const int64_t rows = B * L;
-  const int64_t items = rows * (int64_t)(H * dh / vec);
-  if (vec == 2)
-    hipLaunchKernelGGL((epi_bwd_act_kernel<T, 2>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                       (const T*)gate, (const T*)dz, (T*)dy, (T*)dgate, (T*)dv, rows, L, H, dh, K, Ct, lambda_c, w,
-                       s);
-  else
-    hipLaunchKernelGGL((epi_bwd_act_kernel<T, 1>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                       (const T*)gate, (const T*)dz, (T*)dy, (T*)dgate, (T*)dv, rows, L, H, dh, K, Ct, lambda_c, w,
-                       s);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int64_t nblk = B * ((L + EPI_ROWS - 1) / EPI_ROWS);
-  hipLaunchKernelGGL((epi_bwd_param_kernel<T>), dim3((unsigned)nblk), dim3(256), 0, st, (const T*)y, (const T*)gate, (const T*)v, (const T*)dz, L, H, dh, K, w, s, part);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  constexpr int WIDE = tile_wide<T>(true);
+  const int64_t nblk = B * ((L + EPI_ROWS - 1) / EPI_ROWS);  // partial rows the workspace holds
+  int64_t nparts = nblk;
+  hipError_t e;
+  const int cpt = epi_tile_cpt<T>(vec, H * dh, H, K, true);
+  if (cpt) {
+    // one partial row per block; blocks loop over chunks, so fewer blocks than chunks
+    nparts = nblk < 1024 ? nblk : 1024;
+    const unsigned np = (unsigned)nparts;
+    if (cpt == WIDE && H <= 8)
+      tile_bwd<T, WIDE, 8>(y, gate, v, dz, dy, dgate, dv, B, L, H, dh, K, Ct, lambda_c, w, s, part, np, st);
+    else if (cpt == WIDE)
+      tile_bwd<T, WIDE, EPI_H_MAX>(y, gate, v, dz, dy, dgate, dv, B, L, H, dh, K, Ct, lambda_c, w, s, part, np, st);
+    else if (H <= 8)
+      tile_bwd<T, 1, 8>(y, gate, v, dz, dy, dgate, dv, B, L, H, dh, K, Ct, lambda_c, w, s, part, np, st);
+    else
+      tile_bwd<T, 1, EPI_H_MAX>(y, gate, v, dz, dy, dgate, dv, B, L, H, dh, K, Ct, lambda_c, w, s, part, np, st);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
+    const int64_t rows = B * L;
+    const int ov = vec >= 2 ? 2 : 1;
+    const int64_t items = rows * (int64_t)(H * dh / ov);
+    if (ov == 2)
+      hipLaunchKernelGGL((epi_bwd_act_kernel<T, 2>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
+                         (const T*)gate, (const T*)dz, (T*)dy, (T*)dgate, (T*)dv, rows, L, H, dh, K, Ct, lambda_c,
+                         w, s);
+    else
+      hipLaunchKernelGGL((epi_bwd_act_kernel<T, 1>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
+                         (const T*)gate, (const T*)dz, (T*)dy, (T*)dgate, (T*)dv, rows, L, H, dh, K, Ct, lambda_c,
+                         w, s);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    hipLaunchKernelGGL((epi_bwd_param_kernel<T>), dim3((unsigned)nblk), dim3(256), 0, st, (const T*)y,
+                       (const T*)gate, (const T*)v, (const T*)dz, L, H, dh, K, w, s, part);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const int P = H * H + H * dh + H * dh * K;
   double* lam_terms = reinterpret_cast<double*>(part + epi_part_floats(B, L, H, dh, K));
-  hipLaunchKernelGGL(epi_bwd_reduce_kernel, dim3((unsigned)((P + 15) / 16)), dim3(256), 0, st, part, nblk, H,
+  hipLaunchKernelGGL(epi_bwd_reduce_kernel, dim3((unsigned)((P + 15) / 16)), dim3(256), 0, st, part, nparts, H,
                      H * dh, K, Ct, lambda_c, dCt, dw, ds, lam_terms);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(epi_bwd_lambda_kernel, dim3(1), dim3(1), 0, st, lam_terms, H, dlambda_c);

@@ -28,6 +28,13 @@ CASES = [
     (2, 65, 8, 4, 0, "bf16"),
     (1, 40, 1, 16, 2, "f32"),
     (1, 33, 32, 2, 16, "f32"),
+    # 16-byte (forward) and 8-byte (backward) channel pieces, several chunks per block
+    (2, 77, 8, 32, 4, "bf16"),
+    (1, 50, 4, 16, 3, "f32"),
+    (1, 45, 2, 96, 2, "bf16"),   # 24 / 48 pieces a row: not a power of two
+    (1, 30, 16, 8, 2, "bf16"),   # more than eight heads
+    (1, 20, 4, 72, 2, "bf16"),   # D = 288
+    (1, 20, 3, 91, 2, "f32"),    # D = 273, one channel per thread: the generic kernels
 ]
 
 
@@ -126,3 +133,21 @@ def test_epilogue_fwd_full_size_sampled():
         ref = O.epilogue_fwd(sl(p["y"]), sl(p["gate"]), sl(p["v"]), p["Ct"], p["lambda_c"], p["w"], p["s"], H)
         err = rel_err(zh[b, t0], ref[0, -1])
         assert err <= 1.5e-2, (b, t0, err)
+
+
+def test_epilogue_bwd_many_blocks():
+    """More row chunks than backward blocks (each block loops over chunks and keeps
+    its parameter sums across them): B2 L40000 H8 dh32 K4 bf16, every output."""
+    B, L, H, dh, K, act = 2, 40000, 8, 32, 4, "bf16"
+    say("epilogue bwd many blocks")
+    p = W.epilogue_inputs(11, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    g = ops.resonator_epilogue_bwd(t["y"], t["gate"], t["v"], t["dz"], t["Ct"], p["lambda_c"], t["w"], t["s"], H)
+    torch.cuda.synchronize()
+    r = _ref_inputs(p, act)
+    ref = O.epilogue_bwd(r["y"], r["gate"], r["v"], r["dz"], p["Ct"], p["lambda_c"], p["w"], p["s"], H)
+    names = ("dy", "dgate", "dv", "dCt", "dlambda_c", "dw", "ds")
+    errs = {n: rel_err(host(g[i]).reshape(np.shape(ref[i])), ref[i]) for i, n in enumerate(names)}
+    say("  errs " + " ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+    for n, e in errs.items():
+        assert e <= (1.5e-2 if n in ("dy", "dgate", "dv") else 1e-3), n
