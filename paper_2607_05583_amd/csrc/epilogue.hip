@@ -51,6 +51,8 @@ template <> struct Vec<bf16_t, 2> {
 };
 
 __device__ __forceinline__ float sigmoidf_(float u) { return 1.f / (1.f + __expf(-u)); }
+// with the hardware reciprocal (about 1 ulp), for the tile kernels
+__device__ __forceinline__ float sigmoid_fast(float u) { return __builtin_amdgcn_rcpf(1.f + __expf(-u)); }
 
 // C = I + (lambda_c / sqrt(H)) tanh(Ct) into LDS (all threads; the caller syncs)
 __device__ __forceinline__ void coupling_to_lds(float* sC, const float* Ct, float lambda_c, int H) {
@@ -59,54 +61,6 @@ __device__ __forceinline__ void coupling_to_lds(float* sC, const float* Ct, floa
     sC[i] = (i / H == i % H ? 1.f : 0.f) + scale * tanhf(Ct[i]);
 }
 
-// One work item = (row r = b L + t, channels c .. c+VEC-1 of head g).
-template <typename T, int VEC>
-__global__ __launch_bounds__(256) void epi_fwd_kernel(const T* __restrict__ y, const T* __restrict__ gate,
-                                                      const T* __restrict__ v, T* __restrict__ z, int64_t rows,
-                                                      int64_t L, int H, int dh, int K, const float* __restrict__ Ct,
-                                                      float lambda_c, const float* __restrict__ w,
-                                                      const float* __restrict__ s) {
-  __shared__ float sC[EPI_H_MAX * EPI_H_MAX];
-  coupling_to_lds(sC, Ct, lambda_c, H);
-  __syncthreads();
-  typedef Vec<T, VEC> V;
-  const int D = H * dh, gpr = D / VEC;  // channel groups per row
-  for (int64_t it = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; it < rows * gpr;
-       it += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = it / gpr;
-    const int c = (int)(it % gpr) * VEC, g = c / dh, j = c % dh;
-    const T* yr = y + r * D;
-    float acc[VEC], u[VEC];
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
-    for (int h = 0; h < H; ++h) {
-      V::load(yr + h * dh + j, u);
-      const float ch = sC[g * H + h];
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) acc[e] = fmaf(ch, u[e], acc[e]);
-    }
-    float gt[VEC], out[VEC];
-    V::load(gate + r * D + c, gt);
-#pragma unroll
-    for (int e = 0; e < VEC; ++e) out[e] = sigmoidf_(gt[e]) * acc[e];
-    if (K > 0) {
-      const int64_t t = r % L;
-      float l[VEC];
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) l[e] = 0.f;
-      for (int k = 0; k < K && k <= t; ++k) {
-        V::load(v + (r - k) * D + c, u);
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) l[e] = fmaf(w[(c + e) * K + k], u[e], l[e]);
-      }
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) out[e] = fmaf(s[c + e], l[e], out[e]);
-    }
-    V::store(z + r * D + c, out);
-  }
-}
-
-// dy, dgate, dv (elementwise over the same work items)
 template <typename T, int VEC>
 __global__ __launch_bounds__(256) void epi_bwd_act_kernel(const T* __restrict__ y, const T* __restrict__ gate,
                                                           const T* __restrict__ dz, T* __restrict__ dy,
@@ -373,138 +327,229 @@ __host__ __device__ inline TileGeo tile_geo(int D, int cpt) {
   return t;
 }
 
-// Row windows to copy: rows t_first .. t_first + nrows - 1 of batch row b (zero
-// outside [0, L)) into dst[nrows][G], as float32 (Win) or as they are (WinRaw).
-template <typename T, int CPT> struct Win {
-  typename Pc<T, CPT>::fraw* dst;
-  const T* src;
-  int64_t t_first;
-  int nrows;
-};
-template <typename T, int CPT> struct WinRaw {
-  typename Pc<T, CPT>::raw* dst;
-  const T* src;
-  int64_t t_first;
-  int nrows;
-};
-
-template <typename T, int CPT, int NF>
-__device__ __forceinline__ void stage_windows(const WinRaw<T, CPT>& wr, const Win<T, CPT> (&wf)[NF], int64_t b,
-                                              int64_t L, int D, int G, int rr, int cg, int RP, int maxrows) {
+// Forward, one thread per (row, column piece): the thread owns channels
+// j0 .. j0+CPT-1 of every head in one row, so it loads each y and gate element
+// of its piece exactly once and forms all H mixed heads from them in registers
+// (H*H*CPT multiply-adds).  The local path reads v at the K-1 previous rows too;
+// those are the current rows of neighbouring threads, so they hit in cache.  No
+// LDS staging, no barriers after the prologue: every load of a row is issued
+// before any of it is used.
+template <typename T, int CPT, int HM, bool WL>
+__global__ __launch_bounds__(256) void epi_fwd_col_kernel(const T* __restrict__ y, const T* __restrict__ gate,
+                                                          const T* __restrict__ v, T* __restrict__ z,
+                                                          int64_t rows, int64_t L, int H, int dh, int K,
+                                                          const float* __restrict__ Ct, float lambda_c,
+                                                          const float* __restrict__ w,
+                                                          const float* __restrict__ s) {
   typedef Pc<T, CPT> PC;
   typedef typename PC::raw P;
-  for (int i0 = rr; i0 < maxrows; i0 += 4 * RP) {
-    P rg[4], r[NF][4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = i0 + u * RP;
-      const int64_t t = wr.t_first + i;
-      if (i < wr.nrows && t >= 0 && t < L)
-        rg[u] = *reinterpret_cast<const P*>(wr.src + (b * L + t) * D + cg * CPT);
-      else
-        rg[u] = P(0);
-    }
-#pragma unroll
-    for (int q = 0; q < NF; ++q)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int i = i0 + u * RP;
-        const int64_t t = wf[q].t_first + i;
-        if (i < wf[q].nrows && t >= 0 && t < L)
-          r[q][u] = *reinterpret_cast<const P*>(wf[q].src + (b * L + t) * D + cg * CPT);
-        else
-          r[q][u] = P(0);
-      }
-#pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (i0 + u * RP < wr.nrows) wr.dst[(i0 + u * RP) * G + cg] = rg[u];
-#pragma unroll
-    for (int q = 0; q < NF; ++q)
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (i0 + u * RP < wf[q].nrows) {
-          float f[CPT];
-          PC::unpack(r[q][u], f);
-          wf[q].dst[(i0 + u * RP) * G + cg] = fpack(f);
-        }
-  }
-}
-
-template <typename T, int CPT>
-__global__ __launch_bounds__(256) void epi_fwd_tile_kernel(const T* __restrict__ y, const T* __restrict__ gate,
-                                                           const T* __restrict__ v, T* __restrict__ z, int64_t B,
-                                                           int64_t L, int H, int dh, int K, int R,
-                                                           const float* __restrict__ Ct, float lambda_c,
-                                                           const float* __restrict__ w,
-                                                           const float* __restrict__ s) {
-  typedef Pc<T, CPT> PC;
-  typedef typename PC::raw P;
-  typedef typename PC::fraw PF;
-  constexpr int KM = tile_kmax(CPT);
   __shared__ float sC[EPI_H_MAX * EPI_H_MAX];
-  extern __shared__ __align__(16) unsigned char smem[];
-  const TileGeo tg = tile_geo(H * dh, CPT);
-  const int D = tg.D, G = tg.G, RP = tg.RP, KH = K > 0 ? K - 1 : 0;
-  PF* ys = reinterpret_cast<PF*>(smem);  // [R][G]
-  PF* vs = ys + R * G;                   // [R + KH][G]: rows t0 - KH .. t0 + R - 1
-  P* gs = reinterpret_cast<P*>(vs + (K > 0 ? R + KH : 0) * G);  // [R][G] gate as it is
+  extern __shared__ __align__(16) float sW[];  // w as [K][D], then s[D] (WL: taps in LDS)
   coupling_to_lds(sC, Ct, lambda_c, H);
-  const int rr = threadIdx.x / G, cg = threadIdx.x % G;
-  const bool act = rr < RP;
-  const int c0 = cg * CPT, g = c0 / dh, j0 = c0 % dh;
-  float wk[KM][CPT], sc[CPT];
-#pragma unroll
-  for (int e = 0; e < CPT; ++e) {
-    sc[e] = (act && K > 0) ? s[c0 + e] : 0.f;
-#pragma unroll
-    for (int k = 0; k < KM; ++k) wk[k][e] = (act && k < K) ? w[(c0 + e) * K + k] : 0.f;
+  const int D = H * dh, np = dh / CPT;
+  if (WL) {
+    for (int x = threadIdx.x; x < D * K; x += blockDim.x) sW[(x % K) * D + x / K] = w[x];
+    if (K > 0)
+      for (int x = threadIdx.x; x < D; x += blockDim.x) sW[D * K + x] = s[x];
   }
-  const int64_t nct = (L + R - 1) / R;
-  for (int64_t ch = blockIdx.x; ch < B * nct; ch += gridDim.x) {
-    const int64_t b = ch / nct, t0 = (ch % nct) * R;
-    const int n = (int)(L - t0 < R ? L - t0 : R);
-    __syncthreads();  // the previous chunk's LDS reads are done
-    if (act) {
-      const WinRaw<T, CPT> wg = {gs, gate, t0, n};
-      const Win<T, CPT> win[2] = {{ys, y, t0, n}, {vs, v, t0 - KH, K > 0 ? n + KH : 0}};
-      stage_windows<T, CPT, 2>(wg, win, b, L, D, G, rr, cg, RP, n + KH);
-    }
-    __syncthreads();
-    if (!act) continue;
-    for (int i = rr; i < n; i += RP) {
-      const int64_t o = (b * L + t0 + i) * D + c0;
-      float acc[CPT], u[CPT];
-      PC::unpack(gs[i * G + cg], u);
+  __syncthreads();
+  // A block step covers RB rows x PB pieces (PB = min(np, 256)); the row and its
+  // position in the batch row come from block-uniform (scalar) arithmetic.
+  const int PB = np < (int)blockDim.x ? np : (int)blockDim.x, RB = (int)blockDim.x / PB;
+  const int rl = (int)threadIdx.x / PB, pl = (int)threadIdx.x - rl * PB;
+  const int64_t ncb = (np + PB - 1) / PB, nq = (rows + RB - 1) / RB * ncb;
+  if (rl >= RB) return;  // no barrier follows
+  for (int64_t q = blockIdx.x; q < nq; q += gridDim.x) {
+    const int64_t rb = q / ncb * RB;
+    const int p = (int)(q % ncb) * PB + pl;
+    const int64_t r = rb + rl;
+    if (r >= rows || p >= np) continue;
+    int64_t t = rb % L + rl;
+    while (t >= L) t -= L;  // the step's rows may cross into the next batch row
+    const int j0 = p * CPT;
+    const int64_t o = r * D + j0;
+    if constexpr (HM == 8 && CPT > 1) {
+      // Every load of the row is issued before any is used: a head at or beyond
+      // H, a tap at or beyond K and a tap before t = 0 read a valid row of this
+      // batch row and get a zero weight, so no load waits behind a branch.  v is
+      // read only when K > 0 (it may be null otherwise); that branch is uniform.
+      P yr[8], gr[8], vr[8][4];
 #pragma unroll
-      for (int e = 0; e < CPT; ++e) acc[e] = 0.f;
-      for (int h = 0; h < H; ++h) {
+      for (int h = 0; h < 8; ++h) {
+        const int hh = h < H ? h : 0;
+        yr[h] = *reinterpret_cast<const P*>(y + o + hh * dh);
+        gr[h] = *reinterpret_cast<const P*>(gate + o + hh * dh);
+      }
+      if (K > 0) {
+#pragma unroll
+        for (int h = 0; h < 8; ++h) {
+          const int hh = h < H ? h : 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const bool tap = k < K && k <= t;  // then row r - k is in this batch row
+            vr[h][k] = *reinterpret_cast<const P*>(v + o - (tap ? (int64_t)k * D : 0) + hh * dh);
+          }
+        }
+      }
+      float acc[8][CPT];
+#pragma unroll
+      for (int g = 0; g < 8; ++g)
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) acc[g][e] = 0.f;
+#pragma unroll
+      for (int h = 0; h < 8; ++h) {
         float yh[CPT];
-        funpack(ys[i * G + (h * dh + j0) / CPT], yh);
-        const float cgh = sC[g * H + h];
+        PC::unpack(yr[h], yh);
 #pragma unroll
-        for (int e = 0; e < CPT; ++e) acc[e] = fmaf(cgh, yh[e], acc[e]);
+        for (int g = 0; g < 8; ++g) {
+          const float cgh = (g < H && h < H) ? sC[g * H + h] : 0.f;
+#pragma unroll
+          for (int e = 0; e < CPT; ++e) acc[g][e] = fmaf(cgh, yh[e], acc[g][e]);
+        }
       }
 #pragma unroll
-      for (int e = 0; e < CPT; ++e) acc[e] *= sigmoidf_(u[e]);
-      if (K > 0) {
-        float l[CPT];
+      for (int g = 0; g < 8; ++g) {
+        if (g >= H) continue;
+        const int c0 = g * dh + j0;
+        float u[CPT], out[CPT], l[CPT];
+        PC::unpack(gr[g], u);
 #pragma unroll
-        for (int e = 0; e < CPT; ++e) l[e] = 0.f;
+        for (int e = 0; e < CPT; ++e) out[e] = sigmoid_fast(u[e]) * acc[g][e], l[e] = 0.f;
+        if (K > 0) {
 #pragma unroll
-        for (int k = 0; k < KM; ++k)
-          if (k < K) {
+          for (int k = 0; k < 4; ++k) {
+            const bool tap = k < K && k <= t;
             float vv[CPT];
-            funpack(vs[(i + KH - k) * G + cg], vv);
+            PC::unpack(vr[g][k], vv);
 #pragma unroll
-            for (int e = 0; e < CPT; ++e) l[e] = fmaf(wk[k][e], vv[e], l[e]);
+            for (int e = 0; e < CPT; ++e)
+              l[e] = fmaf(tap ? (WL ? sW[k * D + c0 + e] : w[(c0 + e) * K + k]) : 0.f, vv[e], l[e]);
           }
 #pragma unroll
-        for (int e = 0; e < CPT; ++e) acc[e] = fmaf(sc[e], l[e], acc[e]);
+          for (int e = 0; e < CPT; ++e) out[e] = fmaf(WL ? sW[D * K + c0 + e] : s[c0 + e], l[e], out[e]);
+        }
+        *reinterpret_cast<P*>(z + o + g * dh) = PC::pack(out);
       }
-      *reinterpret_cast<P*>(z + o) = PC::pack(acc);
+    } else {
+      float acc[HM][CPT];
+#pragma unroll
+      for (int g = 0; g < HM; ++g)
+#pragma unroll
+        for (int e = 0; e < CPT; ++e) acc[g][e] = 0.f;
+#pragma unroll
+      for (int h = 0; h < HM; ++h) {
+        if (h < H) {
+          float yh[CPT];
+          PC::unpack(*reinterpret_cast<const P*>(y + o + h * dh), yh);
+#pragma unroll
+          for (int g = 0; g < HM; ++g) {
+            if (g < H) {
+              const float cgh = sC[g * H + h];
+#pragma unroll
+              for (int e = 0; e < CPT; ++e) acc[g][e] = fmaf(cgh, yh[e], acc[g][e]);
+            }
+          }
+        }
+      }
+#pragma unroll
+      for (int g = 0; g < HM; ++g) {
+        if (g < H) {
+          const int c0 = g * dh + j0;
+          float u[CPT], out[CPT];
+          PC::unpack(*reinterpret_cast<const P*>(gate + o + g * dh), u);
+#pragma unroll
+          for (int e = 0; e < CPT; ++e) out[e] = sigmoid_fast(u[e]) * acc[g][e];
+          if (K > 0) {
+            float l[CPT];
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) l[e] = 0.f;
+            for (int k = 0; k < K && k <= t; ++k) {
+              float vv[CPT];
+              PC::unpack(*reinterpret_cast<const P*>(v + o - (int64_t)k * D + g * dh), vv);
+#pragma unroll
+              for (int e = 0; e < CPT; ++e)
+                l[e] = fmaf(WL ? sW[k * D + c0 + e] : w[(c0 + e) * K + k], vv[e], l[e]);
+            }
+#pragma unroll
+            for (int e = 0; e < CPT; ++e) out[e] = fmaf(WL ? sW[D * K + c0 + e] : s[c0 + e], l[e], out[e]);
+          }
+          *reinterpret_cast<P*>(z + o + g * dh) = PC::pack(out);
+        }
+      }
     }
   }
 }
+
+// Row windows of a chunk: rows t_first .. t_first + nrows - 1 of batch row b,
+// zero outside [0, L).  Thread (rr, cg) moves piece cg of window rows rr + u RP,
+// u < U; the host keeps every window within U RP rows.  Loads for the next
+// chunk are issued into registers before the current chunk is computed, and
+// written to LDS (as float32, the gate as it is) after it.
+struct WinSrc {
+  int64_t t_first;
+  int nrows;
+};
+
+template <typename T, int CPT, int U, int NW>
+__device__ __forceinline__ void win_load(typename Pc<T, CPT>::raw (&r)[NW][U], const T* const (&src)[NW],
+                                         const WinSrc (&w)[NW], int64_t b, int64_t L, int D, int rr, int cg,
+                                         int RP) {
+  typedef typename Pc<T, CPT>::raw P;
+#pragma unroll
+  for (int q = 0; q < NW; ++q)
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = rr + u * RP;
+      const int64_t t = w[q].t_first + i;
+      if (i < w[q].nrows && t >= 0 && t < L)
+        r[q][u] = *reinterpret_cast<const P*>(src[q] + (b * L + t) * D + cg * CPT);
+      else
+        r[q][u] = P(0);
+    }
+}
+
+// window 0 (the gate) is stored as it is, windows 1.. as float32
+template <typename T, int CPT, int U, int NW>
+__device__ __forceinline__ void win_store(const typename Pc<T, CPT>::raw (&r)[NW][U],
+                                          typename Pc<T, CPT>::raw* gdst,
+                                          typename Pc<T, CPT>::fraw* const (&fdst)[NW - 1], const WinSrc (&w)[NW],
+                                          int G, int rr, int cg, int RP) {
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (rr + u * RP < w[0].nrows) gdst[(rr + u * RP) * G + cg] = r[0][u];
+#pragma unroll
+  for (int q = 1; q < NW; ++q)
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (rr + u * RP < w[q].nrows) {
+        float f[CPT];
+        Pc<T, CPT>::unpack(r[q][u], f);
+        fdst[q - 1][(rr + u * RP) * G + cg] = fpack(f);
+      }
+}
+
+// Per-thread local-path parameters, read once before the chunk loop.  They go
+// through LDS: the compiler waits for every outstanding global load before a
+// loop that stores but does not load whenever that loop uses a register
+// loaded from global memory, which would stall on the next chunk's prefetch.
+template <int CPT, int KM>
+__device__ __forceinline__ void params_via_lds(float (&wk)[KM][CPT], float (&sc)[CPT], const float* w,
+                                               const float* s, int D, int K, int c0, bool act, float* sp) {
+  for (int x = threadIdx.x; x < D * K; x += blockDim.x) sp[x] = w[x];
+  if (K > 0)
+    for (int x = threadIdx.x; x < D; x += blockDim.x) sp[D * K + x] = s[x];
+  __syncthreads();
+#pragma unroll
+  for (int e = 0; e < CPT; ++e) {
+    sc[e] = (act && K > 0) ? sp[D * K + c0 + e] : 0.f;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) wk[k][e] = (act && k < K) ? sp[(c0 + e) * K + k] : 0.f;
+  }
+  __syncthreads();  // the area is reused for the row windows
+}
+
+// rows of one window slot per thread: the forward moves 3 windows, the backward 4
+template <int CPT> constexpr int tile_u(bool bwd) { return CPT == 1 ? 16 : (bwd ? 4 : 3); }
 
 template <typename T, int CPT, int HM>
 __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__ y, const T* __restrict__ gate,
@@ -512,13 +557,12 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
                                                            T* __restrict__ dy, T* __restrict__ dgate,
                                                            T* __restrict__ dv, int64_t B, int64_t L, int H, int dh,
                                                            int K, int R, const float* __restrict__ Ct,
-                                                           float lambda_c,
-                                                           const float* __restrict__ w,
+                                                           float lambda_c, const float* __restrict__ w,
                                                            const float* __restrict__ s, float* __restrict__ part) {
   typedef Pc<T, CPT> PC;
   typedef typename PC::raw P;
   typedef typename PC::fraw PF;
-  constexpr int KM = tile_kmax(CPT);
+  constexpr int KM = tile_kmax(CPT), U = tile_u<CPT>(true);
   __shared__ float sC[EPI_H_MAX * EPI_H_MAX];
   extern __shared__ __align__(16) unsigned char smem[];
   const TileGeo tg = tile_geo(H * dh, CPT);
@@ -533,39 +577,53 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
   const bool act = rr < RP;
   const int c0 = cg * CPT, g = c0 / dh, j0 = c0 % dh;
   float wk[KM][CPT], sc[CPT], dw[KM][CPT], ds[CPT], dc[HM];
+  params_via_lds<CPT, KM>(wk, sc, w, s, D, K, c0, act, reinterpret_cast<float*>(smem));
 #pragma unroll
   for (int e = 0; e < CPT; ++e) {
-    sc[e] = (act && K > 0) ? s[c0 + e] : 0.f;
     ds[e] = 0.f;
 #pragma unroll
-    for (int k = 0; k < KM; ++k) {
-      wk[k][e] = (act && k < K) ? w[(c0 + e) * K + k] : 0.f;
-      dw[k][e] = 0.f;
-    }
+    for (int k = 0; k < KM; ++k) dw[k][e] = 0.f;
   }
 #pragma unroll
   for (int h = 0; h < HM; ++h) dc[h] = 0.f;
-  const int64_t nct = (L + R - 1) / R;
-  for (int64_t ch = blockIdx.x; ch < B * nct; ch += gridDim.x) {
-    const int64_t b = ch / nct, t0 = (ch % nct) * R;
+  const int64_t nct = (L + R - 1) / R, nch = B * nct;
+  const T* const src[4] = {gate, y, dz, v};
+  PF* const fdst[3] = {ys, dzs, vs};
+  auto wins = [&](int64_t c, WinSrc (&wv)[4]) {
+    const int64_t t0 = (c % nct) * R;
+    const int n = (int)(L - t0 < R ? L - t0 : R);
+    wv[0] = {t0, n}, wv[1] = {t0, n}, wv[2] = {t0, n + KH}, wv[3] = {t0 - KH, K > 0 ? n + KH : 0};
+  };
+  P r[4][U];
+  WinSrc wv[4];
+  int64_t c = blockIdx.x;
+  if (act && c < nch) {
+    wins(c, wv);
+    win_load<T, CPT, U, 4>(r, src, wv, c / nct, L, D, rr, cg, RP);
+  }
+  for (; c < nch; c += gridDim.x) {
+    const int64_t b = c / nct, t0 = (c % nct) * R;
     const int n = (int)(L - t0 < R ? L - t0 : R);
     __syncthreads();
     if (act) {
-      const WinRaw<T, CPT> wg = {gs, gate, t0, n};
-      const Win<T, CPT> win[3] = {
-          {ys, y, t0, n}, {dzs, dz, t0, n + KH}, {vs, v, t0 - KH, K > 0 ? n + KH : 0}};
-      stage_windows<T, CPT, 3>(wg, win, b, L, D, G, rr, cg, RP, n + KH);
-      for (int i = rr; i < n; i += RP) {  // own pieces, staged by this thread
+      wins(c, wv);
+      win_store<T, CPT, U, 4>(r, gs, fdst, wv, G, rr, cg, RP);
+      for (int i = rr; i < n; i += RP) {  // own pieces, just stored by this thread
         float u[CPT], zz[CPT], db[CPT];
         PC::unpack(gs[i * G + cg], u);
         funpack(dzs[i * G + cg], zz);
 #pragma unroll
-        for (int e = 0; e < CPT; ++e) db[e] = zz[e] * sigmoidf_(u[e]);
+        for (int e = 0; e < CPT; ++e) db[e] = zz[e] * sigmoid_fast(u[e]);
         dybs[i * G + cg] = fpack(db);
       }
     }
     __syncthreads();
     if (!act) continue;
+    const int64_t cn = c + gridDim.x;
+    if (cn < nch) {
+      wins(cn, wv);
+      win_load<T, CPT, U, 4>(r, src, wv, cn / nct, L, D, rr, cg, RP);
+    }
     for (int i = rr; i < n; i += RP) {
       const int64_t o = (b * L + t0 + i) * D + c0;
       float zz[CPT], sg[CPT], db[CPT], ybar[CPT], dyh[CPT];
@@ -573,7 +631,7 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
       PC::unpack(gs[i * G + cg], sg);
       funpack(dybs[i * G + cg], db);
 #pragma unroll
-      for (int e = 0; e < CPT; ++e) sg[e] = sigmoidf_(sg[e]);
+      for (int e = 0; e < CPT; ++e) sg[e] = sigmoid_fast(sg[e]);
 #pragma unroll
       for (int e = 0; e < CPT; ++e) ybar[e] = dyh[e] = 0.f;
 #pragma unroll
@@ -665,18 +723,25 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
 // LDS bytes of the tile kernels for chunks of R rows
 inline size_t epi_tile_lds(bool bwd, int D, int H, int K, int cpt, size_t es, int R) {
   const size_t KH = K > 0 ? K - 1 : 0, halo = K > 0 ? R + KH : 0;
-  if (!bwd) return (R + halo) * D * 4 + (size_t)R * D * es;
+  const size_t prm = (size_t)D * (K + 1) * 4;  // local-path parameters, before the chunk loop
+  if (!bwd) {
+    const size_t stage = (R + halo) * D * 4 + (size_t)R * D * es;
+    return stage > prm ? stage : prm;
+  }
   const size_t stage = (2 * R + (R + KH) + halo) * D * 4 + (size_t)R * D * es;
-  const size_t xchg = (size_t)256 * (H > (1 + K) * cpt ? H : (1 + K) * cpt) * 4;
+  size_t xchg = (size_t)256 * (H > (1 + K) * cpt ? H : (1 + K) * cpt) * 4;
+  xchg = xchg > prm ? xchg : prm;
   return stage > xchg ? stage : xchg;
 }
-// Rows per chunk: a multiple of the rows per pass, at least 16 (forward) or 8
-// (backward) where the LDS allows, within 64 KB; 0 when one pass does not fit.
+// Rows per chunk: each thread moves window rows rr + u RP, u < U, so a chunk and
+// its K-1 halo rows fit in U RP rows; within a third of the compute unit's LDS
+// (three blocks resident); 0 when no chunk fits.
+constexpr size_t EPI_TILE_LDS_MAX = 53 * 1024;
 inline int epi_tile_rows(bool bwd, int D, int H, int K, int cpt, size_t es) {
   const TileGeo tg = tile_geo(D, cpt);
-  const int want = bwd ? 8 : 16;
-  for (int m = (want + tg.RP - 1) / tg.RP; m >= 1; --m)
-    if (epi_tile_lds(bwd, D, H, K, cpt, es, tg.RP * m) <= 64 * 1024) return tg.RP * m;
+  const int U = cpt == 1 ? tile_u<1>(bwd) : tile_u<2>(bwd);
+  for (int R = U * tg.RP - (K > 0 ? K - 1 : 0); R >= 1; --R)
+    if (epi_tile_lds(bwd, D, H, K, cpt, es, R) <= EPI_TILE_LDS_MAX) return R;
   return 0;
 }
 // channels per piece of the tile kernels for these shapes, 0 when they do not apply
@@ -695,16 +760,6 @@ static unsigned epi_grid(int64_t items) {
   return (unsigned)(g < 8192 ? (g > 0 ? g : 1) : 8192);
 }
 
-template <typename T, int CPT>
-static void tile_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H, int dh,
-                     int K, const float* Ct, float lambda_c, const float* w, const float* s, hipStream_t st) {
-  const int R = epi_tile_rows(false, H * dh, H, K, CPT, sizeof(T));
-  const int64_t nch = B * ((L + R - 1) / R);
-  hipLaunchKernelGGL((epi_fwd_tile_kernel<T, CPT>), dim3((unsigned)(nch < 4096 ? nch : 4096)), dim3(256),
-                     epi_tile_lds(false, H * dh, H, K, CPT, sizeof(T), R), st, (const T*)y, (const T*)gate,
-                     (const T*)v, (T*)z, B, L, H, dh, K, R, Ct, lambda_c, w, s);
-}
-
 template <typename T, int CPT, int HM>
 static void tile_bwd(const void* y, const void* gate, const void* v, const void* dz, void* dy, void* dgate, void* dv,
                      int64_t B, int64_t L, int H, int dh, int K, const float* Ct, float lambda_c, const float* w,
@@ -716,27 +771,29 @@ static void tile_bwd(const void* y, const void* gate, const void* v, const void*
                      part);
 }
 
+template <typename T, int CPT, int HM, bool WL>
+static void col_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H, int dh,
+                    int K, const float* Ct, float lambda_c, const float* w, const float* s, hipStream_t st) {
+  const int64_t np = dh / CPT, PB = np < 256 ? np : 256, RB = 256 / PB;
+  const int64_t items = (B * L + RB - 1) / RB * ((np + PB - 1) / PB) * 256;  // 256 threads per block step
+  const size_t lds = WL ? (size_t)H * dh * (K + 1) * sizeof(float) : 0;
+  hipLaunchKernelGGL((epi_fwd_col_kernel<T, CPT, HM, WL>), dim3(epi_grid(items)), dim3(256), lds, st,
+                     (const T*)y, (const T*)gate, (const T*)v, (T*)z, B * L, L, H, dh, K, Ct, lambda_c, w, s);
+}
+
 template <typename T>
 hipError_t launch_epi_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H,
                           int dh, int K, const float* Ct, float lambda_c, const float* w, const float* s, int vec,
                           hipStream_t st) {
-  constexpr int WIDE = tile_wide<T>(false);
-  const int cpt = epi_tile_cpt<T>(vec, H * dh, H, K, false);
-  if (cpt == WIDE)
-    tile_fwd<T, WIDE>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
-  else if (cpt == 1)
-    tile_fwd<T, 1>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
-  else {
-    const int64_t rows = B * L;
-    const int ov = vec >= 2 ? 2 : 1;
-    const int64_t items = rows * (int64_t)(H * dh / ov);
-    if (ov == 2)
-      hipLaunchKernelGGL((epi_fwd_kernel<T, 2>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                         (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
-    else
-      hipLaunchKernelGGL((epi_fwd_kernel<T, 1>), dim3(epi_grid(items)), dim3(256), 0, st, (const T*)y,
-                         (const T*)gate, (const T*)v, (T*)z, rows, L, H, dh, K, Ct, lambda_c, w, s);
-  }
+  constexpr int WIDE = 8 / sizeof(T);  // 8-byte pieces: H*CPT accumulators stay in registers
+  if ((size_t)H * dh * (K + 1) * sizeof(float) > 64 * 1024)  // taps read from global memory (cached)
+    col_fwd<T, 1, EPI_H_MAX, false>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
+  else if (H <= 8 && vec >= WIDE && K <= 4)
+    col_fwd<T, WIDE, 8, true>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
+  else if (H <= 8)
+    col_fwd<T, 1, 8, true>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
+  else
+    col_fwd<T, 1, EPI_H_MAX, true>(y, gate, v, z, B, L, H, dh, K, Ct, lambda_c, w, s, st);
   return hipGetLastError();
 }
 
