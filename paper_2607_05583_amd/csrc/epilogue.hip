@@ -135,8 +135,8 @@ __global__ __launch_bounds__(256) void epi_bwd_param_kernel(const T* __restrict_
   const int64_t nblk_t = (L + EPI_ROWS - 1) / EPI_ROWS;
   const int64_t b = blockIdx.x / nblk_t, t0 = (blockIdx.x % nblk_t) * EPI_ROWS;
   const int nr = (int)(L - t0 < EPI_ROWS ? L - t0 : EPI_ROWS);
-  const int P = H * H + D + D * K;
-  float* out = part + (size_t)blockIdx.x * P;
+  // partials are stored column-major: entry e of this block at part[e * gridDim.x + blockIdx.x]
+  auto out = [&](int e) -> float& { return part[(size_t)e * gridDim.x + blockIdx.x]; };
   for (int cb = 0; cb < D; cb += blockDim.x) {
     const int c = cb + threadIdx.x;
     const bool live = c < D;
@@ -171,10 +171,10 @@ __global__ __launch_bounds__(256) void epi_bwd_param_kernel(const T* __restrict_
         }
       }
       if (K > 0) {
-        out[H * H + c] = ds;
+        out(H * H + c) = ds;
 #pragma unroll
         for (int k = 0; k < EPI_K_MAX; ++k)
-          if (k < K) out[H * H + D + c * K + k] = dw[k];
+          if (k < K) out(H * H + D + c * K + k) = dw[k];
       }
     }
     // dC[g, h] += sum over this channel block's channels of head g, in order
@@ -184,12 +184,12 @@ __global__ __launch_bounds__(256) void epi_bwd_param_kernel(const T* __restrict_
     __syncthreads();
     for (int e = threadIdx.x; e < H * H; e += blockDim.x) {
       const int gg = e / H, h = e % H;
-      float acc = cb == 0 ? 0.f : out[e];
+      float acc = cb == 0 ? 0.f : out(e);
       for (int q = 0; q < (int)blockDim.x; ++q) {
         const int cc = cb + q;
         if (cc < D && cc / dh == gg) acc += sdc[q * EPI_H_MAX + h];
       }
-      out[e] = acc;
+      out(e) = acc;
     }
     __syncthreads();
   }
@@ -199,29 +199,30 @@ __global__ __launch_bounds__(256) void epi_bwd_param_kernel(const T* __restrict_
 // the coupling map.  A block takes 16 partial columns; its 16 row groups each sum
 // every 16th block partial (two interleaved accumulators), and the row groups
 // are added in order.
-__global__ __launch_bounds__(256) void epi_bwd_reduce_kernel(const float* __restrict__ part, int64_t nblk, int H,
+// One wave per partial column (the partials are column-major, so a column is
+// contiguous): lane l sums partial rows l, l + 64, ... in float64 with four
+// accumulators in a fixed order, then the lane sums meet in a fixed shuffle tree.
+__global__ __launch_bounds__(256) void epi_bwd_reduce_kernel(const float* __restrict__ part, int64_t nparts, int H,
                                                              int D, int K, const float* __restrict__ Ct,
                                                              float lambda_c, float* __restrict__ dCt,
                                                              float* __restrict__ dw, float* __restrict__ ds,
                                                              double* __restrict__ lam_terms) {
   const int P = H * H + D + D * K;
-  const int cl = threadIdx.x % 16, rg = threadIdx.x / 16;
-  const int col = blockIdx.x * 16 + cl;
-  __shared__ double s_acc[256];
-  double a0 = 0.0, a1 = 0.0;
-  if (col < P) {
-    int64_t k = rg;
-    for (; k + 16 < nblk; k += 32) {
-      a0 += part[(size_t)k * P + col];
-      a1 += part[(size_t)(k + 16) * P + col];
-    }
-    if (k < nblk) a0 += part[(size_t)k * P + col];
+  const int lane = threadIdx.x & 63, col = blockIdx.x * 4 + threadIdx.x / 64;
+  if (col >= P) return;  // the whole wave: no barrier follows
+  const float* pc = part + (size_t)col * nparts;
+  double a0 = 0.0, a1 = 0.0, a2 = 0.0, a3 = 0.0;
+  int64_t k = lane;
+  for (; k + 192 < nparts; k += 256) {
+    a0 += pc[k];
+    a1 += pc[k + 64];
+    a2 += pc[k + 128];
+    a3 += pc[k + 192];
   }
-  s_acc[threadIdx.x] = a0 + a1;
-  __syncthreads();
-  if (rg != 0 || col >= P) return;
-  double acc = 0.0;
-  for (int r = 0; r < 16; ++r) acc += s_acc[r * 16 + cl];
+  for (; k < nparts; k += 64) a0 += pc[k];
+  double acc = (a0 + a1) + (a2 + a3);
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_down(acc, off, 64);
+  if (lane != 0) return;
   if (col < H * H) {
     const double th = tanh((double)Ct[col]);
     dCt[col] = (float)(acc * (double)lambda_c / sqrt((double)H) * (1.0 - th * th));
@@ -233,11 +234,13 @@ __global__ __launch_bounds__(256) void epi_bwd_reduce_kernel(const float* __rest
   }
 }
 
-// dlambda_c = sum_{g,h} dC[g,h] tanh(Ct[g,h]) / sqrt(H), summed in order (one thread)
-__global__ void epi_bwd_lambda_kernel(const double* __restrict__ lam_terms, int H, float* __restrict__ dlambda_c) {
+// dlambda_c = sum_{g,h} dC[g,h] tanh(Ct[g,h]) / sqrt(H), one wave, fixed order
+__global__ __launch_bounds__(64) void epi_bwd_lambda_kernel(const double* __restrict__ lam_terms, int H,
+                                                            float* __restrict__ dlambda_c) {
   double u = 0.0;
-  for (int i = 0; i < H * H; ++i) u += lam_terms[i];
-  *dlambda_c = (float)(u / sqrt((double)H));
+  for (int i = threadIdx.x; i < H * H; i += 64) u += lam_terms[i];
+  for (int off = 32; off > 0; off >>= 1) u += __shfl_down(u, off, 64);
+  if (threadIdx.x == 0) *dlambda_c = (float)(u / sqrt((double)H));
 }
 
 // ---------------------------------------------------------------------------
@@ -679,8 +682,8 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
     }
   }
   // block partial [H*H dC | D ds | D*K dw]; sums over threads in a fixed order
-  const int PW = H * H + D + D * K;
-  float* out = part + (size_t)blockIdx.x * PW;
+  // stored column-major: entry e of this block at part[e * gridDim.x + blockIdx.x]
+  auto out = [&](int e) -> float& { return part[(size_t)e * gridDim.x + blockIdx.x]; };
   float* sx = reinterpret_cast<float*>(smem);
   __syncthreads();
 #pragma unroll
@@ -693,7 +696,7 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
     float acc = 0.f;
     for (int r = 0; r < RP; ++r)
       for (int q = gg * gpp; q < (gg + 1) * gpp; ++q) acc += sx[(r * G + q) * H + h];
-    out[e] = acc;
+    out(e) = acc;
   }
   if (K == 0) return;
   __syncthreads();
@@ -714,9 +717,9 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
     float acc = 0.f;
     for (int r = 0; r < RP; ++r) acc += sx[(r * G + q) * NX + f * CPT + e];
     if (f == 0)
-      out[H * H + c] = acc;
+      out(H * H + c) = acc;
     else
-      out[H * H + D + c * K + (f - 1)] = acc;
+      out(H * H + D + c * K + (f - 1)) = acc;
   }
 }
 
@@ -839,10 +842,10 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
   }
   const int P = H * H + H * dh + H * dh * K;
   double* lam_terms = reinterpret_cast<double*>(part + epi_part_floats(B, L, H, dh, K));
-  hipLaunchKernelGGL(epi_bwd_reduce_kernel, dim3((unsigned)((P + 15) / 16)), dim3(256), 0, st, part, nparts, H,
+  hipLaunchKernelGGL(epi_bwd_reduce_kernel, dim3((unsigned)((P + 3) / 4)), dim3(256), 0, st, part, nparts, H,
                      H * dh, K, Ct, lambda_c, dCt, dw, ds, lam_terms);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  hipLaunchKernelGGL(epi_bwd_lambda_kernel, dim3(1), dim3(1), 0, st, lam_terms, H, dlambda_c);
+  hipLaunchKernelGGL(epi_bwd_lambda_kernel, dim3(1), dim3(64), 0, st, lam_terms, H, dlambda_c);
   return hipGetLastError();
 }
 
