@@ -225,6 +225,41 @@ def main():
     dec_graph_us = d0.elapsed_time(d1) * 1e3 / (reps * G)
     dec_bytes = Bd * Dd * (Md * 16 + 2 + 2)
     log(f"decode: eager {dec_eager_us:.2f} us/step, graph {dec_graph_us:.2f} us/step")
+    # several steps per launch, for drives known in advance: 8 drafted tokens to
+    # verify per launch, and a long run of known drives in one launch
+    xbn = xdec.permute(1, 0, 2).contiguous()  # [B, N, D]
+    ybn = torch.empty_like(xbn)
+    xk = xbn[:, :8].contiguous()
+    yk = torch.empty_like(xk)
+    st_ms = state.clone()
+    msp = ctypes.c_void_p(st_ms.data_ptr())
+
+    def msteps(xt, yt):
+        _lib.check(lib.resonator_decode_steps(ctypes.c_void_p(xt.data_ptr()), _lib.RES_BF16,
+                                              ctypes.c_void_p(yt.data_ptr()), _lib.RES_BF16, Bd, xt.shape[1],
+                                              Dd, Md, *DP, msp, sp))
+
+    for _ in range(5):
+        msteps(xk, yk)
+    msteps(xbn, ybn)
+    torch.cuda.synchronize()
+    nk = 2000
+    d0.record(stream)
+    for _ in range(nk):
+        msteps(xk, yk)
+    d1.record(stream)
+    torch.cuda.synchronize()
+    k8_us = d0.elapsed_time(d1) * 1e3 / nk
+    nl = 5
+    d0.record(stream)
+    for _ in range(nl):
+        msteps(xbn, ybn)
+    d1.record(stream)
+    torch.cuda.synchronize()
+    long_us = d0.elapsed_time(d1) * 1e3 / (nl * xbn.shape[1])
+    log(f"decode, several steps per launch: 8 steps {k8_us:.2f} us per launch ({k8_us / 8:.2f} us/step), "
+        f"{xbn.shape[1]} steps {long_us:.3f} us/step")
+    del xbn, ybn, st_ms
 
     # ---------------- training layer (fwd + bwd) ----------------
     c5 = W.CONFIGS[5]
@@ -297,6 +332,9 @@ def main():
         "config": {"workload": cfg.name, "B": B, "L": L, "D": D, "M": M,
                    "activations": "bf16 in/out, fp32 accumulate, split-bf16 MFMA operands",
                    "terminal_state": True, "buffer_sets": NSET},
+        "decode_multi_step": {"workload": f"{c4.name}: drives known in advance",
+                              "k8_us_per_launch": k8_us, "k8_us_per_step": k8_us / 8,
+                              "long_steps_per_launch": int(xdec.shape[0]), "long_us_per_step": long_us},
         "decode": {"workload": c4.name, "steps": nsteps,
                    "steps_per_s_eager": 1e6 / dec_eager_us, "us_per_step_eager": dec_eager_us,
                    "steps_per_s_graph": 1e6 / dec_graph_us, "us_per_step_graph": dec_graph_us,

@@ -137,6 +137,20 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
                           const float* amp, const float* phase, float* state, void* stream);
 
 /*
+ * N decode steps in one launch, for drives known in advance (a prompt chunk,
+ * drafted tokens to verify) (Sec. 3.3):
+ *   for n = 0 .. N-1:  state <- lambda state + x[:, n];  y[:, n] = Re sum_m c state.
+ *   x      [B][N][D] of x_dt;  y [B][N][D] of y_dt (not overlapping x or state)
+ *   state  [B][D][M][2] float32, read once and written once, in place
+ * Each step uses the constants, arithmetic and order of resonator_decode_step,
+ * so the results are bitwise those of N calls of it.  Supported (x_dt, y_dt) as
+ * for resonator_mix_fwd.  N >= 1, B <= 262140.  Needs no workspace.
+ */
+int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t N,
+                           int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                           const float* phase, float* state, void* stream);
+
+/*
  * Mixer epilogue around the mixing output (Sec. 3.4, head coupling and local
  * lexical path; the gate of Sec. 3.1's last paragraph):
  *   C = I + (lambda_c / sqrt(H)) tanh(Ct)                          (coupling eq.)

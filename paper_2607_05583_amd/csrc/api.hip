@@ -419,6 +419,35 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
   return e == hipSuccess ? RES_OK : hip_fail(e, "decode launch");
 }
 
+int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t N,
+                           int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                           const float* phase, float* state, void* stream) {
+  int rc = check_sizes(B, N, D, M, false);
+  if (rc) return rc;
+  if (B > 4 * 65535LL) return fail(RES_ERR_UNSUPPORTED, "B must be <= %lld for this launch (got %lld)",
+                                   4 * 65535LL, (long long)B);
+  if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (x_dt == RES_F32 && y_dt == RES_BF16)
+    return fail(RES_ERR_UNSUPPORTED, "dtype pair f32 -> bf16 is not supported");
+  if (!x || !y || !state) return fail(RES_ERR_INVALID_ARG, "x, y and state must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  if (!aligned(x, elt_size(x_dt)) || !aligned(y, elt_size(y_dt)) || !aligned(state, 8))
+    return fail(RES_ERR_MISALIGNED, "x/y aligned to their element, state to 8 bytes");
+  const size_t n = (size_t)(B * N * D);
+  if (overlap(y, n * elt_size(y_dt), x, n * elt_size(x_dt)) ||
+      overlap(y, n * elt_size(y_dt), state, (size_t)(B * D * M) * 8))
+    return fail(RES_ERR_INVALID_ARG, "y must not overlap x or state");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (x_dt == RES_F32)
+    e = launch_decode_steps<float, float>(B, N, D, M, x, y, gamma, omega, amp, phase, state, st);
+  else if (y_dt == RES_BF16)
+    e = launch_decode_steps<bf16_t, bf16_t>(B, N, D, M, x, y, gamma, omega, amp, phase, state, st);
+  else
+    e = launch_decode_steps<bf16_t, float>(B, N, D, M, x, y, gamma, omega, amp, phase, state, st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "decode steps launch");
+}
+
 // ---------------------------------------------------------------------------
 // Mixer epilogue (Sec. 3.4)
 // ---------------------------------------------------------------------------

@@ -14,6 +14,17 @@ namespace res {
 constexpr int DEC_CH = 4;
 constexpr int DEC_ROWS = 64;
 
+// One mode's update h <- (hi + lo) h + x and its readout term, with explicit
+// fused multiply-adds so that every decode kernel rounds alike.
+__device__ __forceinline__ float2 mode_step(float2 h, float2 hi, float2 lo, float xv) {
+  const float tx = fmaf(lo.x, h.x, -(lo.y * h.y));
+  const float ty = fmaf(lo.x, h.y, lo.y * h.x);
+  return make_float2(fmaf(hi.x, h.x, fmaf(-hi.y, h.y, tx + xv)), fmaf(hi.x, h.y, fmaf(hi.y, h.x, ty)));
+}
+__device__ __forceinline__ float mode_readout(float2 c, float2 hn, float yv) {
+  return fmaf(c.x, hn.x, fmaf(-c.y, hn.y, yv));
+}
+
 template <typename TX, typename TY, int MF>
 __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
     const TX* __restrict__ x, TY* __restrict__ y, int B, int D, int M,
@@ -73,11 +84,10 @@ __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int m = 2 * i + j;
-        const float2 hi = lhi[dl][m], lo = llo[dl][m], c = cs[dl][m];
-        const float2 t = cmul(lo, make_float2(h[2 * j], h[2 * j + 1]));
-        hn[2 * j] = fmaf(hi.x, h[2 * j], fmaf(-hi.y, h[2 * j + 1], t.x + xf));
-        hn[2 * j + 1] = fmaf(hi.x, h[2 * j + 1], fmaf(hi.y, h[2 * j], t.y));
-        yv = fmaf(c.x, hn[2 * j], fmaf(-c.y, hn[2 * j + 1], yv));
+        const float2 r = mode_step(make_float2(h[2 * j], h[2 * j + 1]), lhi[dl][m], llo[dl][m], xf);
+        hn[2 * j] = r.x;
+        hn[2 * j + 1] = r.y;
+        yv = mode_readout(cs[dl][m], r, yv);
       }
       sv[i] = make_float4(hn[0], hn[1], hn[2], hn[3]);
     }
@@ -87,14 +97,9 @@ __global__ __launch_bounds__(DEC_CH* DEC_ROWS) void decode_kernel(
   const float xv = to_f32(x[row]);
   float2* st = reinterpret_cast<float2*>(state) + row * M;
   for (int m = 0; m < M; ++m) {
-    const float2 h = st[m];
-    const float2 hi = lhi[dl][m], lo = llo[dl][m], c = cs[dl][m];
-    const float2 t = cmul(lo, h);
-    float2 hn;
-    hn.x = fmaf(hi.x, h.x, fmaf(-hi.y, h.y, t.x + xv));
-    hn.y = fmaf(hi.x, h.y, fmaf(hi.y, h.x, t.y));
+    const float2 hn = mode_step(st[m], lhi[dl][m], llo[dl][m], xv);
     st[m] = hn;
-    yv = fmaf(c.x, hn.x, fmaf(-c.y, hn.y, yv));
+    yv = mode_readout(cs[dl][m], hn, yv);
   }
   y[row] = from_f32<TY>(yv);
 }
@@ -124,5 +129,124 @@ template hipError_t launch_decode<bf16_t, bf16_t>(int64_t, int64_t, int64_t, con
 template hipError_t launch_decode<bf16_t, float>(int64_t, int64_t, int64_t, const void*, void*,
                                                  const float*, const float*, const float*,
                                                  const float*, float*, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Several decode steps in one launch, for drives known in advance (a prompt
+// chunk, drafted tokens to verify).  Step n applies the update and readout of
+// decode_kernel with the same constants and in the same order, so N steps here
+// give the same bits as N single steps.  A thread owns one (b, d) and keeps its
+// M modes in registers for all N steps; a wave covers 64 consecutive channels
+// of one batch row, so every step's drive and output rows are coalesced, and
+// the next step's drive is loaded before the current step is computed.
+// ---------------------------------------------------------------------------
+constexpr int DMS_CH = 64;
+constexpr int DMS_ROWS = 4;
+
+template <typename TX, typename TY, int MM>
+__global__ __launch_bounds__(DMS_CH* DMS_ROWS) void decode_steps_kernel(
+    const TX* __restrict__ x, TY* __restrict__ y, int B, int64_t N, int D, int M,
+    const float* __restrict__ gamma, const float* __restrict__ omega, const float* __restrict__ amp,
+    const float* __restrict__ phase, float* __restrict__ state) {
+  __shared__ float2 lhi[DMS_CH][MM], llo[DMS_CH][MM], cs[DMS_CH][MM];
+  const int tid = threadIdx.x;
+  const int d0 = blockIdx.x * DMS_CH;
+  const int b0 = blockIdx.y * DMS_ROWS;
+  for (int t = tid; t < DMS_CH * M; t += blockDim.x) {
+    const int dl = t / M, m = t % M, d = d0 + dl;
+    float2 hi = make_float2(0.f, 0.f), lo = hi, c = hi;
+    if (d < D) {
+      const double g = gamma[d * M + m], w = omega[d * M + m];
+      const double a = amp[d * M + m], ph = phase[d * M + m];
+      double s, co;
+      sincos(w, &s, &co);
+      const double e = exp(-g);
+      const double lr = e * co, lim = e * s;
+      hi = make_float2((float)lr, (float)lim);
+      lo = make_float2((float)(lr - (double)hi.x), (float)(lim - (double)hi.y));
+      sincos(ph, &s, &co);
+      c = make_float2((float)(a * co), (float)(a * s));
+    }
+    lhi[dl][m] = hi;
+    llo[dl][m] = lo;
+    cs[dl][m] = c;
+  }
+  __syncthreads();
+  const int dl = tid % DMS_CH;
+  const int b = b0 + tid / DMS_CH;
+  const int d = d0 + dl;
+  if (b >= B || d >= D) return;  // no barrier follows
+  float2 h[MM], hi[MM], lo[MM], c[MM];
+  float2* st = reinterpret_cast<float2*>(state) + ((size_t)b * D + d) * M;
+#pragma unroll
+  for (int m = 0; m < MM; ++m) {
+    if (m < M) {
+      h[m] = st[m];
+      hi[m] = lhi[dl][m];
+      lo[m] = llo[dl][m];
+      c[m] = cs[dl][m];
+    }
+  }
+  const TX* xr = x + (size_t)b * N * D + d;
+  TY* yr = y + (size_t)b * N * D + d;
+  // Drives of the next DPF steps are loaded while the current DPF are computed.
+  // Past the last step the index is clamped to it (the value is not used), so
+  // the loads are unconditional and none waits behind a branch.
+  constexpr int DPF = 8;
+  TX xb[DPF];
+#pragma unroll
+  for (int j = 0; j < DPF; ++j) xb[j] = xr[(j < N ? (int64_t)j : N - 1) * D];
+  for (int64_t n0 = 0; n0 < N; n0 += DPF) {
+    TX xn[DPF];
+#pragma unroll
+    for (int j = 0; j < DPF; ++j) {
+      const int64_t nn = n0 + DPF + j;
+      xn[j] = xr[(nn < N ? nn : N - 1) * D];
+    }
+#pragma unroll
+    for (int j = 0; j < DPF; ++j) {
+      if (n0 + j < N) {
+        float yv = 0.f;
+#pragma unroll
+        for (int m = 0; m < MM; ++m) {
+          if (m < M) {
+            h[m] = mode_step(h[m], hi[m], lo[m], to_f32(xb[j]));
+            yv = mode_readout(c[m], h[m], yv);
+          }
+        }
+        yr[(n0 + j) * D] = from_f32<TY>(yv);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < DPF; ++j) xb[j] = xn[j];
+  }
+#pragma unroll
+  for (int m = 0; m < MM; ++m)
+    if (m < M) st[m] = h[m];
+}
+
+template <typename TX, typename TY>
+hipError_t launch_decode_steps(int64_t B, int64_t N, int64_t D, int64_t M, const void* x, void* y,
+                               const float* gamma, const float* omega, const float* amp,
+                               const float* phase, float* state, hipStream_t st) {
+  const dim3 grid((unsigned)((D + DMS_CH - 1) / DMS_CH), (unsigned)((B + DMS_ROWS - 1) / DMS_ROWS));
+  if (M <= 8)
+    hipLaunchKernelGGL((decode_steps_kernel<TX, TY, 8>), grid, dim3(DMS_CH * DMS_ROWS), 0, st,
+                       reinterpret_cast<const TX*>(x), reinterpret_cast<TY*>(y), (int)B, N, (int)D,
+                       (int)M, gamma, omega, amp, phase, state);
+  else
+    hipLaunchKernelGGL((decode_steps_kernel<TX, TY, RES_M_MAX_DEV>), grid, dim3(DMS_CH * DMS_ROWS), 0, st,
+                       reinterpret_cast<const TX*>(x), reinterpret_cast<TY*>(y), (int)B, N, (int)D,
+                       (int)M, gamma, omega, amp, phase, state);
+  return hipGetLastError();
+}
+
+#define RES_DECODE_STEPS_INST(TX, TY)                                                                   \
+  template hipError_t launch_decode_steps<TX, TY>(int64_t, int64_t, int64_t, int64_t, const void*, void*, \
+                                                  const float*, const float*, const float*, const float*, \
+                                                  float*, hipStream_t);
+RES_DECODE_STEPS_INST(float, float)
+RES_DECODE_STEPS_INST(bf16_t, bf16_t)
+RES_DECODE_STEPS_INST(bf16_t, float)
+#undef RES_DECODE_STEPS_INST
 
 }  // namespace res

@@ -106,6 +106,10 @@ template <typename TX, typename TY>
 hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y,
                          const float* gamma, const float* omega, const float* amp,
                          const float* phase, float* state, hipStream_t st);
+template <typename TX, typename TY>
+hipError_t launch_decode_steps(int64_t B, int64_t N, int64_t D, int64_t M, const void* x, void* y,
+                               const float* gamma, const float* omega, const float* amp,
+                               const float* phase, float* state, hipStream_t st);
 
 template <typename TX>
 hipError_t launch_bwd_tile(const Geometry& g, int mode, const BwdArgs& a, hipStream_t st,

@@ -157,6 +157,24 @@ def resonator_decode_step(x_t, gamma, omega, amp, phase, state, out_dtype=None, 
     return y
 
 
+def resonator_decode_steps(x, gamma, omega, amp, phase, state, out_dtype=None, out=None):
+    """N decode steps in one launch: x [B, N, D] drives known in advance; updates
+    state [B, D, M, 2] in place and returns y [B, N, D] (bitwise N decode steps)."""
+    _dev(x, "x")
+    _dev(state, "state")
+    B, N, D = x.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    if state.dtype != torch.float32 or tuple(state.shape) != (B, D, M, 2):
+        raise ValueError("state must be float32 [B, D, M, 2]")
+    out_dtype = x.dtype if out_dtype is None else out_dtype
+    y = out if out is not None else torch.empty((B, N, D), dtype=out_dtype, device=x.device)
+    check(_lib.lib().resonator_decode_steps(
+        _ptr(x), _code(x), _ptr(y), _code(y), B, N, D, M, _ptr(gamma), _ptr(omega), _ptr(amp),
+        _ptr(phase), _ptr(state), _stream(x.device)))
+    return y
+
+
 class ResonatorMixFunction(torch.autograd.Function):
     """Autograd wrapper: forward = resonator_mix_fwd, backward = resonator_mix_bwd."""
 

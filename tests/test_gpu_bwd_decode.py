@@ -130,6 +130,32 @@ def test_decode_small(B, D, M, L0, steps, seed, act, out):
     assert rel_err(host(st), hr) <= (1e-4 if act == "f32" else 2e-2)
 
 
+@pytest.mark.parametrize("B,D,M,L0,steps,seed", [(1, 1, 1, 0, 1, 61), (3, 7, 3, 10, 40, 62),
+                                                 (64, 256, 8, 300, 200, 63), (5, 70, 16, 1, 64, 64),
+                                                 (9, 130, 5, 0, 33, 65)])
+@pytest.mark.parametrize("act,out", [("f32", "f32"), ("bf16", "bf16"), ("bf16", "f32")])
+def test_decode_steps(B, D, M, L0, steps, seed, act, out):
+    """N steps in one launch: bitwise the same outputs and state as N single decode
+    steps, and within the decode tolerance of the oracle recurrence."""
+    say(f"decode steps B={B} D={D} M={M} L0={L0} steps={steps} {act}->{out}")
+    prob = W.random_problem(seed, B, L0 + steps, D, M, act=act, gamma_range=(1e-4, 1.0),
+                            gamma_log=True)
+    x = dev_act(prob["x"], act)
+    pr = params_dev(prob)
+    od = torch.float32 if out == "f32" else x.dtype
+    st1 = ops.resonator_state_init(x[:, :L0].contiguous(), *pr)
+    st2 = st1.clone()
+    ys = [ops.resonator_decode_step(x[:, t].contiguous(), *pr, st1, out_dtype=od)
+          for t in range(L0, L0 + steps)]
+    yn = ops.resonator_decode_steps(x[:, L0:].contiguous(), *pr, st2, out_dtype=od)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.stack(ys, 1), yn)
+    assert torch.equal(st1, st2)
+    yr, hr = O.mix_recurrence(act64(prob["x"], act), *params_np(prob))
+    assert rel_err(host(yn), yr[:, L0:]) <= tol(act, out)
+    assert rel_err(host(st2), hr) <= (1e-4 if act == "f32" else 2e-2)
+
+
 def test_config4_decode_full():
     """Decode config: prompt 1024 -> state_init, then 32768 decode steps at B64 D256 M8 (bf16).
 
