@@ -56,10 +56,12 @@ def params_map(theta_gamma, theta_omega, alpha_min: float = ALPHA_MIN):
 
 def params_map_bwd(theta_gamma, theta_omega, dgamma, domega):
     """Chain rule of ``params_map``: d/dtheta softplus = sigmoid, d/dtheta pi sigmoid
-    = pi sigmoid (1 - sigmoid)."""
+    = pi sigmoid (1 - sigmoid), written as pi sigmoid(u) sigmoid(-u) (the same value,
+    without the cancellation of 1 - sigmoid for large u)."""
     sg = _sigmoid(theta_gamma)
-    so = _sigmoid(theta_omega)
-    return np.asarray(dgamma, dtype=np.float64) * sg, np.asarray(domega, dtype=np.float64) * math.pi * so * (1.0 - so)
+    tw = np.asarray(theta_omega, dtype=np.float64)
+    return (np.asarray(dgamma, dtype=np.float64) * sg,
+            np.asarray(domega, dtype=np.float64) * math.pi * _sigmoid(tw) * _sigmoid(-tw))
 
 
 def _log_spaced(lo: float, hi: float, n: int):
