@@ -151,6 +151,40 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
                            const float* phase, float* state, void* stream);
 
 /*
+ * Constrained parameterization (Sec. 3.1, last paragraph): unconstrained
+ * parameters are mapped into the valid ranges of the damping and frequency,
+ *   gamma = alpha_min + softplus(theta_gamma)      (> alpha_min; the paper's floor is 1e-4)
+ *   omega = pi * sigmoid(theta_omega)              (in (0, pi))
+ * amplitude and phase are used as they are.  Arrays are float32 of n elements
+ * (the [D][M] bank flattened), device memory, caller-owned; outputs must not
+ * overlap each other.  n in [1, 2^31].
+ */
+int resonator_params_map(const float* theta_gamma, const float* theta_omega, int64_t n, float alpha_min,
+                         float* gamma, float* omega, void* stream);
+
+/*
+ * Chain rule of resonator_params_map:
+ *   dtheta_gamma = dgamma * sigmoid(theta_gamma)
+ *   dtheta_omega = domega * pi * sigmoid(theta_omega) * (1 - sigmoid(theta_omega))
+ * Same array conventions; the two outputs must not overlap.
+ */
+int resonator_params_map_bwd(const float* theta_gamma, const float* theta_omega, const float* dgamma,
+                             const float* domega, int64_t n, float* dtheta_gamma, float* dtheta_omega,
+                             void* stream);
+
+/*
+ * Initialization with log-spaced timescales (Sec. 3.1, last paragraph): writes
+ * theta_gamma, theta_omega [D][M] whose mapped values have half-lives
+ * ln 2 / gamma log-spaced from hl_min to hl_max and periods 2 pi / omega
+ * log-spaced from per_max down to per_min, over the M modes of every channel
+ * (over the D channels when M = 1, one mode per head as in the paper).  Needs
+ * 0 < hl_min <= hl_max, 2 <= per_min <= per_max and ln 2 / hl_max > alpha_min.
+ * The paper reports half-lives from about 2 to 2048 tokens.
+ */
+int resonator_params_init(int64_t D, int64_t M, double hl_min, double hl_max, double per_min, double per_max,
+                          float alpha_min, float* theta_gamma, float* theta_omega, void* stream);
+
+/*
  * Mixer epilogue around the mixing output (Sec. 3.4, head coupling and local
  * lexical path; the gate of Sec. 3.1's last paragraph):
  *   C = I + (lambda_c / sqrt(H)) tanh(Ct)                          (coupling eq.)

@@ -20,7 +20,8 @@ RES_M_MAX = 16
 SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd",
            "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
-           "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps")
+           "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
+           "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init")
 
 _lib = None
 
@@ -59,6 +60,13 @@ def _declare(lib):
                                            fp, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_decode_step.restype = i32
     lib.resonator_decode_step.argtypes = [vp, i32, vp, i32, i64, i64, i64, fp, fp, fp, fp, fp, vp]
+    lib.resonator_params_map.restype = i32
+    lib.resonator_params_map.argtypes = [fp, fp, i64, f32, fp, fp, vp]
+    lib.resonator_params_map_bwd.restype = i32
+    lib.resonator_params_map_bwd.argtypes = [fp, fp, fp, fp, i64, fp, fp, vp]
+    lib.resonator_params_init.restype = i32
+    lib.resonator_params_init.argtypes = [i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
+                                          ctypes.c_double, f32, fp, fp, vp]
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

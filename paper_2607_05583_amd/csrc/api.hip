@@ -1,6 +1,7 @@
 // C ABI of the resonant mixing library: argument validation, workspace layout
 // and kernel dispatch.  Declared in include/resonator.h.
 #include <cstdarg>
+#include <cmath>
 #include <initializer_list>
 #include <cstdio>
 #include <string>
@@ -446,6 +447,69 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
   else
     e = launch_decode_steps<bf16_t, float>(B, N, D, M, x, y, gamma, omega, amp, phase, state, st);
   return e == hipSuccess ? RES_OK : hip_fail(e, "decode steps launch");
+}
+
+// ---------------------------------------------------------------------------
+// Constrained parameterization (Sec. 3.1, last paragraph)
+// ---------------------------------------------------------------------------
+static int prm_check_n(int64_t n) {
+  if (n < 1 || n > (1LL << 31)) return fail(RES_ERR_INVALID_ARG, "n must be in [1, 2^31] (got %lld)", (long long)n);
+  return RES_OK;
+}
+
+int resonator_params_map(const float* theta_gamma, const float* theta_omega, int64_t n, float alpha_min,
+                         float* gamma, float* omega, void* stream) {
+  int rc = prm_check_n(n);
+  if (rc) return rc;
+  if (!theta_gamma || !theta_omega || !gamma || !omega)
+    return fail(RES_ERR_INVALID_ARG, "theta_gamma, theta_omega, gamma and omega must be non-null");
+  if (!(alpha_min >= 0.f) || !std::isfinite(alpha_min))
+    return fail(RES_ERR_INVALID_ARG, "alpha_min must be finite and >= 0");
+  for (const void* q : {(const void*)theta_gamma, (const void*)theta_omega, (const void*)gamma, (const void*)omega})
+    if (!aligned(q, 4)) return fail(RES_ERR_MISALIGNED, "arrays must be 4-byte aligned");
+  const size_t b = (size_t)n * 4;
+  if (overlap(gamma, b, omega, b)) return fail(RES_ERR_INVALID_ARG, "gamma and omega must not overlap");
+  const hipError_t e = launch_params_map(theta_gamma, theta_omega, n, alpha_min, gamma, omega, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "parameter map launch");
+}
+
+int resonator_params_map_bwd(const float* theta_gamma, const float* theta_omega, const float* dgamma,
+                             const float* domega, int64_t n, float* dtheta_gamma, float* dtheta_omega,
+                             void* stream) {
+  int rc = prm_check_n(n);
+  if (rc) return rc;
+  if (!theta_gamma || !theta_omega || !dgamma || !domega || !dtheta_gamma || !dtheta_omega)
+    return fail(RES_ERR_INVALID_ARG, "all arrays must be non-null");
+  for (const void* q : {(const void*)theta_gamma, (const void*)theta_omega, (const void*)dgamma,
+                        (const void*)domega, (const void*)dtheta_gamma, (const void*)dtheta_omega})
+    if (!aligned(q, 4)) return fail(RES_ERR_MISALIGNED, "arrays must be 4-byte aligned");
+  const size_t b = (size_t)n * 4;
+  if (overlap(dtheta_gamma, b, dtheta_omega, b))
+    return fail(RES_ERR_INVALID_ARG, "dtheta_gamma and dtheta_omega must not overlap");
+  const hipError_t e = launch_params_map_bwd(theta_gamma, theta_omega, dgamma, domega, n, dtheta_gamma,
+                                             dtheta_omega, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "parameter map backward launch");
+}
+
+int resonator_params_init(int64_t D, int64_t M, double hl_min, double hl_max, double per_min, double per_max,
+                          float alpha_min, float* theta_gamma, float* theta_omega, void* stream) {
+  if (D < 1 || M < 1 || D * M > (1LL << 31))
+    return fail(RES_ERR_INVALID_ARG, "need D, M >= 1 and D M <= 2^31 (got D=%lld M=%lld)", (long long)D,
+                (long long)M);
+  if (!theta_gamma || !theta_omega) return fail(RES_ERR_INVALID_ARG, "theta_gamma and theta_omega must be non-null");
+  if (!aligned(theta_gamma, 4) || !aligned(theta_omega, 4))
+    return fail(RES_ERR_MISALIGNED, "arrays must be 4-byte aligned");
+  if (!(hl_min > 0.0) || !(hl_max >= hl_min) || !(per_min >= 2.0) || !(per_max >= per_min) ||
+      !std::isfinite(hl_max) || !std::isfinite(per_max) || !(alpha_min >= 0.f))
+    return fail(RES_ERR_INVALID_ARG, "need 0 < hl_min <= hl_max, 2 <= per_min <= per_max, alpha_min >= 0");
+  if (!(std::log(2.0) / hl_max > (double)alpha_min))
+    return fail(RES_ERR_INVALID_ARG, "the longest half-life must map above alpha_min (ln 2 / hl_max > alpha_min)");
+  const size_t b = (size_t)(D * M) * 4;
+  if (overlap(theta_gamma, b, theta_omega, b))
+    return fail(RES_ERR_INVALID_ARG, "theta_gamma and theta_omega must not overlap");
+  const hipError_t e = launch_params_init(D, M, hl_min, hl_max, per_min, per_max, (double)alpha_min, theta_gamma,
+                                          theta_omega, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "parameter init launch");
 }
 
 // ---------------------------------------------------------------------------

@@ -106,6 +106,12 @@ template <typename TX, typename TY>
 hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y,
                          const float* gamma, const float* omega, const float* amp,
                          const float* phase, float* state, hipStream_t st);
+hipError_t launch_params_map(const float* tg, const float* tw, int64_t n, float alpha_min, float* gamma,
+                             float* omega, hipStream_t st);
+hipError_t launch_params_map_bwd(const float* tg, const float* tw, const float* dg, const float* dw, int64_t n,
+                                 float* dtg, float* dtw, hipStream_t st);
+hipError_t launch_params_init(int64_t D, int64_t M, double hl_min, double hl_max, double per_min, double per_max,
+                              double alpha_min, float* tg, float* tw, hipStream_t st);
 template <typename TX, typename TY>
 hipError_t launch_decode_steps(int64_t B, int64_t N, int64_t D, int64_t M, const void* x, void* y,
                                const float* gamma, const float* omega, const float* amp,

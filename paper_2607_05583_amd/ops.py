@@ -175,6 +175,63 @@ def resonator_decode_steps(x, gamma, omega, amp, phase, state, out_dtype=None, o
     return y
 
 
+ALPHA_MIN = 1e-4  # the paper's floor on the damping
+
+
+def _f32_pair(a, b, name_a, name_b):
+    _dev(a, name_a)
+    _dev(b, name_b)
+    if a.dtype != torch.float32 or b.dtype != torch.float32 or a.shape != b.shape:
+        raise ValueError(f"{name_a} and {name_b} must be float32 of one shape")
+
+
+def resonator_params_map(theta_gamma, theta_omega, alpha_min=ALPHA_MIN):
+    """(gamma, omega) = (alpha_min + softplus(theta_gamma), pi sigmoid(theta_omega)), Sec. 3.1."""
+    _f32_pair(theta_gamma, theta_omega, "theta_gamma", "theta_omega")
+    gamma, omega = torch.empty_like(theta_gamma), torch.empty_like(theta_omega)
+    check(_lib.lib().resonator_params_map(_ptr(theta_gamma), _ptr(theta_omega), theta_gamma.numel(),
+                                          float(alpha_min), _ptr(gamma), _ptr(omega), _stream(gamma.device)))
+    return gamma, omega
+
+
+def resonator_params_map_bwd(theta_gamma, theta_omega, dgamma, domega):
+    """Chain rule of resonator_params_map: returns (dtheta_gamma, dtheta_omega)."""
+    _f32_pair(theta_gamma, theta_omega, "theta_gamma", "theta_omega")
+    _f32_pair(dgamma, domega, "dgamma", "domega")
+    if dgamma.shape != theta_gamma.shape:
+        raise ValueError("gradients must match the parameters in shape")
+    dtg, dtw = torch.empty_like(theta_gamma), torch.empty_like(theta_omega)
+    check(_lib.lib().resonator_params_map_bwd(_ptr(theta_gamma), _ptr(theta_omega), _ptr(dgamma), _ptr(domega),
+                                              theta_gamma.numel(), _ptr(dtg), _ptr(dtw), _stream(dtg.device)))
+    return dtg, dtw
+
+
+def resonator_params_init(D, M, hl_min=2.0, hl_max=2048.0, per_min=4.0, per_max=2048.0, alpha_min=ALPHA_MIN,
+                          device="cuda"):
+    """Unconstrained (theta_gamma, theta_omega) [D, M] with log-spaced half-lives and periods."""
+    tg = torch.empty((D, M), dtype=torch.float32, device=device)
+    tw = torch.empty_like(tg)
+    check(_lib.lib().resonator_params_init(D, M, float(hl_min), float(hl_max), float(per_min), float(per_max),
+                                           float(alpha_min), _ptr(tg), _ptr(tw), _stream(tg.device)))
+    return tg, tw
+
+
+class ResonatorParamMapFunction(torch.autograd.Function):
+    """Autograd wrapper of the parameter map (forward and chain rule on the GPU)."""
+
+    @staticmethod
+    def forward(ctx, theta_gamma, theta_omega, alpha_min=ALPHA_MIN):
+        ctx.save_for_backward(theta_gamma, theta_omega)
+        return resonator_params_map(theta_gamma.contiguous(), theta_omega.contiguous(), alpha_min)
+
+    @staticmethod
+    def backward(ctx, dgamma, domega):
+        tg, tw = ctx.saved_tensors
+        dtg, dtw = resonator_params_map_bwd(tg.contiguous(), tw.contiguous(), dgamma.contiguous(),
+                                            domega.contiguous())
+        return dtg, dtw, None
+
+
 class ResonatorMixFunction(torch.autograd.Function):
     """Autograd wrapper: forward = resonator_mix_fwd, backward = resonator_mix_bwd."""
 
