@@ -310,7 +310,34 @@ def main():
     log(f"mixer epilogue: fwd {ep_fwd_us:.1f} us, bwd {ep_bwd_us:.1f} us")
     del et
 
+    # ---------------- kernel tail: mixing vs a quadratic causal reference ----------------
+    kt = []
+    for Lk in (8192, 32768):
+        pk = W.random_problem(12, 1, Lk, 256, 8, act="f32", gamma_range=(1e-4, 1.0), gamma_log=True)
+        xk = torch.from_numpy(pk["x"]).to(dev)
+        prk = [torch.from_numpy(pk[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+        ops.resonator_mix_fwd(xk, *prk)
+        ops.resonator_quadratic_reference(xk, *prk)
+        torch.cuda.synchronize()
+        reps = 20
+        t0e.record(stream)
+        for _ in range(reps):
+            ops.resonator_mix_fwd(xk, *prk)
+        t1e.record(stream)
+        for _ in range(3):
+            ops.resonator_quadratic_reference(xk, *prk)
+        t2e.record(stream)
+        torch.cuda.synchronize()
+        mix_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        quad_us = t1e.elapsed_time(t2e) * 1e3 / 3
+        kt.append({"L": Lk, "mix_us": mix_us, "quadratic_us": quad_us, "speedup": quad_us / mix_us,
+                   "quadratic_TFLOPs": Lk * (Lk + 1) / 2 * 256 * 2 / (quad_us * 1e-6) / 1e12})
+        log(f"kernel tail L={Lk}: mixing {mix_us:.1f} us, quadratic reference {quad_us:.0f} us, "
+            f"speedup {quad_us / mix_us:.0f}x")
+        del xk
+
     cpu = None
+    if not args.no_cpu:    cpu = None
     if not args.no_cpu:
         log("cpu baseline (oracle recurrence) ...")
         cpu = cpu_baseline(cfg)
@@ -332,6 +359,9 @@ def main():
         "config": {"workload": cfg.name, "B": B, "L": L, "D": D, "M": M,
                    "activations": "bf16 in/out, fp32 accumulate, split-bf16 MFMA operands",
                    "terminal_state": True, "buffer_sets": NSET},
+        "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
+                                    "causal reference (taps + Toeplitz sum), paper Table 5 protocol",
+                        "points": kt},
         "decode_multi_step": {"workload": f"{c4.name}: drives known in advance",
                               "k8_us_per_launch": k8_us, "k8_us_per_step": k8_us / 8,
                               "long_steps_per_launch": int(xdec.shape[0]), "long_us_per_step": long_us},

@@ -151,6 +151,21 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
                            const float* phase, float* state, void* stream);
 
 /*
+ * Quadratic causal reference mixer: the baseline of the kernel-tail benchmark
+ * (Sec. 5.3, Table 5), not part of the mixing path.  Computes
+ *   y[b,t,d] = sum_{s<=t} K_d[t-s] x[b,s,d],  K_d[tau] = sum_m a exp(-gamma tau) cos(omega tau + phi)
+ * directly, O(L^2 D) float32 multiply-adds, with the taps tabulated per call in
+ * float64 (rounded to float32) into the workspace.
+ *   x, y   [B][L][D] float32 device memory (y must not overlap x or ws)
+ *   ws     resonator_quadratic_reference_workspace_bytes(L, D) bytes, 4-byte aligned
+ * B <= 65535, L D <= 2^31; otherwise as resonator_mix_fwd.
+ */
+size_t resonator_quadratic_reference_workspace_bytes(int64_t L, int64_t D);
+int resonator_quadratic_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                                  const float* gamma, const float* omega, const float* amp, const float* phase,
+                                  void* ws, size_t ws_bytes, void* stream);
+
+/*
  * Constrained parameterization (Sec. 3.1, last paragraph): unconstrained
  * parameters are mapped into the valid ranges of the damping and frequency,
  *   gamma = alpha_min + softplus(theta_gamma)      (> alpha_min; the paper's floor is 1e-4)

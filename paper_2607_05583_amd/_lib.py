@@ -21,7 +21,8 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
            "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
-           "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init")
+           "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
+           "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes")
 
 _lib = None
 
@@ -67,6 +68,10 @@ def _declare(lib):
     lib.resonator_params_init.restype = i32
     lib.resonator_params_init.argtypes = [i64, i64, ctypes.c_double, ctypes.c_double, ctypes.c_double,
                                           ctypes.c_double, f32, fp, fp, vp]
+    lib.resonator_quadratic_reference_workspace_bytes.restype = sz
+    lib.resonator_quadratic_reference_workspace_bytes.argtypes = [i64, i64]
+    lib.resonator_quadratic_reference.restype = i32
+    lib.resonator_quadratic_reference.argtypes = [vp, vp, i64, i64, i64, i64, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

@@ -450,6 +450,36 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
 }
 
 // ---------------------------------------------------------------------------
+// Quadratic causal reference (kernel-tail baseline, Sec. 5.3)
+// ---------------------------------------------------------------------------
+size_t resonator_quadratic_reference_workspace_bytes(int64_t L, int64_t D) {
+  if (L < 1 || D < 1 || L * D > (1LL << 31)) return 0;
+  return quad_workspace_bytes(L, D);
+}
+
+int resonator_quadratic_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                                  const float* gamma, const float* omega, const float* amp, const float* phase,
+                                  void* ws, size_t ws_bytes, void* stream) {
+  int rc = check_sizes(B, L, D, M, false);
+  if (rc) return rc;
+  if (B > 65535 || L * D > (1LL << 31))
+    return fail(RES_ERR_UNSUPPORTED, "quadratic reference needs B <= 65535 and L D <= 2^31");
+  if (!x || !y) return fail(RES_ERR_INVALID_ARG, "x and y must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  const size_t need = quad_workspace_bytes(L, D);
+  if (!ws || ws_bytes < need)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned(x, 4) || !aligned(y, 4) || !aligned(ws, 4))
+    return fail(RES_ERR_MISALIGNED, "x, y and the workspace must be 4-byte aligned");
+  const size_t n = (size_t)(B * L * D) * 4;
+  if (overlap(y, n, x, n) || overlap(y, n, ws, need) || overlap(x, n, ws, need))
+    return fail(RES_ERR_INVALID_ARG, "x, y and the workspace must not overlap");
+  const hipError_t e = launch_quad_reference(x, y, B, L, D, M, gamma, omega, amp, phase, (float*)ws,
+                                             (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "quadratic reference launch");
+}
+
+// ---------------------------------------------------------------------------
 // Constrained parameterization (Sec. 3.1, last paragraph)
 // ---------------------------------------------------------------------------
 static int prm_check_n(int64_t n) {

@@ -106,6 +106,10 @@ template <typename TX, typename TY>
 hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y,
                          const float* gamma, const float* omega, const float* amp,
                          const float* phase, float* state, hipStream_t st);
+size_t quad_workspace_bytes(int64_t L, int64_t D);
+hipError_t launch_quad_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                                 const float* gamma, const float* omega, const float* amp, const float* phase,
+                                 float* K, hipStream_t st);
 hipError_t launch_params_map(const float* tg, const float* tw, int64_t n, float alpha_min, float* gamma,
                              float* omega, hipStream_t st);
 hipError_t launch_params_map_bwd(const float* tg, const float* tw, const float* dg, const float* dw, int64_t n,

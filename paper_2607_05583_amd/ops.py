@@ -175,6 +175,22 @@ def resonator_decode_steps(x, gamma, omega, amp, phase, state, out_dtype=None, o
     return y
 
 
+def resonator_quadratic_reference(x, gamma, omega, amp, phase):
+    """The O(L^2) direct causal mixer (kernel-tail baseline), float32 [B, L, D]."""
+    _dev(x, "x")
+    if x.dtype != torch.float32 or x.dim() != 3:
+        raise ValueError("x must be float32 [B, L, D]")
+    B, L, D = x.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    y = torch.empty_like(x)
+    n = _lib.lib().resonator_quadratic_reference_workspace_bytes(L, D)
+    ws = torch.empty(max(n, 4), dtype=torch.uint8, device=x.device)
+    check(_lib.lib().resonator_quadratic_reference(_ptr(x), _ptr(y), B, L, D, M, _ptr(gamma), _ptr(omega),
+                                                   _ptr(amp), _ptr(phase), _ptr(ws), n, _stream(x.device)))
+    return y
+
+
 ALPHA_MIN = 1e-4  # the paper's floor on the damping
 
 
