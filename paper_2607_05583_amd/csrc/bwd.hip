@@ -52,11 +52,13 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
   typedef TileGeom<TX, DW> GX;
   constexpr int XP = GX::PITCH;
   // Mode groups are processed one after another; the scan buffer holds one group.
-  constexpr int NSTR = 32;               // floats per chunk: 16 Q comps | 16 rho comps
+  constexpr int NSTR = 36;               // floats per chunk: 16 Q comps | 16 rho comps | 4 pad (banks)
   constexpr int KSTR = 16 * NSTR + 16;   // floats per channel
   constexpr int WSB = 8 * KSTR;          // floats per wave
   constexpr int NM = 1 + 5 * MG;
-  constexpr int PST = 256 + 64;          // reduction dump per channel: P | DW pairs | DR pairs
+  constexpr int PP = 17;                 // row pitch of the P dump (odd: rows on distinct banks)
+  constexpr int PDW = 16 * PP;           // DW pairs after P
+  constexpr int PST = PDW + 64 + 4;      // dump per channel: P | DW pairs | DR pairs | pad (banks)
 
   __shared__ __align__(16) TX dyt[DW * XP];
   __shared__ __align__(16) TX xt[MODE == MODE_APPLY ? DW * XP : 8];
@@ -182,15 +184,15 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
         float* dst = &sb[k * PST];
         if (g == 0) {
 #pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(4 * lq + r) * 16 + li] = pacc[k][r];
+          for (int r = 0; r < 4; ++r) dst[(4 * lq + r) * PP + li] = pacc[k][r];
         }
         // lane (col li, q) holds rows 4q..4q+3; the 2x2 diagonal blocks are in lanes li/4 == q
         if ((li >> 2) == lq) {
           const int r0 = li & 2;  // rows li&~1 and li|1
-          dst[256 + li * 2 + 0] = dwacc[k][r0];
-          dst[256 + li * 2 + 1] = dwacc[k][r0 + 1];
-          dst[256 + 32 + li * 2 + 0] = dracc[k][r0];
-          dst[256 + 32 + li * 2 + 1] = dracc[k][r0 + 1];
+          dst[PDW + li * 2 + 0] = dwacc[k][r0];
+          dst[PDW + li * 2 + 1] = dwacc[k][r0 + 1];
+          dst[PDW + 32 + li * 2 + 0] = dracc[k][r0];
+          dst[PDW + 32 + li * 2 + 1] = dracc[k][r0 + 1];
         }
       }
       __syncthreads();
@@ -205,12 +207,12 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
           for (int h = 0; h < 2; ++h) {
             const int tau = sj + 8 * h;
             float s = 0.f;
-            for (int j = 0; j + tau < 16; ++j) s += src[(j + tau) * 16 + j];
+            for (int j = 0; j + tau < 16; ++j) s += src[(j + tau) * PP + j];
             out[tau] = s;
           }
         }
         // column c holds (D[c&~1][c], D[c|1][c]) at [2c], [2c+1]
-        const float* dwp = &src[256];
+        const float* dwp = &src[PDW];
         const float* drp = dwp + 32;
         const int c0 = 2 * sj, c1 = 2 * sj + 1;
         const float w_rr = dwp[2 * c0], w_ir = dwp[2 * c0 + 1], w_ri = dwp[2 * c1], w_ii = dwp[2 * c1 + 1];
