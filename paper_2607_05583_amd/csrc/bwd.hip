@@ -42,19 +42,28 @@ __device__ __forceinline__ f4 chunk_gather(const float* row, int i, int q) {
 // Layout of the per-tile partial sums: [G(16) | per mode (W re, W im, R re, R im)].
 __host__ __device__ inline int part_stride(int Mp) { return 16 + 4 * Mp; }
 
+// A block of BW_WAVES waves takes one tile; each wave owns CPW channels and
+// works through them in groups of GS (the scan uses GS x 8 lanes, one per
+// (channel, mode)).  Eight waves of 8 channels hold the same LDS as four waves
+// of 16 would, with twice the waves to hide latency.
+constexpr int BW_WAVES = 8;
+constexpr int BW_THREADS = 64 * BW_WAVES;
+
 template <typename TX, int MG, int MODE>
-__global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
+__global__ __launch_bounds__(BW_THREADS) void bwd_tile_kernel(BwdArgs a) {
   typedef Path<TX> PT;
   typedef typename PT::XOp XOp;
   constexpr int DW = tile_channels<TX>();
-  constexpr int CPW = DW / NWAVES;
-  constexpr int NCG = CPW / 8;
+  constexpr int GS = 4;                  // channels per group
+  constexpr int CPW = DW / BW_WAVES;
+  constexpr int NCG = CPW / GS;
+  static_assert(CPW % GS == 0, "a wave's channels split into whole groups");
   typedef TileGeom<TX, DW> GX;
   constexpr int XP = GX::PITCH;
   // Mode groups are processed one after another; the scan buffer holds one group.
   constexpr int NSTR = 36;               // floats per chunk: 16 Q comps | 16 rho comps | 4 pad (banks)
   constexpr int KSTR = 16 * NSTR + 16;   // floats per channel
-  constexpr int WSB = 8 * KSTR;          // floats per wave
+  constexpr int WSB = GS * KSTR;         // floats per wave
   constexpr int NM = 1 + 5 * MG;
   constexpr int PP = 17;                 // row pitch of the P dump (odd: rows on distinct banks)
   constexpr int PDW = 16 * PP;           // DW pairs after P
@@ -62,7 +71,7 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
 
   __shared__ __align__(16) TX dyt[DW * XP];
   __shared__ __align__(16) TX xt[MODE == MODE_APPLY ? DW * XP : 8];
-  __shared__ __align__(16) float sbuf[NWAVES * WSB];
+  __shared__ __align__(16) float sbuf[BW_WAVES * WSB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 15, lq = lane >> 4;
@@ -76,25 +85,27 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
   const int64_t t0 = p * TILE_T;
   const int d0 = nb * DW;
 
-  load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.dy), dyt, b, t0, d0, a.L, a.D, tid);
-  if (MODE == MODE_APPLY)
-    load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
+  if (tid < NTHREADS) {  // the tile movers are written for NWAVES waves
+    load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.dy), dyt, b, t0, d0, a.L, a.D, tid);
+    if (MODE == MODE_APPLY)
+      load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
+  }
   __syncthreads();
 
   const char* tab = reinterpret_cast<const char*>(a.tab);
   float* sb = sbuf + wave * WSB;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
   const size_t tm = (size_t)(b * a.P + p) * a.Dp;  // tile row in [B][P][Dp]
-  static_assert(8 * PST <= WSB, "reduction dump must fit the scan buffer");
+  static_assert(GS * PST <= WSB, "reduction dump must fit the scan buffer");
 
 #pragma unroll
   for (int cg = 0; cg < NCG; ++cg) {
-    f4 dxacc[8];
-    f4 pacc[8];
+    f4 dxacc[GS];
+    f4 pacc[GS];
     if (MODE == MODE_APPLY) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int ch = wave * CPW + cg * 8 + k;
+      for (int k = 0; k < GS; ++k) {
+        const int ch = wave * CPW + cg * GS + k;
         const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
         const XOp dyv = PT::load_x(&dyt[ch * XP + PT::x_off(li, lq)]);
         dxacc[k] = PT::mma(PT::load_a(tp), dyv, zero);
@@ -107,8 +118,8 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
     for (int g = 0; g < MG; ++g) {
       // ---- chunk sums of dy: Eq, Er -------------------------------------------
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int ch = wave * CPW + cg * 8 + k;
+      for (int k = 0; k < GS; ++k) {
+        const int ch = wave * CPW + cg * GS + k;
         const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
         const XOp dyv = PT::load_x(&dyt[ch * XP + PT::x_off(li, lq)]);
         const f4 eq = PT::mma(PT::load_a(tp + (1 + 5 * g) * TAB_MAT_BYTES), dyv, zero);
@@ -118,8 +129,8 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
       }
       __syncthreads();
       // ---- reverse scan over the tile's chunks, one lane per (channel, mode) ---
-      {
-        const int ch = wave * CPW + cg * 8 + sk;
+      if (sk < GS) {
+        const int ch = wave * CPW + cg * GS + sk;
         const int dch = d0 + ch;
         const int m = g * 8 + sj;
         const float2 mu = a.scal[(size_t)dch * a.Mp + m].mu;
@@ -154,10 +165,10 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
       if (MODE == MODE_STATE) continue;
 
       // ---- dx correction, chunk sums of x, cross products over chunks ---------
-      f4 dwacc[8], dracc[8];
+      f4 dwacc[GS], dracc[GS];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int ch = wave * CPW + cg * 8 + k;
+      for (int k = 0; k < GS; ++k) {
+        const int ch = wave * CPW + cg * GS + k;
         const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
         const XOp xv = PT::load_x(&xt[ch * XP + PT::x_off(li, lq)]);
         const float* srow = &sb[k * KSTR];
@@ -180,7 +191,7 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
       __syncthreads();
       // ---- dump P (first group) and the 2x2 diagonal blocks, then reduce -------
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < GS; ++k) {
         float* dst = &sb[k * PST];
         if (g == 0) {
 #pragma unroll
@@ -196,9 +207,9 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
         }
       }
       __syncthreads();
-      {
+      if (sk < GS) {
         // lane (sk, sj): channel sk of the group; G[sj], G[sj + 8]; mode g*8 + sj
-        const int ch = wave * CPW + cg * 8 + sk;
+        const int ch = wave * CPW + cg * GS + sk;
         const int dch = d0 + ch;
         const float* src = &sb[sk * PST];
         float* out = a.part + (tm + dch) * part_stride(a.Mp);
@@ -229,8 +240,8 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
     if (MODE == MODE_APPLY) {
       // dx -> LDS in place of dy (each wave owns its channels' rows)
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int ch = wave * CPW + cg * 8 + k;
+      for (int k = 0; k < GS; ++k) {
+        const int ch = wave * CPW + cg * GS + k;
         TX v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = from_f32<TX>(dxacc[k][r]);
@@ -244,7 +255,7 @@ __global__ __launch_bounds__(NTHREADS) void bwd_tile_kernel(BwdArgs a) {
   }
   if (MODE == MODE_APPLY) {
     __syncthreads();
-    store_tile_any<TX, DW>(reinterpret_cast<TX*>(a.dx), dyt, b, t0, d0, a.L, a.D, tid);
+    if (tid < NTHREADS) store_tile_any<TX, DW>(reinterpret_cast<TX*>(a.dx), dyt, b, t0, d0, a.L, a.D, tid);
   }
 }
 
@@ -395,7 +406,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
 template <typename TX>
 hipError_t launch_bwd_tile(const Geometry& g, int mode, const BwdArgs& a, hipStream_t st,
                            hipEvent_t ev0, hipEvent_t ev1) {
-  const dim3 grid((unsigned)(g.B * g.P * g.NB)), block(NTHREADS);
+  const dim3 grid((unsigned)(g.B * g.P * g.NB)), block(BW_THREADS);
   if (g.MG == 1) {
     if (mode == MODE_STATE)
       launch_timed(bwd_tile_kernel<TX, 1, MODE_STATE>, grid, block, st, ev0, ev1, a);
