@@ -283,8 +283,10 @@ __global__ __launch_bounds__(256) void carry_bwd_kernel(const float4* __restrict
     float4 ag[BATCH];
 #pragma unroll
     for (int j = 0; j < BATCH; ++j) {
-      const int64_t p = p1 - j;
-      ag[j] = (p >= 0) ? agg[((size_t)(b * P + p) * Dp + d) * Mp + m] : make_float4(0, 0, 0, 0);
+      // past the first tile the index is clamped (the value is not used), so
+      // the loads are unconditional and all of them are in flight at once
+      const int64_t p = p1 - j >= 0 ? p1 - j : 0;
+      ag[j] = agg[((size_t)(b * P + p) * Dp + d) * Mp + m];
     }
 #pragma unroll
     for (int j = 0; j < BATCH; ++j) {
@@ -317,9 +319,9 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     int64_t P, int D, int M, int Dp, int Mp) {
   // One block per channel d.  The ps columns of the per-tile partial rows of d
   // are summed over the B P tiles in float64: thread (row group rg, column col)
-  // takes tiles rg, rg + NRG, ... in order (two interleaved accumulators, so that
-  // loads overlap), then the row groups are added in order.  The order is fixed,
-  // so the result is bitwise reproducible.
+  // takes tiles rg, rg + NRG, ... into eight interleaved accumulators (eight
+  // loads in flight), then the row groups are added in order.  The order is
+  // fixed, so the result is bitwise reproducible.
   const int d = blockIdx.x;
   const int ps = part_stride(Mp);
   const int nrg = blockDim.x / ps;
@@ -330,14 +332,17 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const int col = threadIdx.x % ps, rg = threadIdx.x / ps;
     double acc = 0.0;
     if (rg < nrg) {
-      double a0 = 0.0, a1 = 0.0;
+      double ac[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
       int64_t bp = rg;
-      for (; bp + nrg < nbp; bp += 2 * nrg) {
-        a0 += part[((size_t)bp * Dp + d) * ps + col];
-        a1 += part[((size_t)(bp + nrg) * Dp + d) * ps + col];
+      for (; bp + 7 * nrg < nbp; bp += 8 * nrg) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part[((size_t)(bp + u * nrg) * Dp + d) * ps + col];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) ac[u] += v[u];
       }
-      if (bp < nbp) a0 += part[((size_t)bp * Dp + d) * ps + col];
-      acc = a0 + a1;
+      for (; bp < nbp; bp += nrg) ac[0] += part[((size_t)bp * Dp + d) * ps + col];
+      acc = ((ac[0] + ac[1]) + (ac[2] + ac[3])) + ((ac[4] + ac[5]) + (ac[6] + ac[7]));
     }
     s_acc[threadIdx.x] = acc;
   }
