@@ -6,10 +6,14 @@
 //   l[b,t,c] = sum_{k<K} w[c,k] v[b,t-k,c]   (zero before t = 0)  local path
 //   z = sigmoid(gate) * ybar + s * l                            combine eq.
 //
-// Every kernel is bound by HBM traffic: the activations are read once from
-// HBM; the H reads of a row for the head sum and the K reads for the local taps
-// hit in L1/L2.  A thread owns VEC adjacent channels of one head (same j block
-// in every head), so its loads are VEC-element vectors.
+// The kernels are meant to be bound by HBM traffic: every activation element is
+// read once from HBM.  Forward: a thread owns a piece of adjacent channels at
+// the same position j of every head (epi_fwd_col_kernel), so the head mixing
+// needs no other thread's data; the K-1 earlier rows of the local path are
+// neighbouring threads' rows and hit in cache.  Backward: row chunks are staged
+// in LDS (epi_bwd_tile_kernel), since dy at one head needs dz sigmoid(gate) of
+// every head.  Shapes outside those kernels' limits take the generic kernels
+// below (one piece of VEC channels of one head per thread).
 //
 // Backward (loss sum(dz z)), with sg = sigmoid(gate), dyb = dz sg, dl = dz s:
 //   dgate = dz ybar sg (1 - sg);  dy[h dh + j] = sum_g C[g,h] dyb[g dh + j];
