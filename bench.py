@@ -170,6 +170,51 @@ def main():
     log(f"prefill: {ms_step * 1e3:.1f} us/step (events), segment kernel {k_avg_ms * 1e3:.1f} us, "
         f"wall {t_wall / args.steps * 1e3:.1f} us/step")
 
+    # ---------------- prefill across lengths (1K .. 32K tokens) ----------------
+    # B4 D256 M8 bf16 as the prefill config, L from 1K to 32K; the step and the
+    # segment kernel alone, with the segment kernel's share of the HBM roofline
+    sweep = []
+    for Ls in (1024, 2048, 4096, 8192, 16384, 32768):
+        xl = torch.randn((B, Ls, D), generator=torch.Generator(device=dev).manual_seed(Ls), device=dev,
+                         dtype=torch.float32).to(torch.bfloat16)
+        yl = torch.empty_like(xl)
+        hl = torch.empty((B, D, M, 2), dtype=torch.float32, device=dev)
+        wn = ops.workspace_bytes(RES_OP_FWD, torch.bfloat16, B, Ls, D, M)
+        wl = torch.empty(wn, dtype=torch.uint8, device=dev)
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+        def fwd_l(timed):
+            if timed:
+                _lib.check(lib.resonator_set_kernel_timer(ctypes.c_void_p(ev[0].cuda_event),
+                                                          ctypes.c_void_p(ev[1].cuda_event)))
+            _lib.check(lib.resonator_mix_fwd(
+                ctypes.c_void_p(xl.data_ptr()), _lib.RES_BF16, ctypes.c_void_p(yl.data_ptr()), _lib.RES_BF16,
+                B, Ls, D, M, *P, None, ctypes.c_void_p(hl.data_ptr()), ctypes.c_void_p(wl.data_ptr()), wn, sp))
+
+        ev[0].record(stream)
+        ev[1].record(stream)
+        for _ in range(3):
+            fwd_l(False)
+        torch.cuda.synchronize()
+        reps = max(5, min(200, (1 << 22) // Ls))
+        start.record(stream)
+        for _ in range(reps):
+            fwd_l(False)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        st_us = start.elapsed_time(stop) * 1e3 / reps
+        kus = []
+        for _ in range(5):
+            fwd_l(True)
+            torch.cuda.synchronize()
+            kus.append(ev[0].elapsed_time(ev[1]) * 1e3)
+        k_us = float(np.median(kus))
+        gbs = B * Ls * D * 4 / (k_us * 1e-6) / 1e9
+        sweep.append({"L": Ls, "B": B, "step_us": st_us, "tokens_ch_per_s": B * Ls * D / (st_us * 1e-6),
+                      "seg_kernel_us": k_us, "seg_kernel_GBs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS})
+        log(f"prefill L={Ls}: step {st_us:.1f} us, segment kernel {k_us:.1f} us ({gbs:.0f} GB/s)")
+        del xl, yl, wl
+
     # ---------------- decode ----------------
     c4 = W.CONFIGS[4]
     log(f"decode workload {c4.name}")
@@ -359,6 +404,10 @@ def main():
         "config": {"workload": cfg.name, "B": B, "L": L, "D": D, "M": M,
                    "activations": "bf16 in/out, fp32 accumulate, split-bf16 MFMA operands",
                    "terminal_state": True, "buffer_sets": NSET},
+        "prefill_sweep": {"workload": "B4 D256 M8 bf16, L = 1K .. 32K (segment kernel GB/s: 4 algorithmic bytes per "
+                                      "token-channel); one buffer set per length, so inputs stay in the 256 MB "
+                                      "Infinity Cache between calls (the headline line rotates three sets)",
+                          "points": sweep},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol",
                         "points": kt},
