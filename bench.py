@@ -355,6 +355,34 @@ def main():
     log(f"mixer epilogue: fwd {ep_fwd_us:.1f} us, bwd {ep_bwd_us:.1f} us")
     del et
 
+    # ---------------- mixer block forward (projections, mixing, epilogue) ----------------
+    blk = []
+    for Lb in (2048, 8192, 32768):
+        pb_ = W.block_inputs(13, 4, Lb, 256, 8, 4, 8, 8, "bf16")
+        bt = {k: torch.from_numpy(pb_[k].view(np.int16)).view(torch.bfloat16).to(dev) for k in ("x", "Wu", "Wg", "Wo")}
+        bp = [torch.from_numpy(pb_[k]).to(dev) for k in ("gamma", "omega", "amp", "phase", "Ct", "w", "s")]
+        del pb_
+
+        dense = tuple(ops.resonator_block_diag_weight(bt[k]) for k in ("Wu", "Wg", "Wo"))
+
+        def block():
+            return ops.resonator_block_fwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6], 8,
+                                           dense=dense)
+
+        for _ in range(3):
+            block()
+        torch.cuda.synchronize()
+        reps = 10
+        t0e.record(stream)
+        for _ in range(reps):
+            block()
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        b_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        blk.append({"L": Lb, "us": b_us, "tokens_per_s": 4 * Lb / (b_us * 1e-6)})
+        log(f"mixer block forward B4 L={Lb} d256: {b_us:.1f} us ({4 * Lb / (b_us * 1e-6) / 1e6:.1f} M tokens/s)")
+        del bt
+
     # ---------------- kernel tail: mixing vs a quadratic causal reference ----------------
     kt = []
     for Lk in (8192, 32768):
@@ -408,6 +436,10 @@ def main():
                                       "token-channel); one buffer set per length, so inputs stay in the 256 MB "
                                       "Infinity Cache between calls (the headline line rotates three sets)",
                           "points": sweep},
+        "mixer_block": {"workload": "B4 d_model 256, bf16: grouped in-projections (8 groups, run as dense GEMMs on the "
+                                    "block-diagonal weights) to drive and gate, "
+                                    "mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection; forward",
+                        "points": blk},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol",
                         "points": kt},

@@ -151,6 +151,29 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
                            const float* phase, float* state, void* stream);
 
 /*
+ * Grouped linear projection (Sec. 3.1 drive and gate projection, Sec. 3.4
+ * output projection): a block-diagonal weight of G groups,
+ *   y[n, g dq + j] = sum_i x[n, g di + i] W[g][i][j],   di = d_in / G, dq = d_out / G.
+ *   x  [N][d_in], W [G][d_in/G][d_out/G], y [N][d_out], all of dtype dt (bf16 or
+ *      f32), device memory, row-major; y must not overlap x or W
+ * Float32 accumulation; a plain GEMM, run as one rocBLAS strided-batched GEMM on
+ * the given stream.  Calls from several host threads on one device must not
+ * overlap (they share that device's rocBLAS handle).  N, d_in, d_out < 2^31.
+ */
+int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void* y, int64_t N, int64_t d_in,
+                             int64_t d_out, int64_t G, void* stream);
+
+/*
+ * Dense [d_in][d_out] copy of a grouped weight W [G][d_in/G][d_out/G], zero off
+ * the diagonal blocks, so that resonator_grouped_linear with G = 1 on it gives
+ * exactly the grouped product (the zero blocks add exact zeros) with the GEMM
+ * library's efficient tile shapes.  Same dtype conventions; W_dense must not
+ * overlap W; d_in d_out <= 2^31.
+ */
+int resonator_block_diag_weight(const void* W, res_dtype_t dt, int64_t d_in, int64_t d_out, int64_t G,
+                                void* W_dense, void* stream);
+
+/*
  * Quadratic causal reference mixer: the baseline of the kernel-tail benchmark
  * (Sec. 5.3, Table 5), not part of the mixing path.  Computes
  *   y[b,t,d] = sum_{s<=t} K_d[t-s] x[b,s,d],  K_d[tau] = sum_m a exp(-gamma tau) cos(omega tau + phi)

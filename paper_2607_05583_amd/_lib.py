@@ -22,7 +22,8 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
            "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
-           "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes")
+           "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
+           "resonator_grouped_linear", "resonator_block_diag_weight")
 
 _lib = None
 
@@ -72,6 +73,10 @@ def _declare(lib):
     lib.resonator_quadratic_reference_workspace_bytes.argtypes = [i64, i64]
     lib.resonator_quadratic_reference.restype = i32
     lib.resonator_quadratic_reference.argtypes = [vp, vp, i64, i64, i64, i64, fp, fp, fp, fp, vp, sz, vp]
+    lib.resonator_grouped_linear.restype = i32
+    lib.resonator_grouped_linear.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, vp]
+    lib.resonator_block_diag_weight.restype = i32
+    lib.resonator_block_diag_weight.argtypes = [vp, i32, i64, i64, i64, vp, vp]
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

@@ -2,6 +2,7 @@
 // and kernel dispatch.  Declared in include/resonator.h.
 #include <cstdarg>
 #include <cmath>
+#include <cstdint>
 #include <initializer_list>
 #include <cstdio>
 #include <string>
@@ -447,6 +448,45 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
   else
     e = launch_decode_steps<bf16_t, float>(B, N, D, M, x, y, gamma, omega, amp, phase, state, st);
   return e == hipSuccess ? RES_OK : hip_fail(e, "decode steps launch");
+}
+
+// ---------------------------------------------------------------------------
+// Grouped linear projection (Sec. 3.1, 3.4)
+// ---------------------------------------------------------------------------
+int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void* y, int64_t N, int64_t d_in,
+                             int64_t d_out, int64_t G, void* stream) {
+  if (N < 1 || d_in < 1 || d_out < 1 || G < 1)
+    return fail(RES_ERR_INVALID_ARG, "N, d_in, d_out and G must be >= 1");
+  if (d_in % G || d_out % G)
+    return fail(RES_ERR_INVALID_ARG, "d_in (%lld) and d_out (%lld) must be multiples of G (%lld)", (long long)d_in,
+                (long long)d_out, (long long)G);
+  if (N > INT32_MAX || d_in > INT32_MAX || d_out > INT32_MAX)
+    return fail(RES_ERR_UNSUPPORTED, "N, d_in and d_out must be below 2^31");
+  if (!dtype_ok(dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!x || !W || !y) return fail(RES_ERR_INVALID_ARG, "x, W and y must be non-null");
+  const size_t es = elt_size(dt);
+  if (!aligned(x, es) || !aligned(W, es) || !aligned(y, es))
+    return fail(RES_ERR_MISALIGNED, "x, W and y must be aligned to their element");
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * es;
+  if (overlap(y, ny, x, nx) || overlap(y, ny, W, nw)) return fail(RES_ERR_INVALID_ARG, "y must not overlap x or W");
+  const char* err = launch_grouped_linear(x, W, y, N, d_in, d_out, G, dt == RES_BF16, (hipStream_t)stream);
+  if (err) return fail(RES_ERR_HIP, "grouped linear: %s", err);
+  return RES_OK;
+}
+
+int resonator_block_diag_weight(const void* W, res_dtype_t dt, int64_t d_in, int64_t d_out, int64_t G,
+                                void* W_dense, void* stream) {
+  if (d_in < 1 || d_out < 1 || G < 1 || d_in % G || d_out % G)
+    return fail(RES_ERR_INVALID_ARG, "need d_in, d_out >= 1 and multiples of G >= 1");
+  if (d_in * d_out > (1LL << 31)) return fail(RES_ERR_UNSUPPORTED, "d_in d_out must be <= 2^31");
+  if (!dtype_ok(dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!W || !W_dense) return fail(RES_ERR_INVALID_ARG, "W and W_dense must be non-null");
+  const size_t es = elt_size(dt);
+  if (!aligned(W, es) || !aligned(W_dense, es)) return fail(RES_ERR_MISALIGNED, "W and W_dense must be aligned");
+  if (overlap(W_dense, (size_t)(d_in * d_out) * es, W, (size_t)(d_in * (d_out / G)) * es))
+    return fail(RES_ERR_INVALID_ARG, "W_dense must not overlap W");
+  const hipError_t e = launch_block_diag(W, W_dense, d_in, d_out, G, dt == RES_BF16, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "block-diagonal weight launch");
 }
 
 // ---------------------------------------------------------------------------

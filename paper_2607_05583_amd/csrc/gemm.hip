@@ -1,0 +1,78 @@
+// Grouped linear projection (Sec. 3.1 drive/gate projection, Sec. 3.4 output
+// projection): y[:, g-th output slice] = x[:, g-th input slice] W[g], for G
+// groups of a block-diagonal weight.  A plain GEMM, so it goes to rocBLAS as one
+// strided-batched GEMM over the groups (float32 accumulation).
+//
+// Row-major x [N, d_in] is, column-major, x^T [d_in, N] with leading dimension
+// d_in, and group g's slice starts d_in / G elements further; row-major W[g]
+// [d_in/G, d_out/G] is, column-major, W[g]^T; so y^T_g = W[g]^T x^T_g with
+// m = d_out/G, n = N, k = d_in/G, and y^T_g starts d_out / G further.
+#include <mutex>
+
+#include <rocblas/rocblas.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace res {
+
+namespace {
+constexpr int MAX_DEVICES = 64;
+rocblas_handle g_handle[MAX_DEVICES] = {};
+std::mutex g_handle_mu;
+
+rocblas_handle handle_for(int dev) {
+  std::lock_guard<std::mutex> lk(g_handle_mu);
+  if (!g_handle[dev] && rocblas_create_handle(&g_handle[dev]) != rocblas_status_success) g_handle[dev] = nullptr;
+  return g_handle[dev];
+}
+}  // namespace
+
+// 0 on success; otherwise a message for the caller's error report
+const char* launch_grouped_linear(const void* x, const void* W, void* y, int64_t N, int64_t d_in, int64_t d_out,
+                                  int64_t G, bool bf16, hipStream_t st) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return "no current HIP device";
+  rocblas_handle h = handle_for(dev);
+  if (!h) return "rocblas_create_handle failed";
+  if (rocblas_set_stream(h, st) != rocblas_status_success) return "rocblas_set_stream failed";
+  const rocblas_datatype t = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+  const int64_t di = d_in / G, dq = d_out / G;
+  const float alpha = 1.f, beta = 0.f;
+  const rocblas_status s = rocblas_gemm_strided_batched_ex(
+      h, rocblas_operation_none, rocblas_operation_none, (rocblas_int)dq, (rocblas_int)N, (rocblas_int)di, &alpha,
+      W, t, (rocblas_int)dq, (rocblas_stride)(di * dq), x, t, (rocblas_int)d_in, (rocblas_stride)di, &beta, y, t,
+      (rocblas_int)d_out, (rocblas_stride)dq, y, t, (rocblas_int)d_out, (rocblas_stride)dq, (rocblas_int)G,
+      rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  return s == rocblas_status_success ? nullptr : rocblas_status_to_string(s);
+}
+
+// Dense [d_in][d_out] copy of a block-diagonal weight W [G][d_in/G][d_out/G]
+// (zeros off the diagonal blocks): one dense GEMM then gives exactly the grouped
+// product (the zero blocks add exact zeros to float32 sums) with the library's
+// efficient tile shapes, where G small GEMMs of d/G columns would not.
+template <typename T>
+__global__ __launch_bounds__(256) void block_diag_kernel(const T* __restrict__ W, T* __restrict__ Wd,
+                                                         int64_t d_in, int64_t d_out, int64_t G) {
+  const int64_t di = d_in / G, dq = d_out / G;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < d_in * d_out;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t i = e / d_out, j = e % d_out, gi = i / di, gj = j / dq;
+    Wd[e] = gi == gj ? W[(gi * di + i % di) * dq + j % dq] : T(0);
+  }
+}
+
+hipError_t launch_block_diag(const void* W, void* Wd, int64_t d_in, int64_t d_out, int64_t G, bool bf16,
+                             hipStream_t st) {
+  const int64_t n = d_in * d_out;
+  const unsigned grid = (unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
+  if (bf16)
+    hipLaunchKernelGGL(block_diag_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, (const bf16_t*)W, (bf16_t*)Wd, d_in,
+                       d_out, G);
+  else
+    hipLaunchKernelGGL(block_diag_kernel<float>, dim3(grid), dim3(256), 0, st, (const float*)W, (float*)Wd, d_in,
+                       d_out, G);
+  return hipGetLastError();
+}
+
+}  // namespace res

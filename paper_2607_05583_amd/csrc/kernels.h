@@ -106,6 +106,10 @@ template <typename TX, typename TY>
 hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y,
                          const float* gamma, const float* omega, const float* amp,
                          const float* phase, float* state, hipStream_t st);
+const char* launch_grouped_linear(const void* x, const void* W, void* y, int64_t N, int64_t d_in, int64_t d_out,
+                                  int64_t G, bool bf16, hipStream_t st);
+hipError_t launch_block_diag(const void* W, void* Wd, int64_t d_in, int64_t d_out, int64_t G, bool bf16,
+                             hipStream_t st);
 size_t quad_workspace_bytes(int64_t L, int64_t D);
 hipError_t launch_quad_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
                                  const float* gamma, const float* omega, const float* amp, const float* phase,

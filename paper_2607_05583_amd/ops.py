@@ -191,6 +191,48 @@ def resonator_quadratic_reference(x, gamma, omega, amp, phase):
     return y
 
 
+def resonator_grouped_linear(x, W, out=None):
+    """y = x W for a block-diagonal W of G groups: x [..., d_in], W [G, d_in/G, d_out/G]."""
+    _dev(x, "x")
+    _dev(W, "W")
+    if W.dim() != 3 or W.dtype != x.dtype:
+        raise ValueError("W must be [G, d_in/G, d_out/G] of x's dtype")
+    G, di, dq = W.shape
+    d_in = x.shape[-1]
+    if d_in != G * di:
+        raise ValueError(f"x has {d_in} features, W expects {G * di}")
+    N = x.numel() // d_in
+    y = out if out is not None else torch.empty(x.shape[:-1] + (G * dq,), dtype=x.dtype, device=x.device)
+    _dev(y, "out")
+    check(_lib.lib().resonator_grouped_linear(_ptr(x), _ptr(W), _code(x), _ptr(y), N, d_in, G * dq, G,
+                                              _stream(x.device)))
+    return y
+
+
+def resonator_block_diag_weight(W):
+    """Dense [1, d_in, d_out] block-diagonal copy of a grouped weight [G, d_in/G, d_out/G]."""
+    _dev(W, "W")
+    G, di, dq = W.shape
+    Wd = torch.empty((1, G * di, G * dq), dtype=W.dtype, device=W.device)
+    check(_lib.lib().resonator_block_diag_weight(_ptr(W), _code(W), G * di, G * dq, G, _ptr(Wd), _stream(W.device)))
+    return Wd
+
+
+def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, dense=None):
+    """The mixer block forward (Sec. 3.1, 3.4): drive u and gate g from grouped
+    projections of x, y = mixing of u, z = sigmoid(g) (C y) + s conv(u), and the
+    grouped output projection of z.  x [B, L, d]; returns [B, L, d_out].
+
+    ``dense`` = (Wu, Wg, Wo) as resonator_block_diag_weight copies: the
+    projections then run as dense GEMMs (the same result)."""
+    Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
+    u = resonator_grouped_linear(x, Pu)
+    g = resonator_grouped_linear(x, Pg)
+    y = resonator_mix_fwd(u, gamma, omega, amp, phase)
+    z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
+    return resonator_grouped_linear(z, Po)
+
+
 ALPHA_MIN = 1e-4  # the paper's floor on the damping
 
 

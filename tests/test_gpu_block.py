@@ -1,0 +1,79 @@
+"""GPU parity of the grouped linear projection and of the mixer block forward
+(Sec. 3.1, 3.4) against the CPU oracle, through the C ABI.
+
+Tolerances.  Grouped linear: float32 1e-5 (float32 products summed in float32
+over at most 256 terms); bf16 inputs give exact products summed in float32 and
+one bf16 rounding of the result, 1e-2.  Block: float32 1e-4 (the mixing
+bound); bf16 2.5e-2: the block rounds u, g, y and z to bf16 (four roundings of
+at most 2^-9 relative each, carried through maps of gain about one) and its
+output once more, and the oracle rounds none of them.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import workloads as W
+from gpu_util import act64, dev_act, dev_f32, host, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+ops = None
+
+
+def setup_module(module):
+    global ops
+    from paper_2607_05583_amd import ops as _ops
+    ops = _ops
+    assert torch.cuda.is_available(), "GPU tests need a HIP device"
+
+
+@pytest.mark.parametrize("N,G,di,dq,act", [(1, 1, 3, 5, "f32"), (1000, 4, 64, 64, "f32"), (777, 8, 32, 32, "bf16"),
+                                           (4096, 1, 256, 256, "bf16"), (130, 3, 7, 11, "f32")])
+def test_grouped_linear_parity(N, G, di, dq, act):
+    say(f"grouped linear N={N} G={G} di={di} dq={dq} {act}")
+    r = np.random.default_rng(N + G)
+    x = W._act(r, (N, G * di), act)
+    Wt = W._act(r, (G, di, dq), act)
+    y = ops.resonator_grouped_linear(dev_act(x, act), dev_act(Wt, act))
+    torch.cuda.synchronize()
+    ref = O.grouped_linear(act64(x, act), act64(Wt, act))
+    err = rel_err(host(y), ref)
+    say(f"  err {err:.2e}")
+    assert err <= (1e-5 if act == "f32" else 1e-2)
+
+
+@pytest.mark.parametrize("B,L,d,H,K,G,M,act", [(2, 300, 64, 4, 3, 4, 4, "f32"), (1, 1000, 256, 8, 4, 8, 8, "bf16"),
+                                               (2, 257, 32, 2, 0, 1, 3, "bf16")])
+def test_block_fwd_parity(B, L, d, H, K, G, M, act):
+    say(f"block fwd B={B} L={L} d={d} H={H} K={K} G={G} M={M} {act}")
+    p = W.block_inputs(B * L + d, B, L, d, H, K, G, M, act)
+    dev = lambda a: dev_act(a, act)
+    pk = ("gamma", "omega", "amp", "phase")
+    o = ops.resonator_block_fwd(dev(p["x"]), dev(p["Wu"]), dev(p["Wg"]), dev(p["Wo"]), *[dev_f32(p[k]) for k in pk],
+                                dev_f32(p["Ct"]), p["lambda_c"], dev_f32(p["w"]) if K else None,
+                                dev_f32(p["s"]) if K else None, H)
+    torch.cuda.synchronize()
+    ref = O.block_fwd(act64(p["x"], act), act64(p["Wu"], act), act64(p["Wg"], act), act64(p["Wo"], act),
+                      *[p[k] for k in pk], p["Ct"], p["lambda_c"], p["w"] if K else np.zeros((d, 0)), p["s"], H)
+    err = rel_err(host(o), ref)
+    say(f"  err {err:.2e}")
+    assert err <= (1e-4 if act == "f32" else 2.5e-2)
+    # the dense block-diagonal route gives the same result
+    dense = tuple(ops.resonator_block_diag_weight(dev(p[k])) for k in ("Wu", "Wg", "Wo"))
+    od = ops.resonator_block_fwd(dev(p["x"]), dev(p["Wu"]), dev(p["Wg"]), dev(p["Wo"]),
+                                 *[dev_f32(p[k]) for k in pk], dev_f32(p["Ct"]), p["lambda_c"],
+                                 dev_f32(p["w"]) if K else None, dev_f32(p["s"]) if K else None, H, dense=dense)
+    torch.cuda.synchronize()
+    assert rel_err(host(od), ref) <= (1e-4 if act == "f32" else 2.5e-2)
+
+
+@pytest.mark.parametrize("G,di,dq,act", [(8, 32, 32, "bf16"), (3, 5, 7, "f32"), (1, 4, 4, "f32")])
+def test_block_diag_weight(G, di, dq, act):
+    r = np.random.default_rng(G)
+    Wt = W._act(r, (G, di, dq), act)
+    Wd = host(ops.resonator_block_diag_weight(dev_act(Wt, act)))[0]
+    ref = np.zeros((G * di, G * dq))
+    for g in range(G):
+        ref[g * di:(g + 1) * di, g * dq:(g + 1) * dq] = act64(Wt, act)[g]
+    assert np.array_equal(Wd, ref)

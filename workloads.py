@@ -188,3 +188,27 @@ def epilogue_inputs(seed: int, B: int, L: int, H: int, dh: int, K: int, act: str
     w = (rng.standard_normal((D, K)) / math.sqrt(max(K, 1))).astype(np.float32)
     s = rng.standard_normal(D).astype(np.float32)
     return dict(y=y, gate=gate, v=v, dz=dz, Ct=Ct, w=w, s=s, lambda_c=float(lambda_c), H=H, K=K)
+
+
+# --------------------------------------------------------------------------
+# mixer block (grouped projections around the mixing and the epilogue)
+# --------------------------------------------------------------------------
+def block_inputs(seed: int, B: int, L: int, d: int, H: int, K: int, G: int, M: int, act: str = "f32"):
+    """Seeded inputs of the mixer block: x [B, L, d] standard normal; W_u, W_g,
+    W_out [G, d/G, d/G] normal with variance G/d (unit gain on average); mode
+    parameters as the 8K config (gamma log-uniform in [1e-4, 1]); Ct [H, H]
+    standard normal, lambda_c = 0.5, taps w [d, K] N(0, 1/K), scales s [d] N(0, 1).
+    Activations and weights are float32 or bf16 bits.  Draw order x, W_u, W_g,
+    W_out, mode parameters, Ct, w, s."""
+    rng = np.random.default_rng(seed)
+    x = _act(rng, (B, L, d), act)
+    sd = 1.0 / math.sqrt(d // G)
+    Ws = []
+    for _ in range(3):
+        w32 = (rng.standard_normal((G, d // G, d // G)) * sd).astype(np.float32)
+        Ws.append(f32_to_bf16_bits(w32) if act == "bf16" else w32)
+    p = draw_params(rng, d, M, (1e-4, 1.0), True)
+    Ct = rng.standard_normal((H, H)).astype(np.float32)
+    w = (rng.standard_normal((d, K)) / math.sqrt(max(K, 1))).astype(np.float32)
+    s = rng.standard_normal(d).astype(np.float32)
+    return dict(x=x, Wu=Ws[0], Wg=Ws[1], Wo=Ws[2], **p, Ct=Ct, lambda_c=0.5, w=w, s=s, H=H, K=K, G=G)
