@@ -101,3 +101,37 @@ def test_planted_mistakes_are_caught():
     y = O.mix_direct(0.5 * p["x"], p["gamma"], p["omega"], p["amp"], p["phase"])
     # drive and gate swapped would give sigmoid(x) * mix(x / 2): must differ from the true block
     assert not np.allclose(swapped, expit(p["x"]) * y, rtol=1e-6)
+
+
+def test_block_backward_by_finite_differences():
+    """Every gradient of the block against central differences of block_fwd."""
+    p = _problem(seed=11, B=1, L=12, d=4, H=2, K=2, G=2, M=2)
+    r = np.random.default_rng(0)
+    do = r.normal(size=p["x"].shape)
+    g = BO.block_bwd(**p, do=do)
+    names = {"x": "dx", "Wu": "dWu", "Wg": "dWg", "Wo": "dWo", "gamma": "dgamma", "omega": "domega", "amp": "damp",
+             "phase": "dphase", "Ct": "dCt", "w": "dw", "s": "ds"}
+    h = 1e-6
+    for k, gk in names.items():
+        base = np.asarray(p[k], dtype=np.float64)
+        flat = base.reshape(-1)
+        for i in r.choice(flat.size, size=min(4, flat.size), replace=False):
+            e = np.zeros_like(flat)
+            e[i] = h
+            fp = np.sum(do * BO.block_fwd(**{**p, k: (flat + e).reshape(base.shape)}))
+            fm = np.sum(do * BO.block_fwd(**{**p, k: (flat - e).reshape(base.shape)}))
+            fd = (fp - fm) / (2 * h)
+            assert abs(np.asarray(g[gk]).reshape(-1)[i] - fd) <= 1e-6 * max(1.0, abs(fd)), (k, i)
+    fp = np.sum(do * BO.block_fwd(**{**p, "lambda_c": p["lambda_c"] + h}))
+    fm = np.sum(do * BO.block_fwd(**{**p, "lambda_c": p["lambda_c"] - h}))
+    assert abs(g["dlambda_c"] - (fp - fm) / (2 * h)) <= 1e-6 * max(1.0, abs((fp - fm) / (2 * h)))
+
+
+def test_grouped_linear_backward_against_block_diagonal():
+    r = np.random.default_rng(4)
+    x, Wt, dy = r.normal(size=(9, 12)), r.normal(size=(3, 4, 2)), r.normal(size=(9, 6))
+    dx, dW = BO.grouped_linear_bwd(x, Wt, dy)
+    np.testing.assert_allclose(dx, dy @ _block_diag(Wt).T, rtol=1e-12, atol=1e-12)
+    full = x.T @ dy
+    for g in range(3):
+        np.testing.assert_allclose(dW[g], full[g * 4:(g + 1) * 4, g * 2:(g + 1) * 2], rtol=1e-12, atol=1e-12)
