@@ -379,9 +379,25 @@ def main():
         t1e.record(stream)
         torch.cuda.synchronize()
         b_us = t0e.elapsed_time(t1e) * 1e3 / reps
-        blk.append({"L": Lb, "us": b_us, "tokens_per_s": 4 * Lb / (b_us * 1e-6)})
-        log(f"mixer block forward B4 L={Lb} d256: {b_us:.1f} us ({4 * Lb / (b_us * 1e-6) / 1e6:.1f} M tokens/s)")
-        del bt
+        # backward (recomputes the forward's intermediates, then the chain rule)
+        dob = torch.randn_like(bt["x"], dtype=torch.float32).to(torch.bfloat16)
+
+        def block_bwd():
+            return ops.resonator_block_bwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6],
+                                           8, dob, dense=dense)
+
+        block_bwd()
+        torch.cuda.synchronize()
+        t0e.record(stream)
+        for _ in range(reps):
+            block_bwd()
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        bb_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        blk.append({"L": Lb, "fwd_us": b_us, "bwd_us": bb_us, "fwd_tokens_per_s": 4 * Lb / (b_us * 1e-6)})
+        log(f"mixer block B4 L={Lb} d256: forward {b_us:.1f} us ({4 * Lb / (b_us * 1e-6) / 1e6:.1f} M tokens/s), "
+            f"backward {bb_us:.1f} us")
+        del bt, dob
 
     # ---------------- kernel tail: mixing vs a quadratic causal reference ----------------
     kt = []
@@ -438,7 +454,8 @@ def main():
                           "points": sweep},
         "mixer_block": {"workload": "B4 d_model 256, bf16: grouped in-projections (8 groups, run as dense GEMMs on the "
                                     "block-diagonal weights) to drive and gate, "
-                                    "mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection; forward",
+                                    "mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection; forward, and backward "
+                                    "(recomputed forward, then the chain rule)",
                         "points": blk},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol",

@@ -164,6 +164,19 @@ int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void*
                              int64_t d_out, int64_t G, void* stream);
 
 /*
+ * Backward of resonator_grouped_linear (loss sum(dy * y)):
+ *   data:    dx[n, g di + i] = sum_j dy[n, g dq + j] W[g][i][j]     (dx of dtype dt)
+ *   weight:  dW[g][i][j]    = sum_n x[n, g di + i] dy[n, g dq + j]  (dW float32)
+ * With accumulate != 0 the result is added to the output instead of replacing
+ * it (gradients of several uses of one input or weight).  Same array
+ * conventions as the forward; outputs must not overlap the inputs.
+ */
+int resonator_grouped_linear_bwd_data(const void* dy, const void* W, res_dtype_t dt, void* dx, int64_t N,
+                                      int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream);
+int resonator_grouped_linear_bwd_weight(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,
+                                        int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream);
+
+/*
  * Dense [d_in][d_out] copy of a grouped weight W [G][d_in/G][d_out/G], zero off
  * the diagonal blocks, so that resonator_grouped_linear with G = 1 on it gives
  * exactly the grouped product (the zero blocks add exact zeros) with the GEMM

@@ -474,6 +474,50 @@ int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void*
   return RES_OK;
 }
 
+static int gl_check(int64_t N, int64_t d_in, int64_t d_out, int64_t G, res_dtype_t dt) {
+  if (N < 1 || d_in < 1 || d_out < 1 || G < 1)
+    return fail(RES_ERR_INVALID_ARG, "N, d_in, d_out and G must be >= 1");
+  if (d_in % G || d_out % G)
+    return fail(RES_ERR_INVALID_ARG, "d_in (%lld) and d_out (%lld) must be multiples of G (%lld)", (long long)d_in,
+                (long long)d_out, (long long)G);
+  if (N > INT32_MAX || d_in > INT32_MAX || d_out > INT32_MAX)
+    return fail(RES_ERR_UNSUPPORTED, "N, d_in and d_out must be below 2^31");
+  if (!dtype_ok(dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  return RES_OK;
+}
+
+int resonator_grouped_linear_bwd_data(const void* dy, const void* W, res_dtype_t dt, void* dx, int64_t N,
+                                      int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream) {
+  int rc = gl_check(N, d_in, d_out, G, dt);
+  if (rc) return rc;
+  if (!dy || !W || !dx) return fail(RES_ERR_INVALID_ARG, "dy, W and dx must be non-null");
+  const size_t es = elt_size(dt);
+  if (!aligned(dy, es) || !aligned(W, es) || !aligned(dx, es))
+    return fail(RES_ERR_MISALIGNED, "dy, W and dx must be aligned to their element");
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * es;
+  if (overlap(dx, nx, dy, ny) || overlap(dx, nx, W, nw)) return fail(RES_ERR_INVALID_ARG, "dx must not overlap dy or W");
+  const char* err = launch_grouped_linear_bwd_data(dy, W, dx, N, d_in, d_out, G, dt == RES_BF16, accumulate != 0,
+                                                   (hipStream_t)stream);
+  if (err) return fail(RES_ERR_HIP, "grouped linear backward (data): %s", err);
+  return RES_OK;
+}
+
+int resonator_grouped_linear_bwd_weight(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,
+                                        int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream) {
+  int rc = gl_check(N, d_in, d_out, G, dt);
+  if (rc) return rc;
+  if (!x || !dy || !dW) return fail(RES_ERR_INVALID_ARG, "x, dy and dW must be non-null");
+  const size_t es = elt_size(dt);
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(dW, 4))
+    return fail(RES_ERR_MISALIGNED, "x and dy aligned to their element, dW to 4 bytes");
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * 4;
+  if (overlap(dW, nw, x, nx) || overlap(dW, nw, dy, ny)) return fail(RES_ERR_INVALID_ARG, "dW must not overlap x or dy");
+  const char* err = launch_grouped_linear_bwd_weight(x, dy, dW, N, d_in, d_out, G, dt == RES_BF16, accumulate != 0,
+                                                     (hipStream_t)stream);
+  if (err) return fail(RES_ERR_HIP, "grouped linear backward (weight): %s", err);
+  return RES_OK;
+}
+
 int resonator_block_diag_weight(const void* W, res_dtype_t dt, int64_t d_in, int64_t d_out, int64_t G,
                                 void* W_dense, void* stream) {
   if (d_in < 1 || d_out < 1 || G < 1 || d_in % G || d_out % G)

@@ -47,6 +47,47 @@ const char* launch_grouped_linear(const void* x, const void* W, void* y, int64_t
   return s == rocblas_status_success ? nullptr : rocblas_status_to_string(s);
 }
 
+// Backward of the grouped projection, in the same column-major view:
+//   data:   dx^T_g [di x N] = W[g] [di x dq] dy^T_g [dq x N]    (A = W^T stored, transposed)
+//   weight: dW[g]^T [dq x di] = dy^T_g [dq x N] x_g [N x di]      (B = x^T stored, transposed)
+// accumulate adds into the output (beta = 1) instead of overwriting it.
+const char* launch_grouped_linear_bwd_data(const void* dy, const void* W, void* dx, int64_t N, int64_t d_in,
+                                           int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return "no current HIP device";
+  rocblas_handle h = handle_for(dev);
+  if (!h) return "rocblas_create_handle failed";
+  if (rocblas_set_stream(h, st) != rocblas_status_success) return "rocblas_set_stream failed";
+  const rocblas_datatype t = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+  const int64_t di = d_in / G, dq = d_out / G;
+  const float alpha = 1.f, beta = accumulate ? 1.f : 0.f;
+  const rocblas_status s = rocblas_gemm_strided_batched_ex(
+      h, rocblas_operation_transpose, rocblas_operation_none, (rocblas_int)di, (rocblas_int)N, (rocblas_int)dq,
+      &alpha, W, t, (rocblas_int)dq, (rocblas_stride)(di * dq), dy, t, (rocblas_int)d_out, (rocblas_stride)dq, &beta,
+      dx, t, (rocblas_int)d_in, (rocblas_stride)di, dx, t, (rocblas_int)d_in, (rocblas_stride)di, (rocblas_int)G,
+      rocblas_datatype_f32_r, rocblas_gemm_algo_standard, 0, 0);
+  return s == rocblas_status_success ? nullptr : rocblas_status_to_string(s);
+}
+
+const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, float* dW, int64_t N, int64_t d_in,
+                                             int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAX_DEVICES) return "no current HIP device";
+  rocblas_handle h = handle_for(dev);
+  if (!h) return "rocblas_create_handle failed";
+  if (rocblas_set_stream(h, st) != rocblas_status_success) return "rocblas_set_stream failed";
+  const rocblas_datatype t = bf16 ? rocblas_datatype_bf16_r : rocblas_datatype_f32_r;
+  const int64_t di = d_in / G, dq = d_out / G;
+  const float alpha = 1.f, beta = accumulate ? 1.f : 0.f;
+  const rocblas_status s = rocblas_gemm_strided_batched_ex(
+      h, rocblas_operation_none, rocblas_operation_transpose, (rocblas_int)dq, (rocblas_int)di, (rocblas_int)N,
+      &alpha, dy, t, (rocblas_int)d_out, (rocblas_stride)dq, x, t, (rocblas_int)d_in, (rocblas_stride)di, &beta, dW,
+      rocblas_datatype_f32_r, (rocblas_int)dq, (rocblas_stride)(di * dq), dW, rocblas_datatype_f32_r,
+      (rocblas_int)dq, (rocblas_stride)(di * dq), (rocblas_int)G, rocblas_datatype_f32_r, rocblas_gemm_algo_standard,
+      0, 0);
+  return s == rocblas_status_success ? nullptr : rocblas_status_to_string(s);
+}
+
 // Dense [d_in][d_out] copy of a block-diagonal weight W [G][d_in/G][d_out/G]
 // (zeros off the diagonal blocks): one dense GEMM then gives exactly the grouped
 // product (the zero blocks add exact zeros to float32 sums) with the library's

@@ -108,6 +108,10 @@ hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y
                          const float* phase, float* state, hipStream_t st);
 const char* launch_grouped_linear(const void* x, const void* W, void* y, int64_t N, int64_t d_in, int64_t d_out,
                                   int64_t G, bool bf16, hipStream_t st);
+const char* launch_grouped_linear_bwd_data(const void* dy, const void* W, void* dx, int64_t N, int64_t d_in,
+                                           int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
+const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, float* dW, int64_t N, int64_t d_in,
+                                             int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
 hipError_t launch_block_diag(const void* W, void* Wd, int64_t d_in, int64_t d_out, int64_t G, bool bf16,
                              hipStream_t st);
 size_t quad_workspace_bytes(int64_t L, int64_t D);

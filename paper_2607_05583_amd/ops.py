@@ -209,6 +209,36 @@ def resonator_grouped_linear(x, W, out=None):
     return y
 
 
+def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
+    """Gradients of sum(dy * grouped_linear(x, W)): (dx of x's dtype, dW float32).
+
+    With ``accumulate`` the gradients are added into the given ``dx``/``dW``; pass
+    x = None to skip dW, W = None to skip dx."""
+    ref = x if x is not None else dy
+    _dev(dy, "dy")
+    d_out = dy.shape[-1]
+    N = dy.numel() // d_out
+    out = []
+    if W is not None:
+        _dev(W, "W")
+        G, di, dq = W.shape
+        if dx is None:
+            dx = torch.empty(dy.shape[:-1] + (G * di,), dtype=dy.dtype, device=dy.device)
+        check(_lib.lib().resonator_grouped_linear_bwd_data(_ptr(dy), _ptr(W), _code(dy), _ptr(dx), N, G * di, d_out, G,
+                                                           int(accumulate), _stream(dy.device)))
+    if x is not None:
+        _dev(x, "x")
+        d_in = x.shape[-1]
+        G = (W.shape[0] if W is not None else None) if dW is None else dW.shape[0]
+        if G is None:
+            raise ValueError("need W or dW to know the groups")
+        if dW is None:
+            dW = torch.empty((G, d_in // G, d_out // G), dtype=torch.float32, device=ref.device)
+        check(_lib.lib().resonator_grouped_linear_bwd_weight(_ptr(x), _ptr(dy), _code(x), _ptr(dW), N, d_in, d_out, G,
+                                                             int(accumulate), _stream(dy.device)))
+    return dx, dW
+
+
 def resonator_block_diag_weight(W):
     """Dense [1, d_in, d_out] block-diagonal copy of a grouped weight [G, d_in/G, d_out/G]."""
     _dev(W, "W")
@@ -231,6 +261,33 @@ def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
     return resonator_grouped_linear(z, Po)
+
+
+def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, do, dense=None):
+    """Gradients of sum(do * resonator_block_fwd(...)): the forward's intermediates
+    are recomputed, then the chain rule runs backwards through the output
+    projection, the epilogue, the mixing and the two input projections.  Returns
+    a dict: dx, dWu, dWg, dWo (float32), dgamma, domega, damp, dphase, dCt,
+    dlambda_c, dw, ds.  ``dense`` as for resonator_block_fwd (data gradients
+    then run as dense GEMMs; weight gradients always per group)."""
+    Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
+    u = resonator_grouped_linear(x, Pu)
+    g = resonator_grouped_linear(x, Pg)
+    y = resonator_mix_fwd(u, gamma, omega, amp, phase)
+    z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
+    G = Wo.shape[0]
+    dz, _ = resonator_grouped_linear_bwd(None, Po, do)
+    _, dWo = resonator_grouped_linear_bwd(z, None, do, dW=torch.empty_like(Wo, dtype=torch.float32))
+    dy, dg, dv, dCt, dlam, dw, ds = resonator_epilogue_bwd(y, g, u, dz, Ct, lambda_c, w, s, H)
+    mb = resonator_mix_bwd(u, dy, gamma, omega, amp, phase)
+    # du = mb["dx"] + dv enters both the data and the weight gradient of W_u by accumulation
+    dx, dWu = resonator_grouped_linear_bwd(x, Pu, mb["dx"], dW=torch.empty_like(Wu, dtype=torch.float32))
+    if dv is not None:
+        resonator_grouped_linear_bwd(x, Pu, dv, dx=dx, dW=dWu, accumulate=True)
+    _, dWg = resonator_grouped_linear_bwd(x, None, dg, dW=torch.empty_like(Wg, dtype=torch.float32))
+    resonator_grouped_linear_bwd(None, Pg, dg, dx=dx, accumulate=True)
+    return dict(dx=dx, dWu=dWu, dWg=dWg, dWo=dWo, dgamma=mb["dgamma"], domega=mb["domega"], damp=mb["damp"],
+                dphase=mb["dphase"], dCt=dCt, dlambda_c=dlam, dw=dw, ds=ds)
 
 
 ALPHA_MIN = 1e-4  # the paper's floor on the damping

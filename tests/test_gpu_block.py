@@ -77,3 +77,56 @@ def test_block_diag_weight(G, di, dq, act):
     for g in range(G):
         ref[g * di:(g + 1) * di, g * dq:(g + 1) * dq] = act64(Wt, act)[g]
     assert np.array_equal(Wd, ref)
+
+
+@pytest.mark.parametrize("N,G,di,dq,act", [(1000, 4, 16, 8, "f32"), (777, 8, 32, 32, "bf16"), (300, 1, 24, 40, "f32")])
+def test_grouped_linear_backward_parity(N, G, di, dq, act):
+    say(f"grouped linear bwd N={N} G={G} di={di} dq={dq} {act}")
+    r = np.random.default_rng(N + 3 * G)
+    x = W._act(r, (N, G * di), act)
+    Wt = W._act(r, (G, di, dq), act)
+    dy = W._act(r, (N, G * dq), act)
+    dx, dW = ops.resonator_grouped_linear_bwd(dev_act(x, act), dev_act(Wt, act), dev_act(dy, act))
+    # accumulation adds a second gradient of the same size
+    dx2, dW2 = ops.resonator_grouped_linear_bwd(dev_act(x, act), dev_act(Wt, act), dev_act(dy, act), dx=dx.clone(),
+                                                dW=dW.clone(), accumulate=True)
+    torch.cuda.synchronize()
+    rdx, rdW = O.grouped_linear_bwd(act64(x, act), act64(Wt, act), act64(dy, act))
+    b = 1e-5 if act == "f32" else 1e-2
+    assert rel_err(host(dx), rdx) <= b and rel_err(host(dW), rdW) <= 1e-5
+    assert rel_err(host(dx2), 2 * rdx) <= b and rel_err(host(dW2), 2 * rdW) <= 1e-5
+
+
+@pytest.mark.parametrize("B,L,d,H,K,G,M,act", [(2, 300, 64, 4, 3, 4, 4, "f32"), (1, 1000, 256, 8, 4, 8, 8, "bf16"),
+                                               (2, 257, 32, 2, 0, 1, 3, "f32")])
+def test_block_bwd_parity(B, L, d, H, K, G, M, act):
+    say(f"block bwd B={B} L={L} d={d} H={H} K={K} G={G} M={M} {act}")
+    p = W.block_inputs(7 * B * L + d, B, L, d, H, K, G, M, act)
+    r = np.random.default_rng(d)
+    do = W._act(r, (B, L, d), act)
+    dev = lambda a: dev_act(a, act)
+    pk = ("gamma", "omega", "amp", "phase")
+    args = [dev(p["x"]), dev(p["Wu"]), dev(p["Wg"]), dev(p["Wo"]), *[dev_f32(p[k]) for k in pk], dev_f32(p["Ct"]),
+            p["lambda_c"], dev_f32(p["w"]) if K else None, dev_f32(p["s"]) if K else None, H, dev(do)]
+    gr = ops.resonator_block_bwd(*args)
+    dense = tuple(ops.resonator_block_diag_weight(dev(p[k])) for k in ("Wu", "Wg", "Wo"))
+    grd = ops.resonator_block_bwd(*args, dense=dense)
+    torch.cuda.synchronize()
+    ref = O.block_bwd(act64(p["x"], act), act64(p["Wu"], act), act64(p["Wg"], act), act64(p["Wo"], act),
+                      *[p[k] for k in pk], p["Ct"], p["lambda_c"], p["w"] if K else np.zeros((d, 0)), p["s"], H,
+                      act64(do, act))
+    # bf16: the backward rounds the recomputed u, g, y, z and the gradients dz,
+    # dy, dgate, dv and the mixing's dx to bf16 (about ten roundings of at most
+    # 2^-9 relative, some multiplied together, as in dgate = dz ybar sg (1 - sg)),
+    # none of which the oracle rounds; the float32 cases check the chain itself
+    b_act, b_par = (1e-4, 1e-4) if act == "f32" else (4e-2, 4e-2)
+    for g in (gr, grd):
+        errs = {}
+        for k, v in ref.items():
+            if v is None:
+                assert g[k] is None
+                continue
+            errs[k] = rel_err(host(g[k]).reshape(np.shape(v)), v)
+        say("  errs " + " ".join(f"{k}={e:.2e}" for k, e in errs.items()))
+        for k, e in errs.items():
+            assert e <= (b_act if k == "dx" else b_par), k
