@@ -317,7 +317,7 @@ def main():
         ops.resonator_mix_bwd(tx, tdy, *tprm)
     torch.cuda.synchronize()
     nt = 10
-    t0e, t1e, t2e = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    t0e, t1e, t2e, t3e = (torch.cuda.Event(enable_timing=True) for _ in range(4))
     t0e.record(stream)
     for _ in range(nt):
         ops.resonator_mix_fwd(tx, *tprm)
@@ -407,6 +407,7 @@ def main():
         prk = [torch.from_numpy(pk[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
         ops.resonator_mix_fwd(xk, *prk)
         ops.resonator_quadratic_reference(xk, *prk)
+        ops.resonator_fft_reference(xk, *prk)
         torch.cuda.synchronize()
         reps = 20
         t0e.record(stream)
@@ -416,13 +417,18 @@ def main():
         for _ in range(3):
             ops.resonator_quadratic_reference(xk, *prk)
         t2e.record(stream)
+        for _ in range(reps):
+            ops.resonator_fft_reference(xk, *prk)
+        t3e.record(stream)
         torch.cuda.synchronize()
         mix_us = t0e.elapsed_time(t1e) * 1e3 / reps
         quad_us = t1e.elapsed_time(t2e) * 1e3 / 3
+        fft_us = t2e.elapsed_time(t3e) * 1e3 / reps
         kt.append({"L": Lk, "mix_us": mix_us, "quadratic_us": quad_us, "speedup": quad_us / mix_us,
-                   "quadratic_TFLOPs": Lk * (Lk + 1) / 2 * 256 * 2 / (quad_us * 1e-6) / 1e12})
-        log(f"kernel tail L={Lk}: mixing {mix_us:.1f} us, quadratic reference {quad_us:.0f} us, "
-            f"speedup {quad_us / mix_us:.0f}x")
+                   "quadratic_TFLOPs": Lk * (Lk + 1) / 2 * 256 * 2 / (quad_us * 1e-6) / 1e12,
+                   "fft_us": fft_us, "fft_over_mix": fft_us / mix_us})
+        log(f"kernel tail L={Lk}: mixing {mix_us:.1f} us, quadratic reference {quad_us:.0f} us "
+            f"(speedup {quad_us / mix_us:.0f}x), FFT convolution {fft_us:.1f} us ({fft_us / mix_us:.1f}x)")
         del xk
 
     cpu = None
@@ -458,7 +464,8 @@ def main():
                                     "(recomputed forward, then the chain rule)",
                         "points": blk},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
-                                    "causal reference (taps + Toeplitz sum), paper Table 5 protocol",
+                                    "causal reference (taps + Toeplitz sum), paper Table 5 protocol, and vs the "
+                                    "zero-padded FFT convolution (rocFFT, the paper's prefill form)",
                         "points": kt},
         "decode_multi_step": {"workload": f"{c4.name}: drives known in advance",
                               "k8_us_per_launch": k8_us, "k8_us_per_step": k8_us / 8,

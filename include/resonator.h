@@ -202,6 +202,26 @@ int resonator_quadratic_reference(const float* x, float* y, int64_t B, int64_t L
                                   void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * FFT causal convolution: the paper's own prefill evaluation of the mixing
+ * (Sec. 3.2, the FFT form), kept as a baseline for the chunked scan, not part
+ * of the mixing path.  Per channel d, with n the next power of two >= 2L,
+ *   y[b,:,d] = IFFT( FFT(x[b,:,d] zero-padded to n) . FFT(K_d zero-padded to n) )[0:L]
+ * in float32 through rocFFT (batched real transforms), with the taps K_d[tau],
+ * tau < L, evaluated in float64 and rounded to float32.  Zero initial state.
+ *   x, y   [B][L][D] float32 device memory (y must not overlap x or ws)
+ *   ws     resonator_fft_reference_workspace_bytes(B, L, D) bytes, 256-byte
+ *          aligned: the padded time-major signal [B D][n+2], the padded taps
+ *          [D][n+2] and rocFFT's work area
+ * Plans are created on first use per (device, n, batch) and kept for the
+ * process; the workspace-size query creates them too (it returns 0 on error,
+ * with the message in resonator_last_error).  B <= 65535, L <= 2^26.
+ */
+size_t resonator_fft_reference_workspace_bytes(int64_t B, int64_t L, int64_t D);
+int resonator_fft_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                            const float* gamma, const float* omega, const float* amp, const float* phase, void* ws,
+                            size_t ws_bytes, void* stream);
+
+/*
  * Constrained parameterization (Sec. 3.1, last paragraph): unconstrained
  * parameters are mapped into the valid ranges of the damping and frequency,
  *   gamma = alpha_min + softplus(theta_gamma)      (> alpha_min; the paper's floor is 1e-4)

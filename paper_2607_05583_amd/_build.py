@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libresonator.so")
-SOURCES = ["fwd.hip", "bwd.hip", "decode.hip", "epilogue.hip", "params.hip", "quadref.hip", "gemm.hip", "api.hip"]
+SOURCES = ["fwd.hip", "bwd.hip", "decode.hip", "epilogue.hip", "params.hip", "quadref.hip", "gemm.hip", "fftref.hip", "api.hip"]
 ARCH = "gfx950"
 
 
@@ -60,7 +60,7 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("HIP compile failed:\n" + "\n".join(f"--- {s}\n{e}" for s, e in failed))
     tmp = LIB + ".tmp"
     rc, err = _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp,
-                    *[j[1] for j in jobs], "-L/opt/rocm/lib", "-lrocblas", "-Wl,-rpath,/opt/rocm/lib"])
+                    *[j[1] for j in jobs], "-L/opt/rocm/lib", "-lrocblas", "-lrocfft", "-Wl,-rpath,/opt/rocm/lib"])
     if rc != 0:
         raise RuntimeError("link failed:\n" + err)
     os.replace(tmp, LIB)

@@ -23,6 +23,7 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
+           "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
            "resonator_grouped_linear", "resonator_block_diag_weight",
            "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_weight")
 
@@ -74,6 +75,10 @@ def _declare(lib):
     lib.resonator_quadratic_reference_workspace_bytes.argtypes = [i64, i64]
     lib.resonator_quadratic_reference.restype = i32
     lib.resonator_quadratic_reference.argtypes = [vp, vp, i64, i64, i64, i64, fp, fp, fp, fp, vp, sz, vp]
+    lib.resonator_fft_reference_workspace_bytes.restype = sz
+    lib.resonator_fft_reference_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.resonator_fft_reference.restype = i32
+    lib.resonator_fft_reference.argtypes = [vp, vp, i64, i64, i64, i64, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_grouped_linear.restype = i32
     lib.resonator_grouped_linear.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, vp]
     lib.resonator_block_diag_weight.restype = i32

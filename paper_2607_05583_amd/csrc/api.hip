@@ -564,6 +564,48 @@ int resonator_quadratic_reference(const float* x, float* y, int64_t B, int64_t L
 }
 
 // ---------------------------------------------------------------------------
+// FFT convolution (the paper's own prefill evaluation, Sec. 3.2) as a baseline
+// ---------------------------------------------------------------------------
+static int fft_check(int64_t B, int64_t L, int64_t D) {
+  if (B < 1 || L < 1 || D < 1) return fail(RES_ERR_INVALID_ARG, "B, L and D must be >= 1");
+  if (B > 65535 || D > 65535 * 32 || L > (1LL << 26) || B * D * (int64_t)(fft_next_pow2(L) + 2) > (1LL << 40))
+    return fail(RES_ERR_UNSUPPORTED, "FFT reference needs B <= 65535, L <= 2^26 and a padded buffer under 2^40");
+  return RES_OK;
+}
+
+size_t resonator_fft_reference_workspace_bytes(int64_t B, int64_t L, int64_t D) {
+  if (fft_check(B, L, D)) return 0;
+  size_t bytes = 0;
+  if (const char* e = fft_workspace_bytes(B, L, D, &bytes)) {
+    fail(RES_ERR_HIP, "FFT plan: %s", e);
+    return 0;
+  }
+  return bytes;
+}
+
+int resonator_fft_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                            const float* gamma, const float* omega, const float* amp, const float* phase, void* ws,
+                            size_t ws_bytes, void* stream) {
+  int rc = check_sizes(B, L, D, M, false);
+  if (rc) return rc;
+  if ((rc = fft_check(B, L, D))) return rc;
+  if (!x || !y) return fail(RES_ERR_INVALID_ARG, "x and y must be non-null");
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  size_t need = 0;
+  if (const char* e = fft_workspace_bytes(B, L, D, &need)) return fail(RES_ERR_HIP, "FFT plan: %s", e);
+  if (!ws || ws_bytes < need)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned(x, 4) || !aligned(y, 4) || !aligned(ws, 256))
+    return fail(RES_ERR_MISALIGNED, "x and y must be 4-byte and the workspace 256-byte aligned");
+  const size_t n = (size_t)(B * L * D) * 4;
+  if (overlap(y, n, x, n) || overlap(y, n, ws, need) || overlap(x, n, ws, need))
+    return fail(RES_ERR_INVALID_ARG, "x, y and the workspace must not overlap");
+  if (const char* e = launch_fft_reference(x, y, B, L, D, M, gamma, omega, amp, phase, ws, (hipStream_t)stream))
+    return fail(RES_ERR_HIP, "FFT reference: %s", e);
+  return RES_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Constrained parameterization (Sec. 3.1, last paragraph)
 // ---------------------------------------------------------------------------
 static int prm_check_n(int64_t n) {

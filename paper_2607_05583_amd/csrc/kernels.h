@@ -115,6 +115,11 @@ const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, floa
 hipError_t launch_block_diag(const void* W, void* Wd, int64_t d_in, int64_t d_out, int64_t G, bool bf16,
                              hipStream_t st);
 size_t quad_workspace_bytes(int64_t L, int64_t D);
+size_t fft_next_pow2(int64_t L);
+const char* fft_workspace_bytes(int64_t B, int64_t L, int64_t D, size_t* bytes);
+const char* launch_fft_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
+                                 const float* gamma, const float* omega, const float* amp, const float* phase,
+                                 void* ws, hipStream_t st);
 hipError_t launch_quad_reference(const float* x, float* y, int64_t B, int64_t L, int64_t D, int64_t M,
                                  const float* gamma, const float* omega, const float* amp, const float* phase,
                                  float* K, hipStream_t st);

@@ -191,6 +191,25 @@ def resonator_quadratic_reference(x, gamma, omega, amp, phase):
     return y
 
 
+def resonator_fft_reference(x, gamma, omega, amp, phase):
+    """The mixing by zero-padded FFT convolution (the paper's prefill form), float32 [B, L, D]."""
+    _dev(x, "x")
+    if x.dtype != torch.float32 or x.dim() != 3:
+        raise ValueError("x must be float32 [B, L, D]")
+    B, L, D = x.shape
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase, D)
+    M = gamma.shape[1]
+    y = torch.empty_like(x)
+    n = _lib.lib().resonator_fft_reference_workspace_bytes(B, L, D)
+    if n == 0:
+        raise _lib.ResonatorError(0, "FFT workspace query failed: "
+                                  + _lib.lib().resonator_last_error().decode(errors="replace"))
+    ws = torch.empty(n, dtype=torch.uint8, device=x.device)
+    check(_lib.lib().resonator_fft_reference(_ptr(x), _ptr(y), B, L, D, M, _ptr(gamma), _ptr(omega),
+                                             _ptr(amp), _ptr(phase), _ptr(ws), n, _stream(x.device)))
+    return y
+
+
 def resonator_grouped_linear(x, W, out=None):
     """y = x W for a block-diagonal W of G groups: x [..., d_in], W [G, d_in/G, d_out/G]."""
     _dev(x, "x")

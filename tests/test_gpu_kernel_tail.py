@@ -1,9 +1,13 @@
-"""GPU parity of the quadratic causal reference (the kernel-tail baseline of
-Sec. 5.3) against the oracle's direct O(L^2) form, and of the mixing path
-against that reference at a length where the oracle would be slow.
+"""GPU parity of the two baselines of the mixing: the quadratic causal
+reference (the kernel-tail baseline of Sec. 5.3) against the oracle's direct
+O(L^2) form, and the FFT convolution (the paper's prefill form, Sec. 3.2)
+against the oracle's FFT form and its direct form; and of the mixing path
+against both at a length where the oracle would be slow.
 
-Tolerance 1e-4 (float32 sums of up to L products of float32 taps, fp32 configs'
-bound)."""
+Tolerance 1e-4: float32 sums of up to L products of float32 taps for the
+quadratic form; for the FFT form the float32 transform error, about
+3 log2(n) eps relative in the 2-norm (under 3e-6 at n = 2^14), an order of
+magnitude more elementwise against the floor of the reference's RMS."""
 import numpy as np
 import pytest
 import torch
@@ -46,4 +50,40 @@ def test_mixing_matches_the_quadratic_reference_at_8k():
     torch.cuda.synchronize()
     err = rel_err(host(ym), host(yq))
     say(f"  mixing vs quadratic reference at 8K: {err:.2e}")
+    assert err <= 1e-4
+
+
+@pytest.mark.parametrize("B,L,D,M,seed", [(1, 1, 1, 1, 81), (2, 130, 70, 3, 82), (1, 1000, 64, 8, 83),
+                                          (3, 257, 129, 16, 84), (1, 4096, 33, 5, 85)])
+def test_fft_reference_matches_the_fft_and_direct_oracles(B, L, D, M, seed):
+    say(f"FFT reference B={B} L={L} D={D} M={M}")
+    prob = W.random_problem(seed, B, L, D, M, act="f32", gamma_range=(1e-3, 0.5), gamma_log=True)
+    y = host(ops.resonator_fft_reference(dev_f32(prob["x"]), *params_dev(prob)))
+    torch.cuda.synchronize()
+    pr = params_np(prob)
+    err_fft = rel_err(y, O.mix_fft(prob["x"], *pr))
+    err_dir = rel_err(y, O.mix_direct(prob["x"], *pr)) if L * L * D <= 1e9 else err_fft
+    say(f"  err vs FFT oracle {err_fft:.2e}, vs direct oracle {err_dir:.2e}")
+    assert err_fft <= 1e-4 and err_dir <= 1e-4
+
+
+def test_fft_reference_repeated_calls_and_two_plan_shapes():
+    """Cached plans: two shapes in turn, each twice, give the same results."""
+    outs = []
+    for seed, (B, L, D) in ((86, (2, 300, 16)), (87, (1, 700, 40)), (86, (2, 300, 16)), (87, (1, 700, 40))):
+        prob = W.random_problem(seed, B, L, D, 4, act="f32", gamma_range=(1e-3, 0.5), gamma_log=True)
+        outs.append(host(ops.resonator_fft_reference(dev_f32(prob["x"]), *params_dev(prob))))
+    np.testing.assert_array_equal(outs[0], outs[2])
+    np.testing.assert_array_equal(outs[1], outs[3])
+
+
+def test_mixing_matches_the_fft_reference_at_32k():
+    prob = W.random_problem(88, 1, 32768, 256, 8, act="f32", gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_f32(prob["x"])
+    pr = params_dev(prob)
+    yf = ops.resonator_fft_reference(x, *pr)
+    ym = ops.resonator_mix_fwd(x, *pr)
+    torch.cuda.synchronize()
+    err = rel_err(host(ym), host(yf))
+    say(f"  mixing vs FFT reference at 32K: {err:.2e}")
     assert err <= 1e-4
