@@ -568,7 +568,8 @@ int resonator_quadratic_reference(const float* x, float* y, int64_t B, int64_t L
 // ---------------------------------------------------------------------------
 static int fft_check(int64_t B, int64_t L, int64_t D) {
   if (B < 1 || L < 1 || D < 1) return fail(RES_ERR_INVALID_ARG, "B, L and D must be >= 1");
-  if (B > 65535 || D > 65535 * 32 || L > (1LL << 26) || B * D * (int64_t)(fft_next_pow2(L) + 2) > (1LL << 40))
+  if (B > 65535 || D > 65535 * 32 || L > (1LL << 26) || B * D * (int64_t)(fft_next_pow2(L) + 2) > (1LL << 40) ||
+      D * (int64_t)((fft_next_pow2(L) + 2 + 8191) / 8192) > (1LL << 31) - 1)
     return fail(RES_ERR_UNSUPPORTED, "FFT reference needs B <= 65535, L <= 2^26 and a padded buffer under 2^40");
   return RES_OK;
 }

@@ -4,7 +4,8 @@
 // (n >= 2L - 1, so the circular product has no wrap-around), in float32, with
 // rocFFT.  Not part of the mixing path: a baseline for the chunked scan.
 //
-// Steps: the taps K_d[tau], tau < L, from float64 into a padded [D][n+2] buffer;
+// Steps: the taps K_d[tau], tau < L, in float64 (rounded to float32) into a
+// padded [D][n+2] buffer;
 // x [B][L][D] transposed into a padded time-major [B*D][n+2] buffer (LDS tiles);
 // batched in-place real FFTs of both; the spectra multiplied (with the 1/n of
 // the inverse); the inverse real FFT; the first L steps transposed back.
@@ -93,20 +94,47 @@ size_t fft_next_pow2(int64_t L) {
   return n;
 }
 
+// Taps K_d[tau] = Re sum_m c_m lambda_m^tau into [D][rows] (zero for tau >= L).
+// A wave covers 64 FT_KS consecutive taps of one channel; lane l holds taps
+// tau0 + l + 64 k, k < FT_KS (coalesced stores).  Per mode it evaluates
+// c lambda^tau0 directly in float64 and steps by lambda^64 (at most FT_KS
+// products, so about FT_KS 2^-53 relative error before the float32 rounding).
+constexpr int FT_KS = 32;
+constexpr int FT_SPAN = 4 * 64 * FT_KS;  // taps per 256-thread block
+
 __global__ __launch_bounds__(256) void fft_taps_kernel(const float* __restrict__ gamma, const float* __restrict__ omega,
                                                        const float* __restrict__ amp, const float* __restrict__ phase,
-                                                       int64_t L, int D, int M, int64_t rows, float* __restrict__ Kp) {
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < (int64_t)D * rows;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int d = (int)(i / rows);
-    const int64_t tau = i % rows;
-    double k = 0.0;
-    if (tau < L)
-      for (int m = 0; m < M; ++m) {
-        const double g = gamma[d * M + m], w = omega[d * M + m], a = amp[d * M + m], p = phase[d * M + m];
-        k += a * exp(-g * (double)tau) * cos(w * (double)tau + p);
+                                                       int64_t L, int M, int64_t rows, int64_t nb,
+                                                       float* __restrict__ Kp) {
+  const int64_t d = blockIdx.x / nb, j = blockIdx.x % nb;
+  const int lane = threadIdx.x % 64;
+  const int64_t wave0 = j * FT_SPAN + (int64_t)(threadIdx.x / 64) * (64 * FT_KS);
+  const int64_t t0 = wave0 + lane;
+  double acc[FT_KS];
+#pragma unroll
+  for (int k = 0; k < FT_KS; ++k) acc[k] = 0.0;
+  if (wave0 < L)
+    for (int m = 0; m < M; ++m) {
+      const double g = gamma[d * M + m], w = omega[d * M + m], a = amp[d * M + m], p = phase[d * M + m];
+      double sn, cs, s1, c1;
+      sincos(w * (double)t0 + p, &sn, &cs);
+      const double e = a * exp(-g * (double)t0);
+      double zr = e * cs, zi = e * sn;
+      sincos(w * 64.0, &s1, &c1);
+      const double e1 = exp(-g * 64.0), sr = e1 * c1, si = e1 * s1;
+#pragma unroll
+      for (int k = 0; k < FT_KS; ++k) {
+        acc[k] += zr;
+        const double nr = zr * sr - zi * si;
+        zi = zr * si + zi * sr;
+        zr = nr;
       }
-    Kp[i] = (float)k;
+    }
+  float* out = Kp + d * rows;
+#pragma unroll
+  for (int k = 0; k < FT_KS; ++k) {
+    const int64_t t = t0 + 64 * k;
+    if (t < rows) out[t] = t < L ? (float)acc[k] : 0.f;
   }
 }
 
@@ -188,10 +216,9 @@ const char* launch_fft_reference(const float* x, float* y, int64_t B, int64_t L,
   work = reinterpret_cast<char*>(((uintptr_t)work + 255) & ~(uintptr_t)255);
   const size_t wb = px->work > pk->work ? px->work : pk->work;
   {
-    const int64_t nk = D * rows;
-    const unsigned g = (unsigned)((nk + 255) / 256 < 8192 ? (nk + 255) / 256 : 8192);
-    hipLaunchKernelGGL(fft_taps_kernel, dim3(g), dim3(256), 0, st, gamma, omega, amp, phase, L, (int)D, (int)M, rows,
-                       Kp);
+    const int64_t nb = (rows + FT_SPAN - 1) / FT_SPAN;
+    hipLaunchKernelGGL(fft_taps_kernel, dim3((unsigned)(D * nb)), dim3(256), 0, st, gamma, omega, amp, phase, L,
+                       (int)M, rows, nb, Kp);
   }
   hipLaunchKernelGGL(fft_pack_kernel, dim3((unsigned)((rows + 31) / 32), (unsigned)((D + 31) / 32), (unsigned)B),
                      dim3(256), 0, st, x, Xp, L, (int)D, rows);

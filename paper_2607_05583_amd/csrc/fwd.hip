@@ -24,14 +24,18 @@ namespace res {
 
 // ---------------------------------------------------------------------------
 // Parameter tables.  One block per (padded) channel.  Every power lambda^n used
-// (n = 0..16, 128, 256, last_len) is evaluated directly as
-// exp(-gamma n) (cos(omega n), sin(omega n)) in float64 from the exact
-// products gamma n and omega n (float32 times a small integer), and c =
-// a (cos phi, sin phi); all are independent, so the block does them in
-// parallel.  Entries are rounded once to the operand type.
+// (n = 0..16, 128, 256, last_len, 16 j for j < 16 and seg_steps n for n <= 16)
+// is evaluated directly as exp(-gamma n) (cos(omega n), sin(omega n)) in
+// float64 from the products gamma n and omega n (float32 times an integer:
+// exact below 2^29), and c = a (cos phi, sin phi); all are independent, so
+// the block does them in one parallel round (the time of this kernel is its
+// longest dependent chain, not its work).  Entries are rounded once to the
+// operand type.
 // ---------------------------------------------------------------------------
+constexpr int PREP_THREADS = 512;
+
 template <typename TA, bool BWD>
-__global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gamma,
+__global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restrict__ gamma,
                                                    const float* __restrict__ omega,
                                                    const float* __restrict__ amp,
                                                    const float* __restrict__ phase, int D, int M,
@@ -55,7 +59,29 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
          i += (int64_t)gridDim.x * blockDim.x)
       flags[i] = i < SEG_HEADER_WORDS ? 0u : PAY_EMPTY_WORD;
   const bool dvalid = d < D;
-  for (int t = threadIdx.x; t < Mp * (NPW + 1); t += blockDim.x) {
+  // one round: the table powers and c, then lambda^(16 j) as [d][j][Mp] and
+  // lambda^(seg_steps n) as [d][n][Mp], both straight to global memory
+  const int n_pw = Mp * (NPW + 1), n_mp = mpow ? Mp * CHUNK : 0, n_sp = spow ? Mp * (CHUNK + 1) : 0;
+  for (int t = threadIdx.x; t < n_pw + n_mp + n_sp; t += blockDim.x) {
+    if (t >= n_pw) {
+      const int u = t - n_pw;
+      const bool is_mp = u < n_mp;
+      const int v = is_mp ? u : u - n_mp;
+      const int m = v % Mp, j = v / Mp;
+      const double n = is_mp ? (double)(CHUNK * j) : (double)seg_steps * (double)j;
+      double2 z = make_double2(0.0, 0.0);
+      if (dvalid && m < M) {
+        double sn, cs;
+        sincos((double)omega[d * M + m] * n, &sn, &cs);
+        const double e = exp(-(double)gamma[d * M + m] * n);
+        z = make_double2(e * cs, e * sn);
+      }
+      if (is_mp)
+        mpow[((size_t)d * CHUNK + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
+      else
+        spow[((size_t)d * (CHUNK + 1) + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
+      continue;
+    }
     const int m = t / (NPW + 1), k = t % (NPW + 1);
     const bool valid = dvalid && m < M;
     if (k < NPW) {
@@ -98,37 +124,6 @@ __global__ __launch_bounds__(256) void prep_kernel(const float* __restrict__ gam
     mc.lamEll = pw[m][CHUNK + 3];
     mc.mu8 = lH;
     cc[(size_t)d * Mp + m] = mc;
-  }
-  // lambda^(16 j), j = 0..15, as [d][j][Mp], and lambda^(seg_steps n), n =
-  // 0..16, as [d][n][Mp]: float64 powers of mu = lambda^16 and of
-  // lambda^seg_steps (the latter evaluated directly), by repeated products
-  // (at most 16 roundings of 2^-53 each)
-  for (int t = threadIdx.x; t < 2 * Mp; t += blockDim.x) {
-    const int m = t % Mp;
-    const bool valid = dvalid && m < M;
-    if (t < Mp) {
-      if (mpow == nullptr) continue;
-      const double2 mu = pw[m][CHUNK];
-      double2 z = make_double2(valid ? 1.0 : 0.0, 0.0);
-      for (int j = 0; j < CHUNK; ++j) {
-        mpow[((size_t)d * CHUNK + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
-        z = zmul(z, mu);
-      }
-    } else {
-      if (spow == nullptr) continue;
-      double2 ls = make_double2(0.0, 0.0);
-      if (valid) {
-        double sn, cs;
-        sincos((double)omega[d * M + m] * (double)seg_steps, &sn, &cs);
-        const double e = exp(-(double)gamma[d * M + m] * (double)seg_steps);
-        ls = make_double2(e * cs, e * sn);
-      }
-      double2 z = make_double2(valid ? 1.0 : 0.0, 0.0);
-      for (int n = 0; n <= CHUNK; ++n) {
-        spow[((size_t)d * (CHUNK + 1) + n) * Mp + m] = make_float2((float)z.x, (float)z.y);
-        z = zmul(z, ls);
-      }
-    }
   }
   for (int tau = threadIdx.x; tau <= CHUNK; tau += blockDim.x) {  // K[tau] = Re sum_m c lambda^tau
     double s = 0.0;
@@ -1424,11 +1419,11 @@ hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
                        hipStream_t st, float2* mpow, float2* spow, uint32_t* flags, int64_t nflags) {
   if (bwd)
-    hipLaunchKernelGGL((prep_kernel<TA, true>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
+    hipLaunchKernelGGL((prep_kernel<TA, true>), dim3(g.Dp), dim3(PREP_THREADS), 0, st, gamma, omega, amp,
                        phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
                        spow, flags, nflags);
   else
-    hipLaunchKernelGGL((prep_kernel<TA, false>), dim3(g.Dp), dim3(256), 0, st, gamma, omega, amp,
+    hipLaunchKernelGGL((prep_kernel<TA, false>), dim3(g.Dp), dim3(PREP_THREADS), 0, st, gamma, omega, amp,
                        phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
                        spow, flags, nflags);
   return hipGetLastError();
