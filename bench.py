@@ -247,20 +247,13 @@ def main():
     torch.cuda.synchronize()
     dec_eager_us = d0.elapsed_time(d1) * 1e3 / nsteps
     # graph replay of the same calls (kernel launches only; no allocation, no memset)
-    G = 512
-    g = torch.cuda.CUDAGraph()
-    cap = torch.cuda.Stream(dev)
-    cap.wait_stream(stream)
-    with torch.cuda.stream(cap):
-        with torch.cuda.graph(g, stream=cap):
-            csp = ctypes.c_void_p(cap.cuda_stream)
-            for j in range(G):
-                _lib.check(lib.resonator_decode_step(xptr[j], _lib.RES_BF16, yptr[j], _lib.RES_BF16,
-                                                     Bd, Dd, Md, *DP, sptr, csp))
-    stream.wait_stream(cap)
+    G = min(512, int(xdec.shape[0]))
+    dgraph = ops.DecodeGraph(*dprm, state, G, x_dtype=torch.bfloat16)
+    dgraph.x.copy_(xdec[:G])
     torch.cuda.synchronize()
-    g.replay()
+    dgraph.replay()
     torch.cuda.synchronize()
+    g = dgraph.graph
     reps = max(1, nsteps // G)
     d0.record(stream)
     for _ in range(reps):

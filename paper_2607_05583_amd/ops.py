@@ -175,6 +175,52 @@ def resonator_decode_steps(x, gamma, omega, amp, phase, state, out_dtype=None, o
     return y
 
 
+class DecodeGraph:
+    """K decode steps (Sec. 3.3) captured once as a HIP graph and replayed: one
+    token's step is a single short launch, so a replay issues the K launches of a
+    block of tokens without K host round trips.
+
+    Static buffers: ``x`` [K, B, D] holds the drives of the next K tokens (copy
+    them in, or pass them to ``replay``), ``y`` [K, B, D] receives the outputs;
+    ``state`` [B, D, M, 2] is updated in place by every replay.  The parameters
+    and the state are captured by address: update them in place, never rebind
+    them.  The capture records the decode kernels only (no allocation, no memset),
+    and nothing runs until the first replay."""
+
+    def __init__(self, gamma, omega, amp, phase, state, steps: int, x_dtype=torch.bfloat16, out_dtype=None):
+        _dev(state, "state")
+        gamma, omega, amp, phase = _params(gamma, omega, amp, phase)
+        D, M = gamma.shape
+        if state.dtype != torch.float32 or state.dim() != 4 or tuple(state.shape[1:]) != (D, M, 2):
+            raise ValueError("state must be float32 [B, D, M, 2]")
+        if steps < 1:
+            raise ValueError("steps must be >= 1")
+        B = state.shape[0]
+        dev = state.device
+        out_dtype = x_dtype if out_dtype is None else out_dtype
+        self.params = (gamma, omega, amp, phase)
+        self.state = state
+        self.x = torch.zeros((steps, B, D), dtype=x_dtype, device=dev)
+        self.y = torch.empty((steps, B, D), dtype=out_dtype, device=dev)
+        _lib.lib()  # loaded before the capture
+        self.graph = torch.cuda.CUDAGraph()
+        cur = torch.cuda.current_stream(dev)
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(cur)
+        with torch.cuda.stream(cap), torch.cuda.graph(self.graph, stream=cap):
+            for k in range(steps):
+                resonator_decode_step(self.x[k], *self.params, state, out=self.y[k])
+        cur.wait_stream(cap)
+
+    def replay(self, x=None):
+        """Run the K steps on the current stream (after copying ``x`` [K, B, D] into
+        the drive buffer when given); returns the output buffer ``y``."""
+        if x is not None:
+            self.x.copy_(x)
+        self.graph.replay()
+        return self.y
+
+
 def resonator_quadratic_reference(x, gamma, omega, amp, phase):
     """The O(L^2) direct causal mixer (kernel-tail baseline), float32 [B, L, D]."""
     _dev(x, "x")

@@ -156,6 +156,31 @@ def test_decode_steps(B, D, M, L0, steps, seed, act, out):
     assert rel_err(host(st2), hr) <= (1e-4 if act == "f32" else 2e-2)
 
 
+@pytest.mark.parametrize("B,D,M,K,act", [(3, 70, 5, 16, "bf16"), (64, 256, 8, 64, "bf16"), (2, 33, 16, 7, "f32")])
+def test_decode_graph_replays_match_eager_steps(B, D, M, K, act):
+    """A captured K-step decode loop, replayed three times with new drives (eager
+    work and synchronisations between the replays), gives bitwise the outputs and
+    state of K eager decode steps every time."""
+    say(f"decode graph B={B} D={D} M={M} K={K} {act}")
+    prob = W.random_problem(92 + K, B, 20 + 3 * K, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], act)
+    pr = params_dev(prob)
+    st_g = ops.resonator_state_init(x[:, :20].contiguous(), *pr)
+    st_e = st_g.clone()
+    g = ops.DecodeGraph(*pr, st_g, K, x_dtype=x.dtype)
+    torch.cuda.synchronize()
+    assert torch.equal(st_g, st_e)  # capture runs nothing
+    for r in range(3):
+        drives = x[:, 20 + r * K:20 + (r + 1) * K].transpose(0, 1).contiguous()  # [K, B, D]
+        ye = torch.stack([ops.resonator_decode_step(drives[k], *pr, st_e) for k in range(K)])
+        torch.cuda.synchronize()
+        yg = g.replay(drives)
+        torch.cuda.synchronize()
+        assert torch.equal(yg, ye), r
+        assert torch.equal(st_g, st_e), r
+        _ = (x.float() * 2).sum().item()  # unrelated eager work between the replays
+
+
 def test_config4_decode_full():
     """Decode config: prompt 1024 -> state_init, then 32768 decode steps at B64 D256 M8 (bf16).
 
