@@ -377,6 +377,18 @@ def main():
         t1e.record(stream)
         torch.cuda.synchronize()
         b_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        # the same forward replayed from a captured graph (no host issue time)
+        bgraph = ops.BlockForwardGraph(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6], 8,
+                                       dense=dense)
+        bgraph.replay()
+        torch.cuda.synchronize()
+        t0e.record(stream)
+        for _ in range(reps):
+            bgraph.replay()
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        bg_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        del bgraph
         # backward (recomputes the forward's intermediates, then the chain rule)
         dob = torch.randn_like(bt["x"], dtype=torch.float32).to(torch.bfloat16)
 
@@ -392,9 +404,10 @@ def main():
         t1e.record(stream)
         torch.cuda.synchronize()
         bb_us = t0e.elapsed_time(t1e) * 1e3 / reps
-        blk.append({"L": Lb, "fwd_us": b_us, "bwd_us": bb_us, "fwd_tokens_per_s": 4 * Lb / (b_us * 1e-6)})
+        blk.append({"L": Lb, "fwd_us": b_us, "fwd_graph_us": bg_us, "bwd_us": bb_us,
+                    "fwd_tokens_per_s": 4 * Lb / (b_us * 1e-6), "fwd_graph_tokens_per_s": 4 * Lb / (bg_us * 1e-6)})
         log(f"mixer block B4 L={Lb} d256: forward {b_us:.1f} us ({4 * Lb / (b_us * 1e-6) / 1e6:.1f} M tokens/s), "
-            f"backward {bb_us:.1f} us")
+            f"graph replay {bg_us:.1f} us, backward {bb_us:.1f} us")
         del bt, dob
 
     # ---------------- kernel tail: mixing vs a quadratic causal reference ----------------

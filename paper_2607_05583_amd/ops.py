@@ -328,6 +328,44 @@ def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     return resonator_grouped_linear(z, Po)
 
 
+class BlockForwardGraph:
+    """The mixer block forward (``resonator_block_fwd``) for one fixed shape,
+    captured once as a HIP graph and replayed: at short lengths the block's
+    launches cost more host time than device time.
+
+    ``x`` is a static input buffer (copy new inputs in, or pass them to
+    ``replay``); the output and the intermediates live in the graph's memory
+    pool and are overwritten by every replay.  Weights and mode parameters are
+    captured by address (update them in place, never rebind them); ``lambda_c``
+    and ``H`` are fixed at capture.  One eager call before the capture loads the
+    library and sizes the GEMM library's workspace, so the capture records
+    kernel launches only."""
+
+    def __init__(self, x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, dense=None):
+        _dev(x, "x")
+        self.x = x.clone()
+        self._args = (Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H)
+        self._dense = dense
+        dev = x.device
+        cur = torch.cuda.current_stream(dev)
+        resonator_block_fwd(self.x, *self._args, dense=dense)
+        torch.cuda.synchronize(dev)
+        self.graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(cur)
+        with torch.cuda.stream(cap), torch.cuda.graph(self.graph, stream=cap):
+            self.out = resonator_block_fwd(self.x, *self._args, dense=dense)
+        cur.wait_stream(cap)
+
+    def replay(self, x=None):
+        """Run the block on the current stream (after copying ``x`` into the input
+        buffer when given); returns the output buffer."""
+        if x is not None:
+            self.x.copy_(x)
+        self.graph.replay()
+        return self.out
+
+
 def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, do, dense=None):
     """Gradients of sum(do * resonator_block_fwd(...)): the forward's intermediates
     are recomputed, then the chain rule runs backwards through the output

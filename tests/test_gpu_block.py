@@ -130,3 +130,27 @@ def test_block_bwd_parity(B, L, d, H, K, G, M, act):
         say("  errs " + " ".join(f"{k}={e:.2e}" for k, e in errs.items()))
         for k, e in errs.items():
             assert e <= (b_act if k == "dx" else b_par), k
+
+
+@pytest.mark.parametrize("B,L,d,H,K,G,M,act,use_dense", [(2, 300, 64, 4, 3, 4, 4, "f32", False),
+                                                         (4, 2048, 256, 8, 4, 8, 8, "bf16", True)])
+def test_block_forward_graph_replays_match_eager(B, L, d, H, K, G, M, act, use_dense):
+    """The captured block forward, replayed three times with new inputs (eager work
+    and synchronisations between the replays), equals the eager block bitwise."""
+    say(f"block forward graph B={B} L={L} d={d} {act} dense={use_dense}")
+    p = W.block_inputs(7 + L, B, L, d, H, K, G, M, act)
+    dev = lambda a: dev_act(a, act)
+    ws = [dev(p[k]) for k in ("Wu", "Wg", "Wo")]
+    prm = [dev_f32(p[k]) for k in ("gamma", "omega", "amp", "phase")]
+    args = (*ws, *prm, dev_f32(p["Ct"]), p["lambda_c"], dev_f32(p["w"]), dev_f32(p["s"]), H)
+    dense = tuple(ops.resonator_block_diag_weight(t) for t in ws) if use_dense else None
+    x0 = dev(p["x"])
+    bg = ops.BlockForwardGraph(x0, *args, dense=dense)
+    for r in range(3):
+        xr = (x0.float() * (1.0 + 0.25 * r)).flip(1).contiguous().to(x0.dtype)
+        ref = ops.resonator_block_fwd(xr, *args, dense=dense)
+        torch.cuda.synchronize()
+        out = bg.replay(xr)
+        torch.cuda.synchronize()
+        assert torch.equal(out, ref), r
+        _ = (xr.float() * 3).sum().item()  # unrelated eager work between the replays
