@@ -109,3 +109,65 @@ def test_product_path_has_no_fallback(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         L.lib()
+
+
+F3 = ctypes.c_void_p(0x7F0200000000)
+F4 = ctypes.c_void_p(0x7F0300000000)
+ODD = ctypes.c_void_p(0x7F0400000002)   # not 4-byte aligned
+
+
+def test_decode_steps_and_projection_validation_codes():
+    lib = L.lib()
+    ds = lib.resonator_decode_steps
+    assert ds(None, L.RES_BF16, FAKE2, L.RES_BF16, 2, 3, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, None) == \
+        L.RES_ERR_INVALID_ARG
+    assert ds(FAKE, L.RES_F32, FAKE2, L.RES_BF16, 2, 3, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, None) == \
+        L.RES_ERR_UNSUPPORTED
+    assert ds(FAKE, L.RES_BF16, FAKE, L.RES_BF16, 2, 3, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, None) == \
+        L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    gl = lib.resonator_grouped_linear
+    assert gl(FAKE, FAKE2, L.RES_F32, F3, 5, 8, 8, 3, None) == L.RES_ERR_INVALID_ARG and "multiples" in _err()
+    assert gl(FAKE, FAKE2, L.RES_F32, F3, 0, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG
+    assert gl(FAKE, FAKE2, 7, F3, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG
+    assert gl(FAKE, FAKE2, L.RES_F32, FAKE, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert gl(ODD, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, None) == L.RES_ERR_MISALIGNED
+    assert lib.resonator_grouped_linear_bwd_data(None, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_INVALID_ARG
+    assert lib.resonator_grouped_linear_bwd_weight(FAKE, FAKE2, L.RES_BF16, FAKE, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    bd = lib.resonator_block_diag_weight
+    assert bd(FAKE, L.RES_F32, 8, 8, 0, FAKE2, None) == L.RES_ERR_INVALID_ARG
+    assert bd(FAKE, L.RES_F32, 8, 8, 2, FAKE, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+
+
+def test_reference_params_and_epilogue_validation_codes():
+    lib = L.lib()
+    assert lib.resonator_quadratic_reference_workspace_bytes(0, 4) == 0
+    qr = lib.resonator_quadratic_reference
+    assert qr(None, FAKE2, 1, 16, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, 1 << 20, None) == L.RES_ERR_INVALID_ARG
+    assert qr(FAKE, FAKE2, 1, 16, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, 8, None) == L.RES_ERR_WORKSPACE
+    # the FFT reference rejects sizes before it makes any plan (no HIP call)
+    assert lib.resonator_fft_reference_workspace_bytes(0, 16, 4) == 0
+    assert lib.resonator_fft_reference_workspace_bytes(1, (1 << 26) + 1, 4) == 0
+    fr = lib.resonator_fft_reference
+    assert fr(None, FAKE2, 1, 16, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, 1 << 20, None) == L.RES_ERR_INVALID_ARG
+    assert fr(FAKE, FAKE2, 70000, 16, 4, 2, FAKE, FAKE, FAKE, FAKE, F3, 1 << 20, None) == L.RES_ERR_UNSUPPORTED
+    pm = lib.resonator_params_map
+    assert pm(FAKE, FAKE2, 0, 1e-4, F3, F4, None) == L.RES_ERR_INVALID_ARG
+    assert pm(FAKE, FAKE2, 8, float("nan"), F3, F4, None) == L.RES_ERR_INVALID_ARG
+    assert pm(FAKE, FAKE2, 8, 1e-4, F3, F3, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert pm(FAKE, FAKE2, 8, 1e-4, ODD, F4, None) == L.RES_ERR_MISALIGNED
+    pi = lib.resonator_params_init
+    assert pi(0, 2, 2.0, 2048.0, 4.0, 2048.0, 1e-4, FAKE, FAKE2, None) == L.RES_ERR_INVALID_ARG
+    assert pi(4, 2, 100.0, 2.0, 4.0, 2048.0, 1e-4, FAKE, FAKE2, None) == L.RES_ERR_INVALID_ARG
+    assert pi(4, 2, 2.0, 2048.0, 1.0, 2048.0, 1e-4, FAKE, FAKE2, None) == L.RES_ERR_INVALID_ARG
+    # ln 2 / 1e5 is below alpha_min = 1e-4: the longest half-life cannot be reached
+    assert pi(4, 2, 2.0, 1e5, 4.0, 2048.0, 1e-4, FAKE, FAKE2, None) == L.RES_ERR_INVALID_ARG and "half-life" in _err()
+    ef = lib.resonator_epilogue_fwd
+    assert ef(FAKE, FAKE2, F3, L.RES_BF16, F4, 1, 16, 0, 8, 2, FAKE, 0.5, FAKE, FAKE, None) == L.RES_ERR_INVALID_ARG
+    assert ef(FAKE, FAKE2, None, L.RES_BF16, F4, 1, 16, 2, 8, 2, FAKE, 0.5, FAKE, FAKE, None) == \
+        L.RES_ERR_INVALID_ARG
+    assert ef(FAKE, FAKE2, F3, L.RES_BF16, FAKE, 1, 16, 2, 8, 2, FAKE, 0.5, FAKE, FAKE, None) == \
+        L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert ef(FAKE, FAKE2, F3, L.RES_BF16, F4, 1, 16, 2, 8, 1000, FAKE, 0.5, FAKE, FAKE, None) == \
+        L.RES_ERR_UNSUPPORTED
