@@ -219,6 +219,7 @@ const char* launch_fft_reference(const float* x, float* y, int64_t B, int64_t L,
     const int64_t nb = (rows + FT_SPAN - 1) / FT_SPAN;
     hipLaunchKernelGGL(fft_taps_kernel, dim3((unsigned)(D * nb)), dim3(256), 0, st, gamma, omega, amp, phase, L,
                        (int)M, rows, nb, Kp);
+    if (hipGetLastError() != hipSuccess) return "taps launch";
   }
   hipLaunchKernelGGL(fft_pack_kernel, dim3((unsigned)((rows + 31) / 32), (unsigned)((D + 31) / 32), (unsigned)B),
                      dim3(256), 0, st, x, Xp, L, (int)D, rows);
@@ -231,6 +232,7 @@ const char* launch_fft_reference(const float* x, float* y, int64_t B, int64_t L,
     hipLaunchKernelGGL(fft_mul_kernel, dim3(g), dim3(256), 0, st, reinterpret_cast<float2*>(Xp),
                        reinterpret_cast<const float2*>(Kp), B * D, (int)D, bins, 1.f / (float)n);
   }
+  if (hipGetLastError() != hipSuccess) return "spectrum product launch";
   if (const char* e = run_plan(px->inv, Xp, work, wb, st)) return e;
   hipLaunchKernelGGL(fft_unpack_kernel, dim3((unsigned)((L + 31) / 32), (unsigned)((D + 31) / 32), (unsigned)B),
                      dim3(256), 0, st, Xp, y, L, (int)D, rows);
