@@ -187,6 +187,37 @@ int resonator_block_diag_weight(const void* W, res_dtype_t dt, int64_t d_in, int
                                 void* W_dense, void* stream);
 
 /*
+ * Grouped weight gradient with the contraction split (Sec. 3.1, 3.4
+ * projections): the same result as resonator_grouped_linear_bwd_weight, for a
+ * long contraction (N tokens) over small weights.  The N rows are cut into at
+ * most 64 chunks (at least 256 rows each); one batched GEMM writes each chunk's
+ * dense float32 product x_s^T dy_s [d_in][d_out] into the workspace, and a
+ * second kernel sums the chunks' diagonal blocks in a fixed order into
+ * dW [G][d_in/G][d_out/G] (added when accumulate != 0).  Deterministic.
+ *   ws   resonator_grouped_linear_bwd_weight_split_workspace_bytes(N, d_in,
+ *        d_out) bytes of device memory, 256-byte aligned, not overlapping the
+ *        other arguments (0 from the size query means invalid sizes)
+ * Other arguments, dtypes and errors as resonator_grouped_linear_bwd_weight;
+ * d_in d_out <= 2^31.
+ */
+size_t resonator_grouped_linear_bwd_weight_split_workspace_bytes(int64_t N, int64_t d_in, int64_t d_out);
+int resonator_grouped_linear_bwd_weight_split(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,
+                                              int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* ws,
+                                              size_t ws_bytes, void* stream);
+
+/*
+ * The diagonal blocks of a dense float32 [d_in][d_out] matrix into a grouped
+ * W [G][d_in/G][d_out/G] (W[g] = W_dense[g-th row block][g-th column block]),
+ * added into W when accumulate != 0.  With the dense weight gradient from
+ * resonator_grouped_linear_bwd_weight with G = 1, this gives the grouped weight
+ * gradients (Sec. 3.1, 3.4 projections) from one efficient GEMM.  Device
+ * memory, caller-owned, 4-byte aligned; W must not overlap W_dense;
+ * d_in d_out <= 2^31.
+ */
+int resonator_block_diag_extract(const float* W_dense, int64_t d_in, int64_t d_out, int64_t G, float* W,
+                                 int accumulate, void* stream);
+
+/*
  * Quadratic causal reference mixer: the baseline of the kernel-tail benchmark
  * (Sec. 5.3, Table 5), not part of the mixing path.  Computes
  *   y[b,t,d] = sum_{s<=t} K_d[t-s] x[b,s,d],  K_d[tau] = sum_m a exp(-gamma tau) cos(omega tau + phi)

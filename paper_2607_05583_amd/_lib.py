@@ -24,8 +24,9 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
            "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
-           "resonator_grouped_linear", "resonator_block_diag_weight",
-           "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_weight")
+           "resonator_grouped_linear", "resonator_block_diag_weight", "resonator_block_diag_extract",
+           "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_weight",
+           "resonator_grouped_linear_bwd_weight_split", "resonator_grouped_linear_bwd_weight_split_workspace_bytes")
 
 _lib = None
 
@@ -83,10 +84,16 @@ def _declare(lib):
     lib.resonator_grouped_linear.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, vp]
     lib.resonator_block_diag_weight.restype = i32
     lib.resonator_block_diag_weight.argtypes = [vp, i32, i64, i64, i64, vp, vp]
+    lib.resonator_block_diag_extract.restype = i32
+    lib.resonator_block_diag_extract.argtypes = [fp, i64, i64, i64, fp, i32, vp]
     lib.resonator_grouped_linear_bwd_data.restype = i32
     lib.resonator_grouped_linear_bwd_data.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, i32, vp]
     lib.resonator_grouped_linear_bwd_weight.restype = i32
     lib.resonator_grouped_linear_bwd_weight.argtypes = [vp, vp, i32, fp, i64, i64, i64, i64, i32, vp]
+    lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes.restype = sz
+    lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes.argtypes = [i64, i64, i64]
+    lib.resonator_grouped_linear_bwd_weight_split.restype = i32
+    lib.resonator_grouped_linear_bwd_weight_split.argtypes = [vp, vp, i32, fp, i64, i64, i64, i64, i32, vp, sz, vp]
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

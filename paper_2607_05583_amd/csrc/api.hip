@@ -533,6 +533,48 @@ int resonator_block_diag_weight(const void* W, res_dtype_t dt, int64_t d_in, int
   return e == hipSuccess ? RES_OK : hip_fail(e, "block-diagonal weight launch");
 }
 
+size_t resonator_grouped_linear_bwd_weight_split_workspace_bytes(int64_t N, int64_t d_in, int64_t d_out) {
+  if (N < 1 || d_in < 1 || d_out < 1 || N >= (1LL << 31) || d_in * d_out > (1LL << 31)) return 0;
+  return (size_t)(splitk_parts(N) * d_in * d_out) * sizeof(float);
+}
+
+int resonator_grouped_linear_bwd_weight_split(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,
+                                              int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* ws,
+                                              size_t ws_bytes, void* stream) {
+  int rc = gl_check(N, d_in, d_out, G, dt);
+  if (rc) return rc;
+  if (d_in * d_out > (1LL << 31)) return fail(RES_ERR_UNSUPPORTED, "d_in d_out must be <= 2^31");
+  if (!x || !dy || !dW) return fail(RES_ERR_INVALID_ARG, "x, dy and dW must be non-null");
+  const size_t es = dt == RES_BF16 ? 2 : 4;
+  if (!aligned(x, es) || !aligned(dy, es) || !aligned(dW, 4))
+    return fail(RES_ERR_MISALIGNED, "x and dy aligned to their element, dW to 4 bytes");
+  const size_t need = resonator_grouped_linear_bwd_weight_split_workspace_bytes(N, d_in, d_out);
+  if (!ws || ws_bytes < need)
+    return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * 4;
+  if (overlap(dW, nw, x, nx) || overlap(dW, nw, dy, ny) || overlap(ws, need, x, nx) || overlap(ws, need, dy, ny) ||
+      overlap(ws, need, dW, nw))
+    return fail(RES_ERR_INVALID_ARG, "dW and the workspace must not overlap x, dy or each other");
+  const char* err = launch_grouped_linear_bwd_weight_splitk(x, dy, dW, N, d_in, d_out, G, dt == RES_BF16,
+                                                            accumulate != 0, (float*)ws, (hipStream_t)stream);
+  if (err) return fail(RES_ERR_HIP, "grouped linear backward (weight, split): %s", err);
+  return RES_OK;
+}
+
+int resonator_block_diag_extract(const float* W_dense, int64_t d_in, int64_t d_out, int64_t G, float* W,
+                                 int accumulate, void* stream) {
+  if (G < 1 || d_in < 1 || d_out < 1 || d_in % G || d_out % G)
+    return fail(RES_ERR_INVALID_ARG, "need d_in, d_out >= 1 and multiples of G >= 1");
+  if (d_in * d_out > (1LL << 31)) return fail(RES_ERR_UNSUPPORTED, "d_in d_out must be <= 2^31");
+  if (!W || !W_dense) return fail(RES_ERR_INVALID_ARG, "W and W_dense must be non-null");
+  if (!aligned(W, 4) || !aligned(W_dense, 4)) return fail(RES_ERR_MISALIGNED, "W and W_dense must be 4-byte aligned");
+  if (overlap(W, (size_t)(d_in * (d_out / G)) * 4, W_dense, (size_t)(d_in * d_out) * 4))
+    return fail(RES_ERR_INVALID_ARG, "W must not overlap W_dense");
+  const hipError_t e = launch_block_extract(W_dense, W, d_in, d_out, G, accumulate != 0, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "block-diagonal extract launch");
+}
+
 // ---------------------------------------------------------------------------
 // Quadratic causal reference (kernel-tail baseline, Sec. 5.3)
 // ---------------------------------------------------------------------------

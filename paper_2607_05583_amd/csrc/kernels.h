@@ -114,6 +114,15 @@ const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, floa
                                              int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
 hipError_t launch_block_diag(const void* W, void* Wd, int64_t d_in, int64_t d_out, int64_t G, bool bf16,
                              hipStream_t st);
+constexpr int64_t SPLITK_TARGET = 64;     // partial products of the split-K weight gradient
+constexpr int64_t SPLITK_MIN_ROWS = 256;  // rows per partial at least
+int64_t splitk_rows(int64_t N);
+int64_t splitk_parts(int64_t N);
+const char* launch_grouped_linear_bwd_weight_splitk(const void* x, const void* dy, float* dW, int64_t N,
+                                                    int64_t d_in, int64_t d_out, int64_t G, bool bf16,
+                                                    bool accumulate, float* P, hipStream_t st);
+hipError_t launch_block_extract(const float* Wd, float* W, int64_t d_in, int64_t d_out, int64_t G, bool accumulate,
+                                hipStream_t st);
 size_t quad_workspace_bytes(int64_t L, int64_t D);
 size_t fft_next_pow2(int64_t L);
 const char* fft_workspace_bytes(int64_t B, int64_t L, int64_t D, size_t* bytes);

@@ -304,6 +304,23 @@ def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
     return dx, dW
 
 
+def resonator_grouped_linear_bwd_weight_split(x, dy, dW, accumulate=False):
+    """Grouped weight gradient dW [G, d_in/G, d_out/G] (float32) of a long
+    contraction, split into chunks (dense partial products, then their diagonal
+    blocks summed in a fixed order); the same result as the unsplit form."""
+    _dev(x, "x")
+    _dev(dy, "dy")
+    _dev(dW, "dW")
+    d_in, d_out = x.shape[-1], dy.shape[-1]
+    N = x.numel() // d_in
+    n = _lib.lib().resonator_grouped_linear_bwd_weight_split_workspace_bytes(N, d_in, d_out)
+    ws = torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
+    check(_lib.lib().resonator_grouped_linear_bwd_weight_split(_ptr(x), _ptr(dy), _code(x), _ptr(dW), N, d_in, d_out,
+                                                               dW.shape[0], int(accumulate), _ptr(ws), n,
+                                                               _stream(x.device)))
+    return dW
+
+
 def resonator_block_diag_weight(W):
     """Dense [1, d_in, d_out] block-diagonal copy of a grouped weight [G, d_in/G, d_out/G]."""
     _dev(W, "W")
@@ -311,6 +328,23 @@ def resonator_block_diag_weight(W):
     Wd = torch.empty((1, G * di, G * dq), dtype=W.dtype, device=W.device)
     check(_lib.lib().resonator_block_diag_weight(_ptr(W), _code(W), G * di, G * dq, G, _ptr(Wd), _stream(W.device)))
     return Wd
+
+
+def resonator_block_diag_extract(Wd, G, out=None, accumulate=False):
+    """The G diagonal blocks of a dense float32 [.., d_in, d_out] matrix as
+    [G, d_in/G, d_out/G] (added into ``out`` when ``accumulate``)."""
+    _dev(Wd, "W_dense")
+    if Wd.dtype != torch.float32 or Wd.dim() < 2:
+        raise ValueError("W_dense must be float32 [..., d_in, d_out]")
+    d_in, d_out = Wd.shape[-2], Wd.shape[-1]
+    if Wd.numel() != d_in * d_out:
+        raise ValueError("W_dense must hold one d_in x d_out matrix")
+    W = out if out is not None else torch.empty((G, d_in // G, d_out // G), dtype=torch.float32, device=Wd.device)
+    if out is not None:
+        _dev(out, "out")
+    check(_lib.lib().resonator_block_diag_extract(_ptr(Wd), d_in, d_out, G, _ptr(W), int(accumulate),
+                                                  _stream(Wd.device)))
+    return W
 
 
 def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, dense=None):
@@ -378,16 +412,28 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     g = resonator_grouped_linear(x, Pg)
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
-    G = Wo.shape[0]
+
+    def wgrad(xin, dys, Wt):
+        # grouped weight gradient of the sum over dys; on the dense route with
+        # the contraction split (dense partial products, then diagonal blocks)
+        dW = torch.empty_like(Wt, dtype=torch.float32)
+        for i, d_ in enumerate(dys):
+            if dense is None:
+                resonator_grouped_linear_bwd(xin, None, d_, dW=dW, accumulate=i > 0)
+            else:
+                resonator_grouped_linear_bwd_weight_split(xin, d_, dW, accumulate=i > 0)
+        return dW
+
     dz, _ = resonator_grouped_linear_bwd(None, Po, do)
-    _, dWo = resonator_grouped_linear_bwd(z, None, do, dW=torch.empty_like(Wo, dtype=torch.float32))
+    dWo = wgrad(z, [do], Wo)
     dy, dg, dv, dCt, dlam, dw, ds = resonator_epilogue_bwd(y, g, u, dz, Ct, lambda_c, w, s, H)
     mb = resonator_mix_bwd(u, dy, gamma, omega, amp, phase)
     # du = mb["dx"] + dv enters both the data and the weight gradient of W_u by accumulation
-    dx, dWu = resonator_grouped_linear_bwd(x, Pu, mb["dx"], dW=torch.empty_like(Wu, dtype=torch.float32))
+    dx, _ = resonator_grouped_linear_bwd(None, Pu, mb["dx"])
     if dv is not None:
-        resonator_grouped_linear_bwd(x, Pu, dv, dx=dx, dW=dWu, accumulate=True)
-    _, dWg = resonator_grouped_linear_bwd(x, None, dg, dW=torch.empty_like(Wg, dtype=torch.float32))
+        resonator_grouped_linear_bwd(None, Pu, dv, dx=dx, accumulate=True)
+    dWu = wgrad(x, [mb["dx"]] + ([dv] if dv is not None else []), Wu)
+    dWg = wgrad(x, [dg], Wg)
     resonator_grouped_linear_bwd(None, Pg, dg, dx=dx, accumulate=True)
     return dict(dx=dx, dWu=dWu, dWg=dWg, dWo=dWo, dgamma=mb["dgamma"], domega=mb["domega"], damp=mb["damp"],
                 dphase=mb["dphase"], dCt=dCt, dlambda_c=dlam, dw=dw, ds=ds)

@@ -138,6 +138,15 @@ def test_decode_steps_and_projection_validation_codes():
     bd = lib.resonator_block_diag_weight
     assert bd(FAKE, L.RES_F32, 8, 8, 0, FAKE2, None) == L.RES_ERR_INVALID_ARG
     assert bd(FAKE, L.RES_F32, 8, 8, 2, FAKE, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes(0, 8, 8) == 0
+    assert lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes(131072, 256, 256) == 64 * 256 * 256 * 4
+    ws_ = lib.resonator_grouped_linear_bwd_weight_split
+    assert ws_(FAKE, FAKE2, L.RES_F32, F3, 1000, 8, 8, 2, 0, None, 0, None) == L.RES_ERR_WORKSPACE
+    assert ws_(FAKE, FAKE2, L.RES_F32, FAKE, 1000, 8, 8, 2, 0, F4, 1 << 20, None) == L.RES_ERR_INVALID_ARG
+    be = lib.resonator_block_diag_extract
+    assert be(FAKE, 8, 6, 4, FAKE2, 0, None) == L.RES_ERR_INVALID_ARG
+    assert be(FAKE, 8, 8, 2, FAKE, 0, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert be(ODD, 8, 8, 2, FAKE2, 1, None) == L.RES_ERR_MISALIGNED
 
 
 def test_reference_params_and_epilogue_validation_codes():

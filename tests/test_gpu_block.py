@@ -154,3 +154,45 @@ def test_block_forward_graph_replays_match_eager(B, L, d, H, K, G, M, act, use_d
         torch.cuda.synchronize()
         assert torch.equal(out, ref), r
         _ = (xr.float() * 3).sum().item()  # unrelated eager work between the replays
+
+
+@pytest.mark.parametrize("G,di,dq", [(1, 5, 3), (8, 32, 32), (3, 7, 11)])
+def test_block_diag_extract_inverts_block_diag_and_accumulates(G, di, dq):
+    r = np.random.default_rng(G * 100 + di)
+    Wt = r.normal(size=(G, di, dq)).astype(np.float32)
+    Wd = ops.resonator_block_diag_weight(dev_f32(Wt))
+    back = ops.resonator_block_diag_extract(Wd, G)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(back), Wt)
+    # off-diagonal entries are ignored; accumulate adds
+    full = r.normal(size=(G * di, G * dq)).astype(np.float32)
+    out = dev_f32(Wt.copy())
+    ops.resonator_block_diag_extract(dev_f32(full), G, out=out, accumulate=True)
+    torch.cuda.synchronize()
+    ref = Wt.copy()
+    for g in range(G):
+        ref[g] += full[g * di:(g + 1) * di, g * dq:(g + 1) * dq]
+    np.testing.assert_array_equal(host(out), ref)
+
+
+@pytest.mark.parametrize("N,G,di,dq,act", [(1, 1, 3, 5, "f32"), (1000, 4, 64, 64, "f32"), (131072, 8, 32, 32, "bf16"),
+                                           (70001, 3, 7, 11, "f32")])
+def test_split_weight_gradient_matches_oracle_and_unsplit(N, G, di, dq, act):
+    """The split-contraction weight gradient: the oracle's grouped gradient, and
+    the unsplit form to float32 summation order; accumulate adds."""
+    say(f"split weight gradient N={N} G={G} di={di} dq={dq} {act}")
+    r = np.random.default_rng(N + 3 * G)
+    x = W._act(r, (N, G * di), act)
+    dy = W._act(r, (N, G * dq), act)
+    xd, dyd = dev_act(x, act), dev_act(dy, act)
+    dW = torch.empty((G, di, dq), dtype=torch.float32, device=xd.device)
+    ops.resonator_grouped_linear_bwd_weight_split(xd, dyd, dW)
+    _, dWu = ops.resonator_grouped_linear_bwd(xd, None, dyd, dW=torch.empty_like(dW))
+    dW2 = dW.clone()
+    ops.resonator_grouped_linear_bwd_weight_split(xd, dyd, dW2, accumulate=True)
+    torch.cuda.synchronize()
+    _, ref = O.grouped_linear_bwd(act64(x, act), np.zeros((G, di, dq)), act64(dy, act))
+    err = rel_err(host(dW), ref)
+    say(f"  err vs oracle {err:.2e}, vs unsplit {rel_err(host(dW), host(dWu)):.2e}")
+    assert err <= 1e-5 and rel_err(host(dW), host(dWu)) <= 1e-5
+    assert rel_err(host(dW2), 2 * ref) <= 1e-5
