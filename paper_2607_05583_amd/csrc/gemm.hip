@@ -164,7 +164,8 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
     const int64_t r = e / dq, j = e % dq, g = r / di;
     const float* src = P + r * d_out + g * dq + j;
     float v = 0.f;
-    for (int64_t q = 0; q < S; ++q) v += src[q * slab];
+#pragma unroll 8
+    for (int64_t q = 0; q < S; ++q) v += src[q * slab];  // loads issued ahead, sums in order
     W[e] = accumulate ? W[e] + v : v;
   }
 }
