@@ -13,7 +13,7 @@ exceeds the 256 MB Infinity Cache.  The JSON line also carries
             replayed from a captured HIP graph of the same calls;
   train     one forward + backward of a training layer (B=8, L=8192, D=256, M=8,
             bf16), as time per layer;
-  roofline  the dominant kernel (the single-pass forward segment kernel) against the HBM
+  roofline  the dominant kernel (the single-pass streaming forward kernel) against the HBM
             peak: algorithmic bytes (2 B read + 2 B written per token-channel)
             per launch over its average launch time, measured with HIP events
             recorded around that kernel alone;
@@ -37,7 +37,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 COPY_BYTES = 256 << 20  # calibration copy of the counter run
 METRIC = "prefill mix tokens·ch/s + decode steps/s at L=32K; % of HBM peak"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_seg_prefill_B4_L32768_D256_M8.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fwd_stream_prefill_B4_L32768_D256_M8.json")
 
 
 def log(msg):
@@ -57,26 +57,66 @@ def counter_traffic(per_launch_tokens: int):
     return t.get("bytes_per_launch")
 
 
-def cpu_baseline(cfg):
-    """The oracle's sequential recurrence on the prefill workload, timed on the host."""
+def _oracle_passes(args):
+    """Worker of the multi-process CPU leg: whole passes of the oracle recurrence
+    over one channel slice until min_s seconds of work; returns (passes, seconds)."""
+    x, prm, min_s = args
+    os.environ.setdefault("OMP_NUM_THREADS", "1")
     import oracle as O
-    import workloads as W
-    inp = W.fwd_inputs(cfg)
-    x = W.act_to_f32(inp["x"], cfg.act).astype(np.float64)
-    prm = [inp[k] for k in ("gamma", "omega", "amp", "phase")]
-    # whole passes over the workload until at least 10 s of CPU work
     passes, t0 = 0, time.perf_counter()
     while True:
         O.mix_recurrence(x, *prm)
         passes += 1
         dt = time.perf_counter() - t0
-        if dt >= 10.0 or passes >= 30:
+        if dt >= min_s:
+            return passes, dt
+
+
+def cpu_baseline(cfg, min_s=10.0):
+    """The oracle's sequential recurrence on the prefill workload, timed on the
+    host: one thread, then the channels split over one process per available
+    core (the recurrence of one channel is independent of the others)."""
+    import multiprocessing as mp
+    from concurrent.futures import ProcessPoolExecutor
+
+    import oracle as O
+    import workloads as W
+    inp = W.fwd_inputs(cfg)
+    x = W.act_to_f32(inp["x"], cfg.act).astype(np.float64)
+    prm = [inp[k] for k in ("gamma", "omega", "amp", "phase")]
+    # one thread: whole passes over the workload until min_s seconds of CPU work
+    passes, t0 = 0, time.perf_counter()
+    while True:
+        O.mix_recurrence(x, *prm)
+        passes += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_s or passes >= 30:
             break
-    n = cfg.B * cfg.L * cfg.D * passes
-    return {"value": n / dt, "unit": "tokens*ch/s", "cores": 1, "kind": "oracle",
-            "sample": f"{passes} passes over the whole prefill workload B={cfg.B} L={cfg.L} D={cfg.D} M={cfg.M}: "
-                      f"float64 numpy recurrence vectorised over (b, d, m), one host thread, "
-                      f"{dt:.1f} s in all"}
+    n1 = cfg.B * cfg.L * cfg.D * passes
+    single = {"value": n1 / dt, "unit": "tokens*ch/s", "cores": 1, "kind": "oracle",
+              "sample": f"{passes} passes over the whole prefill workload B={cfg.B} L={cfg.L} D={cfg.D} "
+                        f"M={cfg.M}: float64 numpy recurrence vectorised over (b, d, m), one host thread, "
+                        f"{dt:.1f} s in all"}
+    # all cores: the channels split into one slice per process (spawned before
+    # this process touches the GPU), each running whole passes for min_s seconds
+    cores = len(os.sched_getaffinity(0))
+    nproc = max(1, min(cores, 16, cfg.D))
+    bounds = np.linspace(0, cfg.D, nproc + 1).astype(int)
+    tasks = [(np.ascontiguousarray(x[:, :, a:b]), [v[a:b] for v in prm], min_s)
+             for a, b in zip(bounds[:-1], bounds[1:])]
+    t0 = time.perf_counter()
+    with ProcessPoolExecutor(max_workers=nproc, mp_context=mp.get_context("spawn")) as ex:
+        res = list(ex.map(_oracle_passes, tasks))
+    wall = time.perf_counter() - t0
+    done = sum(p * cfg.B * cfg.L * (b - a) for (p, _), a, b in zip(res, bounds[:-1], bounds[1:]))
+    longest = max(t for _, t in res)
+    return {"value": done / longest, "unit": "tokens*ch/s", "cores": nproc, "kind": "oracle",
+            "sample": f"the prefill workload B={cfg.B} L={cfg.L} D={cfg.D} M={cfg.M} with its channels split "
+                      f"over {nproc} processes ({cores} cores available), each running whole float64 passes of "
+                      f"the oracle recurrence over its {cfg.D // nproc}-{-(-cfg.D // nproc)} channels for at "
+                      f"least {min_s:.0f} s ({wall:.1f} s wall with start-up); throughput = channel-steps done "
+                      f"over the longest worker time",
+            "single_thread": single}
 
 
 def main():
@@ -97,8 +137,13 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
-    import torch
     import workloads as W
+    cpu = None
+    if not args.no_cpu and not args.counters:
+        log("cpu baseline (oracle recurrence, one thread and all cores) ...")
+        cpu = cpu_baseline(W.CONFIGS[3])
+
+    import torch
     from paper_2607_05583_amd import _lib, ops
     from paper_2607_05583_amd._lib import RES_OP_FWD
 
@@ -119,7 +164,7 @@ def main():
     hs = [torch.empty((cfg.B, cfg.D, cfg.M, 2), dtype=torch.float32, device=dev) for _ in range(NSET)]
     B, L, D, M = cfg.B, cfg.L, cfg.D, cfg.M
     wsn = ops.workspace_bytes(RES_OP_FWD, torch.bfloat16, B, L, D, M)
-    ws = torch.empty(wsn, dtype=torch.uint8, device=dev)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     import ctypes
     sp = ctypes.c_void_p(stream.cuda_stream)
@@ -172,12 +217,12 @@ def main():
     value = n_tok / (ms_step * 1e-3)
     alg_bytes = n_tok * 4
     achieved = alg_bytes / (k_avg_ms * 1e-3) / 1e9
-    log(f"prefill: {ms_step * 1e3:.1f} us/step (events), segment kernel {k_avg_ms * 1e3:.1f} us, "
+    log(f"prefill: {ms_step * 1e3:.1f} us/step (events), forward kernel {k_avg_ms * 1e3:.1f} us, "
         f"wall {t_wall / args.steps * 1e3:.1f} us/step")
 
     # ---------------- prefill across lengths (1K .. 32K tokens) ----------------
     # B4 D256 M8 bf16 as the prefill config, L from 1K to 32K; the step and the
-    # segment kernel alone, with the segment kernel's share of the HBM roofline
+    # forward kernel alone, with its share of the HBM roofline
     sweep = []
     for Ls in (1024, 2048, 4096, 8192, 16384, 32768):
         xl = torch.randn((B, Ls, D), generator=torch.Generator(device=dev).manual_seed(Ls), device=dev,
@@ -185,7 +230,7 @@ def main():
         yl = torch.empty_like(xl)
         hl = torch.empty((B, D, M, 2), dtype=torch.float32, device=dev)
         wn = ops.workspace_bytes(RES_OP_FWD, torch.bfloat16, B, Ls, D, M)
-        wl = torch.empty(wn, dtype=torch.uint8, device=dev)
+        wl = torch.zeros(wn, dtype=torch.uint8, device=dev)
         ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
 
         def fwd_l(timed):
@@ -216,9 +261,72 @@ def main():
         k_us = float(np.median(kus))
         gbs = B * Ls * D * 4 / (k_us * 1e-6) / 1e9
         sweep.append({"L": Ls, "B": B, "step_us": st_us, "tokens_ch_per_s": B * Ls * D / (st_us * 1e-6),
-                      "seg_kernel_us": k_us, "seg_kernel_GBs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS})
-        log(f"prefill L={Ls}: step {st_us:.1f} us, segment kernel {k_us:.1f} us ({gbs:.0f} GB/s)")
+                      "fwd_kernel_us": k_us, "fwd_kernel_GBs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS})
+        log(f"prefill L={Ls}: step {st_us:.1f} us, forward kernel {k_us:.1f} us ({gbs:.0f} GB/s)")
         del xl, yl, wl
+
+    # ---------------- measured copy bandwidth (the practical HBM ceiling) ----------------
+    # a device-to-device copy of 1 GiB (read + write), well beyond the Infinity Cache
+    csrc = torch.empty(1 << 30, dtype=torch.uint8, device=dev).fill_(1)
+    cdst = torch.empty_like(csrc)
+    for _ in range(2):
+        cdst.copy_(csrc)
+    torch.cuda.synchronize()
+    creps = 10
+    start.record(stream)
+    for _ in range(creps):
+        cdst.copy_(csrc)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2 * csrc.numel() / (start.elapsed_time(stop) * 1e-3 / creps) / 1e9
+    del csrc, cdst
+    log(f"device copy: {copy_gbs:.0f} GB/s (read + write)")
+
+    # ---------------- configs 1 and 2 (float32 forward) ----------------
+    fcfg = []
+    for k in (1, 2):
+        ck = W.CONFIGS[k]
+        ik = W.fwd_inputs(ck)
+        xk_ = torch.from_numpy(ik["x"]).to(dev)
+        yk_ = torch.empty_like(xk_)
+        pk_ = [torch.from_numpy(ik[n]).to(dev) for n in ("gamma", "omega", "amp", "phase")]
+        wn_ = ops.workspace_bytes(RES_OP_FWD, torch.float32, ck.B, ck.L, ck.D, ck.M)
+        wk_ = torch.zeros(wn_, dtype=torch.uint8, device=dev)
+        PK = [ctypes.c_void_p(p.data_ptr()) for p in pk_]
+        evk = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+        def fwd_k(timed):
+            if timed:
+                _lib.check(lib.resonator_set_kernel_timer(ctypes.c_void_p(evk[0].cuda_event),
+                                                          ctypes.c_void_p(evk[1].cuda_event)))
+            _lib.check(lib.resonator_mix_fwd(
+                ctypes.c_void_p(xk_.data_ptr()), _lib.RES_F32, ctypes.c_void_p(yk_.data_ptr()), _lib.RES_F32,
+                ck.B, ck.L, ck.D, ck.M, *PK, None, None, ctypes.c_void_p(wk_.data_ptr()), wn_, sp))
+
+        evk[0].record(stream)
+        evk[1].record(stream)
+        for _ in range(3):
+            fwd_k(False)
+        torch.cuda.synchronize()
+        reps = 50
+        start.record(stream)
+        for _ in range(reps):
+            fwd_k(False)
+        stop.record(stream)
+        torch.cuda.synchronize()
+        st_us = start.elapsed_time(stop) * 1e3 / reps
+        kus = []
+        for _ in range(10):
+            fwd_k(True)
+            torch.cuda.synchronize()
+            kus.append(evk[0].elapsed_time(evk[1]) * 1e3)
+        k_us = float(np.median(kus))
+        ntk = ck.B * ck.L * ck.D
+        gbs = ntk * 8 / (k_us * 1e-6) / 1e9
+        fcfg.append({"config": k, "workload": ck.name, "step_us": st_us, "tokens_ch_per_s": ntk / (st_us * 1e-6),
+                     "kernel_us": k_us, "kernel_alg_GBs": gbs, "frac_of_hbm_peak": gbs / HBM_PEAK_GBS})
+        log(f"config {k} ({ck.name}): step {st_us:.1f} us, kernel {k_us:.1f} us ({gbs:.0f} GB/s)")
+        del xk_, yk_, wk_
 
     # ---------------- decode ----------------
     c4 = W.CONFIGS[4]
@@ -266,8 +374,27 @@ def main():
     d1.record(stream)
     torch.cuda.synchronize()
     dec_graph_us = d0.elapsed_time(d1) * 1e3 / (reps * G)
+    # launch floor of a replayed graph: G launches of a one-element kernel
+    tiny = torch.zeros(1, dtype=torch.float32, device=dev)
+    fgraph = torch.cuda.CUDAGraph()
+    fcap = torch.cuda.Stream(dev)
+    fcap.wait_stream(stream)
+    with torch.cuda.stream(fcap), torch.cuda.graph(fgraph, stream=fcap):
+        for _ in range(G):
+            tiny.add_(1.0)
+    stream.wait_stream(fcap)
+    fgraph.replay()
+    torch.cuda.synchronize()
+    d0.record(stream)
+    for _ in range(reps):
+        fgraph.replay()
+    d1.record(stream)
+    torch.cuda.synchronize()
+    floor_us = d0.elapsed_time(d1) * 1e3 / (reps * G)
+    del fgraph
     dec_bytes = Bd * Dd * (Md * 16 + 2 + 2)
-    log(f"decode: eager {dec_eager_us:.2f} us/step, graph {dec_graph_us:.2f} us/step")
+    log(f"decode: eager {dec_eager_us:.2f} us/step, graph {dec_graph_us:.2f} us/step "
+        f"(replayed one-element launches: {floor_us:.2f} us each)")
     # several steps per launch, for drives known in advance: 8 drafted tokens to
     # verify per launch, and a long run of known drives in one launch
     xbn = xdec.permute(1, 0, 2).contiguous()  # [B, N, D]
@@ -442,11 +569,6 @@ def main():
             f"(speedup {quad_us / mix_us:.0f}x), FFT convolution {fft_us:.1f} us ({fft_us / mix_us:.1f}x)")
         del xk
 
-    cpu = None
-    if not args.no_cpu:
-        log("cpu baseline (oracle recurrence) ...")
-        cpu = cpu_baseline(cfg)
-
     traffic = counter_traffic(n_tok)
     out = {
         "metric": METRIC,
@@ -464,7 +586,11 @@ def main():
         "config": {"workload": cfg.name, "B": B, "L": L, "D": D, "M": M,
                    "activations": "bf16 in/out, fp32 accumulate, split-bf16 MFMA operands",
                    "terminal_state": True, "buffer_sets": NSET},
-        "prefill_sweep": {"workload": "B4 D256 M8 bf16, L = 1K .. 32K (segment kernel GB/s: 4 algorithmic bytes per "
+        "fp32_configs": {"workload": "configs 1 and 2, float32 in/out: the step (all kernels of a forward call) and "
+                                     "the dominant kernel alone (8 algorithmic bytes per token-channel)",
+                         "points": fcfg},
+        "copy_GBs": copy_gbs,
+        "prefill_sweep": {"workload": "B4 D256 M8 bf16, L = 1K .. 32K (forward kernel GB/s: 4 algorithmic bytes per "
                                       "token-channel); one buffer set per length, so inputs stay in the 256 MB "
                                       "Infinity Cache between calls (the headline line rotates three sets)",
                           "points": sweep},
@@ -473,7 +599,7 @@ def main():
                                     "mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection; forward, and backward "
                                     "(recomputed forward, then the chain rule)",
                         "points": blk},
-        "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (prep + segment kernel) vs the O(L^2) direct "
+        "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (forward kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol, and vs the "
                                     "zero-padded FFT convolution (rocFFT, the paper's prefill form)",
                         "points": kt},
@@ -483,6 +609,7 @@ def main():
         "decode": {"workload": c4.name, "steps": nsteps,
                    "steps_per_s_eager": 1e6 / dec_eager_us, "us_per_step_eager": dec_eager_us,
                    "steps_per_s_graph": 1e6 / dec_graph_us, "us_per_step_graph": dec_graph_us,
+                   "graph_launch_floor_us": floor_us, "graph_over_floor": dec_graph_us / floor_us,
                    "alg_GBs_graph": dec_bytes / (dec_graph_us * 1e-6) / 1e9},
         "train_layer": {"workload": "B8 L8192 D256 M8 bf16 (one of the 6 layers)",
                         "fwd_us": tr_fwd_us, "bwd_us": tr_bwd_us,
@@ -491,9 +618,9 @@ def main():
                            "fwd_us": ep_fwd_us, "bwd_us": ep_bwd_us,
                            "fwd_alg_GBs": n_ep * 8 / (ep_fwd_us * 1e-6) / 1e9,
                            "bwd_alg_GBs": n_ep * 14 / (ep_bwd_us * 1e-6) / 1e9},
-        "roofline": {"bound": "hbm", "kernel": "fwd_seg_kernel",
+        "roofline": {"bound": "hbm", "kernel": "fwd_stream_kernel",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS,
+                     "frac": achieved / HBM_PEAK_GBS, "frac_of_copy": achieved / copy_gbs,
                      "traffic": traffic,
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_us": k_avg_ms * 1e3},
         "cpu_baseline": cpu,

@@ -71,7 +71,14 @@ int resonator_version(void);
  * Bytes of device workspace that op (RES_OP_*) needs for activations of type
  * act_dt at sizes (B, L, D, M).  Returns 0 for invalid arguments.  The workspace
  * holds parameter tables, per-tile chunk states, carries and (for bwd) per-tile
- * partial sums; its contents need not be initialised and are clobbered.
+ * partial sums.
+ *   - RES_OP_FWD: the workspace must be zero-filled before its first forward call;
+ *     every forward call leaves it ready for the next one (any sizes whose need
+ *     it covers).  Its first 4 bytes are the forward status word (see
+ *     resonator_fwd_status).  Forward calls that share a workspace must not
+ *     overlap in time.
+ *   - RES_OP_BWD, RES_OP_STATE_INIT: contents need not be initialised and are
+ *     clobbered.
  */
 size_t resonator_workspace_bytes(int op, res_dtype_t act_dt, int64_t B, int64_t L, int64_t D,
                                  int64_t M);
@@ -110,9 +117,24 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
                       size_t ws_bytes, void* stream);
 
 /*
- * Prompt state for decoding (Sec. 3.2, cache construction): the weighted sum of
- * past drives under the complex decay factor, state[b,d,m] = sum_s lambda^(L-1-s)
- * x[b,s,d] (newest drive weight 1), from a zero initial state.
+ * Forward status word (the first 4 bytes of a forward workspace), an OR over the
+ * forward calls made with ws since it was last cleared:
+ *   bit 0  a bounded wait for another work-group's published state gave up (the
+ *          outputs of that call are wrong);
+ *   bit 1  the workspace counters were not in their initial state when a call
+ *          started (workspace not zero-filled before first use, or used by
+ *          overlapping calls): that call computed nothing and left y untouched.
+ * Neither happens with a zero-filled workspace used by one call at a time.  This
+ * call enqueues a copy of the word into *status (host memory) and a clear of the
+ * word on stream, then synchronises the stream.  Returns RES_OK, or
+ * RES_ERR_INVALID_ARG / RES_ERR_MISALIGNED / RES_ERR_HIP.
+ */
+int resonator_fwd_status(void* ws, uint32_t* status, void* stream);
+
+/*
+ * Prompt state for decoding (Sec. 3.2, cache construction): the terminal state
+ * state[b,d,m] = sum_s lambda^(L-1-s) x[b,s,d], each drive scaled by the pole
+ * raised to its age (newest drive weight 1), from a zero initial state.
  *   x_prompt  [B][L_prompt][D] of x_dt, may be NULL when L_prompt == 0
  *   state_out [B][D][M][2] float32       written
  *   ws        workspace of resonator_workspace_bytes(RES_OP_STATE_INIT, x_dt, B, L_prompt, D, M)

@@ -217,9 +217,9 @@ def mix_lfilter(x, gamma, omega, amp, phase) -> np.ndarray:
 def state_init(x, gamma, omega, amp, phase) -> np.ndarray:
     """Terminal state after a prompt, [B, D, M, 2] (re, im).
 
-    Sec. 3.2, cache construction: the prompt state is the weighted sum of past
-    drives under the complex decay factor, h_{L-1} = sum_s lambda^(L-1-s) x_s
-    (newest drive weight 1; reading of the terminal-state index).  Powers are
+    Sec. 3.2, cache construction: terminal state h_{L-1} = sum_s lambda^(L-1-s) x_s,
+    every past drive scaled by the pole raised to its age (newest drive weight 1;
+    reading of the terminal-state index).  Powers are
     evaluated directly from their exact integer lags.  L = 0 gives the zero state.
     """
     x = as_f64(x)

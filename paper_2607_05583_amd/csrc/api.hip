@@ -45,16 +45,6 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 // Geometry of the tiled kernels for activations of type act (tile width depends
 // on the element size: 128-byte rows).
-// words ahead of the segment flags: [0] segment ticket, [1] error word
-// payload words of the single-kernel forward: per segment and channel, 8 modes (re, im)
-inline size_t seg_payload_words(const Geometry& g) {
-  const int64_t segs = g.B * g.NB * ((g.P + g.seg_len - 1) / g.seg_len);
-  return (size_t)segs * g.Dp / g.NB * MODES_PER_GROUP * 2;
-}
-// segments of the single-kernel forward: one work-group per compute unit of an
-// MI355X (256)
-constexpr int64_t SEG_TARGET = 256;
-
 Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) {
   Geometry g;
   g.B = B;
@@ -68,18 +58,54 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
   g.Mp = MODES_PER_GROUP * g.MG;
   g.P = L > 0 ? (L + TILE_T - 1) / TILE_T : 0;
   g.last_len = L > 0 ? (int)(L - (g.P - 1) * TILE_T) : 0;
-  // single-kernel forward: about SEG_TARGET segments over all rows, so that all
-  // of them are resident at once
-  const int64_t tiles = B * g.NB * g.P;
-  g.seg_len = tiles > 0 ? (int)((tiles + SEG_TARGET - 1) / SEG_TARGET) : 1;
-  if (g.seg_len > g.P) g.seg_len = (int)(g.P > 0 ? g.P : 1);
+  g.seg_len = 1;
   return g;
+}
+
+// Workspace of the single-pass forward (M <= 8), byte offsets.  The first 256
+// bytes are the header (status word first); the forward workspace must be zero
+// before its first use and each call leaves it ready for the next.
+struct StreamLayout {
+  size_t hdr, ticket, claim, tflag, flag, tab, scal, agg, inc, total;
+};
+StreamLayout make_stream_layout(const Geometry& g) {
+  StreamLayout w{};
+  const int NW = g.DW / 4, NQ = g.DW / 16;
+  const size_t nchains = (size_t)g.B * g.NB, tiles = nchains * (size_t)g.P;
+  size_t off = 0;
+  w.hdr = off;
+  off += 256;
+  w.ticket = off;
+  off += align256(nchains * sizeof(uint32_t));
+  w.claim = off;
+  off += align256((size_t)g.NB * sizeof(uint32_t));
+  w.tflag = off;
+  off += align256((size_t)g.NB * NW * sizeof(uint32_t));
+  w.flag = off;
+  off += align256(tiles * NQ * sizeof(uint32_t));
+  w.tab = off;
+  off += align256((size_t)g.Dp * 3 * 64 * 16);
+  w.scal = off;
+  off += align256((size_t)g.Dp * 8 * 4 * sizeof(float2));
+  w.agg = off;
+  off += align256(tiles * NQ * 64 * 16);
+  w.inc = off;
+  off += align256(tiles * NQ * 64 * 16);
+  w.total = off;
+  return w;
 }
 
 WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
   WsLayout w{};
   size_t off = 0;
   (void)act;
+  if (op == RES_OP_FWD) {
+    if (g.MG == 1) {
+      w.total = make_stream_layout(g).total;
+      return w;
+    }
+    off = 256;  // header (status word), as in the single-pass layout
+  }
   const int nm = op == RES_OP_BWD ? bwd_mats(g.MG) : fwd_mats(g.MG);
   const size_t tiles_modes = (size_t)g.B * g.P * g.Dp * g.Mp;  // = tiles * DW * Mp
   w.tab = off;
@@ -98,14 +124,6 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
     }
     w.alast = off;  // [B][Dp][Mp] state at t = L-1 from a zero start at the last tile
     off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float2));
-    if (op == RES_OP_FWD) {  // single-kernel forward: header words, then per (segment, wave) payloads
-      w.flags = off;
-      off += align256((SEG_HEADER_WORDS + seg_payload_words(g)) * sizeof(uint32_t));
-      w.mpow = off;  // [Dp][16][Mp] lambda^(16 j)
-      off += align256((size_t)g.Dp * CHUNK * g.Mp * sizeof(float2));
-      w.spow = off;  // [Dp][17][Mp] lambda^(256 seg_len n)
-      off += align256((size_t)g.Dp * (CHUNK + 1) * g.Mp * sizeof(float2));
-    }
   } else {
     w.agg = off;
     off += align256(tiles_modes * sizeof(float4));
@@ -175,10 +193,14 @@ size_t resonator_workspace_bytes(int op, res_dtype_t act_dt, int64_t B, int64_t 
   return make_layout(op, act_dt, make_geom(act_dt, B, L, D, M)).total;
 }
 
-int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B,
-                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
-                      const float* amp, const float* phase, const float* h0, float* h_out,
-                      void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation and dispatch of the forward.
+int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t L, int64_t D,
+                 int64_t M, const float* gamma, const float* omega, const float* amp, const float* phase,
+                 const float* h0, float* h_out, void* ws, size_t ws_bytes, void* stream) {
   int rc = check_sizes(B, L, D, M, false);
   if (rc) return rc;
   if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
@@ -200,19 +222,60 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
 
   hipStream_t st = (hipStream_t)stream;
   char* base = (char*)ws;
+  // 16-byte row segments: both activation pointers 16-byte aligned, rows a multiple of 16 bytes
+  const int fast_io = aligned(x, 16) && aligned(y, 16) && (D * elt_size(x_dt)) % 16 == 0 &&
+                      (D * elt_size(y_dt)) % 16 == 0;
+  hipEvent_t ev0, ev1;
+  take_timer(&ev0, &ev1);
+  hipError_t e;
+  if (g.MG == 1) {  // single-pass forward
+    const StreamLayout sl = make_stream_layout(g);
+    int dev = 0, ncu = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+      return hip_fail(e, "device attribute");
+    StreamArgs a{};
+    a.x = x;
+    a.y = y;
+    a.B = B;
+    a.L = L;
+    a.D = (int)D;
+    a.M = (int)M;
+    a.NB = g.NB;
+    a.nchains = (int)(B * g.NB);
+    a.P = g.P;
+    a.last_len = g.last_len;
+    a.fast_io = fast_io;
+    a.gamma = gamma;
+    a.omega = omega;
+    a.amp = amp;
+    a.phase = phase;
+    a.h0 = h0;
+    a.h_out = h_out;
+    a.hdr = (uint32_t*)(base + sl.hdr);
+    a.ticket = (uint32_t*)(base + sl.ticket);
+    a.claim = (uint32_t*)(base + sl.claim);
+    a.tflag = (uint32_t*)(base + sl.tflag);
+    a.flag = (uint32_t*)(base + sl.flag);
+    a.tab = (uint4*)(base + sl.tab);
+    a.scal = (float2*)(base + sl.scal);
+    a.agg = (uint4*)(base + sl.agg);
+    a.inc = (uint4*)(base + sl.inc);
+    const int grid = fwd_stream_grid(B * g.NB, g.P, ncu > 0 ? ncu : 256);
+    if (x_dt == RES_F32)
+      e = launch_fwd_stream<float, float>(a, grid, st, ev0, ev1);
+    else if (y_dt == RES_BF16)
+      e = launch_fwd_stream<bf16_t, bf16_t>(a, grid, st, ev0, ev1);
+    else
+      e = launch_fwd_stream<bf16_t, float>(a, grid, st, ev0, ev1);
+    if (e != hipSuccess) return hip_fail(e, "forward launch");
+    return RES_OK;
+  }
   ModeScalars* scal = (ModeScalars*)(base + w.scal);
   ModeCarry* cc = (ModeCarry*)(base + w.carryc);
-  const bool segs = g.MG == 1;  // single-kernel forward for M <= 8
-  uint32_t* fl = (uint32_t*)(base + w.flags);
-  float2* mpow = (float2*)(base + w.mpow);
-  float2* spow = (float2*)(base + w.spow);
-  const int64_t nflags = segs ? (int64_t)(SEG_HEADER_WORDS + seg_payload_words(g)) : 0;
-  hipError_t e =
-      x_dt == RES_BF16
-          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
-                                segs ? mpow : nullptr, segs ? spow : nullptr, segs ? fl : nullptr, nflags)
-          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st,
-                               segs ? mpow : nullptr, segs ? spow : nullptr, segs ? fl : nullptr, nflags);
+  e = x_dt == RES_BF16
+          ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st)
+          : launch_prep<float>(g, gamma, omega, amp, phase, false, base + w.tab, scal, cc, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
   FwdArgs a{};
   a.x = x;
@@ -226,33 +289,12 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   a.Mp = g.Mp;
   a.P = g.P;
   a.last_len = g.last_len;
-  // 16-byte row segments: both activation pointers 16-byte aligned, rows a multiple of 16 bytes
-  a.fast_io = aligned(x, 16) && aligned(y, 16) && (D * elt_size(x_dt)) % 16 == 0 &&
-              (D * elt_size(y_dt)) % 16 == 0;
+  a.fast_io = fast_io;
   a.tab = base + w.tab;
   a.scal = scal;
   a.cc = cc;
-  a.mpow = mpow;
-  a.spow = spow;
   a.h0 = h0;
   a.h_out = h_out;
-  hipEvent_t ev0, ev1;
-  take_timer(&ev0, &ev1);
-  if (segs) {
-    a.seg_len = g.seg_len;
-    a.seg_per_chain = (int)((g.P + g.seg_len - 1) / g.seg_len);
-    a.ticket = fl;
-    a.error = fl + 1;
-    a.pay_agg = (float2*)(fl + SEG_HEADER_WORDS);
-    if (x_dt == RES_F32)
-      e = launch_fwd_segments<float, float>(g, a, st, ev0, ev1);
-    else if (y_dt == RES_BF16)
-      e = launch_fwd_segments<bf16_t, bf16_t>(g, a, st, ev0, ev1);
-    else
-      e = launch_fwd_segments<bf16_t, float>(g, a, st, ev0, ev1);
-    if (e != hipSuccess) return hip_fail(e, "forward launch");
-    return RES_OK;
-  }
   a.agg = base + w.agg;
   a.car = base + w.carry;
   a.alast = (float2*)(base + w.alast);
@@ -266,6 +308,29 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
   else
     e = launch_fwd_apply<bf16_t, float>(g, a, st, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "apply launch");
+  return RES_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B,
+                      int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
+                      const float* amp, const float* phase, const float* h0, float* h_out,
+                      void* ws, size_t ws_bytes, void* stream) {
+  return mix_fwd_impl(x, x_dt, y, y_dt, B, L, D, M, gamma, omega, amp, phase, h0, h_out, ws, ws_bytes, stream);
+}
+
+int resonator_fwd_status(void* ws, uint32_t* status, void* stream) {
+  if (!ws || !status) return fail(RES_ERR_INVALID_ARG, "ws and status must be non-null");
+  if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if ((e = hipMemcpyAsync(status, ws, sizeof(uint32_t), hipMemcpyDeviceToHost, st)) != hipSuccess)
+    return hip_fail(e, "status copy");
+  if ((e = hipMemsetAsync(ws, 0, sizeof(uint32_t), st)) != hipSuccess) return hip_fail(e, "status clear");
+  if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(e, "status synchronize");
   return RES_OK;
 }
 

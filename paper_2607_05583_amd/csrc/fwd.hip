@@ -308,6 +308,10 @@ template <> struct FPath<float> {
   typedef f4 AOp;
   typedef f4 XOp;
   __device__ static __forceinline__ AOp load_a(const void* p) { return load_f4(p); }
+  __device__ static __forceinline__ AOp load_a_u4(uint4 u) {
+    const f4 r = {__uint_as_float(u.x), __uint_as_float(u.y), __uint_as_float(u.z), __uint_as_float(u.w)};
+    return r;
+  }
   __device__ static __forceinline__ f4 mma(const AOp& a, const XOp& x, f4 c) { return mma_f32(a, x, c); }
   // (A x)^T: lane (i, q) gets columns 4q .. 4q+3 of row i of A x
   __device__ static __forceinline__ f4 mma_t(const XOp& x, const AOp& a, f4 c) { return mma_f32(x, a, c); }
@@ -331,8 +335,8 @@ template <> struct FPath<bf16_t> {
     s4 hi, lo;
   };
   typedef s4 XOp;
-  __device__ static __forceinline__ AOp load_a(const void* p) {
-    const uint4 u = *reinterpret_cast<const uint4*>(p);
+  __device__ static __forceinline__ AOp load_a(const void* p) { return load_a_u4(*reinterpret_cast<const uint4*>(p)); }
+  __device__ static __forceinline__ AOp load_a_u4(uint4 u) {
     AOp a;
     a.hi = __builtin_bit_cast(s4, make_uint2(u.x, u.y));
     a.lo = __builtin_bit_cast(s4, make_uint2(u.z, u.w));
@@ -629,6 +633,9 @@ __global__ __launch_bounds__(256) void fwd_carry_kernel(FwdArgs a, int seg_len, 
     ent = make_double2(h[0], h[1]);
   }
   for (int s2 = 0; s2 < seg; ++s2) ent = zfma(lamS, ent, sg[s2 * pw + pl]);
+  // every thread of a (row, pair) has read h0 before the last segment's thread
+  // writes h_out below, so h_out may be the h0 buffer
+  __syncthreads();
   if (!valid) return;
   // pass 2: replay, writing the entry states of every tile of the segment
   double2 cst = ent;
@@ -773,32 +780,39 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
 }
 
 // ---------------------------------------------------------------------------
-// Single-kernel forward over row segments (one mode group, M <= 8).
+// Single-pass forward (one mode group, M <= 8).
 //
-// A work-group (8 waves) owns seg_len consecutive tiles of one chain (batch row
-// b, channel block); each wave owns CW channels of the tile and keeps their
-// operands in registers for the whole segment.  Per channel the state MFMA
-// S = V x leaves, in lane (n, q), the drives of chunk n for the modes 2q and
-// 2q+1; everything on the chunk axis then runs across the 16 lanes of a row.
-//   pass 1  per tile, lane-wise acc = lambda^256 acc + mu^(15-n) S; the row sum
-//           of acc is the segment's own end state from a zero start (agg_s);
-//   carry   per wave (its channels form their own sub-chain): publish agg_s,
-//           wait for the aggregates of all earlier segments of the row and
-//           fold them, with the row's initial state, into the state entering
-//           the segment (a fixed-order weighted sum, lanes in parallel);
-//   pass 2  the segment streams again: per tile and channel, the entering state
-//           c is added to lane 0 as mu c, the chunk recurrence
-//           Q[n] = mu Q[n-1] + S[n] is a four-step prefix scan over the row
-//           (shifts 1, 2, 4, 8 with multipliers mu, mu^2, mu^4, mu^8), the
-//           state entering chunk n is Q[n-1] (c for n = 0) and feeds
-//           y = T x + U H directly as the float32 MFMA operand; Q[15] is the
-//           next tile's entering state.
-// Tiles stream through three LDS tile buffers; wave 0 alone issues the
-// direct-to-LDS loads (two tiles in flight), the other waves store the output
-// rows.  Work-groups take segments in ticket order (time-major over the chains),
-// so every wait is on a smaller ticket, which a running work-group took and
-// publishes without waiting; every wait is bounded.  Payloads and flags are agent-coherent (device-scope)
-// accesses; a publisher completes its payload stores before the flag store.
+// A chain is one batch row and one block of DW channels (128-byte rows).  Its
+// tiles (256 steps) are taken in time order, by ticket, by the work-groups that
+// serve the chain, so that a tile's predecessors hold smaller tickets and belong
+// to running work-groups.  Per tile:
+//   pass 1   per channel, S = V x on MFMA (lane (c, q): component c of chunks
+//            4q .. 4q+3); the results of a wave's four channels are exchanged
+//            across lane rows (lane swaps), after which lane (c, k) holds
+//            component c of channel k for all 16 chunks, and the tile's end state
+//            from a zero start, A = sum_n mu^(15-n) S[n] (mu = lambda^16), is 16
+//            steps A <- mu A + S[n] in the lane's own registers.
+//   carry    control waves (one per 16 channels) publish A, find the nearest
+//            earlier tile of the chain whose inclusive end state I is published
+//            (or their work-group's own previous tile, or h0 at the chain start),
+//            fold the published A of the tiles in between, oldest first,
+//            E <- lambda^256 E + A, and publish this tile's I = lambda^256 E + A.
+//   pass 2   the states entering the chunks, H[0] = E, H[n+1] = mu H[n] + S[n]
+//            (the same 16 steps), move through LDS into the MFMA operand layout;
+//            y = T x + U H is rounded into the tile buffer and leaves as 128-byte
+//            rows.
+// Load waves issue the tile loads (direct to LDS, four buffers, three tiles
+// ahead) and the row stores; control waves issue no tile traffic, so that their
+// waits on published states never wait behind tile loads (a wave's vector memory
+// operations complete in order).  A published state is a set of device-coherent
+// stores followed, once they have completed, by a flag store; a reader polls the
+// flag, then loads the state with device-coherent loads.  Flags carry the call's
+// epoch, so they are never reset; the counters are reset by the last work-group
+// to finish.
+// Operand tables are built in the kernel: the channels of a block form units of
+// 4 (one wave's channels); a work-group claims units of its block by ticket,
+// builds them in float64 and publishes them; every wave waits for the units it
+// reads.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void st_agent(float2* p, float2 v) {
   __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v),
@@ -808,15 +822,17 @@ __device__ __forceinline__ float2 ld_agent(const float2* p) {
   return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const uint64_t*>(p),
                                                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
 }
-// the two modes of a lane as (re, im, re, im)
-__device__ __forceinline__ void st_agent4(float2* p, f4 v) {
-  st_agent(p, make_float2(v[0], v[1]));
-  st_agent(p + 1, make_float2(v[2], v[3]));
+// 16 bytes as two device-coherent 8-byte accesses
+__device__ __forceinline__ void st_dev16(void* p, uint4 v) {
+  uint64_t* q = reinterpret_cast<uint64_t*>(p);
+  __hip_atomic_store(q, (uint64_t)v.x | ((uint64_t)v.y << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(q + 1, (uint64_t)v.z | ((uint64_t)v.w << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ f4 ld_agent4(const float2* p) {
-  const float2 u = ld_agent(p), w = ld_agent(p + 1);
-  const f4 r = {u.x, u.y, w.x, w.y};
-  return r;
+__device__ __forceinline__ uint4 ld_dev16(const void* p) {
+  const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
+  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
 }
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
   return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -824,11 +840,14 @@ __device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
 __device__ __forceinline__ void st_flag(uint32_t* f, uint32_t v) {
   __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Upper bound on window polls (about a second); reached only if a predecessor
-// never publishes, which the ticket order rules out.  The wave then starts from
-// the row's initial state and records the event in the error word.
-constexpr uint32_t SPIN_LIMIT = 1u << 20;
-constexpr uint32_t PAY_EMPTY = PAY_EMPTY_WORD;
+// Upper bound on polls of one wait (with a short sleep between polls, well over
+// 0.1 s).  In ticket order every wait ends long before it; it is reached only
+// with a workspace that was not zeroed before its first use (or was changed
+// meanwhile): the kernel then records bit 0 in the status word and goes on.
+constexpr uint32_t SPIN_LIMIT = 1u << 18;
+// Polls of the wait that spaces a work-group's first claims (some tens of
+// microseconds at most; past it the claim is made anyway).
+constexpr uint32_t CLAIM_WAIT = 64;
 
 // Complex arithmetic on the two modes of a lane, (re_a, im_a, re_b, im_b).
 __device__ __forceinline__ f4 c2mul(const f4& a, const f4& b) {
@@ -852,26 +871,6 @@ __device__ __forceinline__ f4 mode_pair(float2 u, float2 w) {
   return r;
 }
 
-// Lane moves inside rows of 16 lanes (DPP).  BOUND0: lanes without a source
-// lane read zero; otherwise they keep `old`.
-constexpr int DPP_ROW_SHL(int n) { return 0x100 + n; }   // lane i <- lane i + n
-constexpr int DPP_ROW_SHR(int n) { return 0x110 + n; }   // lane i <- lane i - n
-constexpr int DPP_QUAD(int a, int b, int c, int d) { return a | (b << 2) | (c << 4) | (d << 6); }
-constexpr int DPP_ROW_MIRROR = 0x140;                    // lane i <- lane 15 - i
-constexpr int DPP_ROW_HALF_MIRROR = 0x141;               // lane i <- lane 7 - i (per half row)
-template <int CTRL, bool BOUND0>
-__device__ __forceinline__ f4 dpp4(const f4& old, const f4& v) {
-  f4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const float o = old[i], x = v[i];  // scalars: a vector element is no lvalue for bit_cast
-    r[i] = __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(__builtin_bit_cast(int, o),
-                                                                 __builtin_bit_cast(int, x), CTRL,
-                                                                 0xF, 0xF, BOUND0));
-  }
-  return r;
-}
-
 // One complex multiply-add on the lane's component of a (re, im) lane pair:
 // zr v + zs v' + add, with v' the value of lane i ^ 1 (the other component),
 // zs = -Im z on the re lane and +Im z on the im lane.  The partner product is
@@ -887,31 +886,6 @@ __device__ __forceinline__ float cfma_pair(float zr, float zs, float v, float ad
   return acc;
 }
 
-// Sum over the 16 lanes of each row, in every lane of the row (the same order in
-// every lane, so the copies agree bitwise).
-__device__ __forceinline__ f4 row_sum(f4 v) {
-  v += dpp4<DPP_QUAD(1, 0, 3, 2), false>(v, v);
-  v += dpp4<DPP_QUAD(2, 3, 0, 1), false>(v, v);
-  v += dpp4<DPP_ROW_HALF_MIRROR, false>(v, v);
-  v += dpp4<DPP_ROW_MIRROR, false>(v, v);
-  return v;
-}
-
-template <typename TX>
-struct SegGeo {
-  static constexpr int DW = tile_channels<TX>();
-  static constexpr int NW = sizeof(TX) == 2 ? 16 : 8;  // waves
-  static constexpr int CW = DW / NW;    // channels per wave (4)
-  // 16 waves: one channel at a time through the scan (one LDS slot per wave);
-  // 8 waves: four channels at a time (four slots per wave)
-  static constexpr int SLOTS = NW == 16 ? 1 : 4;
-  static constexpr int NG = CW / 4;     // operand gathers of 4 channels per wave
-  static constexpr int NT = 64 * NW;    // threads
-  // tile buffers; the waves w with w % NBUF == u load the tiles of buffer u
-  static constexpr int NBUF = seg_bufs((int)sizeof(TX));
-  static_assert(NBUF <= NW, "a loading wave per buffer");
-};
-
 // One 16-byte-per-lane load straight into LDS (64 lanes, 1 KB at lds) from
 // base + off (base wave-uniform, off the lane's byte offset).  Issued as an
 // opaque instruction: the compiler then does not wait for it before every later
@@ -923,31 +897,34 @@ __device__ __forceinline__ void lds_dma16(const void* base, uint32_t off, const 
   asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(la) : "memory");
 }
 
-// Wait until at most n vector memory operations of the wave are outstanding
-// (n <= 15; exp and lgkm counts not waited for).
+// Wait until at most n (0 <= n <= 63) vector memory operations of the wave are
+// outstanding (exp and lgkm counts not waited for).
 __device__ __forceinline__ void wait_vmcnt(int n) {
   switch (n) {
-#define RES_VMCNT(k) \
-  case k: __builtin_amdgcn_s_waitcnt(0x0F70 | k); break;
-    RES_VMCNT(0) RES_VMCNT(1) RES_VMCNT(2) RES_VMCNT(3) RES_VMCNT(4) RES_VMCNT(5) RES_VMCNT(6) RES_VMCNT(7)
-    RES_VMCNT(8) RES_VMCNT(9) RES_VMCNT(10) RES_VMCNT(11) RES_VMCNT(12) RES_VMCNT(13) RES_VMCNT(14)
-#undef RES_VMCNT
-    default: __builtin_amdgcn_s_waitcnt(0x0F70 | 15); break;
+#define RES_VMC(k) \
+  case k: __builtin_amdgcn_s_waitcnt(0x0F70 | ((k) & 15) | (((k) >> 4) << 14)); break;
+#define RES_VMC8(k) RES_VMC(k) RES_VMC(k + 1) RES_VMC(k + 2) RES_VMC(k + 3) RES_VMC(k + 4) RES_VMC(k + 5) \
+  RES_VMC(k + 6) RES_VMC(k + 7)
+    RES_VMC8(0) RES_VMC8(8) RES_VMC8(16) RES_VMC8(24) RES_VMC8(32) RES_VMC8(40) RES_VMC8(48) RES_VMC8(56)
+#undef RES_VMC8
+#undef RES_VMC
+    default: __builtin_amdgcn_s_waitcnt(0x0F70); break;
   }
 }
 
 // 16-byte store of each lane to base + off (base wave-uniform), as an opaque
 // instruction like lds_dma16, so that the compiler keeps the 64-bit base in
-// scalar registers and the lane offset in one vector register.
+// scalar registers and the lane offset in one vector register.  A store of more
+// than 8 bytes reads its data registers after issue: on gfx950 a vector write to
+// them needs two wait states after the store, which the compiler's hazard
+// tracking cannot see inside an asm statement, so the asm carries them.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void st_row16(void* base, uint32_t off, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, %2" ::"v"(off), "v"(v), "s"(base) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, %2\n\ts_nop 1" ::"v"(off), "v"(v), "s"(base) : "memory");
 }
 
 // Direct-to-LDS load of row group g (8 rows of 128 bytes, one 16-byte load
-// per lane) of a full tile by the calling wave.  While the memory system is
-// busy, issuing such a load holds the wave for a while, so a tile's groups are
-// spread over all waves and over their compute.
+// per lane) of a full tile by the calling wave.
 template <typename TX>
 __device__ __forceinline__ void dma_group(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
                                           int D, int lane, int g) {
@@ -978,13 +955,12 @@ __device__ __forceinline__ void store_group(TY* y, const char* xt, int64_t b, in
   st_row16(dst, loff, v);
 }
 
-// Element copy of a tile that is not full (all threads); zeros outside the tensor.
-template <typename TX>
+// Element copy of a tile that is not full (NT threads); zeros outside the tensor.
+template <typename TX, int NT>
 __device__ __forceinline__ void copy_tile(char* xt, const TX* x, int64_t b, int64_t t0, int d0, int64_t L,
                                           int D, int tid) {
-  typedef SegGeo<TX> G;
-  constexpr int DW = G::DW, XE = (int)sizeof(TX);
-  for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
+  constexpr int DW = tile_channels<TX>(), XE = (int)sizeof(TX);
+  for (int idx = tid; idx < TILE_T * DW; idx += NT) {
     const int t = idx / DW, c = idx % DW;
     TX v = from_f32<TX>(0.f);
     if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
@@ -992,416 +968,561 @@ __device__ __forceinline__ void copy_tile(char* xt, const TX* x, int64_t b, int6
   }
 }
 
-// Output tile that is not full, from its LDS buffer (all threads): guarded
+// Output tile that is not full, from its LDS buffer (NT threads): guarded
 // element stores.
-template <typename TY>
+template <typename TY, int NT>
 __device__ __forceinline__ void store_tile_part(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
                                                 int D, int tid) {
-  typedef SegGeo<TY> G;
-  constexpr int DW = G::DW, YE = (int)sizeof(TY);
-  for (int idx = tid; idx < TILE_T * DW; idx += G::NT) {
+  constexpr int DW = tile_channels<TY>(), YE = (int)sizeof(TY);
+  for (int idx = tid; idx < TILE_T * DW; idx += NT) {
     const int t = idx / DW, c = idx % DW;
     if (t0 + t < L && d0 + c < D)
       y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TY*>(xt + XLay<YE>::off(t) + c * YE);
   }
 }
 
+template <typename TX>
+struct StreamGeo {
+  static constexpr int DW = tile_channels<TX>();   // channels per tile: 64 (bf16) | 32 (float)
+  static constexpr int NW = DW / 4;                // waves, 4 channels each: 16 | 8
+  static constexpr int NT = 64 * NW;
+  static constexpr int NQ = DW / 16;               // control waves (16 channels each): waves 0 .. NQ-1
+  static constexpr int LW = NW == 16 ? 8 : 4;      // load waves: NQ .. NQ+LW-1
+  static constexpr int GPL = (TILE_T / 8) / LW;    // row groups per load wave and tile
+  static constexpr int NBUF = 4;                   // tile buffers
+  static constexpr int HR = NW == 16 ? 2 : 4;      // channels per round of the H transposition
+  static constexpr int HKS = 16 * 16 + 16;         // floats per channel there (16 floats of bank offset)
+  static constexpr int XB = XLay<(int)sizeof(TX)>::BYTES;
+  static constexpr int HB = NW * HR * HKS * 4;
+  static constexpr int BUFB = XB > HB ? XB : HB;   // bytes per buffer (tile, or H transposition)
+  static_assert(GPL * LW == TILE_T / 8, "the load waves cover a tile");
+  static_assert(NQ + LW <= NW, "control and load waves are distinct");
+};
+
+// z^n for 0 <= n <= 16, float64 (binary powers)
+__device__ __forceinline__ double2 zpow16(double2 z, int n) {
+  double2 r = make_double2(1.0, 0.0), s = z;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) {
+    if (n & (1 << i)) r = zmul(r, s);
+    s = zmul(s, s);
+  }
+  return r;
+}
+
+// Operand tables of the channels d0u .. d0u+3 (one unit), as the MFMA lanes
+// read them: T (lower Toeplitz taps K[i-k]), V (lambda^(15-k), re/im rows), U
+// (c lambda^(i+1), re/-im columns, float32), T and V split into bf16 halves
+// for bf16 activations; and per (channel, mode) mu = lambda^16, lambda^256,
+// lambda and lambda^(jstar+1).  Every power is built in float64 from lambda =
+// exp(-gamma) (cos omega, sin omega) by products (a relative error of a few
+// 2^-53 per product), then rounded once.  All threads take part (LDS stages at
+// lds); the waves that issue no tile loads store the results.
+template <typename TX>
+__device__ void build_unit(const StreamArgs& a, int d0u, char* lds, int tid, int wave) {
+  typedef StreamGeo<TX> G;
+  double2* lam = reinterpret_cast<double2*>(lds);  // [32] (channel k, mode m) = 8 k + m
+  double2* cm = lam + 32;                          // [32] c
+  double2* pw = cm + 32;                           // [32][17] lambda^j
+  double2* l256 = pw + 32 * 17;                    // [32] lambda^256
+  double* taps = reinterpret_cast<double*>(l256 + 32);  // [4][16]
+  if (tid < 32) {
+    const int k = tid >> 3, m = tid & 7, d = d0u + k;
+    double2 z = make_double2(0.0, 0.0), cz = z;
+    if (d < a.D && m < a.M) {
+      const int i = d * a.M + m;
+      double sn, cs;
+      sincos((double)a.omega[i], &sn, &cs);
+      const double e = exp(-(double)a.gamma[i]);
+      z = make_double2(e * cs, e * sn);
+      sincos((double)a.phase[i], &sn, &cs);
+      const double av = (double)a.amp[i];
+      cz = make_double2(av * cs, av * sn);
+    }
+    lam[tid] = z;
+    cm[tid] = cz;
+  }
+  __syncthreads();
+  for (int t = tid; t < 32 * 17 + 32; t += G::NT) {
+    if (t < 32 * 17) {
+      pw[t] = zpow16(lam[t / 17], t % 17);
+    } else {
+      double2 z = lam[t - 32 * 17];
+#pragma unroll
+      for (int s = 0; s < 8; ++s) z = zmul(z, z);
+      l256[t - 32 * 17] = z;
+    }
+  }
+  __syncthreads();
+  if (tid < 64) {  // K[tau] = Re sum_m c lambda^tau
+    const int k = tid >> 4, tau = tid & 15;
+    double s = 0.0;
+    for (int m = 0; m < 8; ++m) {
+      const double2 c = cm[8 * k + m], p = pw[(8 * k + m) * 17 + tau];
+      s += c.x * p.x - c.y * p.y;
+    }
+    taps[tid] = s;
+  }
+  __syncthreads();
+  if (wave < G::NQ || wave >= G::NQ + G::LW) {
+    const int bt = wave < G::NQ ? tid : tid - 64 * G::LW;
+    constexpr int NBT = 64 * (G::NW - G::LW);
+    const int jt = (a.last_len - 1) % CHUNK + 1;  // jstar + 1
+    // entry (mat, channel k, row i, column kk)
+    auto entry = [&](int mat, int k, int i, int kk) -> double {
+      if (mat == 0) return i >= kk ? taps[16 * k + i - kk] : 0.0;
+      if (mat == 1) {
+        const double2 z = pw[(8 * k + i / 2) * 17 + CHUNK - 1 - kk];
+        return (i & 1) ? z.y : z.x;
+      }
+      const int m = 8 * k + kk / 2;
+      const double2 z = zmul(cm[m], pw[m * 17 + i + 1]);
+      return (kk & 1) ? -z.y : z.x;
+    };
+    for (int t = bt; t < 4 * 3 * 64 + 32; t += NBT) {
+      if (t < 4 * 3 * 64) {
+        const int k = t / 192, mat = (t / 64) % 3, l = t % 64, i = l % 16, q = l / 16;
+        uint4 out;
+        if (sizeof(TX) == 4 || mat == 2) {
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = (float)entry(mat, k, i, 4 * q + r);
+          out = *reinterpret_cast<const uint4*>(v);
+        } else {  // Ah[i][4q..4q+3], then Al[i][4q..4q+3]
+          bf16_t v[8];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const double e = entry(mat, k, i, 4 * q + r);
+            const bf16_t hi = from_f32<bf16_t>((float)e);
+            v[r] = hi;
+            v[4 + r] = from_f32<bf16_t>((float)(e - (double)to_f32(hi)));
+          }
+          out = *reinterpret_cast<const uint4*>(v);
+        }
+        st_dev16(a.tab + ((size_t)(d0u + k) * 3 + mat) * 64 + l, out);
+      } else {
+        const int km = t - 4 * 3 * 64, k = km >> 3, m = km & 7;
+        const double2 mu = pw[km * 17 + CHUNK], la = pw[km * 17 + 1], lt = pw[km * 17 + jt], l2 = l256[km];
+        float2* s = a.scal + ((size_t)(d0u + k) * 8 + m) * 4;
+        st_dev16(s, make_uint4(__float_as_uint((float)mu.x), __float_as_uint((float)mu.y),
+                               __float_as_uint((float)l2.x), __float_as_uint((float)l2.y)));
+        st_dev16(s + 2, make_uint4(__float_as_uint((float)la.x), __float_as_uint((float)la.y),
+                                   __float_as_uint((float)lt.x), __float_as_uint((float)lt.y)));
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // the unit's stores have completed
+  }
+}
+
+// S = V x of a wave's four channels (xv: their activation operands), moved so
+// that lane (c, k) holds component c of channel k, chunk n in S[n].  The MFMA
+// leaves component c of chunks 4q .. 4q+3 of channel k in lane (c, q) of R[k];
+// exchanging rows of 16 lanes between the four results (two 32-lane and two
+// 16-lane swaps per register) gives lane (c, q) of R[j] the chunks 4j .. 4j+3
+// of channel q.
+template <typename TX>
+__device__ __forceinline__ void chunk_states(const typename FPath<TX>::XOp (&xv)[4],
+                                             const typename FPath<TX>::AOp (&vop)[4], float (&S)[16]) {
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  f4 R[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) R[k] = FPath<TX>::mma_t(xv[k], vop[k], zero);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const uint32_t v0 = __float_as_uint(R[0][r]), v1 = __float_as_uint(R[1][r]);
+    const uint32_t v2 = __float_as_uint(R[2][r]), v3 = __float_as_uint(R[3][r]);
+    const auto s02 = __builtin_amdgcn_permlane32_swap(v0, v2, false, false);
+    const auto s13 = __builtin_amdgcn_permlane32_swap(v1, v3, false, false);
+    const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+    const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+    S[r] = __uint_as_float(s01[0]);
+    S[4 + r] = __uint_as_float(s01[1]);
+    S[8 + r] = __uint_as_float(s23[0]);
+    S[12 + r] = __uint_as_float(s23[1]);
+  }
+}
+
+// Wave-uniform bounded poll of one flag until it reads `want`; false on give-up
+// (after SPIN_LIMIT polls, or at once once any work-group of the call has given
+// up, word gave_up, so that a broken call ends after one wait limit rather than
+// one per tile).
+__device__ __forceinline__ bool wait_flag_eq(const uint32_t* f, uint32_t want, const uint32_t* gave_up) {
+  for (uint32_t it = 0; it < SPIN_LIMIT; ++it) {
+    if (ld_flag(f) == want) return true;
+    if ((it & 63) == 63 && ld_flag(gave_up) != 0) return false;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return false;
+}
+
 template <typename TX, typename TY>
-__global__ __launch_bounds__(SegGeo<TX>::NT, 1) void fwd_seg_kernel(FwdArgs a) {
-  typedef SegGeo<TX> G;
+__global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(StreamArgs a) {
+  typedef StreamGeo<TX> G;
   typedef FPath<TX> PT;
-  constexpr int DW = G::DW, NW = G::NW, CW = G::CW, NG = G::NG, NBUF = G::NBUF, XE = (int)sizeof(TX);
-  constexpr int NM = fwd_mats(1);  // T, V, U
+  constexpr int DW = G::DW, NW = G::NW, NT = G::NT, NQ = G::NQ, LW = G::LW, GPL = G::GPL, NBUF = G::NBUF;
+  constexpr int XE = (int)sizeof(TX), HR = G::HR, HKS = G::HKS;
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
-  __shared__ __align__(16) char xb[NBUF][XLay<XE>::BYTES];  // the segment's tile buffers
-  // per wave and slot: the chunk states of one channel [component][chunk]
-  // (rows of HSTR floats) and, in the 4 spare floats of each row, the block
-  // aggregates [component][block]
-  constexpr int HSTR = 20;
-  constexpr int SLOTS = G::SLOTS;
-  __shared__ __align__(16) float s_h[NW][SLOTS][16 * HSTR];
-  // per (channel, row q), last tile of a row: the drive part of the state at
-  // t = L-1, then the state entering its chunk
-  __shared__ __align__(16) f4 s_tail[DW * 4], s_hn[DW * 4];
-  __shared__ uint32_t s_tk;
+  __shared__ __align__(16) char xb[NBUF][G::BUFB];
+  __shared__ __align__(16) f4 sA[NQ][64];  // pass 1's A: control lane l, slot = wave within the quarter
+  __shared__ __align__(16) f4 sE[NQ][64];  // the entering states from the control waves
+  __shared__ __align__(16) float2 sL2[NQ][64][4];  // control lanes: lambda^256 as (Re, -+Im)
+  __shared__ __align__(16) f4 sI[NQ][64];  // control lanes: the own previous tile's I
+  __shared__ uint32_t s_tk[NBUF];          // tile (ticket) of each buffer slot
+  __shared__ uint32_t s_u[4];
 
   const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform (scalar)
-  const int ln = lane & 15, lq = lane >> 4;                   // chunk, mode pair (2 lq, 2 lq + 1)
-  const int nchains = (int)(a.B * a.NB);
-  const f4 zero = {0.f, 0.f, 0.f, 0.f}, one = {1.f, 0.f, 1.f, 0.f};
-  const char* tab = reinterpret_cast<const char*>(a.tab);
-  const int c0 = wave * CW;  // this wave's first channel within the tile
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ln = lane & 15, lq = lane >> 4;  // MFMA lane (i, q); scan lane (component ln, channel lq)
+  const int c0 = wave * 4;                   // this wave's first channel in the tile
+  const int Q = wave >> 2, wq = wave & 3;    // quarter (16 channels) and slot in it
+  const bool is_ctl = wave < NQ, is_ld = wave >= NQ && wave < NQ + LW;
+  const int chain = (int)(blockIdx.x % (unsigned)a.nchains);
+  const int64_t b = chain / a.NB;
+  const int blk = chain % a.NB;
+  const int d0 = blk * DW;
+  const int64_t P = a.P;
+  const uint32_t ep = ld_flag(a.hdr + 1);
+  const uint32_t MK_A = 2 * ep + 1, MK_I = 2 * ep + 2, MK_T = ep + 1;
+  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  const bool full_block = a.fast_io && d0 + DW <= a.D;
+  auto tile_full = [&](int64_t p) { return full_block && (p + 1) * TILE_T <= a.L; };
 
-  // segment of the ticket: time-major over the chains, so that every segment's
-  // predecessors in its row hold smaller tickets (taken by running work-groups)
-  if (tid == 0) s_tk = atomicAdd(a.ticket, 1u);
+  // ---- arrival, the first tile, the first table claim -------------------------
+  if (tid == 0) {
+    const uint32_t arr = atomicAdd(a.hdr + 2, 1u);
+    const uint32_t t0 = atomicAdd(a.ticket + chain, 1u);
+    const uint32_t cl = atomicAdd(a.claim + blk, 1u);
+    s_u[0] = arr;
+    s_tk[0] = t0;
+    s_u[1] = cl;
+  }
   __syncthreads();
-  const int64_t tk = (int64_t)__builtin_amdgcn_readfirstlane(s_tk);
-  // a ticket past the last segment means the counter was not reset for this
-  // launch: flag it and touch nothing (uniform over the work-group)
-  if (tk >= (int64_t)nchains * a.seg_per_chain) {
-    if (tid == 0) atomicOr(a.error, 2u);
+  // more arrivals than work-groups: the counters were not in their initial
+  // state (workspace not zeroed, or changed meanwhile); touch nothing
+  if (s_u[0] >= gridDim.x) {
+    if (tid == 0) atomicOr(a.hdr, 2u);
     return;
   }
-  const int64_t seg = tk / nchains;
-  const int chain = (int)(tk % nchains);
-  const int64_t b = chain / a.NB;
-  const int d0 = (chain % a.NB) * DW;
-  const int64_t pb = seg * a.seg_len;                                 // first tile
-  const int nt = (int)(a.P - pb < a.seg_len ? a.P - pb : a.seg_len);  // tiles of the segment
-  const bool last_seg = (seg == a.seg_per_chain - 1);
-  const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
+  if (is_ld) {
+    const int64_t p = s_tk[0];
+    if (p < P && tile_full(p)) {
+#pragma unroll
+      for (int i = 0; i < GPL; ++i)
+        dma_group<TX>(xb[0], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, lane,
+                      (wave - NQ) + LW * i);
+    }
+  }
 
-  // the lane's operand rows (the lane offset recomputed at each use rather than
-  // kept live in a 64-bit register)
-  auto tab_of = [&](int k) {
-    int l = lane;
-    asm volatile("" : "+v"(l));
-    return tab + (size_t)(d0 + c0 + k) * NM * TAB_MAT_BYTES + (uint32_t)l * TAB_LANE_BYTES;
-  };
-  auto scal_of = [&](int k) { return a.scal + (size_t)(d0 + c0 + k) * a.Mp + 2 * lq; };
-  // tiles 0 .. nfull-1 of the segment are full: whole channel block, aligned
-  // rows, all TILE_T steps inside the sequence (only a row's last tile can be short)
-  const int nfull = __builtin_amdgcn_readfirstlane(
-      (a.fast_io && d0 + DW <= a.D) ? ((pb + nt) * TILE_T <= a.L ? nt : nt - 1) : 0);
-  auto tile_full = [&](int t) { return t < nfull; };
-  // Tile t of the segment into buffer u.  Full tiles go straight to LDS, each
-  // wave loading row groups wave, wave + NW, ... (while the memory system is
-  // busy, issuing a load holds the wave; spread over all waves, that time is the
-  // same for each).  Other tiles are copied by all threads when they are used.
-  constexpr int LPT = TILE_T / 8 / NW;  // row groups per wave and tile (loads, stores)
-  // this wave's row group i (< LPT) of tile t into buffer u
-  auto request_group = [&](int t, int u, int i) {
-    if (t < nt && tile_full(t))
-      dma_group<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, lane, wave + NW * i);
-  };
-  auto request = [&](int t, int u) {
+  // ---- operand tables: build the units claimed, then wait for the ones read --
+  for (uint32_t u = s_u[1]; u < (uint32_t)NW;) {
+    build_unit<TX>(a, d0 + 4 * (int)u, xb[NBUF - 1], tid, wave);
+    __syncthreads();
+    if (tid == 0) {
+      st_flag(a.tflag + (size_t)blk * NW + u, MK_T);
+      s_u[1] = atomicAdd(a.claim + blk, 1u);
+    }
+    __syncthreads();
+    u = s_u[1];
+  }
+  {
+    bool ok = wait_flag_eq(a.tflag + (size_t)blk * NW + wave, MK_T, a.hdr + 4);
+    if (is_ctl)  // control wave c reads the constants of quarter c: units 4c .. 4c+3
+      for (int j = 0; j < 4; ++j) ok = ok && wait_flag_eq(a.tflag + (size_t)blk * NW + 4 * wave + j, MK_T, a.hdr + 4);
+    if (!ok && lane == 0) {
+      atomicOr(a.hdr, 1u);
+      atomicOr(a.hdr + 4, 1u);
+    }
+  }
+  // The second and third tiles.  A tile's A is published only once its
+  // work-group has finished the tile before it, so tiles of one chain that
+  // follow each other must not sit in one work-group's queue: each of these
+  // claims waits (briefly, bounded) until every work-group of the chain has made
+  // its previous claim, which leaves the tiles a work-group holds one round of
+  // the chain's work-groups apart.  Tickets remain first come, first served, so
+  // a tile waited for always belongs to a running work-group.
+  if (tid == 0) {
+    const uint32_t G = gridDim.x / (uint32_t)a.nchains;
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) request_group(t, u, i);
-  };
-  // the row groups a wave issues after its channel k: i with i CW / LPT == k
-  auto groups_at = [&](int k, auto&& f) {
+    for (int k = 1; k < 3; ++k) {
+      for (uint32_t n = 0; n < CLAIM_WAIT && ld_flag(a.ticket + chain) < (uint32_t)k * G; ++n)
+        __builtin_amdgcn_s_sleep(2);
+      s_tk[k] = atomicAdd(a.ticket + chain, 1u);
+    }
+  }
+  typename PT::AOp vop[4], top[4];
+  f4 uop[4];
 #pragma unroll
-    for (int i = 0; i < LPT; ++i)
-      if ((i * CW) / LPT == k) f(i);
-  };
-  auto full_in = [&](int lo, int hi) {  // full tiles among lo .. hi
-    int n = 0;
-    for (int u = lo; u <= hi; ++u) n += tile_full(u) ? 1 : 0;
-    return n;
-  };
-  // Make tile t in buffer u usable: wait for this wave's share of it, or copy
-  // it; the caller synchronises.  `later` full tiles have been requested after
-  // tile t.  Loads complete in order, so while a load of tile t is pending, so
-  // are the LPT * later loads issued after it: vmcnt(LPT * later) waits for
-  // tile t exactly (pending stores only raise the count, which errs on the
-  // side of waiting).
-  auto arrive = [&](int t, int u, int later) {
-    if (tile_full(t)) {
-      wait_vmcnt(LPT * later);
+  for (int k = 0; k < 4; ++k) {
+    const uint4* tp = a.tab + (size_t)(d0 + c0 + k) * 3 * 64 + lane;
+    top[k] = PT::load_a_u4(ld_dev16(tp));
+    vop[k] = PT::load_a_u4(ld_dev16(tp + 64));
+    const uint4 uu = ld_dev16(tp + 128);
+    uop[k] = f4{__uint_as_float(uu.x), __uint_as_float(uu.y), __uint_as_float(uu.z), __uint_as_float(uu.w)};
+  }
+  // scan constant of lane (component ln, channel lq): mu, as (Re, -+Im)
+  const float2* scl = a.scal + ((size_t)(d0 + c0 + lq) * 8 + (ln >> 1)) * 4;
+  const float sgn = (ln & 1) ? 1.f : -1.f;
+  float mur, mus;
+  {
+    const float2 mu = ld_agent(scl);
+    mur = mu.x, mus = sgn * mu.y;
+  }
+  // control wave c (quarter c): lambda^256 of control lane (ln, lq), slot j (channel
+  // 16 c + 4 j + lq, mode ln / 2), kept in LDS
+  if (is_ctl) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float2 v = ld_agent(a.scal + ((size_t)(d0 + 16 * wave + 4 * j + lq) * 8 + (ln >> 1)) * 4 + 1);
+      sL2[wave][lane][j] = make_float2(v.x, sgn * v.y);
+    }
+  }
+  // every earlier vector memory operation of the wave has completed (the first
+  // tile among them); then the loads of the second and third tiles, counted
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  __syncthreads();
+  uint32_t issued = 0, mark[NBUF] = {0, 0, 0, 0};
+  if (is_ld) {
+#pragma unroll
+    for (int u = 1; u < 3; ++u) {
+      const int64_t p = s_tk[u];
+      if (p < P && tile_full(p)) {
+#pragma unroll
+        for (int i = 0; i < GPL; ++i)
+          dma_group<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, lane,
+                        (wave - NQ) + LW * i);
+        issued += GPL;
+      }
+      mark[u] = issued;
+    }
+  }
+
+  // ---- the tiles ------------------------------------------------------------
+  int64_t p_prev = -1;
+  for (int it = 0;; ++it) {
+    const int u = it & (NBUF - 1);
+    const int64_t p = s_tk[u];
+    if (p >= P) break;
+    const bool full = tile_full(p);
+    const bool lastp = (p == P - 1);
+    char* xt = xb[u];
+    // arrival: this wave's share of a full tile, or a copy of one that is not full
+    if (full) {
+      if (is_ld) wait_vmcnt(SEPY ? 0 : (int)(issued - mark[u]));
     } else {
-      copy_tile<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, (pb + t) * TILE_T, d0, a.L, a.D, tid);
+      copy_tile<TX, NT>(xt, reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, tid);
     }
-  };
+    __syncthreads();
+    // the ticket of the tile three ahead (its buffer holds tile it-1, already stored)
+    uint32_t tk3 = 0;
+    if (tid == 0) tk3 = atomicAdd(a.ticket + chain, 1u);
 
-  // operands and multipliers first, so that waiting for them waits for no tile
-  typename PT::AOp vop[CW];
-#pragma unroll
-  for (int k = 0; k < CW; ++k) vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);
-  // pass 1 weights: mu^(15-n) of the lane's modes (rows [d][j][Mp] of lambda^(16 j)), lambda^256
-  f4 ww[CW], lt[CW];
-#pragma unroll
-  for (int k = 0; k < CW; ++k) {
-    ww[k] = load_f4(a.mpow + ((size_t)(d0 + c0 + k) * CHUNK + (CHUNK - 1 - ln)) * a.Mp + 2 * lq);
-    const ModeScalars* ms = scal_of(k);
-    lt[k] = mode_pair(ms[0].lamT, ms[1].lamT);
-  }
-  // Pass 1 visits the tiles last to first, so that tiles 0 .. R-1 (R =
-  // min(nt, NBUF)) are the ones still in the buffers when pass 2 starts.  Pass
-  // 1's j-th tile (tile nt-1-j) uses buffer j % NBUF; in pass 2 tile t uses
-  // buffer (nt-1-(t % NBUF)) % NBUF, which agrees for t < R, and tile t >= R
-  // follows tile t - NBUF into its buffer.
-  const int R = nt < NBUF ? nt : NBUF;
-  auto buf2 = [&](int t) { return (nt - 1 - (t % NBUF)) % NBUF; };
-  // block aggregate slot of (channel slot kk, component i): 4 floats
-  auto blk = [&](int j, int i) -> float* { return &s_h[wave][j][i * HSTR + 16]; };
-  // The operand loads above are complete before the first tile is requested:
-  // the compiler does not see the tile loads, and a wait it places for an
-  // operand inside the loops would also wait for them.
-  __builtin_amdgcn_s_waitcnt(0);
-  for (int j = 0; j < NBUF && j < nt; ++j) request(nt - 1 - j, j);
-
-  // ---- pass 1: the segment's own end state ---------------------------------
-  // sagg = sum over tiles t and chunks n of lambda^(256 (nt-1-t)) mu^(15-n) S_t[n];
-  // lane-wise, with the weight carried from tile to tile (last tile first)
-  f4 sagg[CW];
-  {
-#pragma unroll
-    for (int k = 0; k < CW; ++k) sagg[k] = zero;
-    for (int j = 0; j < nt; ++j) {
-      const int t = nt - 1 - j;
-      // visits requested so far: 0 .. NBUF-1, then one more per visit from the second on
-      const int last = min((j == 0 ? NBUF - 1 : j + NBUF - 2), nt - 1);
-      arrive(t, j % NBUF, full_in(nt - 1 - last, t - 1));
-      __syncthreads();  // tile t is in; the buffer of the tile visited before it is free
-      // the next request (into the buffer of the tile visited before), spread over the channels
-      const bool req = j >= 1 && j + NBUF - 1 < nt;
-      const int rt = nt - j - NBUF, ru = (j + NBUF - 1) % NBUF;
-      const char* xt = xb[j % NBUF];
-#pragma unroll
-      for (int gr = 0; gr < NG; ++gr) {
-        typename PT::XOp xv[4];
-        PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int k = 4 * gr + kk;
-          sagg[k] = c2fma(ww[k], PT::mma(vop[k], xv[kk], zero), sagg[k]);
-          ww[k] = c2mul(ww[k], lt[k]);
-          if (req) groups_at(k, [&](int i) { request_group(rt, ru, i); });
-        }
-      }
-      if (pb + t == a.P - 1 && a.h_out != nullptr && ln == nstar) {
-        // last tile of the row: sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
-        for (int k = 0; k < CW; ++k) {
-          const ModeScalars* ms = scal_of(k);
-          const f4 lam = mode_pair(ms[0].lam, ms[1].lam);
-          f4 tl = zero;
-          for (int i = 0; i <= jstar; ++i) {
-            const float xr =
-                to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + i) + (c0 + k) * XE));
-            const f4 xin = {xr, 0.f, xr, 0.f};
-            tl = c2fma(lam, tl, xin);
-          }
-          s_tail[(c0 + k) * 4 + lq] = tl;
-        }
-      }
-    }
-  }
-#pragma unroll
-  for (int k = 0; k < CW; ++k) sagg[k] = row_sum(sagg[k]);
-
-  // ---- the state entering the segment (per wave sub-chain) ----------------------
-  // c = lamS^seg h0 + sum_{j<seg} lamS^(seg-1-j) agg_j with lamS = lambda^(256
-  // seg_len): term u = seg-1-j (u = seg: h0) goes to lane u % 16 of every row,
-  // weighted by lamS^(u % 16) and summed over the row; blocks of 16 terms are
-  // combined farthest first by Horner's rule with lamS^16.  The order is fixed
-  // by seg alone, so the result is bitwise reproducible.  Payload words start
-  // as a signalling-NaN pattern, which arithmetic never produces, so a word
-  // that differs from it has been published.
-  const int64_t sub = tk * NW + wave;
-  // payload of sub-chain s, channel k: 8 modes as float2; the lane's pair at 2 lq
-  auto pay = [&](int64_t s, int k) { return ((size_t)s * CW + k) * MODES_PER_GROUP + 2 * lq; };
-  // pass 2's T and U operands and chunk multipliers, requested now (ahead of
-  // the publishing stores, whose completion later loads of the wave wait for)
-  // so that their latency overlaps the wait for the predecessors
-  typename PT::AOp top[CW];
-  typename PT::UOp uop[CW];
-  float2 z1[CW], z4[CW];
-#pragma unroll
-  for (int k = 0; k < CW; ++k) {
-    top[k] = PT::load_a(tab_of(k));
-    uop[k] = PT::u_op(load_f4(tab_of(k) + 2 * TAB_MAT_BYTES));
-    z1[k] = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 1) * a.Mp + (ln >> 1)];
-    z4[k] = a.mpow[((size_t)(d0 + c0 + k) * CHUNK + 4) * a.Mp + (ln >> 1)];
-  }
-  if (!last_seg && ln == 0)  // publish this segment's own end state
-#pragma unroll
-    for (int k = 0; k < CW; ++k) st_agent4(a.pay_agg + pay(sub, k), sagg[k]);
-  f4 carry[CW];
-  {
-    // lamS^n (n the lane's chunk) and lamS^16 of the lane's modes, from the table
-    auto spw = [&](int k, int n) {
-      return load_f4(a.spow + ((size_t)(d0 + c0 + k) * (CHUNK + 1) + n) * a.Mp + 2 * lq);
-    };
-#pragma unroll
-    for (int k = 0; k < CW; ++k) carry[k] = zero;
-    for (int64_t blk = seg / CHUNK; blk >= 0; --blk) {
-      const int64_t u = blk * CHUNK + ln;
-      const float2* src = a.pay_agg + pay(((seg - 1 - u) * nchains + chain) * NW + wave, 0);
-      f4 v[CW];
-      for (uint32_t it = 0;; ++it) {
-        bool ok = true;
-        if (u < seg) {
-#pragma unroll
-          for (int k = 0; k < CW; ++k) {
-            v[k] = ld_agent4(src + (size_t)k * MODES_PER_GROUP);
-            ok = ok && __float_as_uint(v[k][0]) != PAY_EMPTY && __float_as_uint(v[k][1]) != PAY_EMPTY &&
-                 __float_as_uint(v[k][2]) != PAY_EMPTY && __float_as_uint(v[k][3]) != PAY_EMPTY;
-          }
-        }
-        if (__ballot(!ok) == 0) break;
-        if (it >= SPIN_LIMIT) {  // unreachable in ticket order; give up and flag it
-          if (lane == 0) atomicOr(a.error, 1u);
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-#pragma unroll
-      for (int k = 0; k < CW; ++k) {
-        if (u >= seg) {
-          v[k] = zero;
-          if (u == seg && a.h0 != nullptr && d0 + c0 + k < a.D) {
-            const float* h = a.h0 + ((size_t)(b * a.D + d0 + c0 + k) * a.M + 2 * lq) * 2;
-            if (2 * lq < a.M) v[k][0] = h[0], v[k][1] = h[1];
-            if (2 * lq + 1 < a.M) v[k][2] = h[2], v[k][3] = h[3];
-          }
-        }
-        const f4 blk_sum = row_sum(c2mul(spw(k, ln), v[k]));
-        // (the farthest block starts from zero)
-        carry[k] = blk == seg / CHUNK ? blk_sum : c2fma(spw(k, CHUNK), carry[k], blk_sum);
-      }
-    }
-  }
-
-  // ---- pass 2: the chunk scans and the outputs ----------------------------------
-  // S^T = (V x)^T puts component c = ln of chunks 4q .. 4q+3 (q = lq) in lane
-  // (c, q); the partner component (re <-> im of the same mode) is in lane c ^ 1.
-  // Per tile and channel: block aggregates A_q (Horner over the lane's 4
-  // chunks), their exchange through LDS, the block entry states
-  // E_{q+1} = mu^4 E_q + A_q from the tile's entering state E_0, the lane's 4
-  // chunk states from E_q, and their transpose through LDS into the B operand
-  // of y += U H.  A complex factor z acts on a component v with partner p as
-  // Re z v + s Im z p, s = -1 for the real part and +1 for the imaginary part.
-  float cin[CW], m1r[CW], m1s[CW], m4r[CW], m4s[CW];
-  // the entering state as component ln (the fold leaves modes 2 lq, 2 lq + 1 in row lq)
-  if (ln == 0)
-#pragma unroll
-    for (int k = 0; k < CW; ++k) *reinterpret_cast<f4*>(&s_h[wave][0][k * 16 + 4 * lq]) = carry[k];
-  wave_lds_order();
-#pragma unroll
-  for (int k = 0; k < CW; ++k) cin[k] = s_h[wave][0][k * 16 + ln];
-  wave_lds_order();
-#pragma unroll
-  for (int k = 0; k < CW; ++k) {
-    vop[k] = PT::load_a(tab_of(k) + TAB_MAT_BYTES);  // (not held through the carry phase)
-    const float sgn = (ln & 1) ? 1.f : -1.f;
-    m1r[k] = z1[k].x;
-    m1s[k] = sgn * z1[k].y;
-    m4r[k] = z4[k].x;
-    m4s[k] = sgn * z4[k].y;
-  }
-  // z v + (partner): one complex multiply-add on the lane's component
-  auto cstep = [](float zr, float zs, float v, float add) { return cfma_pair(zr, zs, v, add); };
-  // At the top of tile t (after the barrier) all threads store tile t-1's
-  // outputs from its buffer, and the buffer whose stores were issued one tile
-  // earlier (all waves have since passed a barrier, so its LDS reads are done)
-  // takes the next tile.  With float32 outputs leaving from the MFMA registers,
-  // tile t-1's buffer is free at once.
-  constexpr int LAG = SEPY ? 1 : 2;
-  static_assert(NBUF > LAG, "a tile is requested before the tile that follows it into its buffer arrives");
-  // (pass 2's operands are in registers before its first tile load; the wait
-  // also covers the loads of the carry phase)
-  __builtin_amdgcn_s_waitcnt(0);
-  for (int t = 0; t < nt; ++t) {
-    // tiles 0 .. R-1 are still in their buffers from pass 1; before tile t,
-    // tiles up to t - 1 - LAG + NBUF have been requested
-    if (t >= R) arrive(t, buf2(t), full_in(t + 1, min(t - 1 - LAG + NBUF, nt - 1)));
-    __syncthreads();  // tile t is in; tile t-1's outputs are in its buffer
-    // tile t-1's stores and the next request, spread over the channels (a tile
-    // that is not full is stored here by all threads)
-    const bool stf = !SEPY && t >= 1 && tile_full(t - 1);
-    if (!SEPY && t >= 1 && !tile_full(t - 1))
-      store_tile_part<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(t - 1)], b, (pb + t - 1) * TILE_T, d0, a.L, a.D,
-                          tid);
-    const bool req = t >= LAG;
-    const int rt = t - LAG + NBUF, ru = req ? buf2(t - LAG) : 0;
-    auto side = [&](int k) {
-      groups_at(k, [&](int i) {
-        if (stf)
-          store_group<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(t - 1)], b, (pb + t - 1) * TILE_T, d0, a.L, a.D,
-                          lane, wave + NW * i);
-        if (req) request_group(rt, ru, i);
-      });
-    };
-    char* xt = xb[buf2(t)];
-    const int64_t p = pb + t;
-#pragma unroll
-    for (int gr = 0; gr < NG; ++gr) {
+    // ---- pass 1: S = V x, moved so that lane (c, k) holds component c of channel
+    // k; A = sum_n mu^(15-n) S[n], the tile's end state from a zero start
+    float A;
+    {
       typename PT::XOp xv[4];
-      PT::gather4(xt, c0 + 4 * gr, ln, lq, xv);
-      f4 acc[4];
-      // y of channel k from its transposed states: lane (n, q) takes components
-      // 4q .. 4q+3 of chunk n
-      auto apply = [&](int kk, int k, const float* sh) {
-        f4 hb;
+      float S[16];
+      PT::gather4(xt, c0, ln, lq, xv);
+      chunk_states<TX>(xv, vop, S);
+      A = S[0];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) hb[j] = sh[(4 * lq + j) * HSTR + ln];
-        acc[kk] = PT::mma_u(uop[k], hb, PT::mma(top[k], xv[kk], zero));
-        if (p == a.P - 1 && ln == nstar) s_hn[(c0 + k) * 4 + lq] = hb;  // state entering chunk nstar
-      };
-      // SLOTS channels at a time: block aggregates (A_q, into the spare
-      // columns of the channel's slot), block entry states E_q, chunk entry
-      // states (into the slot, transposed on the way out), then y
+      for (int n = 1; n < 16; ++n) A = cfma_pair(mur, mus, A, S[n]);
+    }
+    // last tile of the chain: sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
+    float tail = 0.f;
+    if (lastp && a.h_out != nullptr) {
+      const float2 la = ld_agent(scl + 2);
+      for (int j = 0; j <= jstar; ++j) {
+        const float xj = to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + j) + (c0 + lq) * XE));
+        tail = cfma_pair(la.x, sgn * la.y, tail, (ln & 1) ? 0.f : xj);
+      }
+    }
+    reinterpret_cast<float*>(&sA[Q][lane])[wq] = A;
+    __syncthreads();
+
+    // ---- carry: control waves publish A, fold the entering state, publish I ----
+    if (is_ctl) {
+      const int QC = wave;  // the quarter this control wave carries
+      const f4 Av = sA[QC][lane];
+      const size_t slot = ((size_t)chain * P + p) * NQ + QC;
+      st_dev16(a.agg + slot * 64 + lane, __builtin_bit_cast(uint4, Av));
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      if (lane == 0) st_flag(a.flag + slot, MK_A);
+      f4 E = zero;
+      if (p == 0) {
+        if (a.h0 != nullptr) {
 #pragma unroll
-      for (int k0 = 0; k0 < 4; k0 += SLOTS) {
-        f4 sk[SLOTS];
-#pragma unroll
-        for (int j = 0; j < SLOTS; ++j) {
-          const int kk = k0 + j, k = 4 * gr + kk;
-          sk[j] = PT::mma_t(xv[kk], vop[k], zero);
-          float ag = sk[j][0];
-#pragma unroll
-          for (int r = 1; r < 4; ++r) ag = cstep(m1r[k], m1s[k], ag, sk[j][r]);
-          blk(j, ln)[lq] = ag;  // A_lq of component ln
-          side(k);
-        }
-        wave_lds_order();
-#pragma unroll
-        for (int j = 0; j < SLOTS; ++j) {
-          const int kk = k0 + j, k = 4 * gr + kk;
-          const f4 A = *reinterpret_cast<const f4*>(blk(j, ln));
-          // E_0 = c, E_{q+1} = mu^4 E_q + A_q; E_4 enters the next tile
-          float e = cin[k], eq = e;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            e = cstep(m4r[k], m4s[k], e, A[q]);
-            if (lq == q + 1) eq = e;
+          for (int j = 0; j < 4; ++j) {
+            const int d = d0 + 16 * QC + 4 * j + lq, m = ln >> 1;
+            if (d < a.D && m < a.M) E[j] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
           }
-          cin[k] = e;
-          // states entering chunks 4 lq .. 4 lq + 3
-          f4 h;
-          h[0] = eq;
+        }
+      } else {
+        // the nearest stop: the own previous tile, or a tile with I published;
+        // every tile between it and this one must have A published
+        int s = -1;
+        for (uint32_t n = 0;; ++n) {
+          const int64_t q = p - 1 - lane;
+          bool stop = false, ready = true;
+          if (p_prev >= 0 && q == p_prev) {
+            stop = true;
+          } else if (q > p_prev && q >= 0) {
+            const uint32_t f = ld_flag(a.flag + ((size_t)chain * P + q) * NQ + QC);
+            stop = f == MK_I;
+            ready = f == MK_A || f == MK_I;
+          }
+          const uint64_t stops = __ballot(stop), notready = __ballot(!ready);
+          if (stops != 0) {
+            const int s0 = __builtin_ctzll(stops);
+            if ((notready & ((1ull << s0) - 1)) == 0) {
+              s = s0;
+              break;
+            }
+          }
+          if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        if (s < 0) {
+          if (lane == 0) {  // gave up: the fold starts from zero
+            atomicOr(a.hdr, 1u);
+            atomicOr(a.hdr + 4, 1u);
+          }
+        } else {
+          const int64_t qs = p - 1 - s;
+          if (p_prev >= 0 && qs == p_prev) {
+            E = sI[QC][lane];
+          } else {
+            E = __builtin_bit_cast(f4, ld_dev16(a.inc + (((size_t)chain * P + qs) * NQ + QC) * 64 + lane));
+          }
+          // E <- lambda^256 E + A_q for q = qs+1 .. p-1, FB loads at a time
+          constexpr int FB = 4;
+          for (int jb = s - 1; jb >= 0; jb -= FB) {
+            f4 Aq[FB];
 #pragma unroll
-          for (int r = 1; r < 4; ++r) h[r] = cstep(m1r[k], m1s[k], h[r - 1], sk[j][r - 1]);
-          *reinterpret_cast<f4*>(&s_h[wave][j][ln * HSTR + 4 * lq]) = h;
+            for (int i = 0; i < FB; ++i) {
+              const int jj = jb - i < 0 ? 0 : jb - i;  // clamped: an extra load of a published state
+              Aq[i] = __builtin_bit_cast(f4, ld_dev16(a.agg + (((size_t)chain * P + (p - 1 - jj)) * NQ + QC) * 64 + lane));
+            }
+#pragma unroll
+            for (int i = 0; i < FB; ++i) {
+              if (jb - i >= 0) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                  const float2 l2 = sL2[QC][lane][j];
+                  E[j] = cfma_pair(l2.x, l2.y, E[j], Aq[i][j]);
+                }
+              }
+            }
+          }
+        }
+      }
+      f4 I;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float2 l2 = sL2[QC][lane][j];
+        I[j] = cfma_pair(l2.x, l2.y, E[j], Av[j]);
+      }
+      st_dev16(a.inc + slot * 64 + lane, __builtin_bit_cast(uint4, I));
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      if (lane == 0) st_flag(a.flag + slot, MK_I);
+      sE[QC][lane] = E;
+      sI[QC][lane] = I;
+    }
+    p_prev = p;
+    if (tid == 0) s_tk[(it + 3) & (NBUF - 1)] = tk3;
+    __syncthreads();
+
+    // ---- pass 2: chunk entering states, y = T x + U H -------------------------
+    // (x is still in the tile buffer: S and the operands are formed again rather
+    // than held in registers through the carry phase)
+    typename PT::XOp xv[4];
+    float S[16];
+    PT::gather4(xt, c0, ln, lq, xv);
+    chunk_states<TX>(xv, vop, S);
+    {
+      float h = reinterpret_cast<const float*>(&sE[Q][lane])[wq];
+      float hn = 0.f;
+#pragma unroll
+      for (int n = 0; n < 16; ++n) {
+        if (n == nstar) hn = h;
+        const float nx = cfma_pair(mur, mus, h, S[n]);
+        S[n] = h;  // now the state entering chunk n
+        h = nx;
+      }
+      if (lastp && a.h_out != nullptr) {
+        // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
+        const float2 lt = ld_agent(scl + 3);
+        const float hl = cfma_pair(lt.x, sgn * lt.y, hn, tail);
+        const int d = d0 + c0 + lq, m = ln >> 1;
+        if (d < a.D && m < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)] = hl;
+      }
+    }
+    f4 acc[4];
+    {
+      // H through LDS (the buffer that takes the tile three ahead, free until
+      // the end of this tile), HR channels per round: lane (c, k) writes
+      // component c of chunk n at [k][n][c], lane (n, q) reads components
+      // 4q .. 4q+3 of chunk n
+      float* hs = reinterpret_cast<float*>(xb[(it + 3) & (NBUF - 1)]) + wave * HR * HKS;
+#pragma unroll
+      for (int r0 = 0; r0 < 4; r0 += HR) {
+        if (lq >= r0 && lq < r0 + HR) {
+#pragma unroll
+          for (int n = 0; n < 16; ++n) hs[(lq - r0) * HKS + n * 16 + ln] = S[n];
         }
         wave_lds_order();
 #pragma unroll
-        for (int j = 0; j < SLOTS; ++j) apply(k0 + j, 4 * gr + k0 + j, s_h[wave][j]);
+        for (int kk = 0; kk < HR; ++kk) {
+          const int k = r0 + kk;
+          const f4 hb = *reinterpret_cast<const f4*>(&hs[kk * HKS + ln * 16 + 4 * lq]);
+          acc[k] = mma_f32(uop[k], hb, PT::mma(top[k], xv[k], zero));
+        }
         wave_lds_order();
       }
-      wave_lds_order();
-      if (SEPY)
-        put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4,
-                      d0 + c0 + 4 * gr, a.L, a.D);
-      else
-        put_y4<TY>(xt, c0 + 4 * gr, ln, lq, acc);
     }
-  }
-  __syncthreads();  // the last tile's outputs are in its buffer
-  if (!SEPY) {
-    if (tile_full(nt - 1)) {
+    if (SEPY)
+      put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4, d0 + c0, a.L, a.D);
+    else
+      put_y4<TY>(xt, c0, ln, lq, acc);
+    __syncthreads();
+
+    // ---- load waves: the tile three ahead, then this tile's rows --------------
+    if (is_ld) {
+      const int u3 = (it + 3) & (NBUF - 1);
+      const int64_t p3 = s_tk[u3];
+      if (p3 < P && tile_full(p3)) {
 #pragma unroll
-      for (int i = 0; i < LPT; ++i)
-        store_group<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(nt - 1)], b, (pb + nt - 1) * TILE_T, d0, a.L, a.D,
-                        lane, wave + NW * i);
-    } else {
-      store_tile_part<TY>(reinterpret_cast<TY*>(a.y), xb[buf2(nt - 1)], b, (pb + nt - 1) * TILE_T, d0, a.L, a.D,
-                          tid);
+        for (int i = 0; i < GPL; ++i)
+          dma_group<TX>(xb[u3], reinterpret_cast<const TX*>(a.x), b, p3 * TILE_T, d0, a.L, a.D, lane,
+                        (wave - NQ) + LW * i);
+        issued += GPL;
+      }
+      mark[u3] = issued;
+      if (!SEPY && full) {
+#pragma unroll
+        for (int i = 0; i < GPL; ++i)
+          store_group<TY>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, lane, (wave - NQ) + LW * i);
+        issued += GPL;
+      }
     }
+    if (!SEPY && !full)
+      store_tile_part<TY, NT>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, tid);
   }
-  if (pb + nt == a.P && a.h_out != nullptr && lane < 4 * CW) {
-    // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar,
-    // plus the drive part from pass 1 (the wave's own entries)
-    const int k = lane >> 2, r = lane & 3, d = d0 + c0 + k;
-    const ModeScalars* ms = a.scal + (size_t)d * a.Mp + 2 * r;
-    const f4 hl = c2fma(mode_pair(ms[0].lamTail, ms[1].lamTail), s_hn[(c0 + k) * 4 + r], s_tail[(c0 + k) * 4 + r]);
-    if (d < a.D) {
-      float* ho = a.h_out + ((size_t)(b * a.D + d) * a.M + 2 * r) * 2;
-      if (2 * r < a.M) ho[0] = hl[0], ho[1] = hl[1];
-      if (2 * r + 1 < a.M) ho[2] = hl[2], ho[3] = hl[3];
+
+  // ---- the last work-group to finish resets the counters for the next call --
+  __syncthreads();
+  if (tid == 0) s_u[2] = atomicAdd(a.hdr + 3, 1u);
+  __syncthreads();
+  if (s_u[2] == gridDim.x - 1) {
+    for (int i = tid; i < a.nchains; i += NT) st_flag(a.ticket + i, 0u);
+    for (int i = tid; i < a.NB; i += NT) st_flag(a.claim + i, 0u);
+    if (tid == 0) {
+      st_flag(a.hdr + 2, 0u);
+      st_flag(a.hdr + 3, 0u);
+      st_flag(a.hdr + 4, 0u);
+      st_flag(a.hdr + 1, ep + 1);
     }
   }
 }
@@ -1467,19 +1588,25 @@ hipError_t launch_fwd_carry(const Geometry& g, const FwdArgs& a, hipStream_t st)
   return hipGetLastError();
 }
 
+int fwd_stream_grid(int64_t nchains, int64_t P, int num_cus) {
+  // every work-group of a chain resident at once (one per compute unit), and
+  // no more of them than the chain has tiles; one per chain when there are more
+  // chains than compute units (a chain is then served by one work-group alone)
+  if (nchains >= num_cus) return (int)nchains;
+  int64_t per = num_cus / nchains;
+  if (per > P) per = P;
+  if (per < 1) per = 1;
+  return (int)(nchains * per);
+}
+
 template <typename TX, typename TY>
-hipError_t launch_fwd_segments(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
-                               hipEvent_t ev1) {
-  const dim3 grid((unsigned)(g.B * g.NB * a.seg_per_chain)), block(SegGeo<TX>::NT);
-  launch_timed(fwd_seg_kernel<TX, TY>, grid, block, st, ev0, ev1, a);
+hipError_t launch_fwd_stream(const StreamArgs& a, int grid, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  launch_timed(fwd_stream_kernel<TX, TY>, dim3((unsigned)grid), dim3(StreamGeo<TX>::NT), st, ev0, ev1, a);
   return hipGetLastError();
 }
-template hipError_t launch_fwd_segments<float, float>(const Geometry&, const FwdArgs&, hipStream_t,
-                                                      hipEvent_t, hipEvent_t);
-template hipError_t launch_fwd_segments<bf16_t, bf16_t>(const Geometry&, const FwdArgs&, hipStream_t,
-                                                        hipEvent_t, hipEvent_t);
-template hipError_t launch_fwd_segments<bf16_t, float>(const Geometry&, const FwdArgs&, hipStream_t,
-                                                       hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_stream<float, float>(const StreamArgs&, int, hipStream_t, hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_stream<bf16_t, bf16_t>(const StreamArgs&, int, hipStream_t, hipEvent_t, hipEvent_t);
+template hipError_t launch_fwd_stream<bf16_t, float>(const StreamArgs&, int, hipStream_t, hipEvent_t, hipEvent_t);
 
 template <typename TX, typename TY>
 hipError_t launch_fwd_apply(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,

@@ -54,6 +54,38 @@ struct FwdArgs {
   float2* pay_agg;   // per (segment, wave) [channels][8 modes]: the segment's own end state
 };
 
+// Single-pass forward (M <= 8): problem, parameters and the workspace regions.
+// Flags hold the call's epoch (hdr[1]): a tile state is published with
+// 2 epoch + 1 (its end state from zero, A) and 2 epoch + 2 (also its inclusive
+// end state, I); a table unit with epoch + 1.
+struct StreamArgs {
+  const void* x;
+  void* y;
+  int64_t B, L;
+  int D, M;
+  int NB;              // channel blocks of DW channels
+  int nchains;         // B * NB
+  int64_t P;           // tiles per chain
+  int last_len;        // valid steps of a chain's last tile
+  int fast_io;         // x and y 16-byte aligned and rows a multiple of 16 bytes
+  const float* gamma;
+  const float* omega;
+  const float* amp;
+  const float* phase;
+  const float* h0;     // [B][D][M][2] or null
+  float* h_out;        // [B][D][M][2] or null
+  uint32_t* hdr;       // [0] status (bit 0: a wait gave up, bit 1: stale counters), [1] epoch,
+                       // [2] arrived work-groups, [3] finished work-groups, [4] a wait of this call gave up
+  uint32_t* ticket;    // [nchains] next tile of each chain
+  uint32_t* claim;     // [NB] next table unit of each channel block
+  uint32_t* tflag;     // [NB][DW / 4] table unit published
+  uint32_t* flag;      // [nchains][P][DW / 16] tile state published
+  uint4* tab;          // [NB DW][3][64] T, V, U in lane order (16 bytes per lane)
+  float2* scal;        // [NB DW][8][4] mu = lambda^16, lambda^256, lambda, lambda^(jstar+1)
+  uint4* agg;          // [nchains][P][DW / 16][64] A (four floats per control lane)
+  uint4* inc;          // [nchains][P][DW / 16][64] I
+};
+
 struct BwdArgs {
   const void* x;
   const void* dy;
@@ -82,9 +114,10 @@ hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st,
 
 hipError_t launch_fwd_carry(const Geometry& g, const FwdArgs& a, hipStream_t st);
 
+// Work-groups per call of the single-pass forward, and its launch.
+int fwd_stream_grid(int64_t nchains, int64_t P, int num_cus);
 template <typename TX, typename TY>
-hipError_t launch_fwd_segments(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,
-                               hipEvent_t ev1);
+hipError_t launch_fwd_stream(const StreamArgs& a, int grid, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1);
 
 template <typename TX, typename TY>
 hipError_t launch_fwd_apply(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,

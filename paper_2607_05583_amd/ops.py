@@ -62,17 +62,44 @@ def workspace_bytes(op: int, act_dtype: torch.dtype, B: int, L: int, D: int, M: 
 
 
 def _workspace(op, act_dtype, B, L, D, M, device, ws=None):
+    """The caller's workspace (checked for size), or a new one.  A forward
+    workspace must be zero before its first forward call (the calls keep it
+    reusable), so a new one is zero-filled."""
     n = workspace_bytes(op, act_dtype, B, L, D, M)
     if ws is not None:
         if ws.numel() * ws.element_size() < n:
             raise ValueError(f"workspace too small: need {n} bytes")
         return ws, n
-    return torch.empty(max(n, 1), dtype=torch.uint8, device=device), n
+    alloc = torch.zeros if op == RES_OP_FWD else torch.empty
+    return alloc(max(n, 256), dtype=torch.uint8, device=device), n
+
+
+def forward_workspace(act_dtype, B, L, D, M, device):
+    """A zero-filled forward workspace for sizes (B, L, D, M), reusable across calls."""
+    return torch.zeros(max(workspace_bytes(RES_OP_FWD, act_dtype, B, L, D, M), 256), dtype=torch.uint8,
+                       device=device)
+
+
+def resonator_fwd_status(ws) -> int:
+    """The forward status word of workspace ``ws`` (bit 0: a bounded wait gave up,
+    bit 1: stale counters), read and cleared; synchronises the current stream."""
+    _dev(ws, "ws")
+    st = ctypes.c_uint32(0)
+    check(_lib.lib().resonator_fwd_status(_ptr(ws), ctypes.byref(st), _stream(ws.device)))
+    return int(st.value)
+
+
+# When set (the GPU tests set it), every resonator_mix_fwd reads its workspace's
+# status word after the call (a synchronisation) and raises if it is not zero.
+CHECK_FWD_STATUS = False
 
 
 def resonator_mix_fwd(x, gamma, omega, amp, phase, h0=None, out_dtype=None, return_state=False,
-                      out=None, ws=None):
-    """y = causal resonant mixing of x (and the terminal state if return_state)."""
+                      out=None, ws=None, h_out=None):
+    """y = causal resonant mixing of x (and the terminal state if return_state).
+
+    ``h_out`` [B, D, M, 2] float32 receives the terminal state (it may be the
+    ``h0`` tensor itself: the state is then advanced in place)."""
     _dev(x, "x")
     if x.dim() != 3:
         raise ValueError("x must be [B, L, D]")
@@ -82,7 +109,12 @@ def resonator_mix_fwd(x, gamma, omega, amp, phase, h0=None, out_dtype=None, retu
     out_dtype = x.dtype if out_dtype is None else out_dtype
     y = out if out is not None else torch.empty((B, L, D), dtype=out_dtype, device=x.device)
     _dev(y, "out")
-    h_out = torch.empty((B, D, M, 2), dtype=torch.float32, device=x.device) if return_state else None
+    if h_out is not None:
+        _dev(h_out, "h_out")
+        if h_out.dtype != torch.float32 or tuple(h_out.shape) != (B, D, M, 2):
+            raise ValueError("h_out must be float32 [B, D, M, 2]")
+    elif return_state:
+        h_out = torch.empty((B, D, M, 2), dtype=torch.float32, device=x.device)
     if h0 is not None:
         _dev(h0, "h0")
         if h0.dtype != torch.float32 or tuple(h0.shape) != (B, D, M, 2):
@@ -91,6 +123,11 @@ def resonator_mix_fwd(x, gamma, omega, amp, phase, h0=None, out_dtype=None, retu
     check(_lib.lib().resonator_mix_fwd(
         _ptr(x), _code(x), _ptr(y), _code(y), B, L, D, M, _ptr(gamma), _ptr(omega), _ptr(amp),
         _ptr(phase), _ptr(h0), _ptr(h_out), _ptr(w), n, _stream(x.device)))
+    if CHECK_FWD_STATUS and not torch.cuda.is_current_stream_capturing():
+        st = resonator_fwd_status(w)
+        if st != 0:
+            raise _lib.ResonatorError(_lib.RES_ERR_HIP, f"forward status word {st:#x} (bit 0: a wait gave up, "
+                                                        "bit 1: stale workspace counters)")
     return (y, h_out) if return_state else y
 
 
@@ -281,12 +318,18 @@ def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
     x = None to skip dW, W = None to skip dx."""
     ref = x if x is not None else dy
     _dev(dy, "dy")
+    _code(dy)
     d_out = dy.shape[-1]
     N = dy.numel() // d_out
-    out = []
     if W is not None:
         _dev(W, "W")
+        if W.dtype != dy.dtype or W.dim() != 3 or W.shape[0] * W.shape[2] != d_out:
+            raise ValueError("W must be [G, d_in/G, d_out/G] of dy's dtype")
         G, di, dq = W.shape
+        if dx is not None:
+            _dev(dx, "dx")
+            if dx.dtype != dy.dtype or dx.numel() != N * G * di:
+                raise ValueError("dx must have dy's dtype and [N, d_in] elements")
         if dx is None:
             dx = torch.empty(dy.shape[:-1] + (G * di,), dtype=dy.dtype, device=dy.device)
         check(_lib.lib().resonator_grouped_linear_bwd_data(_ptr(dy), _ptr(W), _code(dy), _ptr(dx), N, G * di, d_out, G,
@@ -294,11 +337,19 @@ def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
     if x is not None:
         _dev(x, "x")
         d_in = x.shape[-1]
+        if x.dtype != dy.dtype or x.numel() != N * d_in:
+            raise ValueError("x must have dy's dtype and the same number of rows")
         G = (W.shape[0] if W is not None else None) if dW is None else dW.shape[0]
         if G is None:
             raise ValueError("need W or dW to know the groups")
+        if d_in % G or d_out % G:
+            raise ValueError("d_in and d_out must be multiples of the group count")
         if dW is None:
             dW = torch.empty((G, d_in // G, d_out // G), dtype=torch.float32, device=ref.device)
+        else:
+            _dev(dW, "dW")
+            if dW.dtype != torch.float32 or tuple(dW.shape) != (G, d_in // G, d_out // G):
+                raise ValueError("dW must be float32 [G, d_in/G, d_out/G]")
         check(_lib.lib().resonator_grouped_linear_bwd_weight(_ptr(x), _ptr(dy), _code(x), _ptr(dW), N, d_in, d_out, G,
                                                              int(accumulate), _stream(dy.device)))
     return dx, dW
@@ -311,8 +362,18 @@ def resonator_grouped_linear_bwd_weight_split(x, dy, dW, accumulate=False):
     _dev(x, "x")
     _dev(dy, "dy")
     _dev(dW, "dW")
+    _code(x)
     d_in, d_out = x.shape[-1], dy.shape[-1]
     N = x.numel() // d_in
+    if dy.dtype != x.dtype:
+        raise ValueError(f"dy must have x's dtype ({x.dtype}), got {dy.dtype}")
+    if dy.numel() != N * d_out:
+        raise ValueError("x and dy must have the same number of rows")
+    if dW.dtype != torch.float32 or dW.dim() != 3:
+        raise ValueError("dW must be float32 [G, d_in/G, d_out/G]")
+    G = dW.shape[0]
+    if G < 1 or d_in % G or d_out % G or tuple(dW.shape) != (G, d_in // G, d_out // G):
+        raise ValueError(f"dW must be [G, d_in/G, d_out/G] = [{G}, {d_in}/{G}, {d_out}/{G}]")
     n = _lib.lib().resonator_grouped_linear_bwd_weight_split_workspace_bytes(N, d_in, d_out)
     ws = torch.empty(max(n, 256), dtype=torch.uint8, device=x.device)
     check(_lib.lib().resonator_grouped_linear_bwd_weight_split(_ptr(x), _ptr(dy), _code(x), _ptr(dW), N, d_in, d_out,
@@ -407,6 +468,13 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     a dict: dx, dWu, dWg, dWo (float32), dgamma, domega, damp, dphase, dCt,
     dlambda_c, dw, ds.  ``dense`` as for resonator_block_fwd (data gradients
     then run as dense GEMMs; weight gradients always per group)."""
+    _dev(x, "x")
+    _dev(do, "do")
+    if do.dtype != x.dtype:
+        raise ValueError(f"do must have x's dtype ({x.dtype}), got {do.dtype}")
+    d_out = Wo.shape[0] * Wo.shape[2]
+    if tuple(do.shape) != tuple(x.shape[:-1]) + (d_out,):
+        raise ValueError(f"do must be {tuple(x.shape[:-1]) + (d_out,)}, got {tuple(do.shape)}")
     Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
     u = resonator_grouped_linear(x, Pu)
     g = resonator_grouped_linear(x, Pg)

@@ -27,16 +27,16 @@ import os
 import sqlite3
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-FUSED = "fwd_seg_kernel"
+FUSED = "fwd_stream_kernel"
 COPY = "copyBuffer"
 
 
-# the segment kernel's code, its launcher and the entry point that sizes its grid
+# the streaming forward kernel, its launcher and the entry point that sizes its grid
 SEG_SOURCES = ("api.hip", "common.h", "fwd.hip", "tile_io.h")
 
 
 def source_hash() -> str:
-    """Hash of the sources the segment kernel is built and launched from: a counter
+    """Hash of the sources the streaming forward kernel is built and launched from: a counter
     summary is valid only for the code it was taken on."""
     h = hashlib.sha256()
     csrc = os.path.join(PKG, "csrc")

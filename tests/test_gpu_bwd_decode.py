@@ -181,41 +181,81 @@ def test_decode_graph_replays_match_eager_steps(B, D, M, K, act):
         _ = (x.float() * 2).sum().item()  # unrelated eager work between the replays
 
 
+def _oracle_rows(args):
+    """Oracle recurrence over one group of batch rows (a worker thread's share)."""
+    x, h0, prm = args
+    return O.mix_recurrence(x, *prm, h0=h0)
+
+
 def test_config4_decode_full():
     """Decode config: prompt 1024 -> state_init, then 32768 decode steps at B64 D256 M8 (bf16).
 
-    The GPU runs the full batch; the oracle follows 4 sampled batch rows through
-    all 32768 steps and is compared on every step of those rows and on the final
-    state.
+    Every output of every batch row and the final state are compared with the
+    oracle's recurrence (Sec. 3.3) started from the oracle's prompt state; the
+    oracle runs chunk by chunk over eight groups of rows in worker threads.
     """
+    from concurrent.futures import ThreadPoolExecutor
+
     cfg = W.CONFIGS[4]
     say(f"config 4 {cfg.name}")
     di = W.DecodeInputs(cfg)
     pr = params_dev(di.params)
-    rows = np.array([0, 17, 40, 63])
+    prm = params_np(di.params)
     prompt = dev_act(di.prompt, "bf16")
     st = ops.resonator_state_init(prompt, *pr)
     torch.cuda.synchronize()
-    st_ref = O.state_init(act64(di.prompt[rows], "bf16"), *params_np(di.params))
-    assert rel_err(host(st)[rows], st_ref) <= 2e-2
+    st_ref = O.state_init(act64(di.prompt, "bf16"), *prm)
+    assert rel_err(host(st), st_ref) <= 2e-2
     n_total, chunk = cfg.steps, 4096
-    lam, c = O.modes(*params_np(di.params))
-    h = st_ref[..., 0] + 1j * st_ref[..., 1]
+    groups = [slice(g, g + 8) for g in range(0, cfg.B, 8)]
+    h = [st_ref[g] for g in groups]
     worst = 0.0
-    y_dev = torch.empty((n_total, cfg.B, cfg.D), dtype=torch.bfloat16, device="cuda")
-    for s0 in range(0, n_total, chunk):
-        xs = di.steps(chunk)
-        xd = dev_act(xs, "bf16")
-        for j in range(chunk):
-            ops.resonator_decode_step(xd[j], *pr, st, out=y_dev[s0 + j])
-        torch.cuda.synchronize()
-        yg = host(y_dev[s0:s0 + chunk])[:, rows]
-        x64 = act64(xs[:, rows], "bf16")
-        yr = np.empty_like(yg)
-        for j in range(chunk):
-            h = lam[None] * h + x64[j][..., None]
-            yr[j] = (c[None] * h).real.sum(-1)
-        worst = max(worst, rel_err(yg, yr))
+    y_dev = torch.empty((chunk, cfg.B, cfg.D), dtype=torch.bfloat16, device="cuda")
+    with ThreadPoolExecutor(max_workers=8) as pool:
+        for s0 in range(0, n_total, chunk):
+            xs = di.steps(chunk)  # [chunk, B, D]
+            xd = dev_act(xs, "bf16")
+            for j in range(chunk):
+                ops.resonator_decode_step(xd[j], *pr, st, out=y_dev[j])
+            x64 = np.ascontiguousarray(act64(xs, "bf16").transpose(1, 0, 2))  # [B, chunk, D]
+            res = list(pool.map(_oracle_rows, [(x64[g], h[i], prm) for i, g in enumerate(groups)]))
+            torch.cuda.synchronize()
+            yg = host(y_dev).transpose(1, 0, 2)  # [B, chunk, D]
+            yr = np.concatenate([r[0] for r in res], 0)
+            h = [r[1] for r in res]
+            worst = max(worst, rel_err(yg, yr))
+            say(f"  steps {s0 + chunk}: worst step err so far {worst:.3e}")
     say(f"config 4 worst step err {worst:.3e}")
     assert worst <= 2e-2
-    assert rel_err(host(st)[rows], np.stack([h.real, h.imag], -1)) <= 2e-2
+    assert rel_err(host(st), np.concatenate(h, 0)) <= 2e-2
+
+
+@pytest.mark.parametrize("single", [False, True])
+def test_decode_long_f32_within_1e4(single):
+    """32768 float32 decode steps (slow modes down to gamma = 1e-5) stay within the
+    float32 bound of the oracle recurrence on every output and on the final
+    state: the pole is applied as a float32 hi + lo pair, so the phase error of a
+    single rounded pole does not build up over the run.  Drives come in blocks
+    of 2048 steps per launch (resonator_decode_steps, bitwise single steps) or,
+    for one block, as single steps."""
+    B, D, M, steps, blk = 2, 24, 8, 32768, 2048
+    say(f"decode long f32 B={B} D={D} M={M} steps={steps} single={single}")
+    prob = W.random_problem(301, B, steps, D, M, act="f32", gamma_range=(1e-5, 1.0), gamma_log=True,
+                            with_h0=True)
+    x = dev_act(prob["x"], "f32")
+    pr = params_dev(prob)
+    st = dev_f32(prob["h0"])
+    ys = []
+    for s0 in range(0, steps, blk):
+        if single and s0 == steps - blk:
+            ys.append(torch.stack([ops.resonator_decode_step(x[:, t].contiguous(), *pr, st)
+                                   for t in range(s0, s0 + blk)], 1))
+        else:
+            ys.append(ops.resonator_decode_steps(x[:, s0:s0 + blk].contiguous(), *pr, st))
+    torch.cuda.synchronize()
+    yg = host(torch.cat(ys, 1))
+    yr, hr = O.mix_recurrence(prob["x"], *params_np(prob), h0=prob["h0"])
+    e, eh = rel_err(yg, yr), rel_err(host(st), hr)
+    say(f"  rel err y {e:.3e} state {eh:.3e}")
+    assert e <= 1e-4
+    assert eh <= 1e-4

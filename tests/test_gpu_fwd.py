@@ -154,3 +154,64 @@ def test_fwd_repeatable():
     b = ops.resonator_mix_fwd(x, *pr)
     torch.cuda.synchronize()
     assert torch.equal(a, b)
+
+
+# Geometries that reach every branch of the forward's work split: many carry
+# fold blocks per row, long float32 rows with an initial state, a partial last
+# tile inside a multi-tile work unit, short last units, ragged channel blocks,
+# units of two and three tiles.  Each is compared element by element with the
+# oracle recurrence (y and h_out) and spot-checked against the direct sum.
+TILING = [
+    # B, L, D, M, act, out, h0, seed
+    (1, 16384, 64, 8, "bf16", "bf16", False, 31),
+    (1, 32768, 256, 8, "f32", "f32", True, 32),
+    (4, 32001, 256, 8, "bf16", "bf16", True, 33),
+    (8, 8191, 200, 8, "f32", "f32", False, 34),
+    (4, 8492, 256, 8, "bf16", "bf16", True, 35),
+    (4, 8192, 256, 8, "bf16", "f32", False, 36),
+    (2, 5000, 96, 5, "f32", "f32", True, 37),
+    (3, 4097, 130, 8, "bf16", "bf16", True, 38),
+]
+
+
+@pytest.mark.parametrize("B,L,D,M,act,out,use_h0,seed", TILING)
+def test_fwd_tiling_geometries(B, L, D, M, act, out, use_h0, seed):
+    say(f"fwd tiling B={B} L={L} D={D} M={M} {act}->{out} h0={use_h0}")
+    prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-5, 1.0), gamma_log=True,
+                            with_h0=use_h0)
+    x = dev_act(prob["x"], act)
+    h0 = dev_f32(prob["h0"]) if use_h0 else None
+    y, hout = ops.resonator_mix_fwd(x, *params_dev(prob), h0=h0,
+                                    out_dtype=torch.float32 if out == "f32" else x.dtype,
+                                    return_state=True)
+    torch.cuda.synchronize()
+    yg, hg = host(y), host(hout)
+    x64 = act64(prob["x"], act)
+    yr, hr = O.mix_recurrence(x64, *params_np(prob), h0=prob["h0"] if use_h0 else None)
+    e, eh = rel_err(yg, yr), rel_err(hg, hr)
+    say(f"  rel err y {e:.3e} h_out {eh:.3e}")
+    assert e <= tol(act, out)
+    assert eh <= (1e-4 if act == "f32" else 2e-2)
+    pos = _spot_positions(np.random.default_rng(seed), B, L, D, 64)
+    yd = O.mix_direct_at(x64, *params_np(prob), pos, h0=prob["h0"] if use_h0 else None)
+    got = yg[pos[:, 0], pos[:, 1], pos[:, 2]]
+    den = np.maximum(np.abs(yd), np.sqrt(np.mean(yr ** 2)))
+    assert float((np.abs(got - yd) / den).max()) <= tol(act, out)
+
+
+def test_h_out_may_alias_h0():
+    """h_out written over h0 (in-place state hand-over) gives the same y and state
+    as separate buffers, for the single-kernel forward and the M > 8 path."""
+    for M, act, seed in ((8, "bf16", 41), (8, "f32", 42), (12, "f32", 43)):
+        say(f"h_out aliases h0 M={M} {act}")
+        prob = W.random_problem(seed, 4, 8192 + 77, 256, M, act=act, gamma_range=(1e-5, 1.0),
+                                gamma_log=True, with_h0=True)
+        x = dev_act(prob["x"], act)
+        pr = params_dev(prob)
+        h0 = dev_f32(prob["h0"])
+        y1, h1 = ops.resonator_mix_fwd(x, *pr, h0=h0.clone(), return_state=True)
+        st = h0.clone()
+        y2 = ops.resonator_mix_fwd(x, *pr, h0=st, h_out=st)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2)
+        assert torch.equal(h1, st)

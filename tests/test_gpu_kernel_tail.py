@@ -77,13 +77,23 @@ def test_fft_reference_repeated_calls_and_two_plan_shapes():
     np.testing.assert_array_equal(outs[1], outs[3])
 
 
-def test_mixing_matches_the_fft_reference_at_32k():
+def test_mixing_and_fft_reference_match_the_oracle_at_32k():
+    """The kernel-tail shape at 32K (B1 D256 M8 float32): the mixing and the FFT
+    convolution, each against the oracle recurrence (and the mixing against
+    direct-sum spot checks), and against each other."""
     prob = W.random_problem(88, 1, 32768, 256, 8, act="f32", gamma_range=(1e-4, 1.0), gamma_log=True)
     x = dev_f32(prob["x"])
     pr = params_dev(prob)
-    yf = ops.resonator_fft_reference(x, *pr)
-    ym = ops.resonator_mix_fwd(x, *pr)
+    yf = host(ops.resonator_fft_reference(x, *pr))
+    ym = host(ops.resonator_mix_fwd(x, *pr))
     torch.cuda.synchronize()
-    err = rel_err(host(ym), host(yf))
-    say(f"  mixing vs FFT reference at 32K: {err:.2e}")
-    assert err <= 1e-4
+    yr = O.mix_recurrence(prob["x"], *params_np(prob))[0]
+    em, ef, emf = rel_err(ym, yr), rel_err(yf, yr), rel_err(ym, yf)
+    say(f"  at 32K: mixing vs oracle {em:.2e}, FFT vs oracle {ef:.2e}, mixing vs FFT {emf:.2e}")
+    assert em <= 1e-4 and ef <= 1e-4 and emf <= 1e-4
+    rng = np.random.default_rng(89)
+    pos = np.stack([np.zeros(64, np.int64), np.concatenate([rng.integers(0, 32768, 60), [0, 255, 256, 32767]]),
+                    rng.integers(0, 256, 64)], 1)
+    yd = O.mix_direct_at(prob["x"], *params_np(prob), pos)
+    den = np.maximum(np.abs(yd), np.sqrt(np.mean(yr ** 2)))
+    assert float((np.abs(ym[pos[:, 0], pos[:, 1], pos[:, 2]] - yd) / den).max()) <= 1e-4
