@@ -66,31 +66,27 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
 // bytes are the header (status word first); the forward workspace must be zero
 // before its first use and each call leaves it ready for the next.
 struct StreamLayout {
-  size_t hdr, ticket, claim, tflag, flag, tab, scal, agg, inc, total;
+  size_t hdr, chainw, agg, total;
 };
+// The single-pass forward keeps per-chain counters in a fixed area of the
+// workspace (every call resets the counters it used), ahead of the tagged
+// states, so that one workspace serves calls of any shapes: a call's states
+// never land on another call's counters.
+constexpr int64_t STREAM_MAX_CHAINS = 1 << 16;
+bool stream_forward(const Geometry& g) { return g.MG == 1 && g.B * g.NB <= STREAM_MAX_CHAINS; }
+
 StreamLayout make_stream_layout(const Geometry& g) {
   StreamLayout w{};
-  const int NW = g.DW / 4, NQ = g.DW / 16;
   const size_t nchains = (size_t)g.B * g.NB, tiles = nchains * (size_t)g.P;
+  // a tile's published end state: one 8-byte word per channel and state component
+  const size_t state = (size_t)g.DW * 16 * sizeof(uint64_t);
   size_t off = 0;
   w.hdr = off;
   off += 256;
-  w.ticket = off;
-  off += align256(nchains * sizeof(uint32_t));
-  w.claim = off;
-  off += align256((size_t)g.NB * sizeof(uint32_t));
-  w.tflag = off;
-  off += align256((size_t)g.NB * NW * sizeof(uint32_t));
-  w.flag = off;
-  off += align256(tiles * NQ * sizeof(uint32_t));
-  w.tab = off;
-  off += align256((size_t)g.Dp * 3 * 64 * 16);
-  w.scal = off;
-  off += align256((size_t)g.Dp * 8 * 4 * sizeof(float2));
+  w.chainw = off;
+  off += (size_t)STREAM_MAX_CHAINS * 4 * sizeof(uint32_t);
   w.agg = off;
-  off += align256(tiles * NQ * 64 * 16);
-  w.inc = off;
-  off += align256(tiles * NQ * 64 * 16);
+  off += align256(tiles * state);
   w.total = off;
   return w;
 }
@@ -100,7 +96,7 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
   size_t off = 0;
   (void)act;
   if (op == RES_OP_FWD) {
-    if (g.MG == 1) {
+    if (stream_forward(g)) {
       w.total = make_stream_layout(g).total;
       return w;
     }
@@ -228,7 +224,7 @@ int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int
   hipEvent_t ev0, ev1;
   take_timer(&ev0, &ev1);
   hipError_t e;
-  if (g.MG == 1) {  // single-pass forward
+  if (stream_forward(g)) {  // single-pass forward
     const StreamLayout sl = make_stream_layout(g);
     int dev = 0, ncu = 0;
     if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -253,14 +249,8 @@ int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int
     a.h0 = h0;
     a.h_out = h_out;
     a.hdr = (uint32_t*)(base + sl.hdr);
-    a.ticket = (uint32_t*)(base + sl.ticket);
-    a.claim = (uint32_t*)(base + sl.claim);
-    a.tflag = (uint32_t*)(base + sl.tflag);
-    a.flag = (uint32_t*)(base + sl.flag);
-    a.tab = (uint4*)(base + sl.tab);
-    a.scal = (float2*)(base + sl.scal);
-    a.agg = (uint4*)(base + sl.agg);
-    a.inc = (uint4*)(base + sl.inc);
+    a.chainw = (uint32_t*)(base + sl.chainw);
+    a.agg = (uint64_t*)(base + sl.agg);
     const int grid = fwd_stream_grid(B * g.NB, g.P, ncu > 0 ? ncu : 256);
     if (x_dt == RES_F32)
       e = launch_fwd_stream<float, float>(a, grid, st, ev0, ev1);

@@ -782,10 +782,16 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
 // ---------------------------------------------------------------------------
 // Single-pass forward (one mode group, M <= 8).
 //
-// A chain is one batch row and one block of DW channels (128-byte rows).  Its
-// tiles (256 steps) are taken in time order, by ticket, by the work-groups that
-// serve the chain, so that a tile's predecessors hold smaller tickets and belong
-// to running work-groups.  Per tile:
+// A chain is one batch row and one block of DW channels (128-byte rows); the
+// work-groups that serve a chain take its tiles (256 steps) in time order.  On
+// arrival a work-group draws its rank r in the chain.  Once all G work-groups of
+// the chain have arrived (they are then all running), the chain is processed in
+// rounds: the work-group of rank r takes tiles r, r + G, r + 2G, ..., so that the
+// tiles a tile waits for are processed at the same time as it or earlier.  If
+// the work-groups do not all arrive within a short bounded wait (part of the
+// device is busy with other work), the chain takes its tiles by ticket instead,
+// first come first served, so that every tile waited for belongs to a running
+// work-group.  Per tile:
 //   pass 1   per channel, S = V x on MFMA (lane (c, q): component c of chunks
 //            4q .. 4q+3); the results of a wave's four channels are exchanged
 //            across lane rows (lane swaps), after which lane (c, k) holds
@@ -809,45 +815,26 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
 // flag, then loads the state with device-coherent loads.  Flags carry the call's
 // epoch, so they are never reset; the counters are reset by the last work-group
 // to finish.
-// Operand tables are built in the kernel: the channels of a block form units of
-// 4 (one wave's channels); a work-group claims units of its block by ticket,
-// builds them in float64 and publishes them; every wave waits for the units it
-// reads.
+// Every work-group builds the operand tables of its DW channels itself, in LDS,
+// while its first tile loads.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void st_agent(float2* p, float2 v) {
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), __builtin_bit_cast(uint64_t, v),
-                     __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float2 ld_agent(const float2* p) {
-  return __builtin_bit_cast(float2, __hip_atomic_load(reinterpret_cast<const uint64_t*>(p),
-                                                      __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-}
-// 16 bytes as two device-coherent 8-byte accesses
-__device__ __forceinline__ void st_dev16(void* p, uint4 v) {
-  uint64_t* q = reinterpret_cast<uint64_t*>(p);
-  __hip_atomic_store(q, (uint64_t)v.x | ((uint64_t)v.y << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __hip_atomic_store(q + 1, (uint64_t)v.z | ((uint64_t)v.w << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ uint4 ld_dev16(const void* p) {
-  const uint64_t* q = reinterpret_cast<const uint64_t*>(p);
-  const uint64_t lo = __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  const uint64_t hi = __hip_atomic_load(q + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi, (uint32_t)(hi >> 32));
-}
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
   return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void st_flag(uint32_t* f, uint32_t v) {
   __hip_atomic_store(f, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Upper bound on polls of one wait (with a short sleep between polls, well over
-// 0.1 s).  In ticket order every wait ends long before it; it is reached only
-// with a workspace that was not zeroed before its first use (or was changed
-// meanwhile): the kernel then records bit 0 in the status word and goes on.
+// Upper bound on polls of one wait for a published state (with a short sleep
+// between polls, well over 0.1 s).  Every such wait ends long before it; it is
+// reached only with a workspace that was not zeroed before its first use (or was
+// changed meanwhile): the kernel then records bit 0 in the status word and goes on.
 constexpr uint32_t SPIN_LIMIT = 1u << 18;
-// Polls of the wait that spaces a work-group's first claims (some tens of
-// microseconds at most; past it the claim is made anyway).
-constexpr uint32_t CLAIM_WAIT = 64;
+// Polls of the wait for the other work-groups of a chain to arrive (some tens of
+// microseconds at most); past it the chain takes its tiles by ticket.
+constexpr uint32_t ARRIVE_WAIT = 64;
+#ifndef RES_FOLD_WORDS
+#define RES_FOLD_WORDS 16
+#endif
 
 // Complex arithmetic on the two modes of a lane, (re_a, im_a, re_b, im_b).
 __device__ __forceinline__ f4 c2mul(const f4& a, const f4& b) {
@@ -938,21 +925,27 @@ __device__ __forceinline__ void dma_group(char* xt, const TX* x, int64_t b, int6
   lds_dma16(src, loff, xt + g * XLay<XE>::GRP);
 }
 
-// Row group g of a full output tile from its LDS buffer by the calling wave:
-// a 16-byte row store per lane, read from LDS as an 8-byte pair.
-template <typename TY>
-__device__ __forceinline__ void store_group(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
-                                            int D, int lane, int g) {
+// Row groups g0, g0 + step, ... (n of them) of a full output tile from its LDS
+// buffer by the calling wave: all the LDS reads first (a 16-byte row piece per
+// lane, read as two 8-byte halves), then the 16-byte row stores.
+template <typename TY, int N>
+__device__ __forceinline__ void store_groups(TY* y, const char* xt, int64_t b, int64_t t0, int d0, int64_t L,
+                                             int D, int lane, int g0, int step) {
   constexpr int YE = (int)sizeof(TY);
   const int64_t rowb = (int64_t)D * YE;
-  char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE + (int64_t)(8 * g) * rowb;
+  char* dst = reinterpret_cast<char*>(y) + ((b * L + t0) * D + d0) * YE;
   int ln = lane;
   asm volatile("" : "+v"(ln));
+  u32x4 v[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const uint2* s = reinterpret_cast<const uint2*>(xt + (g0 + step * i) * XLay<YE>::GRP + ln * 16);
+    const uint2 u = s[0], w = s[1];
+    v[i] = u32x4{u.x, u.y, w.x, w.y};
+  }
   const uint32_t loff = (uint32_t)((ln >> 3) * rowb) + (ln & 7) * 16;
-  const uint2* s = reinterpret_cast<const uint2*>(xt + g * XLay<YE>::GRP + ln * 16);
-  const uint2 u = s[0], w = s[1];
-  const u32x4 v = {u.x, u.y, w.x, w.y};
-  st_row16(dst, loff, v);
+#pragma unroll
+  for (int i = 0; i < N; ++i) st_row16(dst + (int64_t)(8 * (g0 + step * i)) * rowb, loff, v[i]);
 }
 
 // Element copy of a tile that is not full (NT threads); zeros outside the tensor.
@@ -984,133 +977,160 @@ __device__ __forceinline__ void store_tile_part(TY* y, const char* xt, int64_t b
 template <typename TX>
 struct StreamGeo {
   static constexpr int DW = tile_channels<TX>();   // channels per tile: 64 (bf16) | 32 (float)
-  static constexpr int NW = DW / 4;                // waves, 4 channels each: 16 | 8
+  static constexpr int NW = 8;                     // waves (two per SIMD: 256 registers each)
+  static constexpr int NG = DW / (4 * NW);         // groups of 4 channels per wave: 2 | 1
   static constexpr int NT = 64 * NW;
   static constexpr int NQ = DW / 16;               // control waves (16 channels each): waves 0 .. NQ-1
-  static constexpr int LW = NW == 16 ? 8 : 4;      // load waves: NQ .. NQ+LW-1
+  static constexpr int LW = 4;                     // load waves: NQ .. NQ+3
   static constexpr int GPL = (TILE_T / 8) / LW;    // row groups per load wave and tile
   static constexpr int NBUF = 4;                   // tile buffers
-  static constexpr int HR = NW == 16 ? 2 : 4;      // channels per round of the H transposition
-  static constexpr int HKS = 16 * 16 + 16;         // floats per channel there (16 floats of bank offset)
+  static constexpr int HKS = 16 * 16 + 16;         // floats per channel in the H transposition (16 of bank offset)
   static constexpr int XB = XLay<(int)sizeof(TX)>::BYTES;
-  static constexpr int HB = NW * HR * HKS * 4;
+  static constexpr int HB = NW * 4 * HKS * 4;      // every wave's 4 channels of one group
   static constexpr int BUFB = XB > HB ? XB : HB;   // bytes per buffer (tile, or H transposition)
   static_assert(GPL * LW == TILE_T / 8, "the load waves cover a tile");
   static_assert(NQ + LW <= NW, "control and load waves are distinct");
+  static_assert(NG * 4 * NW == DW, "the waves cover the tile's channels");
 };
 
-// z^n for 0 <= n <= 16, float64 (binary powers)
-__device__ __forceinline__ double2 zpow16(double2 z, int n) {
-  double2 r = make_double2(1.0, 0.0), s = z;
-#pragma unroll
-  for (int i = 0; i < 5; ++i) {
-    if (n & (1 << i)) r = zmul(r, s);
-    s = zmul(s, s);
+// LDS stage of a work-group's tables, per channel k of the block and mode m:
+// lambda^j (j = 0 .. 16) and c as float2, the taps K[tau] (tau = 0 .. 15) as
+// float32 or as a bf16 pair (high | low << 16), and the scan constants mu =
+// lambda^16, lambda^256, lambda and lambda^(jstar+1).
+template <typename TX>
+struct TabStage {
+  static constexpr int DW = tile_channels<TX>();
+  static constexpr int PW = 0;                     // float2 [DW][8][17]
+  static constexpr int CM = PW + DW * 8 * 17 * 8;  // float2 [DW][8]
+  static constexpr int TAP = CM + DW * 8 * 8;      // uint32 [DW][16]
+  static constexpr int SC = TAP + DW * 16 * 4;     // float2 [DW][8][4]
+  static constexpr int BYTES = SC + DW * 8 * 4 * 8;
+};
+
+// The float32 parameters of thread (k, m) = 8 k + m: channel d0 + k, mode m
+// (zeros outside D x M and for threads beyond the block's channels).
+struct ModeIn {
+  float gamma, omega, amp, phase;
+};
+template <typename TX>
+__device__ __forceinline__ ModeIn load_mode(const StreamArgs& a, int d0, int tid) {
+  ModeIn r{0.f, 0.f, 0.f, 0.f};
+  const int k = tid >> 3, m = tid & 7, d = d0 + k;
+  if (tid < TabStage<TX>::DW * 8 && d < a.D && m < a.M) {
+    const int i = d * a.M + m;
+    r.gamma = a.gamma[i];
+    r.omega = a.omega[i];
+    r.amp = a.amp[i];
+    r.phase = a.phase[i];
   }
   return r;
 }
 
-// Operand tables of the channels d0u .. d0u+3 (one unit), as the MFMA lanes
-// read them: T (lower Toeplitz taps K[i-k]), V (lambda^(15-k), re/im rows), U
-// (c lambda^(i+1), re/-im columns, float32), T and V split into bf16 halves
-// for bf16 activations; and per (channel, mode) mu = lambda^16, lambda^256,
-// lambda and lambda^(jstar+1).  Every power is built in float64 from lambda =
-// exp(-gamma) (cos omega, sin omega) by products (a relative error of a few
-// 2^-53 per product), then rounded once.  All threads take part (LDS stages at
-// lds); the waves that issue no tile loads store the results.
+// The tables of channels d0 .. d0+DW-1 into the stage st (threads (k, m) =
+// 8 k + m, one per channel and mode, with their parameters pin).  lambda =
+// exp(-gamma) (cos omega, sin omega) and c = amp (cos phase, sin phase) in
+// float64, the powers lambda^j by successive products and lambda^256 by eight
+// squarings (a relative error of a few 2^-53 per product); the taps
+// K[tau] = Re sum_m c lambda^tau, summed in float64 over the eight mode lanes of
+// a channel, are rounded once.
 template <typename TX>
-__device__ void build_unit(const StreamArgs& a, int d0u, char* lds, int tid, int wave) {
-  typedef StreamGeo<TX> G;
-  double2* lam = reinterpret_cast<double2*>(lds);  // [32] (channel k, mode m) = 8 k + m
-  double2* cm = lam + 32;                          // [32] c
-  double2* pw = cm + 32;                           // [32][17] lambda^j
-  double2* l256 = pw + 32 * 17;                    // [32] lambda^256
-  double* taps = reinterpret_cast<double*>(l256 + 32);  // [4][16]
-  if (tid < 32) {
-    const int k = tid >> 3, m = tid & 7, d = d0u + k;
-    double2 z = make_double2(0.0, 0.0), cz = z;
-    if (d < a.D && m < a.M) {
-      const int i = d * a.M + m;
-      double sn, cs;
-      sincos((double)a.omega[i], &sn, &cs);
-      const double e = exp(-(double)a.gamma[i]);
-      z = make_double2(e * cs, e * sn);
-      sincos((double)a.phase[i], &sn, &cs);
-      const double av = (double)a.amp[i];
-      cz = make_double2(av * cs, av * sn);
-    }
-    lam[tid] = z;
-    cm[tid] = cz;
+__device__ void build_tables(const StreamArgs& a, int d0, char* st, int tid, const ModeIn& pin) {
+  typedef TabStage<TX> S;
+  if (tid >= S::DW * 8) return;
+  const int k = tid >> 3, m = tid & 7, d = d0 + k;
+  double2 z = make_double2(0.0, 0.0), cz = z;
+  if (d < a.D && m < a.M) {
+    double sn, cs;
+    sincos((double)pin.omega, &sn, &cs);
+    const double e = exp(-(double)pin.gamma);
+    z = make_double2(e * cs, e * sn);
+    sincos((double)pin.phase, &sn, &cs);
+    const double av = (double)pin.amp;
+    cz = make_double2(av * cs, av * sn);
   }
-  __syncthreads();
-  for (int t = tid; t < 32 * 17 + 32; t += G::NT) {
-    if (t < 32 * 17) {
-      pw[t] = zpow16(lam[t / 17], t % 17);
-    } else {
-      double2 z = lam[t - 32 * 17];
+  const int jt = (a.last_len - 1) % CHUNK + 1;  // jstar + 1
+  float2* pw = reinterpret_cast<float2*>(st + S::PW) + tid * 17;
+  double tp[16];
+  double2 pj = make_double2(1.0, 0.0), lt = pj;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) z = zmul(z, z);
-      l256[t - 32 * 17] = z;
-    }
+  for (int j = 0; j <= 16; ++j) {
+    pw[j] = make_float2((float)pj.x, (float)pj.y);
+    if (j < 16) tp[j] = cz.x * pj.x - cz.y * pj.y;
+    if (j == jt) lt = pj;
+    if (j < 16) pj = zmul(pj, z);
   }
-  __syncthreads();
-  if (tid < 64) {  // K[tau] = Re sum_m c lambda^tau
-    const int k = tid >> 4, tau = tid & 15;
-    double s = 0.0;
-    for (int m = 0; m < 8; ++m) {
-      const double2 c = cm[8 * k + m], p = pw[(8 * k + m) * 17 + tau];
-      s += c.x * p.x - c.y * p.y;
-    }
-    taps[tid] = s;
+  double2 l2 = z;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) l2 = zmul(l2, l2);
+  reinterpret_cast<float2*>(st + S::CM)[tid] = make_float2((float)cz.x, (float)cz.y);
+  float2* sc = reinterpret_cast<float2*>(st + S::SC) + tid * 4;
+  sc[0] = make_float2((float)pj.x, (float)pj.y);  // lambda^16
+  sc[1] = make_float2((float)l2.x, (float)l2.y);
+  sc[2] = make_float2((float)z.x, (float)z.y);
+  sc[3] = make_float2((float)lt.x, (float)lt.y);
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    double v = tp[j];
+    v += __shfl_xor(v, 1);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 4);
+    tp[j] = v;
   }
-  __syncthreads();
-  if (wave < G::NQ || wave >= G::NQ + G::LW) {
-    const int bt = wave < G::NQ ? tid : tid - 64 * G::LW;
-    constexpr int NBT = 64 * (G::NW - G::LW);
-    const int jt = (a.last_len - 1) % CHUNK + 1;  // jstar + 1
-    // entry (mat, channel k, row i, column kk)
-    auto entry = [&](int mat, int k, int i, int kk) -> double {
-      if (mat == 0) return i >= kk ? taps[16 * k + i - kk] : 0.0;
-      if (mat == 1) {
-        const double2 z = pw[(8 * k + i / 2) * 17 + CHUNK - 1 - kk];
-        return (i & 1) ? z.y : z.x;
-      }
-      const int m = 8 * k + kk / 2;
-      const double2 z = zmul(cm[m], pw[m * 17 + i + 1]);
-      return (kk & 1) ? -z.y : z.x;
-    };
-    for (int t = bt; t < 4 * 3 * 64 + 32; t += NBT) {
-      if (t < 4 * 3 * 64) {
-        const int k = t / 192, mat = (t / 64) % 3, l = t % 64, i = l % 16, q = l / 16;
-        uint4 out;
-        if (sizeof(TX) == 4 || mat == 2) {
-          float v[4];
+  if (m == 0) {
+    uint32_t* tap = reinterpret_cast<uint32_t*>(st + S::TAP) + k * 16;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) v[r] = (float)entry(mat, k, i, 4 * q + r);
-          out = *reinterpret_cast<const uint4*>(v);
-        } else {  // Ah[i][4q..4q+3], then Al[i][4q..4q+3]
-          bf16_t v[8];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const double e = entry(mat, k, i, 4 * q + r);
-            const bf16_t hi = from_f32<bf16_t>((float)e);
-            v[r] = hi;
-            v[4 + r] = from_f32<bf16_t>((float)(e - (double)to_f32(hi)));
-          }
-          out = *reinterpret_cast<const uint4*>(v);
-        }
-        st_dev16(a.tab + ((size_t)(d0u + k) * 3 + mat) * 64 + l, out);
+    for (int j = 0; j < 16; ++j) {
+      if (sizeof(TX) == 4) {
+        tap[j] = __float_as_uint((float)tp[j]);
       } else {
-        const int km = t - 4 * 3 * 64, k = km >> 3, m = km & 7;
-        const double2 mu = pw[km * 17 + CHUNK], la = pw[km * 17 + 1], lt = pw[km * 17 + jt], l2 = l256[km];
-        float2* s = a.scal + ((size_t)(d0u + k) * 8 + m) * 4;
-        st_dev16(s, make_uint4(__float_as_uint((float)mu.x), __float_as_uint((float)mu.y),
-                               __float_as_uint((float)l2.x), __float_as_uint((float)l2.y)));
-        st_dev16(s + 2, make_uint4(__float_as_uint((float)la.x), __float_as_uint((float)la.y),
-                                   __float_as_uint((float)lt.x), __float_as_uint((float)lt.y)));
+        const bf16_t hi = from_f32<bf16_t>((float)tp[j]);
+        const bf16_t lo = from_f32<bf16_t>((float)(tp[j] - (double)to_f32(hi)));
+        tap[j] = (uint32_t)hi | ((uint32_t)lo << 16);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0x0F70);  // the unit's stores have completed
+  }
+}
+
+// Lane (i, q)'s operands of channel k of the stage, as the MFMA lanes read them:
+// T[i][4q+r] = K[i - 4q - r] (zero above the diagonal); V[i][4q+r] = Re or Im
+// (by the parity of i) of lambda^(15 - 4q - r) of mode i/2; U[i][4q+r] = Re or
+// -Im (by the parity of r) of c lambda^(i+1) of mode (4q + r)/2, formed in
+// float32 from the staged float32 power and c.  For bf16 activations T and V are
+// split into bf16 halves (high, low).
+template <typename TX>
+__device__ __forceinline__ void stage_operands(const char* st, int k, int i, int q, typename FPath<TX>::AOp& t,
+                                               typename FPath<TX>::AOp& v, f4& u) {
+  typedef TabStage<TX> S;
+  const float2* pw = reinterpret_cast<const float2*>(st + S::PW) + k * 8 * 17;
+  const float2* cm = reinterpret_cast<const float2*>(st + S::CM) + k * 8;
+  const uint32_t* tap = reinterpret_cast<const uint32_t*>(st + S::TAP) + k * 16;
+  uint32_t tw[4];
+  f4 vv;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int kk = 4 * q + r;
+    tw[r] = i >= kk ? tap[i - kk] : 0u;
+    const float2 pv = pw[(i >> 1) * 17 + 15 - kk];
+    vv[r] = (i & 1) ? pv.y : pv.x;
+    const float2 c = cm[kk >> 1], pu = pw[(kk >> 1) * 17 + i + 1];
+    u[r] = (r & 1) ? -fmaf(c.x, pu.y, c.y * pu.x) : fmaf(c.x, pu.x, -c.y * pu.y);
+  }
+  if (sizeof(TX) == 4) {
+    t = FPath<TX>::load_a_u4(make_uint4(tw[0], tw[1], tw[2], tw[3]));
+    v = FPath<TX>::load_a_u4(make_uint4(__float_as_uint(vv[0]), __float_as_uint(vv[1]), __float_as_uint(vv[2]),
+                                        __float_as_uint(vv[3])));
+  } else {
+    uint32_t vh[4], vl[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const bf16_t h = from_f32<bf16_t>(vv[r]);
+      vh[r] = h;
+      vl[r] = from_f32<bf16_t>(vv[r] - to_f32(h));
+    }
+    t = FPath<TX>::load_a_u4(make_uint4((tw[0] & 0xFFFFu) | (tw[1] << 16), (tw[2] & 0xFFFFu) | (tw[3] << 16),
+                                        (tw[0] >> 16) | (tw[1] & 0xFFFF0000u), (tw[2] >> 16) | (tw[3] & 0xFFFF0000u)));
+    v = FPath<TX>::load_a_u4(make_uint4(vh[0] | (vh[1] << 16), vh[2] | (vh[3] << 16), vl[0] | (vl[1] << 16),
+                                        vl[2] | (vl[3] << 16)));
   }
 }
 
@@ -1142,387 +1162,371 @@ __device__ __forceinline__ void chunk_states(const typename FPath<TX>::XOp (&xv)
   }
 }
 
-// Wave-uniform bounded poll of one flag until it reads `want`; false on give-up
-// (after SPIN_LIMIT polls, or at once once any work-group of the call has given
-// up, word gave_up, so that a broken call ends after one wait limit rather than
-// one per tile).
-__device__ __forceinline__ bool wait_flag_eq(const uint32_t* f, uint32_t want, const uint32_t* gave_up) {
-  for (uint32_t it = 0; it < SPIN_LIMIT; ++it) {
-    if (ld_flag(f) == want) return true;
-    if ((it & 63) == 63 && ld_flag(gave_up) != 0) return false;
-    __builtin_amdgcn_s_sleep(1);
+// Published tile end states: every 64-bit word holds one float (low half) and
+// the tag of the call that wrote it (high half), so that a reader checks the
+// data itself and a writer needs no ordering between data and a flag.  The
+// stores and loads are device-coherent (work-groups of a chain run on any XCD).
+template <int NG>
+__device__ __forceinline__ void put_state(uint64_t* p, const float (&v)[NG], uint32_t tag) {
+#pragma unroll
+  for (int g = 0; g < NG; ++g)
+    __hip_atomic_store(p + g, (uint64_t)__float_as_uint(v[g]) | ((uint64_t)tag << 32), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+}
+// false while any word still carries another tag
+template <int NG>
+__device__ __forceinline__ bool get_state(const uint64_t* p, uint32_t tag, float (&v)[NG]) {
+  bool ok = true;
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const uint64_t w = __hip_atomic_load(p + g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    v[g] = __uint_as_float((uint32_t)w);
+    ok = ok && (uint32_t)(w >> 32) == tag;
   }
-  return false;
+  return ok;
 }
 
 template <typename TX, typename TY>
 __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(StreamArgs a) {
   typedef StreamGeo<TX> G;
   typedef FPath<TX> PT;
-  constexpr int DW = G::DW, NW = G::NW, NT = G::NT, NQ = G::NQ, LW = G::LW, GPL = G::GPL, NBUF = G::NBUF;
-  constexpr int XE = (int)sizeof(TX), HR = G::HR, HKS = G::HKS;
+  typedef TabStage<TX> TS;
+  constexpr int DW = G::DW, NW = G::NW, NG = G::NG, NT = G::NT, NQ = G::NQ, LW = G::LW, GPL = G::GPL;
+  constexpr int NBUF = G::NBUF, XE = (int)sizeof(TX), HKS = G::HKS;
+  static_assert(TS::BYTES <= (NBUF - 1) * G::BUFB, "the table stage fits in buffers 1 .. NBUF-1");
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
+  // published states loaded at a time by a fold (a register budget of 2 RES_FOLD_WORDS)
+  constexpr int FB = RES_FOLD_WORDS / NG;
   __shared__ __align__(16) char xb[NBUF][G::BUFB];
-  __shared__ __align__(16) f4 sA[NQ][64];  // pass 1's A: control lane l, slot = wave within the quarter
-  __shared__ __align__(16) f4 sE[NQ][64];  // the entering states from the control waves
-  __shared__ __align__(16) float2 sL2[NQ][64][4];  // control lanes: lambda^256 as (Re, -+Im)
-  __shared__ __align__(16) f4 sI[NQ][64];  // control lanes: the own previous tile's I
-  __shared__ uint32_t s_tk[NBUF];          // tile (ticket) of each buffer slot
+  __shared__ uint32_t s_tk[NBUF];  // tile of each buffer slot
   __shared__ uint32_t s_u[4];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ln = lane & 15, lq = lane >> 4;  // MFMA lane (i, q); scan lane (component ln, channel lq)
-  const int c0 = wave * 4;                   // this wave's first channel in the tile
-  const int Q = wave >> 2, wq = wave & 3;    // quarter (16 channels) and slot in it
-  const bool is_ctl = wave < NQ, is_ld = wave >= NQ && wave < NQ + LW;
+  const int cb = wave * 4 * NG;              // this wave's first channel; group g: cb + 4 g .. cb + 4 g + 3
+  const bool is_ld = wave >= NQ && wave < NQ + LW;
   const int chain = (int)(blockIdx.x % (unsigned)a.nchains);
   const int64_t b = chain / a.NB;
   const int blk = chain % a.NB;
   const int d0 = blk * DW;
   const int64_t P = a.P;
+  const uint32_t G_ = gridDim.x / (uint32_t)a.nchains;  // work-groups serving each chain
+  uint32_t* cw = a.chainw + 4 * (size_t)chain;  // [0] next ticket, [1] arrived, [2] order, [3] finished
   const uint32_t ep = ld_flag(a.hdr + 1);
-  const uint32_t MK_A = 2 * ep + 1, MK_I = 2 * ep + 2, MK_T = ep + 1;
+  const uint32_t TAG = ep + 1u;
   const int nstar = (a.last_len - 1) / CHUNK, jstar = (a.last_len - 1) % CHUNK;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
   const bool full_block = a.fast_io && d0 + DW <= a.D;
   auto tile_full = [&](int64_t p) { return full_block && (p + 1) * TILE_T <= a.L; };
+  auto load_tile = [&](int u, int64_t p) {  // by the load waves, a full tile
+#pragma unroll
+    for (int i = 0; i < GPL; ++i)
+      dma_group<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, lane,
+                    (wave - NQ) + LW * i);
+  };
+  auto store_tile = [&](int u, int64_t p) {  // rows of output tile p from buffer u
+    if (tile_full(p)) {
+      if (is_ld) {
+        constexpr int SB = GPL < 4 ? GPL : 4;  // row groups per batch of LDS reads
+#pragma unroll
+        for (int i = 0; i < GPL; i += SB)
+          store_groups<TY, SB>(reinterpret_cast<TY*>(a.y), xb[u], b, p * TILE_T, d0, a.L, a.D, lane,
+                               (wave - NQ) + LW * i, LW);
+      }
+    } else {
+      store_tile_part<TY, NT>(reinterpret_cast<TY*>(a.y), xb[u], b, p * TILE_T, d0, a.L, a.D, tid);
+    }
+  };
+  // this lane's words of the published end state of tile q
+  auto a_slot = [&](int64_t q) { return a.agg + ((((size_t)chain * P + q) * NW + wave) * 64 + lane) * NG; };
 
-  // ---- arrival, the first tile, the first table claim -------------------------
-  if (tid == 0) {
-    const uint32_t arr = atomicAdd(a.hdr + 2, 1u);
-    const uint32_t t0 = atomicAdd(a.ticket + chain, 1u);
-    const uint32_t cl = atomicAdd(a.claim + blk, 1u);
-    s_u[0] = arr;
-    s_tk[0] = t0;
-    s_u[1] = cl;
-  }
+  // ---- arrival: rank in the chain, and the rank's first tile ------------------
+  const ModeIn pin = load_mode<TX>(a, d0, tid);  // before any tile load of the wave
+  if (tid == 0) s_u[1] = atomicAdd(cw + 1, 1u);
   __syncthreads();
+  const uint32_t rank = s_u[1];
   // more arrivals than work-groups: the counters were not in their initial
   // state (workspace not zeroed, or changed meanwhile); touch nothing
-  if (s_u[0] >= gridDim.x) {
+  if (rank >= G_) {
     if (tid == 0) atomicOr(a.hdr, 2u);
     return;
   }
-  if (is_ld) {
-    const int64_t p = s_tk[0];
-    if (p < P && tile_full(p)) {
+  // in round order the first tile is the rank (loaded again below if the chain
+  // takes its tiles by ticket)
+  if (is_ld && rank < P && tile_full(rank)) load_tile(0, rank);
+
+  // ---- operand tables, staged in buffers 1 .. 3 --------------------------------
+  char* stg = xb[1];
+  build_tables<TX>(a, d0, stg, tid, pin);
+  __syncthreads();
+  typename PT::AOp vop[NG][4], top[NG][4];
+  typename PT::UOp uop[NG][4];
+  // constants of scan lane (component ln, channel lq of group g), as (Re, -+Im):
+  // mu, lambda^256; for the terminal state lambda and lambda^(jstar+1)
+  const float sgn = (ln & 1) ? 1.f : -1.f;
+  float mur[NG], mus[NG];
+  float2 l256[NG], lam1[NG], lamt[NG];
 #pragma unroll
-      for (int i = 0; i < GPL; ++i)
-        dma_group<TX>(xb[0], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, lane,
-                      (wave - NQ) + LW * i);
+  for (int g = 0; g < NG; ++g) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      f4 uu;
+      stage_operands<TX>(stg, cb + 4 * g + k, ln, lq, top[g][k], vop[g][k], uu);
+      uop[g][k] = PT::u_op(uu);
     }
+    const float2* scg = reinterpret_cast<const float2*>(stg + TS::SC) + ((cb + 4 * g + lq) * 8 + (ln >> 1)) * 4;
+    const float2 mu = scg[0], l2 = scg[1], l1 = scg[2], lj = scg[3];
+    mur[g] = mu.x;
+    mus[g] = sgn * mu.y;
+    l256[g] = make_float2(l2.x, sgn * l2.y);
+    lam1[g] = make_float2(l1.x, sgn * l1.y);
+    lamt[g] = make_float2(lj.x, sgn * lj.y);
   }
 
-  // ---- operand tables: build the units claimed, then wait for the ones read --
-  for (uint32_t u = s_u[1]; u < (uint32_t)NW;) {
-    build_unit<TX>(a, d0 + 4 * (int)u, xb[NBUF - 1], tid, wave);
-    __syncthreads();
-    if (tid == 0) {
-      st_flag(a.tflag + (size_t)blk * NW + u, MK_T);
-      s_u[1] = atomicAdd(a.claim + blk, 1u);
-    }
-    __syncthreads();
-    u = s_u[1];
-  }
-  {
-    bool ok = wait_flag_eq(a.tflag + (size_t)blk * NW + wave, MK_T, a.hdr + 4);
-    if (is_ctl)  // control wave c reads the constants of quarter c: units 4c .. 4c+3
-      for (int j = 0; j < 4; ++j) ok = ok && wait_flag_eq(a.tflag + (size_t)blk * NW + 4 * wave + j, MK_T, a.hdr + 4);
-    if (!ok && lane == 0) {
-      atomicOr(a.hdr, 1u);
-      atomicOr(a.hdr + 4, 1u);
-    }
-  }
-  // The second and third tiles.  A tile's A is published only once its
-  // work-group has finished the tile before it, so tiles of one chain that
-  // follow each other must not sit in one work-group's queue: each of these
-  // claims waits (briefly, bounded) until every work-group of the chain has made
-  // its previous claim, which leaves the tiles a work-group holds one round of
-  // the chain's work-groups apart.  Tickets remain first come, first served, so
-  // a tile waited for always belongs to a running work-group.
+  // ---- the order of the chain's tiles: rounds once every work-group of the
+  // chain has arrived, else tickets; the first CAS decides for the chain -----
   if (tid == 0) {
-    const uint32_t G = gridDim.x / (uint32_t)a.nchains;
-#pragma unroll
-    for (int k = 1; k < 3; ++k) {
-      for (uint32_t n = 0; n < CLAIM_WAIT && ld_flag(a.ticket + chain) < (uint32_t)k * G; ++n)
-        __builtin_amdgcn_s_sleep(2);
-      s_tk[k] = atomicAdd(a.ticket + chain, 1u);
+    bool all = false;
+    for (uint32_t n = 0; n < ARRIVE_WAIT; ++n) {
+      if (ld_flag(cw + 1) >= G_) {
+        all = true;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
     }
-  }
-  typename PT::AOp vop[4], top[4];
-  f4 uop[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint4* tp = a.tab + (size_t)(d0 + c0 + k) * 3 * 64 + lane;
-    top[k] = PT::load_a_u4(ld_dev16(tp));
-    vop[k] = PT::load_a_u4(ld_dev16(tp + 64));
-    const uint4 uu = ld_dev16(tp + 128);
-    uop[k] = f4{__uint_as_float(uu.x), __uint_as_float(uu.y), __uint_as_float(uu.z), __uint_as_float(uu.w)};
-  }
-  // scan constant of lane (component ln, channel lq): mu, as (Re, -+Im)
-  const float2* scl = a.scal + ((size_t)(d0 + c0 + lq) * 8 + (ln >> 1)) * 4;
-  const float sgn = (ln & 1) ? 1.f : -1.f;
-  float mur, mus;
-  {
-    const float2 mu = ld_agent(scl);
-    mur = mu.x, mus = sgn * mu.y;
-  }
-  // control wave c (quarter c): lambda^256 of control lane (ln, lq), slot j (channel
-  // 16 c + 4 j + lq, mode ln / 2), kept in LDS
-  if (is_ctl) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float2 v = ld_agent(a.scal + ((size_t)(d0 + 16 * wave + 4 * j + lq) * 8 + (ln >> 1)) * 4 + 1);
-      sL2[wave][lane][j] = make_float2(v.x, sgn * v.y);
+    const uint32_t want = all ? 1u : 2u;
+    const uint32_t old = atomicCAS(cw + 2, 0u, want);
+    const uint32_t order = old == 0 ? want : old;
+    s_u[2] = order;
+    if (order == 1) {
+      s_tk[0] = rank;
+      s_tk[1] = rank + G_;
+      s_tk[2] = rank + 2 * G_;
+    } else {
+      s_tk[0] = atomicAdd(cw, 1u);
+      s_tk[1] = atomicAdd(cw, 1u);
+      s_tk[2] = atomicAdd(cw, 1u);
     }
   }
   // every earlier vector memory operation of the wave has completed (the first
-  // tile among them); then the loads of the second and third tiles, counted
+  // tile among them)
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
+  const bool by_ticket = s_u[2] != 1;
   uint32_t issued = 0, mark[NBUF] = {0, 0, 0, 0};
   if (is_ld) {
 #pragma unroll
-    for (int u = 1; u < 3; ++u) {
+    for (int u = 0; u < 3; ++u) {
       const int64_t p = s_tk[u];
-      if (p < P && tile_full(p)) {
-#pragma unroll
-        for (int i = 0; i < GPL; ++i)
-          dma_group<TX>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, lane,
-                        (wave - NQ) + LW * i);
+      if ((u > 0 || by_ticket) && p < P && tile_full(p)) {
+        load_tile(u, p);
         issued += GPL;
       }
       mark[u] = issued;
     }
   }
 
-  // ---- the tiles ------------------------------------------------------------
-  int64_t p_prev = -1;
-  for (int it = 0;; ++it) {
-    const int u = it & (NBUF - 1);
-    const int64_t p = s_tk[u];
+  // ---- the tiles, pipelined: iteration it runs pass 1 of tile it+1, then the
+  // carry and pass 2 of tile it, so that the states a carry reads were
+  // published one iteration earlier.  Every wave carries its own channels: lane
+  // (component ln, channel lq of group g) holds one value per group. ----------
+  int64_t p_prev = -1;  // the work-group's previous tile
+  float Icur[NG], Acur[NG], tail[NG];  // its inclusive end state; this tile's A; the partial last chunk
+#pragma unroll
+  for (int g = 0; g < NG; ++g) Icur[g] = Acur[g] = tail[g] = 0.f;
+  int it = -1;
+  for (;; ++it) {
+    const int64_t p = it >= 0 ? (int64_t)s_tk[it & (NBUF - 1)] : -1;  // carry and pass 2
     if (p >= P) break;
-    const bool full = tile_full(p);
-    const bool lastp = (p == P - 1);
-    char* xt = xb[u];
-    // arrival: this wave's share of a full tile, or a copy of one that is not full
-    if (full) {
-      if (is_ld) wait_vmcnt(SEPY ? 0 : (int)(issued - mark[u]));
-    } else {
-      copy_tile<TX, NT>(xt, reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, tid);
-    }
-    __syncthreads();
-    // the ticket of the tile three ahead (its buffer holds tile it-1, already stored)
-    uint32_t tk3 = 0;
-    if (tid == 0) tk3 = atomicAdd(a.ticket + chain, 1u);
-
-    // ---- pass 1: S = V x, moved so that lane (c, k) holds component c of channel
-    // k; A = sum_n mu^(15-n) S[n], the tile's end state from a zero start
-    float A;
-    {
-      typename PT::XOp xv[4];
-      float S[16];
-      PT::gather4(xt, c0, ln, lq, xv);
-      chunk_states<TX>(xv, vop, S);
-      A = S[0];
-#pragma unroll
-      for (int n = 1; n < 16; ++n) A = cfma_pair(mur, mus, A, S[n]);
-    }
-    // last tile of the chain: sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
-    float tail = 0.f;
-    if (lastp && a.h_out != nullptr) {
-      const float2 la = ld_agent(scl + 2);
-      for (int j = 0; j <= jstar; ++j) {
-        const float xj = to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + j) + (c0 + lq) * XE));
-        tail = cfma_pair(la.x, sgn * la.y, tail, (ln & 1) ? 0.f : xj);
-      }
-    }
-    reinterpret_cast<float*>(&sA[Q][lane])[wq] = A;
-    __syncthreads();
-
-    // ---- carry: control waves publish A, fold the entering state, publish I ----
-    if (is_ctl) {
-      const int QC = wave;  // the quarter this control wave carries
-      const f4 Av = sA[QC][lane];
-      const size_t slot = ((size_t)chain * P + p) * NQ + QC;
-      st_dev16(a.agg + slot * 64 + lane, __builtin_bit_cast(uint4, Av));
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-      if (lane == 0) st_flag(a.flag + slot, MK_A);
-      f4 E = zero;
-      if (p == 0) {
-        if (a.h0 != nullptr) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int d = d0 + 16 * QC + 4 * j + lq, m = ln >> 1;
-            if (d < a.D && m < a.M) E[j] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
-          }
-        }
+    const int un = (it + 1) & (NBUF - 1);
+    const int64_t pn = s_tk[un];  // pass 1
+    const bool has_next = pn < P;
+    // arrival of tile it+1: this wave's share of a full tile, or a copy
+    if (has_next) {
+      if (tile_full(pn)) {
+        if (is_ld) wait_vmcnt((int)(issued - mark[un]));
       } else {
-        // the nearest stop: the own previous tile, or a tile with I published;
-        // every tile between it and this one must have A published
-        int s = -1;
-        for (uint32_t n = 0;; ++n) {
-          const int64_t q = p - 1 - lane;
-          bool stop = false, ready = true;
-          if (p_prev >= 0 && q == p_prev) {
-            stop = true;
-          } else if (q > p_prev && q >= 0) {
-            const uint32_t f = ld_flag(a.flag + ((size_t)chain * P + q) * NQ + QC);
-            stop = f == MK_I;
-            ready = f == MK_A || f == MK_I;
-          }
-          const uint64_t stops = __ballot(stop), notready = __ballot(!ready);
-          if (stops != 0) {
-            const int s0 = __builtin_ctzll(stops);
-            if ((notready & ((1ull << s0) - 1)) == 0) {
-              s = s0;
-              break;
-            }
-          }
-          if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) break;
-          __builtin_amdgcn_s_sleep(1);
-        }
-        if (s < 0) {
-          if (lane == 0) {  // gave up: the fold starts from zero
-            atomicOr(a.hdr, 1u);
-            atomicOr(a.hdr + 4, 1u);
-          }
-        } else {
-          const int64_t qs = p - 1 - s;
-          if (p_prev >= 0 && qs == p_prev) {
-            E = sI[QC][lane];
-          } else {
-            E = __builtin_bit_cast(f4, ld_dev16(a.inc + (((size_t)chain * P + qs) * NQ + QC) * 64 + lane));
-          }
-          // E <- lambda^256 E + A_q for q = qs+1 .. p-1, FB loads at a time
-          constexpr int FB = 4;
-          for (int jb = s - 1; jb >= 0; jb -= FB) {
-            f4 Aq[FB];
+        copy_tile<TX, NT>(xb[un], reinterpret_cast<const TX*>(a.x), b, pn * TILE_T, d0, a.L, a.D, tid);
+      }
+    }
+    __syncthreads();
+    // the rows of tile it-1 (p_prev) leave: its buffer is this iteration's H buffer
+    if (!SEPY && it >= 1) {
+      store_tile((it - 1) & (NBUF - 1), p_prev);
+      if (is_ld && tile_full(p_prev)) issued += GPL;
+    }
+    // the tile three ahead (its buffer slot held tile it-1)
+    if (tid == 0 && it >= 0) s_tk[(it + 3) & (NBUF - 1)] = by_ticket ? atomicAdd(cw, 1u) : rank + (uint32_t)(it + 3) * G_;
+
+    // ---- pass 1 (tile it+1): S = V x, moved so that lane (c, k) holds component
+    // c of channel k; A = sum_n mu^(15-n) S[n], the tile's end state from a zero
+    // start, published at once; on the chain's last tile also
+    // sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
+    float Anext[NG];
+    if (has_next) {
+      const char* xn = xb[un];
 #pragma unroll
-            for (int i = 0; i < FB; ++i) {
-              const int jj = jb - i < 0 ? 0 : jb - i;  // clamped: an extra load of a published state
-              Aq[i] = __builtin_bit_cast(f4, ld_dev16(a.agg + (((size_t)chain * P + (p - 1 - jj)) * NQ + QC) * 64 + lane));
-            }
+      for (int g = 0; g < NG; ++g) {
+        typename PT::XOp xv[4];
+        float S[16];
+        PT::gather4(xn, cb + 4 * g, ln, lq, xv);
+        chunk_states<TX>(xv, vop[g], S);
+        float A = S[0];
 #pragma unroll
-            for (int i = 0; i < FB; ++i) {
-              if (jb - i >= 0) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                  const float2 l2 = sL2[QC][lane][j];
-                  E[j] = cfma_pair(l2.x, l2.y, E[j], Aq[i][j]);
-                }
-              }
-            }
+        for (int n = 1; n < 16; ++n) A = cfma_pair(mur[g], mus[g], A, S[n]);
+        Anext[g] = A;
+        if (pn == P - 1 && a.h_out != nullptr) {
+          const int ch = cb + 4 * g + lq;
+          float t = 0.f;
+          for (int j = 0; j <= jstar; ++j) {
+            const float xj = to_f32(*reinterpret_cast<const TX*>(xn + XLay<XE>::off(nstar * CHUNK + j) + ch * XE));
+            t = cfma_pair(lam1[g].x, lam1[g].y, t, (ln & 1) ? 0.f : xj);
           }
+          tail[g] = t;
         }
       }
-      f4 I;
+      put_state<NG>(a_slot(pn), Anext, TAG);
+    }
+    if (it < 0) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const float2 l2 = sL2[QC][lane][j];
-        I[j] = cfma_pair(l2.x, l2.y, E[j], Av[j]);
+      for (int g = 0; g < NG; ++g) Acur[g] = Anext[g];
+      continue;
+    }
+
+    // ---- carry (tile it): E, the state entering the tile, from the work-group's
+    // own previous tile (in round order G tiles back) or h0 at the chain's start,
+    // and the published A of the tiles between, oldest first,
+    // E <- lambda^256 E + A; then I = lambda^256 E + A(this tile) ---------------
+    float E[NG];
+    int64_t q = 0;  // the first tile folded
+    bool ok = true;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) E[g] = 0.f;
+    if (p_prev >= 0) {
+      q = p_prev + 1;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) E[g] = Icur[g];
+    } else if (a.h0 != nullptr) {  // the chain's start
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
+        if (d < a.D && m < a.M) E[g] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
       }
-      st_dev16(a.inc + slot * 64 + lane, __builtin_bit_cast(uint4, I));
-      __builtin_amdgcn_s_waitcnt(0x0F70);
-      if (lane == 0) st_flag(a.flag + slot, MK_I);
-      sE[QC][lane] = E;
-      sI[QC][lane] = I;
+    }
+    for (; ok && q < p; q += FB) {
+      float Aq[FB][NG];
+      for (uint32_t n = 0;; ++n) {
+        bool mine = true;
+#pragma unroll
+        for (int i = 0; i < FB; ++i) mine = get_state<NG>(a_slot(q + i < p ? q + i : q), TAG, Aq[i]) && mine;
+        if (__ballot(!mine) == 0) break;
+        if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (!ok) break;
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        if (q + i < p) {
+#pragma unroll
+          for (int g = 0; g < NG; ++g) E[g] = cfma_pair(l256[g].x, l256[g].y, E[g], Aq[i][g]);
+        }
+      }
+    }
+    if (!ok && lane == 0) {  // gave up: the outputs of this call are wrong
+      atomicOr(a.hdr, 1u);
+      atomicOr(a.hdr + 4, 1u);
+    }
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      Icur[g] = cfma_pair(l256[g].x, l256[g].y, E[g], Acur[g]);
+      Acur[g] = Anext[g];
     }
     p_prev = p;
-    if (tid == 0) s_tk[(it + 3) & (NBUF - 1)] = tk3;
+    // the row stores have read the H buffer before any wave writes H into it
     __syncthreads();
 
-    // ---- pass 2: chunk entering states, y = T x + U H -------------------------
-    // (x is still in the tile buffer: S and the operands are formed again rather
-    // than held in registers through the carry phase)
-    typename PT::XOp xv[4];
-    float S[16];
-    PT::gather4(xt, c0, ln, lq, xv);
-    chunk_states<TX>(xv, vop, S);
-    {
-      float h = reinterpret_cast<const float*>(&sE[Q][lane])[wq];
-      float hn = 0.f;
+    // ---- pass 2 (tile it): chunk entering states, y = T x + U H, group by group.
+    // (x is still in the tile buffer: S and the operands are formed again.)  H
+    // moves through LDS, in the buffer of tile it-1 (its rows have left): lane
+    // (c, k) writes component c of chunk n at [k][n][c], lane (n, q) reads
+    // components 4q .. 4q+3 of chunk n.
+    const bool lastp = (p == P - 1);
+    char* xt = xb[it & (NBUF - 1)];
+    float* hs = reinterpret_cast<float*>(xb[(it + 3) & (NBUF - 1)]) + wave * 4 * HKS;
 #pragma unroll
-      for (int n = 0; n < 16; ++n) {
-        if (n == nstar) hn = h;
-        const float nx = cfma_pair(mur, mus, h, S[n]);
-        S[n] = h;  // now the state entering chunk n
-        h = nx;
-      }
-      if (lastp && a.h_out != nullptr) {
-        // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
-        const float2 lt = ld_agent(scl + 3);
-        const float hl = cfma_pair(lt.x, sgn * lt.y, hn, tail);
-        const int d = d0 + c0 + lq, m = ln >> 1;
-        if (d < a.D && m < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)] = hl;
-      }
-    }
-    f4 acc[4];
-    {
-      // H through LDS (the buffer that takes the tile three ahead, free until
-      // the end of this tile), HR channels per round: lane (c, k) writes
-      // component c of chunk n at [k][n][c], lane (n, q) reads components
-      // 4q .. 4q+3 of chunk n
-      float* hs = reinterpret_cast<float*>(xb[(it + 3) & (NBUF - 1)]) + wave * HR * HKS;
+    for (int g = 0; g < NG; ++g) {
+      typename PT::XOp xv[4];
+      float S[16];
+      PT::gather4(xt, cb + 4 * g, ln, lq, xv);
+      chunk_states<TX>(xv, vop[g], S);
+      {
+        float h = E[g];
+        float hn = 0.f;
 #pragma unroll
-      for (int r0 = 0; r0 < 4; r0 += HR) {
-        if (lq >= r0 && lq < r0 + HR) {
-#pragma unroll
-          for (int n = 0; n < 16; ++n) hs[(lq - r0) * HKS + n * 16 + ln] = S[n];
+        for (int n = 0; n < 16; ++n) {
+          if (n == nstar) hn = h;
+          const float nx = cfma_pair(mur[g], mus[g], h, S[n]);
+          S[n] = h;  // now the state entering chunk n
+          h = nx;
         }
-        wave_lds_order();
-#pragma unroll
-        for (int kk = 0; kk < HR; ++kk) {
-          const int k = r0 + kk;
-          const f4 hb = *reinterpret_cast<const f4*>(&hs[kk * HKS + ln * 16 + 4 * lq]);
-          acc[k] = mma_f32(uop[k], hb, PT::mma(top[k], xv[k], zero));
+        if (lastp && a.h_out != nullptr) {
+          // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
+          const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
+          const float hl = cfma_pair(lamt[g].x, lamt[g].y, hn, tail[g]);
+          if (d < a.D && m < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)] = hl;
         }
-        wave_lds_order();
       }
+#pragma unroll
+      for (int n = 0; n < 16; ++n) hs[lq * HKS + n * 16 + ln] = S[n];
+      wave_lds_order();
+      f4 acc[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const f4 hb = *reinterpret_cast<const f4*>(&hs[k * HKS + ln * 16 + 4 * lq]);
+        acc[k] = PT::mma_u(uop[g][k], hb, PT::mma(top[g][k], xv[k], zero));
+      }
+      wave_lds_order();
+      if (SEPY)
+        put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4, d0 + cb + 4 * g,
+                      a.L, a.D);
+      else
+        put_y4<TY>(xt, cb + 4 * g, ln, lq, acc);
     }
-    if (SEPY)
-      put_y4_global(reinterpret_cast<float*>(a.y), acc, b, p * TILE_T + ln * CHUNK + lq * 4, d0 + c0, a.L, a.D);
-    else
-      put_y4<TY>(xt, c0, ln, lq, acc);
     __syncthreads();
 
-    // ---- load waves: the tile three ahead, then this tile's rows --------------
+    // ---- load waves: the tile three ahead (into this iteration's H buffer) ----
     if (is_ld) {
       const int u3 = (it + 3) & (NBUF - 1);
       const int64_t p3 = s_tk[u3];
       if (p3 < P && tile_full(p3)) {
-#pragma unroll
-        for (int i = 0; i < GPL; ++i)
-          dma_group<TX>(xb[u3], reinterpret_cast<const TX*>(a.x), b, p3 * TILE_T, d0, a.L, a.D, lane,
-                        (wave - NQ) + LW * i);
+        load_tile(u3, p3);
         issued += GPL;
       }
       mark[u3] = issued;
-      if (!SEPY && full) {
-#pragma unroll
-        for (int i = 0; i < GPL; ++i)
-          store_group<TY>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, lane, (wave - NQ) + LW * i);
-        issued += GPL;
-      }
     }
-    if (!SEPY && !full)
-      store_tile_part<TY, NT>(reinterpret_cast<TY*>(a.y), xt, b, p * TILE_T, d0, a.L, a.D, tid);
   }
+  // the rows of the last tile
+  if (!SEPY && it >= 1) store_tile((it - 1) & (NBUF - 1), p_prev);
 
-  // ---- the last work-group to finish resets the counters for the next call --
-  __syncthreads();
-  if (tid == 0) s_u[2] = atomicAdd(a.hdr + 3, 1u);
-  __syncthreads();
-  if (s_u[2] == gridDim.x - 1) {
-    for (int i = tid; i < a.nchains; i += NT) st_flag(a.ticket + i, 0u);
-    for (int i = tid; i < a.NB; i += NT) st_flag(a.claim + i, 0u);
-    if (tid == 0) {
-      st_flag(a.hdr + 2, 0u);
-      st_flag(a.hdr + 3, 0u);
-      st_flag(a.hdr + 4, 0u);
-      st_flag(a.hdr + 1, ep + 1);
+  // ---- the last work-group of a chain resets the chain's counters, the last
+  // chain to finish the call's words ------------------------------------------
+  if (tid == 0) {
+    const uint32_t f = atomicAdd(cw + 3, 1u);
+    if (f == G_ - 1) {
+      st_flag(cw + 0, 0u);
+      st_flag(cw + 1, 0u);
+      st_flag(cw + 2, 0u);
+      st_flag(cw + 3, 0u);
+      if (atomicAdd(a.hdr + 2, 1u) == (uint32_t)a.nchains - 1) {
+        st_flag(a.hdr + 2, 0u);
+        st_flag(a.hdr + 4, 0u);
+        st_flag(a.hdr + 1, ep + 1);
+      }
     }
   }
 }

@@ -75,15 +75,10 @@ struct StreamArgs {
   const float* h0;     // [B][D][M][2] or null
   float* h_out;        // [B][D][M][2] or null
   uint32_t* hdr;       // [0] status (bit 0: a wait gave up, bit 1: stale counters), [1] epoch,
-                       // [2] arrived work-groups, [3] finished work-groups, [4] a wait of this call gave up
-  uint32_t* ticket;    // [nchains] next tile of each chain
-  uint32_t* claim;     // [NB] next table unit of each channel block
-  uint32_t* tflag;     // [NB][DW / 4] table unit published
-  uint32_t* flag;      // [nchains][P][DW / 16] tile state published
-  uint4* tab;          // [NB DW][3][64] T, V, U in lane order (16 bytes per lane)
-  float2* scal;        // [NB DW][8][4] mu = lambda^16, lambda^256, lambda, lambda^(jstar+1)
-  uint4* agg;          // [nchains][P][DW / 16][64] A (four floats per control lane)
-  uint4* inc;          // [nchains][P][DW / 16][64] I
+                       // [2] finished chains, [4] a wait of this call gave up
+  uint32_t* chainw;    // [nchains][4]: next ticket, arrived work-groups, tile order (0 open, 1 rounds,
+                       // 2 tickets), finished work-groups
+  uint64_t* agg;        // [nchains][P][8 waves][64][DW / 32] A of each tile (float | tag << 32 per word)
 };
 
 struct BwdArgs {

@@ -215,3 +215,24 @@ def test_h_out_may_alias_h0():
         torch.cuda.synchronize()
         assert torch.equal(y1, y2)
         assert torch.equal(h1, st)
+
+
+def test_workspace_reused_across_shapes():
+    """One zero-filled forward workspace serves calls of different shapes in turn
+    (different numbers of chains, dtypes and mode counts): every call leaves
+    status 0 and matches the oracle recurrence."""
+    from paper_2607_05583_amd import ops
+    shapes = [(2, 3001, 70, 5, "bf16", 51), (4, 2048, 256, 8, "f32", 52), (1, 1024, 64, 8, "bf16", 53),
+              (8, 700, 256, 8, "f32", 54), (4, 2048, 256, 8, "bf16", 55), (2, 3001, 70, 5, "bf16", 56)]
+    need = max(ops.workspace_bytes(ops.RES_OP_FWD, torch.float32 if act == "f32" else torch.bfloat16, B, L, D, M)
+               for B, L, D, M, act, _ in shapes)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for B, L, D, M, act, seed in shapes:
+        say(f"shared workspace B={B} L={L} D={D} M={M} {act}")
+        prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True, with_h0=True)
+        x = dev_act(prob["x"], act)
+        y, hout = ops.resonator_mix_fwd(x, *params_dev(prob), h0=dev_f32(prob["h0"]), ws=ws, return_state=True)
+        assert ops.resonator_fwd_status(ws) == 0
+        yr, hr = O.mix_recurrence(act64(prob["x"], act), *params_np(prob), h0=prob["h0"])
+        assert rel_err(host(y), yr) <= tol(act, act)
+        assert rel_err(host(hout), hr) <= (1e-4 if act == "f32" else 2e-2)
