@@ -130,6 +130,33 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
  * RES_ERR_INVALID_ARG / RES_ERR_MISALIGNED / RES_ERR_HIP.
  */
 int resonator_fwd_status(void* ws, uint32_t* status, void* stream);
+/* The same for the static scratch of resonator_mix_fwd_noalloc on the current device. */
+int resonator_fwd_status_noalloc(uint32_t* status, void* stream);
+
+/*
+ * Allocation-free forward, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation).  Computes exactly what resonator_mix_fwd computes, with the same
+ * arguments except the workspace: the library uses a static device array of
+ * RES_NOALLOC_SCRATCH_BYTES bytes instead, one per GPU, held until the process
+ * ends.  The call allocates nothing (no hipMalloc, no allocating library call).
+ *   - stream must belong to the calling thread's current device (NULL = that
+ *     device's default stream); else RES_ERR_INVALID_ARG.
+ *   - Sizes whose resonator_workspace_bytes(RES_OP_FWD, ...) exceed
+ *     RES_NOALLOC_SCRATCH_BYTES return RES_ERR_WORKSPACE with nothing launched.
+ *   - All calls on one GPU share its scratch: calls that overlap in time on one
+ *     GPU (concurrent streams, several host threads) race and give wrong results;
+ *     calls ordered on one stream are safe.
+ *   - The first call on a device looks up the scratch's device address (not
+ *     inside a graph capture: make one call before capturing).
+ * Other arguments, dtypes, alignment and errors as resonator_mix_fwd.
+ */
+#define RES_NOALLOC_SCRATCH_BYTES (32u << 20)
+int resonator_mix_fwd_noalloc(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t L,
+                              int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                              const float* phase, const float* h0, float* h_out, void* stream);
+/* RES_NOALLOC_SCRATCH_BYTES, the largest workspace resonator_mix_fwd_noalloc can serve. */
+size_t resonator_mix_fwd_noalloc_max_bytes(void);
 
 /*
  * Prompt state for decoding (Sec. 3.2, cache construction): the terminal state

@@ -27,7 +27,8 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_grouped_linear", "resonator_block_diag_weight", "resonator_block_diag_extract",
            "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_weight",
            "resonator_grouped_linear_bwd_weight_split", "resonator_grouped_linear_bwd_weight_split_workspace_bytes",
-           "resonator_fwd_status")
+           "resonator_mix_fwd_noalloc", "resonator_mix_fwd_noalloc_max_bytes", "resonator_fwd_status",
+           "resonator_fwd_status_noalloc")
 
 _lib = None
 
@@ -95,8 +96,14 @@ def _declare(lib):
     lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes.argtypes = [i64, i64, i64]
     lib.resonator_grouped_linear_bwd_weight_split.restype = i32
     lib.resonator_grouped_linear_bwd_weight_split.argtypes = [vp, vp, i32, fp, i64, i64, i64, i64, i32, vp, sz, vp]
+    lib.resonator_mix_fwd_noalloc.restype = i32
+    lib.resonator_mix_fwd_noalloc.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, fp, vp]
     lib.resonator_fwd_status.restype = i32
     lib.resonator_fwd_status.argtypes = [vp, ctypes.POINTER(ctypes.c_uint32), vp]
+    lib.resonator_fwd_status_noalloc.restype = i32
+    lib.resonator_fwd_status_noalloc.argtypes = [ctypes.POINTER(ctypes.c_uint32), vp]
+    lib.resonator_mix_fwd_noalloc_max_bytes.restype = sz
+    lib.resonator_mix_fwd_noalloc_max_bytes.argtypes = []
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
 

@@ -5,6 +5,7 @@
 #include <cstdint>
 #include <initializer_list>
 #include <cstdio>
+#include <mutex>
 #include <string>
 
 #include "../../include/resonator.h"
@@ -37,6 +38,49 @@ int fail(int code, const char* fmt, ...) {
 
 int hip_fail(hipError_t e, const char* what) {
   return fail(RES_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace
+
+// Workspace of resonator_mix_fwd_noalloc: every GPU the library runs on holds
+// its own copy until the process ends, zero at load like any device variable
+// without an initialiser (a forward workspace must start zero-filled; each
+// forward leaves it ready for the next).  Host code never passes this name to a
+// kernel (on the host it is only a stand-in); it uses the device address that
+// hipGetSymbolAddress gives for the current device.
+static __device__ __align__(256) unsigned char scratch[RES_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[SCRATCH_MAX_DEVICES];  // device address of `scratch`, per device, taken once
+
+// Device address of the static scratch on the device of `stream` (which must be
+// the calling thread's current device), looked up on the first call per device.
+int noalloc_scratch(void* stream, void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (stream != nullptr) {
+    hipDevice_t sdev = 0;
+    if ((e = hipStreamGetDevice((hipStream_t)stream, &sdev)) != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    if ((int)sdev != dev)
+      return fail(RES_ERR_INVALID_ARG, "the stream belongs to device %d, the current device is %d", (int)sdev, dev);
+  }
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES)
+    return fail(RES_ERR_UNSUPPORTED, "device index %d beyond the %d the scratch table covers", dev,
+                SCRATCH_MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* p = nullptr;
+    if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+      return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr || ((uintptr_t)p % 256) != 0) return fail(RES_ERR_HIP, "scratch address unusable");
+    g_scratch_addr[dev] = p;
+  }
+  *out = g_scratch_addr[dev];
+  return RES_OK;
 }
 
 size_t elt_size(res_dtype_t t) { return t == RES_BF16 ? 2 : 4; }
@@ -193,10 +237,11 @@ size_t resonator_workspace_bytes(int op, res_dtype_t act_dt, int64_t B, int64_t 
 
 namespace {
 
-// Validation and dispatch of the forward.
+// Validation and dispatch of the forward; noalloc: the allocation-free entry
+// point (ws and ws_bytes ignored, the workspace is the device's static scratch).
 int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t L, int64_t D,
                  int64_t M, const float* gamma, const float* omega, const float* amp, const float* phase,
-                 const float* h0, float* h_out, void* ws, size_t ws_bytes, void* stream) {
+                 const float* h0, float* h_out, void* ws, size_t ws_bytes, void* stream, bool noalloc) {
   int rc = check_sizes(B, L, D, M, false);
   if (rc) return rc;
   if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
@@ -212,6 +257,15 @@ int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int
     return fail(RES_ERR_INVALID_ARG, "y must not overlap x");
   const Geometry g = make_geom(x_dt, B, L, D, M);
   const WsLayout w = make_layout(RES_OP_FWD, x_dt, g);
+  if (noalloc) {
+    if (w.total > (size_t)RES_NOALLOC_SCRATCH_BYTES)
+      return fail(RES_ERR_WORKSPACE,
+                  "sizes need %zu bytes of workspace, more than the %zu-byte static scratch of "
+                  "resonator_mix_fwd_noalloc; call resonator_mix_fwd with a workspace",
+                  w.total, (size_t)RES_NOALLOC_SCRATCH_BYTES);
+    if ((rc = noalloc_scratch(stream, &ws))) return rc;
+    ws_bytes = (size_t)RES_NOALLOC_SCRATCH_BYTES;
+  }
   if (!ws || ws_bytes < w.total)
     return fail(RES_ERR_WORKSPACE, "workspace too small: need %zu bytes, got %zu", w.total, ws_bytes);
   if (!aligned(ws, 256)) return fail(RES_ERR_MISALIGNED, "workspace must be 256-byte aligned");
@@ -309,8 +363,18 @@ int resonator_mix_fwd(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt
                       int64_t L, int64_t D, int64_t M, const float* gamma, const float* omega,
                       const float* amp, const float* phase, const float* h0, float* h_out,
                       void* ws, size_t ws_bytes, void* stream) {
-  return mix_fwd_impl(x, x_dt, y, y_dt, B, L, D, M, gamma, omega, amp, phase, h0, h_out, ws, ws_bytes, stream);
+  return mix_fwd_impl(x, x_dt, y, y_dt, B, L, D, M, gamma, omega, amp, phase, h0, h_out, ws, ws_bytes, stream,
+                      false);
 }
+
+int resonator_mix_fwd_noalloc(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t L,
+                              int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                              const float* phase, const float* h0, float* h_out, void* stream) {
+  return mix_fwd_impl(x, x_dt, y, y_dt, B, L, D, M, gamma, omega, amp, phase, h0, h_out, nullptr, 0, stream,
+                      true);
+}
+
+size_t resonator_mix_fwd_noalloc_max_bytes(void) { return (size_t)RES_NOALLOC_SCRATCH_BYTES; }
 
 int resonator_fwd_status(void* ws, uint32_t* status, void* stream) {
   if (!ws || !status) return fail(RES_ERR_INVALID_ARG, "ws and status must be non-null");
@@ -322,6 +386,13 @@ int resonator_fwd_status(void* ws, uint32_t* status, void* stream) {
   if ((e = hipMemsetAsync(ws, 0, sizeof(uint32_t), st)) != hipSuccess) return hip_fail(e, "status clear");
   if ((e = hipStreamSynchronize(st)) != hipSuccess) return hip_fail(e, "status synchronize");
   return RES_OK;
+}
+
+int resonator_fwd_status_noalloc(uint32_t* status, void* stream) {
+  void* ws = nullptr;
+  const int rc = noalloc_scratch(stream, &ws);
+  if (rc) return rc;
+  return resonator_fwd_status(ws, status, stream);
 }
 
 int resonator_state_init(const void* x_prompt, res_dtype_t x_dt, int64_t B, int64_t L_prompt,
