@@ -1,5 +1,6 @@
 // C ABI of the resonant mixing library: argument validation, workspace layout
 // and kernel dispatch.  Declared in include/resonator.h.
+#include <algorithm>
 #include <cstdarg>
 #include <cmath>
 #include <cstdint>
@@ -110,7 +111,7 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
 // bytes are the header (status word first); the forward workspace must be zero
 // before its first use and each call leaves it ready for the next.
 struct StreamLayout {
-  size_t hdr, chainw, agg, total;
+  size_t hdr, chainw, agg, ring, total;
 };
 // The single-pass forward keeps per-chain counters in a fixed area of the
 // workspace (every call resets the counters it used), ahead of the tagged
@@ -131,6 +132,8 @@ StreamLayout make_stream_layout(const Geometry& g) {
   off += (size_t)STREAM_MAX_CHAINS * 4 * sizeof(uint32_t);
   w.agg = off;
   off += align256(tiles * state);
+  w.ring = off;
+  off += align256((size_t)std::min(nchains, (size_t)STREAM_RING_CHAINS) * STREAM_RING * state);
   w.total = off;
   return w;
 }
@@ -305,6 +308,7 @@ int mix_fwd_impl(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int
     a.hdr = (uint32_t*)(base + sl.hdr);
     a.chainw = (uint32_t*)(base + sl.chainw);
     a.agg = (uint64_t*)(base + sl.agg);
+    a.ring = B * g.NB <= STREAM_RING_CHAINS ? (uint64_t*)(base + sl.ring) : nullptr;
     const int grid = fwd_stream_grid(B * g.NB, g.P, ncu > 0 ? ncu : 256);
     if (x_dt == RES_F32)
       e = launch_fwd_stream<float, float>(a, grid, st, ev0, ev1);

@@ -1007,6 +1007,15 @@ struct TabStage {
   static constexpr int BYTES = SC + DW * 8 * 4 * 8;
 };
 
+// A float64 moved across lanes by a DPP pattern (its two halves).
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, 0xF, 0xF, false);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, 0xF, 0xF, false);
+  return __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+}
+
 // The float32 parameters of thread (k, m) = 8 k + m: channel d0 + k, mode m
 // (zeros outside D x M and for threads beyond the block's channels).
 struct ModeIn {
@@ -1068,23 +1077,31 @@ __device__ void build_tables(const StreamArgs& a, int d0, char* st, int tid, con
   sc[1] = make_float2((float)l2.x, (float)l2.y);
   sc[2] = make_float2((float)z.x, (float)z.y);
   sc[3] = make_float2((float)lt.x, (float)lt.y);
+  // sum over the 8 mode lanes of the channel, halving the taps at each of three
+  // exchanges (DPP moves of the two halves of a float64): lane m <-> 7-m keeps
+  // taps 0..7 (m < 4) or 8..15, then lane m <-> m^2 keeps a half of those by bit
+  // 1 of m, then m <-> m^1 by bit 0; lane m ends with the full sums of taps
+  // tau0 and tau0 + 1, tau0 = 8 [m >= 4] + 4 bit1(m) + 2 bit0(m)
+  double t8[8], t4[4], t2[2];
+  {
+    const bool h = m >= 4, b1 = (m >> 1) & 1, b0 = m & 1;
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    double v = tp[j];
-    v += __shfl_xor(v, 1);
-    v += __shfl_xor(v, 2);
-    v += __shfl_xor(v, 4);
-    tp[j] = v;
+    for (int i = 0; i < 8; ++i) t8[i] = (h ? tp[8 + i] : tp[i]) + dpp_f64<0x141>(h ? tp[i] : tp[8 + i]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t4[i] = (b1 ? t8[4 + i] : t8[i]) + dpp_f64<0x4E>(b1 ? t8[i] : t8[4 + i]);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) t2[i] = (b0 ? t4[2 + i] : t4[i]) + dpp_f64<0xB1>(b0 ? t4[i] : t4[2 + i]);
   }
-  if (m == 0) {
-    uint32_t* tap = reinterpret_cast<uint32_t*>(st + S::TAP) + k * 16;
+  {
+    const int tau0 = (m >= 4 ? 8 : 0) + ((m >> 1) & 1) * 4 + (m & 1) * 2;
+    uint32_t* tap = reinterpret_cast<uint32_t*>(st + S::TAP) + k * 16 + tau0;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
+    for (int j = 0; j < 2; ++j) {
       if (sizeof(TX) == 4) {
-        tap[j] = __float_as_uint((float)tp[j]);
+        tap[j] = __float_as_uint((float)t2[j]);
       } else {
-        const bf16_t hi = from_f32<bf16_t>((float)tp[j]);
-        const bf16_t lo = from_f32<bf16_t>((float)(tp[j] - (double)to_f32(hi)));
+        const bf16_t hi = from_f32<bf16_t>((float)t2[j]);
+        const bf16_t lo = from_f32<bf16_t>((float)(t2[j] - (double)to_f32(hi)));
         tap[j] = (uint32_t)hi | ((uint32_t)lo << 16);
       }
     }
@@ -1239,27 +1256,50 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       store_tile_part<TY, NT>(reinterpret_cast<TY*>(a.y), xb[u], b, p * TILE_T, d0, a.L, a.D, tid);
     }
   };
-  // this lane's words of the published end state of tile q
+  // this lane's words of the published A of tile q, and of the ring slot of the
+  // published I of tile q (tagged with q: a slot is used again RING tiles later)
   auto a_slot = [&](int64_t q) { return a.agg + ((((size_t)chain * P + q) * NW + wave) * 64 + lane) * NG; };
+  auto i_slot = [&](int64_t q) {
+    return a.ring + ((((size_t)chain * STREAM_RING + (size_t)(q % STREAM_RING)) * NW + wave) * 64 + lane) * NG;
+  };
+  auto tag_i = [&](int64_t q) { return (ep + 1u) * 65536u + (uint32_t)(q & 0xFFFF); };
 
-  // ---- arrival: rank in the chain, and the rank's first tile ------------------
+  // ---- arrival, the first tile, the tables ----------------------------------
+  // In round order the j-th work-group of a chain by block index takes tiles
+  // j, j + G, ... (round order is chosen only once all G have arrived).  Its
+  // first tile loads at once (again below if the chain takes tickets); the
+  // arrival count and a first look at the chain's arrivals come back while the
+  // tables are built.
+  const uint32_t rank = blockIdx.x / (uint32_t)a.nchains;
   const ModeIn pin = load_mode<TX>(a, d0, tid);  // before any tile load of the wave
-  if (tid == 0) s_u[1] = atomicAdd(cw + 1, 1u);
-  __syncthreads();
-  const uint32_t rank = s_u[1];
-  // more arrivals than work-groups: the counters were not in their initial
-  // state (workspace not zeroed, or changed meanwhile); touch nothing
-  if (rank >= G_) {
-    if (tid == 0) atomicOr(a.hdr, 2u);
-    return;
+  uint32_t arr = 0, arrived = 0;
+  if (tid == 0) {
+    arr = atomicAdd(cw + 1, 1u);
+    arrived = ld_flag(cw + 1);
   }
-  // in round order the first tile is the rank (loaded again below if the chain
-  // takes its tiles by ticket)
   if (is_ld && rank < P && tile_full(rank)) load_tile(0, rank);
-
-  // ---- operand tables, staged in buffers 1 .. 3 --------------------------------
-  char* stg = xb[1];
+  char* stg = xb[1];  // the tables are staged in buffers 1 .. 3
   build_tables<TX>(a, d0, stg, tid, pin);
+  // ---- the order of the chain's tiles: rounds once every work-group of the
+  // chain has arrived, else tickets; the first CAS decides for the chain (its
+  // answer is read after the operands are formed).  More arrivals than
+  // work-groups: the counters were not in their initial state (workspace not
+  // zeroed, or changed meanwhile); such a work-group touches nothing. -------
+  uint32_t order_old = 0, order_want = 0;
+  if (tid == 0) {
+    if (arr >= G_) {
+      atomicOr(a.hdr, 2u);
+      order_want = 0;  // stale
+    } else {
+      bool all = arrived >= G_;
+      for (uint32_t n = 0; !all && n < ARRIVE_WAIT; ++n) {
+        __builtin_amdgcn_s_sleep(2);
+        all = ld_flag(cw + 1) >= G_;
+      }
+      order_want = all ? 1u : 2u;
+      order_old = atomicCAS(cw + 2, 0u, order_want);
+    }
+  }
   __syncthreads();
   typename PT::AOp vop[NG][4], top[NG][4];
   typename PT::UOp uop[NG][4];
@@ -1285,26 +1325,14 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
     lamt[g] = make_float2(lj.x, sgn * lj.y);
   }
 
-  // ---- the order of the chain's tiles: rounds once every work-group of the
-  // chain has arrived, else tickets; the first CAS decides for the chain -----
   if (tid == 0) {
-    bool all = false;
-    for (uint32_t n = 0; n < ARRIVE_WAIT; ++n) {
-      if (ld_flag(cw + 1) >= G_) {
-        all = true;
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-    const uint32_t want = all ? 1u : 2u;
-    const uint32_t old = atomicCAS(cw + 2, 0u, want);
-    const uint32_t order = old == 0 ? want : old;
+    const uint32_t order = order_want == 0 ? 0u : order_old == 0 ? order_want : order_old;
     s_u[2] = order;
     if (order == 1) {
       s_tk[0] = rank;
       s_tk[1] = rank + G_;
       s_tk[2] = rank + 2 * G_;
-    } else {
+    } else if (order == 2) {
       s_tk[0] = atomicAdd(cw, 1u);
       s_tk[1] = atomicAdd(cw, 1u);
       s_tk[2] = atomicAdd(cw, 1u);
@@ -1314,6 +1342,7 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
   // tile among them)
   __builtin_amdgcn_s_waitcnt(0x0F70);
   __syncthreads();
+  if (s_u[2] == 0) return;  // stale counters
   const bool by_ticket = s_u[2] != 1;
   uint32_t issued = 0, mark[NBUF] = {0, 0, 0, 0};
   if (is_ld) {
@@ -1395,16 +1424,29 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       continue;
     }
 
-    // ---- carry (tile it): E, the state entering the tile, from the work-group's
-    // own previous tile (in round order G tiles back) or h0 at the chain's start,
-    // and the published A of the tiles between, oldest first,
-    // E <- lambda^256 E + A; then I = lambda^256 E + A(this tile) ---------------
+    // ---- carry (tile it): E, the state entering the tile, from a stop tile's
+    // inclusive end state I and the published A of the tiles between, oldest
+    // first, E <- lambda^256 E + A; then I = lambda^256 E + A(this tile).  The
+    // stop is the work-group's own previous tile (in rounds G tiles back; h0 at
+    // the chain's start), except for chains of 2 to 4 work-groups in rounds,
+    // where every tile starts from the previous tile's I, published in a ring. -
     float E[NG];
     int64_t q = 0;  // the first tile folded
     bool ok = true;
 #pragma unroll
     for (int g = 0; g < NG; ++g) E[g] = 0.f;
-    if (p_prev >= 0) {
+    const bool chained = a.ring != nullptr && !by_ticket && G_ >= 2 && G_ <= 4;
+    if (chained && p > 0) {
+      q = p;
+      for (uint32_t n = 0;; ++n) {
+        if (__ballot(!get_state<NG>(i_slot(p - 1), tag_i(p - 1), E)) == 0) break;
+        if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) {
+          ok = false;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+    } else if (p_prev >= 0) {
       q = p_prev + 1;
 #pragma unroll
       for (int g = 0; g < NG; ++g) E[g] = Icur[g];
@@ -1446,6 +1488,7 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       Icur[g] = cfma_pair(l256[g].x, l256[g].y, E[g], Acur[g]);
       Acur[g] = Anext[g];
     }
+    if (chained && p + 1 < P) put_state<NG>(i_slot(p), Icur, tag_i(p));
     p_prev = p;
     // the row stores have read the H buffer before any wave writes H into it
     __syncthreads();

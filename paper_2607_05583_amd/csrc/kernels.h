@@ -58,6 +58,15 @@ struct FwdArgs {
 // Flags hold the call's epoch (hdr[1]): a tile state is published with
 // 2 epoch + 1 (its end state from zero, A) and 2 epoch + 2 (also its inclusive
 // end state, I); a table unit with epoch + 1.
+// Tile-to-tile chains (2 to 4 work-groups per chain) pass each tile's inclusive
+// end state to the next tile through a ring of STREAM_RING slots per chain; a
+// slot is written again only after the tile that read it has published its own
+// state, so any ring length is safe.  The ring is laid out for at most
+// STREAM_RING_CHAINS chains (more chains leave at most one work-group each on a
+// 256-CU device).
+constexpr int STREAM_RING = 4;
+constexpr int64_t STREAM_RING_CHAINS = 128;
+
 struct StreamArgs {
   const void* x;
   void* y;
@@ -79,6 +88,8 @@ struct StreamArgs {
   uint32_t* chainw;    // [nchains][4]: next ticket, arrived work-groups, tile order (0 open, 1 rounds,
                        // 2 tickets), finished work-groups
   uint64_t* agg;        // [nchains][P][8 waves][64][DW / 32] A of each tile (float | tag << 32 per word)
+  uint64_t* ring;       // [nchains][STREAM_RING][8 waves][64][DW / 32] I of recent tiles, or null:
+                        // no tile-to-tile chains
 };
 
 struct BwdArgs {

@@ -171,6 +171,10 @@ TILING = [
     (4, 8192, 256, 8, "bf16", "f32", False, 36),
     (2, 5000, 96, 5, "f32", "f32", True, 37),
     (3, 4097, 130, 8, "bf16", "bf16", True, 38),
+    # many chains, few work-groups each (2, 3 and 4 on 256 compute units)
+    (16, 2085, 256, 8, "f32", "f32", True, 39),
+    (8, 3001, 320, 8, "f32", "f32", False, 40),
+    (16, 3000, 256, 8, "bf16", "bf16", True, 44),
 ]
 
 
@@ -236,3 +240,68 @@ def test_workspace_reused_across_shapes():
         yr, hr = O.mix_recurrence(act64(prob["x"], act), *params_np(prob), h0=prob["h0"])
         assert rel_err(host(y), yr) <= tol(act, act)
         assert rel_err(host(hout), hr) <= (1e-4 if act == "f32" else 2e-2)
+
+
+# Counter words of the single-pass forward's workspace (kernels.h, StreamArgs):
+# a 256-byte header, then four 32-bit words per chain (next ticket, arrived
+# work-groups, tile order, finished work-groups).
+def _set_chain_word(ws, chain, j, value):
+    ws.view(torch.int32)[(256 + 16 * chain + 4 * j) // 4] = value
+
+
+def _chain_g(nchains, P):
+    """Work-groups per chain, as the host sizes the grid (one per compute unit)."""
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    return 1 if nchains >= ncu else min(ncu // nchains, P)
+
+
+def test_stale_counters_are_reported_and_touch_nothing(monkeypatch):
+    """A chain whose arrival counter is not zero at the start (a workspace not
+    zero-filled) sets bit 1 of the status word and leaves that chain's outputs
+    untouched; every kernel ends normally; a zero-filled workspace then gives the
+    oracle's result."""
+    from paper_2607_05583_amd import ops
+    monkeypatch.setattr(ops, "CHECK_FWD_STATUS", False)
+    B, L, D, M = 2, 2048, 128, 8  # bf16: two blocks of 64 channels, four chains
+    prob = W.random_problem(61, B, L, D, M, act="bf16", gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], "bf16")
+    ws = ops.forward_workspace(torch.bfloat16, B, L, D, M, "cuda")
+    _set_chain_word(ws, 0, 1, 0x7FFFFFFF)  # chain 0 = batch row 0, channels 0 .. 63
+    y = torch.full((B, L, D), 7.0, dtype=torch.bfloat16, device="cuda")
+    ops.resonator_mix_fwd(x, *params_dev(prob), out=y, ws=ws)
+    st = ops.resonator_fwd_status(ws)
+    assert st & 2
+    assert bool((y[0, :, :64] == 7.0).all())
+    yr, _ = O.mix_recurrence(act64(prob["x"], "bf16"), *params_np(prob))
+    assert rel_err(host(y[1]), yr[1]) <= 2e-2
+    ws.zero_()
+    y2 = ops.resonator_mix_fwd(x, *params_dev(prob), ws=ws)
+    assert ops.resonator_fwd_status(ws) == 0
+    assert rel_err(host(y2), yr) <= 2e-2
+
+
+def test_forced_give_up_is_reported(monkeypatch):
+    """Only one work-group of a chain runs (the others see a seeded arrival count
+    and stop), and it holds two tiles of the chain: the look-back of the later
+    one never sees the states of the tiles between them, so the bounded wait
+    gives up, the call ends, and the status word has bit 0 (a wait gave up) and
+    bit 1 (stale counters)."""
+    from paper_2607_05583_amd import ops
+    monkeypatch.setattr(ops, "CHECK_FWD_STATUS", False)
+    B, L, D, M = 1, 16384, 512, 8  # bf16: 8 chains (blocks of 64 channels) of 64 tiles
+    nchains, P = D // 64, (L + 255) // 256
+    G = _chain_g(nchains, P)
+    if not 2 <= G <= P // 2:
+        pytest.skip("this device does not give two tiles to each work-group of a chain")
+    prob = W.random_problem(62, B, L, D, M, act="bf16", gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], "bf16")
+    ws = ops.forward_workspace(torch.bfloat16, B, L, D, M, "cuda")
+    _set_chain_word(ws, 0, 1, G - 1)
+    ops.resonator_mix_fwd(x, *params_dev(prob), ws=ws)
+    st = ops.resonator_fwd_status(ws)
+    assert st & 1 and st & 2
+    ws.zero_()
+    y2 = ops.resonator_mix_fwd(x, *params_dev(prob), ws=ws)
+    assert ops.resonator_fwd_status(ws) == 0
+    yr, _ = O.mix_recurrence(act64(prob["x"], "bf16"), *params_np(prob))
+    assert rel_err(host(y2), yr) <= 2e-2
