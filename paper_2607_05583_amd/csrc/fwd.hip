@@ -980,11 +980,11 @@ struct StreamGeo {
   static constexpr int NW = 8;                     // waves (two per SIMD: 256 registers each)
   static constexpr int NG = DW / (4 * NW);         // groups of 4 channels per wave: 2 | 1
   static constexpr int NT = 64 * NW;
-  static constexpr int NQ = DW / 16;               // control waves (16 channels each): waves 0 .. NQ-1
-  static constexpr int LW = 4;                     // load waves: NQ .. NQ+3
+  static constexpr int NQ = 0;                     // first load wave
+  static constexpr int LW = NW;                    // load waves (every wave loads and stores rows)
   static constexpr int GPL = (TILE_T / 8) / LW;    // row groups per load wave and tile
   static constexpr int NBUF = 4;                   // tile buffers
-  static constexpr int HKS = 16 * 16 + 16;         // floats per channel in the H transposition (16 of bank offset)
+  static constexpr int HKS = 16 * 16 + 8;          // floats per channel in the H transposition (8 of bank offset)
   static constexpr int XB = XLay<(int)sizeof(TX)>::BYTES;
   static constexpr int HB = NW * 4 * HKS * 4;      // every wave's 4 channels of one group
   static constexpr int BUFB = XB > HB ? XB : HB;   // bytes per buffer (tile, or H transposition)
@@ -995,16 +995,23 @@ struct StreamGeo {
 
 // LDS stage of a work-group's tables, per channel k of the block and mode m:
 // lambda^j (j = 0 .. 16) and c as float2, the taps K[tau] (tau = 0 .. 15) as
-// float32 or as a bf16 pair (high | low << 16), and the scan constants mu =
-// lambda^16, lambda^256, lambda and lambda^(jstar+1).
+// float32 or as a bf16 pair (high | low << 16).
 template <typename TX>
 struct TabStage {
   static constexpr int DW = tile_channels<TX>();
   static constexpr int PW = 0;                     // float2 [DW][8][17]
   static constexpr int CM = PW + DW * 8 * 17 * 8;  // float2 [DW][8]
   static constexpr int TAP = CM + DW * 8 * 8;      // uint32 [DW][16]
-  static constexpr int SC = TAP + DW * 16 * 4;     // float2 [DW][8][4]
-  static constexpr int BYTES = SC + DW * 8 * 4 * 8;
+  static constexpr int BYTES = TAP + DW * 16 * 4;
+};
+
+// Per (channel, mode) constants a work-group keeps in LDS for the whole call
+// (each is needed once per tile or less): lambda, lambda^(jstar+1) (the
+// terminal state), the segment hops lambda^(256 n) and lambda^(256 (n + 1)) as
+// (Re, Im), and lambda^256 in float64 (the powers over a segment).
+struct KConst {
+  double2 l256;
+  float2 lam1, lamt, hop0, hop1;
 };
 
 // A float64 moved across lanes by a DPP pattern (its two halves).
@@ -1039,11 +1046,13 @@ __device__ __forceinline__ ModeIn load_mode(const StreamArgs& a, int d0, int tid
 // 8 k + m, one per channel and mode, with their parameters pin).  lambda =
 // exp(-gamma) (cos omega, sin omega) and c = amp (cos phase, sin phase) in
 // float64, the powers lambda^j by successive products and lambda^256 by eight
-// squarings (a relative error of a few 2^-53 per product); the taps
+// squarings and the segment hops by binary powering of it (a relative error of
+// a few 2^-53 per product); the taps
 // K[tau] = Re sum_m c lambda^tau, summed in float64 over the eight mode lanes of
 // a channel, are rounded once.
 template <typename TX>
-__device__ void build_tables(const StreamArgs& a, int d0, char* st, int tid, const ModeIn& pin) {
+__device__ void build_tables(const StreamArgs& a, int d0, char* st, KConst* kc, int tid, const ModeIn& pin,
+                             int64_t seg) {
   typedef TabStage<TX> S;
   if (tid >= S::DW * 8) return;
   const int k = tid >> 3, m = tid & 7, d = d0 + k;
@@ -1057,26 +1066,38 @@ __device__ void build_tables(const StreamArgs& a, int d0, char* st, int tid, con
     const double av = (double)pin.amp;
     cz = make_double2(av * cs, av * sn);
   }
-  const int jt = (a.last_len - 1) % CHUNK + 1;  // jstar + 1
   float2* pw = reinterpret_cast<float2*>(st + S::PW) + tid * 17;
   double tp[16];
-  double2 pj = make_double2(1.0, 0.0), lt = pj;
+  double2 pj = make_double2(1.0, 0.0);
 #pragma unroll
   for (int j = 0; j <= 16; ++j) {
     pw[j] = make_float2((float)pj.x, (float)pj.y);
     if (j < 16) tp[j] = cz.x * pj.x - cz.y * pj.y;
-    if (j == jt) lt = pj;
     if (j < 16) pj = zmul(pj, z);
   }
   double2 l2 = z;
 #pragma unroll
   for (int s = 0; s < 8; ++s) l2 = zmul(l2, l2);
+  // the segment hops (lambda^256)^seg and (lambda^256)^(seg+1) by binary powering
+  double2 zs0 = make_double2(1.0, 0.0);
+  {
+    double2 sq = l2;
+    for (int64_t e = seg; e > 0; e >>= 1) {
+      if (e & 1) zs0 = zmul(zs0, sq);
+      sq = zmul(sq, sq);
+    }
+  }
+  const double2 zs1 = zmul(zs0, l2);
   reinterpret_cast<float2*>(st + S::CM)[tid] = make_float2((float)cz.x, (float)cz.y);
-  float2* sc = reinterpret_cast<float2*>(st + S::SC) + tid * 4;
-  sc[0] = make_float2((float)pj.x, (float)pj.y);  // lambda^16
-  sc[1] = make_float2((float)l2.x, (float)l2.y);
-  sc[2] = make_float2((float)z.x, (float)z.y);
-  sc[3] = make_float2((float)lt.x, (float)lt.y);
+  {
+    KConst c;
+    c.l256 = l2;
+    c.lam1 = make_float2((float)z.x, (float)z.y);
+    c.lamt = pw[(a.last_len - 1) % CHUNK + 1];
+    c.hop0 = make_float2((float)zs0.x, (float)zs0.y);
+    c.hop1 = make_float2((float)zs1.x, (float)zs1.y);
+    kc[tid] = c;
+  }
   // sum over the 8 mode lanes of the channel, halving the taps at each of three
   // exchanges (DPP moves of the two halves of a float64): lane m <-> 7-m keeps
   // taps 0..7 (m < 4) or 8..15, then lane m <-> m^2 keeps a half of those by bit
@@ -1211,12 +1232,13 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
   constexpr int DW = G::DW, NW = G::NW, NG = G::NG, NT = G::NT, NQ = G::NQ, LW = G::LW, GPL = G::GPL;
   constexpr int NBUF = G::NBUF, XE = (int)sizeof(TX), HKS = G::HKS;
   static_assert(TS::BYTES <= (NBUF - 1) * G::BUFB, "the table stage fits in buffers 1 .. NBUF-1");
+  static_assert(NBUF == 4, "buffer rotation assumes four buffers");
   // bf16 drive with float32 output: y leaves straight from the MFMA registers
   constexpr bool SEPY = !__is_same(TX, TY);
-  // published states loaded at a time by a fold (a register budget of 2 RES_FOLD_WORDS)
+  // published states loaded at a time by the look-back (a register budget of 2 RES_FOLD_WORDS)
   constexpr int FB = RES_FOLD_WORDS / NG;
   __shared__ __align__(16) char xb[NBUF][G::BUFB];
-  __shared__ uint32_t s_tk[NBUF];  // tile of each buffer slot
+  __shared__ KConst s_kc[DW * 8];
   __shared__ uint32_t s_u[4];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -1229,7 +1251,12 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
   const int blk = chain % a.NB;
   const int d0 = blk * DW;
   const int64_t P = a.P;
-  const uint32_t G_ = gridDim.x / (uint32_t)a.nchains;  // work-groups serving each chain
+  const uint32_t G_ = gridDim.x / (uint32_t)a.nchains;  // work-groups (segments) of each chain
+  // (channel, mode) of scan lane (component ln, channel lq) of group g
+  auto kmode = [&](int g) { return (cb + 4 * g + lq) * 8 + (ln >> 1); };
+  // segment j: tiles [j Sf + min(j, Sr), ... + Sf + (j < Sr))
+  const int64_t Sf = P / G_, Sr = P % G_;
+  auto seg_start = [&](int64_t j) { return j * Sf + (j < Sr ? j : Sr); };
   uint32_t* cw = a.chainw + 4 * (size_t)chain;  // [0] next ticket, [1] arrived, [2] order, [3] finished
   const uint32_t ep = ld_flag(a.hdr + 1);
   const uint32_t TAG = ep + 1u;
@@ -1256,20 +1283,15 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       store_tile_part<TY, NT>(reinterpret_cast<TY*>(a.y), xb[u], b, p * TILE_T, d0, a.L, a.D, tid);
     }
   };
-  // this lane's words of the published A of tile q, and of the ring slot of the
-  // published I of tile q (tagged with q: a slot is used again RING tiles later)
-  auto a_slot = [&](int64_t q) { return a.agg + ((((size_t)chain * P + q) * NW + wave) * 64 + lane) * NG; };
-  auto i_slot = [&](int64_t q) {
-    return a.ring + ((((size_t)chain * STREAM_RING + (size_t)(q % STREAM_RING)) * NW + wave) * 64 + lane) * NG;
-  };
-  auto tag_i = [&](int64_t q) { return (ep + 1u) * 65536u + (uint32_t)(q & 0xFFFF); };
+  // this lane's words of the published aggregate of segment j
+  auto a_slot = [&](int64_t j) { return a.agg + ((((size_t)chain * G_ + j) * NW + wave) * 64 + lane) * NG; };
 
   // ---- arrival, the first tile, the tables ----------------------------------
-  // In round order the j-th work-group of a chain by block index takes tiles
-  // j, j + G, ... (round order is chosen only once all G have arrived).  Its
-  // first tile loads at once (again below if the chain takes tickets); the
-  // arrival count and a first look at the chain's arrivals come back while the
-  // tables are built.
+  // In static order the j-th work-group of a chain by block index takes segment
+  // j (static order is chosen only once all G have arrived).  Its segment's last
+  // tile loads at once (again below if the chain takes tickets); the arrival
+  // count and a first look at the chain's arrivals come back while the tables
+  // are built.
   const uint32_t rank = blockIdx.x / (uint32_t)a.nchains;
   const ModeIn pin = load_mode<TX>(a, d0, tid);  // before any tile load of the wave
   uint32_t arr = 0, arrived = 0;
@@ -1277,14 +1299,20 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
     arr = atomicAdd(cw + 1, 1u);
     arrived = ld_flag(cw + 1);
   }
-  if (is_ld && rank < P && tile_full(rank)) load_tile(0, rank);
+  // With one work-group per chain there is no aggregate to publish (phase A is
+  // skipped) and the chain's first tile loads at once.
+  const bool phaseA = G_ > 1;
+  {
+    const int64_t e0 = phaseA ? seg_start(rank + 1) - 1 : 0;
+    if (is_ld && tile_full(e0)) load_tile(0, e0);
+  }
   char* stg = xb[1];  // the tables are staged in buffers 1 .. 3
-  build_tables<TX>(a, d0, stg, tid, pin);
-  // ---- the order of the chain's tiles: rounds once every work-group of the
-  // chain has arrived, else tickets; the first CAS decides for the chain (its
+  build_tables<TX>(a, d0, stg, s_kc, tid, pin, Sf);
+  // ---- the order of the chain's segments: static once every work-group of the
+  // chain has arrived, else by ticket; the first CAS decides for the chain (its
   // answer is read after the operands are formed).  More arrivals than
   // work-groups: the counters were not in their initial state (workspace not
-  // zeroed, or changed meanwhile); such a work-group touches nothing. -------
+  // zeroed, or changed meanwhile); such a work-group touches nothing. ----------
   uint32_t order_old = 0, order_want = 0;
   if (tid == 0) {
     if (arr >= G_) {
@@ -1303,11 +1331,11 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
   __syncthreads();
   typename PT::AOp vop[NG][4], top[NG][4];
   typename PT::UOp uop[NG][4];
-  // constants of scan lane (component ln, channel lq of group g), as (Re, -+Im):
-  // mu, lambda^256; for the terminal state lambda and lambda^(jstar+1)
+  // mu = lambda^16 of scan lane (component ln, channel lq of group g), as
+  // (Re, -+Im): the re lane keeps -Im, the im lane +Im (cfma_pair)
   const float sgn = (ln & 1) ? 1.f : -1.f;
+  auto lane_c = [&](float2 z) { return make_float2(z.x, sgn * z.y); };
   float mur[NG], mus[NG];
-  float2 l256[NG], lam1[NG], lamt[NG];
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
 #pragma unroll
@@ -1316,27 +1344,19 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       stage_operands<TX>(stg, cb + 4 * g + k, ln, lq, top[g][k], vop[g][k], uu);
       uop[g][k] = PT::u_op(uu);
     }
-    const float2* scg = reinterpret_cast<const float2*>(stg + TS::SC) + ((cb + 4 * g + lq) * 8 + (ln >> 1)) * 4;
-    const float2 mu = scg[0], l2 = scg[1], l1 = scg[2], lj = scg[3];
+    const float2 mu = reinterpret_cast<const float2*>(stg + TS::PW)[kmode(g) * 17 + 16];
     mur[g] = mu.x;
     mus[g] = sgn * mu.y;
-    l256[g] = make_float2(l2.x, sgn * l2.y);
-    lam1[g] = make_float2(l1.x, sgn * l1.y);
-    lamt[g] = make_float2(lj.x, sgn * lj.y);
   }
-
   if (tid == 0) {
     const uint32_t order = order_want == 0 ? 0u : order_old == 0 ? order_want : order_old;
-    s_u[2] = order;
-    if (order == 1) {
-      s_tk[0] = rank;
-      s_tk[1] = rank + G_;
-      s_tk[2] = rank + 2 * G_;
-    } else if (order == 2) {
-      s_tk[0] = atomicAdd(cw, 1u);
-      s_tk[1] = atomicAdd(cw, 1u);
-      s_tk[2] = atomicAdd(cw, 1u);
-    }
+    const uint32_t seg = order == 1 ? rank : order == 2 ? atomicAdd(cw, 1u) : 0u;
+    // a ticket past the chain's segments: the counters were not in their initial
+    // state either
+    const bool stale = order == 0 || seg >= G_;
+    if (stale && order != 0) atomicOr(a.hdr, 2u);
+    s_u[2] = stale ? 0u : order;
+    s_u[0] = seg;
   }
   // every earlier vector memory operation of the wave has completed (the first
   // tile among them)
@@ -1344,188 +1364,206 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
   __syncthreads();
   if (s_u[2] == 0) return;  // stale counters
   const bool by_ticket = s_u[2] != 1;
+  const int64_t j = s_u[0];         // this work-group's segment
+  const int64_t s = seg_start(j);   // its first tile
+  const int S = (int)(seg_start(j + 1) - s);  // its tiles
+  // ---- phase A: the segment's tiles from last to first, k-th into buffer k & 3;
+  // its aggregate Aseg = sum_t lambda^(256 (e-1-t)) A_t, A_t the tile's end state
+  // from a zero start.  The first three tiles of the segment stay in their
+  // buffers; the fourth's buffer is left free for phase B. ---------------------
   uint32_t issued = 0, mark[NBUF] = {0, 0, 0, 0};
-  if (is_ld) {
+  auto tileA = [&](int k) { return s + S - 1 - k; };
+  if (!phaseA && is_ld) {
+    // phase B's first tiles in buffers 0, 1, 2 (the first loaded above)
 #pragma unroll
-    for (int u = 0; u < 3; ++u) {
-      const int64_t p = s_tk[u];
-      if ((u > 0 || by_ticket) && p < P && tile_full(p)) {
-        load_tile(u, p);
+    for (int k = 1; k < 3; ++k) {
+      if (k < S && tile_full(s + k)) {
+        load_tile(k, s + k);
         issued += GPL;
       }
-      mark[u] = issued;
+      mark[k] = issued;
     }
   }
-
-  // ---- the tiles, pipelined: iteration it runs pass 1 of tile it+1, then the
-  // carry and pass 2 of tile it, so that the states a carry reads were
-  // published one iteration earlier.  Every wave carries its own channels: lane
-  // (component ln, channel lq of group g) holds one value per group. ----------
-  int64_t p_prev = -1;  // the work-group's previous tile
-  float Icur[NG], Acur[NG], tail[NG];  // its inclusive end state; this tile's A; the partial last chunk
+  if (phaseA && is_ld) {
+    // the segment's last tile is in buffer 0 unless the segment came by ticket
+    mark[0] = 0;
+    if (by_ticket && tile_full(tileA(0))) {
+      load_tile(0, tileA(0));
+      issued += GPL;
+      mark[0] = issued;
+    }
 #pragma unroll
-  for (int g = 0; g < NG; ++g) Icur[g] = Acur[g] = tail[g] = 0.f;
-  int it = -1;
-  for (;; ++it) {
-    const int64_t p = it >= 0 ? (int64_t)s_tk[it & (NBUF - 1)] : -1;  // carry and pass 2
-    if (p >= P) break;
-    const int un = (it + 1) & (NBUF - 1);
-    const int64_t pn = s_tk[un];  // pass 1
-    const bool has_next = pn < P;
-    // arrival of tile it+1: this wave's share of a full tile, or a copy
-    if (has_next) {
-      if (tile_full(pn)) {
-        if (is_ld) wait_vmcnt((int)(issued - mark[un]));
-      } else {
-        copy_tile<TX, NT>(xb[un], reinterpret_cast<const TX*>(a.x), b, pn * TILE_T, d0, a.L, a.D, tid);
+    for (int k = 1; k < 3; ++k) {
+      if (k < S && tile_full(tileA(k))) {
+        load_tile(k, tileA(k));
+        issued += GPL;
       }
+      mark[k] = issued;
+    }
+  }
+  float Aseg[NG];
+  double2 pw[NG];  // lambda^(256 k), float64
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    Aseg[g] = 0.f;
+    pw[g] = make_double2(1.0, 0.0);
+  }
+  for (int k = 0; phaseA && k < S; ++k) {
+    const int u = k & (NBUF - 1);
+    const int64_t p = tileA(k);
+    if (tile_full(p)) {
+      if (is_ld) wait_vmcnt((int)(issued - mark[u]));
+    } else {
+      copy_tile<TX, NT>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, tid);
     }
     __syncthreads();
-    // the rows of tile it-1 (p_prev) leave: its buffer is this iteration's H buffer
-    if (!SEPY && it >= 1) {
-      store_tile((it - 1) & (NBUF - 1), p_prev);
-      if (is_ld && tile_full(p_prev)) issued += GPL;
-    }
-    // the tile three ahead (its buffer slot held tile it-1)
-    if (tid == 0 && it >= 0) s_tk[(it + 3) & (NBUF - 1)] = by_ticket ? atomicAdd(cw, 1u) : rank + (uint32_t)(it + 3) * G_;
-
-    // ---- pass 1 (tile it+1): S = V x, moved so that lane (c, k) holds component
-    // c of channel k; A = sum_n mu^(15-n) S[n], the tile's end state from a zero
-    // start, published at once; on the chain's last tile also
-    // sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j]
-    float Anext[NG];
-    if (has_next) {
-      const char* xn = xb[un];
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        typename PT::XOp xv[4];
-        float S[16];
-        PT::gather4(xn, cb + 4 * g, ln, lq, xv);
-        chunk_states<TX>(xv, vop[g], S);
-        float A = S[0];
-#pragma unroll
-        for (int n = 1; n < 16; ++n) A = cfma_pair(mur[g], mus[g], A, S[n]);
-        Anext[g] = A;
-        if (pn == P - 1 && a.h_out != nullptr) {
-          const int ch = cb + 4 * g + lq;
-          float t = 0.f;
-          for (int j = 0; j <= jstar; ++j) {
-            const float xj = to_f32(*reinterpret_cast<const TX*>(xn + XLay<XE>::off(nstar * CHUNK + j) + ch * XE));
-            t = cfma_pair(lam1[g].x, lam1[g].y, t, (ln & 1) ? 0.f : xj);
-          }
-          tail[g] = t;
-        }
+    // the tile three ahead, into the buffer of the previous one (read by every
+    // wave before this barrier)
+    if (is_ld) {
+      const int u3 = (k + 3) & (NBUF - 1);
+      if (k + 3 < S && tile_full(tileA(k + 3))) {
+        load_tile(u3, tileA(k + 3));
+        issued += GPL;
       }
-      put_state<NG>(a_slot(pn), Anext, TAG);
+      mark[u3] = issued;
     }
-    if (it < 0) {
-#pragma unroll
-      for (int g = 0; g < NG; ++g) Acur[g] = Anext[g];
-      continue;
-    }
-
-    // ---- carry (tile it): E, the state entering the tile, from a stop tile's
-    // inclusive end state I and the published A of the tiles between, oldest
-    // first, E <- lambda^256 E + A; then I = lambda^256 E + A(this tile).  The
-    // stop is the work-group's own previous tile (in rounds G tiles back; h0 at
-    // the chain's start), except for chains of 2 to 4 work-groups in rounds,
-    // where every tile starts from the previous tile's I, published in a ring. -
-    float E[NG];
-    int64_t q = 0;  // the first tile folded
-    bool ok = true;
-#pragma unroll
-    for (int g = 0; g < NG; ++g) E[g] = 0.f;
-    const bool chained = a.ring != nullptr && !by_ticket && G_ >= 2 && G_ <= 4;
-    if (chained && p > 0) {
-      q = p;
-      for (uint32_t n = 0;; ++n) {
-        if (__ballot(!get_state<NG>(i_slot(p - 1), tag_i(p - 1), E)) == 0) break;
-        if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) {
-          ok = false;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-    } else if (p_prev >= 0) {
-      q = p_prev + 1;
-#pragma unroll
-      for (int g = 0; g < NG; ++g) E[g] = Icur[g];
-    } else if (a.h0 != nullptr) {  // the chain's start
-#pragma unroll
-      for (int g = 0; g < NG; ++g) {
-        const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
-        if (d < a.D && m < a.M) E[g] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
-      }
-    }
-    for (; ok && q < p; q += FB) {
-      float Aq[FB][NG];
-      for (uint32_t n = 0;; ++n) {
-        bool mine = true;
-#pragma unroll
-        for (int i = 0; i < FB; ++i) mine = get_state<NG>(a_slot(q + i < p ? q + i : q), TAG, Aq[i]) && mine;
-        if (__ballot(!mine) == 0) break;
-        if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) {
-          ok = false;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-      }
-      if (!ok) break;
-#pragma unroll
-      for (int i = 0; i < FB; ++i) {
-        if (q + i < p) {
-#pragma unroll
-          for (int g = 0; g < NG; ++g) E[g] = cfma_pair(l256[g].x, l256[g].y, E[g], Aq[i][g]);
-        }
-      }
-    }
-    if (!ok && lane == 0) {  // gave up: the outputs of this call are wrong
-      atomicOr(a.hdr, 1u);
-      atomicOr(a.hdr + 4, 1u);
-    }
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      Icur[g] = cfma_pair(l256[g].x, l256[g].y, E[g], Acur[g]);
-      Acur[g] = Anext[g];
-    }
-    if (chained && p + 1 < P) put_state<NG>(i_slot(p), Icur, tag_i(p));
-    p_prev = p;
-    // the row stores have read the H buffer before any wave writes H into it
-    __syncthreads();
-
-    // ---- pass 2 (tile it): chunk entering states, y = T x + U H, group by group.
-    // (x is still in the tile buffer: S and the operands are formed again.)  H
-    // moves through LDS, in the buffer of tile it-1 (its rows have left): lane
-    // (c, k) writes component c of chunk n at [k][n][c], lane (n, q) reads
-    // components 4q .. 4q+3 of chunk n.
-    const bool lastp = (p == P - 1);
-    char* xt = xb[it & (NBUF - 1)];
-    float* hs = reinterpret_cast<float*>(xb[(it + 3) & (NBUF - 1)]) + wave * 4 * HKS;
+    const char* xt = xb[u];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
       typename PT::XOp xv[4];
-      float S[16];
+      float S16[16];
       PT::gather4(xt, cb + 4 * g, ln, lq, xv);
-      chunk_states<TX>(xv, vop[g], S);
+      chunk_states<TX>(xv, vop[g], S16);
+      float A = S16[0];
+#pragma unroll
+      for (int n = 1; n < 16; ++n) A = cfma_pair(mur[g], mus[g], A, S16[n]);
+      // Aseg += lambda^(256 k) A; then the power moves one tile on
+      Aseg[g] = cfma_pair((float)pw[g].x, sgn * (float)pw[g].y, A, Aseg[g]);
+      pw[g] = zmul(pw[g], s_kc[kmode(g)].l256);
+    }
+  }
+
+  // ---- look-back: publish Aseg, then the state entering the segment from h0
+  // and the aggregates of the chain's earlier segments, oldest first,
+  // E <- lambda^(256 S_i) E + Aseg_i -------------------------------------------
+  if (G_ > 1) put_state<NG>(a_slot(j), Aseg, TAG);
+  float E[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    E[g] = 0.f;
+    const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
+    if (a.h0 != nullptr && d < a.D && m < a.M) E[g] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
+  }
+  bool ok = true;
+  for (int64_t q = 0; ok && q < j; q += FB) {
+    float Aq[FB][NG];
+    for (uint32_t n = 0;; ++n) {
+      bool mine = true;
+#pragma unroll
+      for (int i = 0; i < FB; ++i) mine = get_state<NG>(a_slot(q + i < j ? q + i : q), TAG, Aq[i]) && mine;
+      if (__ballot(!mine) == 0) break;
+      if (n >= SPIN_LIMIT || ((n & 63) == 63 && ld_flag(a.hdr + 4) != 0)) {
+        ok = false;
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+    if (!ok) break;
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+      if (q + i < j) {
+        const bool longer = q + i < Sr;  // segment q+i has Sf + 1 tiles
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const float2 z = lane_c(longer ? s_kc[kmode(g)].hop1 : s_kc[kmode(g)].hop0);
+          E[g] = cfma_pair(z.x, z.y, E[g], Aq[i][g]);
+        }
+      }
+    }
+  }
+  if (!ok && lane == 0) {  // gave up: the outputs of this call are wrong
+    atomicOr(a.hdr, 1u);
+    atomicOr(a.hdr + 4, 1u);
+  }
+
+  // ---- phase B: the segment's tiles in order; after phase A tile s+m is in
+  // buffer (S-1-m) & 3 and its H goes to buffer (S-m) & 3 (the previous tile's,
+  // or the free one), which then takes tile s+m+3; without phase A the same
+  // rotation runs the other way (tile s+m in buffer m & 3).  E moves from tile to
+  // tile as the scan's end state. ----------------------------------------------
+  if (phaseA && is_ld) {
+    // the buffers of phase B's resident tiles count as landed
+#pragma unroll
+    for (int u = 0; u < NBUF; ++u) mark[u] = issued;
+  }
+  for (int m = 0; m < S; ++m) {
+    const int64_t p = s + m;
+    const int u = (phaseA ? S - 1 - m : m) & (NBUF - 1), uh = (phaseA ? S - m : m + 3) & (NBUF - 1);
+    if (!phaseA || m >= 3) {  // a tile not left in its buffer by phase A
+      if (tile_full(p)) {
+        if (is_ld) wait_vmcnt((int)(issued - mark[u]));
+      } else {
+        copy_tile<TX, NT>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, tid);
+      }
+    }
+    // the tile is in; the previous tile's rows have been read out of buffer uh
+    __syncthreads();
+    const bool lastp = (p == P - 1);
+    char* xt = xb[u];
+    float* hs = reinterpret_cast<float*>(xb[uh]) + wave * 4 * HKS;
+    float tail[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      tail[g] = 0.f;
+      if (lastp && a.h_out != nullptr) {
+        // sum_{j <= jstar} lambda^(jstar-j) x[16 nstar + j] (before y overwrites x)
+        const int ch = cb + 4 * g + lq;
+        const float2 l1 = lane_c(s_kc[kmode(g)].lam1);
+        float t = 0.f;
+        for (int jj = 0; jj <= jstar; ++jj) {
+          const float xj = to_f32(*reinterpret_cast<const TX*>(xt + XLay<XE>::off(nstar * CHUNK + jj) + ch * XE));
+          t = cfma_pair(l1.x, l1.y, t, (ln & 1) ? 0.f : xj);
+        }
+        tail[g] = t;
+      }
+    }
+    // pass 2: chunk entering states, y = T x + U H, group by group
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      typename PT::XOp xv[4];
+      float S16[16];
+      PT::gather4(xt, cb + 4 * g, ln, lq, xv);
+      chunk_states<TX>(xv, vop[g], S16);
       {
         float h = E[g];
         float hn = 0.f;
+        if (lastp) {
 #pragma unroll
-        for (int n = 0; n < 16; ++n) {
-          if (n == nstar) hn = h;
-          const float nx = cfma_pair(mur[g], mus[g], h, S[n]);
-          S[n] = h;  // now the state entering chunk n
-          h = nx;
+          for (int n = 0; n < 16; ++n) {
+            if (n == nstar) hn = h;
+            const float nx = cfma_pair(mur[g], mus[g], h, S16[n]);
+            S16[n] = h;  // now the state entering chunk n
+            h = nx;
+          }
+        } else {
+#pragma unroll
+          for (int n = 0; n < 16; ++n) {
+            const float nx = cfma_pair(mur[g], mus[g], h, S16[n]);
+            S16[n] = h;
+            h = nx;
+          }
         }
+        E[g] = h;  // the state entering the next tile
         if (lastp && a.h_out != nullptr) {
           // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
-          const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
-          const float hl = cfma_pair(lamt[g].x, lamt[g].y, hn, tail[g]);
-          if (d < a.D && m < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)] = hl;
+          const int d = d0 + cb + 4 * g + lq, mm = ln >> 1;
+          const float2 lt = lane_c(s_kc[kmode(g)].lamt);
+          const float hl = cfma_pair(lt.x, lt.y, hn, tail[g]);
+          if (d < a.D && mm < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + mm) * 2 + (ln & 1)] = hl;
         }
       }
 #pragma unroll
-      for (int n = 0; n < 16; ++n) hs[lq * HKS + n * 16 + ln] = S[n];
+      for (int n = 0; n < 16; ++n) hs[lq * HKS + n * 16 + ln] = S16[n];
       wave_lds_order();
       f4 acc[4];
 #pragma unroll
@@ -1541,20 +1579,19 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
         put_y4<TY>(xt, cb + 4 * g, ln, lq, acc);
     }
     __syncthreads();
-
-    // ---- load waves: the tile three ahead (into this iteration's H buffer) ----
+    // the rows of tile p leave; the tile three ahead loads into the H buffer
+    if (!SEPY) {
+      store_tile(u, p);
+      if (is_ld && tile_full(p)) issued += GPL;
+    }
     if (is_ld) {
-      const int u3 = (it + 3) & (NBUF - 1);
-      const int64_t p3 = s_tk[u3];
-      if (p3 < P && tile_full(p3)) {
-        load_tile(u3, p3);
+      if (m + 3 < S && tile_full(p + 3)) {
+        load_tile(uh, p + 3);
         issued += GPL;
       }
-      mark[u3] = issued;
+      mark[uh] = issued;
     }
   }
-  // the rows of the last tile
-  if (!SEPY && it >= 1) store_tile((it - 1) & (NBUF - 1), p_prev);
 
   // ---- the last work-group of a chain resets the chain's counters, the last
   // chain to finish the call's words ------------------------------------------
