@@ -1418,15 +1418,18 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
     }
     __syncthreads();
     // the tile three ahead, into the buffer of the previous one (read by every
-    // wave before this barrier)
-    if (is_ld) {
+    // wave before this barrier): the first half of the waves issues its loads
+    // before pass 1, the other half after it
+    auto memory = [&]() {
       const int u3 = (k + 3) & (NBUF - 1);
       if (k + 3 < S && tile_full(tileA(k + 3))) {
         load_tile(u3, tileA(k + 3));
         issued += GPL;
       }
       mark[u3] = issued;
-    }
+    };
+    const bool mem_first = wave < NW / 2;
+    if (mem_first) memory();
     const char* xt = xb[u];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -1441,18 +1444,31 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       Aseg[g] = cfma_pair((float)pw[g].x, sgn * (float)pw[g].y, A, Aseg[g]);
       pw[g] = zmul(pw[g], s_kc[kmode(g)].l256);
     }
+    if (!mem_first) memory();
   }
 
-  // ---- look-back: publish Aseg, then the state entering the segment from h0
-  // and the aggregates of the chain's earlier segments, oldest first,
-  // E <- lambda^(256 S_i) E + Aseg_i -------------------------------------------
-  if (G_ > 1) put_state<NG>(a_slot(j), Aseg, TAG);
+  // ---- look-back: the state entering the segment, E, from the published states
+  // of the chain's earlier segments, oldest first, E <- lambda^(256 S_i) E + P_i.
+  // Segment 0 alone reads h0 and publishes its inclusive end state
+  // P_0 = lambda^(256 S_0) h0 + Aseg_0; every other segment publishes P_j = Aseg_j.
+  // (h0 is then read before anything the chain's last tile waits for, so h_out
+  // may be h0's memory.) ----------------------------------------------------------
   float E[NG];
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
     E[g] = 0.f;
     const int d = d0 + cb + 4 * g + lq, m = ln >> 1;
-    if (a.h0 != nullptr && d < a.D && m < a.M) E[g] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
+    if (j == 0 && a.h0 != nullptr && d < a.D && m < a.M)
+      E[g] = a.h0[((size_t)(b * a.D + d) * a.M + m) * 2 + (ln & 1)];
+  }
+  if (G_ > 1) {
+    float Pj[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const float2 z = lane_c(Sr > 0 ? s_kc[kmode(g)].hop1 : s_kc[kmode(g)].hop0);  // segment 0's hop
+      Pj[g] = j == 0 ? cfma_pair(z.x, z.y, E[g], Aseg[g]) : Aseg[g];
+    }
+    put_state<NG>(a_slot(j), Pj, TAG);
   }
   bool ok = true;
   for (int64_t q = 0; ok && q < j; q += FB) {
@@ -1486,31 +1502,56 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
     atomicOr(a.hdr + 4, 1u);
   }
 
-  // ---- phase B: the segment's tiles in order; after phase A tile s+m is in
-  // buffer (S-1-m) & 3 and its H goes to buffer (S-m) & 3 (the previous tile's,
-  // or the free one), which then takes tile s+m+3; without phase A the same
-  // rotation runs the other way (tile s+m in buffer m & 3).  E moves from tile to
-  // tile as the scan's end state. ----------------------------------------------
-  if (phaseA && is_ld) {
-    // the buffers of phase B's resident tiles count as landed
-#pragma unroll
-    for (int u = 0; u < NBUF; ++u) mark[u] = issued;
-  }
+  // ---- phase B: the segment's tiles in order, E moving from tile to tile as the
+  // scan's end state.  The states H go through one fixed buffer (the one phase A
+  // left free, or buffer 3); tiles rotate through the other three: tile s+m is
+  // in buffer U[m mod 3], the first three as phase A left them (or as loaded
+  // above), each later one loaded into the buffer of the tile three before it
+  // once that tile's rows have been read out.  Iteration m: the tile's arrival
+  // and one barrier, the load of tile s+m+1, the rows of tile s+m-1 (read out of
+  // LDS while pass 2 runs), pass 2 of tile s+m. ---------------------------------
+  const int U0 = phaseA ? (S - 1) & 3 : 0, U1 = phaseA ? (S - 2) & 3 : 1, U2 = phaseA ? (S - 3) & 3 : 2;
+  const int UH = phaseA ? S & 3 : 3;
+  auto ubuf = [&](int m) {
+    const int r = m % 3;
+    return r == 0 ? U0 : r == 1 ? U1 : U2;
+  };
+  float* hs = reinterpret_cast<float*>(xb[UH]) + wave * 4 * HKS;
+  const int resident = phaseA ? 3 : 0;  // tiles left in their buffers by phase A
   for (int m = 0; m < S; ++m) {
     const int64_t p = s + m;
-    const int u = (phaseA ? S - 1 - m : m) & (NBUF - 1), uh = (phaseA ? S - m : m + 3) & (NBUF - 1);
-    if (!phaseA || m >= 3) {  // a tile not left in its buffer by phase A
+    const int u = ubuf(m);
+    if (m >= resident) {
       if (tile_full(p)) {
         if (is_ld) wait_vmcnt((int)(issued - mark[u]));
       } else {
         copy_tile<TX, NT>(xb[u], reinterpret_cast<const TX*>(a.x), b, p * TILE_T, d0, a.L, a.D, tid);
       }
     }
-    // the tile is in; the previous tile's rows have been read out of buffer uh
+    // the tile is in; the rows of tile s+m-2 have been read out of its buffer;
+    // every wave is done with H and with the outputs of tile s+m-1
     __syncthreads();
+    // the rows of tile s+m-1 and the load of tile s+m+1: the first half of the
+    // waves issues them before pass 2, the other half after it, so that on
+    // every SIMD one wave computes while the other issues its memory operations
+    const int un = ubuf(m + 1), up = ubuf(m + 2);  // ubuf(m - 1) == ubuf(m + 2)
+    auto memory = [&]() {
+      if (!SEPY && m >= 1) {
+        store_tile(up, p - 1);
+        if (tile_full(p - 1)) issued += GPL;
+      }
+      if (m + 1 >= 3 && m + 1 < S) {
+        if (tile_full(p + 1)) {
+          load_tile(un, p + 1);
+          issued += GPL;
+        }
+        mark[un] = issued;
+      }
+    };
+    const bool mem_first = wave < NW / 2;
+    if (mem_first || !tile_full(p - 1)) memory();  // a tile that is not full is stored by every thread at once
     const bool lastp = (p == P - 1);
     char* xt = xb[u];
-    float* hs = reinterpret_cast<float*>(xb[uh]) + wave * 4 * HKS;
     float tail[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
@@ -1527,49 +1568,44 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
         tail[g] = t;
       }
     }
-    // pass 2: chunk entering states, y = T x + U H, group by group
+    // pass 2: the x operands and S of every group first, the scans (independent
+    // chains, one per group) next, then per group H through LDS and
+    // y = T x + U H.  On the chain's last tile the state entering chunk nstar
+    // is read back from the H buffer.
+    typename PT::XOp xv[NG][4];
+    float S16[NG][16];
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      typename PT::XOp xv[4];
-      float S16[16];
-      PT::gather4(xt, cb + 4 * g, ln, lq, xv);
-      chunk_states<TX>(xv, vop[g], S16);
-      {
-        float h = E[g];
-        float hn = 0.f;
-        if (lastp) {
+      PT::gather4(xt, cb + 4 * g, ln, lq, xv[g]);
+      chunk_states<TX>(xv[g], vop[g], S16[g]);
+    }
 #pragma unroll
-          for (int n = 0; n < 16; ++n) {
-            if (n == nstar) hn = h;
-            const float nx = cfma_pair(mur[g], mus[g], h, S16[n]);
-            S16[n] = h;  // now the state entering chunk n
-            h = nx;
-          }
-        } else {
+    for (int n = 0; n < 16; ++n) {
 #pragma unroll
-          for (int n = 0; n < 16; ++n) {
-            const float nx = cfma_pair(mur[g], mus[g], h, S16[n]);
-            S16[n] = h;
-            h = nx;
-          }
-        }
-        E[g] = h;  // the state entering the next tile
-        if (lastp && a.h_out != nullptr) {
-          // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
-          const int d = d0 + cb + 4 * g + lq, mm = ln >> 1;
-          const float2 lt = lane_c(s_kc[kmode(g)].lamt);
-          const float hl = cfma_pair(lt.x, lt.y, hn, tail[g]);
-          if (d < a.D && mm < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + mm) * 2 + (ln & 1)] = hl;
-        }
+      for (int g = 0; g < NG; ++g) {
+        const float nx = cfma_pair(mur[g], mus[g], E[g], S16[g][n]);
+        S16[g][n] = E[g];  // now the state entering chunk n
+        E[g] = nx;         // at the end, the state entering the next tile
       }
+    }
 #pragma unroll
-      for (int n = 0; n < 16; ++n) hs[lq * HKS + n * 16 + ln] = S16[n];
+    for (int g = 0; g < NG; ++g) {
+#pragma unroll
+      for (int n = 0; n < 16; ++n) hs[lq * HKS + n * 16 + ln] = S16[g][n];
       wave_lds_order();
+      if (lastp && a.h_out != nullptr) {
+        // state at t = L-1: lambda^(jstar+1) times the state entering chunk nstar, plus the tail
+        const float hn = hs[lq * HKS + nstar * 16 + ln];
+        const int d = d0 + cb + 4 * g + lq, mm = ln >> 1;
+        const float2 lt = lane_c(s_kc[kmode(g)].lamt);
+        const float hl = cfma_pair(lt.x, lt.y, hn, tail[g]);
+        if (d < a.D && mm < a.M) a.h_out[((size_t)(b * a.D + d) * a.M + mm) * 2 + (ln & 1)] = hl;
+      }
       f4 acc[4];
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const f4 hb = *reinterpret_cast<const f4*>(&hs[k * HKS + ln * 16 + 4 * lq]);
-        acc[k] = PT::mma_u(uop[g][k], hb, PT::mma(top[g][k], xv[k], zero));
+        acc[k] = PT::mma_u(uop[g][k], hb, PT::mma(top[g][k], xv[g][k], zero));
       }
       wave_lds_order();
       if (SEPY)
@@ -1578,20 +1614,11 @@ __global__ __launch_bounds__(StreamGeo<TX>::NT, 1) void fwd_stream_kernel(Stream
       else
         put_y4<TY>(xt, cb + 4 * g, ln, lq, acc);
     }
-    __syncthreads();
-    // the rows of tile p leave; the tile three ahead loads into the H buffer
-    if (!SEPY) {
-      store_tile(u, p);
-      if (is_ld && tile_full(p)) issued += GPL;
-    }
-    if (is_ld) {
-      if (m + 3 < S && tile_full(p + 3)) {
-        load_tile(uh, p + 3);
-        issued += GPL;
-      }
-      mark[uh] = issued;
-    }
+    if (!mem_first && tile_full(p - 1)) memory();
   }
+  // the rows of the segment's last tile
+  __syncthreads();
+  if (!SEPY) store_tile(ubuf(S - 1), s + S - 1);
 
   // ---- the last work-group of a chain resets the chain's counters, the last
   // chain to finish the call's words ------------------------------------------
