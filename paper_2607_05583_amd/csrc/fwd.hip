@@ -369,16 +369,22 @@ template <> struct FPath<bf16_t> {
     return r;
   }
   __device__ static __forceinline__ f4 mma_u(const UOp& u, const f4& h, f4 c) {
-    // pairs rounded together; the float value of each rounded half read back
-    // from the packed word (low half: shift, high half: mask)
+    // pairs rounded together; each remainder h - bf16(h) (exact: the two are
+    // within a factor of two) as one bf16 dot product of the rounded pair with
+    // (-1, 0) or (0, -1), accumulated onto h
     typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+    // the two selectors live in registers: a packed bf16 operand given as a
+    // 32-bit inline constant is not read as the pair written here
+    uint32_t u10 = 0x0000BF80u, u01 = 0xBF800000u;
+    asm volatile("" : "+v"(u10), "+v"(u01));
+    const b2 m10 = __builtin_bit_cast(b2, u10), m01 = __builtin_bit_cast(b2, u01);
     uint32_t ph[2], pl[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const b2 hi = {(__bf16)h[2 * i], (__bf16)h[2 * i + 1]};
       ph[i] = __builtin_bit_cast(uint32_t, hi);
-      const b2 lo = {(__bf16)(h[2 * i] - __uint_as_float(ph[i] << 16)),
-                     (__bf16)(h[2 * i + 1] - __uint_as_float(ph[i] & 0xFFFF0000u))};
+      const b2 lo = {(__bf16)__builtin_amdgcn_fdot2_f32_bf16(hi, m10, h[2 * i], false),
+                     (__bf16)__builtin_amdgcn_fdot2_f32_bf16(hi, m01, h[2 * i + 1], false)};
       pl[i] = __builtin_bit_cast(uint32_t, lo);
     }
     const s4 bh = __builtin_bit_cast(s4, make_uint2(ph[0], ph[1]));
