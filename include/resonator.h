@@ -186,6 +186,23 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
                           const float* amp, const float* phase, float* state, void* stream);
 
 /*
+ * Decode from a constants table (Sec. 3.3), for token-by-token loops:
+ * resonator_decode_constants evaluates, once, the per-(channel, mode) constants
+ * that resonator_decode_step evaluates on every call,
+ *   tab [D][M][6] float32 = (Re, Im) of lambda's float32 pair hi and lo, and of c,
+ * and resonator_decode_step_tab runs one step from it.  The step's arithmetic and
+ * its order are those of resonator_decode_step, so the results are bitwise the
+ * same.  tab: device memory of D*M*24 bytes, 16-byte aligned for the fast path,
+ * owned by the caller; it stays valid until the parameters change.  Other
+ * arguments, layouts and errors as for resonator_decode_step.  Needs no
+ * workspace.
+ */
+int resonator_decode_constants(int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                               const float* phase, float* tab, void* stream);
+int resonator_decode_step_tab(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtype_t y_dt, int64_t B,
+                              int64_t D, int64_t M, const float* tab, float* state, void* stream);
+
+/*
  * N decode steps in one launch, for drives known in advance (a prompt chunk,
  * drafted tokens to verify) (Sec. 3.3):
  *   for n = 0 .. N-1:  state <- lambda state + x[:, n];  y[:, n] = Re sum_m c state.

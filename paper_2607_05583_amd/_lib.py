@@ -21,6 +21,7 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
            "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
+           "resonator_decode_constants", "resonator_decode_step_tab",
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
            "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
@@ -106,6 +107,10 @@ def _declare(lib):
     lib.resonator_mix_fwd_noalloc_max_bytes.argtypes = []
     lib.resonator_decode_steps.restype = i32
     lib.resonator_decode_steps.argtypes = [vp, i32, vp, i32, i64, i64, i64, i64, fp, fp, fp, fp, fp, vp]
+    lib.resonator_decode_constants.restype = i32
+    lib.resonator_decode_constants.argtypes = [i64, i64, fp, fp, fp, fp, fp, vp]
+    lib.resonator_decode_step_tab.restype = i32
+    lib.resonator_decode_step_tab.argtypes = [vp, i32, vp, i32, i64, i64, i64, fp, fp, vp]
 
 
 def lib():

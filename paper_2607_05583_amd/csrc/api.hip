@@ -551,6 +551,48 @@ int resonator_decode_step(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtyp
   return e == hipSuccess ? RES_OK : hip_fail(e, "decode launch");
 }
 
+int resonator_decode_constants(int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                               const float* phase, float* tab, void* stream) {
+  int rc = check_sizes(1, 1, D, M, false);
+  if (rc) return rc;
+  if ((rc = check_params(gamma, omega, amp, phase))) return rc;
+  if (!tab) return fail(RES_ERR_INVALID_ARG, "tab must be non-null");
+  if (!aligned(tab, 8)) return fail(RES_ERR_MISALIGNED, "tab must be 8-byte aligned");
+  if (overlap(tab, (size_t)(D * M) * 24, gamma, (size_t)(D * M) * 4) ||
+      overlap(tab, (size_t)(D * M) * 24, omega, (size_t)(D * M) * 4) ||
+      overlap(tab, (size_t)(D * M) * 24, amp, (size_t)(D * M) * 4) ||
+      overlap(tab, (size_t)(D * M) * 24, phase, (size_t)(D * M) * 4))
+    return fail(RES_ERR_INVALID_ARG, "tab must not overlap the parameters");
+  const hipError_t e = launch_decode_consts(D, M, gamma, omega, amp, phase, tab, (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "decode constants launch");
+}
+
+int resonator_decode_step_tab(const void* x_t, res_dtype_t x_dt, void* y_t, res_dtype_t y_dt, int64_t B,
+                              int64_t D, int64_t M, const float* tab, float* state, void* stream) {
+  int rc = check_sizes(B, 1, D, M, false);
+  if (rc) return rc;
+  if (!dtype_ok(x_dt) || !dtype_ok(y_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (x_dt == RES_F32 && y_dt == RES_BF16)
+    return fail(RES_ERR_UNSUPPORTED, "dtype pair f32 -> bf16 is not supported");
+  if (!x_t || !y_t || !state || !tab) return fail(RES_ERR_INVALID_ARG, "x_t, y_t, tab and state must be non-null");
+  if (!aligned(x_t, elt_size(x_dt)) || !aligned(y_t, elt_size(y_dt)) || !aligned(state, 8) || !aligned(tab, 8))
+    return fail(RES_ERR_MISALIGNED, "x_t/y_t aligned to their element, state and tab to 8 bytes");
+  const size_t n = (size_t)(B * D);
+  if (overlap(y_t, n * elt_size(y_dt), x_t, n * elt_size(x_dt)) ||
+      overlap(y_t, n * elt_size(y_dt), state, n * M * 8) || overlap(y_t, n * elt_size(y_dt), tab, (size_t)(D * M) * 24) ||
+      overlap(state, n * M * 8, tab, (size_t)(D * M) * 24))
+    return fail(RES_ERR_INVALID_ARG, "y_t must not overlap x_t, state or tab, nor state tab");
+  hipStream_t st = (hipStream_t)stream;
+  hipError_t e;
+  if (x_dt == RES_F32)
+    e = launch_decode_tab<float, float>(B, D, M, x_t, y_t, tab, state, st);
+  else if (y_dt == RES_BF16)
+    e = launch_decode_tab<bf16_t, bf16_t>(B, D, M, x_t, y_t, tab, state, st);
+  else
+    e = launch_decode_tab<bf16_t, float>(B, D, M, x_t, y_t, tab, state, st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "decode launch");
+}
+
 int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t y_dt, int64_t B, int64_t N,
                            int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
                            const float* phase, float* state, void* stream) {

@@ -177,6 +177,11 @@ hipError_t launch_params_map_bwd(const float* tg, const float* tw, const float* 
                                  float* dtg, float* dtw, hipStream_t st);
 hipError_t launch_params_init(int64_t D, int64_t M, double hl_min, double hl_max, double per_min, double per_max,
                               double alpha_min, float* tg, float* tw, hipStream_t st);
+hipError_t launch_decode_consts(int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,
+                                const float* phase, float* tab, hipStream_t st);
+template <typename TX, typename TY>
+hipError_t launch_decode_tab(int64_t B, int64_t D, int64_t M, const void* x, void* y, const float* tab,
+                             float* state, hipStream_t st);
 template <typename TX, typename TY>
 hipError_t launch_decode_steps(int64_t B, int64_t N, int64_t D, int64_t M, const void* x, void* y,
                                const float* gamma, const float* omega, const float* amp,

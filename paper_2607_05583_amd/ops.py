@@ -194,6 +194,38 @@ def resonator_decode_step(x_t, gamma, omega, amp, phase, state, out_dtype=None, 
     return y
 
 
+def resonator_decode_constants(gamma, omega, amp, phase, out=None):
+    """The decode constants table [D, M, 6] float32 (lambda's float32 pair hi, lo
+    and c, as (Re, Im)), evaluated once for resonator_decode_step_tab."""
+    gamma, omega, amp, phase = _params(gamma, omega, amp, phase)
+    D, M = gamma.shape
+    tab = out if out is not None else torch.empty((D, M, 6), dtype=torch.float32, device=gamma.device)
+    if tab.dtype != torch.float32 or tuple(tab.shape) != (D, M, 6) or not tab.is_contiguous():
+        raise ValueError("tab must be a contiguous float32 [D, M, 6] tensor")
+    check(_lib.lib().resonator_decode_constants(D, M, _ptr(gamma), _ptr(omega), _ptr(amp), _ptr(phase),
+                                                _ptr(tab), _stream(gamma.device)))
+    return tab
+
+
+def resonator_decode_step_tab(x_t, tab, state, out_dtype=None, out=None):
+    """One decode step from a constants table (bitwise resonator_decode_step):
+    updates state [B, D, M, 2] in place, returns y_t [B, D]."""
+    _dev(x_t, "x_t")
+    _dev(state, "state")
+    _dev(tab, "tab")
+    B, D = x_t.shape
+    if tab.dtype != torch.float32 or tab.dim() != 3 or tab.shape[0] != D or tab.shape[2] != 6:
+        raise ValueError("tab must be float32 [D, M, 6]")
+    M = tab.shape[1]
+    if state.dtype != torch.float32 or tuple(state.shape) != (B, D, M, 2):
+        raise ValueError("state must be float32 [B, D, M, 2]")
+    out_dtype = x_t.dtype if out_dtype is None else out_dtype
+    y = out if out is not None else torch.empty((B, D), dtype=out_dtype, device=x_t.device)
+    check(_lib.lib().resonator_decode_step_tab(_ptr(x_t), _code(x_t), _ptr(y), _code(y), B, D, M, _ptr(tab),
+                                               _ptr(state), _stream(x_t.device)))
+    return y
+
+
 def resonator_decode_steps(x, gamma, omega, amp, phase, state, out_dtype=None, out=None):
     """N decode steps in one launch: x [B, N, D] drives known in advance; updates
     state [B, D, M, 2] in place and returns y [B, N, D] (bitwise N decode steps)."""
@@ -221,8 +253,11 @@ class DecodeGraph:
     them in, or pass them to ``replay``), ``y`` [K, B, D] receives the outputs;
     ``state`` [B, D, M, 2] is updated in place by every replay.  The parameters
     and the state are captured by address: update them in place, never rebind
-    them.  The capture records the decode kernels only (no allocation, no memset),
-    and nothing runs until the first replay."""
+    them.  A replay first evaluates the decode constants from the parameters into
+    a table (one launch), then runs the K steps from the table
+    (resonator_decode_step_tab, bitwise resonator_decode_step).  The capture
+    records these kernels only (no allocation, no memset), and nothing runs until
+    the first replay."""
 
     def __init__(self, gamma, omega, amp, phase, state, steps: int, x_dtype=torch.bfloat16, out_dtype=None):
         _dev(state, "state")
@@ -239,14 +274,16 @@ class DecodeGraph:
         self.state = state
         self.x = torch.zeros((steps, B, D), dtype=x_dtype, device=dev)
         self.y = torch.empty((steps, B, D), dtype=out_dtype, device=dev)
+        self.tab = torch.empty((D, M, 6), dtype=torch.float32, device=dev)
         _lib.lib()  # loaded before the capture
         self.graph = torch.cuda.CUDAGraph()
         cur = torch.cuda.current_stream(dev)
         cap = torch.cuda.Stream(dev)
         cap.wait_stream(cur)
         with torch.cuda.stream(cap), torch.cuda.graph(self.graph, stream=cap):
+            resonator_decode_constants(*self.params, out=self.tab)
             for k in range(steps):
-                resonator_decode_step(self.x[k], *self.params, state, out=self.y[k])
+                resonator_decode_step_tab(self.x[k], self.tab, state, out=self.y[k])
         cur.wait_stream(cap)
 
     def replay(self, x=None):

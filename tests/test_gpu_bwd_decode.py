@@ -259,3 +259,36 @@ def test_decode_long_f32_within_1e4(single):
     say(f"  rel err y {e:.3e} state {eh:.3e}")
     assert e <= 1e-4
     assert eh <= 1e-4
+
+
+@pytest.mark.parametrize("B,D,M,act,out,shift", [(64, 256, 8, "bf16", "bf16", False), (5, 70, 5, "f32", "f32", False),
+                                                 (3, 33, 16, "bf16", "f32", False), (17, 40, 8, "f32", "f32", True)])
+def test_decode_step_from_table_is_bitwise_the_step(B, D, M, act, out, shift):
+    """Decode from the constants table (one evaluation of the constants, then
+    table-driven steps) gives bitwise the outputs and state of resonator_decode_step
+    over 12 steps, with the table 16-byte aligned (the fast path) or only 8-byte
+    aligned (shift); and it follows the oracle's recurrence."""
+    say(f"decode from table B={B} D={D} M={M} {act}->{out} shift={shift}")
+    prob = W.random_problem(71 + M, B, 40, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True)
+    x = dev_act(prob["x"], act)
+    pr = params_dev(prob)
+    od = torch.float32 if out == "f32" else torch.bfloat16
+    st1 = ops.resonator_state_init(x[:, :28].contiguous(), *pr)
+    st2 = st1.clone()
+    if shift:
+        buf = torch.empty(D * M * 6 + 2, dtype=torch.float32, device="cuda")
+        tab = ops.resonator_decode_constants(*pr, out=buf[2:].view(D, M, 6))
+    else:
+        tab = ops.resonator_decode_constants(*pr)
+    ys = []
+    for k in range(28, 40):
+        xk = x[:, k].contiguous()
+        y1 = ops.resonator_decode_step(xk, *pr, st1, out_dtype=od)
+        y2 = ops.resonator_decode_step_tab(xk, tab, st2, out_dtype=od)
+        torch.cuda.synchronize()
+        assert torch.equal(y1, y2), k
+        assert torch.equal(st1, st2), k
+        ys.append(y2)
+    yr, hr = O.mix_recurrence(act64(prob["x"], act), *params_np(prob))
+    assert rel_err(host(torch.stack(ys, 1)), yr[:, 28:]) <= tol(act, out)
+    assert rel_err(host(st2), hr) <= (1e-4 if act == "f32" else 2e-2)
