@@ -103,7 +103,6 @@ Geometry make_geom(res_dtype_t act, int64_t B, int64_t L, int64_t D, int64_t M) 
   g.Mp = MODES_PER_GROUP * g.MG;
   g.P = L > 0 ? (L + TILE_T - 1) / TILE_T : 0;
   g.last_len = L > 0 ? (int)(L - (g.P - 1) * TILE_T) : 0;
-  g.seg_len = 1;
   return g;
 }
 

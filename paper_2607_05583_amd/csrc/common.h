@@ -146,7 +146,6 @@ struct Geometry {
   int Mp;        // padded modes 8 * MG
   int64_t P;     // tiles along time
   int last_len;  // valid steps of the last tile (1..TILE_T)
-  int seg_len;   // tiles per segment of the single-kernel forward (1 elsewhere)
 };
 
 __host__ __device__ inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -183,14 +182,7 @@ struct ModeCarry {
 
 // Offsets (bytes) of the workspace regions.
 struct WsLayout {
-  size_t tab, scal, carryc, mpow, spow, agg, carry, alast, flags, part, q0, total;
+  size_t tab, scal, carryc, agg, carry, alast, part, q0, total;
 };
-
-// Flags of the segment look-back.
-// Single-kernel forward: header words (ticket, error) before the payloads, and
-// the pattern of an unpublished payload word (a signalling NaN, which no
-// arithmetic result is).
-constexpr int64_t SEG_HEADER_WORDS = 64;
-constexpr uint32_t PAY_EMPTY_WORD = 0x7FBADBADu;
 
 }  // namespace res

@@ -39,13 +39,10 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
                                                    const float* __restrict__ omega,
                                                    const float* __restrict__ amp,
                                                    const float* __restrict__ phase, int D, int M,
-                                                   int MG, int last_len, int seg_steps,
+                                                   int MG, int last_len,
                                                    TA* __restrict__ tab,
                                                    ModeScalars* __restrict__ scal,
-                                                   ModeCarry* __restrict__ cc,
-                                                   float2* __restrict__ mpow,
-                                                   float2* __restrict__ spow,
-                                                   uint32_t* __restrict__ flags, int64_t nflags) {
+                                                   ModeCarry* __restrict__ cc) {
   // lambda^0..16, then lambda^128, lambda^256, lambda^last_len
   constexpr int NPW = CHUNK + 1 + 3;
   const int d = blockIdx.x;
@@ -54,34 +51,10 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
   __shared__ double2 cm[MODES_PER_GROUP * MG_MAX];  // c
   __shared__ double taps[CHUNK + 1];
 
-  if (flags != nullptr)  // single-kernel forward: header words, then unpublished payload words
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nflags;
-         i += (int64_t)gridDim.x * blockDim.x)
-      flags[i] = i < SEG_HEADER_WORDS ? 0u : PAY_EMPTY_WORD;
   const bool dvalid = d < D;
-  // one round: the table powers and c, then lambda^(16 j) as [d][j][Mp] and
-  // lambda^(seg_steps n) as [d][n][Mp], both straight to global memory
-  const int n_pw = Mp * (NPW + 1), n_mp = mpow ? Mp * CHUNK : 0, n_sp = spow ? Mp * (CHUNK + 1) : 0;
-  for (int t = threadIdx.x; t < n_pw + n_mp + n_sp; t += blockDim.x) {
-    if (t >= n_pw) {
-      const int u = t - n_pw;
-      const bool is_mp = u < n_mp;
-      const int v = is_mp ? u : u - n_mp;
-      const int m = v % Mp, j = v / Mp;
-      const double n = is_mp ? (double)(CHUNK * j) : (double)seg_steps * (double)j;
-      double2 z = make_double2(0.0, 0.0);
-      if (dvalid && m < M) {
-        double sn, cs;
-        sincos((double)omega[d * M + m] * n, &sn, &cs);
-        const double e = exp(-(double)gamma[d * M + m] * n);
-        z = make_double2(e * cs, e * sn);
-      }
-      if (is_mp)
-        mpow[((size_t)d * CHUNK + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
-      else
-        spow[((size_t)d * (CHUNK + 1) + j) * Mp + m] = make_float2((float)z.x, (float)z.y);
-      continue;
-    }
+  // one round: the table powers and c
+  const int n_pw = Mp * (NPW + 1);
+  for (int t = threadIdx.x; t < n_pw; t += blockDim.x) {
     const int m = t / (NPW + 1), k = t % (NPW + 1);
     const bool valid = dvalid && m < M;
     if (k < NPW) {
@@ -788,41 +761,34 @@ __global__ __launch_bounds__(NTHREADS, MG == 1 ? 4 : 2) void fwd_apply_kernel(Fw
 // ---------------------------------------------------------------------------
 // Single-pass forward (one mode group, M <= 8).
 //
-// A chain is one batch row and one block of DW channels (128-byte rows); the
-// work-groups that serve a chain take its tiles (256 steps) in time order.  On
-// arrival a work-group draws its rank r in the chain.  Once all G work-groups of
-// the chain have arrived (they are then all running), the chain is processed in
-// rounds: the work-group of rank r takes tiles r, r + G, r + 2G, ..., so that the
-// tiles a tile waits for are processed at the same time as it or earlier.  If
-// the work-groups do not all arrive within a short bounded wait (part of the
-// device is busy with other work), the chain takes its tiles by ticket instead,
-// first come first served, so that every tile waited for belongs to a running
-// work-group.  Per tile:
-//   pass 1   per channel, S = V x on MFMA (lane (c, q): component c of chunks
-//            4q .. 4q+3); the results of a wave's four channels are exchanged
-//            across lane rows (lane swaps), after which lane (c, k) holds
-//            component c of channel k for all 16 chunks, and the tile's end state
-//            from a zero start, A = sum_n mu^(15-n) S[n] (mu = lambda^16), is 16
-//            steps A <- mu A + S[n] in the lane's own registers.
-//   carry    control waves (one per 16 channels) publish A, find the nearest
-//            earlier tile of the chain whose inclusive end state I is published
-//            (or their work-group's own previous tile, or h0 at the chain start),
-//            fold the published A of the tiles in between, oldest first,
-//            E <- lambda^256 E + A, and publish this tile's I = lambda^256 E + A.
-//   pass 2   the states entering the chunks, H[0] = E, H[n+1] = mu H[n] + S[n]
-//            (the same 16 steps), move through LDS into the MFMA operand layout;
+// A chain is one batch row and one block of DW channels (128-byte rows).  The G
+// work-groups that serve a chain cut it into G contiguous segments of tiles
+// (256 steps).  On arrival a work-group counts itself in the chain; once all G
+// have arrived (they are then all running) the work-group of rank r (block
+// index over the number of chains) takes segment r.  If they do not all arrive
+// within a short bounded wait (part of the device is busy with other work), the
+// chain hands out its segments by ticket instead, first come first served, so
+// that every segment a look-back waits for belongs to a running work-group.
+//   tables   built in LDS by the work-group itself while its first tile loads;
+//            each wave keeps its channels' T, V, U operands in registers.
+//   phase A  the segment's tiles, last to first: per channel S = V x on MFMA
+//            (lane (c, q): component c of chunks 4q .. 4q+3); lane swaps leave
+//            component c of channel k in lane (c, k) for all 16 chunks; the
+//            tile's end state from a zero start, A = sum_n mu^(15-n) S[n]
+//            (mu = lambda^16), is 16 steps A <- mu A + S[n] in the lane's own
+//            registers, and the segment's Aseg = sum_k lambda^(256 k) A of its
+//            k-th last tile.  The first three tiles stay in LDS.
+//   look-back  the segment publishes P_j (segment 0: its inclusive end state
+//            from h0; the others: Aseg), then folds the published P_i of the
+//            earlier segments, oldest first, E <- lambda^(256 S_i) E + P_i.
+//   phase B  the segment's tiles in order: H[0] = E, H[n+1] = mu H[n] + S[n]
+//            (the same 16 steps), moved through LDS into the MFMA operand layout;
 //            y = T x + U H is rounded into the tile buffer and leaves as 128-byte
-//            rows.
-// Load waves issue the tile loads (direct to LDS, four buffers, three tiles
-// ahead) and the row stores; control waves issue no tile traffic, so that their
-// waits on published states never wait behind tile loads (a wave's vector memory
-// operations complete in order).  A published state is a set of device-coherent
-// stores followed, once they have completed, by a flag store; a reader polls the
-// flag, then loads the state with device-coherent loads.  Flags carry the call's
-// epoch, so they are never reset; the counters are reset by the last work-group
-// to finish.
-// Every work-group builds the operand tables of its DW channels itself, in LDS,
-// while its first tile loads.
+//            rows; E moves on as the scan's end state.
+// Every wave issues its share of the tile loads (direct to LDS) and row stores.
+// A published state is a set of 64-bit device-coherent words, each a float and
+// the call's tag, so a reader checks the data itself; the counters are reset by
+// the last work-group of a chain to finish.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint32_t ld_flag(const uint32_t* f) {
   return __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -841,28 +807,6 @@ constexpr uint32_t ARRIVE_WAIT = 64;
 #ifndef RES_FOLD_WORDS
 #define RES_FOLD_WORDS 16
 #endif
-
-// Complex arithmetic on the two modes of a lane, (re_a, im_a, re_b, im_b).
-__device__ __forceinline__ f4 c2mul(const f4& a, const f4& b) {
-  f4 r;
-  r[0] = fmaf(a[0], b[0], -a[1] * b[1]);
-  r[1] = fmaf(a[0], b[1], a[1] * b[0]);
-  r[2] = fmaf(a[2], b[2], -a[3] * b[3]);
-  r[3] = fmaf(a[2], b[3], a[3] * b[2]);
-  return r;
-}
-__device__ __forceinline__ f4 c2fma(const f4& a, const f4& b, const f4& c) {  // a b + c
-  f4 r;
-  r[0] = fmaf(a[0], b[0], fmaf(-a[1], b[1], c[0]));
-  r[1] = fmaf(a[0], b[1], fmaf(a[1], b[0], c[1]));
-  r[2] = fmaf(a[2], b[2], fmaf(-a[3], b[3], c[2]));
-  r[3] = fmaf(a[2], b[3], fmaf(a[3], b[2], c[3]));
-  return r;
-}
-__device__ __forceinline__ f4 mode_pair(float2 u, float2 w) {
-  const f4 r = {u.x, u.y, w.x, w.y};
-  return r;
-}
 
 // One complex multiply-add on the lane's component of a (re, im) lane pair:
 // zr v + zs v' + add, with v' the value of lane i ^ 1 (the other component),
@@ -1655,23 +1599,19 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t n) {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st, float2* mpow, float2* spow, uint32_t* flags, int64_t nflags) {
+                       hipStream_t st) {
   if (bwd)
     hipLaunchKernelGGL((prep_kernel<TA, true>), dim3(g.Dp), dim3(PREP_THREADS), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
-                       spow, flags, nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc);
   else
     hipLaunchKernelGGL((prep_kernel<TA, false>), dim3(g.Dp), dim3(PREP_THREADS), 0, st, gamma, omega, amp,
-                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, g.seg_len * TILE_T, (TA*)tab, scal, cc, mpow,
-                       spow, flags, nflags);
+                       phase, (int)g.D, (int)g.M, g.MG, g.last_len, (TA*)tab, scal, cc);
   return hipGetLastError();
 }
 template hipError_t launch_prep<float>(const Geometry&, const float*, const float*, const float*,
-                                       const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                       hipStream_t, float2*, float2*, uint32_t*, int64_t);
+                                       const float*, bool, void*, ModeScalars*, ModeCarry*, hipStream_t);
 template hipError_t launch_prep<bf16_t>(const Geometry&, const float*, const float*, const float*,
-                                        const float*, bool, void*, ModeScalars*, ModeCarry*,
-                                        hipStream_t, float2*, float2*, uint32_t*, int64_t);
+                                        const float*, bool, void*, ModeScalars*, ModeCarry*, hipStream_t);
 
 template <typename TX>
 hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st, hipEvent_t ev0,

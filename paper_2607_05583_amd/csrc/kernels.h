@@ -40,24 +40,16 @@ struct FwdArgs {
   const void* tab;
   const ModeScalars* scal;
   const ModeCarry* cc;
-  const float2* mpow;  // [Dp][16][Mp]: lambda^(16 j), j = 0..15 (single-kernel forward)
-  const float2* spow;  // [Dp][17][Mp]: lambda^(256 seg_len n), n = 0..16
   const float* h0;   // [B][D][M][2] or null
   float* h_out;      // [B][D][M][2] or null: state at t = L-1
   void* agg;         // per tile [DW * Mp] float4: half-tile end states (A_0, A_1)
   void* car;         // per tile [DW * Mp] float4: entry states of both halves (null: none)
   float2* alast;     // [B][Dp][Mp]: state at t = L-1 from a zero start at the last tile
-  // single-kernel forward: segments of seg_len tiles, ticket order time-major over chains
-  int seg_len, seg_per_chain;
-  uint32_t* ticket;  // segment ticket counter
-  uint32_t* error;   // bit 0: a bounded wait gave up; bit 1: a ticket past the last segment
-  float2* pay_agg;   // per (segment, wave) [channels][8 modes]: the segment's own end state
 };
 
 // Single-pass forward (M <= 8): problem, parameters and the workspace regions.
-// Flags hold the call's epoch (hdr[1]): a tile state is published with
-// 2 epoch + 1 (its end state from zero, A) and 2 epoch + 2 (also its inclusive
-// end state, I); a table unit with epoch + 1.
+// A published segment state is a set of 64-bit words, each a float (low half)
+// and the call's tag, epoch + 1 (high half); hdr[1] holds the epoch.
 // Tile-to-tile chains (2 to 4 work-groups per chain) pass each tile's inclusive
 // end state to the next tile through a ring of STREAM_RING slots per chain; a
 // slot is written again only after the tile that read it has published its own
@@ -85,9 +77,10 @@ struct StreamArgs {
   float* h_out;        // [B][D][M][2] or null
   uint32_t* hdr;       // [0] status (bit 0: a wait gave up, bit 1: stale counters), [1] epoch,
                        // [2] finished chains, [4] a wait of this call gave up
-  uint32_t* chainw;    // [nchains][4]: next ticket, arrived work-groups, tile order (0 open, 1 rounds,
-                       // 2 tickets), finished work-groups
-  uint64_t* agg;        // [nchains][P][8 waves][64][DW / 32] A of each tile (float | tag << 32 per word)
+  uint32_t* chainw;    // [nchains][4]: next ticket, arrived work-groups, segment order (0 open,
+                       // 1 static, 2 tickets), finished work-groups
+  uint64_t* agg;       // [nchains][G][8 waves][64][DW / 32] published state of each segment
+                       // (float | tag << 32 per word); laid out for up to P segments
   uint64_t* ring;       // [nchains][STREAM_RING][8 waves][64][DW / 32] I of recent tiles, or null:
                         // no tile-to-tile chains
 };
@@ -111,8 +104,7 @@ struct BwdArgs {
 template <typename TA>
 hipError_t launch_prep(const Geometry& g, const float* gamma, const float* omega, const float* amp,
                        const float* phase, bool bwd, void* tab, ModeScalars* scal, ModeCarry* cc,
-                       hipStream_t st, float2* mpow = nullptr, float2* spow = nullptr,
-                       uint32_t* flags = nullptr, int64_t nflags = 0);
+                       hipStream_t st);
 
 template <typename TX>
 hipError_t launch_fwd_agg(const Geometry& g, const FwdArgs& a, hipStream_t st,
