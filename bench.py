@@ -126,10 +126,12 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--decode-steps", type=int, default=32768)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--counters", action="store_true",
+    ap.add_argument("--counters", nargs="?", const="fwd", choices=("fwd", "bwd", "decode"),
                     help="short run for rocprofv3 --pmc: one runtime buffer copy of COPY_BYTES "
-                         "(the counter calibration), then --steps prefill forwards on rotating "
-                         "buffers; prints one JSON line and skips everything else")
+                         "(the counter calibration), then --steps launches of one workload: the "
+                         "prefill forward on rotating buffers (fwd, the default), one training "
+                         "layer's forward and backward (bwd), or graph decode replays of 64 steps "
+                         "(decode); prints one JSON line and skips everything else")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build runs the operator on a single "
@@ -185,11 +187,34 @@ def main():
         torch.cuda.synchronize()
         dst.copy_(src)
         torch.cuda.synchronize()
-        for i in range(args.steps):
-            fwd(i % NSET)
+        name = cfg.name
+        if args.counters == "fwd":
+            for i in range(args.steps):
+                fwd(i % NSET)
+        elif args.counters == "bwd":
+            c5 = W.CONFIGS[5]
+            name = c5.name + " layer 0"
+            li = W.train_layer_inputs(c5, 0)
+            tprm = [torch.from_numpy(li[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+            tx = torch.from_numpy(li["x"].view(np.int16)).view(torch.bfloat16).to(dev)
+            tdy = torch.from_numpy(li["dy"].view(np.int16)).view(torch.bfloat16).to(dev)
+            for _ in range(args.steps):
+                ops.resonator_mix_fwd(tx, *tprm)
+                ops.resonator_mix_bwd(tx, tdy, *tprm)
+        else:
+            c4 = W.CONFIGS[4]
+            name = c4.name + " graph replays of 64 steps"
+            di = W.DecodeInputs(c4)
+            dprm = [torch.from_numpy(di.params[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
+            prompt = torch.from_numpy(di.prompt.view(np.int16)).view(torch.bfloat16).to(dev)
+            state = ops.resonator_state_init(prompt, *dprm)
+            g = ops.DecodeGraph(*dprm, state, 64, x_dtype=torch.bfloat16)
+            g.x.copy_(torch.randn(g.x.shape, device=dev).to(torch.bfloat16))
+            for _ in range(args.steps):
+                g.replay()
         torch.cuda.synchronize()
-        print(json.dumps({"counters_run": True, "copy_bytes": COPY_BYTES, "fwd_launches": args.steps,
-                          "workload": cfg.name}), flush=True)
+        print(json.dumps({"counters_run": True, "copy_bytes": COPY_BYTES, "launches": args.steps,
+                          "counters": args.counters, "workload": name}), flush=True)
         return
 
     for i in range(args.warmup):

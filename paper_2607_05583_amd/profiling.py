@@ -9,13 +9,17 @@ writes the few figures that the benchmark line cites:
   traffic       HBM bytes per launch of the single-pass forward kernel from a
                 ``FETCH_SIZE`` run and a ``WRITE_SIZE`` run, each scaled by what the
                 same counter reads for the runtime's plain buffer copy of known
-                size in the same process (``bench.py --counters``).
+                size in the same process (``bench.py --counters``);
+  counters      every counter of several ``--pmc`` runs per dispatch of the
+                kernels named (``bench.py --counters bwd|decode``).
 
 Usage:
   python -m paper_2607_05583_amd.profiling kernel-trace DB_DIR OUT.md --command "..." \
       [--prefill-launches N]
   python -m paper_2607_05583_amd.profiling traffic FETCH_DIR WRITE_DIR OUT.json \
       --copy-bytes N --command "..."
+  python -m paper_2607_05583_amd.profiling counters OUT.md DB_DIR [DB_DIR ...] \
+      --kernels PATTERN[,PATTERN] --command "..."
 """
 from __future__ import annotations
 
@@ -144,6 +148,63 @@ def write_traffic(fetch_dir: str, write_dir: str, out: str, command: str, copy_b
     return res
 
 
+def _all_counters(db_dir: str):
+    """{kernel short name: {counter: average per dispatch}} (instances of a counter
+    summed per dispatch) and {kernel: dispatches} of one --pmc run."""
+    cur = _db(db_dir).cursor()
+    q = ("select name, counter_name, dispatch_id, sum(counter_value) from pmc_events "
+         "group by name, counter_name, dispatch_id")
+    acc, disp = {}, {}
+    for name, cn, did, v in cur.execute(q):
+        k = short_name(name)
+        acc.setdefault(k, {}).setdefault(cn, []).append(v)
+        disp.setdefault(k, set()).add(did)
+    return {k: {cn: sum(v) / len(v) for cn, v in d.items()} for k, d in acc.items()}, \
+        {k: len(v) for k, v in disp.items()}
+
+
+def write_counters(db_dirs, out: str, command: str, kernels, copy_bytes: int):
+    """A table of every counter of the given --pmc runs, per dispatch of each kernel
+    whose name contains one of the patterns; FETCH_SIZE and WRITE_SIZE (KiB per
+    dispatch) are also given in bytes, scaled by the same counters' reading for
+    the runtime's buffer copy of copy_bytes in the same run."""
+    rows, ndisp, scale = {}, {}, {}
+    for d in db_dirs:
+        c, n = _all_counters(d)
+        for k, vals in c.items():
+            if COPY in k:
+                for cn in ("FETCH_SIZE", "WRITE_SIZE"):
+                    if cn in vals:
+                        scale[cn] = copy_bytes / (max(_counter(d, cn, COPY)) * 1024.0)
+                continue
+            if not any(p in k for p in kernels):
+                continue
+            rows.setdefault(k, {}).update(vals)
+            ndisp[k] = max(ndisp.get(k, 0), n[k])
+    names = sorted({cn for v in rows.values() for cn in v})
+    lines = ["# rocprofv3 counters", "", "Commands (from the repository root, on one MI355X), one per counter set:",
+             "", "```", command, "```", "",
+             "Per dispatch, averaged over the dispatches of each kernel (instances of a counter summed). "
+             "SQ cycle and busy counters are as the hardware reports them (summed over the shader engines).", "",
+             "| kernel | dispatches | " + " | ".join(names) + " |",
+             "|---|---:|" + "---:|" * len(names)]
+    for k in sorted(rows):
+        lines.append(f"| `{k}` | {ndisp[k]} | " + " | ".join(f"{rows[k].get(cn, float('nan')):.4g}" for cn in names)
+                     + " |")
+    if scale:
+        lines += ["", "HBM bytes per dispatch (counter KiB x 1024 x the copy's scale: "
+                  + ", ".join(f"{cn} {v:.3f}" for cn, v in sorted(scale.items())) + "):", "",
+                  "| kernel | fetch MB | write MB |", "|---|---:|---:|"]
+        for k in sorted(rows):
+            f = rows[k].get("FETCH_SIZE", float("nan")) * 1024 * scale.get("FETCH_SIZE", float("nan")) / 1e6
+            w = rows[k].get("WRITE_SIZE", float("nan")) * 1024 * scale.get("WRITE_SIZE", float("nan")) / 1e6
+            lines.append(f"| `{k}` | {f:.2f} | {w:.2f} |")
+    lines.append("")
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines))
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -159,7 +220,18 @@ def main():
     b.add_argument("out")
     b.add_argument("--copy-bytes", type=int, required=True)
     b.add_argument("--command", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("out")
+    c.add_argument("db_dirs", nargs="+")
+    c.add_argument("--kernels", required=True, help="comma-separated name patterns")
+    c.add_argument("--copy-bytes", type=int, default=256 << 20)
+    c.add_argument("--command", required=True)
     args = ap.parse_args()
+    if args.cmd == "counters":
+        rows = write_counters(args.db_dirs, args.out, args.command, args.kernels.split(","), args.copy_bytes)
+        for k, v in rows.items():
+            print(k, {cn: round(x, 1) for cn, x in v.items()})
+        return
     if args.cmd == "kernel-trace":
         for r in write_kernel_trace(args.db_dir, args.out, args.command,
                                     prefill_launches=args.prefill_launches)[:8]:
