@@ -167,9 +167,8 @@ WsLayout make_layout(int op, res_dtype_t act, const Geometry& g) {
     w.alast = off;  // [B][Dp][Mp] state at t = L-1 from a zero start at the last tile
     off += align256((size_t)g.B * g.Dp * g.Mp * sizeof(float2));
   } else {
+    // per segment (at most one per tile) records, partial sums, then q0
     w.agg = off;
-    off += align256(tiles_modes * sizeof(float4));
-    w.carry = off;
     off += align256(tiles_modes * sizeof(float4));
     w.part = off;
     off += align256((size_t)g.B * g.P * g.Dp * (16 + 4 * g.Mp) * sizeof(float));
@@ -488,6 +487,10 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
           ? launch_prep<bf16_t>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st)
           : launch_prep<float>(g, gamma, omega, amp, phase, true, base + w.tab, scal, cc, st);
   if (e != hipSuccess) return hip_fail(e, "prep launch");
+  int dev = 0, ncu = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if ((e = hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+    return hip_fail(e, "device attribute");
   BwdArgs a{};
   a.x = x;
   a.dy = dy;
@@ -496,28 +499,26 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
   a.L = L;
   a.D = (int)D;
   a.M = (int)M;
-  a.NB = g.NB;
+  const int dwb = bwd_block_channels((int)es);
+  a.NB = (int)((D + dwb - 1) / dwb);
   a.Dp = g.Dp;
   a.Mp = g.Mp;
   a.P = g.P;
-  a.last_len = g.last_len;
+  a.nseg = bwd_segments(B * a.NB, g.P, ncu);
+  a.S = (g.P + a.nseg - 1) / a.nseg;
+  a.nseg = (int)((g.P + a.S - 1) / a.S);
+  a.fast_io = aligned(x, 16) && aligned(dy, 16) && aligned(dx, 16) && (D * (int64_t)es) % 16 == 0;
   a.tab = base + w.tab;
   a.scal = scal;
+  a.cc = cc;
   a.agg = (float4*)(base + w.agg);
-  a.carry = (const float4*)(base + w.carry);
   a.part = (float*)(base + w.part);
-  float4* q0 = (float4*)(base + w.q0);
+  a.q0 = (float4*)(base + w.q0);
   hipEvent_t ev0, ev1;
   take_timer(&ev0, &ev1);
-  auto tile = [&](int mode, hipEvent_t e0, hipEvent_t e1) {
-    return act_dt == RES_BF16 ? launch_bwd_tile<bf16_t>(g, mode, a, st, e0, e1)
-                              : launch_bwd_tile<float>(g, mode, a, st, e0, e1);
-  };
-  if ((e = tile(MODE_STATE, nullptr, nullptr)) != hipSuccess) return hip_fail(e, "bwd tile-state launch");
-  if ((e = launch_carry_bwd(g, a.agg, (float4*)(base + w.carry), q0, cc, st)) != hipSuccess)
-    return hip_fail(e, "bwd carry launch");
-  if ((e = tile(MODE_APPLY, ev0, ev1)) != hipSuccess) return hip_fail(e, "bwd tile-apply launch");
-  if ((e = launch_bwd_reduce(g, a.part, q0, gamma, omega, amp, phase, h0, dgamma, domega, damp,
+  e = act_dt == RES_BF16 ? launch_bwd<bf16_t>(a, st, ev0, ev1) : launch_bwd<float>(a, st, ev0, ev1);
+  if (e != hipSuccess) return hip_fail(e, "bwd launch");
+  if ((e = launch_bwd_reduce(g, a.nseg, a.part, a.q0, gamma, omega, amp, phase, h0, dgamma, domega, damp,
                              dphase, dh0, st)) != hipSuccess)
     return hip_fail(e, "bwd reduce launch");
   return RES_OK;

@@ -8,306 +8,671 @@
 //   damp = Re(e^{i phi} W), dphase = -Im(c W), dgamma = -Re(c R), domega = -Im(c R)
 // (plus the h0 terms, see bwd_reduce_kernel).
 //
-// Chunked form (chunk n = steps 16n..16n+15, Qin[n], rin[n] = (q, rho) at 16(n+1)):
-//   dx[16n+j]  = sum_{i>=j} K[i-j] dy[16n+i] + Re sum_m c lambda^(16-j) Qin[n]  Tt, Ub
-//   Eq[n] = sum_i lambda^i dy[16n+i],  Er[n] = sum_i i lambda^i dy[16n+i]          Eq, Er
-//   Qin[n-1] = Eq[n] + mu Qin[n],  rin[n-1] = Er[n] + mu (16 Qin[n] + rin[n])     reverse scan
-//   W = sum_n Xs[n] Qin[n] + sum_tau lambda^tau G[tau]
-//   R = sum_n (Xw[n] Qin[n] + Xs[n] rin[n]) + sum_tau tau lambda^tau G[tau]
-//   Xs[n] = sum_j lambda^(16-j) x[16n+j],  Xw[n] = sum_j (16-j) lambda^(16-j) x[16n+j]
-//   G[tau] = sum_n sum_j dy[16n+j+tau] x[16n+j]   (diagonal sums of P = DY X^T)
-// Every product is a 16x16x16 MFMA per channel over the 16 chunks of a tile; the
-// sums over chunks of Xs Qin etc. are MFMAs contracting over the chunk index.
+// Chunked form.  Chunk n of a 256-step tile is steps 16n .. 16n+15; (Q_n, R_n)
+// is (q, rho) at step 16n from every drive at or after it, mu = lambda^16:
+//   Q_n = Eq[n] + mu Q_{n+1},   R_n = Er[n] + mu (16 Q_{n+1} + R_{n+1})
+//   Eq[n] = sum_i lambda^i dy[16n+i],   Er[n] = sum_i i lambda^i dy[16n+i]
+//   dx[16n+j] = sum_{i>=j} K[i-j] dy[16n+i] + Re sum_m c lambda^(16-j) Q_{n+1}     (Tt, Ub)
+//   W = lambda sum_n Xs[n] Q_{n+1} + sum_tau lambda^tau G[tau]
+//   R = lambda sum_n ((Xs + Xw)[n] Q_{n+1} + Xs[n] R_{n+1}) + sum_tau tau lambda^tau G[tau]
+//   Xs[n] = sum_k lambda^k x[16n+15-k],   Xw[n] = sum_k k lambda^k x[16n+15-k]
+//   G[tau] = sum_n sum_j dy[16n+j+tau] x[16n+j]      (diagonal sums of P = DY X^T)
+// The chunk sums of x weighted by lambda^(16-j) and (16-j) lambda^(16-j) that the
+// carried states meet are lambda Xs and lambda (Xs + Xw): the tables of Eq and Er
+// applied to x read backwards inside each chunk, with the factor lambda taken
+// out of the sums.  Every product is a 16x16 MFMA per channel over the 16 chunks
+// of a tile.
+//
+// Work decomposition.  A chain is one batch row and one block of 64-byte rows of
+// channels (32 bf16 or 16 float channels); it is cut into segments of S tiles,
+// one work-group each, four channels per wave.
+//   bwd_state_kernel: the (Q, R) of each segment's own drives at its left edge.
+//   bwd_apply_kernel: the state entering the segment from the right (the later
+//     segments' records folded in float64), then the tiles from right to left:
+//     the products above, the chunk scan carried from tile to tile in
+//     registers, dx, and the segment's partial sums of G, W and R.
+//   bwd_reduce_kernel: fixed-order float64 sums of the partials, the gradients.
+// The per-channel tables (Tt, Eq, Er, Ub) stay in registers for a whole segment.
 #include "common.h"
 #include "kernels.h"
-#include "tile_io.h"
+#include "stream.h"
 
 namespace res {
 
-// Four activations at steps 16(4q + r) + i, r = 0..3, of one LDS tile row: the
-// operand that contracts over the tile's chunks.
-__device__ __forceinline__ s4 chunk_gather(const bf16_t* row, int i, int q) {
-  s4 v;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) v[r] = (short)row[CHUNK * (4 * q + r) + i];
-  return v;
-}
-__device__ __forceinline__ f4 chunk_gather(const float* row, int i, int q) {
-  f4 v;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) v[r] = row[CHUNK * (4 * q + r) + i];
-  return v;
-}
-
-// Layout of the per-tile partial sums: [G(16) | per mode (W re, W im, R re, R im)].
+// Layout of the per-segment partial sums: [G(16) | per mode (W re, W im, R re, R im)]
+// (W and R without the factor lambda of the carried part).
 __host__ __device__ inline int part_stride(int Mp) { return 16 + 4 * Mp; }
 
-// A block of BW_WAVES waves takes one tile; each wave owns CPW channels and
-// works through them in groups of GS (the scan uses GS x 8 lanes, one per
-// (channel, mode)).  Eight waves of 8 channels hold the same LDS as four waves
-// of 16 would, with twice the waves to hide latency.
-constexpr int BW_WAVES = 8;
-constexpr int BW_THREADS = 64 * BW_WAVES;
+// Chain block of the backward: 64-byte rows, four channels per wave.  The
+// time-major LDS tile holds 16 groups of 16 rows (1 KB) filled by direct-to-LDS
+// loads; each group is padded so that the 8-byte (bf16) or 16-byte (float)
+// operand reads of 16 lanes from 16 groups fall on different banks.
+template <typename TX>
+struct BGeo {
+  static constexpr int XE = (int)sizeof(TX);
+  static constexpr int DW = 64 / XE;   // channels per block
+  static constexpr int NW = DW / 4;    // waves
+  static constexpr int NT = 64 * NW;
+  static constexpr int ROWB = 64;
+  static constexpr int GRP = 16 * ROWB + (XE == 2 ? 8 : 16);
+  static constexpr int TB = 16 * GRP;  // bytes of a tile
+  static constexpr int GPW = 16 / NW;  // row groups of a tile per wave
+  __device__ static __forceinline__ int off(int t) { return (t >> 4) * GRP + (t & 15) * ROWB; }
+};
 
-template <typename TX, int MG, int MODE>
-__global__ __launch_bounds__(BW_THREADS) void bwd_tile_kernel(BwdArgs a) {
-  typedef Path<TX> PT;
-  typedef typename PT::XOp XOp;
-  constexpr int DW = tile_channels<TX>();
-  constexpr int GS = 4;                  // channels per group
-  constexpr int CPW = DW / BW_WAVES;
-  constexpr int NCG = CPW / GS;
-  static_assert(CPW % GS == 0, "a wave's channels split into whole groups");
-  typedef TileGeom<TX, DW> GX;
-  constexpr int XP = GX::PITCH;
-  // Mode groups are processed one after another; the scan buffer holds one group.
-  constexpr int NSTR = 36;               // floats per chunk: 16 Q comps | 16 rho comps | 4 pad (banks)
-  constexpr int KSTR = 16 * NSTR + 16;   // floats per channel
-  constexpr int WSB = GS * KSTR;         // floats per wave
-  constexpr int NM = 1 + 5 * MG;
-  constexpr int PP = 17;                 // row pitch of the P dump (odd: rows on distinct banks)
-  constexpr int PDW = 16 * PP;           // DW pairs after P
-  constexpr int PST = PDW + 64 + 4;      // dump per channel: P | DW pairs | DR pairs | pad (banks)
-
-  __shared__ __align__(16) TX dyt[DW * XP];
-  __shared__ __align__(16) TX xt[MODE == MODE_APPLY ? DW * XP : 8];
-  __shared__ __align__(16) float sbuf[BW_WAVES * WSB];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int li = lane & 15, lq = lane >> 4;
-  const int sk = lane >> 3, sj = lane & 7;
-
-  const int64_t tile = blockIdx.x;
-  const int nb = (int)(tile % a.NB);
-  const int64_t rest = tile / a.NB;
-  const int64_t b = rest % a.B;
-  const int64_t p = rest / a.B;
-  const int64_t t0 = p * TILE_T;
-  const int d0 = nb * DW;
-
-  if (tid < NTHREADS) {  // the tile movers are written for NWAVES waves
-    load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.dy), dyt, b, t0, d0, a.L, a.D, tid);
-    if (MODE == MODE_APPLY)
-      load_tile_any<TX, DW>(reinterpret_cast<const TX*>(a.x), xt, b, t0, d0, a.L, a.D, tid);
+// Activation operands of channels ch0 .. ch0+3 in the MFMA B layout: lane (n, q)
+// holds steps 16n + 4q + r, r = 0..3 (REV: steps 16n + 15 - 4q - r).
+template <typename TX, bool REV>
+__device__ __forceinline__ void bgather(const char* xt, int ch0, int n, int q, typename FPath<TX>::XOp (&v)[4]) {
+  typedef BGeo<TX> G;
+  const char* p = xt + n * G::GRP + ch0 * G::XE;
+  if constexpr (sizeof(TX) == 2) {
+    typedef unsigned short us4 __attribute__((ext_vector_type(4)));
+    us4 w[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const us4*>(p + (REV ? 15 - 4 * q - r : 4 * q + r) * G::ROWB);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const us4 e = {w[0][c], w[1][c], w[2][c], w[3][c]};
+      v[c] = __builtin_bit_cast(s4, e);
+    }
+  } else {
+    f4 w[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const f4*>(p + (REV ? 15 - 4 * q - r : 4 * q + r) * G::ROWB);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = f4{w[0][c], w[1][c], w[2][c], w[3][c]};
   }
-  __syncthreads();
+}
+
+// Operands contracting over the tile's chunks: lane (i, q) holds steps
+// 16 (4q + r) + i, r = 0..3, of channels ch0 .. ch0+3.
+template <typename TX>
+__device__ __forceinline__ void cgather(const char* xt, int ch0, int i, int q, typename FPath<TX>::XOp (&v)[4]) {
+  typedef BGeo<TX> G;
+  const char* p = xt + i * G::ROWB + ch0 * G::XE;
+  if constexpr (sizeof(TX) == 2) {
+    typedef unsigned short us4 __attribute__((ext_vector_type(4)));
+    us4 w[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const us4*>(p + (4 * q + r) * G::GRP);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const us4 e = {w[0][c], w[1][c], w[2][c], w[3][c]};
+      v[c] = __builtin_bit_cast(s4, e);
+    }
+  } else {
+    f4 w[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) w[r] = *reinterpret_cast<const f4*>(p + (4 * q + r) * G::GRP);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = f4{w[0][c], w[1][c], w[2][c], w[3][c]};
+  }
+}
+
+// Outputs of channels ch0 .. ch0+3 in the MFMA D layout (lane (n, q) holds steps
+// 16n + 4q + r) into the time-major tile.
+template <typename TX>
+__device__ __forceinline__ void bput4(char* xt, int ch0, int n, int q, const f4 (&acc)[4]) {
+  typedef BGeo<TX> G;
+  char* p = xt + n * G::GRP + 4 * q * G::ROWB + ch0 * G::XE;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    if constexpr (sizeof(TX) == 2) {
+      typedef __bf16 bf4 __attribute__((ext_vector_type(4)));
+      const bf4 v = {(__bf16)acc[0][r], (__bf16)acc[1][r], (__bf16)acc[2][r], (__bf16)acc[3][r]};
+      *reinterpret_cast<bf4*>(p + r * G::ROWB) = v;
+    } else {
+      *reinterpret_cast<f4*>(p + r * G::ROWB) = f4{acc[0][r], acc[1][r], acc[2][r], acc[3][r]};
+    }
+  }
+}
+
+// Direct-to-LDS load of the calling wave's row groups (g = wave + NW i) of a full
+// tile: one 16-byte piece per lane, lane l taking row l / 4, piece l % 4.
+template <typename TX>
+__device__ __forceinline__ void bload(char* buf, const TX* src, int64_t b, int64_t t0, int d0, int64_t L, int D,
+                                      int lane, int wave) {
+  typedef BGeo<TX> G;
+  const int64_t rowb = (int64_t)D * G::XE;
+  const char* base = reinterpret_cast<const char*>(src) + ((b * L + t0) * D + d0) * G::XE;
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
+  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (ln & 3) * 16;
+#pragma unroll
+  for (int i = 0; i < G::GPW; ++i) {
+    const int g = wave + G::NW * i;
+    lds_dma16(base + (int64_t)(16 * g) * rowb, loff, buf + g * G::GRP);
+  }
+}
+
+// Row stores of the calling wave's row groups of a full tile (the same groups
+// as its loads), the LDS reads first, as two 8-byte halves.
+template <typename TX>
+__device__ __forceinline__ void bstore(TX* dst, const char* buf, int64_t b, int64_t t0, int d0, int64_t L, int D,
+                                       int lane, int wave) {
+  typedef BGeo<TX> G;
+  const int64_t rowb = (int64_t)D * G::XE;
+  char* base = reinterpret_cast<char*>(dst) + ((b * L + t0) * D + d0) * G::XE;
+  int ln = lane;
+  asm volatile("" : "+v"(ln));
+  u32x4 v[G::GPW];
+#pragma unroll
+  for (int i = 0; i < G::GPW; ++i) {
+    const uint2* s = reinterpret_cast<const uint2*>(buf + (wave + G::NW * i) * G::GRP + ln * 16);
+    const uint2 u = s[0], w = s[1];
+    v[i] = u32x4{u.x, u.y, w.x, w.y};
+  }
+  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (ln & 3) * 16;
+#pragma unroll
+  for (int i = 0; i < G::GPW; ++i) st_row16(base + (int64_t)(16 * (wave + G::NW * i)) * rowb, loff, v[i]);
+}
+
+// Element copy of a tile that is not full (every thread); zeros outside the tensor.
+template <typename TX>
+__device__ __forceinline__ void bcopy(char* buf, const TX* x, int64_t b, int64_t t0, int d0, int64_t L, int D,
+                                      int tid) {
+  typedef BGeo<TX> G;
+  for (int idx = tid; idx < TILE_T * G::DW; idx += G::NT) {
+    const int t = idx / G::DW, c = idx % G::DW;
+    TX v = from_f32<TX>(0.f);
+    if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
+    *reinterpret_cast<TX*>(buf + G::off(t) + c * G::XE) = v;
+  }
+}
+
+// Guarded element stores of a tile that is not full (every thread).
+template <typename TX>
+__device__ __forceinline__ void bstore_part(TX* y, const char* buf, int64_t b, int64_t t0, int d0, int64_t L,
+                                            int D, int tid) {
+  typedef BGeo<TX> G;
+  for (int idx = tid; idx < TILE_T * G::DW; idx += G::NT) {
+    const int t = idx / G::DW, c = idx % G::DW;
+    if (t0 + t < L && d0 + c < D)
+      y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TX*>(buf + G::off(t) + c * G::XE);
+  }
+}
+
+// The value of the other lane of a (re, im) lane pair (DPP quad_perm [1,0,3,2];
+// every lane is written, so no old value is needed).
+__device__ __forceinline__ float pair_val(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+// A float moved across lanes by a DPP pattern.
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+// Sum over the 16 lanes of a row (every lane of the row gets it): quad pairs,
+// quads, half-row mirror, row mirror.
+__device__ __forceinline__ float row_sum16(float v) {
+  v += dppf<0xB1>(v);
+  v += dppf<0x4E>(v);
+  v += dppf<0x141>(v);
+  v += dppf<0x140>(v);
+  return v;
+}
+
+// One chunk of the right-to-left scan on the lane's component (lane pair = re, im
+// of one mode; the partner's values read by DPP quad_perm [1,0,3,2]):
+//   products with the state (Q, R) = (Q_{n+1}, R_{n+1}):
+//     b1o += xs Q, b1p += xs Q', b2o += xs R + xw Q, b2p += xs R' + xw Q'
+//   then Q <- mur Q + mus Q' + eq, R <- mur t + mus t' + er, t = 16 Q + R
+// (mus = -Im mu on the re lane, +Im mu on the im lane).  A DPP read needs two
+// wait states after a vector write of its source: every DPP source here was
+// written at least two instructions earlier inside this block or before it.
+__device__ __forceinline__ void scan_step(float& Q, float& R, float xs, float xw, float eq, float er, float mur,
+                                          float mus, float c16, float& b1o, float& b1p, float& b2o, float& b2p) {
+  float t, qn, rn;
+  asm volatile(
+      "v_fmac_f32 %[b1o], %[Q], %[xs]\n\t"
+      "v_fmac_f32 %[b2o], %[R], %[xs]\n\t"
+      "v_fmac_f32 %[b2o], %[Q], %[xw]\n\t"
+      "v_fmac_f32_dpp %[b1p], %[Q], %[xs] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %[b2p], %[Q], %[xw] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fmac_f32_dpp %[b2p], %[R], %[xs] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fma_f32 %[t], %[Q], %[c16], %[R]\n\t"
+      "v_fma_f32 %[qn], %[mur], %[Q], %[eq]\n\t"
+      "v_fmac_f32_dpp %[qn], %[Q], %[mus] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf\n\t"
+      "v_fma_f32 %[rn], %[mur], %[t], %[er]\n\t"
+      "v_fmac_f32_dpp %[rn], %[t], %[mus] quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf"
+      : [b1o] "+v"(b1o), [b1p] "+v"(b1p), [b2o] "+v"(b2o), [b2p] "+v"(b2p), [t] "=&v"(t), [qn] "=&v"(qn),
+        [rn] "=&v"(rn)
+      : [Q] "v"(Q), [R] "v"(R), [xs] "v"(xs), [xw] "v"(xw), [eq] "v"(eq), [er] "v"(er), [mur] "v"(mur),
+        [mus] "v"(mus), [c16] "s"(c16));
+  Q = qn;
+  R = rn;
+}
+
+// z^e for e >= 0 by binary powering (float64).
+__device__ __forceinline__ double2 zpow(double2 z, int64_t e) {
+  double2 r = make_double2(1.0, 0.0);
+  for (; e > 0; e >>= 1) {
+    if (e & 1) r = zmul(r, z);
+    z = zmul(z, z);
+  }
+  return r;
+}
+// z^e for 0 <= e < 16 by binary powering (float32).
+__device__ __forceinline__ float2 cpow16(float2 z, int e) {
+  float2 r = make_float2(1.f, 0.f);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    if ((e >> i) & 1) r = cmul(r, z);
+    z = cmul(z, z);
+  }
+  return r;
+}
+
+// Work-group -> (batch row, segment, channel block).  The two 64-byte halves of
+// a 128-byte row (blocks 2k and 2k+1) go to work-groups 8 apart, which the
+// dispatcher places on the same XCD (work-groups go round-robin over the 8
+// XCDs), so that both halves of every line are served by one L2.  Work-groups
+// past the last block or row have no task.
+struct BwdTask {
+  int64_t b;
+  int seg, nb;
+  bool valid;
+};
+__device__ __forceinline__ BwdTask bwd_task(const BwdArgs& a) {
+  const unsigned x = blockIdx.x;
+  const unsigned hf = (x >> 3) & 1u, v = (x >> 4) * 8u + (x & 7u);
+  const unsigned npair = (unsigned)(a.NB + 1) / 2u;
+  const unsigned rest = v / npair;
+  BwdTask t;
+  t.nb = (int)(2u * (v % npair) + hf);
+  t.seg = (int)(rest % (unsigned)a.nseg);
+  t.b = (int64_t)(rest / (unsigned)a.nseg);
+  t.valid = t.nb < a.NB && t.b < a.B;
+  return t;
+}
+inline unsigned bwd_grid(const BwdArgs& a) {
+  const int64_t v = (int64_t)((a.NB + 1) / 2) * a.B * a.nseg;
+  return (unsigned)(((v + 7) / 8) * 16);
+}
+
+// ---------------------------------------------------------------------------
+// Segment records.  Work-group (chain, segment), tiles p0 .. p0 + nt - 1, four
+// channels per wave.  Lane (n, q) of a channel's product Eq (MFMA D layout)
+// holds modes 2q, 2q+1 of chunk n; it accumulates
+//   A_Q += lambda^(256 k + 16 n) Eq_k[n],
+//   A_R += lambda^(256 k + 16 n) (Er_k[n] + (256 k + 16 n) Eq_k[n])
+// over the segment's tiles k (its weight moving on by lambda^256 per tile), and
+// the 16 chunk lanes are summed at the end: the segment's (Q, rho) at its left
+// edge.  Eight tile buffers, seven tiles ahead (a segment of up to eight tiles
+// is in flight at once).
+// ---------------------------------------------------------------------------
+template <typename TX, int MG>
+__global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
+  typedef BGeo<TX> G;
+  typedef FPath<TX> PT;
+  constexpr int NBUF = 8;
+  constexpr int NM = bwd_mats(MG);
+  __shared__ __align__(16) char tb[NBUF][G::TB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ln = lane & 15, lq = lane >> 4;
+  const BwdTask task = bwd_task(a);
+  if (!task.valid) return;
+  const int nb = task.nb, seg = task.seg;
+  const int64_t b = task.b;
+  const int d0 = nb * G::DW, ch0 = 4 * wave;
+  const int64_t p0 = (int64_t)seg * a.S;
+  const int nt = (int)(a.P - p0 < a.S ? a.P - p0 : a.S);
+  const TX* dy = reinterpret_cast<const TX*>(a.dy);
+  auto tile_full = [&](int64_t p) { return a.fast_io && (p + 1) * TILE_T <= a.L && d0 + G::DW <= a.D; };
+
+  uint32_t issued = 0, mark[NBUF];
+#pragma unroll
+  for (int k = 0; k < NBUF - 1; ++k) {
+    if (k < nt && tile_full(p0 + k)) {
+      bload<TX>(tb[k], dy, b, (p0 + k) * TILE_T, d0, a.L, a.D, lane, wave);
+      issued += G::GPW;
+    }
+    mark[k] = issued;
+  }
 
   const char* tab = reinterpret_cast<const char*>(a.tab);
-  float* sb = sbuf + wave * WSB;
-  const f4 zero = {0.f, 0.f, 0.f, 0.f};
-  const size_t tm = (size_t)(b * a.P + p) * a.Dp;  // tile row in [B][P][Dp]
-  static_assert(GS * PST <= WSB, "reduction dump must fit the scan buffer");
+  typename PT::AOp teq[MG][4], ter[MG][4];
+  float2 w[MG][4][2], hop[MG][4][2], aq[MG][4][2], ar[MG][4][2];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int d = d0 + ch0 + c;
+    const char* tp = tab + (size_t)d * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      teq[g][c] = PT::load_a(tp + (1 + 3 * g) * TAB_MAT_BYTES);
+      ter[g][c] = PT::load_a(tp + (2 + 3 * g) * TAB_MAT_BYTES);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const ModeScalars& ms = a.scal[(size_t)d * a.Mp + 8 * g + 2 * lq + h];
+        w[g][c][h] = cpow16(ms.mu, ln);
+        hop[g][c][h] = ms.lamT;
+        aq[g][c][h] = make_float2(0.f, 0.f);
+        ar[g][c][h] = aq[g][c][h];
+      }
+    }
+  }
 
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < nt; ++k) {
+    const int u = k & (NBUF - 1);
+    const int64_t p = p0 + k;
+    if (tile_full(p))
+      wait_vmcnt((int)(issued - mark[u]));
+    else
+      bcopy<TX>(tb[u], dy, b, p * TILE_T, d0, a.L, a.D, tid);
+    __syncthreads();
+    // tile k+7 into the buffer of tile k-1, which every wave has finished with
+    if (k + NBUF - 1 < nt) {
+      const int u7 = (k + NBUF - 1) & (NBUF - 1);
+      if (tile_full(p + NBUF - 1)) {
+        bload<TX>(tb[u7], dy, b, (p + NBUF - 1) * TILE_T, d0, a.L, a.D, lane, wave);
+        issued += G::GPW;
+      }
+      mark[u7] = issued;
+    }
+    typename PT::XOp dyv[4];
+    bgather<TX, false>(tb[u], ch0, ln, lq, dyv);
+    const float s = (float)(TILE_T * k) + 16.f * (float)ln;
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg) {
-    f4 dxacc[GS];
-    f4 pacc[GS];
-    if (MODE == MODE_APPLY) {
+    for (int g = 0; g < MG; ++g) {
 #pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int ch = wave * CPW + cg * GS + k;
-        const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-        const XOp dyv = PT::load_x(&dyt[ch * XP + PT::x_off(li, lq)]);
-        dxacc[k] = PT::mma(PT::load_a(tp), dyv, zero);
-        // P = DY X^T, contracting over the tile's chunks (exact products)
-        pacc[k] = mma_k16_act(chunk_gather(&dyt[ch * XP], li, lq), chunk_gather(&xt[ch * XP], li, lq),
-                              zero);
+      for (int c = 0; c < 4; ++c) {
+        const f4 eq = PT::mma(teq[g][c], dyv[c], zero);
+        const f4 er = PT::mma(ter[g][c], dyv[c], zero);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const float2 e = make_float2(eq[2 * h], eq[2 * h + 1]);
+          const float2 f = make_float2(fmaf(s, eq[2 * h], er[2 * h]), fmaf(s, eq[2 * h + 1], er[2 * h + 1]));
+          aq[g][c][h] = cfma(w[g][c][h], e, aq[g][c][h]);
+          ar[g][c][h] = cfma(w[g][c][h], f, ar[g][c][h]);
+          w[g][c][h] = cmul(w[g][c][h], hop[g][c][h]);
+        }
+      }
+    }
+  }
+
+  const size_t rec = (size_t)(b * a.nseg + seg) * a.Dp;
+#pragma unroll
+  for (int g = 0; g < MG; ++g) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const float4 v = make_float4(row_sum16(aq[g][c][h].x), row_sum16(aq[g][c][h].y),
+                                     row_sum16(ar[g][c][h].x), row_sum16(ar[g][c][h].y));
+        if (ln == 0) a.agg[(rec + d0 + ch0 + c) * a.Mp + 8 * g + 2 * lq + h] = v;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Segment pass.  Work-group (chain, segment), tiles from the segment's last to
+// its first; three buffer pairs (x, dy), two tiles ahead.  Per tile and wave
+// (channels ch0 .. ch0+3):
+//   products: P += DY X^T, dx = Tt dy, and per mode group Eq, Er (of dy), Xs, Xw
+//     (of x read backwards) in the transposed layout, moved by lane swaps so
+//     that lane (component i, channel c) holds chunks 0..15 of component i;
+//   scan: from the state entering the tile on the right, chunk 15 down to 0, with
+//     the partner component of each complex product read across the lane pair;
+//     the states Q_{n+1} go through a per-wave LDS block to the MFMA layout for
+//     dx += Ub Q, and the sums for W and R accumulate per lane;
+//   dx replaces the wave's own dy columns of the tile; the rows leave after the
+//   next tile's barrier (one barrier per tile), and each wave then loads tile
+//   j+2 into the row groups it has just read out.
+// The state at the tile's left edge carries to the next tile in registers.
+// ---------------------------------------------------------------------------
+constexpr int BH_P = 20;               // floats per chunk row of the state block (16 + 4 of bank offset)
+constexpr int BH_K = 16 * BH_P + 4;    // floats per channel of the state block
+static_assert(4 * BH_K >= 4 * 16 * 17, "the state block also holds the P dump");
+
+template <typename TX, int MG>
+__global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
+  typedef BGeo<TX> G;
+  typedef FPath<TX> PT;
+  typedef typename PT::XOp XOp;
+  constexpr int NBUF = 3;
+  constexpr int NM = bwd_mats(MG);
+  __shared__ __align__(16) char xb[NBUF][G::TB];
+  __shared__ __align__(16) char yb[NBUF][G::TB];
+  __shared__ __align__(16) float hb[G::NW * 4 * BH_K];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ln = lane & 15, lq = lane >> 4;
+  const BwdTask task = bwd_task(a);
+  if (!task.valid) return;
+  const int nb = task.nb, seg = task.seg;
+  const int64_t b = task.b;
+  const int d0 = nb * G::DW, ch0 = 4 * wave;
+  const int64_t p0 = (int64_t)seg * a.S;
+  const int nt = (int)(a.P - p0 < a.S ? a.P - p0 : a.S);
+  const int64_t plast = p0 + nt - 1;
+  const TX* x = reinterpret_cast<const TX*>(a.x);
+  const TX* dy = reinterpret_cast<const TX*>(a.dy);
+  TX* dx = reinterpret_cast<TX*>(a.dx);
+  auto tile_full = [&](int64_t p) { return a.fast_io && (p + 1) * TILE_T <= a.L && d0 + G::DW <= a.D; };
+  auto load = [&](int u, int64_t p) {
+    bload<TX>(xb[u], x, b, p * TILE_T, d0, a.L, a.D, lane, wave);
+    bload<TX>(yb[u], dy, b, p * TILE_T, d0, a.L, a.D, lane, wave);
+  };
+
+  uint32_t issued = 0, mark[NBUF] = {0u, 0u, 0u};
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    if (j < nt && tile_full(plast - j)) {
+      load(j, plast - j);
+      issued += 2 * G::GPW;
+    }
+    mark[j] = issued;
+  }
+
+  // tables of the wave's channels
+  const char* tab = reinterpret_cast<const char*>(a.tab);
+  typename PT::AOp tt[4], teq[MG][4], ter[MG][4];
+  typename PT::UOp ub[MG][4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const char* tp = tab + (size_t)(d0 + ch0 + c) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+    tt[c] = PT::load_a(tp);
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      teq[g][c] = PT::load_a(tp + (1 + 3 * g) * TAB_MAT_BYTES);
+      ter[g][c] = PT::load_a(tp + (2 + 3 * g) * TAB_MAT_BYTES);
+      ub[g][c] = PT::u_op(load_f4(tp + (3 + 3 * g) * TAB_MAT_BYTES));
+    }
+  }
+
+  // scan lane (component ln, channel lq): channel sd, mode 8 g + ln / 2
+  const int sd = d0 + ch0 + lq;
+  const int hc = ln & 1;
+  float mur[MG], mus[MG], Qc[MG], Rc[MG];
+#pragma unroll
+  for (int g = 0; g < MG; ++g) {
+    const size_t im = (size_t)sd * a.Mp + 8 * g + (ln >> 1);
+    const float2 mu = a.scal[im].mu;
+    mur[g] = mu.x;
+    mus[g] = hc ? mu.y : -mu.y;
+    // the state entering the segment from the right: the records of the later
+    // segments j, right to left, C <- (lambda^(256 S) C_Q, lambda^(256 S) (C_R + 256 S C_Q)) + A_j
+    const double2 hop = zpow(a.cc[im].lamT, a.S);
+    const double span = (double)TILE_T * (double)a.S;
+    double2 CQ = make_double2(0.0, 0.0), CR = CQ;
+    constexpr int FB = 8;
+    for (int j1 = a.nseg - 1; j1 > seg; j1 -= FB) {
+      float4 A[FB];
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        const int j = j1 - i > seg ? j1 - i : j1;  // past the first later segment: any valid record, unused
+        A[i] = a.agg[((size_t)(b * a.nseg + j) * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1)];
+      }
+#pragma unroll
+      for (int i = 0; i < FB; ++i) {
+        if (j1 - i > seg) {
+          const double2 t = make_double2(fma(span, CQ.x, CR.x), fma(span, CQ.y, CR.y));
+          CR = zfma(hop, t, make_double2(A[i].z, A[i].w));
+          CQ = zfma(hop, CQ, make_double2(A[i].x, A[i].y));
+        }
+      }
+    }
+    Qc[g] = (float)(hc ? CQ.y : CQ.x);
+    Rc[g] = (float)(hc ? CR.y : CR.x);
+  }
+
+  float b1o[MG], b1p[MG], b2o[MG], b2p[MG];
+#pragma unroll
+  for (int g = 0; g < MG; ++g) b1o[g] = b1p[g] = b2o[g] = b2p[g] = 0.f;
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  f4 pacc[4] = {zero, zero, zero, zero};
+  float* hw = hb + wave * 4 * BH_K;
+  const float c16 = __builtin_amdgcn_readfirstlane(16.f);
+
+  for (int j = 0; j < nt; ++j) {
+    const int u = j % NBUF;
+    const int64_t p = plast - j;
+    if (tile_full(p)) {
+      wait_vmcnt((int)(issued - mark[u]));
+    } else {
+      bcopy<TX>(xb[u], x, b, p * TILE_T, d0, a.L, a.D, tid);
+      bcopy<TX>(yb[u], dy, b, p * TILE_T, d0, a.L, a.D, tid);
+    }
+    // tile j is in; every wave is done with tile j-1 (its x read, its dx written)
+    __syncthreads();
+    // the rows of tile j-1 and the load of tile j+2: the upper half of the waves
+    // issues them before the products, the lower half after, so that the two
+    // waves of a SIMD run their matrix and vector phases out of step
+    auto memory = [&]() {
+    if (j >= 1) {
+      // the rows of dx of tile j-1, then tile j+2 into the same buffers (each
+      // wave loads the row groups it has just read out)
+      const int up = (j - 1) % NBUF;
+      if (tile_full(p + 1)) {
+        bstore<TX>(dx, yb[up], b, (p + 1) * TILE_T, d0, a.L, a.D, lane, wave);
+        issued += G::GPW;
+      } else {
+        bstore_part<TX>(dx, yb[up], b, (p + 1) * TILE_T, d0, a.L, a.D, tid);
+        __syncthreads();  // every thread read the whole tile
+      }
+    }
+    if (j + 2 < nt) {
+      const int u2 = (j + 2) % NBUF;
+      if (tile_full(p - 2)) {
+        load(u2, p - 2);
+        issued += 2 * G::GPW;
+      }
+      mark[u2] = issued;
+    }
+    };
+    const bool mem_first = wave >= G::NW / 2 || !tile_full(p + 1) || j == 0;
+    if (mem_first) memory();
+
+    const char* xt = xb[u];
+    char* yt = yb[u];
+    f4 dxa[4];
+    XOp dyv[4], xrv[4];
+    {
+      XOp dyc[4], xc[4];
+      cgather<TX>(yt, ch0, ln, lq, dyc);
+      cgather<TX>(xt, ch0, ln, lq, xc);
+      bgather<TX, false>(yt, ch0, ln, lq, dyv);
+      bgather<TX, true>(xt, ch0, ln, lq, xrv);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        pacc[c] = mma_k16_act(dyc[c], xc[c], pacc[c]);
+        dxa[c] = PT::mma(tt[c], dyv[c], zero);
       }
     }
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
-      // ---- chunk sums of dy: Eq, Er -------------------------------------------
+      float Eq[16], Er[16], Xs[16], Xw[16];
+      {
+        f4 R[4];
 #pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int ch = wave * CPW + cg * GS + k;
-        const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-        const XOp dyv = PT::load_x(&dyt[ch * XP + PT::x_off(li, lq)]);
-        const f4 eq = PT::mma(PT::load_a(tp + (1 + 5 * g) * TAB_MAT_BYTES), dyv, zero);
-        const f4 er = PT::mma(PT::load_a(tp + (2 + 5 * g) * TAB_MAT_BYTES), dyv, zero);
-        *reinterpret_cast<f4*>(&sb[k * KSTR + li * NSTR + lq * 4]) = eq;
-        *reinterpret_cast<f4*>(&sb[k * KSTR + li * NSTR + 16 + lq * 4]) = er;
-      }
-      __syncthreads();
-      // ---- reverse scan over the tile's chunks, one lane per (channel, mode) ---
-      if (sk < GS) {
-        const int ch = wave * CPW + cg * GS + sk;
-        const int dch = d0 + ch;
-        const int m = g * 8 + sj;
-        const float2 mu = a.scal[(size_t)dch * a.Mp + m].mu;
-        float2 Q = make_float2(0.f, 0.f), Rr = Q;
-        float2 wQ = Q, wR = Q;
-        if (MODE == MODE_APPLY) {
-          const float4 c = a.carry[(tm + dch) * a.Mp + m];
-          wQ = make_float2(c.x, c.y);
-          wR = make_float2(c.z, c.w);
-        }
-        float* eqp = &sb[sk * KSTR + 2 * sj];
-        float* erp = eqp + 16;
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(dyv[c], teq[g][c], zero);
+        lanes_to_chunks(R, Eq);
 #pragma unroll
-        for (int n = NCHUNK - 1; n >= 0; --n) {
-          const float2 eq = *reinterpret_cast<const float2*>(eqp + n * NSTR);
-          const float2 er = *reinterpret_cast<const float2*>(erp + n * NSTR);
-          if (MODE == MODE_APPLY) {
-            // (q, rho) entering chunk n from the right: local part + propagated carry
-            *reinterpret_cast<float2*>(eqp + n * NSTR) = make_float2(Q.x + wQ.x, Q.y + wQ.y);
-            *reinterpret_cast<float2*>(erp + n * NSTR) = make_float2(Rr.x + wR.x, Rr.y + wR.y);
-            const float2 nwQ = cmul(mu, wQ);
-            wR = cmul(mu, make_float2(fmaf(16.f, wQ.x, wR.x), fmaf(16.f, wQ.y, wR.y)));
-            wQ = nwQ;
-          }
-          const float2 nQ = cfma(mu, Q, eq);
-          Rr = cfma(mu, make_float2(fmaf(16.f, Q.x, Rr.x), fmaf(16.f, Q.y, Rr.y)), er);
-          Q = nQ;
-        }
-        if (MODE == MODE_STATE) a.agg[(tm + dch) * a.Mp + m] = make_float4(Q.x, Q.y, Rr.x, Rr.y);
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(dyv[c], ter[g][c], zero);
+        lanes_to_chunks(R, Er);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(xrv[c], teq[g][c], zero);
+        lanes_to_chunks(R, Xs);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(xrv[c], ter[g][c], zero);
+        lanes_to_chunks(R, Xw);
       }
-      __syncthreads();
-      if (MODE == MODE_STATE) continue;
+      float Q = Qc[g], Rr = Rc[g];
+#pragma unroll
+      for (int n = 15; n >= 0; --n) {
+        // (Q, Rr) = (Q_{n+1}, R_{n+1}): to the state block, then the chunk
+        hw[lq * BH_K + n * BH_P + ln] = Q;
+        scan_step(Q, Rr, Xs[n], Xw[n], Eq[n], Er[n], mur[g], mus[g], c16, b1o[g], b1p[g], b2o[g], b2p[g]);
+      }
+      Qc[g] = Q;
+      Rc[g] = Rr;
+      wave_lds_order();
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const f4 h = *reinterpret_cast<const f4*>(&hw[c * BH_K + ln * BH_P + 4 * lq]);
+        dxa[c] = PT::mma_u(ub[g][c], h, dxa[c]);
+      }
+      wave_lds_order();
+    }
+    // dx in place of the wave's own dy columns (read above by this wave only)
+    bput4<TX>(yt, ch0, ln, lq, dxa);
+    if (!mem_first) memory();
+  }
+  __syncthreads();
+  {
+    const int up = (nt - 1) % NBUF;
+    if (tile_full(p0))
+      bstore<TX>(dx, yb[up], b, p0 * TILE_T, d0, a.L, a.D, lane, wave);
+    else
+      bstore_part<TX>(dx, yb[up], b, p0 * TILE_T, d0, a.L, a.D, tid);
+  }
 
-      // ---- dx correction, chunk sums of x, cross products over chunks ---------
-      f4 dwacc[GS], dracc[GS];
+  // (Q, rho) at t = 0
+  if (seg == 0) {
 #pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int ch = wave * CPW + cg * GS + k;
-        const char* tp = tab + (size_t)(d0 + ch) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-        const XOp xv = PT::load_x(&xt[ch * XP + PT::x_off(li, lq)]);
-        const float* srow = &sb[k * KSTR];
-        // dx += Ub Qin (float32 product of the carried states)
-        dxacc[k] = mma_f32(load_f4(tp + (5 + 5 * g) * TAB_MAT_BYTES),
-                           load_f4(&srow[li * NSTR + lq * 4]), dxacc[k]);
-        // Xs^T, Xw^T: rows = chunks, columns = components (the table is the B operand)
-        const f4 xs = PT::mma(xv, PT::load_a(tp + (3 + 5 * g) * TAB_MAT_BYTES), zero);
-        const f4 xw = PT::mma(xv, PT::load_a(tp + (4 + 5 * g) * TAB_MAT_BYTES), zero);
-        // Qin^T, rin^T contracting over chunks: lane (comp, q) holds chunks 4q..4q+3
-        f4 qt, rt;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          qt[r] = srow[(4 * lq + r) * NSTR + li];
-          rt[r] = srow[(4 * lq + r) * NSTR + 16 + li];
-        }
-        dwacc[k] = mma_f32(xs, qt, zero);
-        dracc[k] = mma_f32(xs, rt, mma_f32(xw, qt, zero));
-      }
-      __syncthreads();
-      // ---- dump P (first group) and the 2x2 diagonal blocks, then reduce -------
-#pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        float* dst = &sb[k * PST];
-        if (g == 0) {
-#pragma unroll
-          for (int r = 0; r < 4; ++r) dst[(4 * lq + r) * PP + li] = pacc[k][r];
-        }
-        // lane (col li, q) holds rows 4q..4q+3; the 2x2 diagonal blocks are in lanes li/4 == q
-        if ((li >> 2) == lq) {
-          const int r0 = li & 2;  // rows li&~1 and li|1
-          dst[PDW + li * 2 + 0] = dwacc[k][r0];
-          dst[PDW + li * 2 + 1] = dwacc[k][r0 + 1];
-          dst[PDW + 32 + li * 2 + 0] = dracc[k][r0];
-          dst[PDW + 32 + li * 2 + 1] = dracc[k][r0 + 1];
-        }
-      }
-      __syncthreads();
-      if (sk < GS) {
-        // lane (sk, sj): channel sk of the group; G[sj], G[sj + 8]; mode g*8 + sj
-        const int ch = wave * CPW + cg * GS + sk;
-        const int dch = d0 + ch;
-        const float* src = &sb[sk * PST];
-        float* out = a.part + (tm + dch) * part_stride(a.Mp);
-        if (g == 0) {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            const int tau = sj + 8 * h;
-            float s = 0.f;
-            for (int j = 0; j + tau < 16; ++j) s += src[(j + tau) * PP + j];
-            out[tau] = s;
-          }
-        }
-        // column c holds (D[c&~1][c], D[c|1][c]) at [2c], [2c+1]
-        const float* dwp = &src[PDW];
-        const float* drp = dwp + 32;
-        const int c0 = 2 * sj, c1 = 2 * sj + 1;
-        const float w_rr = dwp[2 * c0], w_ir = dwp[2 * c0 + 1], w_ri = dwp[2 * c1], w_ii = dwp[2 * c1 + 1];
-        const float r_rr = drp[2 * c0], r_ir = drp[2 * c0 + 1], r_ri = drp[2 * c1], r_ii = drp[2 * c1 + 1];
-        float4 v;
-        v.x = w_rr - w_ii;
-        v.y = w_ri + w_ir;
-        v.z = r_rr - r_ii;
-        v.w = r_ri + r_ir;
-        *reinterpret_cast<float4*>(&out[16 + 4 * (g * 8 + sj)]) = v;
-      }
-      __syncthreads();
-    }
-    if (MODE == MODE_APPLY) {
-      // dx -> LDS in place of dy (each wave owns its channels' rows)
-#pragma unroll
-      for (int k = 0; k < GS; ++k) {
-        const int ch = wave * CPW + cg * GS + k;
-        TX v[4];
-#pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = from_f32<TX>(dxacc[k][r]);
-        TX* dst = &dyt[ch * XP + li * CHUNK + lq * 4];
-        if (sizeof(TX) == 2)
-          *reinterpret_cast<uint2*>(dst) = *reinterpret_cast<const uint2*>(v);
-        else
-          *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(v);
-      }
+    for (int g = 0; g < MG; ++g) {
+      float* q = reinterpret_cast<float*>(a.q0 + ((size_t)b * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1));
+      q[hc] = Qc[g];
+      q[2 + hc] = Rc[g];
     }
   }
-  if (MODE == MODE_APPLY) {
-    __syncthreads();
-    if (tid < NTHREADS) store_tile_any<TX, DW>(reinterpret_cast<TX*>(a.dx), dyt, b, t0, d0, a.L, a.D, tid);
+  // partial sums of the segment: W = B1, R = B1 + B2 per mode from the lane pair
+  // (re lane: own products minus the partner's, im lane: cross products added)
+  const size_t rec = (size_t)(b * a.nseg + seg) * a.Dp;
+  const int ps = part_stride(a.Mp);
+#pragma unroll
+  for (int g = 0; g < MG; ++g) {
+    const float o1 = swap_pair(b1o[g]), p1 = swap_pair(b1p[g]);
+    const float o2 = swap_pair(b2o[g]), p2 = swap_pair(b2p[g]);
+    if (hc == 0) {
+      const float wr = b1o[g] - o1, wi = b1p[g] + p1;
+      const float4 v = make_float4(wr, wi, wr + (b2o[g] - o2), wi + (b2p[g] + p2));
+      *reinterpret_cast<float4*>(a.part + (rec + sd) * ps + 16 + 4 * (8 * g + (ln >> 1))) = v;
+    }
   }
+  // G[tau]: P (lane (j, q) holds P[4q + r][j]) through the state block, then the
+  // diagonal sums by lane (tau, channel)
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) hw[c * 272 + (4 * lq + r) * 17 + ln] = pacc[c][r];
+  }
+  wave_lds_order();
+  float sg = 0.f;
+  for (int jj = 0; jj + ln < 16; ++jj) sg += hw[lq * 272 + (jj + ln) * 17 + jj];
+  a.part[(rec + sd) * ps + ln] = sg;
 }
 
 // ---------------------------------------------------------------------------
-// Cross-tile carry, right to left, in float64.  With Incl(p) the (q, rho) pair at
-// the left edge of tile p from all drives at or after it:
-//   carry[p]  = Incl(p+1)  (state entering tile p from the right; 0 for the last)
-//   Incl(p)   = agg[p] + (Lambda Incl_q, Lambda (TILE_T Incl_q + Incl_rho))(p+1)
-//   q0[b,d,m] = Incl(0)   ((q, rho) at t = 0)
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void carry_bwd_kernel(const float4* __restrict__ agg,
-                                                        float4* __restrict__ carry,
-                                                        float4* __restrict__ q0,
-                                                        const ModeCarry* __restrict__ cc, int B,
-                                                        int64_t P, int Dp, int Mp) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)B * Dp * Mp) return;
-  const int m = (int)(idx % Mp);
-  const int d = (int)((idx / Mp) % Dp);
-  const int64_t b = idx / ((int64_t)Mp * Dp);
-  const double2 lT = cc[(size_t)d * Mp + m].lamT;
-  double2 Q = make_double2(0.0, 0.0), Rr = Q;
-  constexpr int BATCH = 16;
-  for (int64_t p1 = P - 1; p1 >= 0; p1 -= BATCH) {
-    float4 ag[BATCH];
-#pragma unroll
-    for (int j = 0; j < BATCH; ++j) {
-      // past the first tile the index is clamped (the value is not used), so
-      // the loads are unconditional and all of them are in flight at once
-      const int64_t p = p1 - j >= 0 ? p1 - j : 0;
-      ag[j] = agg[((size_t)(b * P + p) * Dp + d) * Mp + m];
-    }
-#pragma unroll
-    for (int j = 0; j < BATCH; ++j) {
-      const int64_t p = p1 - j;
-      if (p >= 0) {
-        carry[((size_t)(b * P + p) * Dp + d) * Mp + m] =
-            make_float4((float)Q.x, (float)Q.y, (float)Rr.x, (float)Rr.y);
-        // propagate over tile p (TILE_T steps), then add its own aggregate
-        const double2 tq = make_double2(fma((double)TILE_T, Q.x, Rr.x), fma((double)TILE_T, Q.y, Rr.y));
-        Rr = zfma(lT, tq, make_double2(ag[j].z, ag[j].w));
-        Q = zfma(lT, Q, make_double2(ag[j].x, ag[j].y));
-      }
-    }
-  }
-  q0[((size_t)b * Dp + d) * Mp + m] = make_float4((float)Q.x, (float)Q.y, (float)Rr.x, (float)Rr.y);
-}
-
-// ---------------------------------------------------------------------------
-// Fixed-order reduction of the per-tile partials (float64), one block per channel d:
-//   W = sum_tiles W_inter + sum_tau lambda^tau G[tau] + sum_b lambda q0 h0
-//   R = sum_tiles R_inter + sum_tau tau lambda^tau G[tau] + sum_b lambda (q0 + rho0) h0
+// Fixed-order reduction of the per-segment partials (float64), one block per channel d:
+//   W = lambda sum_segments W' + sum_tau lambda^tau G[tau] + sum_b lambda q0 h0
+//   R = lambda sum_segments R' + sum_tau tau lambda^tau G[tau] + sum_b lambda (q0 + rho0) h0
 //   damp = Re(e^{i phi} W), dphase = -Im(c W), dgamma = -Re(c R), domega = -Im(c R)
 //   dh0[b,d,m] = (Re(c lambda q0), -Im(c lambda q0))
 // ---------------------------------------------------------------------------
@@ -316,16 +681,15 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const float* __restrict__ omega, const float* __restrict__ amp, const float* __restrict__ phase,
     const float* __restrict__ h0, float* __restrict__ dgamma, float* __restrict__ domega,
     float* __restrict__ damp, float* __restrict__ dphase, float* __restrict__ dh0, int B,
-    int64_t P, int D, int M, int Dp, int Mp) {
-  // One block per channel d.  The ps columns of the per-tile partial rows of d
-  // are summed over the B P tiles in float64: thread (row group rg, column col)
-  // takes tiles rg, rg + NRG, ... into eight interleaved accumulators (eight
-  // loads in flight), then the row groups are added in order.  The order is
-  // fixed, so the result is bitwise reproducible.
+    int64_t nrows, int D, int M, int Dp, int Mp) {
+  // One block per channel d.  The ps columns of the partial rows of d are summed
+  // over the nrows (batch row, segment) records in float64: thread (row group rg,
+  // column col) takes records rg, rg + NRG, ... into eight interleaved
+  // accumulators (eight loads in flight), then the row groups are added in
+  // order.  The order is fixed, so the result is bitwise reproducible.
   const int d = blockIdx.x;
   const int ps = part_stride(Mp);
   const int nrg = blockDim.x / ps;
-  const int64_t nbp = (int64_t)B * P;
   __shared__ double s_acc[256];
   __shared__ double s_col[16 + 4 * MODES_PER_GROUP * MG_MAX];
   {
@@ -334,14 +698,14 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     if (rg < nrg) {
       double ac[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
       int64_t bp = rg;
-      for (; bp + 7 * nrg < nbp; bp += 8 * nrg) {
+      for (; bp + 7 * nrg < nrows; bp += 8 * nrg) {
         float v[8];
 #pragma unroll
         for (int u = 0; u < 8; ++u) v[u] = part[((size_t)(bp + u * nrg) * Dp + d) * ps + col];
 #pragma unroll
         for (int u = 0; u < 8; ++u) ac[u] += v[u];
       }
-      for (; bp < nbp; bp += nrg) ac[0] += part[((size_t)bp * Dp + d) * ps + col];
+      for (; bp < nrows; bp += nrg) ac[0] += part[((size_t)bp * Dp + d) * ps + col];
       acc = ((ac[0] + ac[1]) + (ac[2] + ac[3])) + ((ac[4] + ac[5]) + (ac[6] + ac[7]));
     }
     s_acc[threadIdx.x] = acc;
@@ -356,27 +720,27 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
   const int m = threadIdx.x;
   if (m >= M) return;
   const int idx = d * M + m;
-  double G[16];
-#pragma unroll
-  for (int t = 0; t < 16; ++t) G[t] = s_col[t];
-  double Wr = s_col[16 + 4 * m], Wi = s_col[16 + 4 * m + 1], Rr = s_col[16 + 4 * m + 2],
-         Ri = s_col[16 + 4 * m + 3];
   const double g = gamma[idx], w = omega[idx], a = amp[idx], ph = phase[idx];
-#pragma unroll
-  for (int t = 0; t < 16; ++t) {
-    double s, c;
-    sincos(w * t, &s, &c);
-    const double e = exp(-g * t);
-    Wr += e * c * G[t];
-    Wi += e * s * G[t];
-    Rr += t * e * c * G[t];
-    Ri += t * e * s * G[t];
-  }
   double sp, cp, sw, cw;
   sincos(ph, &sp, &cp);
   sincos(w, &sw, &cw);
   const double el = exp(-g);
   const double2 lam = make_double2(el * cw, el * sw);
+  // the carried parts, times lambda
+  const double2 W0 = zmul(lam, make_double2(s_col[16 + 4 * m], s_col[16 + 4 * m + 1]));
+  const double2 R0 = zmul(lam, make_double2(s_col[16 + 4 * m + 2], s_col[16 + 4 * m + 3]));
+  double Wr = W0.x, Wi = W0.y, Rr = R0.x, Ri = R0.y;
+  // the taps: lambda^tau by successive products (float64)
+  double2 pt = make_double2(1.0, 0.0);
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    const double Gt = s_col[t];
+    Wr = fma(pt.x, Gt, Wr);
+    Wi = fma(pt.y, Gt, Wi);
+    Rr = fma(t * pt.x, Gt, Rr);
+    Ri = fma(t * pt.y, Gt, Ri);
+    pt = zmul(pt, lam);
+  }
   const double2 cc = make_double2(a * cp, a * sp);
   const double2 cl = zmul(cc, lam);
   for (int b = 0; b < B; ++b) {
@@ -408,43 +772,41 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
 }
 
 // ---------------------------------------------------------------------------
+int bwd_segments(int64_t nchains, int64_t P, int num_cus) {
+  // about one work-group per compute unit, at least one tile per segment
+  int64_t n = num_cus > nchains ? num_cus / nchains : 1;
+  if (n > P) n = P;
+  if (n < 1) n = 1;
+  return (int)n;
+}
+
 template <typename TX>
-hipError_t launch_bwd_tile(const Geometry& g, int mode, const BwdArgs& a, hipStream_t st,
-                           hipEvent_t ev0, hipEvent_t ev1) {
-  const dim3 grid((unsigned)(g.B * g.P * g.NB)), block(BW_THREADS);
-  if (g.MG == 1) {
-    if (mode == MODE_STATE)
-      launch_timed(bwd_tile_kernel<TX, 1, MODE_STATE>, grid, block, st, ev0, ev1, a);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  typedef BGeo<TX> G;
+  const dim3 grid(bwd_grid(a)), block(G::NT);
+  const bool mg1 = a.Mp == MODES_PER_GROUP;
+  if (a.nseg > 1) {
+    if (mg1)
+      hipLaunchKernelGGL((bwd_state_kernel<TX, 1>), grid, block, 0, st, a);
     else
-      launch_timed(bwd_tile_kernel<TX, 1, MODE_APPLY>, grid, block, st, ev0, ev1, a);
-  } else {
-    if (mode == MODE_STATE)
-      launch_timed(bwd_tile_kernel<TX, 2, MODE_STATE>, grid, block, st, ev0, ev1, a);
-    else
-      launch_timed(bwd_tile_kernel<TX, 2, MODE_APPLY>, grid, block, st, ev0, ev1, a);
+      hipLaunchKernelGGL((bwd_state_kernel<TX, 2>), grid, block, 0, st, a);
   }
+  if (mg1)
+    launch_timed(bwd_apply_kernel<TX, 1>, grid, block, st, ev0, ev1, a);
+  else
+    launch_timed(bwd_apply_kernel<TX, 2>, grid, block, st, ev0, ev1, a);
   return hipGetLastError();
 }
-template hipError_t launch_bwd_tile<float>(const Geometry&, int, const BwdArgs&, hipStream_t,
-                                           hipEvent_t, hipEvent_t);
-template hipError_t launch_bwd_tile<bf16_t>(const Geometry&, int, const BwdArgs&, hipStream_t,
-                                            hipEvent_t, hipEvent_t);
+template hipError_t launch_bwd<float>(const BwdArgs&, hipStream_t, hipEvent_t, hipEvent_t);
+template hipError_t launch_bwd<bf16_t>(const BwdArgs&, hipStream_t, hipEvent_t, hipEvent_t);
 
-hipError_t launch_carry_bwd(const Geometry& g, const float4* agg, float4* carry, float4* q0,
-                            const ModeCarry* cc, hipStream_t st) {
-  const int64_t n = g.B * (int64_t)g.Dp * g.Mp;
-  hipLaunchKernelGGL(carry_bwd_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, agg,
-                     carry, q0, cc, (int)g.B, g.P, g.Dp, g.Mp);
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_reduce(const Geometry& g, const float* part, const float4* q0,
+hipError_t launch_bwd_reduce(const Geometry& g, int nseg, const float* part, const float4* q0,
                              const float* gamma, const float* omega, const float* amp,
                              const float* phase, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st) {
   hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g.D), dim3(256), 0, st, part,
                      q0, gamma, omega, amp, phase, h0, dgamma, domega, damp, dphase, dh0,
-                     (int)g.B, g.P, (int)g.D, (int)g.M, g.Dp, g.Mp);
+                     (int)g.B, g.B * (int64_t)nseg, (int)g.D, (int)g.M, g.Dp, g.Mp);
   return hipGetLastError();
 }
 

@@ -157,13 +157,13 @@ constexpr size_t TAB_MAT_BYTES = 64 * TAB_LANE_BYTES;
 
 // Number of 16x16 operand matrices per channel in the parameter table.
 // Forward: T, then per mode group V[g], U[g].  Backward: Tt, then per mode group
-// Eq[g], Er[g], Xs[g], Xw[g], Ub[g].  Matrices that multiply an activation use
-// the activation path's layout; those that multiply computed float32 states
-// (the forward's U, the backward's Ub) use the float32 layout.
+// Eq[g], Er[g], Ub[g].  Matrices that multiply an activation use the activation
+// path's layout; those that multiply computed float32 states (the forward's U,
+// the backward's Ub) use the float32 layout.
 __host__ __device__ constexpr int fwd_mats(int MG) { return 1 + 2 * MG; }
 __host__ __device__ inline bool fwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 2 == 1; }
-__host__ __device__ inline int bwd_mats(int MG) { return 1 + 5 * MG; }
-__host__ __device__ inline bool bwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 5 == 4; }
+__host__ __device__ constexpr int bwd_mats(int MG) { return 1 + 3 * MG; }
+__host__ __device__ inline bool bwd_mat_is_state(int mat) { return mat > 0 && (mat - 1) % 3 == 2; }
 
 // Per-mode float scalars of the tables (fwd and bwd).
 struct ModeScalars {

@@ -85,20 +85,27 @@ struct StreamArgs {
                         // no tile-to-tile chains
 };
 
+// Backward (M <= 16).  A chain is one batch row and one block of DW channels
+// (64-byte rows: 32 bf16 or 16 float channels), cut into nseg segments of S
+// tiles (the last may be shorter), one work-group per segment.
 struct BwdArgs {
   const void* x;
   const void* dy;
   void* dx;
   int64_t B, L;
   int D, M;
-  int NB, Dp, Mp;
-  int64_t P;
-  int last_len;
+  int NB;               // channel blocks of the backward
+  int Dp, Mp;           // padded channels and modes (record strides)
+  int64_t P;            // tiles per row
+  int64_t S;            // tiles per segment
+  int nseg;             // segments per row
+  int fast_io;          // x, dy and dx 16-byte aligned and rows a multiple of 16 bytes
   const void* tab;
   const ModeScalars* scal;
-  float4* agg;          // per tile (Q, rho) at the tile's left edge, zero entering from the right
-  const float4* carry;  // per tile (Q, rho) entering from the right edge
-  float* part;          // per tile partial sums
+  const ModeCarry* cc;
+  float4* agg;          // [B][nseg][Dp][Mp]: (Q, rho) of a segment's own drives at its left edge
+  float* part;          // [B][nseg][Dp][16 + 4 Mp]: partial sums of G, W and R per segment
+  float4* q0;           // [B][Dp][Mp]: (Q, rho) at t = 0
 };
 
 template <typename TA>
@@ -179,14 +186,15 @@ hipError_t launch_decode_steps(int64_t B, int64_t N, int64_t D, int64_t M, const
                                const float* gamma, const float* omega, const float* amp,
                                const float* phase, float* state, hipStream_t st);
 
+// Segments per row of the backward for a device of num_cus compute units.
+int bwd_segments(int64_t nchains, int64_t P, int num_cus);
+// Channels per block of the backward.
+inline int bwd_block_channels(int elem_bytes) { return 64 / elem_bytes; }
+
 template <typename TX>
-hipError_t launch_bwd_tile(const Geometry& g, int mode, const BwdArgs& a, hipStream_t st,
-                           hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
+hipError_t launch_bwd(const BwdArgs& a, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
-hipError_t launch_carry_bwd(const Geometry& g, const float4* agg, float4* carry, float4* q0,
-                            const ModeCarry* cc, hipStream_t st);
-
-hipError_t launch_bwd_reduce(const Geometry& g, const float* part, const float4* q0,
+hipError_t launch_bwd_reduce(const Geometry& g, int nseg, const float* part, const float4* q0,
                              const float* gamma, const float* omega, const float* amp,
                              const float* phase, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st);
