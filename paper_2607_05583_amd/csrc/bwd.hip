@@ -46,7 +46,10 @@ __host__ __device__ inline int part_stride(int Mp) { return 16 + 4 * Mp; }
 // Chain block of the backward: 64-byte rows, four channels per wave.  The
 // time-major LDS tile holds 16 groups of 16 rows (1 KB) filled by direct-to-LDS
 // loads; each group is padded so that the 8-byte (bf16) or 16-byte (float)
-// operand reads of 16 lanes from 16 groups fall on different banks.
+// operand reads of 16 lanes from 16 groups fall on different banks.  Inside a
+// row the four 16-byte pieces are swizzled: piece k of row t sits in slot
+// k ^ ((t >> 2) & 3), so that 16 lanes reading one piece of the 16 rows of a
+// group also meet 16 different slots.
 template <typename TX>
 struct BGeo {
   static constexpr int XE = (int)sizeof(TX);
@@ -57,7 +60,14 @@ struct BGeo {
   static constexpr int GRP = 16 * ROWB + (XE == 2 ? 8 : 16);
   static constexpr int TB = 16 * GRP;  // bytes of a tile
   static constexpr int GPW = 16 / NW;  // row groups of a tile per wave
-  __device__ static __forceinline__ int off(int t) { return (t >> 4) * GRP + (t & 15) * ROWB; }
+  // byte offset of channel byte cb (0..63) of step t
+  __device__ static __forceinline__ int off(int t, int cb) {
+    return (t >> 4) * GRP + (t & 15) * ROWB + ((((cb >> 4) ^ (t >> 2)) & 3) << 4) + (cb & 15);
+  }
+  // the piece slot of the 4 consecutive channels at ch0 in row group quarter s
+  __device__ static __forceinline__ int slot(int ch0, int s) {
+    return ((((ch0 * XE) >> 4) ^ s) & 3) * 16 + ((ch0 * XE) & 15);
+  }
 };
 
 // Activation operands of channels ch0 .. ch0+3 in the MFMA B layout: lane (n, q)
@@ -65,7 +75,7 @@ struct BGeo {
 template <typename TX, bool REV>
 __device__ __forceinline__ void bgather(const char* xt, int ch0, int n, int q, typename FPath<TX>::XOp (&v)[4]) {
   typedef BGeo<TX> G;
-  const char* p = xt + n * G::GRP + ch0 * G::XE;
+  const char* p = xt + n * G::GRP + G::slot(ch0, REV ? 3 - q : q);
   if constexpr (sizeof(TX) == 2) {
     typedef unsigned short us4 __attribute__((ext_vector_type(4)));
     us4 w[4];
@@ -85,12 +95,61 @@ __device__ __forceinline__ void bgather(const char* xt, int ch0, int n, int q, t
   }
 }
 
+// Table products of the backward (the activation times a per-channel table).
+//   bf16: split-bf16 on v_mfma_f32_16x16x32_bf16.  A table A (from float64) is
+//     stored as Ah = bf16(A), Al = bf16(A - Ah), lane (i, q) holding
+//     Ah[i][8q..8q+7] (q < 2) or Al[i][8(q-2)..8(q-2)+7] (q >= 2); lane (n, q) of
+//     the activation operand holds steps 8 (q & 1) .. 8 (q & 1) + 7 of column n,
+//     so that both halves of the 32-deep contraction meet the same steps and one
+//     instruction gives (Ah + Al) x.
+//   float: four v_mfma_f32_16x16x4_f32, 4 steps per lane (FPath<float>).
+// The activation operand of channels ch0 .. ch0+3: lane (n, q) holds the steps of
+// chunk n above (REV: step 16n + 15 - k in place of 16n + k).
+template <typename TX> struct BPath;
+template <> struct BPath<bf16_t> {
+  typedef bf8 AOp;
+  typedef bf8 XOp;
+  __device__ static __forceinline__ AOp load_a_u4(uint4 u) { return __builtin_bit_cast(bf8, u); }
+  __device__ static __forceinline__ f4 mma(const bf8& a, const bf8& b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  template <bool REV>
+  __device__ static __forceinline__ void gather(const char* xt, int ch0, int n, int q, XOp (&v)[4]) {
+    typedef BGeo<bf16_t> G;
+    typedef unsigned short us4 __attribute__((ext_vector_type(4)));
+    typedef unsigned short us8 __attribute__((ext_vector_type(8)));
+    const char* p = xt + n * G::GRP;
+    const int h = 8 * (q & 1);
+    us4 w[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int row = REV ? 15 - h - r : h + r;
+      w[r] = *reinterpret_cast<const us4*>(p + row * G::ROWB + G::slot(ch0, row >> 2));
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const us8 e = {w[0][c], w[1][c], w[2][c], w[3][c], w[4][c], w[5][c], w[6][c], w[7][c]};
+      v[c] = __builtin_bit_cast(bf8, e);
+    }
+  }
+};
+template <> struct BPath<float> {
+  typedef f4 AOp;
+  typedef f4 XOp;
+  __device__ static __forceinline__ AOp load_a_u4(uint4 u) { return __builtin_bit_cast(f4, u); }
+  __device__ static __forceinline__ f4 mma(const f4& a, const f4& b, f4 c) { return mma_f32(a, b, c); }
+  template <bool REV>
+  __device__ static __forceinline__ void gather(const char* xt, int ch0, int n, int q, XOp (&v)[4]) {
+    bgather<float, REV>(xt, ch0, n, q, v);
+  }
+};
+
 // Operands contracting over the tile's chunks: lane (i, q) holds steps
 // 16 (4q + r) + i, r = 0..3, of channels ch0 .. ch0+3.
 template <typename TX>
 __device__ __forceinline__ void cgather(const char* xt, int ch0, int i, int q, typename FPath<TX>::XOp (&v)[4]) {
   typedef BGeo<TX> G;
-  const char* p = xt + i * G::ROWB + ch0 * G::XE;
+  const char* p = xt + i * G::ROWB + G::slot(ch0, i >> 2);
   if constexpr (sizeof(TX) == 2) {
     typedef unsigned short us4 __attribute__((ext_vector_type(4)));
     us4 w[4];
@@ -115,7 +174,7 @@ __device__ __forceinline__ void cgather(const char* xt, int ch0, int i, int q, t
 template <typename TX>
 __device__ __forceinline__ void bput4(char* xt, int ch0, int n, int q, const f4 (&acc)[4]) {
   typedef BGeo<TX> G;
-  char* p = xt + n * G::GRP + 4 * q * G::ROWB + ch0 * G::XE;
+  char* p = xt + n * G::GRP + 4 * q * G::ROWB + G::slot(ch0, q);
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     if constexpr (sizeof(TX) == 2) {
@@ -138,7 +197,8 @@ __device__ __forceinline__ void bload(char* buf, const TX* src, int64_t b, int64
   const char* base = reinterpret_cast<const char*>(src) + ((b * L + t0) * D + d0) * G::XE;
   int ln = lane;
   asm volatile("" : "+v"(ln));
-  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (ln & 3) * 16;
+  // lane l fills slot l & 3 of row l >> 2: piece (l & 3) ^ quarter of the row
+  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (((ln & 3) ^ (ln >> 4)) & 3) * 16;
 #pragma unroll
   for (int i = 0; i < G::GPW; ++i) {
     const int g = wave + G::NW * i;
@@ -163,7 +223,7 @@ __device__ __forceinline__ void bstore(TX* dst, const char* buf, int64_t b, int6
     const uint2 u = s[0], w = s[1];
     v[i] = u32x4{u.x, u.y, w.x, w.y};
   }
-  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (ln & 3) * 16;
+  const uint32_t loff = (uint32_t)((ln >> 2) * rowb) + (((ln & 3) ^ (ln >> 4)) & 3) * 16;
 #pragma unroll
   for (int i = 0; i < G::GPW; ++i) st_row16(base + (int64_t)(16 * (wave + G::NW * i)) * rowb, loff, v[i]);
 }
@@ -177,7 +237,7 @@ __device__ __forceinline__ void bcopy(char* buf, const TX* x, int64_t b, int64_t
     const int t = idx / G::DW, c = idx % G::DW;
     TX v = from_f32<TX>(0.f);
     if (t0 + t < L && d0 + c < D) v = x[(b * L + t0 + t) * (int64_t)D + d0 + c];
-    *reinterpret_cast<TX*>(buf + G::off(t) + c * G::XE) = v;
+    *reinterpret_cast<TX*>(buf + G::off(t, c * G::XE)) = v;
   }
 }
 
@@ -189,7 +249,7 @@ __device__ __forceinline__ void bstore_part(TX* y, const char* buf, int64_t b, i
   for (int idx = tid; idx < TILE_T * G::DW; idx += G::NT) {
     const int t = idx / G::DW, c = idx % G::DW;
     if (t0 + t < L && d0 + c < D)
-      y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TX*>(buf + G::off(t) + c * G::XE);
+      y[(b * L + t0 + t) * (int64_t)D + d0 + c] = *reinterpret_cast<const TX*>(buf + G::off(t, c * G::XE));
   }
 }
 
@@ -292,20 +352,20 @@ inline unsigned bwd_grid(const BwdArgs& a) {
 }
 
 // ---------------------------------------------------------------------------
-// Segment records.  Work-group (chain, segment), tiles p0 .. p0 + nt - 1, four
-// channels per wave.  Lane (n, q) of a channel's product Eq (MFMA D layout)
-// holds modes 2q, 2q+1 of chunk n; it accumulates
-//   A_Q += lambda^(256 k + 16 n) Eq_k[n],
-//   A_R += lambda^(256 k + 16 n) (Er_k[n] + (256 k + 16 n) Eq_k[n])
-// over the segment's tiles k (its weight moving on by lambda^256 per tile), and
-// the 16 chunk lanes are summed at the end: the segment's (Q, rho) at its left
-// edge.  Eight tile buffers, seven tiles ahead (a segment of up to eight tiles
-// is in flight at once).
+// Segment records.  Work-group (chain, segment), tiles p0 .. p0 + nt - 1 from
+// the last to the first, four channels per wave.  Lane (n, q) of a channel's
+// products Eq, Er (MFMA D layout) holds modes 2q, 2q+1 of chunk n; it keeps the
+// pair (Q_n, R_n) of chunk n summed over the tiles by Horner's rule,
+//   R_n <- h (R_n + 256 Q_n) + Er_k[n],   Q_n <- h Q_n + Eq_k[n],   h = lambda^256,
+// and the segment's (Q, rho) at its left edge is, at the end,
+//   Q = sum_n mu^n Q_n,   rho = sum_n mu^n (R_n + 16 n Q_n),   mu = lambda^16
+// (the 16 chunk lanes summed across the row).  Eight tile buffers, seven tiles
+// ahead (a segment of up to eight tiles is in flight at once).
 // ---------------------------------------------------------------------------
 template <typename TX, int MG>
 __global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
   typedef BGeo<TX> G;
-  typedef FPath<TX> PT;
+  typedef BPath<TX> PT;
   constexpr int NBUF = 8;
   constexpr int NM = bwd_mats(MG);
   __shared__ __align__(16) char tb[NBUF][G::TB];
@@ -323,42 +383,51 @@ __global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
   const TX* dy = reinterpret_cast<const TX*>(a.dy);
   auto tile_full = [&](int64_t p) { return a.fast_io && (p + 1) * TILE_T <= a.L && d0 + G::DW <= a.D; };
 
-  uint32_t issued = 0, mark[NBUF];
-#pragma unroll
-  for (int k = 0; k < NBUF - 1; ++k) {
-    if (k < nt && tile_full(p0 + k)) {
-      bload<TX>(tb[k], dy, b, (p0 + k) * TILE_T, d0, a.L, a.D, lane, wave);
-      issued += G::GPW;
-    }
-    mark[k] = issued;
-  }
-
+  // the tables and mode constants first (ahead of the tile loads in the memory queues)
   const char* tab = reinterpret_cast<const char*>(a.tab);
   typename PT::AOp teq[MG][4], ter[MG][4];
-  float2 w[MG][4][2], hop[MG][4][2], aq[MG][4][2], ar[MG][4][2];
+  float2 hop[MG][4][2], mu[MG][4][2], aq[MG][4][2], ar[MG][4][2];
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     const int d = d0 + ch0 + c;
     const char* tp = tab + (size_t)d * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
-      teq[g][c] = PT::load_a(tp + (1 + 3 * g) * TAB_MAT_BYTES);
-      ter[g][c] = PT::load_a(tp + (2 + 3 * g) * TAB_MAT_BYTES);
+      teq[g][c] = PT::load_a_u4(*reinterpret_cast<const uint4*>(tp + (1 + 3 * g) * TAB_MAT_BYTES));
+      ter[g][c] = PT::load_a_u4(*reinterpret_cast<const uint4*>(tp + (2 + 3 * g) * TAB_MAT_BYTES));
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const ModeScalars& ms = a.scal[(size_t)d * a.Mp + 8 * g + 2 * lq + h];
-        w[g][c][h] = cpow16(ms.mu, ln);
         hop[g][c][h] = ms.lamT;
+        mu[g][c][h] = ms.mu;
         aq[g][c][h] = make_float2(0.f, 0.f);
         ar[g][c][h] = aq[g][c][h];
       }
     }
   }
 
+  uint32_t issued = 0, mark[NBUF];
+  auto tile_of = [&](int k) { return p0 + nt - 1 - k; };
+#pragma unroll
+  for (int k = 0; k < NBUF - 1; ++k) {
+    if (k < nt && tile_full(tile_of(k))) {
+      bload<TX>(tb[k], dy, b, tile_of(k) * TILE_T, d0, a.L, a.D, lane, wave);
+      issued += G::GPW;
+    }
+    mark[k] = issued;
+  }
+  // lambda^(16 n) of the lane's chunk, for the end
+#pragma unroll
+  for (int g = 0; g < MG; ++g)
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) mu[g][c][h] = cpow16(mu[g][c][h], ln);
+
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < nt; ++k) {
     const int u = k & (NBUF - 1);
-    const int64_t p = p0 + k;
+    const int64_t p = tile_of(k);
     if (tile_full(p))
       wait_vmcnt((int)(issued - mark[u]));
     else
@@ -367,15 +436,14 @@ __global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
     // tile k+7 into the buffer of tile k-1, which every wave has finished with
     if (k + NBUF - 1 < nt) {
       const int u7 = (k + NBUF - 1) & (NBUF - 1);
-      if (tile_full(p + NBUF - 1)) {
-        bload<TX>(tb[u7], dy, b, (p + NBUF - 1) * TILE_T, d0, a.L, a.D, lane, wave);
+      if (tile_full(tile_of(k + NBUF - 1))) {
+        bload<TX>(tb[u7], dy, b, tile_of(k + NBUF - 1) * TILE_T, d0, a.L, a.D, lane, wave);
         issued += G::GPW;
       }
       mark[u7] = issued;
     }
     typename PT::XOp dyv[4];
-    bgather<TX, false>(tb[u], ch0, ln, lq, dyv);
-    const float s = (float)(TILE_T * k) + 16.f * (float)ln;
+    PT::template gather<false>(tb[u], ch0, ln, lq, dyv);
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
 #pragma unroll
@@ -384,26 +452,30 @@ __global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
         const f4 er = PT::mma(ter[g][c], dyv[c], zero);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const float2 e = make_float2(eq[2 * h], eq[2 * h + 1]);
-          const float2 f = make_float2(fmaf(s, eq[2 * h], er[2 * h]), fmaf(s, eq[2 * h + 1], er[2 * h + 1]));
-          aq[g][c][h] = cfma(w[g][c][h], e, aq[g][c][h]);
-          ar[g][c][h] = cfma(w[g][c][h], f, ar[g][c][h]);
-          w[g][c][h] = cmul(w[g][c][h], hop[g][c][h]);
+          const float2 t = make_float2(fmaf(256.f, aq[g][c][h].x, ar[g][c][h].x),
+                                       fmaf(256.f, aq[g][c][h].y, ar[g][c][h].y));
+          ar[g][c][h] = cfma(hop[g][c][h], t, make_float2(er[2 * h], er[2 * h + 1]));
+          aq[g][c][h] = cfma(hop[g][c][h], aq[g][c][h], make_float2(eq[2 * h], eq[2 * h + 1]));
         }
       }
     }
   }
 
   const size_t rec = (size_t)(b * a.nseg + seg) * a.Dp;
+  const float s16 = 16.f * (float)ln;
 #pragma unroll
   for (int g = 0; g < MG; ++g) {
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
+      const int d = d0 + ch0 + c;
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const float4 v = make_float4(row_sum16(aq[g][c][h].x), row_sum16(aq[g][c][h].y),
-                                     row_sum16(ar[g][c][h].x), row_sum16(ar[g][c][h].y));
-        if (ln == 0) a.agg[(rec + d0 + ch0 + c) * a.Mp + 8 * g + 2 * lq + h] = v;
+        const float2 w = mu[g][c][h];
+        const float2 q = cmul(w, aq[g][c][h]);
+        const float2 r = cmul(w, make_float2(fmaf(s16, aq[g][c][h].x, ar[g][c][h].x),
+                                             fmaf(s16, aq[g][c][h].y, ar[g][c][h].y)));
+        const float4 v = make_float4(row_sum16(q.x), row_sum16(q.y), row_sum16(r.x), row_sum16(r.y));
+        if (ln == 0) a.agg[(rec + d) * a.Mp + 8 * g + 2 * lq + h] = v;
       }
     }
   }
@@ -432,7 +504,8 @@ static_assert(4 * BH_K >= 4 * 16 * 17, "the state block also holds the P dump");
 template <typename TX, int MG>
 __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
   typedef BGeo<TX> G;
-  typedef FPath<TX> PT;
+  typedef BPath<TX> PT;
+  typedef FPath<TX> UT;
   typedef typename PT::XOp XOp;
   constexpr int NBUF = 3;
   constexpr int NM = bwd_mats(MG);
@@ -460,6 +533,45 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
     bload<TX>(yb[u], dy, b, p * TILE_T, d0, a.L, a.D, lane, wave);
   };
 
+  // Loads of the tables, the mode constants and the first records of the later
+  // segments go out first, then the first two tiles; the values are taken up
+  // after the tile loads are issued.
+  const char* tab = reinterpret_cast<const char*>(a.tab);
+  uint4 rtt[4], rteq[MG][4], rter[MG][4];
+  f4 rub[MG][4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const char* tp = tab + (size_t)(d0 + ch0 + c) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
+    rtt[c] = *reinterpret_cast<const uint4*>(tp);
+#pragma unroll
+    for (int g = 0; g < MG; ++g) {
+      rteq[g][c] = *reinterpret_cast<const uint4*>(tp + (1 + 3 * g) * TAB_MAT_BYTES);
+      rter[g][c] = *reinterpret_cast<const uint4*>(tp + (2 + 3 * g) * TAB_MAT_BYTES);
+      rub[g][c] = load_f4(tp + (3 + 3 * g) * TAB_MAT_BYTES);
+    }
+  }
+  // scan lane (component ln, channel lq): channel sd, mode 8 g + ln / 2
+  const int sd = d0 + ch0 + lq;
+  const int hc = ln & 1;
+  constexpr int FB = 8;
+  float2 rmu[MG];
+  double2 rlt[MG];
+  float4 A[MG][FB];
+  auto records = [&](int g, int j1) {
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+      const int j = j1 - i > seg ? j1 - i : j1;  // past the first later segment: any valid record, unused
+      A[g][i] = a.agg[((size_t)(b * a.nseg + j) * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1)];
+    }
+  };
+#pragma unroll
+  for (int g = 0; g < MG; ++g) {
+    const size_t im = (size_t)sd * a.Mp + 8 * g + (ln >> 1);
+    rmu[g] = a.scal[im].mu;
+    rlt[g] = a.cc[im].lamT;
+    if (a.nseg - 1 > seg) records(g, a.nseg - 1);
+  }
+
   uint32_t issued = 0, mark[NBUF] = {0u, 0u, 0u};
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
@@ -470,51 +582,36 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
     mark[j] = issued;
   }
 
-  // tables of the wave's channels
-  const char* tab = reinterpret_cast<const char*>(a.tab);
   typename PT::AOp tt[4], teq[MG][4], ter[MG][4];
-  typename PT::UOp ub[MG][4];
+  typename UT::UOp ub[MG][4];
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
-    const char* tp = tab + (size_t)(d0 + ch0 + c) * NM * TAB_MAT_BYTES + lane * TAB_LANE_BYTES;
-    tt[c] = PT::load_a(tp);
+    tt[c] = PT::load_a_u4(rtt[c]);
 #pragma unroll
     for (int g = 0; g < MG; ++g) {
-      teq[g][c] = PT::load_a(tp + (1 + 3 * g) * TAB_MAT_BYTES);
-      ter[g][c] = PT::load_a(tp + (2 + 3 * g) * TAB_MAT_BYTES);
-      ub[g][c] = PT::u_op(load_f4(tp + (3 + 3 * g) * TAB_MAT_BYTES));
+      teq[g][c] = PT::load_a_u4(rteq[g][c]);
+      ter[g][c] = PT::load_a_u4(rter[g][c]);
+      ub[g][c] = UT::u_op(rub[g][c]);
     }
   }
-
-  // scan lane (component ln, channel lq): channel sd, mode 8 g + ln / 2
-  const int sd = d0 + ch0 + lq;
-  const int hc = ln & 1;
   float mur[MG], mus[MG], Qc[MG], Rc[MG];
 #pragma unroll
   for (int g = 0; g < MG; ++g) {
-    const size_t im = (size_t)sd * a.Mp + 8 * g + (ln >> 1);
-    const float2 mu = a.scal[im].mu;
-    mur[g] = mu.x;
-    mus[g] = hc ? mu.y : -mu.y;
+    mur[g] = rmu[g].x;
+    mus[g] = hc ? rmu[g].y : -rmu[g].y;
     // the state entering the segment from the right: the records of the later
     // segments j, right to left, C <- (lambda^(256 S) C_Q, lambda^(256 S) (C_R + 256 S C_Q)) + A_j
-    const double2 hop = zpow(a.cc[im].lamT, a.S);
+    const double2 hop = zpow(rlt[g], a.S);
     const double span = (double)TILE_T * (double)a.S;
     double2 CQ = make_double2(0.0, 0.0), CR = CQ;
-    constexpr int FB = 8;
     for (int j1 = a.nseg - 1; j1 > seg; j1 -= FB) {
-      float4 A[FB];
-#pragma unroll
-      for (int i = 0; i < FB; ++i) {
-        const int j = j1 - i > seg ? j1 - i : j1;  // past the first later segment: any valid record, unused
-        A[i] = a.agg[((size_t)(b * a.nseg + j) * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1)];
-      }
+      if (j1 != a.nseg - 1) records(g, j1);
 #pragma unroll
       for (int i = 0; i < FB; ++i) {
         if (j1 - i > seg) {
           const double2 t = make_double2(fma(span, CQ.x, CR.x), fma(span, CQ.y, CR.y));
-          CR = zfma(hop, t, make_double2(A[i].z, A[i].w));
-          CQ = zfma(hop, CQ, make_double2(A[i].x, A[i].y));
+          CR = zfma(hop, t, make_double2(A[g][i].z, A[g][i].w));
+          CQ = zfma(hop, CQ, make_double2(A[g][i].x, A[g][i].y));
         }
       }
     }
@@ -574,11 +671,11 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
     f4 dxa[4];
     XOp dyv[4], xrv[4];
     {
-      XOp dyc[4], xc[4];
+      typename FPath<TX>::XOp dyc[4], xc[4];
       cgather<TX>(yt, ch0, ln, lq, dyc);
       cgather<TX>(xt, ch0, ln, lq, xc);
-      bgather<TX, false>(yt, ch0, ln, lq, dyv);
-      bgather<TX, true>(xt, ch0, ln, lq, xrv);
+      PT::template gather<false>(yt, ch0, ln, lq, dyv);
+      PT::template gather<true>(xt, ch0, ln, lq, xrv);
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         pacc[c] = mma_k16_act(dyc[c], xc[c], pacc[c]);
@@ -591,16 +688,16 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
       {
         f4 R[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(dyv[c], teq[g][c], zero);
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma(dyv[c], teq[g][c], zero);
         lanes_to_chunks(R, Eq);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(dyv[c], ter[g][c], zero);
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma(dyv[c], ter[g][c], zero);
         lanes_to_chunks(R, Er);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(xrv[c], teq[g][c], zero);
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma(xrv[c], teq[g][c], zero);
         lanes_to_chunks(R, Xs);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) R[c] = PT::mma_t(xrv[c], ter[g][c], zero);
+        for (int c = 0; c < 4; ++c) R[c] = PT::mma(xrv[c], ter[g][c], zero);
         lanes_to_chunks(R, Xw);
       }
       float Q = Qc[g], Rr = Rc[g];
@@ -616,7 +713,7 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const f4 h = *reinterpret_cast<const f4*>(&hw[c * BH_K + ln * BH_P + 4 * lq]);
-        dxa[c] = PT::mma_u(ub[g][c], h, dxa[c]);
+        dxa[c] = UT::mma_u(ub[g][c], h, dxa[c]);
       }
       wave_lds_order();
     }
@@ -684,9 +781,9 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     int64_t nrows, int D, int M, int Dp, int Mp) {
   // One block per channel d.  The ps columns of the partial rows of d are summed
   // over the nrows (batch row, segment) records in float64: thread (row group rg,
-  // column col) takes records rg, rg + NRG, ... into eight interleaved
-  // accumulators (eight loads in flight), then the row groups are added in
-  // order.  The order is fixed, so the result is bitwise reproducible.
+  // column col) takes records rg, rg + NRG, ... in batches of eight loads issued
+  // together (predicated past the last record), then the row groups are added
+  // in order.  The order is fixed, so the result is bitwise reproducible.
   const int d = blockIdx.x;
   const int ps = part_stride(Mp);
   const int nrg = blockDim.x / ps;
@@ -696,17 +793,16 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     const int col = threadIdx.x % ps, rg = threadIdx.x / ps;
     double acc = 0.0;
     if (rg < nrg) {
-      double ac[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
-      int64_t bp = rg;
-      for (; bp + 7 * nrg < nrows; bp += 8 * nrg) {
+      for (int64_t bp = rg; bp < nrows; bp += 8 * (int64_t)nrg) {
         float v[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = part[((size_t)(bp + u * nrg) * Dp + d) * ps + col];
+        for (int u = 0; u < 8; ++u) {
+          const int64_t r = bp + u * (int64_t)nrg;
+          v[u] = r < nrows ? part[((size_t)r * Dp + d) * ps + col] : 0.f;
+        }
 #pragma unroll
-        for (int u = 0; u < 8; ++u) ac[u] += v[u];
+        for (int u = 0; u < 8; ++u) acc += v[u];
       }
-      for (; bp < nrows; bp += nrg) ac[0] += part[((size_t)bp * Dp + d) * ps + col];
-      acc = ((ac[0] + ac[1]) + (ac[2] + ac[3])) + ((ac[4] + ac[5]) + (ac[6] + ac[7]));
     }
     s_acc[threadIdx.x] = acc;
   }
@@ -743,7 +839,7 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
   }
   const double2 cc = make_double2(a * cp, a * sp);
   const double2 cl = zmul(cc, lam);
-  for (int b = 0; b < B; ++b) {
+  for (int b = 0; (h0 != nullptr || dh0 != nullptr) && b < B; ++b) {
     const float4 qq = q0[((size_t)b * Dp + d) * Mp + m];
     const double2 qz = make_double2(qq.x, qq.y), rz = make_double2(qq.z, qq.w);
     if (h0 != nullptr) {

@@ -143,7 +143,7 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = (float)entry(mat, i, 4 * q + r);
       out = *reinterpret_cast<const uint4*>(v);
-    } else {  // Ah[i][4q..4q+3], then Al[i][4q..4q+3]
+    } else if (!BWD) {  // Ah[i][4q..4q+3], then Al[i][4q..4q+3]
       bf16_t v[8];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -151,6 +151,15 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
         const bf16_t hi = from_f32<bf16_t>((float)e);
         v[r] = hi;
         v[4 + r] = from_f32<bf16_t>((float)(e - (double)to_f32(hi)));
+      }
+      out = *reinterpret_cast<const uint4*>(v);
+    } else {  // [Ah | Al][i][8q..8q+7] (32-deep contraction, activation duplicated)
+      bf16_t v[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        const double e = entry(mat, i, 8 * (q & 1) + r);
+        const bf16_t hi = from_f32<bf16_t>((float)e);
+        v[r] = (q < 2) ? hi : from_f32<bf16_t>((float)(e - (double)to_f32(hi)));
       }
       out = *reinterpret_cast<const uint4*>(v);
     }
