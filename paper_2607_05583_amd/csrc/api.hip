@@ -518,8 +518,8 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
   take_timer(&ev0, &ev1);
   e = act_dt == RES_BF16 ? launch_bwd<bf16_t>(a, st, ev0, ev1) : launch_bwd<float>(a, st, ev0, ev1);
   if (e != hipSuccess) return hip_fail(e, "bwd launch");
-  if ((e = launch_bwd_reduce(g, a.nseg, a.part, a.q0, gamma, omega, amp, phase, h0, dgamma, domega, damp,
-                             dphase, dh0, st)) != hipSuccess)
+  if ((e = launch_bwd_reduce(g, a.nseg, a.part, a.q0, cc, h0, dgamma, domega, damp, dphase, dh0, st)) !=
+      hipSuccess)
     return hip_fail(e, "bwd reduce launch");
   return RES_OK;
 }

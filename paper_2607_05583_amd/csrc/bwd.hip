@@ -774,8 +774,7 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
 //   dh0[b,d,m] = (Re(c lambda q0), -Im(c lambda q0))
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void bwd_reduce_kernel(
-    const float* __restrict__ part, const float4* __restrict__ q0, const float* __restrict__ gamma,
-    const float* __restrict__ omega, const float* __restrict__ amp, const float* __restrict__ phase,
+    const float* __restrict__ part, const float4* __restrict__ q0, const ModeCarry* __restrict__ cc,
     const float* __restrict__ h0, float* __restrict__ dgamma, float* __restrict__ domega,
     float* __restrict__ damp, float* __restrict__ dphase, float* __restrict__ dh0, int B,
     int64_t nrows, int D, int M, int Dp, int Mp) {
@@ -816,12 +815,10 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
   const int m = threadIdx.x;
   if (m >= M) return;
   const int idx = d * M + m;
-  const double g = gamma[idx], w = omega[idx], a = amp[idx], ph = phase[idx];
-  double sp, cp, sw, cw;
-  sincos(ph, &sp, &cp);
-  sincos(w, &sw, &cw);
-  const double el = exp(-g);
-  const double2 lam = make_double2(el * cw, el * sw);
+  // lambda, c and e^{i phase} of the mode, from the parameter tables (float64)
+  const ModeCarry& mc = cc[(size_t)d * Mp + m];
+  const double2 lam = mc.lam1, ph = mc.ephi;
+  const double cp = ph.x, sp = ph.y;
   // the carried parts, times lambda
   const double2 W0 = zmul(lam, make_double2(s_col[16 + 4 * m], s_col[16 + 4 * m + 1]));
   const double2 R0 = zmul(lam, make_double2(s_col[16 + 4 * m + 2], s_col[16 + 4 * m + 3]));
@@ -837,8 +834,8 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
     Ri = fma(t * pt.y, Gt, Ri);
     pt = zmul(pt, lam);
   }
-  const double2 cc = make_double2(a * cp, a * sp);
-  const double2 cl = zmul(cc, lam);
+  const double2 c = mc.c;
+  const double2 cl = zmul(c, lam);
   for (int b = 0; (h0 != nullptr || dh0 != nullptr) && b < B; ++b) {
     const float4 qq = q0[((size_t)b * Dp + d) * Mp + m];
     const double2 qz = make_double2(qq.x, qq.y), rz = make_double2(qq.z, qq.w);
@@ -859,8 +856,8 @@ __global__ __launch_bounds__(256) void bwd_reduce_kernel(
       dh0[s + 1] = (float)(-z.y);
     }
   }
-  const double2 cW = zmul(cc, make_double2(Wr, Wi));
-  const double2 cR = zmul(cc, make_double2(Rr, Ri));
+  const double2 cW = zmul(c, make_double2(Wr, Wi));
+  const double2 cR = zmul(c, make_double2(Rr, Ri));
   damp[idx] = (float)(cp * Wr - sp * Wi);  // Re(e^{i phi} W)
   dphase[idx] = (float)(-cW.y);
   dgamma[idx] = (float)(-cR.x);
@@ -897,12 +894,10 @@ template hipError_t launch_bwd<float>(const BwdArgs&, hipStream_t, hipEvent_t, h
 template hipError_t launch_bwd<bf16_t>(const BwdArgs&, hipStream_t, hipEvent_t, hipEvent_t);
 
 hipError_t launch_bwd_reduce(const Geometry& g, int nseg, const float* part, const float4* q0,
-                             const float* gamma, const float* omega, const float* amp,
-                             const float* phase, const float* h0, float* dgamma, float* domega,
+                             const ModeCarry* cc, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st) {
-  hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g.D), dim3(256), 0, st, part,
-                     q0, gamma, omega, amp, phase, h0, dgamma, domega, damp, dphase, dh0,
-                     (int)g.B, g.B * (int64_t)nseg, (int)g.D, (int)g.M, g.Dp, g.Mp);
+  hipLaunchKernelGGL(bwd_reduce_kernel, dim3((unsigned)g.D), dim3(256), 0, st, part, q0, cc, h0, dgamma,
+                     domega, damp, dphase, dh0, (int)g.B, g.B * (int64_t)nseg, (int)g.D, (int)g.M, g.Dp, g.Mp);
   return hipGetLastError();
 }
 

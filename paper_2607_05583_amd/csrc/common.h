@@ -178,6 +178,9 @@ struct ModeCarry {
   double2 lamT;    // lambda^TILE_T
   double2 lamEll;  // lambda^last_len
   double2 mu8;     // lambda^(TILE_T / 2)
+  double2 lam1;    // lambda
+  double2 c;       // c = amp e^{i phase}
+  double2 ephi;    // e^{i phase}
 };
 
 // Offsets (bytes) of the workspace regions.

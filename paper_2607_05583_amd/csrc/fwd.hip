@@ -50,6 +50,7 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
   const int Mp = MODES_PER_GROUP * MG;
   __shared__ double2 pw[MODES_PER_GROUP * MG_MAX][NPW];
   __shared__ double2 cm[MODES_PER_GROUP * MG_MAX];  // c
+  __shared__ double2 ep[MODES_PER_GROUP * MG_MAX];  // e^{i phase}
   __shared__ double taps[CHUNK + 1];
 
   const bool dvalid = d < D;
@@ -72,14 +73,16 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
       }
       pw[m][k] = z;
     } else {
-      double2 z = make_double2(0.0, 0.0);
+      double2 z = make_double2(0.0, 0.0), e = z;
       if (valid) {
         double sn, cs;
         sincos((double)phase[d * M + m], &sn, &cs);
         const double av = (double)amp[d * M + m];
         z = make_double2(av * cs, av * sn);
+        e = make_double2(cs, sn);
       }
       cm[m] = z;
+      ep[m] = e;
     }
   }
   __syncthreads();
@@ -97,6 +100,9 @@ __global__ __launch_bounds__(PREP_THREADS) void prep_kernel(const float* __restr
     mc.lamT = lT;
     mc.lamEll = pw[m][CHUNK + 3];
     mc.mu8 = lH;
+    mc.lam1 = lam;
+    mc.c = cm[m];
+    mc.ephi = ep[m];
     cc[(size_t)d * Mp + m] = mc;
   }
   for (int tau = threadIdx.x; tau <= CHUNK; tau += blockDim.x) {  // K[tau] = Re sum_m c lambda^tau

@@ -195,8 +195,7 @@ template <typename TX>
 hipError_t launch_bwd(const BwdArgs& a, hipStream_t st, hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 hipError_t launch_bwd_reduce(const Geometry& g, int nseg, const float* part, const float4* q0,
-                             const float* gamma, const float* omega, const float* amp,
-                             const float* phase, const float* h0, float* dgamma, float* domega,
+                             const ModeCarry* cc, const float* h0, float* dgamma, float* domega,
                              float* damp, float* dphase, float* dh0, hipStream_t st);
 
 template <typename T>
