@@ -36,7 +36,7 @@ COPY = "copyBuffer"
 
 
 # the streaming forward kernel, its launcher and the entry point that sizes its grid
-SEG_SOURCES = ("api.hip", "common.h", "fwd.hip", "tile_io.h")
+SEG_SOURCES = ("api.hip", "common.h", "fwd.hip", "stream.h", "tile_io.h")
 
 
 def source_hash() -> str:
