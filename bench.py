@@ -198,9 +198,13 @@ def main():
             tprm = [torch.from_numpy(li[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
             tx = torch.from_numpy(li["x"].view(np.int16)).view(torch.bfloat16).to(dev)
             tdy = torch.from_numpy(li["dy"].view(np.int16)).view(torch.bfloat16).to(dev)
+            TB, TL, TD, TM = tx.shape[0], tx.shape[1], tx.shape[2], tprm[0].shape[1]
+            tfws = ops.forward_workspace(torch.bfloat16, TB, TL, TD, TM, dev)
+            tbws = torch.empty(max(ops.workspace_bytes(ops.RES_OP_BWD, torch.bfloat16, TB, TL, TD, TM), 256),
+                               dtype=torch.uint8, device=dev)
             for _ in range(args.steps):
-                ops.resonator_mix_fwd(tx, *tprm)
-                ops.resonator_mix_bwd(tx, tdy, *tprm)
+                ops.resonator_mix_fwd(tx, *tprm, ws=tfws)
+                ops.resonator_mix_bwd(tx, tdy, *tprm, ws=tbws)
         else:
             c4 = W.CONFIGS[4]
             name = c4.name + " graph replays of 64 steps"
@@ -462,18 +466,23 @@ def main():
     tprm = [torch.from_numpy(li[k]).to(dev) for k in ("gamma", "omega", "amp", "phase")]
     tx = torch.from_numpy(li["x"].view(np.int16)).view(torch.bfloat16).to(dev)
     tdy = torch.from_numpy(li["dy"].view(np.int16)).view(torch.bfloat16).to(dev)
+    # workspaces allocated once and reused by every call, as in a training loop
+    TB, TL, TD, TM = tx.shape[0], tx.shape[1], tx.shape[2], tprm[0].shape[1]
+    tfws = ops.forward_workspace(torch.bfloat16, TB, TL, TD, TM, dev)
+    tbws = torch.empty(max(ops.workspace_bytes(ops.RES_OP_BWD, torch.bfloat16, TB, TL, TD, TM), 256),
+                       dtype=torch.uint8, device=dev)
     for _ in range(3):
-        ops.resonator_mix_fwd(tx, *tprm)
-        ops.resonator_mix_bwd(tx, tdy, *tprm)
+        ops.resonator_mix_fwd(tx, *tprm, ws=tfws)
+        ops.resonator_mix_bwd(tx, tdy, *tprm, ws=tbws)
     torch.cuda.synchronize()
     nt = 10
     t0e, t1e, t2e, t3e = (torch.cuda.Event(enable_timing=True) for _ in range(4))
     t0e.record(stream)
     for _ in range(nt):
-        ops.resonator_mix_fwd(tx, *tprm)
+        ops.resonator_mix_fwd(tx, *tprm, ws=tfws)
     t1e.record(stream)
     for _ in range(nt):
-        ops.resonator_mix_bwd(tx, tdy, *tprm)
+        ops.resonator_mix_bwd(tx, tdy, *tprm, ws=tbws)
     t2e.record(stream)
     torch.cuda.synchronize()
     tr_fwd_us = t0e.elapsed_time(t1e) * 1e3 / nt
