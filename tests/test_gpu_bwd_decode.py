@@ -61,6 +61,38 @@ def test_bwd_small_shapes(B, L, D, M, use_h0, seed, act):
         _check_bwd(prob, act, use_h0, 2e-2, 2e-2)
 
 
+# Segment geometries of the backward (a row of P tiles in nseg segments of S
+# tiles, about one work-group per compute unit): a ragged last segment with a
+# partial last tile, one multi-tile segment per row (no segment records), and
+# short segments with two mode groups, ragged D and h0.
+BWD_SEGMENTS = [
+    (8, 9372, 256, 8, "bf16", True, 37),
+    (8, 9372, 256, 8, "f32", False, 38),
+    (32, 1024, 256, 8, "bf16", False, 39),
+    (3, 5000, 96, 12, "f32", True, 40),
+]
+
+
+def _segments(B, L, D, act):
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    dw = 32 if act == "bf16" else 16
+    chains, P = B * ((D + dw - 1) // dw), (L + 255) // 256
+    nseg = max(1, min(P, ncu // chains if ncu > chains else 1))
+    S = -(-P // nseg)
+    nseg = -(-P // S)
+    return nseg, S, P - (nseg - 1) * S
+
+
+@pytest.mark.parametrize("B,L,D,M,act,use_h0,seed", BWD_SEGMENTS)
+def test_bwd_segment_geometries(B, L, D, M, act, use_h0, seed):
+    nseg, S, last = _segments(B, L, D, act)
+    say(f"bwd segments B={B} L={L} D={D} M={M} {act} h0={use_h0}: {nseg} segments of {S} tiles (last {last})")
+    prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True,
+                            with_h0=use_h0, with_dy=True)
+    tol = 1e-4 if act == "f32" else 2e-2
+    _check_bwd(prob, act, use_h0, tol, tol)
+
+
 def test_bwd_deterministic():
     say("bwd determinism")
     prob = W.random_problem(40, 2, 3000, 64, 8, act="bf16", gamma_range=(1e-4, 1.0), gamma_log=True,
