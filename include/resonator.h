@@ -222,12 +222,29 @@ int resonator_decode_steps(const void* x, res_dtype_t x_dt, void* y, res_dtype_t
  *   y[n, g dq + j] = sum_i x[n, g di + i] W[g][i][j],   di = d_in / G, dq = d_out / G.
  *   x  [N][d_in], W [G][d_in/G][d_out/G], y [N][d_out], all of dtype dt (bf16 or
  *      f32), device memory, row-major; y must not overlap x or W
- * Float32 accumulation; a plain GEMM, run as one rocBLAS strided-batched GEMM on
- * the given stream.  Calls from several host threads on one device must not
- * overlap (they share that device's rocBLAS handle).  N, d_in, d_out < 2^31.
+ * Float32 accumulation, on the given stream.  When d_in/G is a multiple of 32
+ * (bf16) or 16 (f32), d_out/G a multiple of 16 and at most 128, a row of x at
+ * most 1 KB, the weight at most 64 KB (32 KB with bf16 for
+ * resonator_grouped_linear2) and x, W and y 16-byte aligned, it runs as the
+ * library's own MFMA kernel (16 tokens per wave, weights staged in LDS; bf16
+ * outputs rounded once); other shapes go to one rocBLAS strided-batched GEMM.
+ * Calls from several host threads on one device must not overlap (they share
+ * that device's rocBLAS handle).  N, d_in, d_out < 2^31.
  */
 int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void* y, int64_t N, int64_t d_in,
                              int64_t d_out, int64_t G, void* stream);
+
+/*
+ * Two grouped projections of the same input (Sec. 3.1: the drive u and the gate
+ * g are both projections of the block input), from one read of x:
+ *   y0 = x W0,  y1 = x W1   (each as resonator_grouped_linear; W0 and W1 of
+ *   the same shape [G][d_in/G][d_out/G]; y0 and y1 [N][d_out], overlapping
+ *   neither each other, x, W0 nor W1).
+ * Shapes the MFMA kernel does not take run as two library GEMMs.  Errors as
+ * resonator_grouped_linear.
+ */
+int resonator_grouped_linear2(const void* x, const void* W0, const void* W1, res_dtype_t dt, void* y0, void* y1,
+                              int64_t N, int64_t d_in, int64_t d_out, int64_t G, void* stream);
 
 /*
  * Backward of resonator_grouped_linear (loss sum(dy * y)):

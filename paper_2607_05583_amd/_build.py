@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libresonator.so")
-SOURCES = ["fwd.hip", "bwd.hip", "decode.hip", "epilogue.hip", "params.hip", "quadref.hip", "gemm.hip", "fftref.hip", "api.hip"]
+SOURCES = ["fwd.hip", "bwd.hip", "decode.hip", "epilogue.hip", "params.hip", "quadref.hip", "gemm.hip", "proj.hip", "fftref.hip", "api.hip"]
 ARCH = "gfx950"
 
 

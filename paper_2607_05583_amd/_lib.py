@@ -25,7 +25,7 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
            "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
-           "resonator_grouped_linear", "resonator_block_diag_weight", "resonator_block_diag_extract",
+           "resonator_grouped_linear", "resonator_grouped_linear2", "resonator_block_diag_weight", "resonator_block_diag_extract",
            "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_weight",
            "resonator_grouped_linear_bwd_weight_split", "resonator_grouped_linear_bwd_weight_split_workspace_bytes",
            "resonator_mix_fwd_noalloc", "resonator_mix_fwd_noalloc_max_bytes", "resonator_fwd_status",
@@ -85,6 +85,8 @@ def _declare(lib):
     lib.resonator_fft_reference.argtypes = [vp, vp, i64, i64, i64, i64, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_grouped_linear.restype = i32
     lib.resonator_grouped_linear.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, vp]
+    lib.resonator_grouped_linear2.restype = i32
+    lib.resonator_grouped_linear2.argtypes = [vp, vp, vp, i32, vp, vp, i64, i64, i64, i64, vp]
     lib.resonator_block_diag_weight.restype = i32
     lib.resonator_block_diag_weight.argtypes = [vp, i32, i64, i64, i64, vp, vp]
     lib.resonator_block_diag_extract.restype = i32

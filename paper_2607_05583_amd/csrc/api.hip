@@ -41,6 +41,16 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(RES_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// compute units of the current device (256 if the query fails: only a launch
+// shape depends on it)
+int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n < 1)
+    return 256;
+  return n;
+}
+
 }  // namespace
 
 // Workspace of resonator_mix_fwd_noalloc: every GPU the library runs on holds
@@ -641,7 +651,43 @@ int resonator_grouped_linear(const void* x, const void* W, res_dtype_t dt, void*
     return fail(RES_ERR_MISALIGNED, "x, W and y must be aligned to their element");
   const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * es;
   if (overlap(y, ny, x, nx) || overlap(y, ny, W, nw)) return fail(RES_ERR_INVALID_ARG, "y must not overlap x or W");
-  const char* err = launch_grouped_linear(x, W, y, N, d_in, d_out, G, dt == RES_BF16, (hipStream_t)stream);
+  const bool bf = dt == RES_BF16;
+  if (grouped_proj_supported(x, W, nullptr, y, nullptr, d_in, d_out, G, bf)) {
+    const hipError_t e = launch_grouped_proj(x, W, nullptr, y, nullptr, N, d_in, d_out, G, bf, device_cus(),
+                                             (hipStream_t)stream);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "grouped projection launch");
+  }
+  const char* err = launch_grouped_linear(x, W, y, N, d_in, d_out, G, bf, (hipStream_t)stream);
+  if (err) return fail(RES_ERR_HIP, "grouped linear: %s", err);
+  return RES_OK;
+}
+
+int resonator_grouped_linear2(const void* x, const void* W0, const void* W1, res_dtype_t dt, void* y0, void* y1,
+                              int64_t N, int64_t d_in, int64_t d_out, int64_t G, void* stream) {
+  if (N < 1 || d_in < 1 || d_out < 1 || G < 1)
+    return fail(RES_ERR_INVALID_ARG, "N, d_in, d_out and G must be >= 1");
+  if (d_in % G || d_out % G)
+    return fail(RES_ERR_INVALID_ARG, "d_in (%lld) and d_out (%lld) must be multiples of G (%lld)", (long long)d_in,
+                (long long)d_out, (long long)G);
+  if (N > INT32_MAX || d_in > INT32_MAX || d_out > INT32_MAX)
+    return fail(RES_ERR_UNSUPPORTED, "N, d_in and d_out must be below 2^31");
+  if (!dtype_ok(dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (!x || !W0 || !W1 || !y0 || !y1) return fail(RES_ERR_INVALID_ARG, "x, W0, W1, y0 and y1 must be non-null");
+  const size_t es = elt_size(dt);
+  if (!aligned(x, es) || !aligned(W0, es) || !aligned(W1, es) || !aligned(y0, es) || !aligned(y1, es))
+    return fail(RES_ERR_MISALIGNED, "x, W0, W1, y0 and y1 must be aligned to their element");
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * es;
+  if (overlap(y0, ny, x, nx) || overlap(y0, ny, W0, nw) || overlap(y0, ny, W1, nw) || overlap(y1, ny, x, nx) ||
+      overlap(y1, ny, W0, nw) || overlap(y1, ny, W1, nw) || overlap(y0, ny, y1, ny))
+    return fail(RES_ERR_INVALID_ARG, "y0 and y1 must overlap neither each other, x, W0 nor W1");
+  const bool bf = dt == RES_BF16;
+  if (grouped_proj_supported(x, W0, W1, y0, y1, d_in, d_out, G, bf)) {
+    const hipError_t e = launch_grouped_proj(x, W0, W1, y0, y1, N, d_in, d_out, G, bf, device_cus(),
+                                             (hipStream_t)stream);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "grouped projection launch");
+  }
+  const char* err = launch_grouped_linear(x, W0, y0, N, d_in, d_out, G, bf, (hipStream_t)stream);
+  if (!err) err = launch_grouped_linear(x, W1, y1, N, d_in, d_out, G, bf, (hipStream_t)stream);
   if (err) return fail(RES_ERR_HIP, "grouped linear: %s", err);
   return RES_OK;
 }

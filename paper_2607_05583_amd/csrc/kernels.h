@@ -146,6 +146,12 @@ hipError_t launch_decode(int64_t B, int64_t D, int64_t M, const void* x, void* y
                          const float* phase, float* state, hipStream_t st);
 const char* launch_grouped_linear(const void* x, const void* W, void* y, int64_t N, int64_t d_in, int64_t d_out,
                                   int64_t G, bool bf16, hipStream_t st);
+// MFMA grouped projection (proj.hip): one or two weights (W1 null for one) over
+// the same x; shapes and alignments the kernel takes, else the library GEMM
+bool grouped_proj_supported(const void* x, const void* W0, const void* W1, const void* y0, const void* y1,
+                            int64_t d_in, int64_t d_out, int64_t G, bool bf16);
+hipError_t launch_grouped_proj(const void* x, const void* W0, const void* W1, void* y0, void* y1, int64_t N,
+                               int64_t d_in, int64_t d_out, int64_t G, bool bf16, int num_cus, hipStream_t st);
 const char* launch_grouped_linear_bwd_data(const void* dy, const void* W, void* dx, int64_t N, int64_t d_in,
                                            int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
 const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, float* dW, int64_t N, int64_t d_in,

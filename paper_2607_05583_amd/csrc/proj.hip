@@ -1,0 +1,220 @@
+// Grouped linear projections on MFMA (Sec. 3.1 drive and gate projection,
+// Sec. 3.4 output projection): y[:, g-th output slice] = x[:, g-th input slice]
+// W[g] for G groups of a block-diagonal weight W [G][d_in/G][d_out/G].
+//
+// There are d_in/G multiply-adds per output, so the kernel streams: a wave takes
+// 16 tokens (rows of x) at a time, loads each lane's 16-byte pieces of the rows
+// straight into MFMA activation operands (no LDS), and writes y from the
+// accumulators.  The weights of every group are staged once per work-group in
+// LDS, already in the operand layout, and read as one 16-byte fragment per lane
+// and product.  With two weights (the drive and the gate of the same input) one
+// read of x feeds both outputs.
+//   bf16:  v_mfma_f32_16x16x32_bf16 per (group, 32 inputs, 16 outputs):
+//          D = W^T x^T, lane (j, q) of the B operand holds x[t0 + j][32 kb + 8q
+//          .. +7] of the group, lane (i, q) of the A operand W[32 kb + 8q + r][o(i)],
+//          r = 0..7.
+//   float: four v_mfma_f32_16x16x4_f32 per (group, 16 inputs, 16 outputs); the
+//          r-th takes input 16 kc + 4q + r from lane (j, q)'s 16-byte piece, and
+//          the A operand the matching weight rows (full float32 products).
+// D lane (j, q) holds outputs o(4q + r) of token t0 + j.  Output blocks of 16 go
+// in pairs, and inside a pair's 32 outputs o(i) = 8 (i / 4) + 4 (block & 1) +
+// (i & 3), so that each lane ends with 8 adjacent outputs of one token (one
+// 16-byte bf16 store, two float32 stores); an unpaired last block (d_out/G = 16
+// mod 32) keeps o(i) = i.  float32 accumulation; bf16 outputs rounded to nearest
+// even once.
+#include <type_traits>
+
+#include "common.h"
+#include "kernels.h"
+#include "stream.h"
+
+namespace res {
+
+constexpr int GP_THREADS = 256;  // four waves
+constexpr int GP_MAXOB = 8;      // output blocks of 16 per group: d_out/G <= 128
+constexpr int GP_MAXP = 16;      // 16-byte pieces per lane and token tile: d_in * size <= 1024 bytes
+constexpr int GP_FRAG = 64 * 16; // bytes of one weight fragment (16 per lane)
+constexpr int GP_MAXLDS = 64 << 10;
+
+template <typename T>
+struct GPGeo {
+  static constexpr bool BF = sizeof(T) == 2;
+  static constexpr int KC = BF ? 32 : 16;  // inputs per fragment
+  static constexpr int VE = 16 / (int)sizeof(T);
+};
+
+__device__ __forceinline__ f4 gp_mma(const u32x4& a, const u32x4& b, f4 c, bf16_t) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a), __builtin_bit_cast(bf8, b), c, 0, 0,
+                                                 0);
+}
+__device__ __forceinline__ f4 gp_mma(const u32x4& a, const u32x4& b, f4 c, float) {
+  return mma_f32(__builtin_bit_cast(f4, a), __builtin_bit_cast(f4, b), c);
+}
+
+__device__ __forceinline__ uint32_t gp_pack(float a, float b) {
+  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
+  const b2 v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// NO weights sharing x; MP >= pieces per lane and tile, MOB >= output blocks per group
+template <typename T, int NO, int MP, int MOB>
+__global__ __launch_bounds__(GP_THREADS) void gproj_kernel(const T* __restrict__ x, const T* __restrict__ W0,
+                                                           const T* __restrict__ W1, T* __restrict__ y0,
+                                                           T* __restrict__ y1, int64_t N, int d_in, int d_out,
+                                                           int G) {
+  typedef GPGeo<T> GG;
+  extern __shared__ __align__(16) char wfrag[];
+  const int di = d_in / G, dq = d_out / G, KB = di / GG::KC, OB = dq / 16;
+  const int nfrag = G * KB * OB;  // fragments of one weight
+  // ---- the weights into LDS: element (g, k, o) to fragment (g, kb, block of o),
+  // lane (i, q) and slot r; each thread moves one 16-byte run of a weight row ----
+#pragma unroll
+  for (int w = 0; w < NO; ++w) {
+    const T* W = w ? W1 : W0;
+    T* dst = reinterpret_cast<T*>(wfrag + (size_t)w * nfrag * GP_FRAG);
+    const int nrun = G * di * (dq / GG::VE);
+    for (int e = threadIdx.x; e < nrun; e += GP_THREADS) {
+      const int o0 = (e % (dq / GG::VE)) * GG::VE, row = e / (dq / GG::VE);  // row = g di + k
+      const int g = row / di, k = row % di;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(W + (size_t)row * dq + o0);
+      const T* vs = reinterpret_cast<const T*>(&v);
+      const int kb = k / GG::KC, kk = k % GG::KC;
+      const int q = GG::BF ? kk >> 3 : (kk >> 2) & 3, r = GG::BF ? kk & 7 : kk & 3;
+#pragma unroll
+      for (int c = 0; c < GG::VE; ++c) {
+        const int o = o0 + c, pb = o >> 5, oo = o & 31;
+        int ob, i;
+        if ((OB & 1) && 2 * pb == OB - 1) {
+          ob = 2 * pb;
+          i = oo;
+        } else {
+          ob = 2 * pb + ((oo >> 2) & 1);
+          i = 4 * (oo >> 3) + (oo & 3);
+        }
+        const int f = (g * KB + kb) * OB + ob;
+        dst[((size_t)f * 64 + i + 16 * q) * GG::VE + r] = vs[c];
+      }
+    }
+  }
+  __syncthreads();
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, j = lane & 15, q = lane >> 4;
+  const int np = d_in / (GG::KC);  // pieces per lane and tile (one per group and fragment row)
+  const int64_t ntile = (N + 15) / 16;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < ntile; tile += (int64_t)gridDim.x * 4) {
+    const int64_t t = tile * 16 + j;
+    const bool tv = t < N;
+    const T* xr = x + (tv ? t : 0) * (int64_t)d_in + q * (GG::KC / 4);
+    u32x4 xv[MP];
+#pragma unroll
+    for (int p = 0; p < MP; ++p)
+      if (p < np) xv[p] = tv ? *reinterpret_cast<const u32x4*>(xr + p * GG::KC) : zero4;
+    f4 acc[NO][MOB];
+    int g = 0, kb = 0;
+#pragma unroll
+    for (int p = 0; p < MP; ++p) {
+      if (p < np) {
+        if (kb == 0) {
+#pragma unroll
+          for (int w = 0; w < NO; ++w)
+#pragma unroll
+            for (int ob = 0; ob < MOB; ++ob) acc[w][ob] = zero;
+        }
+#pragma unroll
+        for (int w = 0; w < NO; ++w) {
+          const char* fb = wfrag + ((size_t)w * nfrag + (size_t)p * OB) * GP_FRAG + lane * 16;
+#pragma unroll
+          for (int ob = 0; ob < MOB; ++ob)
+            if (ob < OB)
+              acc[w][ob] = gp_mma(*reinterpret_cast<const u32x4*>(fb + ob * GP_FRAG), xv[p], acc[w][ob], T());
+        }
+        if (kb == KB - 1 && tv) {
+#pragma unroll
+          for (int w = 0; w < NO; ++w) {
+            T* yr = (w ? y1 : y0) + t * (int64_t)d_out + g * dq;
+#pragma unroll
+            for (int ob = 0; ob < MOB; ob += 2) {
+              if (ob >= OB) continue;
+              const f4 a0 = acc[w][ob];
+              if (ob + 1 < OB) {  // a pair: 8 adjacent outputs from 32 (ob / 2) + 8 q
+                const f4 a1 = acc[w][ob + 1];
+                T* yp = yr + 16 * ob + 8 * q;
+                if constexpr (GG::BF) {
+                  *reinterpret_cast<u32x4*>(yp) =
+                      u32x4{gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]), gp_pack(a1[0], a1[1]), gp_pack(a1[2], a1[3])};
+                } else {
+                  *reinterpret_cast<f4*>(yp) = a0;
+                  *reinterpret_cast<f4*>(yp + 4) = a1;
+                }
+              } else {  // the unpaired last block: 4 adjacent outputs from 16 ob + 4 q
+                T* yp = yr + 16 * ob + 4 * q;
+                if constexpr (GG::BF)
+                  *reinterpret_cast<uint2*>(yp) = make_uint2(gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]));
+                else
+                  *reinterpret_cast<f4*>(yp) = a0;
+              }
+            }
+          }
+        }
+        if (++kb == KB) {
+          kb = 0;
+          ++g;
+        }
+      }
+    }
+  }
+}
+
+// Whether the MFMA kernel takes this shape: d_in/G a multiple of 32 (bf16) or 16
+// (float), d_out/G a multiple of 16 and at most 128, a row of x at most 1 KB, the
+// staged weights at most 64 KB, and x and the outputs 16-byte aligned.
+bool grouped_proj_supported(const void* x, const void* W0, const void* W1, const void* y0, const void* y1,
+                            int64_t d_in, int64_t d_out, int64_t G, bool bf16) {
+  const int nw = W1 ? 2 : 1;
+  const int64_t es = bf16 ? 2 : 4, kc = bf16 ? 32 : 16;
+  const int64_t di = d_in / G, dq = d_out / G;
+  if (di % kc || dq % 16 || dq > 16 * GP_MAXOB || d_in * es > 16 * 4 * GP_MAXP) return false;
+  if ((int64_t)nw * G * (di / kc) * (dq / 16) * GP_FRAG > GP_MAXLDS) return false;
+  auto al = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
+  return al(x) && al(W0) && al(W1) && al(y0) && al(y1);
+}
+
+hipError_t launch_grouped_proj(const void* x, const void* W0, const void* W1, void* y0, void* y1, int64_t N,
+                               int64_t d_in, int64_t d_out, int64_t G, bool bf16, int num_cus, hipStream_t st) {
+  const int nw = W1 ? 2 : 1;
+  const int64_t kc = bf16 ? 32 : 16;
+  const size_t lds = (size_t)nw * G * (d_in / G / kc) * (d_out / G / 16) * GP_FRAG;
+  const int64_t ntile = (N + 15) / 16, want = (ntile + 3) / 4, cap = 2 * (int64_t)(num_cus > 0 ? num_cus : 256);
+  const dim3 grid((unsigned)(want < cap ? want : cap)), block(GP_THREADS);
+  const int di = (int)d_in, dq = (int)d_out, g = (int)G;
+  const int np = (int)(d_in / kc), nob = (int)(d_out / G / 16);
+  auto go = [&](auto tag, auto no_, auto mp_, auto mob_) {
+    typedef decltype(tag) T;
+    constexpr int NO = decltype(no_)::value, MP = decltype(mp_)::value, MOB = decltype(mob_)::value;
+    const T* w0 = (const T*)W0;
+    hipLaunchKernelGGL((gproj_kernel<T, NO, MP, MOB>), grid, block, lds, st, (const T*)x, w0, NO == 2 ? (const T*)W1 : w0,
+                       (T*)y0, NO == 2 ? (T*)y1 : (T*)y0, N, di, dq, g);
+  };
+  typedef std::integral_constant<int, 1> I1;
+  typedef std::integral_constant<int, 2> I2;
+  typedef std::integral_constant<int, 8> I8;
+  typedef std::integral_constant<int, 16> I16;
+  auto by_shape = [&](auto tag, auto no_) {
+    if (np <= 8) {
+      if (nob <= 2) go(tag, no_, I8(), I2()); else go(tag, no_, I8(), I8());
+    } else {
+      if (nob <= 2) go(tag, no_, I16(), I2()); else go(tag, no_, I16(), I8());
+    }
+  };
+  if (bf16) {
+    if (nw == 2) by_shape(bf16_t(), I2()); else by_shape(bf16_t(), I1());
+  } else {
+    if (nw == 2) by_shape(float(), I2()); else by_shape(float(), I1());
+  }
+  return hipGetLastError();
+}
+
+}  // namespace res

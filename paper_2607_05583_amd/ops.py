@@ -348,6 +348,29 @@ def resonator_grouped_linear(x, W, out=None):
     return y
 
 
+def resonator_grouped_linear2(x, W0, W1, out0=None, out1=None):
+    """y0 = x W0 and y1 = x W1 for block-diagonal weights of one shape (the drive
+    and the gate of Sec. 3.1), from one read of x.  Returns (y0, y1)."""
+    _dev(x, "x")
+    _dev(W0, "W0")
+    _dev(W1, "W1")
+    if W0.dim() != 3 or W0.dtype != x.dtype or W1.shape != W0.shape or W1.dtype != x.dtype:
+        raise ValueError("W0 and W1 must both be [G, d_in/G, d_out/G] of x's dtype")
+    G, di, dq = W0.shape
+    d_in = x.shape[-1]
+    if d_in != G * di:
+        raise ValueError(f"x has {d_in} features, W expects {G * di}")
+    N = x.numel() // d_in
+    shape = x.shape[:-1] + (G * dq,)
+    y0 = out0 if out0 is not None else torch.empty(shape, dtype=x.dtype, device=x.device)
+    y1 = out1 if out1 is not None else torch.empty(shape, dtype=x.dtype, device=x.device)
+    _dev(y0, "out0")
+    _dev(y1, "out1")
+    check(_lib.lib().resonator_grouped_linear2(_ptr(x), _ptr(W0), _ptr(W1), _code(x), _ptr(y0), _ptr(y1), N, d_in,
+                                               G * dq, G, _stream(x.device)))
+    return y0, y1
+
+
 def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
     """Gradients of sum(dy * grouped_linear(x, W)): (dx of x's dtype, dW float32).
 
@@ -450,11 +473,18 @@ def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     projections of x, y = mixing of u, z = sigmoid(g) (C y) + s conv(u), and the
     grouped output projection of z.  x [B, L, d]; returns [B, L, d_out].
 
-    ``dense`` = (Wu, Wg, Wo) as resonator_block_diag_weight copies: the
-    projections then run as dense GEMMs (the same result)."""
-    Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
-    u = resonator_grouped_linear(x, Pu)
-    g = resonator_grouped_linear(x, Pg)
+    Without ``dense`` the drive and the gate come from one grouped projection
+    call (one read of x) and the projections run grouped (the library's MFMA
+    kernel where the shape allows).  ``dense`` = (Wu, Wg, Wo) as
+    resonator_block_diag_weight copies: the projections then run as dense GEMMs
+    (the same result up to the order of float32 sums)."""
+    if dense is None:
+        Po = Wo
+        u, g = resonator_grouped_linear2(x, Wu, Wg)
+    else:
+        Pu, Pg, Po = dense
+        u = resonator_grouped_linear(x, Pu)
+        g = resonator_grouped_linear(x, Pg)
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
     return resonator_grouped_linear(z, Po)
@@ -503,8 +533,9 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     are recomputed, then the chain rule runs backwards through the output
     projection, the epilogue, the mixing and the two input projections.  Returns
     a dict: dx, dWu, dWg, dWo (float32), dgamma, domega, damp, dphase, dCt,
-    dlambda_c, dw, ds.  ``dense`` as for resonator_block_fwd (data gradients
-    then run as dense GEMMs; weight gradients always per group)."""
+    dlambda_c, dw, ds.  The intermediates come from the grouped projections;
+    ``dense`` (as for resonator_block_fwd) runs the data gradients as dense
+    GEMMs and the weight gradients with the contraction split."""
     _dev(x, "x")
     _dev(do, "do")
     if do.dtype != x.dtype:
@@ -513,8 +544,9 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     if tuple(do.shape) != tuple(x.shape[:-1]) + (d_out,):
         raise ValueError(f"do must be {tuple(x.shape[:-1]) + (d_out,)}, got {tuple(do.shape)}")
     Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
-    u = resonator_grouped_linear(x, Pu)
-    g = resonator_grouped_linear(x, Pg)
+    # the forward's intermediates from the grouped projections (one read of x
+    # for the drive and the gate)
+    u, g = resonator_grouped_linear2(x, Wu, Wg)
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
 

@@ -131,6 +131,16 @@ def test_decode_steps_and_projection_validation_codes():
     assert gl(FAKE, FAKE2, 7, F3, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG
     assert gl(FAKE, FAKE2, L.RES_F32, FAKE, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
     assert gl(ODD, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, None) == L.RES_ERR_MISALIGNED
+    gl2 = lib.resonator_grouped_linear2
+    F4_ = ctypes.c_void_p(0x7F0300000000)
+    assert gl2(FAKE, FAKE2, FAKE2, L.RES_F32, F3, F4_, 5, 8, 8, 3, None) == L.RES_ERR_INVALID_ARG and \
+        "multiples" in _err()
+    assert gl2(FAKE, None, FAKE2, L.RES_F32, F3, F4_, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG
+    assert gl2(FAKE, FAKE2, FAKE2, L.RES_F32, F3, F3, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG and \
+        "overlap" in _err()
+    assert gl2(FAKE, FAKE2, FAKE2, L.RES_F32, FAKE, F4_, 5, 8, 8, 2, None) == L.RES_ERR_INVALID_ARG and \
+        "overlap" in _err()
+    assert gl2(ODD, FAKE2, FAKE2, L.RES_F32, F3, F4_, 5, 8, 8, 2, None) == L.RES_ERR_MISALIGNED
     assert lib.resonator_grouped_linear_bwd_data(None, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
         L.RES_ERR_INVALID_ARG
     assert lib.resonator_grouped_linear_bwd_weight(FAKE, FAKE2, L.RES_BF16, FAKE, 5, 8, 8, 2, 0, None) == \

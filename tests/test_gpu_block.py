@@ -43,6 +43,72 @@ def test_grouped_linear_parity(N, G, di, dq, act):
     assert err <= (1e-5 if act == "f32" else 1e-2)
 
 
+# Shapes the MFMA projection kernel takes (d_in/G a multiple of 32 for bf16 and
+# 16 for float32, d_out/G a multiple of 16 up to 128, a row of at most 1 KB):
+# paired and unpaired output blocks, several fragments per group, ragged and
+# short token tails, the longest row.
+MFMA_SHAPES = [
+    (777, 8, 32, 32, "bf16"),   # the block's shape: one fragment, one pair of output blocks; ragged tail
+    (5, 8, 32, 32, "bf16"),     # fewer tokens than one tile
+    (1000, 4, 64, 48, "bf16"),  # two fragments per group; a pair and an unpaired block
+    (333, 2, 32, 16, "bf16"),   # one unpaired block
+    (513, 2, 256, 64, "bf16"),  # a 1 KB row (16 pieces per lane), 64 KB of staged weight
+    (1000, 4, 64, 64, "f32"),
+    (300, 16, 16, 16, "f32"),   # a 1 KB row of float32; unpaired blocks
+    (257, 2, 48, 80, "f32"),    # three fragments; two pairs and an unpaired block
+]
+
+
+def _off_by_one(t, shape):
+    """A buffer of the given shape one element into a larger allocation (aligned
+    to its element, not to 16 bytes, so the projection takes the library GEMM),
+    holding a copy of t when t has that shape."""
+    buf = torch.empty(int(np.prod(shape)) + 1, dtype=t.dtype, device=t.device)
+    v = buf[1:].view(shape)
+    if tuple(t.shape) == tuple(shape):
+        v.copy_(t)
+    return v
+
+
+@pytest.mark.parametrize("N,G,di,dq,act", MFMA_SHAPES)
+def test_grouped_linear_mfma_parity(N, G, di, dq, act):
+    say(f"grouped linear (MFMA kernel and library GEMM) N={N} G={G} di={di} dq={dq} {act}")
+    r = np.random.default_rng(7 * N + G)
+    x = W._act(r, (N, G * di), act)
+    Wt = W._act(r, (G, di, dq), act)
+    xd, wd = dev_act(x, act), dev_act(Wt, act)
+    y = ops.resonator_grouped_linear(xd, wd)
+    xo = _off_by_one(xd, tuple(xd.shape))
+    yo = _off_by_one(xd, (N, G * dq))
+    ops.resonator_grouped_linear(xo, wd, out=yo)
+    torch.cuda.synchronize()
+    ref = O.grouped_linear(act64(x, act), act64(Wt, act))
+    tol = 1e-5 if act == "f32" else 1e-2
+    e_mfma, e_lib = rel_err(host(y), ref), rel_err(host(yo), ref)
+    say(f"  err MFMA {e_mfma:.2e}, library {e_lib:.2e}")
+    assert e_mfma <= tol and e_lib <= tol
+
+
+@pytest.mark.parametrize("N,G,di,dq,act", [(777, 8, 32, 32, "bf16"), (300, 4, 16, 32, "f32"),
+                                           (1000, 4, 64, 48, "bf16"), (130, 3, 7, 11, "f32")])
+def test_grouped_linear2_matches_two_projections(N, G, di, dq, act):
+    say(f"grouped linear, two weights N={N} G={G} di={di} dq={dq} {act}")
+    r = np.random.default_rng(11 * N + G)
+    x = W._act(r, (N, G * di), act)
+    W0 = W._act(r, (G, di, dq), act)
+    W1 = W._act(r, (G, di, dq), act)
+    xd, w0, w1 = dev_act(x, act), dev_act(W0, act), dev_act(W1, act)
+    y0, y1 = ops.resonator_grouped_linear2(xd, w0, w1)
+    s0 = ops.resonator_grouped_linear(xd, w0)
+    s1 = ops.resonator_grouped_linear(xd, w1)
+    torch.cuda.synchronize()
+    # the same arithmetic per output as one projection at a time
+    assert torch.equal(y0, s0) and torch.equal(y1, s1)
+    tol = 1e-5 if act == "f32" else 1e-2
+    for yy, Wk in ((y0, W0), (y1, W1)):
+        assert rel_err(host(yy), O.grouped_linear(act64(x, act), act64(Wk, act))) <= tol
+
+
 @pytest.mark.parametrize("B,L,d,H,K,G,M,act", [(2, 300, 64, 4, 3, 4, 4, "f32"), (1, 1000, 256, 8, 4, 8, 8, "bf16"),
                                                (2, 257, 32, 2, 0, 1, 3, "bf16")])
 def test_block_fwd_parity(B, L, d, H, K, G, M, act):
