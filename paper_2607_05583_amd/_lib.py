@@ -20,7 +20,7 @@ RES_M_MAX = 16
 SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd",
            "resonator_mix_bwd", "resonator_state_init", "resonator_decode_step",
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
-           "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
+           "resonator_epilogue_proj_fwd", "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
            "resonator_decode_constants", "resonator_decode_step_tab",
            "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
@@ -61,6 +61,9 @@ def _declare(lib):
     f32 = ctypes.c_float
     lib.resonator_epilogue_fwd.restype = i32
     lib.resonator_epilogue_fwd.argtypes = [vp, vp, vp, i32, vp, i64, i64, i64, i64, i64, fp, f32, fp, fp, vp]
+    lib.resonator_epilogue_proj_fwd.restype = i32
+    lib.resonator_epilogue_proj_fwd.argtypes = [vp, vp, vp, i32, vp, vp, i64, i64, i64, i64, i64, i64, fp, f32, fp,
+                                                fp, vp]
     lib.resonator_epilogue_workspace_bytes.restype = sz
     lib.resonator_epilogue_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]
     lib.resonator_epilogue_bwd.restype = i32

@@ -983,6 +983,41 @@ int resonator_epilogue_fwd(const void* y, const void* gate, const void* v, res_d
   return e == hipSuccess ? RES_OK : hip_fail(e, "epilogue launch");
 }
 
+int resonator_epilogue_proj_fwd(const void* y, const void* gate, const void* v, res_dtype_t act_dt, const void* Wo,
+                                void* out, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K, int64_t d_out,
+                                const float* Ct, float lambda_c, const float* w, const float* s, void* stream) {
+  int rc = epi_check(B, L, H, dh, K);
+  if (rc) return rc;
+  if (!dtype_ok(act_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
+  if (d_out < 1 || d_out % H)
+    return fail(RES_ERR_INVALID_ARG, "d_out (%lld) must be a positive multiple of H (%lld)", (long long)d_out,
+                (long long)H);
+  if (!y || !gate || !Wo || !out || !Ct) return fail(RES_ERR_INVALID_ARG, "y, gate, Wo, out and Ct must be non-null");
+  if (K > 0 && (!v || !w || !s)) return fail(RES_ERR_INVALID_ARG, "v, w and s must be non-null when K > 0");
+  const bool bf = act_dt == RES_BF16;
+  if (epi_proj_lds((int)H, (int)dh, (int)K, d_out, bf) == 0)
+    return fail(RES_ERR_UNSUPPORTED,
+                "the fused epilogue takes H <= 8, dh = %d, K <= 4 and d_out/H of 16 or 32 (got H %lld, dh %lld, "
+                "K %lld, d_out %lld)",
+                bf ? 32 : 16, (long long)H, (long long)dh, (long long)K, (long long)d_out);
+  const size_t es = elt_size(act_dt), n = (size_t)(B * L * H * dh) * es, no = (size_t)(B * L * d_out) * es;
+  auto a16 = [](const void* p) { return p == nullptr || ((uintptr_t)p & 15) == 0; };
+  if (!a16(y) || !a16(gate) || !a16(Wo) || !a16(out) || (K > 0 && !a16(v)) || !aligned(Ct, 4) ||
+      (w && !aligned(w, 4)) || (s && !aligned(s, 4)))
+    return fail(RES_ERR_MISALIGNED, "activations, Wo and out aligned to 16 bytes, parameters to 4 bytes");
+  const size_t nw = (size_t)(dh * d_out) * es;
+  if (overlap(out, no, y, n) || overlap(out, no, gate, n) || (K > 0 && overlap(out, no, v, n)) ||
+      overlap(out, no, Wo, nw))
+    return fail(RES_ERR_INVALID_ARG, "out must not overlap y, gate, v or Wo");
+  hipStream_t st = (hipStream_t)stream;
+  const hipError_t e =
+      bf ? launch_epi_proj_fwd<bf16_t>(y, gate, v, Wo, out, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
+                                       device_cus(), st)
+         : launch_epi_proj_fwd<float>(y, gate, v, Wo, out, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
+                                      device_cus(), st);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "fused epilogue launch");
+}
+
 int resonator_epilogue_bwd(const void* y, const void* gate, const void* v, const void* dz, res_dtype_t act_dt,
                            void* dy, void* dgate, void* dv, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K,
                            const float* Ct, float lambda_c, const float* w, const float* s, float* dCt,

@@ -21,8 +21,11 @@
 //   dC[g,h] = sum dyb[g dh + j] y[h dh + j],  ds = sum dz l,  dw[k] = sum dl[t] v[t-k],
 // reduced per block of rows (float32, fixed order), then over blocks (float64,
 // fixed order), so they are bitwise reproducible.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
+#include "proj.h"
 
 namespace res {
 
@@ -852,6 +855,165 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
   hipLaunchKernelGGL(epi_bwd_lambda_kernel, dim3(1), dim3(64), 0, st, lam_terms, H, dlambda_c);
   return hipGetLastError();
 }
+
+// ---------------------------------------------------------------------------
+// Epilogue fused with the grouped output projection (Sec. 3.4), one group per
+// head and a head as wide as one MFMA contraction (32 bf16 or 16 float32
+// channels):
+//   out[t, g dq + o] = sum_j z[t, g dh + j] Wo[g][j][o],   z as above.
+// The projection kernel's lane (token j, piece q) holds channels q VE .. q VE +
+// VE-1 of a head as its activation operand; here that lane loads y, the gate and
+// v at those channels of every head of its token (each element once), forms z
+// of every head in registers with the arithmetic and order of the HM = 8 path of
+// epi_fwd_col_kernel, rounds it as that kernel stores it, and feeds each head's
+// z straight into the head's projection (gp_mma, gp_store): z never goes to
+// memory, and the result is bitwise that of the epilogue followed by the
+// projection.  The local path's rows t-1 and t-2 are those of lanes j-1 and j-2
+// of the same 16-lane row (DPP row shifts); each lane also loads row t-3, which
+// is tap 3 and, shifted left, gives the first lanes of the tile their rows
+// before it.  A tap that is not in the batch row multiplies a zero weight by the
+// lane's own row, as in the unfused kernel.
+template <typename T, int MOB, bool HASK>
+__global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, const T* __restrict__ gate,
+                                                       const T* __restrict__ v, const T* __restrict__ Wo,
+                                                       T* __restrict__ out, int64_t rows, int64_t L, int H, int K,
+                                                       int dq, const float* __restrict__ Ct, float lambda_c,
+                                                       const float* __restrict__ w, const float* __restrict__ s) {
+  typedef GPGeo<T> GG;
+  constexpr int VE = GG::VE, dh = GG::KC;
+  typedef Pc<T, VE> PC;
+  typedef typename PC::raw P;
+  extern __shared__ __align__(16) char lds[];
+  const int D = H * dh, OB = dq / 16, d_out = H * dq;
+  char* wfrag = lds;                                                           // H * OB fragments
+  float* sC = reinterpret_cast<float*>(lds + (size_t)H * OB * GP_FRAG);        // C [H][H]
+  float* sW = sC + 64;                                                         // w as [K][D], then s [D]
+  gp_stage<T>(wfrag, Wo, H, dh, dq, threadIdx.x, 256);
+  coupling_to_lds(sC, Ct, lambda_c, H);
+  if (HASK) {
+    for (int x = threadIdx.x; x < D * K; x += 256) sW[(x % K) * D + x / K] = w[x];
+    for (int x = threadIdx.x; x < D; x += 256) sW[D * K + x] = s[x];
+  }
+  __syncthreads();
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, jj = lane & 15, q = lane >> 4, j0 = q * VE;
+  const int64_t ntile = (rows + 15) / 16;
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < ntile; tile += (int64_t)gridDim.x * 4) {
+    const int64_t t = tile * 16 + jj;
+    const bool tv = t < rows;
+    const int64_t tc = tv ? t : rows - 1;                                   // the row loaded (any row if past the end)
+    const int64_t th = t - 3 < 0 ? 0 : (t - 3 < rows ? t - 3 : rows - 1);  // row t-3 (lanes past the end included)
+    const int tl = (int)(tc % L);                                           // position in the batch row
+    P yr[8], gr[8], vm[8], vh[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      const int hh = h < H ? h : 0;
+      const int64_t c = (int64_t)hh * dh + j0;
+      yr[h] = *reinterpret_cast<const P*>(y + tc * D + c);
+      gr[h] = *reinterpret_cast<const P*>(gate + tc * D + c);
+      if (HASK) {
+        vm[h] = *reinterpret_cast<const P*>(v + tc * D + c);
+        vh[h] = *reinterpret_cast<const P*>(v + th * D + c);
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < 8; ++g) {
+      if (g >= H) continue;
+      float acc[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) acc[e] = 0.f;
+#pragma unroll
+      for (int h = 0; h < 8; ++h) {
+        float yh[VE];
+        PC::unpack(yr[h], yh);
+        const float cgh = h < H ? sC[g * H + h] : 0.f;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) acc[e] = fmaf(cgh, yh[e], acc[e]);
+      }
+      float u[VE], o[VE];
+      PC::unpack(gr[g], u);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) o[e] = sigmoid_fast(u[e]) * acc[e];
+      if (HASK) {
+        const int c0 = g * dh + j0;
+        float l[VE];
+#pragma unroll
+        for (int e = 0; e < VE; ++e) l[e] = 0.f;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const bool tap = k < K && k <= tl;
+          P vk;
+#pragma unroll
+          for (int i = 0; i < (int)(sizeof(P) / 4); ++i) {
+            uint32_t val;
+            if (k == 0) {
+              val = vm[g][i];
+            } else if (k == 3) {
+              val = vh[g][i];
+            } else if (k == 1) {
+              // lanes j >= k: lane j-k's own row; lanes j < k: lane j+3-k's row t-3
+              // (row_shl:2 of the t-3 rows, then row_shr:1 of the own rows over it)
+              const int hal = __builtin_amdgcn_update_dpp(0, (int)vh[g][i], 0x102, 0xF, 0xF, false);
+              val = (uint32_t)__builtin_amdgcn_update_dpp(hal, (int)vm[g][i], 0x111, 0xF, 0xF, false);
+            } else {
+              const int hal = __builtin_amdgcn_update_dpp(0, (int)vh[g][i], 0x101, 0xF, 0xF, false);
+              val = (uint32_t)__builtin_amdgcn_update_dpp(hal, (int)vm[g][i], 0x112, 0xF, 0xF, false);
+            }
+            vk[i] = tap ? val : vm[g][i];
+          }
+          float vv[VE];
+          PC::unpack(vk, vv);
+#pragma unroll
+          for (int e = 0; e < VE; ++e) l[e] = fmaf(tap ? sW[k * D + c0 + e] : 0.f, vv[e], l[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < VE; ++e) o[e] = fmaf(sW[D * K + c0 + e], l[e], o[e]);
+      }
+      const P zp = PC::pack(o);
+      const u32x4 zb = __builtin_bit_cast(u32x4, zp);
+      f4 a[MOB];
+      const char* fb = wfrag + (size_t)g * OB * GP_FRAG + lane * 16;
+#pragma unroll
+      for (int ob = 0; ob < MOB; ++ob)
+        if (ob < OB) a[ob] = gp_mma(*reinterpret_cast<const u32x4*>(fb + ob * GP_FRAG), zb, zero, T());
+      if (tv) gp_store<T, MOB>(out + t * d_out + g * dq, a, OB, q);
+    }
+  }
+}
+
+// bytes of LDS of the fused kernel, 0 when the shape is not one it takes
+size_t epi_proj_lds(int H, int dh, int K, int64_t d_out, bool bf16) {
+  const int kc = bf16 ? 32 : 16;
+  if (H < 1 || H > 8 || dh != kc || K < 0 || K > 4 || d_out % H) return 0;
+  const int64_t dq = d_out / H;
+  if (dq != 16 && dq != 32) return 0;  // one or two output blocks per head (registers)
+  const size_t lds = (size_t)H * (dq / 16) * GP_FRAG + 64 * 4 + (size_t)H * dh * (K + 1) * 4;
+  return lds <= (size_t)GP_MAXLDS ? lds : 0;
+}
+
+template <typename T>
+hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, const void* Wo, void* out, int64_t B,
+                               int64_t L, int H, int K, int64_t d_out, const float* Ct, float lambda_c,
+                               const float* w, const float* s, int num_cus, hipStream_t st) {
+  const size_t lds = epi_proj_lds(H, GPGeo<T>::KC, K, d_out, GPGeo<T>::BF);
+  const int64_t rows = B * L, ntile = (rows + 15) / 16, want = (ntile + 3) / 4;
+  const int64_t cap = 2 * (int64_t)(num_cus > 0 ? num_cus : 256);
+  const dim3 grid((unsigned)(want < cap ? want : cap)), block(256);
+  const int dq = (int)(d_out / H);
+  if (K > 0)
+    hipLaunchKernelGGL((epi_proj_kernel<T, 2, true>), grid, block, lds, st, (const T*)y, (const T*)gate, (const T*)v,
+                       (const T*)Wo, (T*)out, rows, L, H, K, dq, Ct, lambda_c, w, s);
+  else
+    hipLaunchKernelGGL((epi_proj_kernel<T, 2, false>), grid, block, lds, st, (const T*)y, (const T*)gate,
+                       (const T*)v, (const T*)Wo, (T*)out, rows, L, H, K, dq, Ct, lambda_c, w, s);
+  return hipGetLastError();
+}
+template hipError_t launch_epi_proj_fwd<float>(const void*, const void*, const void*, const void*, void*, int64_t,
+                                               int64_t, int, int, int64_t, const float*, float, const float*,
+                                               const float*, int, hipStream_t);
+template hipError_t launch_epi_proj_fwd<bf16_t>(const void*, const void*, const void*, const void*, void*, int64_t,
+                                                int64_t, int, int, int64_t, const float*, float, const float*,
+                                                const float*, int, hipStream_t);
 
 template hipError_t launch_epi_fwd<float>(const void*, const void*, const void*, void*, int64_t, int64_t, int, int,
                                           int, const float*, float, const float*, const float*, int, hipStream_t);

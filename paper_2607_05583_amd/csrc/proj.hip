@@ -26,36 +26,9 @@
 
 #include "common.h"
 #include "kernels.h"
-#include "stream.h"
+#include "proj.h"
 
 namespace res {
-
-constexpr int GP_THREADS = 256;  // four waves
-constexpr int GP_MAXOB = 8;      // output blocks of 16 per group: d_out/G <= 128
-constexpr int GP_MAXP = 16;      // 16-byte pieces per lane and token tile: d_in * size <= 1024 bytes
-constexpr int GP_FRAG = 64 * 16; // bytes of one weight fragment (16 per lane)
-constexpr int GP_MAXLDS = 64 << 10;
-
-template <typename T>
-struct GPGeo {
-  static constexpr bool BF = sizeof(T) == 2;
-  static constexpr int KC = BF ? 32 : 16;  // inputs per fragment
-  static constexpr int VE = 16 / (int)sizeof(T);
-};
-
-__device__ __forceinline__ f4 gp_mma(const u32x4& a, const u32x4& b, f4 c, bf16_t) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, a), __builtin_bit_cast(bf8, b), c, 0, 0,
-                                                 0);
-}
-__device__ __forceinline__ f4 gp_mma(const u32x4& a, const u32x4& b, f4 c, float) {
-  return mma_f32(__builtin_bit_cast(f4, a), __builtin_bit_cast(f4, b), c);
-}
-
-__device__ __forceinline__ uint32_t gp_pack(float a, float b) {
-  typedef __bf16 b2 __attribute__((ext_vector_type(2)));
-  const b2 v = {(__bf16)a, (__bf16)b};
-  return __builtin_bit_cast(uint32_t, v);
-}
 
 // NO weights sharing x; MP >= pieces per lane and tile, MOB >= output blocks per group
 template <typename T, int NO, int MP, int MOB>
@@ -67,36 +40,10 @@ __global__ __launch_bounds__(GP_THREADS) void gproj_kernel(const T* __restrict__
   extern __shared__ __align__(16) char wfrag[];
   const int di = d_in / G, dq = d_out / G, KB = di / GG::KC, OB = dq / 16;
   const int nfrag = G * KB * OB;  // fragments of one weight
-  // ---- the weights into LDS: element (g, k, o) to fragment (g, kb, block of o),
-  // lane (i, q) and slot r; each thread moves one 16-byte run of a weight row ----
+  // ---- the weights into LDS, in the operand layout ----
 #pragma unroll
-  for (int w = 0; w < NO; ++w) {
-    const T* W = w ? W1 : W0;
-    T* dst = reinterpret_cast<T*>(wfrag + (size_t)w * nfrag * GP_FRAG);
-    const int nrun = G * di * (dq / GG::VE);
-    for (int e = threadIdx.x; e < nrun; e += GP_THREADS) {
-      const int o0 = (e % (dq / GG::VE)) * GG::VE, row = e / (dq / GG::VE);  // row = g di + k
-      const int g = row / di, k = row % di;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(W + (size_t)row * dq + o0);
-      const T* vs = reinterpret_cast<const T*>(&v);
-      const int kb = k / GG::KC, kk = k % GG::KC;
-      const int q = GG::BF ? kk >> 3 : (kk >> 2) & 3, r = GG::BF ? kk & 7 : kk & 3;
-#pragma unroll
-      for (int c = 0; c < GG::VE; ++c) {
-        const int o = o0 + c, pb = o >> 5, oo = o & 31;
-        int ob, i;
-        if ((OB & 1) && 2 * pb == OB - 1) {
-          ob = 2 * pb;
-          i = oo;
-        } else {
-          ob = 2 * pb + ((oo >> 2) & 1);
-          i = 4 * (oo >> 3) + (oo & 3);
-        }
-        const int f = (g * KB + kb) * OB + ob;
-        dst[((size_t)f * 64 + i + 16 * q) * GG::VE + r] = vs[c];
-      }
-    }
-  }
+  for (int w = 0; w < NO; ++w)
+    gp_stage<T>(wfrag + (size_t)w * nfrag * GP_FRAG, w ? W1 : W0, G, di, dq, threadIdx.x, GP_THREADS);
   __syncthreads();
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, j = lane & 15, q = lane >> 4;
@@ -133,31 +80,7 @@ __global__ __launch_bounds__(GP_THREADS) void gproj_kernel(const T* __restrict__
         }
         if (kb == KB - 1 && tv) {
 #pragma unroll
-          for (int w = 0; w < NO; ++w) {
-            T* yr = (w ? y1 : y0) + t * (int64_t)d_out + g * dq;
-#pragma unroll
-            for (int ob = 0; ob < MOB; ob += 2) {
-              if (ob >= OB) continue;
-              const f4 a0 = acc[w][ob];
-              if (ob + 1 < OB) {  // a pair: 8 adjacent outputs from 32 (ob / 2) + 8 q
-                const f4 a1 = acc[w][ob + 1];
-                T* yp = yr + 16 * ob + 8 * q;
-                if constexpr (GG::BF) {
-                  *reinterpret_cast<u32x4*>(yp) =
-                      u32x4{gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]), gp_pack(a1[0], a1[1]), gp_pack(a1[2], a1[3])};
-                } else {
-                  *reinterpret_cast<f4*>(yp) = a0;
-                  *reinterpret_cast<f4*>(yp + 4) = a1;
-                }
-              } else {  // the unpaired last block: 4 adjacent outputs from 16 ob + 4 q
-                T* yp = yr + 16 * ob + 4 * q;
-                if constexpr (GG::BF)
-                  *reinterpret_cast<uint2*>(yp) = make_uint2(gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]));
-                else
-                  *reinterpret_cast<f4*>(yp) = a0;
-              }
-            }
-          }
+          for (int w = 0; w < NO; ++w) gp_store<T, MOB>((w ? y1 : y0) + t * (int64_t)d_out + g * dq, acc[w], OB, q);
         }
         if (++kb == KB) {
           kb = 0;

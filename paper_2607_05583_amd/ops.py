@@ -474,17 +474,22 @@ def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     grouped output projection of z.  x [B, L, d]; returns [B, L, d_out].
 
     Without ``dense`` the drive and the gate come from one grouped projection
-    call (one read of x) and the projections run grouped (the library's MFMA
-    kernel where the shape allows).  ``dense`` = (Wu, Wg, Wo) as
-    resonator_block_diag_weight copies: the projections then run as dense GEMMs
-    (the same result up to the order of float32 sums)."""
+    call (one read of x), the projections run grouped (the library's MFMA
+    kernel where the shape allows), and with one output group per head the
+    epilogue runs fused into the output projection (z is never written).
+    ``dense`` = (Wu, Wg, Wo) as resonator_block_diag_weight copies: the
+    projections then run as dense GEMMs and the epilogue on its own (the same
+    result up to the order of float32 sums)."""
     if dense is None:
-        Po = Wo
         u, g = resonator_grouped_linear2(x, Wu, Wg)
-    else:
-        Pu, Pg, Po = dense
-        u = resonator_grouped_linear(x, Pu)
-        g = resonator_grouped_linear(x, Pg)
+        y = resonator_mix_fwd(u, gamma, omega, amp, phase)
+        K = 0 if w is None else int(w.shape[1])
+        if epilogue_proj_supported(y, H, K, Wo):
+            return resonator_epilogue_proj_fwd(y, g, u, Ct, lambda_c, w, s, H, Wo)
+        return resonator_grouped_linear(resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H), Wo)
+    Pu, Pg, Po = dense
+    u = resonator_grouped_linear(x, Pu)
+    g = resonator_grouped_linear(x, Pg)
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
     return resonator_grouped_linear(z, Po)
@@ -691,6 +696,45 @@ def resonator_epilogue_fwd(y, gate, v, Ct, lambda_c, w, s, H, out=None):
         _ptr(y), _ptr(gate), _ptr(v) if K else None, _code(y), _ptr(z), B, L, H, D // H, K, _ptr(Ct),
         float(lambda_c), _ptr(w) if K else None, _ptr(s) if K else None, _stream(y.device)))
     return z
+
+
+def epilogue_proj_supported(y, H, K, Wo) -> bool:
+    """Whether resonator_epilogue_proj_fwd takes this shape (one output group
+    per head, a head of 32 bf16 or 16 float32 channels, H <= 8, K <= 4, d_out/H
+    = 16 or 32; the tensors must also be 16-byte aligned)."""
+    D = y.shape[-1]
+    if Wo.dim() != 3 or Wo.shape[0] != H or D % H:
+        return False
+    dh, dq = D // H, Wo.shape[2]
+    return (H <= 8 and K <= 4 and dh == (32 if y.dtype == torch.bfloat16 else 16) and Wo.shape[1] == dh
+            and dq in (16, 32))
+
+
+def resonator_epilogue_proj_fwd(y, gate, v, Ct, lambda_c, w, s, H, Wo, out=None):
+    """The epilogue fused with the grouped output projection (one group per head):
+    GL(resonator_epilogue_fwd(y, gate, v, ...), Wo) without writing z.  Wo is
+    [H, dh, d_out/H] of y's dtype; returns [B, L, d_out].  Bitwise the two
+    separate calls; shapes it does not take raise (epilogue_proj_supported)."""
+    _dev(y, "y"); _dev(gate, "gate"); _dev(Wo, "Wo")
+    B, L, D = y.shape
+    if gate.shape != y.shape or gate.dtype != y.dtype or Wo.dtype != y.dtype:
+        raise ValueError("gate and Wo must have y's dtype, gate y's shape")
+    if D % H:
+        raise ValueError(f"D={D} is not a multiple of H={H}")
+    K = 0 if w is None else int(w.shape[1])
+    if K > 0:
+        _dev(v, "v")
+        if v.shape != y.shape or v.dtype != y.dtype:
+            raise ValueError("v must match y in shape and dtype")
+    _epi_params(Ct, w, s, H, D, K)
+    if Wo.dim() != 3 or Wo.shape[0] != H or Wo.shape[1] != D // H:
+        raise ValueError(f"Wo must be [H, dh, d_out/H] = [{H}, {D // H}, *]")
+    d_out = H * Wo.shape[2]
+    o = torch.empty((B, L, d_out), dtype=y.dtype, device=y.device) if out is None else _dev(out, "out")
+    check(_lib.lib().resonator_epilogue_proj_fwd(
+        _ptr(y), _ptr(gate), _ptr(v) if K else None, _code(y), _ptr(Wo), _ptr(o), B, L, H, D // H, K, d_out,
+        _ptr(Ct), float(lambda_c), _ptr(w) if K else None, _ptr(s) if K else None, _stream(y.device)))
+    return o
 
 
 def resonator_epilogue_bwd(y, gate, v, dz, Ct, lambda_c, w, s, H, ws=None):

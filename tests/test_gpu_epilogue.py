@@ -116,6 +116,47 @@ def test_epilogue_bwd_is_deterministic():
         assert torch.equal(x, y)
 
 
+# (B, L, H, dh, K, dq, act): the epilogue fused with the output projection (one
+# group per head): the block's shape with two batch rows and a ragged last tile;
+# short rows, so that batch rows start inside a 16-row tile; rows of one and
+# two steps (no earlier tap inside the row); no local path; float32 heads of 16.
+FUSED = [
+    (2, 300, 8, 32, 4, 32, "bf16"),
+    (3, 17, 4, 32, 3, 16, "bf16"),
+    (5, 1, 8, 32, 4, 32, "bf16"),
+    (4, 2, 8, 32, 2, 32, "bf16"),
+    (2, 45, 8, 32, 0, 32, "bf16"),
+    (2, 100, 4, 16, 2, 32, "f32"),
+    (1, 33, 2, 16, 4, 16, "f32"),
+]
+
+
+@pytest.mark.parametrize("case", FUSED, ids=lambda c: "B{}_L{}_H{}_dh{}_K{}_dq{}_{}".format(*c))
+def test_epilogue_proj_fused_matches_two_calls_and_oracle(case):
+    B, L, H, dh, K, dq, act = case
+    say(f"epilogue + output projection fused {case}")
+    p = W.epilogue_inputs(13, B, L, H, dh, K, act)
+    t = _dev_inputs(p, act)
+    r = np.random.default_rng(B * L + H)
+    Wo = W._act(r, (H, dh, dq), act)
+    Wd = dev_act(Wo, act)
+    v = t["v"] if K else None
+    assert ops.epilogue_proj_supported(t["y"], H, K, Wd)
+    o = ops.resonator_epilogue_proj_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H, Wd)
+    z = ops.resonator_epilogue_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H)
+    o2 = ops.resonator_grouped_linear(z, Wd)
+    torch.cuda.synchronize()
+    # the same arithmetic and roundings as the epilogue followed by the projection
+    assert torch.equal(o, o2)
+    rr = _ref_inputs(p, act)
+    zr = O.epilogue_fwd(rr["y"], rr["gate"], rr["v"], p["Ct"], p["lambda_c"], p["w"] if K else None, p["s"], H)
+    ref = O.grouped_linear(zr, act64(Wo, act))
+    err = rel_err(host(o), ref)
+    say(f"  err {err:.2e}")
+    # bf16: z and the output are each rounded once (2^-9 relative each)
+    assert err <= (1e-4 if act == "f32" else 2.5e-2)
+
+
 def test_epilogue_fwd_full_size_sampled():
     """The prefill shape (B4 L32768, H8 x dh32 = 256 channels, K = 4, bf16), checked
     on sampled rows against the oracle evaluated on those rows and their K-1
