@@ -997,7 +997,7 @@ hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, c
                                const float* w, const float* s, int num_cus, hipStream_t st) {
   const size_t lds = epi_proj_lds(H, GPGeo<T>::KC, K, d_out, GPGeo<T>::BF);
   const int64_t rows = B * L, ntile = (rows + 15) / 16, want = (ntile + 3) / 4;
-  const int64_t cap = 2 * (int64_t)(num_cus > 0 ? num_cus : 256);
+  const int64_t cap = (int64_t)EP_WG_PER_CU * (num_cus > 0 ? num_cus : 256);
   const dim3 grid((unsigned)(want < cap ? want : cap)), block(256);
   const int dq = (int)(d_out / H);
   if (K > 0)

@@ -14,6 +14,13 @@ constexpr int GP_MAXOB = 8;      // output blocks of 16 per group: d_out/G <= 12
 constexpr int GP_MAXP = 16;      // 16-byte pieces per lane and token tile: d_in * size <= 1024 bytes
 constexpr int GP_FRAG = 64 * 16; // bytes of one weight fragment (16 per lane)
 constexpr int GP_MAXLDS = 64 << 10;
+// Work-groups per compute unit in the projection grids (measured at B4 L32K
+// bf16): one weight streams best with 8 (26 us against 32 us with 2: work-groups
+// that start while others compute keep loads in flight); two weights and the
+// fused epilogue, at twice to four times the registers per lane, with 2.
+constexpr int GP_WG_PER_CU_ONE = 8;
+constexpr int GP_WG_PER_CU_TWO = 2;
+constexpr int EP_WG_PER_CU = 2;
 
 template <typename T>
 struct GPGeo {

@@ -110,7 +110,7 @@ hipError_t launch_grouped_proj(const void* x, const void* W0, const void* W1, vo
   const int nw = W1 ? 2 : 1;
   const int64_t kc = bf16 ? 32 : 16;
   const size_t lds = (size_t)nw * G * (d_in / G / kc) * (d_out / G / 16) * GP_FRAG;
-  const int64_t ntile = (N + 15) / 16, want = (ntile + 3) / 4, cap = 2 * (int64_t)(num_cus > 0 ? num_cus : 256);
+  const int64_t ntile = (N + 15) / 16, want = (ntile + 3) / 4, cap = (int64_t)(nw == 1 ? GP_WG_PER_CU_ONE : GP_WG_PER_CU_TWO) * (num_cus > 0 ? num_cus : 256);
   const dim3 grid((unsigned)(want < cap ? want : cap)), block(GP_THREADS);
   const int di = (int)d_in, dq = (int)d_out, g = (int)G;
   const int np = (int)(d_in / kc), nob = (int)(d_out / G / 16);
