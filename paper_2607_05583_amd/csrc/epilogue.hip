@@ -872,7 +872,10 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
 // of the same 16-lane row (DPP row shifts); each lane also loads row t-3, which
 // is tap 3 and, shifted left, gives the first lanes of the tile their rows
 // before it.  A tap that is not in the batch row multiplies a zero weight by the
-// lane's own row, as in the unfused kernel.
+// lane's own row, as in the unfused kernel.  A wave's next tile's y rows are
+// loaded before the current tile is computed and each head's gate where it is
+// used, which keeps the kernel at two waves per SIMD with loads in flight while
+// it computes (80 us at B4 L32K bf16 against 87 us without the prefetch).
 template <typename T, int MOB, bool HASK>
 __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, const T* __restrict__ gate,
                                                        const T* __restrict__ v, const T* __restrict__ Wo,
@@ -898,19 +901,32 @@ __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, jj = lane & 15, q = lane >> 4, j0 = q * VE;
   const int64_t ntile = (rows + 15) / 16;
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  P yr[8], yn[8];
+  {
+    const int64_t t = ((int64_t)blockIdx.x * 4 + wave) * 16 + jj;
+    const int64_t tc = t < rows ? t : rows - 1;
+#pragma unroll
+    for (int h = 0; h < 8; ++h) yn[h] = *reinterpret_cast<const P*>(y + tc * D + (int64_t)(h < H ? h : 0) * dh + j0);
+  }
   for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < ntile; tile += (int64_t)gridDim.x * 4) {
     const int64_t t = tile * 16 + jj;
     const bool tv = t < rows;
     const int64_t tc = tv ? t : rows - 1;                                   // the row loaded (any row if past the end)
     const int64_t th = t - 3 < 0 ? 0 : (t - 3 < rows ? t - 3 : rows - 1);  // row t-3 (lanes past the end included)
     const int tl = (int)(tc % L);                                           // position in the batch row
-    P yr[8], gr[8], vm[8], vh[8];
+    P vm[8], vh[8];
+#pragma unroll
+    for (int h = 0; h < 8; ++h) yr[h] = yn[h];
+    {
+      const int64_t tn = t + (int64_t)gridDim.x * 64;
+      const int64_t tcn = tn < rows ? tn : rows - 1;
+#pragma unroll
+      for (int h = 0; h < 8; ++h) yn[h] = *reinterpret_cast<const P*>(y + tcn * D + (int64_t)(h < H ? h : 0) * dh + j0);
+    }
 #pragma unroll
     for (int h = 0; h < 8; ++h) {
       const int hh = h < H ? h : 0;
       const int64_t c = (int64_t)hh * dh + j0;
-      yr[h] = *reinterpret_cast<const P*>(y + tc * D + c);
-      gr[h] = *reinterpret_cast<const P*>(gate + tc * D + c);
       if (HASK) {
         vm[h] = *reinterpret_cast<const P*>(v + tc * D + c);
         vh[h] = *reinterpret_cast<const P*>(v + th * D + c);
@@ -931,7 +947,7 @@ __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, 
         for (int e = 0; e < VE; ++e) acc[e] = fmaf(cgh, yh[e], acc[e]);
       }
       float u[VE], o[VE];
-      PC::unpack(gr[g], u);
+      PC::unpack(*reinterpret_cast<const P*>(gate + tc * D + (int64_t)g * dh + j0), u);
 #pragma unroll
       for (int e = 0; e < VE; ++e) o[e] = sigmoid_fast(u[e]) * acc[e];
       if (HASK) {
