@@ -517,6 +517,12 @@ int resonator_mix_bwd(const void* x, const void* dy, res_dtype_t act_dt, void* d
   a.nseg = bwd_segments(B * a.NB, g.P, ncu);
   a.S = (g.P + a.nseg - 1) / a.nseg;
   a.nseg = (int)((g.P + a.S - 1) / a.S);
+  // float32 drives, one mode group and an even number of tiles per segment:
+  // records per half segment, so that the record pass runs two work-groups (of
+  // four waves) per compute unit
+  a.sf = (es == 4 && a.S % 2 == 0 && g.Mp == MODES_PER_GROUP) ? 2 : 1;
+  a.Ss = a.S / a.sf;
+  a.nss = (int)((g.P + a.Ss - 1) / a.Ss);
   a.fast_io = aligned(x, 16) && aligned(dy, 16) && aligned(dx, 16) && (D * (int64_t)es) % 16 == 0;
   a.tab = base + w.tab;
   a.scal = scal;

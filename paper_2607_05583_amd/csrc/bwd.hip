@@ -26,7 +26,8 @@
 // Work decomposition.  A chain is one batch row and one block of 64-byte rows of
 // channels (32 bf16 or 16 float channels); it is cut into segments of S tiles,
 // one work-group each, four channels per wave.
-//   bwd_state_kernel: the (Q, R) of each segment's own drives at its left edge.
+//   bwd_state_kernel: the (Q, R) of each record segment's own drives at its
+//     left edge (a segment, or half of one for float32 drives).
 //   bwd_apply_kernel: the state entering the segment from the right (the later
 //     segments' records folded in float64), then the tiles from right to left:
 //     the products above, the chunk scan carried from tile to tile in
@@ -359,14 +360,18 @@ inline unsigned bwd_grid(const BwdArgs& a) {
 //   R_n <- h (R_n + 256 Q_n) + Er_k[n],   Q_n <- h Q_n + Eq_k[n],   h = lambda^256,
 // and the segment's (Q, rho) at its left edge is, at the end,
 //   Q = sum_n mu^n Q_n,   rho = sum_n mu^n (R_n + 16 n Q_n),   mu = lambda^16
-// (the 16 chunk lanes summed across the row).  Eight tile buffers, seven tiles
-// ahead (a segment of up to eight tiles is in flight at once).
+// (the 16 chunk lanes summed across the row).  NBUF tile buffers, NBUF - 1
+// tiles ahead: eight for segments of up to eight tiles in flight at once, one
+// work-group per compute unit; four for half-segments (float32 drives: the
+// records are taken per half of a segment of the segment pass), two work-groups
+// of four waves per compute unit, so that one's arithmetic overlaps the other's
+// waits (bf16 work-groups have eight waves, and two of them per compute unit
+// would leave 128 registers a lane: measured slower).
 // ---------------------------------------------------------------------------
-template <typename TX, int MG>
-__global__ __launch_bounds__(BGeo<TX>::NT) void bwd_state_kernel(BwdArgs a) {
+template <typename TX, int MG, int NBUF>
+__global__ __launch_bounds__(BGeo<TX>::NT, NBUF == 8 ? 1 : BGeo<TX>::NW / 2) void bwd_state_kernel(BwdArgs a) {
   typedef BGeo<TX> G;
   typedef BPath<TX> PT;
-  constexpr int NBUF = 8;
   constexpr int NM = bwd_mats(MG);
   __shared__ __align__(16) char tb[NBUF][G::TB];
 
@@ -557,11 +562,14 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
   float2 rmu[MG];
   double2 rlt[MG];
   float4 A[MG][FB];
+  // the records are per record segment (a.sf of them per segment of this pass,
+  // a.Ss tiles each); the later ones start at record segment jlo
+  const int jlo = (seg + 1) * a.sf;
   auto records = [&](int g, int j1) {
 #pragma unroll
     for (int i = 0; i < FB; ++i) {
-      const int j = j1 - i > seg ? j1 - i : j1;  // past the first later segment: any valid record, unused
-      A[g][i] = a.agg[((size_t)(b * a.nseg + j) * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1)];
+      const int j = j1 - i >= jlo ? j1 - i : j1;  // past the first later record: any valid record, unused
+      A[g][i] = a.agg[((size_t)(b * a.nss + j) * a.Dp + sd) * a.Mp + 8 * g + (ln >> 1)];
     }
   };
 #pragma unroll
@@ -569,7 +577,7 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
     const size_t im = (size_t)sd * a.Mp + 8 * g + (ln >> 1);
     rmu[g] = a.scal[im].mu;
     rlt[g] = a.cc[im].lamT;
-    if (a.nseg - 1 > seg) records(g, a.nseg - 1);
+    if (a.nss - 1 >= jlo) records(g, a.nss - 1);
   }
 
   uint32_t issued = 0, mark[NBUF] = {0u, 0u, 0u};
@@ -599,16 +607,16 @@ __global__ __launch_bounds__(BGeo<TX>::NT, 1) void bwd_apply_kernel(BwdArgs a) {
   for (int g = 0; g < MG; ++g) {
     mur[g] = rmu[g].x;
     mus[g] = hc ? rmu[g].y : -rmu[g].y;
-    // the state entering the segment from the right: the records of the later
-    // segments j, right to left, C <- (lambda^(256 S) C_Q, lambda^(256 S) (C_R + 256 S C_Q)) + A_j
-    const double2 hop = zpow(rlt[g], a.S);
-    const double span = (double)TILE_T * (double)a.S;
+    // the state entering the segment from the right: the later records j, right
+    // to left, C <- (lambda^(256 Ss) C_Q, lambda^(256 Ss) (C_R + 256 Ss C_Q)) + A_j
+    const double2 hop = zpow(rlt[g], a.Ss);
+    const double span = (double)TILE_T * (double)a.Ss;
     double2 CQ = make_double2(0.0, 0.0), CR = CQ;
-    for (int j1 = a.nseg - 1; j1 > seg; j1 -= FB) {
-      if (j1 != a.nseg - 1) records(g, j1);
+    for (int j1 = a.nss - 1; j1 >= jlo; j1 -= FB) {
+      if (j1 != a.nss - 1) records(g, j1);
 #pragma unroll
       for (int i = 0; i < FB; ++i) {
-        if (j1 - i > seg) {
+        if (j1 - i >= jlo) {
           const double2 t = make_double2(fma(span, CQ.x, CR.x), fma(span, CQ.y, CR.y));
           CR = zfma(hop, t, make_double2(A[g][i].z, A[g][i].w));
           CQ = zfma(hop, CQ, make_double2(A[g][i].x, A[g][i].y));
@@ -879,10 +887,19 @@ hipError_t launch_bwd(const BwdArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent
   const dim3 grid(bwd_grid(a)), block(G::NT);
   const bool mg1 = a.Mp == MODES_PER_GROUP;
   if (a.nseg > 1) {
-    if (mg1)
-      hipLaunchKernelGGL((bwd_state_kernel<TX, 1>), grid, block, 0, st, a);
-    else
-      hipLaunchKernelGGL((bwd_state_kernel<TX, 2>), grid, block, 0, st, a);
+    // the record pass over its own segmentation (a.nss segments of a.Ss tiles)
+    BwdArgs sa = a;
+    sa.nseg = a.nss;
+    sa.S = a.Ss;
+    const dim3 sgrid(bwd_grid(sa));
+    if (sizeof(TX) == 4 && a.sf == 2 && mg1) {
+      hipLaunchKernelGGL((bwd_state_kernel<float, 1, 4>), sgrid, block, 0, st, sa);
+    } else {
+      if (mg1)
+        hipLaunchKernelGGL((bwd_state_kernel<TX, 1, 8>), sgrid, block, 0, st, sa);
+      else
+        hipLaunchKernelGGL((bwd_state_kernel<TX, 2, 8>), sgrid, block, 0, st, sa);
+    }
   }
   if (mg1)
     launch_timed(bwd_apply_kernel<TX, 1>, grid, block, st, ev0, ev1, a);

@@ -99,11 +99,14 @@ struct BwdArgs {
   int64_t P;            // tiles per row
   int64_t S;            // tiles per segment
   int nseg;             // segments per row
+  int64_t Ss;           // tiles per record segment (the record pass's own segmentation)
+  int nss;              // record segments per row
+  int sf;               // record segments per segment (S = sf Ss; 1 or 2)
   int fast_io;          // x, dy and dx 16-byte aligned and rows a multiple of 16 bytes
   const void* tab;
   const ModeScalars* scal;
   const ModeCarry* cc;
-  float4* agg;          // [B][nseg][Dp][Mp]: (Q, rho) of a segment's own drives at its left edge
+  float4* agg;          // [B][nss][Dp][Mp]: (Q, rho) of a record segment's own drives at its left edge
   float* part;          // [B][nseg][Dp][16 + 4 Mp]: partial sums of G, W and R per segment
   float4* q0;           // [B][Dp][Mp]: (Q, rho) at t = 0
 };

@@ -70,6 +70,10 @@ BWD_SEGMENTS = [
     (8, 9372, 256, 8, "f32", False, 38),
     (32, 1024, 256, 8, "bf16", False, 39),
     (3, 5000, 96, 12, "f32", True, 40),
+    # float32 with an even segment length: records per half segment; a partial
+    # last tile, and a last record segment shorter than the others
+    (4, 8000, 256, 8, "f32", True, 41),
+    (4, 7580, 256, 8, "f32", False, 42),
 ]
 
 
@@ -83,10 +87,18 @@ def _segments(B, L, D, act):
     return nseg, S, P - (nseg - 1) * S
 
 
+def _record_segments(M, act, S):
+    """Record segments per segment of the segment pass (float32, one mode group,
+    an even segment length: two)."""
+    return 2 if act == "f32" and M <= 8 and S % 2 == 0 else 1
+
+
 @pytest.mark.parametrize("B,L,D,M,act,use_h0,seed", BWD_SEGMENTS)
 def test_bwd_segment_geometries(B, L, D, M, act, use_h0, seed):
     nseg, S, last = _segments(B, L, D, act)
-    say(f"bwd segments B={B} L={L} D={D} M={M} {act} h0={use_h0}: {nseg} segments of {S} tiles (last {last})")
+    sf = _record_segments(M, act, S)
+    say(f"bwd segments B={B} L={L} D={D} M={M} {act} h0={use_h0}: {nseg} segments of {S} tiles (last {last}), "
+        f"records per {S // sf} tiles")
     prob = W.random_problem(seed, B, L, D, M, act=act, gamma_range=(1e-4, 1.0), gamma_log=True,
                             with_h0=use_h0, with_dy=True)
     tol = 1e-4 if act == "f32" else 2e-2
