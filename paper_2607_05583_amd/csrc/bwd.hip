@@ -360,8 +360,9 @@ inline unsigned bwd_grid(const BwdArgs& a) {
 //   R_n <- h (R_n + 256 Q_n) + Er_k[n],   Q_n <- h Q_n + Eq_k[n],   h = lambda^256,
 // and the segment's (Q, rho) at its left edge is, at the end,
 //   Q = sum_n mu^n Q_n,   rho = sum_n mu^n (R_n + 16 n Q_n),   mu = lambda^16
-// (the 16 chunk lanes summed across the row).  NBUF tile buffers, NBUF - 1
-// tiles ahead: eight for segments of up to eight tiles in flight at once, one
+// (the 16 chunk lanes summed across the row).  NBUF tile buffers, the first
+// NBUF tiles loaded at once and the tiles taken in pairs (one barrier per pair):
+// eight for segments of up to eight tiles in flight at once, one
 // work-group per compute unit; four for half-segments (float32 drives: the
 // records are taken per half of a segment of the segment pass), two work-groups
 // of four waves per compute unit, so that one's arithmetic overlaps the other's
@@ -413,8 +414,9 @@ __global__ __launch_bounds__(BGeo<TX>::NT, NBUF == 8 ? 1 : BGeo<TX>::NW / 2) voi
 
   uint32_t issued = 0, mark[NBUF];
   auto tile_of = [&](int k) { return p0 + nt - 1 - k; };
+  // the first NBUF tiles at once (a whole segment of up to NBUF tiles)
 #pragma unroll
-  for (int k = 0; k < NBUF - 1; ++k) {
+  for (int k = 0; k < NBUF; ++k) {
     if (k < nt && tile_full(tile_of(k))) {
       bload<TX>(tb[k], dy, b, tile_of(k) * TILE_T, d0, a.L, a.D, lane, wave);
       issued += G::GPW;
@@ -430,23 +432,7 @@ __global__ __launch_bounds__(BGeo<TX>::NT, NBUF == 8 ? 1 : BGeo<TX>::NW / 2) voi
       for (int h = 0; h < 2; ++h) mu[g][c][h] = cpow16(mu[g][c][h], ln);
 
   const f4 zero = {0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < nt; ++k) {
-    const int u = k & (NBUF - 1);
-    const int64_t p = tile_of(k);
-    if (tile_full(p))
-      wait_vmcnt((int)(issued - mark[u]));
-    else
-      bcopy<TX>(tb[u], dy, b, p * TILE_T, d0, a.L, a.D, tid);
-    __syncthreads();
-    // tile k+7 into the buffer of tile k-1, which every wave has finished with
-    if (k + NBUF - 1 < nt) {
-      const int u7 = (k + NBUF - 1) & (NBUF - 1);
-      if (tile_full(tile_of(k + NBUF - 1))) {
-        bload<TX>(tb[u7], dy, b, tile_of(k + NBUF - 1) * TILE_T, d0, a.L, a.D, lane, wave);
-        issued += G::GPW;
-      }
-      mark[u7] = issued;
-    }
+  auto tile_records = [&](int u) {
     typename PT::XOp dyv[4];
     PT::template gather<false>(tb[u], ch0, ln, lq, dyv);
 #pragma unroll
@@ -464,6 +450,33 @@ __global__ __launch_bounds__(BGeo<TX>::NT, NBUF == 8 ? 1 : BGeo<TX>::NW / 2) voi
         }
       }
     }
+  };
+  // tiles in pairs, one wait and one barrier per pair (the pair's two tiles in
+  // order, so the sums are those of one tile at a time)
+  for (int k = 0; k < nt; k += 2) {
+    const bool two = k + 1 < nt;
+    const int u0 = k & (NBUF - 1), u1 = (k + 1) & (NBUF - 1);
+    if (!tile_full(tile_of(k))) bcopy<TX>(tb[u0], dy, b, tile_of(k) * TILE_T, d0, a.L, a.D, tid);
+    if (two && !tile_full(tile_of(k + 1))) bcopy<TX>(tb[u1], dy, b, tile_of(k + 1) * TILE_T, d0, a.L, a.D, tid);
+    // the pair's direct loads are in once the later tile's are (loads complete in order)
+    wait_vmcnt((int)(issued - mark[two ? u1 : u0]));
+    __syncthreads();
+    // tiles k+NBUF-2 and k+NBUF-1 (those not loaded at the start) into the buffers
+    // of tiles k-2 and k-1, which every wave has finished with
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int kn = k + NBUF - 2 + i;
+      if (kn >= NBUF && kn < nt) {
+        const int un = kn & (NBUF - 1);
+        if (tile_full(tile_of(kn))) {
+          bload<TX>(tb[un], dy, b, tile_of(kn) * TILE_T, d0, a.L, a.D, lane, wave);
+          issued += G::GPW;
+        }
+        mark[un] = issued;
+      }
+    }
+    tile_records(u0);
+    if (two) tile_records(u1);
   }
 
   const size_t rec = (size_t)(b * a.nseg + seg) * a.Dp;
