@@ -196,10 +196,13 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
 // scalar registers and the lane offset in one vector register.  A store of more
 // than 8 bytes reads its data registers after issue: on gfx950 a vector write to
 // them needs two wait states after the store, which the compiler's hazard
-// tracking cannot see inside an asm statement, so the asm carries them.
+// tracking cannot see inside an asm statement, so the asm carries them.  The
+// rows are outputs no work-group reads again, so the store is non-temporal
+// (nt): it does not leave dirty lines in the L2 to be written back when the
+// kernel ends (the forward at B4 L32K bf16: 65 to 60 us a launch).
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ void st_row16(void* base, uint32_t off, u32x4 v) {
-  asm volatile("global_store_dwordx4 %0, %1, %2\n\ts_nop 1" ::"v"(off), "v"(v), "s"(base) : "memory");
+  asm volatile("global_store_dwordx4 %0, %1, %2 nt\n\ts_nop 1" ::"v"(off), "v"(v), "s"(base) : "memory");
 }
 
 // Transposition of the chunk sums of 4 channels across the wave: R[k] holds
