@@ -636,7 +636,8 @@ def main():
         "mixer_block": {"workload": "B4 d_model 256, bf16: grouped in-projection (8 groups) to drive and gate in one "
                                     "MFMA projection call, mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection "
                                     "(MFMA); forward, and backward (recomputed forward, then the chain rule with the data "
-                                    "gradients as dense GEMMs on the block-diagonal weights and split weight gradients)",
+                                    "gradients from the MFMA data-gradient kernel, the input's three in one pass, and "
+                                    "split weight gradients)",
                         "points": blk},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (forward kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol, and vs the "

@@ -260,6 +260,26 @@ int resonator_grouped_linear_bwd_weight(const void* x, const void* dy, res_dtype
                                         int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream);
 
 /*
+ * Data gradient of n = 1..3 grouped projections of one input (Sec. 3.1: the
+ * block input feeds both the drive and the gate projection, so its gradient is
+ * the sum of theirs):
+ *   dx[n, g di + i] (+)= sum_{k < n} sum_j dy[k][n, g dq + j] W[k][g][i][j]
+ * dy and W are host arrays of n device pointers (dy[k] [N][d_out], W[k]
+ * [G][d_in/G][d_out/G], all of dtype dt); the sum is formed in float32 and dx
+ * (dtype dt) is written once.  With accumulate != 0 dx's present value is added
+ * first.  When d_out/G is a multiple of 32 (bf16) or 16 (f32), d_in/G a multiple
+ * of 16 and at most 128, d_out at most 256 elements (512 bytes of a row with
+ * n = 1), the n weights at most 64 KB and every array 16-byte aligned, it runs as
+ * the library's own MFMA kernel (the weights staged transposed in LDS); other
+ * shapes go to n rocBLAS strided-batched GEMMs.  resonator_grouped_linear_bwd_data
+ * is this call with n = 1.  dx must not overlap any dy[k] or W[k]; n outside
+ * 1..3 is RES_ERR_INVALID_ARG.
+ */
+int resonator_grouped_linear_bwd_data_sum(int n, const void* const* dy, const void* const* W, res_dtype_t dt,
+                                          void* dx, int64_t N, int64_t d_in, int64_t d_out, int64_t G,
+                                          int accumulate, void* stream);
+
+/*
  * Dense [d_in][d_out] copy of a grouped weight W [G][d_in/G][d_out/G], zero off
  * the diagonal blocks, so that resonator_grouped_linear with G = 1 on it gives
  * exactly the grouped product (the zero blocks add exact zeros) with the GEMM

@@ -710,20 +710,43 @@ static int gl_check(int64_t N, int64_t d_in, int64_t d_out, int64_t G, res_dtype
   return RES_OK;
 }
 
-int resonator_grouped_linear_bwd_data(const void* dy, const void* W, res_dtype_t dt, void* dx, int64_t N,
-                                      int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream) {
+int resonator_grouped_linear_bwd_data_sum(int n, const void* const* dy, const void* const* W, res_dtype_t dt,
+                                          void* dx, int64_t N, int64_t d_in, int64_t d_out, int64_t G,
+                                          int accumulate, void* stream) {
   int rc = gl_check(N, d_in, d_out, G, dt);
   if (rc) return rc;
+  if (n < 1 || n > 3) return fail(RES_ERR_INVALID_ARG, "n must be 1, 2 or 3 (got %d)", n);
   if (!dy || !W || !dx) return fail(RES_ERR_INVALID_ARG, "dy, W and dx must be non-null");
   const size_t es = elt_size(dt);
-  if (!aligned(dy, es) || !aligned(W, es) || !aligned(dx, es))
-    return fail(RES_ERR_MISALIGNED, "dy, W and dx must be aligned to their element");
   const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * es;
-  if (overlap(dx, nx, dy, ny) || overlap(dx, nx, W, nw)) return fail(RES_ERR_INVALID_ARG, "dx must not overlap dy or W");
-  const char* err = launch_grouped_linear_bwd_data(dy, W, dx, N, d_in, d_out, G, dt == RES_BF16, accumulate != 0,
-                                                   (hipStream_t)stream);
-  if (err) return fail(RES_ERR_HIP, "grouped linear backward (data): %s", err);
+  if (!aligned(dx, es)) return fail(RES_ERR_MISALIGNED, "dx must be aligned to its element");
+  for (int i = 0; i < n; ++i) {
+    if (!dy[i] || !W[i]) return fail(RES_ERR_INVALID_ARG, "dy[%d] and W[%d] must be non-null", i, i);
+    if (!aligned(dy[i], es) || !aligned(W[i], es))
+      return fail(RES_ERR_MISALIGNED, "dy[%d] and W[%d] must be aligned to their element", i, i);
+    if (overlap(dx, nx, dy[i], ny) || overlap(dx, nx, W[i], nw))
+      return fail(RES_ERR_INVALID_ARG, "dx must not overlap dy[%d] or W[%d]", i, i);
+  }
+  const bool bf = dt == RES_BF16;
+  if (grouped_dgrad_supported(n, dy, W, dx, d_in, d_out, G, bf)) {
+    const hipError_t e = launch_grouped_dgrad(n, dy, W, dx, N, d_in, d_out, G, bf, accumulate != 0, device_cus(),
+                                              (hipStream_t)stream);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "grouped data-gradient launch");
+  }
+  for (int i = 0; i < n; ++i) {
+    const char* err = launch_grouped_linear_bwd_data(dy[i], W[i], dx, N, d_in, d_out, G, bf,
+                                                     accumulate != 0 || i > 0, (hipStream_t)stream);
+    if (err) return fail(RES_ERR_HIP, "grouped linear backward (data): %s", err);
+  }
   return RES_OK;
+}
+
+int resonator_grouped_linear_bwd_data(const void* dy, const void* W, res_dtype_t dt, void* dx, int64_t N,
+                                      int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream) {
+  const void* dys[1] = {dy};
+  const void* Ws[1] = {W};
+  if (!dy || !W) return fail(RES_ERR_INVALID_ARG, "dy, W and dx must be non-null");
+  return resonator_grouped_linear_bwd_data_sum(1, dys, Ws, dt, dx, N, d_in, d_out, G, accumulate, stream);
 }
 
 int resonator_grouped_linear_bwd_weight(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,

@@ -155,6 +155,10 @@ bool grouped_proj_supported(const void* x, const void* W0, const void* W1, const
                             int64_t d_in, int64_t d_out, int64_t G, bool bf16);
 hipError_t launch_grouped_proj(const void* x, const void* W0, const void* W1, void* y0, void* y1, int64_t N,
                                int64_t d_in, int64_t d_out, int64_t G, bool bf16, int num_cus, hipStream_t st);
+bool grouped_dgrad_supported(int n, const void* const* dy, const void* const* W, const void* dx, int64_t d_in,
+                             int64_t d_out, int64_t G, bool bf16);
+hipError_t launch_grouped_dgrad(int n, const void* const* dy, const void* const* W, void* dx, int64_t N, int64_t d_in,
+                                int64_t d_out, int64_t G, bool bf16, bool accumulate, int num_cus, hipStream_t st);
 const char* launch_grouped_linear_bwd_data(const void* dy, const void* W, void* dx, int64_t N, int64_t d_in,
                                            int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
 const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, float* dW, int64_t N, int64_t d_in,

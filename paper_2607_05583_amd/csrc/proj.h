@@ -1,7 +1,8 @@
 // Shared pieces of the grouped projection on MFMA (proj.hip) and of the mixer
 // epilogue fused with the output projection (epilogue.hip): operand types, the
-// staging of a block-diagonal weight into LDS in the operand layout, and the
-// stores of one group's outputs.  Layouts as described in proj.hip.
+// staging of a block-diagonal weight (or of its transpose, for the data
+// gradient) into LDS in the operand layout, and the stores of one group's
+// outputs.  Layouts as described in proj.hip.
 #pragma once
 
 #include "common.h"
@@ -78,17 +79,65 @@ __device__ __forceinline__ void gp_stage(char* dst_bytes, const T* __restrict__ 
   }
 }
 
+// The transpose of W [G][di][dq] (contraction over dq, outputs over di, as the
+// data gradient dy W^T takes it) into LDS at dst as G * (dq / KC) * (di / 16)
+// fragments: element W[g][o][c] to fragment (g, c / KC, block of o), lane
+// (i(o), q) and slot r with c % KC = VE q + r.  A 16-byte run of a weight row
+// holds VE adjacent contraction indices of one output, which is one lane's
+// slots, so every run is one 16-byte LDS store.
+template <typename T>
+__device__ __forceinline__ void gp_stage_t(char* dst_bytes, const T* __restrict__ W, int G, int di, int dq, int tid,
+                                           int nt) {
+  typedef GPGeo<T> GG;
+  const int KB = dq / GG::KC, OB = di / 16, rpr = dq / GG::VE;
+  const int nrun = G * di * rpr;
+  for (int e = tid; e < nrun; e += nt) {
+    const int c0 = (e % rpr) * GG::VE, row = e / rpr;  // row = g di + o
+    const int g = row / di, o = row % di;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(W + (size_t)row * dq + c0);
+    const int kb = c0 / GG::KC, q = (c0 % GG::KC) / GG::VE;
+    const int pb = o >> 5, oo = o & 31;
+    int ob, i;
+    if ((OB & 1) && 2 * pb == OB - 1) {
+      ob = 2 * pb;
+      i = oo;
+    } else {
+      ob = 2 * pb + ((oo >> 2) & 1);
+      i = 4 * (oo >> 3) + (oo & 3);
+    }
+    const int f = (g * KB + kb) * OB + ob;
+    *reinterpret_cast<u32x4*>(dst_bytes + ((size_t)f * 64 + i + 16 * q) * 16) = v;
+  }
+}
+
 // One group's OB output blocks (accumulators a[0 .. OB-1], MFMA D layout) of one
 // token into its output row yr (the group's first output), lane q.
-template <typename T, int MOB>
+// With ACC the outputs' present values are added (in float32) before the
+// rounding.
+template <typename T, int MOB, bool ACC = false>
 __device__ __forceinline__ void gp_store(T* yr, const f4 (&a)[MOB], int OB, int q) {
 #pragma unroll
   for (int ob = 0; ob < MOB; ob += 2) {
     if (ob >= OB) continue;
-    const f4 a0 = a[ob];
+    f4 a0 = a[ob];
     if (ob + 1 < OB) {  // a pair: 8 adjacent outputs from 32 (ob / 2) + 8 q
-      const f4 a1 = a[ob + 1];
+      f4 a1 = a[ob + 1];
       T* yp = yr + 16 * ob + 8 * q;
+      if constexpr (ACC) {
+        if constexpr (GPGeo<T>::BF) {
+          const u32x4 o = *reinterpret_cast<const u32x4*>(yp);
+#pragma unroll
+          for (int r = 0; r < 2; ++r) {
+            a0[2 * r] += __uint_as_float(o[r] << 16);
+            a0[2 * r + 1] += __uint_as_float(o[r] & 0xffff0000u);
+            a1[2 * r] += __uint_as_float(o[2 + r] << 16);
+            a1[2 * r + 1] += __uint_as_float(o[2 + r] & 0xffff0000u);
+          }
+        } else {
+          a0 += *reinterpret_cast<const f4*>(yp);
+          a1 += *reinterpret_cast<const f4*>(yp + 4);
+        }
+      }
       if constexpr (GPGeo<T>::BF) {
         *reinterpret_cast<u32x4*>(yp) =
             u32x4{gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]), gp_pack(a1[0], a1[1]), gp_pack(a1[2], a1[3])};
@@ -98,6 +147,17 @@ __device__ __forceinline__ void gp_store(T* yr, const f4 (&a)[MOB], int OB, int 
       }
     } else {  // the unpaired last block: 4 adjacent outputs from 16 ob + 4 q
       T* yp = yr + 16 * ob + 4 * q;
+      if constexpr (ACC) {
+        if constexpr (GPGeo<T>::BF) {
+          const uint2 o = *reinterpret_cast<const uint2*>(yp);
+          a0[0] += __uint_as_float(o.x << 16);
+          a0[1] += __uint_as_float(o.x & 0xffff0000u);
+          a0[2] += __uint_as_float(o.y << 16);
+          a0[3] += __uint_as_float(o.y & 0xffff0000u);
+        } else {
+          a0 += *reinterpret_cast<const f4*>(yp);
+        }
+      }
       if constexpr (GPGeo<T>::BF)
         *reinterpret_cast<uint2*>(yp) = make_uint2(gp_pack(a0[0], a0[1]), gp_pack(a0[2], a0[3]));
       else

@@ -91,6 +91,147 @@ __global__ __launch_bounds__(GP_THREADS) void gproj_kernel(const T* __restrict__
   }
 }
 
+// Data gradient of up to three grouped projections into one input:
+//   dx[t, g di + k] (+)= sum_i sum_o dy_i[t, g dq + o] W_i[g][k][o]
+// (Sec. 3.1: the block input feeds the drive and the gate projections, so its
+// gradient sums their data gradients).  The same streaming scheme as
+// gproj_kernel with the roles of d_in and d_out exchanged: the B operand is the
+// lane's 16-byte pieces of the dy_i rows, the A operand each W_i transposed in
+// LDS (gp_stage_t); every input accumulates into the same accumulators, group
+// by group, and the sum is rounded once (after adding dx's present value when
+// ACC).
+struct DgradArgs {
+  const void* dy[3];
+  const void* W[3];
+  void* dx;
+  int64_t N;
+  int d_in, d_out, G;
+};
+
+template <typename T, int NI, int MP, int MOB, bool ACC>
+__global__ __launch_bounds__(GP_THREADS) void gproj_dgrad_kernel(DgradArgs a) {
+  typedef GPGeo<T> GG;
+  extern __shared__ __align__(16) char wfrag[];
+  const int di = a.d_in / a.G, dq = a.d_out / a.G, KB = dq / GG::KC, OB = di / 16;
+  const int nfrag = a.G * KB * OB;  // fragments of one weight
+#pragma unroll
+  for (int w = 0; w < NI; ++w)
+    gp_stage_t<T>(wfrag + (size_t)w * nfrag * GP_FRAG, static_cast<const T*>(a.W[w]), a.G, di, dq, threadIdx.x,
+                  GP_THREADS);
+  __syncthreads();
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, j = lane & 15, q = lane >> 4;
+  const int np = a.d_out / GG::KC;  // pieces per lane, input and tile
+  const int64_t ntile = (a.N + 15) / 16;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  T* dx = static_cast<T*>(a.dx);
+  for (int64_t tile = (int64_t)blockIdx.x * 4 + wave; tile < ntile; tile += (int64_t)gridDim.x * 4) {
+    const int64_t t = tile * 16 + j;
+    const bool tv = t < a.N;
+    u32x4 xv[NI][MP];
+#pragma unroll
+    for (int w = 0; w < NI; ++w) {
+      const T* xr = static_cast<const T*>(a.dy[w]) + (tv ? t : 0) * (int64_t)a.d_out + q * (GG::KC / 4);
+#pragma unroll
+      for (int p = 0; p < MP; ++p)
+        if (p < np) xv[w][p] = tv ? *reinterpret_cast<const u32x4*>(xr + p * GG::KC) : zero4;
+    }
+    f4 acc[MOB];
+    int g = 0, kb = 0;
+#pragma unroll
+    for (int p = 0; p < MP; ++p) {
+      if (p < np) {
+        if (kb == 0) {
+#pragma unroll
+          for (int ob = 0; ob < MOB; ++ob) acc[ob] = zero;
+        }
+#pragma unroll
+        for (int w = 0; w < NI; ++w) {
+          const char* fb = wfrag + ((size_t)w * nfrag + (size_t)p * OB) * GP_FRAG + lane * 16;
+#pragma unroll
+          for (int ob = 0; ob < MOB; ++ob)
+            if (ob < OB) acc[ob] = gp_mma(*reinterpret_cast<const u32x4*>(fb + ob * GP_FRAG), xv[w][p], acc[ob], T());
+        }
+        if (kb == KB - 1 && tv) gp_store<T, MOB, ACC>(dx + t * (int64_t)a.d_in + g * di, acc, OB, q);
+        if (++kb == KB) {
+          kb = 0;
+          ++g;
+        }
+      }
+    }
+  }
+}
+
+// Whether the data-gradient kernel takes n inputs of this shape: d_out/G a
+// multiple of 32 (bf16) or 16 (float), d_in/G a multiple of 16 and at most 128,
+// a row of dy at most 256 elements for several inputs (512 bytes for one), the
+// n transposed weights at most 64 KB, and every array 16-byte aligned.
+bool grouped_dgrad_supported(int n, const void* const* dy, const void* const* W, const void* dx, int64_t d_in,
+                             int64_t d_out, int64_t G, bool bf16) {
+  const int64_t kc = bf16 ? 32 : 16;
+  const int64_t di = d_in / G, dq = d_out / G;
+  if (n < 1 || n > 3 || dq % kc || di % 16 || di > 16 * GP_MAXOB) return false;
+  const int64_t np = d_out / kc;
+  if (np > (n == 1 ? GP_MAXP : GP_MAXP / 2)) return false;
+  if ((int64_t)n * G * (dq / kc) * (di / 16) * GP_FRAG > GP_MAXLDS) return false;
+  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (!al(dx)) return false;
+  for (int i = 0; i < n; ++i)
+    if (!al(dy[i]) || !al(W[i])) return false;
+  return true;
+}
+
+hipError_t launch_grouped_dgrad(int n, const void* const* dy, const void* const* W, void* dx, int64_t N, int64_t d_in,
+                                int64_t d_out, int64_t G, bool bf16, bool accumulate, int num_cus, hipStream_t st) {
+  const int64_t kc = bf16 ? 32 : 16;
+  const size_t lds = (size_t)n * G * (d_out / G / kc) * (d_in / G / 16) * GP_FRAG;
+  const int64_t ntile = (N + 15) / 16, want = (ntile + 3) / 4,
+                cap = (int64_t)(n == 1 ? GP_WG_PER_CU_ONE : GP_WG_PER_CU_TWO) * (num_cus > 0 ? num_cus : 256);
+  const dim3 grid((unsigned)(want < cap ? want : cap)), block(GP_THREADS);
+  DgradArgs a{};
+  for (int i = 0; i < 3; ++i) {
+    a.dy[i] = i < n ? dy[i] : dy[0];
+    a.W[i] = i < n ? W[i] : W[0];
+  }
+  a.dx = dx;
+  a.N = N;
+  a.d_in = (int)d_in;
+  a.d_out = (int)d_out;
+  a.G = (int)G;
+  const int np = (int)(d_out / kc), nob = (int)(d_in / G / 16);
+  auto go = [&](auto tag, auto ni_, auto mp_, auto mob_, auto acc_) {
+    typedef decltype(tag) T;
+    constexpr int NI = decltype(ni_)::value, MP = decltype(mp_)::value, MOB = decltype(mob_)::value;
+    constexpr bool ACC = decltype(acc_)::value;
+    hipLaunchKernelGGL((gproj_dgrad_kernel<T, NI, MP, MOB, ACC>), grid, block, lds, st, a);
+  };
+  typedef std::integral_constant<int, 1> I1;
+  typedef std::integral_constant<int, 2> I2;
+  typedef std::integral_constant<int, 3> I3;
+  typedef std::integral_constant<int, 8> I8;
+  typedef std::integral_constant<int, 16> I16;
+  typedef std::integral_constant<bool, true> BT;
+  typedef std::integral_constant<bool, false> BFa;
+  auto by_mob = [&](auto tag, auto ni_, auto mp_, auto acc_) {
+    if (nob <= 2) go(tag, ni_, mp_, I2(), acc_); else go(tag, ni_, mp_, I8(), acc_);
+  };
+  auto by_n = [&](auto tag, auto acc_) {
+    if (n == 1) {
+      if (np <= 8) by_mob(tag, I1(), I8(), acc_); else by_mob(tag, I1(), I16(), acc_);
+    } else if (n == 2) {
+      by_mob(tag, I2(), I8(), acc_);
+    } else {
+      by_mob(tag, I3(), I8(), acc_);
+    }
+  };
+  auto by_acc = [&](auto tag) {
+    if (accumulate) by_n(tag, BT()); else by_n(tag, BFa());
+  };
+  if (bf16) by_acc(bf16_t()); else by_acc(float());
+  return hipGetLastError();
+}
+
 // Whether the MFMA kernel takes this shape: d_in/G a multiple of 32 (bf16) or 16
 // (float), d_out/G a multiple of 16 and at most 128, a row of x at most 1 KB, the
 // staged weights at most 64 KB, and x and the outputs 16-byte aligned.

@@ -415,6 +415,57 @@ def resonator_grouped_linear_bwd(x, W, dy, dx=None, dW=None, accumulate=False):
     return dx, dW
 
 
+def grouped_dgrad_supported(n, d_in, d_out, G, dtype) -> bool:
+    """Whether resonator_grouped_linear_bwd_data_sum runs the library's MFMA
+    kernel for n gradients of this shape (16-byte aligned tensors assumed):
+    d_out/G a multiple of 32 (bf16) or 16 (float32), d_in/G a multiple of 16 and
+    at most 128, d_out at most 256 elements (512 bytes with n = 1), and the n
+    weights at most 64 KB."""
+    bf = dtype == torch.bfloat16
+    kc, es = (32, 2) if bf else (16, 4)
+    if not 1 <= n <= 3 or d_in % G or d_out % G:
+        return False
+    di, dq = d_in // G, d_out // G
+    if dq % kc or di % 16 or di > 128:
+        return False
+    if d_out // kc > (16 if n == 1 else 8):
+        return False
+    return n * G * (dq // kc) * (di // 16) * 1024 <= 64 * 1024
+
+
+def resonator_grouped_linear_bwd_data_sum(dys, Ws, dx=None, accumulate=False):
+    """dx = sum_k dys[k] W_k^T per group (the data gradients of up to three
+    grouped projections of one input, summed in float32 and rounded once); with
+    ``accumulate`` added to the given ``dx``.  Returns dx."""
+    if not 1 <= len(dys) <= 3 or len(dys) != len(Ws):
+        raise ValueError("need 1 to 3 gradients, one weight each")
+    dy0 = dys[0]
+    _dev(dy0, "dy")
+    _code(dy0)
+    d_out = dy0.shape[-1]
+    N = dy0.numel() // d_out
+    G, di, dq = Ws[0].shape
+    for k, (d_, W) in enumerate(zip(dys, Ws)):
+        _dev(d_, f"dys[{k}]")
+        _dev(W, f"Ws[{k}]")
+        if d_.dtype != dy0.dtype or tuple(d_.shape) != tuple(dy0.shape):
+            raise ValueError("every gradient must have the first one's dtype and shape")
+        if W.dtype != dy0.dtype or tuple(W.shape) != (G, di, dq) or G * dq != d_out:
+            raise ValueError("every W must be [G, d_in/G, d_out/G] of the gradients' dtype")
+    if dx is None:
+        dx = torch.empty(dy0.shape[:-1] + (G * di,), dtype=dy0.dtype, device=dy0.device)
+    else:
+        _dev(dx, "dx")
+        if dx.dtype != dy0.dtype or dx.numel() != N * G * di:
+            raise ValueError("dx must have the gradients' dtype and [N, d_in] elements")
+    n = len(dys)
+    arr = ctypes.c_void_p * n
+    check(_lib.lib().resonator_grouped_linear_bwd_data_sum(n, arr(*[_ptr(d_) for d_ in dys]),
+                                                           arr(*[_ptr(W) for W in Ws]), _code(dy0), _ptr(dx), N,
+                                                           G * di, d_out, G, int(accumulate), _stream(dy0.device)))
+    return dx
+
+
 def resonator_grouped_linear_bwd_weight_split(x, dy, dW, accumulate=False):
     """Grouped weight gradient dW [G, d_in/G, d_out/G] (float32) of a long
     contraction, split into chunks (dense partial products, then their diagonal
@@ -538,9 +589,12 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     are recomputed, then the chain rule runs backwards through the output
     projection, the epilogue, the mixing and the two input projections.  Returns
     a dict: dx, dWu, dWg, dWo (float32), dgamma, domega, damp, dphase, dCt,
-    dlambda_c, dw, ds.  The intermediates come from the grouped projections;
-    ``dense`` (as for resonator_block_fwd) runs the data gradients as dense
-    GEMMs and the weight gradients with the contraction split."""
+    dlambda_c, dw, ds.  The intermediates come from the grouped projections and
+    the data gradients from resonator_grouped_linear_bwd_data_sum (dx in one
+    pass over the drive's and the gate's gradients); ``dense`` (as for
+    resonator_block_fwd) runs the weight gradients with the contraction split,
+    and the data gradients as dense GEMMs where the grouped kernel does not
+    take the shape."""
     _dev(x, "x")
     _dev(do, "do")
     if do.dtype != x.dtype:
@@ -566,17 +620,27 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
                 resonator_grouped_linear_bwd_weight_split(xin, d_, dW, accumulate=i > 0)
         return dW
 
-    dz, _ = resonator_grouped_linear_bwd(None, Po, do)
+    def dgrad(dys, Ws, Ps):
+        # data gradient summed over the uses of one input: the library's grouped
+        # kernel where it takes the shape, else the dense GEMMs when given
+        if dense is None or grouped_dgrad_supported(len(dys), Ws[0].shape[0] * Ws[0].shape[1],
+                                                    Ws[0].shape[0] * Ws[0].shape[2], Ws[0].shape[0], x.dtype):
+            return resonator_grouped_linear_bwd_data_sum(dys, Ws)
+        dxs, _ = resonator_grouped_linear_bwd(None, Ps[0], dys[0])
+        for d_, P in zip(dys[1:], Ps[1:]):
+            resonator_grouped_linear_bwd(None, P, d_, dx=dxs, accumulate=True)
+        return dxs
+
+    dz = dgrad([do], [Wo], [Po])
     dWo = wgrad(z, [do], Wo)
     dy, dg, dv, dCt, dlam, dw, ds = resonator_epilogue_bwd(y, g, u, dz, Ct, lambda_c, w, s, H)
     mb = resonator_mix_bwd(u, dy, gamma, omega, amp, phase)
-    # du = mb["dx"] + dv enters both the data and the weight gradient of W_u by accumulation
-    dx, _ = resonator_grouped_linear_bwd(None, Pu, mb["dx"])
-    if dv is not None:
-        resonator_grouped_linear_bwd(None, Pu, dv, dx=dx, accumulate=True)
-    dWu = wgrad(x, [mb["dx"]] + ([dv] if dv is not None else []), Wu)
+    # du = mb["dx"] + dv enters both the data and the weight gradient of W_u;
+    # dx sums the data gradients through W_u (twice) and W_g in one pass
+    dus = [mb["dx"]] + ([dv] if dv is not None else [])
+    dx = dgrad(dus + [dg], [Wu] * len(dus) + [Wg], [Pu] * len(dus) + [Pg])
+    dWu = wgrad(x, dus, Wu)
     dWg = wgrad(x, [dg], Wg)
-    resonator_grouped_linear_bwd(None, Pg, dg, dx=dx, accumulate=True)
     return dict(dx=dx, dWu=dWu, dWg=dWg, dWo=dWo, dgamma=mb["dgamma"], domega=mb["domega"], damp=mb["damp"],
                 dphase=mb["dphase"], dCt=dCt, dlambda_c=dlam, dw=dw, ds=ds)
 

@@ -143,6 +143,16 @@ def test_decode_steps_and_projection_validation_codes():
     assert gl2(ODD, FAKE2, FAKE2, L.RES_F32, F3, F4_, 5, 8, 8, 2, None) == L.RES_ERR_MISALIGNED
     assert lib.resonator_grouped_linear_bwd_data(None, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
         L.RES_ERR_INVALID_ARG
+    dgs = lib.resonator_grouped_linear_bwd_data_sum
+    P3 = ctypes.c_void_p * 3
+    assert dgs(4, P3(FAKE, FAKE, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "n must be" in _err()
+    assert dgs(2, P3(FAKE, None, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "dy[1]" in _err()
+    assert dgs(2, P3(FAKE, F3, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert dgs(1, P3(ODD, FAKE, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
+        L.RES_ERR_MISALIGNED
     assert lib.resonator_grouped_linear_bwd_weight(FAKE, FAKE2, L.RES_BF16, FAKE, 5, 8, 8, 2, 0, None) == \
         L.RES_ERR_INVALID_ARG and "overlap" in _err()
     bd = lib.resonator_block_diag_weight

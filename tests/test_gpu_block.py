@@ -163,6 +163,53 @@ def test_grouped_linear_backward_parity(N, G, di, dq, act):
     assert rel_err(host(dx2), 2 * rdx) <= b and rel_err(host(dW2), 2 * rdW) <= 1e-5
 
 
+# Data gradients summed over n uses of one input, shapes the MFMA kernel takes
+# (d_out/G a multiple of 32 for bf16 and 16 for float32, d_in/G a multiple of 16
+# up to 128): the block's shape with its three gradients, paired and unpaired
+# output blocks, several fragments per group, a 512-byte bf16 row (16 pieces per
+# lane), ragged and short token tails.
+DGRAD_SHAPES = [
+    (777, 8, 32, 32, "bf16", 3),
+    (777, 8, 32, 32, "bf16", 1),
+    (5, 8, 32, 32, "bf16", 2),
+    (1000, 4, 48, 64, "bf16", 2),   # two fragments per group; a pair and an unpaired output block
+    (513, 2, 64, 256, "bf16", 1),   # 16 pieces per lane, 64 KB of staged weight
+    (1000, 4, 64, 32, "f32", 2),
+    (300, 16, 16, 16, "f32", 1),    # 16 pieces per lane; unpaired output blocks
+    (257, 2, 80, 48, "f32", 2),     # three fragments; two pairs and an unpaired block
+]
+
+
+@pytest.mark.parametrize("N,G,di,dq,act,n", DGRAD_SHAPES)
+def test_grouped_dgrad_sum_parity(N, G, di, dq, act, n):
+    say(f"grouped data gradient, {n} inputs (MFMA kernel and library GEMM) N={N} G={G} di={di} dq={dq} {act}")
+    tdt = torch.bfloat16 if act == "bf16" else torch.float32
+    assert ops.grouped_dgrad_supported(n, G * di, G * dq, G, tdt)
+    r = np.random.default_rng(13 * N + G + n)
+    dys = [W._act(r, (N, G * dq), act) for _ in range(n)]
+    Ws = [W._act(r, (G, di, dq), act) for _ in range(n)]
+    dd, wd = [dev_act(a, act) for a in dys], [dev_act(a, act) for a in Ws]
+    dx = ops.resonator_grouped_linear_bwd_data_sum(dd, wd)
+    # accumulation onto a present dx, and the library GEMMs on unaligned views
+    dx2 = ops.resonator_grouped_linear_bwd_data_sum(dd, wd, dx=dx.clone(), accumulate=True)
+    do_ = [_off_by_one(a, tuple(a.shape)) for a in dd]
+    dxo = _off_by_one(dd[0], (N, G * di))
+    ops.resonator_grouped_linear_bwd_data_sum(do_, wd, dx=dxo)
+    torch.cuda.synchronize()
+    zx = np.zeros((N, G * di))
+    ref = sum(O.grouped_linear_bwd(zx, act64(Wk, act), act64(dk, act))[0] for dk, Wk in zip(dys, Ws))
+    # the kernel rounds the sum once; the library route adds one GEMM at a time
+    # into dx and so rounds the running sum n times (bf16)
+    tol = 1e-5 if act == "f32" else 1e-2
+    e, e2, eo = rel_err(host(dx), ref), rel_err(host(dx2), 2 * host(dx).astype(np.float64)), rel_err(host(dxo), ref)
+    say(f"  err MFMA {e:.2e}, accumulated {e2:.2e}, library {eo:.2e}")
+    assert e <= tol and e2 <= tol and eo <= tol * n
+    if n == 1:  # the one-gradient entry point is the same kernel
+        d1, _ = ops.resonator_grouped_linear_bwd(None, wd[0], dd[0])
+        torch.cuda.synchronize()
+        assert torch.equal(d1, dx)
+
+
 @pytest.mark.parametrize("B,L,d,H,K,G,M,act", [(2, 300, 64, 4, 3, 4, 4, "f32"), (1, 1000, 256, 8, 4, 8, 8, "bf16"),
                                                (2, 257, 32, 2, 0, 1, 3, "f32")])
 def test_block_bwd_parity(B, L, d, H, K, G, M, act):
