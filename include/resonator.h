@@ -280,6 +280,33 @@ int resonator_grouped_linear_bwd_data_sum(int n, const void* const* dy, const vo
                                           int accumulate, void* stream);
 
 /*
+ * Weight gradients of n = 1..3 grouped projections of one input x (Sec. 3.1:
+ * the drive's gradient enters W_u twice, from the mixing and from the local
+ * path, and the gate's enters W_g; Sec. 3.4: the output projection):
+ *   dW_m[g][i][j] (+)= sum_{k < n, out[k] = m} sum_t x[t, g di + i] dy[k][t, g dq + j]
+ * for m = 0 and, when some out[k] = 1, m = 1 (dW0, dW1 float32 [G][d_in/G][d_out/G]).
+ * dy and out are host arrays of n entries (device pointers, weight indices 0 or
+ * 1; at least one gradient goes to weight 0).  With bf16, d_in and d_out
+ * multiples of 64 and at most 256, d_in/G and d_out/G multiples of 16, at most
+ * 64 output blocks of 16 x 16 over both weights, and x and dy 16-byte aligned, it
+ * runs as the library's own MFMA kernel: each work-group sums a token range
+ * (32-token chunks staged in LDS and read down the columns) into partials in
+ * ws, and a second kernel adds the partials in a fixed order, so the result is
+ * deterministic.  Other shapes go to one rocBLAS strided-batched GEMM per
+ * gradient and need no workspace.  ws: at least
+ * resonator_grouped_linear_bwd_weight_sum_workspace_bytes(n, nout, N, d_in,
+ * d_out, G, dt) bytes (nout = 2 when some out[k] = 1), 16-byte aligned, owned by
+ * the caller, contents irrelevant; a smaller workspace where one is needed is
+ * RES_ERR_INVALID_ARG.  The outputs must not overlap x, dy, ws or each other.
+ */
+size_t resonator_grouped_linear_bwd_weight_sum_workspace_bytes(int n, int nout, int64_t N, int64_t d_in,
+                                                                int64_t d_out, int64_t G, res_dtype_t dt);
+int resonator_grouped_linear_bwd_weight_sum(int n, const void* x, const void* const* dy, const int* out,
+                                            res_dtype_t dt, float* dW0, float* dW1, int64_t N, int64_t d_in,
+                                            int64_t d_out, int64_t G, int accumulate, void* ws, size_t ws_bytes,
+                                            void* stream);
+
+/*
  * Dense [d_in][d_out] copy of a grouped weight W [G][d_in/G][d_out/G], zero off
  * the diagonal blocks, so that resonator_grouped_linear with G = 1 on it gives
  * exactly the grouped product (the zero blocks add exact zeros) with the GEMM

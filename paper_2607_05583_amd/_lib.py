@@ -27,7 +27,8 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
            "resonator_grouped_linear", "resonator_grouped_linear2", "resonator_block_diag_weight", "resonator_block_diag_extract",
            "resonator_grouped_linear_bwd_data", "resonator_grouped_linear_bwd_data_sum",
-           "resonator_grouped_linear_bwd_weight",
+           "resonator_grouped_linear_bwd_weight", "resonator_grouped_linear_bwd_weight_sum",
+           "resonator_grouped_linear_bwd_weight_sum_workspace_bytes",
            "resonator_grouped_linear_bwd_weight_split", "resonator_grouped_linear_bwd_weight_split_workspace_bytes",
            "resonator_mix_fwd_noalloc", "resonator_mix_fwd_noalloc_max_bytes", "resonator_fwd_status",
            "resonator_fwd_status_noalloc")
@@ -100,6 +101,11 @@ def _declare(lib):
     lib.resonator_grouped_linear_bwd_data_sum.restype = i32
     lib.resonator_grouped_linear_bwd_data_sum.argtypes = [i32, ctypes.POINTER(vp), ctypes.POINTER(vp), i32, vp, i64, i64,
                                                           i64, i64, i32, vp]
+    lib.resonator_grouped_linear_bwd_weight_sum_workspace_bytes.restype = sz
+    lib.resonator_grouped_linear_bwd_weight_sum_workspace_bytes.argtypes = [i32, i32, i64, i64, i64, i64, i32]
+    lib.resonator_grouped_linear_bwd_weight_sum.restype = i32
+    lib.resonator_grouped_linear_bwd_weight_sum.argtypes = [i32, vp, ctypes.POINTER(vp), ctypes.POINTER(i32), i32, fp,
+                                                            fp, i64, i64, i64, i64, i32, vp, sz, vp]
     lib.resonator_grouped_linear_bwd_weight.restype = i32
     lib.resonator_grouped_linear_bwd_weight.argtypes = [vp, vp, i32, fp, i64, i64, i64, i64, i32, vp]
     lib.resonator_grouped_linear_bwd_weight_split_workspace_bytes.restype = sz

@@ -749,6 +749,71 @@ int resonator_grouped_linear_bwd_data(const void* dy, const void* W, res_dtype_t
   return resonator_grouped_linear_bwd_data_sum(1, dys, Ws, dt, dx, N, d_in, d_out, G, accumulate, stream);
 }
 
+size_t resonator_grouped_linear_bwd_weight_sum_workspace_bytes(int n, int nout, int64_t N, int64_t d_in,
+                                                                int64_t d_out, int64_t G, res_dtype_t dt) {
+  if (N < 1 || d_in < 1 || d_out < 1 || G < 1) return 0;
+  const int nb = grouped_wgrad_blocks(n, nout, d_in, d_out, G, dt == RES_BF16);
+  return nb ? (size_t)grouped_wgrad_grid(N, n) * (size_t)nb * 1024 : 0;
+}
+
+int resonator_grouped_linear_bwd_weight_sum(int n, const void* x, const void* const* dy, const int* out,
+                                            res_dtype_t dt, float* dW0, float* dW1, int64_t N, int64_t d_in,
+                                            int64_t d_out, int64_t G, int accumulate, void* ws, size_t ws_bytes,
+                                            void* stream) {
+  int rc = gl_check(N, d_in, d_out, G, dt);
+  if (rc) return rc;
+  if (n < 1 || n > 3) return fail(RES_ERR_INVALID_ARG, "n must be 1, 2 or 3 (got %d)", n);
+  if (!x || !dy || !out || !dW0) return fail(RES_ERR_INVALID_ARG, "x, dy, out and dW0 must be non-null");
+  int nout = 1, used0 = 0;
+  for (int i = 0; i < n; ++i) {
+    if (out[i] != 0 && out[i] != 1) return fail(RES_ERR_INVALID_ARG, "out[%d] must be 0 or 1", i);
+    if (!dy[i]) return fail(RES_ERR_INVALID_ARG, "dy[%d] must be non-null", i);
+    if (out[i] == 1) nout = 2;
+    else used0 = 1;
+  }
+  if (!used0) return fail(RES_ERR_INVALID_ARG, "at least one gradient must go to dW0");
+  if (nout == 2 && !dW1) return fail(RES_ERR_INVALID_ARG, "dW1 must be non-null when out names weight 1");
+  const size_t es = elt_size(dt);
+  const size_t nx = (size_t)(N * d_in) * es, ny = (size_t)(N * d_out) * es, nw = (size_t)(d_in * (d_out / G)) * 4;
+  if (!aligned(x, es) || !aligned(dW0, 4) || (nout == 2 && !aligned(dW1, 4)))
+    return fail(RES_ERR_MISALIGNED, "x aligned to its element, dW0 and dW1 to 4 bytes");
+  float* const dWs[2] = {dW0, nout == 2 ? dW1 : nullptr};
+  for (int m = 0; m < nout; ++m) {
+    if (overlap(dWs[m], nw, x, nx)) return fail(RES_ERR_INVALID_ARG, "dW%d must not overlap x", m);
+    if (ws && ws_bytes && overlap(dWs[m], nw, ws, ws_bytes))
+      return fail(RES_ERR_INVALID_ARG, "dW%d must not overlap the workspace", m);
+  }
+  if (nout == 2 && overlap(dW0, nw, dW1, nw)) return fail(RES_ERR_INVALID_ARG, "dW0 and dW1 must not overlap");
+  for (int i = 0; i < n; ++i) {
+    if (!aligned(dy[i], es)) return fail(RES_ERR_MISALIGNED, "dy[%d] must be aligned to its element", i);
+    for (int m = 0; m < nout; ++m)
+      if (overlap(dWs[m], nw, dy[i], ny)) return fail(RES_ERR_INVALID_ARG, "dW%d must not overlap dy[%d]", m, i);
+    if (ws && ws_bytes && overlap(ws, ws_bytes, dy[i], ny))
+      return fail(RES_ERR_INVALID_ARG, "the workspace must not overlap dy[%d]", i);
+  }
+  if (ws && ws_bytes && overlap(ws, ws_bytes, x, nx)) return fail(RES_ERR_INVALID_ARG, "the workspace must not overlap x");
+  const bool bf = dt == RES_BF16;
+  bool al16 = ((uintptr_t)x & 15) == 0;
+  for (int i = 0; i < n; ++i) al16 = al16 && ((uintptr_t)dy[i] & 15) == 0;
+  const size_t need = resonator_grouped_linear_bwd_weight_sum_workspace_bytes(n, nout, N, d_in, d_out, G, dt);
+  if (need > 0 && al16) {
+    if (!ws || ws_bytes < need || !aligned(ws, 16))
+      return fail(RES_ERR_INVALID_ARG, "workspace of %zu bytes (16-byte aligned) needed, got %zu", need, ws_bytes);
+    const hipError_t e = launch_grouped_wgrad(n, x, dy, out, dW0, dW1, N, d_in, d_out, G, accumulate != 0,
+                                              static_cast<float*>(ws), (hipStream_t)stream);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "grouped weight-gradient launch");
+  }
+  int first[2] = {1, 1};
+  for (int i = 0; i < n; ++i) {
+    const int m = out[i];
+    const char* err = launch_grouped_linear_bwd_weight(x, dy[i], dWs[m], N, d_in, d_out, G, bf,
+                                                       accumulate != 0 || !first[m], (hipStream_t)stream);
+    if (err) return fail(RES_ERR_HIP, "grouped linear backward (weight): %s", err);
+    first[m] = 0;
+  }
+  return RES_OK;
+}
+
 int resonator_grouped_linear_bwd_weight(const void* x, const void* dy, res_dtype_t dt, float* dW, int64_t N,
                                         int64_t d_in, int64_t d_out, int64_t G, int accumulate, void* stream) {
   int rc = gl_check(N, d_in, d_out, G, dt);

@@ -159,6 +159,11 @@ bool grouped_dgrad_supported(int n, const void* const* dy, const void* const* W,
                              int64_t d_out, int64_t G, bool bf16);
 hipError_t launch_grouped_dgrad(int n, const void* const* dy, const void* const* W, void* dx, int64_t N, int64_t d_in,
                                 int64_t d_out, int64_t G, bool bf16, bool accumulate, int num_cus, hipStream_t st);
+int grouped_wgrad_blocks(int n, int nout, int64_t d_in, int64_t d_out, int64_t G, bool bf16);
+int64_t grouped_wgrad_grid(int64_t N, int n);
+hipError_t launch_grouped_wgrad(int n, const void* x, const void* const* dy, const int* out, float* dW0, float* dW1,
+                                int64_t N, int64_t d_in, int64_t d_out, int64_t G, bool accumulate, float* part,
+                                hipStream_t st);
 const char* launch_grouped_linear_bwd_data(const void* dy, const void* W, void* dx, int64_t N, int64_t d_in,
                                            int64_t d_out, int64_t G, bool bf16, bool accumulate, hipStream_t st);
 const char* launch_grouped_linear_bwd_weight(const void* x, const void* dy, float* dW, int64_t N, int64_t d_in,

@@ -22,6 +22,17 @@ constexpr int GP_MAXLDS = 64 << 10;
 constexpr int GP_WG_PER_CU_ONE = 8;
 constexpr int GP_WG_PER_CU_TWO = 2;
 constexpr int EP_WG_PER_CU = 2;
+// Weight gradient: tokens per chunk (the contraction of one MFMA), waves and
+// threads per work-group, output blocks per wave, 8 x 8 staging blocks per
+// thread, work-groups at most (twice as many for a single gradient) and tokens
+// per work-group at least (partials: 1 KB per output block and work-group).
+constexpr int WT_T = 32;
+constexpr int WT_WAVES = 8;
+constexpr int WT_THREADS = 64 * WT_WAVES;
+constexpr int WT_MAXB = 8;
+constexpr int WT_MAXU = 1;
+constexpr int WT_GRID = 256;
+constexpr int WT_MIN_TOKENS = 128;
 
 template <typename T>
 struct GPGeo {

@@ -232,6 +232,215 @@ hipError_t launch_grouped_dgrad(int n, const void* const* dy, const void* const*
   return hipGetLastError();
 }
 
+// Weight gradient of grouped projections of one input x (bf16), summed over up
+// to three output gradients into one or two weights:
+//   dW_m[g][k][o] (+)= sum_t x[t, g di + k] sum_{i: out(i) = m} dy_i[t, g dq + o]
+// The contraction runs over the tokens, so an MFMA operand lane needs 8
+// consecutive tokens of one channel.  A work-group stages chunks of 32 tokens of
+// x and of each dy_i in LDS channel-major: a thread loads an 8 x 8 block (8 rows'
+// 16-byte pieces of 8 channels, prefetched into registers one chunk ahead),
+// transposes it in registers and writes 8 channel pieces of 16 bytes.  Channel c
+// sits at column position c ^ ((c / 8) mod 4) (64 bytes a column), which spreads
+// the block writes over all banks and keeps the 16 channels of one operand read
+// in one contiguous kilobyte; every operand is then one 16-byte LDS read.
+// Output blocks of 16 x 16 (per weight, group, input block kb and output block
+// ob) are split over the eight waves; block (k, o) of lane (j, q) holds rows
+// 4q + r, column j.  Each work-group writes its token range's sums as partials;
+// wgrad_reduce_kernel adds them over the work-groups in a fixed order
+// (deterministic).
+struct WgradArgs {
+  const void* x;
+  const void* dy[3];
+  float* part;
+  int64_t N, tpw;  // tokens, tokens per work-group (a multiple of 32)
+  int d_in, d_out, G, omap, nb;  // omap bit i: the weight input i adds to; nb: output blocks
+};
+
+__device__ __forceinline__ int wt_pos(int c) { return c ^ ((c >> 3) & 3); }
+
+template <int NI>
+__global__ __launch_bounds__(WT_THREADS) void gproj_wgrad_kernel(WgradArgs a) {
+  extern __shared__ __align__(16) char lds[];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, li = lane & 15, lq = lane >> 4;
+  const int di = a.d_in / a.G, dq = a.d_out / a.G, KB = di / 16, OB = dq / 16, per_w = a.G * KB * OB;
+  char* xs = lds;
+  char* ys = lds + a.d_in * 64;  // input i at ys + i d_out 64
+  const int per = (a.nb + WT_WAVES - 1) / WT_WAVES, b0 = wave * per, b1 = b0 + per < a.nb ? b0 + per : a.nb;
+  const int64_t tb = (int64_t)blockIdx.x * a.tpw, te = tb + a.tpw < a.N ? tb + a.tpw : a.N;
+  const f4 zero = {0.f, 0.f, 0.f, 0.f};
+  f4 acc[WT_MAXB];
+#pragma unroll
+  for (int s = 0; s < WT_MAXB; ++s) acc[s] = zero;
+  // 8 x 8 blocks: x has 4 (row blocks) x d_in / 8 of them, each dy_i 4 x d_out / 8
+  const int nbx = a.d_in / 2, nby = a.d_out / 2, nbt = nbx + NI * nby;
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  u32x4 rv[WT_MAXU][8];
+  auto src = [&](int e, const bf16_t*& base, int& d, int& cb, int& rb, char*& dst) {
+    int t = e, k = 0;
+    if (t >= nbx) {
+      t -= nbx;
+      k = 1 + t / nby;
+      t = t % nby;
+    }
+    d = k ? a.d_out : a.d_in;
+    base = static_cast<const bf16_t*>(k ? a.dy[k - 1 < NI ? k - 1 : 0] : a.x);
+    dst = k ? ys + (k - 1) * a.d_out * 64 : xs;
+    cb = t % (d / 8);
+    rb = t / (d / 8);
+  };
+  auto load = [&](int64_t t0) {
+#pragma unroll
+    for (int u = 0; u < WT_MAXU; ++u) {
+      const int e = tid + WT_THREADS * u;
+      if (e < nbt) {
+        const bf16_t* base;
+        int d, cb, rb;
+        char* dst;
+        src(e, base, d, cb, rb, dst);
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int64_t t = t0 + 8 * rb + r;
+          rv[u][r] = t < te ? *reinterpret_cast<const u32x4*>(base + t * d + 8 * cb) : zero4;
+        }
+      }
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int u = 0; u < WT_MAXU; ++u) {
+      const int e = tid + WT_THREADS * u;
+      if (e < nbt) {
+        const bf16_t* base;
+        int d, cb, rb;
+        char* dst;
+        src(e, base, d, cb, rb, dst);
+        (void)base;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {  // channel 8 cb + k: rows 8 rb .. 8 rb + 7
+          u32x4 o;
+#pragma unroll
+          for (int h = 0; h < 4; ++h) {
+            const uint32_t lo = rv[u][2 * h][k >> 1], hi = rv[u][2 * h + 1][k >> 1];
+            o[h] = (k & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+          }
+          *reinterpret_cast<u32x4*>(dst + wt_pos(8 * cb + k) * 64 + rb * 16) = o;
+        }
+      }
+    }
+  };
+  if (tb < te) load(tb);
+  for (int64_t t0 = tb; t0 < te; t0 += WT_T) {
+    __syncthreads();  // the previous chunk's operand reads are done
+    store();
+    __syncthreads();
+    if (t0 + WT_T < te) load(t0 + WT_T);
+#pragma unroll
+    for (int s = 0; s < WT_MAXB; ++s) {
+      const int b = b0 + s;
+      if (b < b1) {
+        const int m = b / per_w, rem = b % per_w, g = rem / (KB * OB), kb = (rem / OB) % KB, ob = rem % OB;
+        const u32x4 A = *reinterpret_cast<const u32x4*>(xs + wt_pos(g * di + kb * 16 + li) * 64 + lq * 16);
+        const int cy = wt_pos(g * dq + ob * 16 + li) * 64 + lq * 16;
+#pragma unroll
+        for (int i = 0; i < NI; ++i)
+          if (((a.omap >> i) & 1) == m)
+            acc[s] = gp_mma(A, *reinterpret_cast<const u32x4*>(ys + i * a.d_out * 64 + cy), acc[s], bf16_t());
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 0; s < WT_MAXB; ++s) {
+    const int b = b0 + s;
+    if (b < b1) *reinterpret_cast<f4*>(a.part + (((size_t)blockIdx.x * a.nb + b) * 64 + lane) * 4) = acc[s];
+  }
+}
+
+// dW_m entries from the partials of nwg work-groups: a block takes 32 entries,
+// its eight slices of 32 threads sum every eighth work-group's partial (slice
+// k: work-groups k, k + 8, ...) in order, and the slices' sums are added in
+// slice order, so the result does not depend on the launch.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ P, float* __restrict__ dW0,
+                                                           float* __restrict__ dW1, int nwg, int nb, int G, int di,
+                                                           int dq, int accumulate) {
+  __shared__ float sp[8][32];
+  const int KB = di / 16, OB = dq / 16, per_w = G * KB * OB;
+  const int el = threadIdx.x & 31, sl = threadIdx.x >> 5;
+  const int64_t E = (int64_t)nb * 256, e = (int64_t)blockIdx.x * 32 + el;
+  float v = 0.f;
+  if (e < E) {
+#pragma unroll 8
+    for (int w = sl; w < nwg; w += 8) v += P[(size_t)w * E + e];
+  }
+  sp[sl][el] = v;
+  __syncthreads();
+  if (sl != 0 || e >= E) return;
+#pragma unroll
+  for (int k = 1; k < 8; ++k) v += sp[k][el];
+  const int b = (int)(e >> 8), lane = (int)(e >> 2) & 63, r = (int)e & 3, j = lane & 15, q = lane >> 4;
+  const int m = b / per_w, rem = b % per_w, g = rem / (KB * OB), kb = (rem / OB) % KB, ob = rem % OB;
+  float* W = m ? dW1 : dW0;
+  const size_t idx = ((size_t)g * di + kb * 16 + 4 * q + r) * dq + ob * 16 + j;
+  W[idx] = accumulate ? W[idx] + v : v;
+}
+
+// Output blocks of the weight-gradient kernel, 0 when it does not take the shape
+// (bf16; d_in and d_out multiples of 64 and at most 256; d_in/G and d_out/G
+// multiples of 16; at most 64 blocks of 16 x 16; the chunk at most 64 KB of LDS).
+int grouped_wgrad_blocks(int n, int nout, int64_t d_in, int64_t d_out, int64_t G, bool bf16) {
+  if (!bf16 || n < 1 || n > 3 || nout < 1 || nout > 2 || G < 1 || d_in % G || d_out % G) return 0;
+  const int64_t di = d_in / G, dq = d_out / G;
+  if (d_in % 64 || d_out % 64 || d_in > 256 || d_out > 256 || di % 16 || dq % 16) return 0;
+  const int64_t nb = nout * G * (di / 16) * (dq / 16);
+  if (nb > WT_WAVES * WT_MAXB || (int64_t)WT_T * (d_in + n * d_out) * 2 > GP_MAXLDS) return 0;
+  if ((d_in + n * d_out) / 2 > WT_THREADS * WT_MAXU) return 0;
+  return (int)nb;
+}
+
+// Work-groups: at least WT_MIN_TOKENS tokens each; at most WT_GRID, or twice
+// as many for one gradient (half the chunk bytes per work-group, so two
+// work-groups per compute unit keep as many loads in flight).
+int64_t grouped_wgrad_grid(int64_t N, int n) {
+  const int64_t cap = n == 1 ? 2 * WT_GRID : WT_GRID;
+  const int64_t g = (N + WT_MIN_TOKENS - 1) / WT_MIN_TOKENS;
+  return g < 1 ? 1 : (g > cap ? cap : g);
+}
+
+hipError_t launch_grouped_wgrad(int n, const void* x, const void* const* dy, const int* out, float* dW0, float* dW1,
+                                int64_t N, int64_t d_in, int64_t d_out, int64_t G, bool accumulate, float* part,
+                                hipStream_t st) {
+  int nout = 1, omap = 0;
+  for (int i = 0; i < n; ++i) {
+    omap |= (out[i] & 1) << i;
+    if (out[i] == 1) nout = 2;
+  }
+  WgradArgs a{};
+  a.x = x;
+  for (int i = 0; i < 3; ++i) a.dy[i] = i < n ? dy[i] : dy[0];
+  a.part = part;
+  a.N = N;
+  a.d_in = (int)d_in;
+  a.d_out = (int)d_out;
+  a.G = (int)G;
+  a.omap = omap;
+  a.nb = grouped_wgrad_blocks(n, nout, d_in, d_out, G, true);
+  const int64_t grid = grouped_wgrad_grid(N, n);
+  a.tpw = ((N + grid - 1) / grid + WT_T - 1) / WT_T * WT_T;
+  const size_t lds = (size_t)WT_T * (d_in + n * d_out) * 2;
+  if (n == 1)
+    hipLaunchKernelGGL(gproj_wgrad_kernel<1>, dim3((unsigned)grid), dim3(WT_THREADS), lds, st, a);
+  else if (n == 2)
+    hipLaunchKernelGGL(gproj_wgrad_kernel<2>, dim3((unsigned)grid), dim3(WT_THREADS), lds, st, a);
+  else
+    hipLaunchKernelGGL(gproj_wgrad_kernel<3>, dim3((unsigned)grid), dim3(WT_THREADS), lds, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int64_t E = (int64_t)a.nb * 256;
+  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)((E + 31) / 32)), dim3(256), 0, st, part, dW0,
+                     nout == 2 ? dW1 : dW0, (int)grid, a.nb, (int)G, (int)(d_in / G), (int)(d_out / G),
+                     (int)accumulate);
+  return hipGetLastError();
+}
+
 // Whether the MFMA kernel takes this shape: d_in/G a multiple of 32 (bf16) or 16
 // (float), d_out/G a multiple of 16 and at most 128, a row of x at most 1 KB, the
 // staged weights at most 64 KB, and x and the outputs 16-byte aligned.

@@ -466,6 +466,50 @@ def resonator_grouped_linear_bwd_data_sum(dys, Ws, dx=None, accumulate=False):
     return dx
 
 
+def grouped_wgrad_supported(n, nout, d_in, d_out, G, dtype) -> bool:
+    """Whether resonator_grouped_linear_bwd_weight_sum runs the library's MFMA
+    kernel for this shape (16-byte aligned x and gradients assumed): bf16, d_in
+    and d_out multiples of 64 up to 256, d_in/G and d_out/G multiples of 16, at
+    most 64 output blocks of 16 x 16."""
+    return _lib.lib().resonator_grouped_linear_bwd_weight_sum_workspace_bytes(
+        n, nout, 1, d_in, d_out, G, RES_BF16 if dtype == torch.bfloat16 else RES_F32) > 0
+
+
+def resonator_grouped_linear_bwd_weight_sum(x, dys, outs, dWs, accumulate=False):
+    """Weight gradients dWs[m] (float32 [G, d_in/G, d_out/G]) of grouped
+    projections of x: dWs[m] (+)= sum over k with outs[k] = m of x^T dys[k] per
+    group, in one pass over x (the library's MFMA kernel where it takes the shape;
+    deterministic).  Returns dWs."""
+    _dev(x, "x")
+    _code(x)
+    n = len(dys)
+    if not 1 <= n <= 3 or len(outs) != n or not 1 <= len(dWs) <= 2:
+        raise ValueError("need 1 to 3 gradients with one weight index each, and 1 or 2 weights")
+    if any(o not in (0, 1) or o >= len(dWs) for o in outs) or 0 not in outs or (len(dWs) == 2 and 1 not in outs):
+        raise ValueError("outs must name every given weight (indices 0 or 1)")
+    d_in = x.shape[-1]
+    N = x.numel() // d_in
+    d_out = dys[0].shape[-1]
+    for k, d_ in enumerate(dys):
+        _dev(d_, f"dys[{k}]")
+        if d_.dtype != x.dtype or d_.numel() != N * d_out or d_.shape[-1] != d_out:
+            raise ValueError("every gradient must have x's dtype, x's rows and one width")
+    G = dWs[0].shape[0]
+    for m, dW in enumerate(dWs):
+        _dev(dW, f"dWs[{m}]")
+        if dW.dtype != torch.float32 or G < 1 or d_in % G or d_out % G or tuple(dW.shape) != (G, d_in // G, d_out // G):
+            raise ValueError(f"dWs[{m}] must be float32 [G, d_in/G, d_out/G]")
+    nout = len(dWs)
+    nb = _lib.lib().resonator_grouped_linear_bwd_weight_sum_workspace_bytes(n, nout, N, d_in, d_out, G, _code(x))
+    ws = torch.empty(max(nb, 256), dtype=torch.uint8, device=x.device)
+    arr = ctypes.c_void_p * n
+    check(_lib.lib().resonator_grouped_linear_bwd_weight_sum(
+        n, _ptr(x), arr(*[_ptr(d_) for d_ in dys]), (ctypes.c_int * n)(*outs), _code(x), _ptr(dWs[0]),
+        _ptr(dWs[1]) if nout == 2 else None, N, d_in, d_out, G, int(accumulate), _ptr(ws), ws.numel(),
+        _stream(x.device)))
+    return dWs
+
+
 def resonator_grouped_linear_bwd_weight_split(x, dy, dW, accumulate=False):
     """Grouped weight gradient dW [G, d_in/G, d_out/G] (float32) of a long
     contraction, split into chunks (dense partial products, then their diagonal
@@ -632,15 +676,25 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
         return dxs
 
     dz = dgrad([do], [Wo], [Po])
-    dWo = wgrad(z, [do], Wo)
+    if grouped_wgrad_supported(1, 1, z.shape[-1], do.shape[-1], Wo.shape[0], z.dtype):
+        dWo = resonator_grouped_linear_bwd_weight_sum(z, [do], [0], [torch.empty_like(Wo, dtype=torch.float32)])[0]
+    else:
+        dWo = wgrad(z, [do], Wo)
     dy, dg, dv, dCt, dlam, dw, ds = resonator_epilogue_bwd(y, g, u, dz, Ct, lambda_c, w, s, H)
     mb = resonator_mix_bwd(u, dy, gamma, omega, amp, phase)
     # du = mb["dx"] + dv enters both the data and the weight gradient of W_u;
-    # dx sums the data gradients through W_u (twice) and W_g in one pass
+    # dx sums the data gradients through W_u (twice) and W_g in one pass, and
+    # dW_u, dW_g come from one pass over x
     dus = [mb["dx"]] + ([dv] if dv is not None else [])
     dx = dgrad(dus + [dg], [Wu] * len(dus) + [Wg], [Pu] * len(dus) + [Pg])
-    dWu = wgrad(x, dus, Wu)
-    dWg = wgrad(x, [dg], Wg)
+    if Wu.shape == Wg.shape and grouped_wgrad_supported(len(dus) + 1, 2, x.shape[-1], Wu.shape[0] * Wu.shape[2],
+                                                        Wu.shape[0], x.dtype):
+        dWu, dWg = resonator_grouped_linear_bwd_weight_sum(
+            x, dus + [dg], [0] * len(dus) + [1],
+            [torch.empty_like(Wu, dtype=torch.float32), torch.empty_like(Wg, dtype=torch.float32)])
+    else:
+        dWu = wgrad(x, dus, Wu)
+        dWg = wgrad(x, [dg], Wg)
     return dict(dx=dx, dWu=dWu, dWg=dWg, dWo=dWo, dgamma=mb["dgamma"], domega=mb["domega"], damp=mb["damp"],
                 dphase=mb["dphase"], dCt=dCt, dlambda_c=dlam, dw=dw, ds=ds)
 

@@ -143,6 +143,23 @@ def test_decode_steps_and_projection_validation_codes():
     assert gl2(ODD, FAKE2, FAKE2, L.RES_F32, F3, F4_, 5, 8, 8, 2, None) == L.RES_ERR_MISALIGNED
     assert lib.resonator_grouped_linear_bwd_data(None, FAKE2, L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \
         L.RES_ERR_INVALID_ARG
+    wgs = lib.resonator_grouped_linear_bwd_weight_sum
+    I3 = ctypes.c_int * 3
+    P3_ = ctypes.c_void_p * 3
+    F5 = ctypes.c_void_p(0x7F0500000000)
+    assert lib.resonator_grouped_linear_bwd_weight_sum_workspace_bytes(3, 2, 131072, 256, 256, 8, L.RES_BF16) == \
+        256 * 64 * 1024
+    assert lib.resonator_grouped_linear_bwd_weight_sum_workspace_bytes(1, 1, 1000, 256, 256, 8, L.RES_F32) == 0
+    assert wgs(1, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(2, 0, 0), L.RES_BF16, F3, F5, 5, 64, 64, 2, 0, None, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "out[0]" in _err()
+    assert wgs(1, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(1, 0, 0), L.RES_BF16, F3, F5, 5, 64, 64, 2, 0, None, 0, None) == \
+        L.RES_ERR_INVALID_ARG and "dW0" in _err()
+    assert wgs(2, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(0, 1, 0), L.RES_BF16, F3, None, 5, 64, 64, 2, 0, None, 0,
+               None) == L.RES_ERR_INVALID_ARG and "dW1" in _err()
+    assert wgs(2, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(0, 1, 0), L.RES_BF16, F3, F3, 5, 64, 64, 2, 0, None, 0,
+               None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
+    assert wgs(1, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(0, 0, 0), L.RES_BF16, F3, None, 5, 64, 64, 2, 0, None, 0,
+               None) == L.RES_ERR_INVALID_ARG and "workspace" in _err()
     dgs = lib.resonator_grouped_linear_bwd_data_sum
     P3 = ctypes.c_void_p * 3
     assert dgs(4, P3(FAKE, FAKE, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \

@@ -210,6 +210,50 @@ def test_grouped_dgrad_sum_parity(N, G, di, dq, act, n):
         assert torch.equal(d1, dx)
 
 
+# Weight gradients summed over n gradients into one or two weights, shapes the
+# MFMA kernel takes (bf16; d_in, d_out multiples of 64 up to 256; d_in/G, d_out/G
+# multiples of 16; at most 64 output blocks): the block's drive and gate weights
+# from its three gradients, at a ragged length and at the full B4 L32K token
+# count; work-groups with partial and empty token ranges; one output block per
+# group; a single group.
+WGRAD_SHAPES = [
+    (777, 8, 32, 32, (0, 0, 1)),
+    (131072, 8, 32, 32, (0, 0, 1)),
+    (5, 8, 32, 32, (0,)),
+    (40000, 4, 64, 16, (0, 1)),
+    (33, 1, 64, 128, (1, 0)),
+    (1000, 2, 64, 96, (0,)),
+]
+
+
+@pytest.mark.parametrize("N,G,di,dq,outs", WGRAD_SHAPES)
+def test_grouped_wgrad_sum_parity(N, G, di, dq, outs):
+    n, nout = len(outs), max(outs) + 1
+    say(f"grouped weight gradient, {n} gradients into {nout} weights N={N} G={G} di={di} dq={dq} bf16")
+    assert ops.grouped_wgrad_supported(n, nout, G * di, G * dq, G, torch.bfloat16)
+    r = np.random.default_rng(17 * N + G + n)
+    x = W._act(r, (N, G * di), "bf16")
+    dys = [W._act(r, (N, G * dq), "bf16") for _ in range(n)]
+    xd, dd = dev_act(x, "bf16"), [dev_act(a, "bf16") for a in dys]
+    mk = lambda: [torch.empty((G, di, dq), dtype=torch.float32, device=xd.device) for _ in range(nout)]
+    dW = ops.resonator_grouped_linear_bwd_weight_sum(xd, dd, list(outs), mk())
+    dW_again = ops.resonator_grouped_linear_bwd_weight_sum(xd, dd, list(outs), mk())
+    dW_acc = ops.resonator_grouped_linear_bwd_weight_sum(xd, dd, list(outs), [t.clone() for t in dW], accumulate=True)
+    # the library GEMMs (one per gradient) on unaligned views of the same data
+    xo = _off_by_one(xd, tuple(xd.shape))
+    dW_lib = ops.resonator_grouped_linear_bwd_weight_sum(xo, [_off_by_one(a, tuple(a.shape)) for a in dd], list(outs),
+                                                         mk())
+    torch.cuda.synchronize()
+    x64 = act64(x, "bf16")
+    zW = np.zeros((G, di, dq))
+    for m in range(nout):
+        ref = sum(O.grouped_linear_bwd(x64, zW, act64(dk, "bf16"))[1] for dk, o in zip(dys, outs) if o == m)
+        e, ea, el = rel_err(host(dW[m]), ref), rel_err(host(dW_acc[m]), 2 * ref), rel_err(host(dW_lib[m]), ref)
+        say(f"  weight {m}: err MFMA {e:.2e}, accumulated {ea:.2e}, library {el:.2e}")
+        assert e <= 1e-5 and ea <= 1e-5 and el <= 1e-5
+        assert torch.equal(dW[m], dW_again[m])  # fixed summation order
+
+
 @pytest.mark.parametrize("B,L,d,H,K,G,M,act", [(2, 300, 64, 4, 3, 4, 4, "f32"), (1, 1000, 256, 8, 4, 8, 8, "bf16"),
                                                (2, 257, 32, 2, 0, 1, 3, "f32")])
 def test_block_bwd_parity(B, L, d, H, K, G, M, act):
