@@ -570,10 +570,28 @@ def main():
         t1e.record(stream)
         torch.cuda.synchronize()
         bb_us = t0e.elapsed_time(t1e) * 1e3 / reps
-        blk.append({"L": Lb, "fwd_us": b_us, "fwd_graph_us": bg_us, "bwd_us": bb_us,
+
+        # a training step that keeps the forward's intermediates: the forward
+        # also writes z, the backward skips the recomputation
+        def block_step_saved():
+            _, sv = ops.resonator_block_fwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6], 8,
+                                            save=True)
+            return ops.resonator_block_bwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6],
+                                           8, dob, dense=dense, saved=sv)
+
+        block_step_saved()
+        torch.cuda.synchronize()
+        t0e.record(stream)
+        for _ in range(reps):
+            block_step_saved()
+        t1e.record(stream)
+        torch.cuda.synchronize()
+        bs_us = t0e.elapsed_time(t1e) * 1e3 / reps
+        blk.append({"L": Lb, "fwd_us": b_us, "fwd_graph_us": bg_us, "bwd_us": bb_us, "step_us": b_us + bb_us,
+                    "step_saved_us": bs_us,
                     "fwd_tokens_per_s": 4 * Lb / (b_us * 1e-6), "fwd_graph_tokens_per_s": 4 * Lb / (bg_us * 1e-6)})
         log(f"mixer block B4 L={Lb} d256: forward {b_us:.1f} us ({4 * Lb / (b_us * 1e-6) / 1e6:.1f} M tokens/s), "
-            f"graph replay {bg_us:.1f} us, backward {bb_us:.1f} us")
+            f"graph replay {bg_us:.1f} us, backward {bb_us:.1f} us, step with saved intermediates {bs_us:.1f} us")
         del bt, dob
 
     # ---------------- kernel tail: mixing vs a quadratic causal reference ----------------
@@ -637,7 +655,8 @@ def main():
                                     "MFMA projection call, mixing (M8), epilogue (H8 x dh32, K4), grouped out-projection "
                                     "(MFMA); forward, and backward (recomputed forward, then the chain rule with the data "
                                     "gradients from the MFMA data-gradient kernel, the input's three in one pass, and "
-                                    "split weight gradients)",
+                                    "the MFMA weight-gradient kernel); step_us = forward + backward with the "
+                                    "recomputation, step_saved_us = forward keeping u, g, y, z + backward on them",
                         "points": blk},
         "kernel_tail": {"workload": "B1 D256 M8 fp32, mixing step (forward kernel) vs the O(L^2) direct "
                                     "causal reference (taps + Toeplitz sum), paper Table 5 protocol, and vs the "

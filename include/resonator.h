@@ -446,15 +446,19 @@ size_t resonator_epilogue_workspace_bytes(int64_t B, int64_t L, int64_t H, int64
  *   out [B][L][d_out] of act_dt, overlapping none of the inputs; parameters as
  *   resonator_epilogue_fwd.
  * z stays in registers, so the call reads y, gate and v once and writes out once;
- * the result is bitwise that of resonator_epilogue_fwd followed by
+ * z (nullable, [B][L][H dh] of act_dt, 16-byte aligned, overlapping no other
+ * argument) also receives it, bitwise resonator_epilogue_fwd's output, for a
+ * backward that keeps the forward's intermediates.  The result is bitwise that
+ * of resonator_epilogue_fwd followed by
  * resonator_grouped_linear on the MFMA kernel.  Takes H <= 8, dh = 32 (bf16) or
  * 16 (f32), K <= 4, d_out/H = 16 or 32, and y, gate, v, Wo and out 16-byte
  * aligned; other shapes return RES_ERR_UNSUPPORTED (run the two calls instead),
  * misaligned pointers RES_ERR_MISALIGNED.
  */
 int resonator_epilogue_proj_fwd(const void* y, const void* gate, const void* v, res_dtype_t act_dt, const void* Wo,
-                                void* out, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K, int64_t d_out,
-                                const float* Ct, float lambda_c, const float* w, const float* s, void* stream);
+                                void* out, void* z, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K,
+                                int64_t d_out, const float* Ct, float lambda_c, const float* w, const float* s,
+                                void* stream);
 
 /*
  * Backward of resonator_epilogue_fwd for the loss sum(dz * z):

@@ -64,7 +64,7 @@ def _declare(lib):
     lib.resonator_epilogue_fwd.restype = i32
     lib.resonator_epilogue_fwd.argtypes = [vp, vp, vp, i32, vp, i64, i64, i64, i64, i64, fp, f32, fp, fp, vp]
     lib.resonator_epilogue_proj_fwd.restype = i32
-    lib.resonator_epilogue_proj_fwd.argtypes = [vp, vp, vp, i32, vp, vp, i64, i64, i64, i64, i64, i64, fp, f32, fp,
+    lib.resonator_epilogue_proj_fwd.argtypes = [vp, vp, vp, i32, vp, vp, vp, i64, i64, i64, i64, i64, i64, fp, f32, fp,
                                                 fp, vp]
     lib.resonator_epilogue_workspace_bytes.restype = sz
     lib.resonator_epilogue_workspace_bytes.argtypes = [i64, i64, i64, i64, i64]

@@ -1078,8 +1078,9 @@ int resonator_epilogue_fwd(const void* y, const void* gate, const void* v, res_d
 }
 
 int resonator_epilogue_proj_fwd(const void* y, const void* gate, const void* v, res_dtype_t act_dt, const void* Wo,
-                                void* out, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K, int64_t d_out,
-                                const float* Ct, float lambda_c, const float* w, const float* s, void* stream) {
+                                void* out, void* z, int64_t B, int64_t L, int64_t H, int64_t dh, int64_t K,
+                                int64_t d_out, const float* Ct, float lambda_c, const float* w, const float* s,
+                                void* stream) {
   int rc = epi_check(B, L, H, dh, K);
   if (rc) return rc;
   if (!dtype_ok(act_dt)) return fail(RES_ERR_INVALID_ARG, "unknown dtype code");
@@ -1103,11 +1104,17 @@ int resonator_epilogue_proj_fwd(const void* y, const void* gate, const void* v, 
   if (overlap(out, no, y, n) || overlap(out, no, gate, n) || (K > 0 && overlap(out, no, v, n)) ||
       overlap(out, no, Wo, nw))
     return fail(RES_ERR_INVALID_ARG, "out must not overlap y, gate, v or Wo");
+  if (z) {
+    if (!a16(z)) return fail(RES_ERR_MISALIGNED, "z must be 16-byte aligned");
+    if (overlap(z, n, y, n) || overlap(z, n, gate, n) || (K > 0 && overlap(z, n, v, n)) || overlap(z, n, Wo, nw) ||
+        overlap(z, n, out, no))
+      return fail(RES_ERR_INVALID_ARG, "z must not overlap y, gate, v, Wo or out");
+  }
   hipStream_t st = (hipStream_t)stream;
   const hipError_t e =
-      bf ? launch_epi_proj_fwd<bf16_t>(y, gate, v, Wo, out, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
+      bf ? launch_epi_proj_fwd<bf16_t>(y, gate, v, Wo, out, z, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
                                        device_cus(), st)
-         : launch_epi_proj_fwd<float>(y, gate, v, Wo, out, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
+         : launch_epi_proj_fwd<float>(y, gate, v, Wo, out, z, B, L, (int)H, (int)K, d_out, Ct, lambda_c, w, s,
                                       device_cus(), st);
   return e == hipSuccess ? RES_OK : hip_fail(e, "fused epilogue launch");
 }

@@ -879,7 +879,8 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
 template <typename T, int MOB, bool HASK>
 __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, const T* __restrict__ gate,
                                                        const T* __restrict__ v, const T* __restrict__ Wo,
-                                                       T* __restrict__ out, int64_t rows, int64_t L, int H, int K,
+                                                       T* __restrict__ out, T* __restrict__ zout, int64_t rows,
+                                                       int64_t L, int H, int K,
                                                        int dq, const float* __restrict__ Ct, float lambda_c,
                                                        const float* __restrict__ w, const float* __restrict__ s) {
   typedef GPGeo<T> GG;
@@ -986,6 +987,7 @@ __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, 
         for (int e = 0; e < VE; ++e) o[e] = fmaf(sW[D * K + c0 + e], l[e], o[e]);
       }
       const P zp = PC::pack(o);
+      if (zout != nullptr && tv) *reinterpret_cast<P*>(zout + t * D + g * dh + j0) = zp;  // z kept for a backward
       const u32x4 zb = __builtin_bit_cast(u32x4, zp);
       f4 a[MOB];
       const char* fb = wfrag + (size_t)g * OB * GP_FRAG + lane * 16;
@@ -1008,8 +1010,8 @@ size_t epi_proj_lds(int H, int dh, int K, int64_t d_out, bool bf16) {
 }
 
 template <typename T>
-hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, const void* Wo, void* out, int64_t B,
-                               int64_t L, int H, int K, int64_t d_out, const float* Ct, float lambda_c,
+hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, const void* Wo, void* out, void* z,
+                               int64_t B, int64_t L, int H, int K, int64_t d_out, const float* Ct, float lambda_c,
                                const float* w, const float* s, int num_cus, hipStream_t st) {
   const size_t lds = epi_proj_lds(H, GPGeo<T>::KC, K, d_out, GPGeo<T>::BF);
   const int64_t rows = B * L, ntile = (rows + 15) / 16, want = (ntile + 3) / 4;
@@ -1018,16 +1020,16 @@ hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, c
   const int dq = (int)(d_out / H);
   if (K > 0)
     hipLaunchKernelGGL((epi_proj_kernel<T, 2, true>), grid, block, lds, st, (const T*)y, (const T*)gate, (const T*)v,
-                       (const T*)Wo, (T*)out, rows, L, H, K, dq, Ct, lambda_c, w, s);
+                       (const T*)Wo, (T*)out, (T*)z, rows, L, H, K, dq, Ct, lambda_c, w, s);
   else
     hipLaunchKernelGGL((epi_proj_kernel<T, 2, false>), grid, block, lds, st, (const T*)y, (const T*)gate,
-                       (const T*)v, (const T*)Wo, (T*)out, rows, L, H, K, dq, Ct, lambda_c, w, s);
+                       (const T*)v, (const T*)Wo, (T*)out, (T*)z, rows, L, H, K, dq, Ct, lambda_c, w, s);
   return hipGetLastError();
 }
-template hipError_t launch_epi_proj_fwd<float>(const void*, const void*, const void*, const void*, void*, int64_t,
+template hipError_t launch_epi_proj_fwd<float>(const void*, const void*, const void*, const void*, void*, void*, int64_t,
                                                int64_t, int, int, int64_t, const float*, float, const float*,
                                                const float*, int, hipStream_t);
-template hipError_t launch_epi_proj_fwd<bf16_t>(const void*, const void*, const void*, const void*, void*, int64_t,
+template hipError_t launch_epi_proj_fwd<bf16_t>(const void*, const void*, const void*, const void*, void*, void*, int64_t,
                                                 int64_t, int, int, int64_t, const float*, float, const float*,
                                                 const float*, int, hipStream_t);
 

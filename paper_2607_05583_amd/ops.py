@@ -563,7 +563,7 @@ def resonator_block_diag_extract(Wd, G, out=None, accumulate=False):
     return W
 
 
-def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, dense=None):
+def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, dense=None, save=False):
     """The mixer block forward (Sec. 3.1, 3.4): drive u and gate g from grouped
     projections of x, y = mixing of u, z = sigmoid(g) (C y) + s conv(u), and the
     grouped output projection of z.  x [B, L, d]; returns [B, L, d_out].
@@ -574,20 +574,30 @@ def resonator_block_fwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     epilogue runs fused into the output projection (z is never written).
     ``dense`` = (Wu, Wg, Wo) as resonator_block_diag_weight copies: the
     projections then run as dense GEMMs and the epilogue on its own (the same
-    result up to the order of float32 sums)."""
+    result up to the order of float32 sums).
+
+    With ``save`` returns (out, saved): saved = dict(u, g, y, z), the forward's
+    intermediates, for resonator_block_bwd(..., saved=saved) to use instead of
+    recomputing them (u, g and y are written by the forward anyway; the fused
+    epilogue also writes z)."""
     if dense is None:
         u, g = resonator_grouped_linear2(x, Wu, Wg)
         y = resonator_mix_fwd(u, gamma, omega, amp, phase)
         K = 0 if w is None else int(w.shape[1])
         if epilogue_proj_supported(y, H, K, Wo):
-            return resonator_epilogue_proj_fwd(y, g, u, Ct, lambda_c, w, s, H, Wo)
-        return resonator_grouped_linear(resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H), Wo)
+            z = torch.empty_like(y) if save else None
+            out = resonator_epilogue_proj_fwd(y, g, u, Ct, lambda_c, w, s, H, Wo, z=z)
+        else:
+            z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
+            out = resonator_grouped_linear(z, Wo)
+        return (out, dict(u=u, g=g, y=y, z=z)) if save else out
     Pu, Pg, Po = dense
     u = resonator_grouped_linear(x, Pu)
     g = resonator_grouped_linear(x, Pg)
     y = resonator_mix_fwd(u, gamma, omega, amp, phase)
     z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
-    return resonator_grouped_linear(z, Po)
+    out = resonator_grouped_linear(z, Po)
+    return (out, dict(u=u, g=g, y=y, z=z)) if save else out
 
 
 class BlockForwardGraph:
@@ -628,7 +638,7 @@ class BlockForwardGraph:
         return self.out
 
 
-def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, do, dense=None):
+def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w, s, H, do, dense=None, saved=None):
     """Gradients of sum(do * resonator_block_fwd(...)): the forward's intermediates
     are recomputed, then the chain rule runs backwards through the output
     projection, the epilogue, the mixing and the two input projections.  Returns
@@ -638,7 +648,8 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     pass over the drive's and the gate's gradients); ``dense`` (as for
     resonator_block_fwd) runs the weight gradients with the contraction split,
     and the data gradients as dense GEMMs where the grouped kernel does not
-    take the shape."""
+    take the shape.  ``saved`` (from resonator_block_fwd(..., save=True) on the
+    same inputs) supplies u, g, y and z instead of the recomputation."""
     _dev(x, "x")
     _dev(do, "do")
     if do.dtype != x.dtype:
@@ -649,9 +660,16 @@ def resonator_block_bwd(x, Wu, Wg, Wo, gamma, omega, amp, phase, Ct, lambda_c, w
     Pu, Pg, Po = dense if dense is not None else (Wu, Wg, Wo)
     # the forward's intermediates from the grouped projections (one read of x
     # for the drive and the gate)
-    u, g = resonator_grouped_linear2(x, Wu, Wg)
-    y = resonator_mix_fwd(u, gamma, omega, amp, phase)
-    z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
+    if saved is not None:
+        u, g, y, z = saved["u"], saved["g"], saved["y"], saved["z"]
+        for k, t in (("u", u), ("g", g), ("y", y), ("z", z)):
+            _dev(t, f"saved[{k!r}]")
+            if t.dtype != x.dtype or t.shape[:-1] != x.shape[:-1]:
+                raise ValueError(f"saved[{k!r}] does not come from a forward of this input")
+    else:
+        u, g = resonator_grouped_linear2(x, Wu, Wg)
+        y = resonator_mix_fwd(u, gamma, omega, amp, phase)
+        z = resonator_epilogue_fwd(y, g, u, Ct, lambda_c, w, s, H)
 
     def wgrad(xin, dys, Wt):
         # grouped weight gradient of the sum over dys; on the dense route with
@@ -828,11 +846,12 @@ def epilogue_proj_supported(y, H, K, Wo) -> bool:
             and dq in (16, 32))
 
 
-def resonator_epilogue_proj_fwd(y, gate, v, Ct, lambda_c, w, s, H, Wo, out=None):
+def resonator_epilogue_proj_fwd(y, gate, v, Ct, lambda_c, w, s, H, Wo, out=None, z=None):
     """The epilogue fused with the grouped output projection (one group per head):
-    GL(resonator_epilogue_fwd(y, gate, v, ...), Wo) without writing z.  Wo is
-    [H, dh, d_out/H] of y's dtype; returns [B, L, d_out].  Bitwise the two
-    separate calls; shapes it does not take raise (epilogue_proj_supported)."""
+    GL(resonator_epilogue_fwd(y, gate, v, ...), Wo) without writing z, unless a
+    tensor ``z`` of y's shape is given to receive it.  Wo is [H, dh, d_out/H] of
+    y's dtype; returns [B, L, d_out].  Bitwise the two separate calls; shapes it
+    does not take raise (epilogue_proj_supported)."""
     _dev(y, "y"); _dev(gate, "gate"); _dev(Wo, "Wo")
     B, L, D = y.shape
     if gate.shape != y.shape or gate.dtype != y.dtype or Wo.dtype != y.dtype:
@@ -849,8 +868,13 @@ def resonator_epilogue_proj_fwd(y, gate, v, Ct, lambda_c, w, s, H, Wo, out=None)
         raise ValueError(f"Wo must be [H, dh, d_out/H] = [{H}, {D // H}, *]")
     d_out = H * Wo.shape[2]
     o = torch.empty((B, L, d_out), dtype=y.dtype, device=y.device) if out is None else _dev(out, "out")
+    if z is not None:
+        _dev(z, "z")
+        if z.shape != y.shape or z.dtype != y.dtype:
+            raise ValueError("z must match y in shape and dtype")
     check(_lib.lib().resonator_epilogue_proj_fwd(
-        _ptr(y), _ptr(gate), _ptr(v) if K else None, _code(y), _ptr(Wo), _ptr(o), B, L, H, D // H, K, d_out,
+        _ptr(y), _ptr(gate), _ptr(v) if K else None, _code(y), _ptr(Wo), _ptr(o), _ptr(z) if z is not None else None,
+        B, L, H, D // H, K, d_out,
         _ptr(Ct), float(lambda_c), _ptr(w) if K else None, _ptr(s) if K else None, _stream(y.device)))
     return o
 

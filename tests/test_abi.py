@@ -219,18 +219,20 @@ def test_reference_params_and_epilogue_validation_codes():
         L.RES_ERR_UNSUPPORTED
     epf = lib.resonator_epilogue_proj_fwd
     W5 = ctypes.c_void_p(0x7F0400000000)
-    # y, gate, v, dt, Wo, out, B, L, H, dh, K, d_out, Ct, lambda_c, w, s, stream
-    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, 1, 16, 16, 32, 4, 512, FAKE, 0.5, FAKE, FAKE, None) == \
+    # y, gate, v, dt, Wo, out, z, B, L, H, dh, K, d_out, Ct, lambda_c, w, s, stream
+    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, None, 1, 16, 16, 32, 4, 512, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_UNSUPPORTED  # more than eight heads
-    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, 1, 16, 8, 16, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, None, 1, 16, 8, 16, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_UNSUPPORTED  # a bf16 head of 16 channels
-    assert epf(FAKE, FAKE2, F3, L.RES_F32, W5, F4, 1, 16, 8, 16, 4, 512, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(FAKE, FAKE2, F3, L.RES_F32, W5, F4, None, 1, 16, 8, 16, 4, 512, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_UNSUPPORTED  # 64 outputs per head
-    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, 1, 16, 8, 32, 4, 100, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, None, 1, 16, 8, 32, 4, 100, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_INVALID_ARG  # d_out not a multiple of H
-    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, FAKE, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, FAKE, None, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_INVALID_ARG and "overlap" in _err()
-    assert epf(ODD, FAKE2, F3, L.RES_BF16, W5, F4, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(ODD, FAKE2, F3, L.RES_BF16, W5, F4, None, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_MISALIGNED
-    assert epf(FAKE, FAKE2, None, L.RES_BF16, W5, F4, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
+    assert epf(FAKE, FAKE2, None, L.RES_BF16, W5, F4, None, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
         L.RES_ERR_INVALID_ARG
+    assert epf(FAKE, FAKE2, F3, L.RES_BF16, W5, F4, FAKE2, 1, 16, 8, 32, 4, 256, FAKE, 0.5, FAKE, FAKE, None) == \
+        L.RES_ERR_INVALID_ARG and "z must not overlap" in _err()

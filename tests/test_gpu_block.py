@@ -268,7 +268,15 @@ def test_block_bwd_parity(B, L, d, H, K, G, M, act):
     gr = ops.resonator_block_bwd(*args)
     dense = tuple(ops.resonator_block_diag_weight(dev(p[k])) for k in ("Wu", "Wg", "Wo"))
     grd = ops.resonator_block_bwd(*args, dense=dense)
+    # the forward's saved intermediates instead of the recomputation: the same
+    # kernels produced them, so the gradients are bitwise the recomputed ones
+    out, saved = ops.resonator_block_fwd(*args[:-1], save=True)
+    grs = ops.resonator_block_bwd(*args, saved=saved)
+    out_plain = ops.resonator_block_fwd(*args[:-1])
     torch.cuda.synchronize()
+    assert torch.equal(out, out_plain)
+    for k, v in gr.items():
+        assert (v is None and grs[k] is None) or torch.equal(v, grs[k]), k
     ref = O.block_bwd(act64(p["x"], act), act64(p["Wu"], act), act64(p["Wg"], act), act64(p["Wo"], act),
                       *[p[k] for k in pk], p["Ct"], p["lambda_c"], p["w"] if K else np.zeros((d, 0)), p["s"], H,
                       act64(do, act))

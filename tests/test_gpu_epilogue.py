@@ -145,9 +145,12 @@ def test_epilogue_proj_fused_matches_two_calls_and_oracle(case):
     o = ops.resonator_epilogue_proj_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H, Wd)
     z = ops.resonator_epilogue_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H)
     o2 = ops.resonator_grouped_linear(z, Wd)
+    zk = torch.empty_like(t["y"])
+    o3 = ops.resonator_epilogue_proj_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H, Wd, z=zk)
     torch.cuda.synchronize()
-    # the same arithmetic and roundings as the epilogue followed by the projection
-    assert torch.equal(o, o2)
+    # the same arithmetic and roundings as the epilogue followed by the projection;
+    # the kept z is the epilogue's output
+    assert torch.equal(o, o2) and torch.equal(o3, o) and torch.equal(zk, z)
     rr = _ref_inputs(p, act)
     zr = O.epilogue_fwd(rr["y"], rr["gate"], rr["v"], p["Ct"], p["lambda_c"], p["w"] if K else None, p["s"], H)
     ref = O.grouped_linear(zr, act64(Wo, act))
