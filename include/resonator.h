@@ -417,6 +417,22 @@ int resonator_params_init(int64_t D, int64_t M, double hl_min, double hl_max, do
                           float alpha_min, float* theta_gamma, float* theta_omega, void* stream);
 
 /*
+ * Diagnostics of a mode bank (Sec. 3.5), float32 outputs, each nullable:
+ *   half_life [D][M]   ln 2 / gamma;
+ *   energy    [D][M][T] exp(-2 gamma t), t = 0 .. T-1 (state energy decay);
+ *   spectrum  [T/2 + 1][D] |sum_{tau<T} K_d[tau] e^{-2 pi i k tau / T}|, the
+ *             magnitude of the real DFT of the length-T impulse response
+ *             K_d[tau] = Re sum_m c_m lambda_m^tau (Sec. 3.1), evaluated in
+ *             closed form per mode in float64 (a geometric sum per bin).
+ * gamma, omega, amp, phase [D][M] float32 device arrays (omega, amp and phase
+ * may be null when spectrum is).  T >= 1 when energy or spectrum is asked for.
+ * Outputs must not overlap the parameters or each other; invalid sizes or null
+ * parameters are RES_ERR_INVALID_ARG.
+ */
+int resonator_diagnostics(const float* gamma, const float* omega, const float* amp, const float* phase, int64_t D,
+                          int64_t M, int64_t T, float* half_life, float* energy, float* spectrum, void* stream);
+
+/*
  * Mixer epilogue around the mixing output (Sec. 3.4, head coupling and local
  * lexical path; the gate of Sec. 3.1's last paragraph):
  *   C = I + (lambda_c / sqrt(H)) tanh(Ct)                          (coupling eq.)

@@ -98,3 +98,11 @@ def energy_decay(gamma, t):
     """State-energy decay exp(-2 gamma t) (Sec. 3.5 diagnostics): [..., len(t)]."""
     g = np.asarray(gamma, dtype=np.float64)[..., None]
     return np.exp(-2.0 * g * np.asarray(t, dtype=np.float64))
+
+
+def spectrum(gamma, omega, amp, phase, T: int):
+    """Magnitude of the real DFT of the length-T impulse response (Sec. 3.5
+    diagnostics): |rfft(K_d[0..T-1])|, [T//2 + 1, D], with K from the direct
+    kernel taps (Sec. 3.1)."""
+    from .resonator_oracle import kernel_taps
+    return np.abs(np.fft.rfft(kernel_taps(gamma, omega, amp, phase, T), axis=1)).T

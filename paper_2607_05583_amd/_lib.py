@@ -22,7 +22,7 @@ SYMBOLS = ("resonator_version", "resonator_workspace_bytes", "resonator_mix_fwd"
            "resonator_set_kernel_timer", "resonator_last_error", "resonator_epilogue_fwd",
            "resonator_epilogue_proj_fwd", "resonator_epilogue_bwd", "resonator_epilogue_workspace_bytes", "resonator_decode_steps",
            "resonator_decode_constants", "resonator_decode_step_tab",
-           "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init",
+           "resonator_params_map", "resonator_params_map_bwd", "resonator_params_init", "resonator_diagnostics",
            "resonator_quadratic_reference", "resonator_quadratic_reference_workspace_bytes",
            "resonator_fft_reference", "resonator_fft_reference_workspace_bytes",
            "resonator_grouped_linear", "resonator_grouped_linear2", "resonator_block_diag_weight", "resonator_block_diag_extract",
@@ -73,6 +73,8 @@ def _declare(lib):
                                            fp, fp, fp, fp, fp, fp, vp, sz, vp]
     lib.resonator_decode_step.restype = i32
     lib.resonator_decode_step.argtypes = [vp, i32, vp, i32, i64, i64, i64, fp, fp, fp, fp, fp, vp]
+    lib.resonator_diagnostics.restype = i32
+    lib.resonator_diagnostics.argtypes = [fp, fp, fp, fp, i64, i64, i64, fp, fp, fp, vp]
     lib.resonator_params_map.restype = i32
     lib.resonator_params_map.argtypes = [fp, fp, i64, f32, fp, fp, vp]
     lib.resonator_params_map_bwd.restype = i32

@@ -1023,6 +1023,34 @@ int resonator_params_init(int64_t D, int64_t M, double hl_min, double hl_max, do
   return e == hipSuccess ? RES_OK : hip_fail(e, "parameter init launch");
 }
 
+int resonator_diagnostics(const float* gamma, const float* omega, const float* amp, const float* phase, int64_t D,
+                          int64_t M, int64_t T, float* half_life, float* energy, float* spectrum, void* stream) {
+  if (D < 1 || M < 1) return fail(RES_ERR_INVALID_ARG, "D and M must be >= 1");
+  if ((energy || spectrum) && T < 1) return fail(RES_ERR_INVALID_ARG, "T must be >= 1 for energy or spectrum");
+  if (D * M > (1LL << 40) || (energy && D * M * T > (1LL << 40)) || (spectrum && (T / 2 + 1) * D > (1LL << 40)))
+    return fail(RES_ERR_UNSUPPORTED, "diagnostics larger than 2^40 entries");
+  if (!gamma) return fail(RES_ERR_INVALID_ARG, "gamma must be non-null");
+  if (spectrum && (!omega || !amp || !phase))
+    return fail(RES_ERR_INVALID_ARG, "omega, amp and phase must be non-null for the spectrum");
+  const float* ins[4] = {gamma, omega, amp, phase};
+  float* outs[3] = {half_life, energy, spectrum};
+  const size_t np = (size_t)(D * M) * 4;
+  const size_t no[3] = {np, (size_t)(D * M * (T > 0 ? T : 0)) * 4, (size_t)((T / 2 + 1) * D) * 4};
+  for (int o = 0; o < 3; ++o) {
+    if (!outs[o]) continue;
+    if (!aligned(outs[o], 4)) return fail(RES_ERR_MISALIGNED, "outputs must be 4-byte aligned");
+    for (int i = 0; i < 4; ++i)
+      if (ins[i] && overlap(outs[o], no[o], ins[i], np)) return fail(RES_ERR_INVALID_ARG, "outputs must not overlap the parameters");
+    for (int q = o + 1; q < 3; ++q)
+      if (outs[q] && overlap(outs[o], no[o], outs[q], no[q])) return fail(RES_ERR_INVALID_ARG, "outputs must not overlap");
+  }
+  for (int i = 0; i < 4; ++i)
+    if (ins[i] && !aligned(ins[i], 4)) return fail(RES_ERR_MISALIGNED, "parameters must be 4-byte aligned");
+  const hipError_t e = launch_diagnostics(gamma, omega, amp, phase, D, M, T, half_life, energy, spectrum,
+                                          (hipStream_t)stream);
+  return e == hipSuccess ? RES_OK : hip_fail(e, "diagnostics launch");
+}
+
 // ---------------------------------------------------------------------------
 // Mixer epilogue (Sec. 3.4)
 // ---------------------------------------------------------------------------

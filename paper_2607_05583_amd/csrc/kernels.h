@@ -192,6 +192,8 @@ hipError_t launch_params_map(const float* tg, const float* tw, int64_t n, float 
                              float* omega, hipStream_t st);
 hipError_t launch_params_map_bwd(const float* tg, const float* tw, const float* dg, const float* dw, int64_t n,
                                  float* dtg, float* dtw, hipStream_t st);
+hipError_t launch_diagnostics(const float* gamma, const float* omega, const float* amp, const float* phase, int64_t D,
+                              int64_t M, int64_t T, float* hl, float* en, float* spec, hipStream_t st);
 hipError_t launch_params_init(int64_t D, int64_t M, double hl_min, double hl_max, double per_min, double per_max,
                               double alpha_min, float* tg, float* tw, hipStream_t st);
 hipError_t launch_decode_consts(int64_t D, int64_t M, const float* gamma, const float* omega, const float* amp,

@@ -85,4 +85,79 @@ hipError_t launch_params_init(int64_t D, int64_t M, double hl_min, double hl_max
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// Diagnostics of a mode bank (Sec. 3.5): half-lives ln 2 / gamma [D][M], state
+// energy decay exp(-2 gamma t) [D][M][T], and the magnitude spectrum of the
+// length-T impulse response K[tau] = Re sum_m c_m lambda_m^tau (Sec. 3.1 kernel),
+//   S[k][d] = |sum_{tau < T} K[tau] e^{-2 pi i k tau / T}|,  k = 0 .. T/2,
+// in closed form: with w = e^{-2 pi i k / T} (so w^T = 1) each mode's geometric
+// sum is (1 - lambda^T) / (1 - lambda w), and K is half the sum of c lambda^tau
+// and its conjugate, so
+//   S = |(1/2) sum_m [c (1 - lambda^T) / (1 - lambda w) + conj(c) (1 - conj(lambda)^T) / (1 - conj(lambda) w)]|,
+// O(M) per bin in float64 instead of an impulse response and an FFT.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void diag_decay_kernel(const float* __restrict__ gamma, int64_t DM, int64_t T,
+                                                         float* __restrict__ hl, float* __restrict__ en) {
+  const int64_t n = en ? DM * T : DM;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t dm = en ? e / T : e;
+    const double g = (double)gamma[dm];
+    if (en) en[e] = (float)exp(-2.0 * g * (double)(e % T));
+    if (hl && (!en || e % T == 0)) hl[dm] = (float)(0.69314718055994530942 / g);
+  }
+}
+
+__global__ __launch_bounds__(256) void diag_spectrum_kernel(const float* __restrict__ gamma,
+                                                            const float* __restrict__ omega,
+                                                            const float* __restrict__ amp,
+                                                            const float* __restrict__ phase, int64_t D, int64_t M,
+                                                            int64_t T, float* __restrict__ spec) {
+  const int64_t nk = T / 2 + 1;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < nk * D; e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t k = e / D, d = e % D;
+    double ws, wc;
+    sincos(-2.0 * 3.14159265358979323846 * (double)k / (double)T, &ws, &wc);
+    double sr = 0.0, si = 0.0;
+    for (int64_t m = 0; m < M; ++m) {
+      const int64_t i = d * M + m;
+      const double g = (double)gamma[i], om = (double)omega[i];
+      double ls, lc, ts, tc, ps, pc;
+      sincos(om, &ls, &lc);
+      sincos(om * (double)T, &ts, &tc);
+      sincos((double)phase[i], &ps, &pc);
+      const double r1 = exp(-g), rT = exp(-g * (double)T), a = (double)amp[i];
+      const double cr = a * pc, ci = a * ps;
+      const double lr = r1 * lc, li = r1 * ls, Tr = rT * tc, Ti = rT * ts;
+      // mode term c (1 - lambda^T) / (1 - lambda w), then the conjugate pole and weight
+#pragma unroll
+      for (int cj = 0; cj < 2; ++cj) {
+        const double sgn = cj ? -1.0 : 1.0;
+        const double nr = cr * (1.0 - Tr) - (sgn * ci) * (-sgn * Ti);
+        const double ni = cr * (-sgn * Ti) + (sgn * ci) * (1.0 - Tr);
+        const double dr = 1.0 - (lr * wc - (sgn * li) * ws), di = -(lr * ws + (sgn * li) * wc);
+        const double q = dr * dr + di * di;
+        sr += 0.5 * (nr * dr + ni * di) / q;
+        si += 0.5 * (ni * dr - nr * di) / q;
+      }
+    }
+    spec[k * D + d] = (float)sqrt(sr * sr + si * si);
+  }
+}
+
+hipError_t launch_diagnostics(const float* gamma, const float* omega, const float* amp, const float* phase, int64_t D,
+                              int64_t M, int64_t T, float* hl, float* en, float* spec, hipStream_t st) {
+  if (hl || en) {
+    const int64_t n = en ? D * M * T : D * M;
+    hipLaunchKernelGGL(diag_decay_kernel, dim3(elem_grid(n)), dim3(256), 0, st, gamma, D * M, T, hl, en);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (spec) {
+    const int64_t n = (T / 2 + 1) * D;
+    hipLaunchKernelGGL(diag_spectrum_kernel, dim3(elem_grid(n)), dim3(256), 0, st, gamma, omega, amp, phase, D, M,
+                       T, spec);
+  }
+  return hipGetLastError();
+}
+
 }  // namespace res

@@ -160,6 +160,13 @@ def test_decode_steps_and_projection_validation_codes():
                None) == L.RES_ERR_INVALID_ARG and "overlap" in _err()
     assert wgs(1, FAKE, P3_(FAKE2, FAKE2, FAKE2), I3(0, 0, 0), L.RES_BF16, F3, None, 5, 64, 64, 2, 0, None, 0,
                None) == L.RES_ERR_INVALID_ARG and "workspace" in _err()
+    dg_ = lib.resonator_diagnostics
+    assert dg_(FAKE, FAKE, FAKE, FAKE, 0, 4, 16, F3, None, None, None) == L.RES_ERR_INVALID_ARG
+    assert dg_(FAKE, None, FAKE, FAKE, 8, 4, 16, None, None, F3, None) == L.RES_ERR_INVALID_ARG and \
+        "spectrum" in _err()
+    assert dg_(FAKE, FAKE, FAKE, FAKE, 8, 4, 0, None, F3, None, None) == L.RES_ERR_INVALID_ARG and "T must" in _err()
+    assert dg_(FAKE, FAKE, FAKE, FAKE, 8, 4, 16, FAKE, None, None, None) == L.RES_ERR_INVALID_ARG and \
+        "overlap" in _err()
     dgs = lib.resonator_grouped_linear_bwd_data_sum
     P3 = ctypes.c_void_p * 3
     assert dgs(4, P3(FAKE, FAKE, FAKE), P3(FAKE2, FAKE2, FAKE2), L.RES_F32, F3, 5, 8, 8, 2, 0, None) == \

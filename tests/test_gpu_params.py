@@ -108,9 +108,14 @@ def test_impulse_response_and_spectrum(D, M, T):
     Kr = O.kernel_taps(*params_np(prob), T)  # [D, T]
     Kr = Kr.T if Kr.shape == (D, T) else Kr
     assert rel_err(host(K), Kr) <= 1e-4
-    S = diag.spectrum(K)
-    Sr = np.abs(np.fft.rfft(Kr, axis=0))
-    assert rel_err(host(S), Sr) <= 1e-4
+    # the library's closed form against the oracle's DFT of its own taps, and
+    # against the FFT of the impulse response the mixing kernel produced
+    S = diag.spectrum(*pr, T)
+    SK = torch.fft.rfft(K, dim=0).abs()
+    torch.cuda.synchronize()
+    Sr = O.spectrum(*params_np(prob), T)
+    assert rel_err(host(S), Sr) <= 1e-5
+    assert rel_err(host(SK), Sr) <= 1e-4
 
 
 def test_half_lives_and_energy_decay():
@@ -119,7 +124,9 @@ def test_half_lives_and_energy_decay():
     assert rel_err(host(diag.half_lives(g)), O.half_lives(prob["gamma"])) <= 1e-6
     e = host(diag.energy_decay(g, 64))
     er = O.energy_decay(prob["gamma"], np.arange(64))
-    assert np.all(np.abs(e - er) <= 1e-5 * np.abs(er) + 1e-30)
+    assert np.all(np.abs(e - er) <= 1e-6 * np.abs(er) + 1e-37)
+    with pytest.raises(Exception):
+        diag.half_lives(g.double())
 
 
 @pytest.mark.parametrize("act,split", [("f32", 1), ("f32", 777), ("bf16", 256), ("bf16", 4000)])

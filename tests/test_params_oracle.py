@@ -118,3 +118,30 @@ def test_planted_mistakes_are_caught():
         assert fails(test_chain_rule_by_finite_differences)
     finally:
         P.params_map, P.params_map_bwd = keep_map, keep_bwd
+
+
+def test_spectrum_against_brute_force_dft_and_the_dc_closed_form():
+    """The spectrum pinned two ways: a brute-force DFT sum over the taps, written
+    as a Python loop over (tau, k) for a tiny T, and the k = 0 bin in closed form
+    for a single mode with a = 1, phi = 0 (the geometric sum Re (1 - lambda^T) /
+    (1 - lambda))."""
+    rng = np.random.default_rng(3)
+    D, M, T = 3, 2, 12
+    gamma = rng.uniform(0.05, 0.8, (D, M))
+    omega = rng.uniform(0.1, 3.0, (D, M))
+    amp = rng.uniform(-1.0, 1.0, (D, M))
+    phase = rng.uniform(-3.0, 3.0, (D, M))
+    S = P.spectrum(gamma, omega, amp, phase, T)
+    assert S.shape == (T // 2 + 1, D)
+    for d in range(D):
+        K = [sum(amp[d, m] * math.exp(-gamma[d, m] * tau) * math.cos(omega[d, m] * tau + phase[d, m])
+                 for m in range(M)) for tau in range(T)]
+        for k in range(T // 2 + 1):
+            re = sum(K[tau] * math.cos(2 * math.pi * k * tau / T) for tau in range(T))
+            im = -sum(K[tau] * math.sin(2 * math.pi * k * tau / T) for tau in range(T))
+            assert abs(S[k, d] - math.hypot(re, im)) <= 1e-12 * (1 + abs(S[k, d]))
+    g, w = 0.3, 1.1
+    lam = complex(math.exp(-g) * math.cos(w), math.exp(-g) * math.sin(w))
+    dc = ((1 - lam ** T) / (1 - lam)).real
+    S1 = P.spectrum(np.array([[g]]), np.array([[w]]), np.array([[1.0]]), np.array([[0.0]]), T)
+    assert abs(S1[0, 0] - abs(dc)) <= 1e-12
