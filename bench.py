@@ -126,7 +126,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--decode-steps", type=int, default=32768)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--counters", nargs="?", const="fwd", choices=("fwd", "bwd", "decode", "block"),
+    ap.add_argument("--counters", nargs="?", const="fwd", choices=("fwd", "bwd", "decode", "block", "block_bwd"),
                     help="short run for rocprofv3 --pmc: one runtime buffer copy of COPY_BYTES "
                          "(the counter calibration), then --steps launches of one workload: the "
                          "prefill forward on rotating buffers (fwd, the default), one training "
@@ -212,6 +212,14 @@ def main():
             bp = [torch.from_numpy(pb_[k]).to(dev) for k in ("gamma", "omega", "amp", "phase", "Ct", "w", "s")]
             for _ in range(args.steps):
                 ops.resonator_block_fwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6], 8)
+        elif args.counters == "block_bwd":
+            name = "mixer block backward B4 L32768 d256 bf16 (H8 x dh32, K4, 8 groups, M8), recomputing the forward"
+            pb_ = W.block_inputs(13, 4, 32768, 256, 8, 4, 8, 8, "bf16")
+            bt = {k: torch.from_numpy(pb_[k].view(np.int16)).view(torch.bfloat16).to(dev) for k in ("x", "Wu", "Wg", "Wo")}
+            bp = [torch.from_numpy(pb_[k]).to(dev) for k in ("gamma", "omega", "amp", "phase", "Ct", "w", "s")]
+            dob = torch.randn_like(bt["x"], dtype=torch.float32).to(torch.bfloat16)
+            for _ in range(args.steps):
+                ops.resonator_block_bwd(bt["x"], bt["Wu"], bt["Wg"], bt["Wo"], *bp[:4], bp[4], 0.5, bp[5], bp[6], 8, dob)
         else:
             c4 = W.CONFIGS[4]
             name = c4.name + " graph replays of 64 steps"
