@@ -1098,6 +1098,15 @@ int resonator_epilogue_fwd(const void* y, const void* gate, const void* v, res_d
     return fail(RES_ERR_INVALID_ARG, "z must not overlap y, gate or v");
   const int vec = epi_vec(dh, es, {y, gate, z, K > 0 ? v : nullptr});
   hipStream_t st = (hipStream_t)stream;
+  auto a16 = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  if (epi_z_lds((int)H, (int)dh, (int)K, act_dt == RES_BF16) > 0 && a16(y) && a16(gate) && a16(z) &&
+      (K == 0 || a16(v))) {  // one token's channel offset of every head per lane; bitwise the same z
+    const hipError_t e =
+        act_dt == RES_BF16
+            ? launch_epi_z_fwd<bf16_t>(y, gate, v, z, B, L, (int)H, (int)K, Ct, lambda_c, w, s, device_cus(), st)
+            : launch_epi_z_fwd<float>(y, gate, v, z, B, L, (int)H, (int)K, Ct, lambda_c, w, s, device_cus(), st);
+    return e == hipSuccess ? RES_OK : hip_fail(e, "epilogue launch");
+  }
   const hipError_t e =
       act_dt == RES_BF16
           ? launch_epi_fwd<bf16_t>(y, gate, v, z, B, L, (int)H, (int)dh, (int)K, Ct, lambda_c, w, s, vec, st)

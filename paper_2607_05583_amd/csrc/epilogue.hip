@@ -876,7 +876,7 @@ hipError_t launch_epi_bwd(const void* y, const void* gate, const void* v, const 
 // loaded before the current tile is computed and each head's gate where it is
 // used, which keeps the kernel at two waves per SIMD with loads in flight while
 // it computes (80 us at B4 L32K bf16 against 87 us without the prefetch).
-template <typename T, int MOB, bool HASK>
+template <typename T, int MOB, bool HASK, bool PROJ = true>
 __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, const T* __restrict__ gate,
                                                        const T* __restrict__ v, const T* __restrict__ Wo,
                                                        T* __restrict__ out, T* __restrict__ zout, int64_t rows,
@@ -889,10 +889,11 @@ __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, 
   typedef typename PC::raw P;
   extern __shared__ __align__(16) char lds[];
   const int D = H * dh, OB = dq / 16, d_out = H * dq;
+  // without PROJ the kernel only writes z (the epilogue forward alone)
   char* wfrag = lds;                                                           // H * OB fragments
-  float* sC = reinterpret_cast<float*>(lds + (size_t)H * OB * GP_FRAG);        // C [H][H]
+  float* sC = reinterpret_cast<float*>(lds + (PROJ ? (size_t)H * OB * GP_FRAG : 0));  // C [H][H]
   float* sW = sC + 64;                                                         // w as [K][D], then s [D]
-  gp_stage<T>(wfrag, Wo, H, dh, dq, threadIdx.x, 256);
+  if (PROJ) gp_stage<T>(wfrag, Wo, H, dh, dq, threadIdx.x, 256);
   coupling_to_lds(sC, Ct, lambda_c, H);
   if (HASK) {
     for (int x = threadIdx.x; x < D * K; x += 256) sW[(x % K) * D + x / K] = w[x];
@@ -988,13 +989,15 @@ __global__ __launch_bounds__(256) void epi_proj_kernel(const T* __restrict__ y, 
       }
       const P zp = PC::pack(o);
       if (zout != nullptr && tv) *reinterpret_cast<P*>(zout + t * D + g * dh + j0) = zp;  // z kept for a backward
-      const u32x4 zb = __builtin_bit_cast(u32x4, zp);
-      f4 a[MOB];
-      const char* fb = wfrag + (size_t)g * OB * GP_FRAG + lane * 16;
+      if (PROJ) {
+        const u32x4 zb = __builtin_bit_cast(u32x4, zp);
+        f4 a[MOB];
+        const char* fb = wfrag + (size_t)g * OB * GP_FRAG + lane * 16;
 #pragma unroll
-      for (int ob = 0; ob < MOB; ++ob)
-        if (ob < OB) a[ob] = gp_mma(*reinterpret_cast<const u32x4*>(fb + ob * GP_FRAG), zb, zero, T());
-      if (tv) gp_store<T, MOB>(out + t * d_out + g * dq, a, OB, q);
+        for (int ob = 0; ob < MOB; ++ob)
+          if (ob < OB) a[ob] = gp_mma(*reinterpret_cast<const u32x4*>(fb + ob * GP_FRAG), zb, zero, T());
+        if (tv) gp_store<T, MOB>(out + t * d_out + g * dq, a, OB, q);
+      }
     }
   }
 }
@@ -1032,6 +1035,37 @@ template hipError_t launch_epi_proj_fwd<float>(const void*, const void*, const v
 template hipError_t launch_epi_proj_fwd<bf16_t>(const void*, const void*, const void*, const void*, void*, void*, int64_t,
                                                 int64_t, int, int, int64_t, const float*, float, const float*,
                                                 const float*, int, hipStream_t);
+
+// The epilogue forward alone on the fused kernel's layout (a lane holds one
+// token's channels at one offset of every head, so the head mixing needs no
+// exchange and the local path's earlier rows come by DPP): for H <= 8, dh = 32
+// (bf16) or 16 (f32), K <= 4; z bitwise that of epi_fwd_col_kernel.
+size_t epi_z_lds(int H, int dh, int K, bool bf16) {
+  const int kc = bf16 ? 32 : 16;
+  if (H < 1 || H > 8 || dh != kc || K < 0 || K > 4) return 0;
+  return 64 * 4 + (size_t)H * dh * (K + 1) * 4;
+}
+
+template <typename T>
+hipError_t launch_epi_z_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H,
+                            int K, const float* Ct, float lambda_c, const float* w, const float* s, int num_cus,
+                            hipStream_t st) {
+  const size_t lds = epi_z_lds(H, GPGeo<T>::KC, K, GPGeo<T>::BF);
+  const int64_t rows = B * L, ntile = (rows + 15) / 16, want = (ntile + 3) / 4;
+  const int64_t cap = (int64_t)EP_WG_PER_CU * (num_cus > 0 ? num_cus : 256);
+  const dim3 grid((unsigned)(want < cap ? want : cap)), block(256);
+  if (K > 0)
+    hipLaunchKernelGGL((epi_proj_kernel<T, 2, true, false>), grid, block, lds, st, (const T*)y, (const T*)gate,
+                       (const T*)v, (const T*)nullptr, (T*)nullptr, (T*)z, rows, L, H, K, 16, Ct, lambda_c, w, s);
+  else
+    hipLaunchKernelGGL((epi_proj_kernel<T, 2, false, false>), grid, block, lds, st, (const T*)y, (const T*)gate,
+                       (const T*)v, (const T*)nullptr, (T*)nullptr, (T*)z, rows, L, H, K, 16, Ct, lambda_c, w, s);
+  return hipGetLastError();
+}
+template hipError_t launch_epi_z_fwd<float>(const void*, const void*, const void*, void*, int64_t, int64_t, int, int,
+                                            const float*, float, const float*, const float*, int, hipStream_t);
+template hipError_t launch_epi_z_fwd<bf16_t>(const void*, const void*, const void*, void*, int64_t, int64_t, int, int,
+                                             const float*, float, const float*, const float*, int, hipStream_t);
 
 template hipError_t launch_epi_fwd<float>(const void*, const void*, const void*, void*, int64_t, int64_t, int, int,
                                           int, const float*, float, const float*, const float*, int, hipStream_t);

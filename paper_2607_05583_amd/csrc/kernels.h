@@ -224,6 +224,11 @@ hipError_t launch_epi_fwd(const void* y, const void* gate, const void* v, void* 
                           hipStream_t st);
 // epilogue fused with the grouped output projection (one group per head)
 size_t epi_proj_lds(int H, int dh, int K, int64_t d_out, bool bf16);
+size_t epi_z_lds(int H, int dh, int K, bool bf16);
+template <typename T>
+hipError_t launch_epi_z_fwd(const void* y, const void* gate, const void* v, void* z, int64_t B, int64_t L, int H,
+                            int K, const float* Ct, float lambda_c, const float* w, const float* s, int num_cus,
+                            hipStream_t st);
 template <typename T>
 hipError_t launch_epi_proj_fwd(const void* y, const void* gate, const void* v, const void* Wo, void* out, void* z, int64_t B,
                                int64_t L, int H, int K, int64_t d_out, const float* Ct, float lambda_c,

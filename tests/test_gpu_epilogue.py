@@ -148,9 +148,19 @@ def test_epilogue_proj_fused_matches_two_calls_and_oracle(case):
     zk = torch.empty_like(t["y"])
     o3 = ops.resonator_epilogue_proj_fwd(t["y"], t["gate"], v, t["Ct"], p["lambda_c"], t["w"], t["s"], H, Wd, z=zk)
     torch.cuda.synchronize()
+    # the epilogue alone on the column kernel (unaligned copies of the inputs)
+    def unaligned(a):
+        buf = torch.empty(a.numel() + 1, dtype=a.dtype, device=a.device)
+        u_ = buf[1:].view(a.shape)
+        u_.copy_(a)
+        return u_
+    zc = unaligned(torch.zeros_like(z))
+    ops.resonator_epilogue_fwd(unaligned(t["y"]), unaligned(t["gate"]), unaligned(v) if K else None, t["Ct"],
+                               p["lambda_c"], t["w"], t["s"], H, out=zc)
+    torch.cuda.synchronize()
     # the same arithmetic and roundings as the epilogue followed by the projection;
-    # the kept z is the epilogue's output
-    assert torch.equal(o, o2) and torch.equal(o3, o) and torch.equal(zk, z)
+    # the kept z, the epilogue on the fused layout and on the column kernel agree bitwise
+    assert torch.equal(o, o2) and torch.equal(o3, o) and torch.equal(zk, z) and torch.equal(zc, z)
     rr = _ref_inputs(p, act)
     zr = O.epilogue_fwd(rr["y"], rr["gate"], rr["v"], p["Ct"], p["lambda_c"], p["w"] if K else None, p["s"], H)
     ref = O.grouped_linear(zr, act64(Wo, act))
