@@ -538,6 +538,19 @@ __device__ __forceinline__ void win_store(const typename Pc<T, CPT>::raw (&r)[NW
       }
 }
 
+// The backward's windows into LDS as loaded (the element type; unpacked to
+// float32 where they are read, which is exact).
+template <typename T, int CPT, int U, int NW>
+__device__ __forceinline__ void win_store_raw(const typename Pc<T, CPT>::raw (&r)[NW][U],
+                                              typename Pc<T, CPT>::raw* const (&dst)[NW], const WinSrc (&w)[NW],
+                                              int G, int rr, int cg, int RP) {
+#pragma unroll
+  for (int q = 0; q < NW; ++q)
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (rr + u * RP < w[q].nrows) dst[q][(rr + u * RP) * G + cg] = r[q][u];
+}
+
 // Per-thread local-path parameters, read once before the chunk loop.  They go
 // through LDS: the compiler waits for every outstanding global load before a
 // loop that stores but does not load whenever that loop uses a register
@@ -559,7 +572,7 @@ __device__ __forceinline__ void params_via_lds(float (&wk)[KM][CPT], float (&sc)
 }
 
 // rows of one window slot per thread: the forward moves 3 windows, the backward 4
-template <int CPT> constexpr int tile_u(bool bwd) { return CPT == 1 ? 16 : (bwd ? 4 : 3); }
+template <int CPT> constexpr int tile_u(bool bwd) { return CPT == 1 ? 16 : (bwd ? 5 : 3); }
 
 template <typename T, int CPT, int HM>
 __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__ y, const T* __restrict__ gate,
@@ -577,11 +590,11 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
   extern __shared__ __align__(16) unsigned char smem[];
   const TileGeo tg = tile_geo(H * dh, CPT);
   const int D = tg.D, G = tg.G, RP = tg.RP, KH = K > 0 ? K - 1 : 0;
-  PF* dybs = reinterpret_cast<PF*>(smem);  // [R][G]  dz sigmoid(gate)
-  PF* ys = dybs + R * G;                   // [R][G]
-  PF* dzs = ys + R * G;                    // [R + KH][G]: rows t0 .. t0 + R + KH - 1
-  PF* vs = dzs + (R + KH) * G;             // [R + KH][G]: rows t0 - KH .. t0 + R - 1
-  P* gs = reinterpret_cast<P*>(vs + (K > 0 ? R + KH : 0) * G);  // [R][G] gate as it is
+  PF* dybs = reinterpret_cast<PF*>(smem);  // [R][G]  dz sigmoid(gate), float32
+  P* ys = reinterpret_cast<P*>(dybs + R * G);  // [R][G]; the windows as loaded
+  P* dzs = ys + R * G;                     // [R + KH][G]: rows t0 .. t0 + R + KH - 1
+  P* vs = dzs + (R + KH) * G;              // [R + KH][G]: rows t0 - KH .. t0 + R - 1
+  P* gs = vs + (K > 0 ? R + KH : 0) * G;   // [R][G] gate
   coupling_to_lds(sC, Ct, lambda_c, H);
   const int rr = threadIdx.x / G, cg = threadIdx.x % G;
   const bool act = rr < RP;
@@ -598,7 +611,7 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
   for (int h = 0; h < HM; ++h) dc[h] = 0.f;
   const int64_t nct = (L + R - 1) / R, nch = B * nct;
   const T* const src[4] = {gate, y, dz, v};
-  PF* const fdst[3] = {ys, dzs, vs};
+  P* const wdst[4] = {gs, ys, dzs, vs};
   auto wins = [&](int64_t c, WinSrc (&wv)[4]) {
     const int64_t t0 = (c % nct) * R;
     const int n = (int)(L - t0 < R ? L - t0 : R);
@@ -617,11 +630,11 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
     __syncthreads();
     if (act) {
       wins(c, wv);
-      win_store<T, CPT, U, 4>(r, gs, fdst, wv, G, rr, cg, RP);
+      win_store_raw<T, CPT, U, 4>(r, wdst, wv, G, rr, cg, RP);
       for (int i = rr; i < n; i += RP) {  // own pieces, just stored by this thread
         float u[CPT], zz[CPT], db[CPT];
         PC::unpack(gs[i * G + cg], u);
-        funpack(dzs[i * G + cg], zz);
+        PC::unpack(dzs[i * G + cg], zz);
 #pragma unroll
         for (int e = 0; e < CPT; ++e) db[e] = zz[e] * sigmoid_fast(u[e]);
         dybs[i * G + cg] = fpack(db);
@@ -637,7 +650,7 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
     for (int i = rr; i < n; i += RP) {
       const int64_t o = (b * L + t0 + i) * D + c0;
       float zz[CPT], sg[CPT], db[CPT], ybar[CPT], dyh[CPT];
-      funpack(dzs[i * G + cg], zz);
+      PC::unpack(dzs[i * G + cg], zz);
       PC::unpack(gs[i * G + cg], sg);
       funpack(dybs[i * G + cg], db);
 #pragma unroll
@@ -648,7 +661,7 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
       for (int h = 0; h < HM; ++h) {
         if (h < H) {
           float yh[CPT], dp[CPT];
-          funpack(ys[i * G + (h * dh + j0) / CPT], yh);
+          PC::unpack(ys[i * G + (h * dh + j0) / CPT], yh);
           funpack(dybs[i * G + (h * dh + j0) / CPT], dp);
           const float cgh = sC[g * H + h], chg = sC[h * H + g];
           float a = 0.f;
@@ -673,8 +686,8 @@ __global__ __launch_bounds__(256) void epi_bwd_tile_kernel(const T* __restrict__
         for (int k = 0; k < KM; ++k)
           if (k < K) {
             float vv[CPT], za[CPT];
-            funpack(vs[(i + KH - k) * G + cg], vv);
-            funpack(dzs[(i + k) * G + cg], za);  // zero past t = L - 1
+            PC::unpack(vs[(i + KH - k) * G + cg], vv);
+            PC::unpack(dzs[(i + k) * G + cg], za);  // zero past t = L - 1
 #pragma unroll
             for (int e = 0; e < CPT; ++e) {
               l[e] = fmaf(wk[k][e], vv[e], l[e]);
@@ -738,7 +751,7 @@ inline size_t epi_tile_lds(bool bwd, int D, int H, int K, int cpt, size_t es, in
     const size_t stage = (R + halo) * D * 4 + (size_t)R * D * es;
     return stage > prm ? stage : prm;
   }
-  const size_t stage = (2 * R + (R + KH) + halo) * D * 4 + (size_t)R * D * es;
+  const size_t stage = (size_t)R * D * 4 + (2 * R + (R + KH) + halo) * D * es;
   size_t xchg = (size_t)256 * (H > (1 + K) * cpt ? H : (1 + K) * cpt) * 4;
   xchg = xchg > prm ? xchg : prm;
   return stage > xchg ? stage : xchg;
