@@ -95,7 +95,7 @@ def write_kernel_trace(db_dir: str, out: str, command: str, top: int = 20, prefi
         # the bench runs the prefill first: its warmup and timed launches are the
         # first ones of the forward kernel (later ones belong to other workloads)
         d = first_launches(db_dir, FUSED, prefill_launches)
-        lines += [f"Prefill workload only (the first {len(d)} `{FUSED}` launches: warm-up and timed steps):",
+        lines += [f"Prefill workload only (the first {len(d)} `{FUSED}` launches: warm-up and both timed loops of steps):",
                   "", "| launches | avg us | min us | max us |", "|---:|---:|---:|---:|",
                   f"| {len(d)} | {sum(d) / len(d):.2f} | {min(d):.2f} | {max(d):.2f} |", ""]
     with open(out, "w") as f:
